@@ -1,0 +1,550 @@
+/*
+ * AECCT inference oracle -- TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.
+ * Only the test suite, the smoke check and the benchmark's CPU-baseline leg use it.
+ *
+ * Plain scalar loops over one word at a time; OpenMP only splits independent
+ * words across threads.  Build with -ffp-contract=off and no fast-math: every
+ * fused multiply-add below is written as fmaf and nothing else is fused.
+ *
+ * Canonical fp32 evaluation order (chosen where the paper fixes none):
+ *   TREE(v, w)  pairwise sum: v[t] += v[t + w/2] for t < w/2, then recurse on
+ *               the first half (w a power of two);
+ *   SEQ         left-to-right from 0 in ascending index;
+ *   EXP         oracle_exp below (Cody-Waite reduction + degree-7 Taylor).
+ */
+#include "aecct_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_MAX_TREE 8192
+
+static int64_t lin_in(const oracle_model *M, int kind) {
+  return kind == ORC_FF2 ? M->d_ff : M->d;
+}
+static int64_t lin_out(const oracle_model *M, int kind) {
+  return kind == ORC_FF1 ? M->d_ff : M->d;
+}
+
+/* Pairwise summation of w values, w a power of two (canonical order TREE). */
+float oracle_tree_sum(const float *v, int32_t w) {
+  float buf[ORC_MAX_TREE];
+  memcpy(buf, v, sizeof(float) * (size_t)w);
+  while (w > 1) {
+    int32_t h = w / 2;
+    for (int32_t t = 0; t < h; ++t) buf[t] = buf[t] + buf[t + h];
+    w = h;
+  }
+  return buf[0];
+}
+
+/*
+ * exp(x) for x <= 0, as used by the softmax of Section 3 (CASA) / Section 4.2
+ * (HPSA).  Cody & Waite (1980) argument reduction x = k ln2 + r with ln2 split
+ * into a 16-bit head (so k * LN2_HI is exact for |k| < 2^7) and its fp32
+ * remainder, then the degree-7 Taylor polynomial of e^r by Horner, then the
+ * exact scaling by 2^k.  Results below exp(-80) are flushed to 0; they are
+ * negligible next to the largest softmax term, which is exactly 1.
+ * Pin: within 2 ulp of libm exp over [-80, 0]; EXP(0) == 1 exactly.
+ */
+float oracle_exp(float x) {
+  const float LOG2E = 1.44269502163f;          /* fp32(log2 e) */
+  const float LN2_HI = 0.693145751953125f;     /* 45426 * 2^-16 */
+  const float LN2_LO = 1.428606765330187e-6f; /* fp32(ln 2 - LN2_HI) */
+  if (x < -80.0f) return 0.0f;
+  float k = rintf(x * LOG2E);
+  float r = fmaf(-k, LN2_HI, x);
+  r = fmaf(-k, LN2_LO, r);
+  float p = 1.0f / 5040.0f;
+  p = fmaf(p, r, 1.0f / 720.0f);
+  p = fmaf(p, r, 1.0f / 120.0f);
+  p = fmaf(p, r, 1.0f / 24.0f);
+  p = fmaf(p, r, 1.0f / 6.0f);
+  p = fmaf(p, r, 0.5f);
+  p = fmaf(p, r, 1.0f);
+  p = fmaf(p, r, 1.0f);
+  return ldexpf(p, (int)k);
+}
+
+/*
+ * HPSA masks (Section 4.2, Fig. 2-3).  Tokens 0..n-1 are variable nodes and
+ * n..n+m-1 check nodes (Section 3: h(y) = [|y|, 1-2s(y)]).  A is the Tanner
+ * graph adjacency; M1 (first ring, c->v and v->c) = A != 0, M2 (second ring,
+ * v->v and c->c) = A.A != 0, which keeps the diagonal so that M1 and M2 split
+ * the ECCT mask of Section 3 (distance <= 2) exactly.
+ * Pin: symmetric, disjoint, union = BFS distance <= 2, closed-form counts.
+ */
+void oracle_masks(const uint8_t *H, int32_t m, int32_t n, uint8_t *M1, uint8_t *M2) {
+  const int32_t L = n + m;
+  memset(M1, 0, (size_t)L * L);
+  memset(M2, 0, (size_t)L * L);
+  for (int32_t j = 0; j < m; ++j)
+    for (int32_t i = 0; i < n; ++i)
+      if (H[(int64_t)j * n + i]) {
+        M1[(int64_t)i * L + n + j] = 1;
+        M1[(int64_t)(n + j) * L + i] = 1;
+      }
+  for (int32_t a = 0; a < L; ++a)
+    for (int32_t k = 0; k < L; ++k)
+      if (M1[(int64_t)a * L + k])
+        for (int32_t b = 0; b < L; ++b)
+          if (M1[(int64_t)k * L + b]) M2[(int64_t)a * L + b] = 1;
+}
+
+/*
+ * Pre-processing h(y) of Section 3: bin(y) = 0.5(1 - sign(y)), i.e. bit 1 iff
+ * y < 0; syndrome s = H bin(y) over GF(2); tokens [|y|, 1 - 2s].
+ * Pin: every noiseless codeword gives s = 0; a single flipped bit gives the
+ * matching column of H.
+ */
+void oracle_preprocess(const uint8_t *H, int32_t m, int32_t n, const float *y, float *t) {
+  for (int32_t i = 0; i < n; ++i) t[i] = fabsf(y[i]);
+  for (int32_t j = 0; j < m; ++j) {
+    int s = 0;
+    for (int32_t i = 0; i < n; ++i)
+      if (H[(int64_t)j * n + i] && y[i] < 0.0f) s ^= 1;
+    t[n + j] = s ? -1.0f : 1.0f;
+  }
+}
+
+/*
+ * Absmax int8 activation quantisation, Eq. 2 with Q_b = 127, applied per token
+ * row: alpha = max|x|, q = RoundClip(x * (Q_b / alpha), -Q_b, Q_b) with
+ * round-half-to-even.  An all-zero row gives q = 0 and alpha = 0.
+ * Pin: |q| <= 127, the argmax maps to +-127, sign kept, monotone, error bound.
+ */
+void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float *r) {
+  for (int64_t i = 0; i < rows; ++i) {
+    const float *xi = x + i * K;
+    int8_t *qi = q + i * K;
+    float a = 0.0f;
+    for (int32_t c = 0; c < K; ++c) {
+      float v = fabsf(xi[c]);
+      if (v > a) a = v;
+    }
+    if (a == 0.0f) {
+      memset(qi, 0, (size_t)K);
+      r[i] = 0.0f;
+      continue;
+    }
+    float inv = 127.0f / a;
+    for (int32_t c = 0; c < K; ++c) {
+      float v = rintf(xi[c] * inv);
+      if (v > 127.0f) v = 127.0f;
+      if (v < -127.0f) v = -127.0f;
+      qi[c] = (int8_t)v;
+    }
+    r[i] = a;
+  }
+}
+
+/*
+ * AAPLinear at inference, Eq. 3: integer product of the int8 activations and
+ * the ternary weights (additions and subtractions only), dequantised by
+ * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  The dequant
+ * and bias are one fused multiply-add: out = fma(acc, (s*alpha)/127, b).
+ * Pin: accumulators equal an int64 library matmul; zero weights give the bias.
+ */
+void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int8_t *T, int32_t K,
+                        int32_t n_out, float s, const float *b, float *out, int32_t *acc) {
+  for (int64_t i = 0; i < rows; ++i) {
+    const int8_t *qi = q + i * K;
+    float sc = (s * r[i]) / 127.0f;
+    for (int32_t o = 0; o < n_out; ++o) {
+      int32_t a = 0;
+      for (int32_t c = 0; c < K; ++c) a += (int32_t)qi[c] * (int32_t)T[(int64_t)c * n_out + o];
+      if (acc) acc[i * n_out + o] = a;
+      out[i * n_out + o] = fmaf((float)a, sc, b[o]);
+    }
+  }
+}
+
+/*
+ * LayerNorm of the Post-LN block (Section 6): mean and biased variance over
+ * the d features (TREE sums), out = (x - mean) / sqrt(var + eps) * g + b,
+ * evaluated as fma((x - mean) * (1 / sqrtf(var + eps)), g, b).
+ * Pin: within 1e-5 of the fp64 library layer_norm.
+ */
+void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float *g, const float *b,
+                           float eps, float *out) {
+  float e[ORC_MAX_TREE], sq[ORC_MAX_TREE];
+  for (int64_t i = 0; i < rows; ++i) {
+    const float *ri = R + i * d;
+    float mean = oracle_tree_sum(ri, d) / (float)d;
+    for (int32_t c = 0; c < d; ++c) {
+      e[c] = ri[c] - mean;
+      sq[c] = e[c] * e[c];
+    }
+    float var = oracle_tree_sum(sq, d) / (float)d;
+    float rho = 1.0f / sqrtf(var + eps);
+    for (int32_t c = 0; c < d; ++c) out[i * d + c] = fmaf(e[c] * rho, g[c], b[c]);
+  }
+}
+
+static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_t h, int32_t dh,
+                       float kappa) {
+  float p[ORC_MAX_TREE];
+  const float *qi = qkv + (int64_t)i * 3 * d + h * dh;
+  const float *kj = qkv + (int64_t)j * 3 * d + d + h * dh;
+  for (int32_t t = 0; t < dh; ++t) p[t] = qi[t] * kj[t];
+  return oracle_tree_sum(p, dh) * kappa;
+}
+
+/*
+ * Head-partitioned self-attention (Section 4.2): heads 0..h_f-1 attend over
+ * the first-ring mask M1, the others over the second-ring mask M2.  Per row i
+ * and head h the softmax of the scaled dot products over the allowed keys j
+ * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.
+ * Score s_j = TREE(q*k, d_h) * kappa; mu = max s_j; e_j = EXP(s_j - mu);
+ * S = SEQ sum e_j; o = (SEQ fma(e_j, v_j, acc)) / S.  Returns 0, or -1 for a
+ * row with no allowed key.
+ * Pin: within 1e-6 relative of the fp64 dense (-inf)-masked softmax; a row
+ * with one allowed key returns that value row exactly.
+ */
+int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
+                          const float *qkv, float *o) {
+  const int32_t L = M->n + M->m, d = M->d, dh = M->d / M->heads;
+  const float kappa = (float)(1.0 / sqrt((double)dh));
+  for (int32_t i = 0; i < L; ++i)
+    for (int32_t h = 0; h < M->heads; ++h) {
+      const uint8_t *row = (h < M->first_ring_heads ? M1 : M2) + (int64_t)i * L;
+      float mu = -INFINITY;
+      int cnt = 0;
+      for (int32_t j = 0; j < L; ++j)
+        if (row[j]) {
+          float s = score_f32(qkv, d, i, j, h, dh, kappa);
+          if (s > mu) mu = s;
+          ++cnt;
+        }
+      if (cnt == 0) return -1;
+      float S = 0.0f, acc[ORC_MAX_TREE];
+      for (int32_t t = 0; t < dh; ++t) acc[t] = 0.0f;
+      for (int32_t j = 0; j < L; ++j)
+        if (row[j]) {
+          float e = oracle_exp(score_f32(qkv, d, i, j, h, dh, kappa) - mu);
+          S = S + e;
+          const float *vj = qkv + (int64_t)j * 3 * d + 2 * d + h * dh;
+          for (int32_t t = 0; t < dh; ++t) acc[t] = fmaf(e, vj[t], acc[t]);
+        }
+      for (int32_t t = 0; t < dh; ++t) o[(int64_t)i * d + h * dh + t] = acc[t] / S;
+    }
+  return 0;
+}
+
+/*
+ * Output head and hard decision (Section 3): per token z_i = W_{d->1} x_i + b1
+ * (TREE over d), noise estimate f_o = sum_i z_i W_o[i][o] + b_o (SEQ over the
+ * L tokens), soft codeword y * f and bit = bin(y * f) = [y < 0] xor [f < 0].
+ * Pin: codeword invariance decode(x_s + e) xor x == decode(1 + x_s e).
+ */
+void oracle_head_word(const oracle_model *M, const float *X, const float *y, float *f, uint8_t *bits,
+                      float *z) {
+  const int32_t L = M->n + M->m, d = M->d, n = M->n;
+  float zz[ORC_MAX_TREE], p[ORC_MAX_TREE];
+  for (int32_t i = 0; i < L; ++i) {
+    for (int32_t c = 0; c < d; ++c) p[c] = X[(int64_t)i * d + c] * M->head_w1[c];
+    zz[i] = oracle_tree_sum(p, d) + M->head_b1;
+    if (z) z[i] = zz[i];
+  }
+  for (int32_t o = 0; o < n; ++o) {
+    float acc = 0.0f;
+    for (int32_t i = 0; i < L; ++i) acc = fmaf(zz[i], M->head_wo[(int64_t)i * n + o], acc);
+    float fo = acc + M->head_bo[o];
+    f[o] = fo;
+    bits[o] = (uint8_t)((y[o] < 0.0f) ^ (fo < 0.0f));
+  }
+}
+
+/* ------------------------------------------------------------------ whole decode */
+
+typedef struct {
+  float *t, *X, *qkv, *O, *X1, *F, *Y, *R;
+  int8_t *q, *gq;
+  float *r, *rg;
+  int32_t *acc, *accf;
+} word_buf;
+
+static int alloc_buf(const oracle_model *M, word_buf *w) {
+  const int64_t L = M->n + M->m, d = M->d, dff = M->d_ff;
+  w->t = malloc(sizeof(float) * L);
+  w->X = malloc(sizeof(float) * L * d);
+  w->qkv = malloc(sizeof(float) * L * 3 * d);
+  w->O = malloc(sizeof(float) * L * d);
+  w->X1 = malloc(sizeof(float) * L * d);
+  w->F = malloc(sizeof(float) * L * dff);
+  w->Y = malloc(sizeof(float) * L * (dff > 3 * d ? dff : 3 * d));
+  w->R = malloc(sizeof(float) * L * d);
+  w->q = malloc((size_t)(L * (dff > d ? dff : d)));
+  w->gq = malloc((size_t)(L * dff));
+  w->r = malloc(sizeof(float) * L);
+  w->rg = malloc(sizeof(float) * L);
+  w->acc = malloc(sizeof(int32_t) * L * d);
+  w->accf = malloc(sizeof(int32_t) * L * dff);
+  return (w->t && w->X && w->qkv && w->O && w->X1 && w->F && w->Y && w->R && w->q && w->gq &&
+          w->r && w->rg && w->acc && w->accf) ? 0 : -1;
+}
+
+static void free_buf(word_buf *w) {
+  free(w->t); free(w->X); free(w->qkv); free(w->O); free(w->X1); free(w->F); free(w->Y);
+  free(w->R); free(w->q); free(w->gq); free(w->r); free(w->rg); free(w->acc); free(w->accf);
+}
+
+static const int8_t *wmat(const oracle_model *M, int kind, int layer) {
+  return M->w[kind] + (int64_t)layer * lin_in(M, kind) * lin_out(M, kind);
+}
+static const float *bvec(const oracle_model *M, int kind, int layer) {
+  return M->bias[kind] + (int64_t)layer * lin_out(M, kind);
+}
+
+/* One word through embedding, N encoder blocks and the head (Sections 3, 4, 6). */
+static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2, const float *y,
+                       uint8_t *bits, float *f, word_buf *w, const oracle_taps *tp) {
+  const int64_t L = M->n + M->m, d = M->d, dff = M->d_ff;
+  /* embedding of the 2n-k input scalars: X_i = t_i * E_i (+ fixed positional row) */
+  oracle_preprocess(M->H, M->m, M->n, y, w->t);
+  for (int64_t i = 0; i < L; ++i)
+    for (int64_t c = 0; c < d; ++c)
+      w->X[i * d + c] = fmaf(w->t[i], M->embed[i * d + c], M->pos ? M->pos[i * d + c] : 0.0f);
+
+  for (int32_t l = 0; l < M->n_layers; ++l) {
+    const float *sc = M->scale + (int64_t)l * 6;
+    const int64_t LD = L * d;
+    if (tp && tp->x_in) memcpy(tp->x_in + l * LD, w->X, sizeof(float) * LD);
+    /* a. Q, K, V from the int8 input */
+    oracle_quant_rows(w->X, L, (int32_t)d, w->q, w->r);
+    if (tp && tp->xq) memcpy(tp->xq + l * LD, w->q, (size_t)LD);
+    if (tp && tp->ax) memcpy(tp->ax + l * L, w->r, sizeof(float) * L);
+    for (int kind = ORC_Q; kind <= ORC_V; ++kind) {
+      oracle_linear_rows(w->q, w->r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d, sc[kind],
+                         bvec(M, kind, l), w->Y, NULL);
+      for (int64_t i = 0; i < L; ++i)
+        memcpy(w->qkv + i * 3 * d + kind * d, w->Y + i * d, sizeof(float) * d);
+    }
+    if (tp && tp->qkv) memcpy(tp->qkv + l * 3 * LD, w->qkv, sizeof(float) * 3 * LD);
+    /* b. head-partitioned attention */
+    if (oracle_attention_word(M, M1, M2, w->qkv, w->O)) return -1;
+    if (tp && tp->o) memcpy(tp->o + l * LD, w->O, sizeof(float) * LD);
+    /* c. output projection, residual, LN1 */
+    oracle_quant_rows(w->O, L, (int32_t)d, w->q, w->r);
+    if (tp && tp->oq) memcpy(tp->oq + l * LD, w->q, (size_t)LD);
+    if (tp && tp->ao) memcpy(tp->ao + l * L, w->r, sizeof(float) * L);
+    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O],
+                       bvec(M, ORC_O, l), w->Y, w->acc);
+    if (tp && tp->acc_o) memcpy(tp->acc_o + l * LD, w->acc, sizeof(int32_t) * LD);
+    for (int64_t e = 0; e < LD; ++e) w->R[e] = w->X[e] + w->Y[e];
+    oracle_layernorm_rows(w->R, L, (int32_t)d, M->ln1_g + l * d, M->ln1_b + l * d, M->ln_eps, w->X1);
+    if (tp && tp->x1) memcpy(tp->x1 + l * LD, w->X1, sizeof(float) * LD);
+    /* d. FFN with ReLU, residual, LN2 */
+    oracle_quant_rows(w->X1, L, (int32_t)d, w->q, w->r);
+    if (tp && tp->x1q) memcpy(tp->x1q + l * LD, w->q, (size_t)LD);
+    if (tp && tp->a1) memcpy(tp->a1 + l * L, w->r, sizeof(float) * L);
+    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sc[ORC_FF1],
+                       bvec(M, ORC_FF1, l), w->F, w->accf);
+    if (tp && tp->acc_ff1) memcpy(tp->acc_ff1 + l * L * dff, w->accf, sizeof(int32_t) * L * dff);
+    for (int64_t e = 0; e < L * dff; ++e) w->F[e] = w->F[e] > 0.0f ? w->F[e] : 0.0f;
+    oracle_quant_rows(w->F, L, (int32_t)dff, w->gq, w->rg);
+    if (tp && tp->gq) memcpy(tp->gq + l * L * dff, w->gq, (size_t)(L * dff));
+    if (tp && tp->ag) memcpy(tp->ag + l * L, w->rg, sizeof(float) * L);
+    oracle_linear_rows(w->gq, w->rg, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sc[ORC_FF2],
+                       bvec(M, ORC_FF2, l), w->Y, w->acc);
+    if (tp && tp->acc_ff2) memcpy(tp->acc_ff2 + l * LD, w->acc, sizeof(int32_t) * LD);
+    for (int64_t e = 0; e < LD; ++e) w->R[e] = w->X1[e] + w->Y[e];
+    oracle_layernorm_rows(w->R, L, (int32_t)d, M->ln2_g + l * d, M->ln2_b + l * d, M->ln_eps, w->X);
+    if (tp && tp->x_out) memcpy(tp->x_out + l * LD, w->X, sizeof(float) * LD);
+  }
+  oracle_head_word(M, w->X, y, f, bits, tp ? tp->z : NULL);
+  return 0;
+}
+
+static int check_model(const oracle_model *M) {
+  if (M->d <= 0 || M->heads <= 0 || M->d % M->heads) return -1;
+  int32_t dh = M->d / M->heads;
+  if ((M->d & (M->d - 1)) || (dh & (dh - 1))) return -1;
+  if (M->d > ORC_MAX_TREE || M->d_ff > ORC_MAX_TREE || M->n + M->m > ORC_MAX_TREE) return -1;
+  return 0;
+}
+
+int oracle_decode(const oracle_model *M, const float *y, int64_t batch, uint8_t *bits, float *f,
+                  int32_t n_threads) {
+  if (check_model(M)) return -1;
+  const int64_t L = M->n + M->m;
+  uint8_t *M1 = malloc((size_t)(L * L)), *M2 = malloc((size_t)(L * L));
+  if (!M1 || !M2) { free(M1); free(M2); return -1; }
+  oracle_masks(M->H, M->m, M->n, M1, M2);
+  int err = 0;
+#ifdef _OPENMP
+  if (n_threads < 1) n_threads = 1;
+#pragma omp parallel num_threads(n_threads) reduction(| : err)
+#endif
+  {
+    word_buf w;
+    if (alloc_buf(M, &w)) {
+      err |= 1;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t b = 0; b < batch; ++b)
+        if (decode_word(M, M1, M2, y + b * M->n, bits + b * M->n, f + b * M->n, &w, NULL)) err |= 1;
+    }
+    free_buf(&w);
+  }
+  free(M1);
+  free(M2);
+  return err ? -1 : 0;
+}
+
+int oracle_decode_taps(const oracle_model *M, const float *y, uint8_t *bits, float *f,
+                       const oracle_taps *taps) {
+  if (check_model(M)) return -1;
+  const int64_t L = M->n + M->m;
+  uint8_t *M1 = malloc((size_t)(L * L)), *M2 = malloc((size_t)(L * L));
+  word_buf w;
+  int err = (!M1 || !M2 || alloc_buf(M, &w)) ? -1 : 0;
+  if (!err) {
+    oracle_masks(M->H, M->m, M->n, M1, M2);
+    err = decode_word(M, M1, M2, y, bits, f, &w, taps);
+    free_buf(&w);
+  }
+  free(M1);
+  free(M2);
+  return err;
+}
+
+/* ------------------------------------------------------------------ fp64 reference mode */
+
+static void quant_rows_f64(const double *x, int64_t rows, int32_t K, int32_t *q, double *r) {
+  for (int64_t i = 0; i < rows; ++i) {
+    double a = 0.0;
+    for (int32_t c = 0; c < K; ++c) a = fmax(a, fabs(x[i * K + c]));
+    r[i] = a;
+    for (int32_t c = 0; c < K; ++c) {
+      double v = a == 0.0 ? 0.0 : rint(x[i * K + c] * (127.0 / a));
+      q[i * K + c] = (int32_t)fmin(127.0, fmax(-127.0, v));
+    }
+  }
+}
+
+static void linear_rows_f64(const int32_t *q, const double *r, int64_t rows, const int8_t *T,
+                            int32_t K, int32_t n_out, double s, const float *b, double *out) {
+  for (int64_t i = 0; i < rows; ++i)
+    for (int32_t o = 0; o < n_out; ++o) {
+      int64_t a = 0;
+      for (int32_t c = 0; c < K; ++c) a += (int64_t)q[i * K + c] * T[(int64_t)c * n_out + o];
+      out[i * n_out + o] = (double)a * (s * r[i] / 127.0) + (double)b[o];
+    }
+}
+
+static void layernorm_f64(double *R, int64_t rows, int32_t d, const float *g, const float *b,
+                          double eps) {
+  for (int64_t i = 0; i < rows; ++i) {
+    double *ri = R + i * d, mean = 0.0, var = 0.0;
+    for (int32_t c = 0; c < d; ++c) mean += ri[c];
+    mean /= d;
+    for (int32_t c = 0; c < d; ++c) var += (ri[c] - mean) * (ri[c] - mean);
+    var /= d;
+    for (int32_t c = 0; c < d; ++c) ri[c] = (ri[c] - mean) / sqrt(var + eps) * g[c] + b[c];
+  }
+}
+
+/* Dense attention: softmax over all L keys with the masked scores set to -inf. */
+int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
+                               const double *qkv, double *o) {
+  const int32_t L = M->n + M->m, d = M->d, dh = M->d / M->heads;
+  double *s = malloc(sizeof(double) * L);
+  if (!s) return -1;
+  for (int32_t i = 0; i < L; ++i)
+    for (int32_t h = 0; h < M->heads; ++h) {
+      const uint8_t *row = (h < M->first_ring_heads ? M1 : M2) + (int64_t)i * L;
+      double mx = -INFINITY;
+      for (int32_t j = 0; j < L; ++j) {
+        double dot = 0.0;
+        for (int32_t t = 0; t < dh; ++t)
+          dot += qkv[(int64_t)i * 3 * d + h * dh + t] * qkv[(int64_t)j * 3 * d + d + h * dh + t];
+        s[j] = row[j] ? dot / sqrt((double)dh) : -INFINITY;
+        if (s[j] > mx) mx = s[j];
+      }
+      if (mx == -INFINITY) { free(s); return -1; }
+      double S = 0.0;
+      for (int32_t j = 0; j < L; ++j) { s[j] = exp(s[j] - mx); S += s[j]; }
+      for (int32_t t = 0; t < dh; ++t) {
+        double acc = 0.0;
+        for (int32_t j = 0; j < L; ++j) acc += s[j] / S * qkv[(int64_t)j * 3 * d + 2 * d + h * dh + t];
+        o[(int64_t)i * d + h * dh + t] = acc;
+      }
+    }
+  free(s);
+  return 0;
+}
+
+int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, uint8_t *bits,
+                        double *f, int32_t n_threads) {
+  if (check_model(M)) return -1;
+  const int64_t L = M->n + M->m, d = M->d, dff = M->d_ff, n = M->n;
+  uint8_t *M1 = malloc((size_t)(L * L)), *M2 = malloc((size_t)(L * L));
+  if (!M1 || !M2) { free(M1); free(M2); return -1; }
+  oracle_masks(M->H, M->m, M->n, M1, M2);
+  int err = 0;
+#ifdef _OPENMP
+  if (n_threads < 1) n_threads = 1;
+#pragma omp parallel for num_threads(n_threads) schedule(dynamic, 1) reduction(| : err)
+#endif
+  for (int64_t b = 0; b < batch; ++b) {
+    const float *yb = y + b * n;
+    double *X = malloc(sizeof(double) * L * d), *qkv = malloc(sizeof(double) * L * 3 * d);
+    double *O = malloc(sizeof(double) * L * d), *Y = malloc(sizeof(double) * L * dff);
+    double *X1 = malloc(sizeof(double) * L * d), *r = malloc(sizeof(double) * L);
+    int32_t *q = malloc(sizeof(int32_t) * L * dff);
+    float *t = malloc(sizeof(float) * L);
+    if (!X || !qkv || !O || !Y || !X1 || !r || !q || !t) {
+      err |= 1;
+    } else {
+      oracle_preprocess(M->H, M->m, M->n, yb, t);
+      for (int64_t i = 0; i < L; ++i)
+        for (int64_t c = 0; c < d; ++c)
+          X[i * d + c] = (double)t[i] * M->embed[i * d + c] + (M->pos ? M->pos[i * d + c] : 0.0);
+      for (int32_t l = 0; l < M->n_layers && !err; ++l) {
+        const float *sc = M->scale + (int64_t)l * 6;
+        quant_rows_f64(X, L, (int32_t)d, q, r);
+        for (int kind = ORC_Q; kind <= ORC_V; ++kind) {
+          linear_rows_f64(q, r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d, sc[kind], bvec(M, kind, l), Y);
+          for (int64_t i = 0; i < L; ++i)
+            for (int64_t c = 0; c < d; ++c) qkv[i * 3 * d + kind * d + c] = Y[i * d + c];
+        }
+        if (oracle_attention_dense_f64(M, M1, M2, qkv, O)) { err |= 1; break; }
+        quant_rows_f64(O, L, (int32_t)d, q, r);
+        linear_rows_f64(q, r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O], bvec(M, ORC_O, l), Y);
+        for (int64_t e = 0; e < L * d; ++e) X1[e] = X[e] + Y[e];
+        layernorm_f64(X1, L, (int32_t)d, M->ln1_g + l * d, M->ln1_b + l * d, M->ln_eps);
+        quant_rows_f64(X1, L, (int32_t)d, q, r);
+        linear_rows_f64(q, r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sc[ORC_FF1], bvec(M, ORC_FF1, l), Y);
+        for (int64_t e = 0; e < L * dff; ++e) Y[e] = Y[e] > 0.0 ? Y[e] : 0.0;
+        quant_rows_f64(Y, L, (int32_t)dff, q, r);
+        linear_rows_f64(q, r, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sc[ORC_FF2], bvec(M, ORC_FF2, l), X);
+        for (int64_t e = 0; e < L * d; ++e) X[e] = X1[e] + X[e];
+        layernorm_f64(X, L, (int32_t)d, M->ln2_g + l * d, M->ln2_b + l * d, M->ln_eps);
+      }
+      if (!err) {
+        for (int64_t i = 0; i < L; ++i) {          /* z_i = W_{d->1} x_i + b1, kept in r */
+          double z = M->head_b1;
+          for (int64_t c = 0; c < d; ++c) z += X[i * d + c] * M->head_w1[c];
+          r[i] = z;
+        }
+        for (int64_t o = 0; o < n; ++o) {
+          double acc = M->head_bo[o];
+          for (int64_t i = 0; i < L; ++i) acc += r[i] * M->head_wo[i * n + o];
+          f[b * n + o] = acc;
+          bits[b * n + o] = (uint8_t)((yb[o] < 0.0f) ^ (acc < 0.0));
+        }
+      }
+    }
+    free(X); free(qkv); free(O); free(Y); free(X1); free(r); free(q); free(t);
+  }
+  free(M1);
+  free(M2);
+  return err ? -1 : 0;
+}

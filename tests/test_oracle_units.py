@@ -1,0 +1,203 @@
+"""Pins of the CPU oracle's building blocks against facts fixed outside it.
+
+Each test checks an oracle function against mathematics or an independent library
+routine (numpy int64 matmul, torch fp64 layer_norm / scaled-dot-product attention,
+Python's math.exp), never against a retyped copy of the oracle's own formula.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from workloads import CONFIGS, build_workload, random_weights
+from workloads.configs import parity_check
+
+
+def _ulp(x):
+    return np.spacing(np.float32(abs(x)))
+
+
+# ------------------------------------------------------------------------ TREE order
+def test_tree_sum_pairs_stride_halving(oracle_mod):
+    # pairs (v0+v2), (v1+v3): the large terms cancel first, so the exact 2 survives;
+    # a left-to-right sum would absorb the first 1 into 1e8 and give 1.
+    assert oracle_mod.tree_sum([1e8, 1.0, -1e8, 1.0]) == np.float32(2.0)
+    # w = 8: stride 4 pairs (0,4),(1,5),(2,6),(3,7)
+    v = np.array([1e8, 0, 0, 1, -1e8, 0, 0, 1], np.float32)
+    assert oracle_mod.tree_sum(v) == np.float32(2.0)
+    rng = np.random.default_rng(0)
+    for w in (1, 2, 4, 8, 16, 32, 64, 128, 512):
+        ints = rng.integers(-1000, 1000, w).astype(np.float32)
+        assert oracle_mod.tree_sum(ints) == np.float32(ints.astype(np.int64).sum())  # exact integer sums
+        x = rng.standard_normal(w).astype(np.float32)
+        exact = math.fsum(x.astype(np.float64))
+        bound = (max(1, math.log2(w)) * 2 ** -24) * np.abs(x).astype(np.float64).sum() * 1.01
+        assert abs(float(oracle_mod.tree_sum(x)) - exact) <= bound + 1e-30
+
+
+# ------------------------------------------------------------------------ EXP
+def test_exp_close_to_libm_and_exact_at_zero(oracle_mod):
+    assert oracle_mod.exp(0.0) == np.float32(1.0)
+    assert oracle_mod.exp(-0.0) == np.float32(1.0)
+    assert oracle_mod.exp(-80.5) == 0.0 and oracle_mod.exp(-1e4) == 0.0
+    xs = np.concatenate([-np.linspace(0, 80, 40001, dtype=np.float32),
+                         -np.random.default_rng(1).random(20000).astype(np.float32) * 80])
+    worst = 0.0
+    for x in xs:
+        e = float(oracle_mod.exp(x))
+        ref = math.exp(float(x))
+        worst = max(worst, abs(e - ref) / float(_ulp(ref)))
+    assert worst <= 2.0, worst
+
+
+# ------------------------------------------------------------------------ pre-processing
+def test_syndrome_of_codewords_is_zero(oracle_mod):
+    for c in (1, 2, 3):
+        cfg, H, G, w, y, x = build_workload(c, batch=64)
+        m, n = H.shape
+        xs = (1.0 - 2.0 * x).astype(np.float32)
+        for b in range(16):
+            t = oracle_mod.preprocess(H, xs[b])
+            assert (t[:n] == 1.0).all()
+            assert (t[n:] == 1.0).all()                       # s = 0  ->  1 - 2s = +1
+            # magnitudes of a noisy word, and -0.0 counts as a positive sign (bit 0)
+            t = oracle_mod.preprocess(H, y[b])
+            assert (t[:n] == np.abs(y[b])).all()
+        z = np.zeros(n, np.float32)
+        z[0] = -0.0
+        assert (oracle_mod.preprocess(H, z)[n:] == 1.0).all()
+
+
+def test_single_error_syndrome_is_column(oracle_mod):
+    H = parity_check(CONFIGS[2])
+    m, n = H.shape
+    for i in range(n):
+        y = np.ones(n, np.float32)
+        y[i] = -0.3
+        t = oracle_mod.preprocess(H, y)
+        s = (1 - t[n:]) / 2
+        assert (s.astype(np.uint8) == H[:, i]).all()
+
+
+# ------------------------------------------------------------------------ quantisation (Eq. 2)
+def test_quant_invariants(oracle_mod):
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal((400, 128)) * rng.exponential(1, (400, 1))).astype(np.float32)
+    q, r = oracle_mod.quant_rows(x)
+    assert (np.abs(q.astype(int)) <= 127).all()
+    assert (r == np.abs(x).max(1)).all()
+    am = np.abs(x).argmax(1)
+    assert (np.abs(q[np.arange(400), am]) == 127).all()
+    assert ((np.sign(q) == np.sign(x)) | (q == 0)).all()
+    # monotone within a row
+    for i in range(20):
+        o = np.argsort(x[i], kind="stable")
+        assert (np.diff(q[i][o].astype(int)) >= 0).all()
+    err = np.abs(x.astype(np.float64) - q * r[:, None].astype(np.float64) / 127)
+    assert (err <= r[:, None] / 254 * (1 + 2 ** -20)).all()
+
+
+def test_quant_zero_row_and_half_even(oracle_mod):
+    q, r = oracle_mod.quant_rows(np.zeros((2, 8), np.float32))
+    assert (q == 0).all() and (r == 0).all()
+    # alpha = 127 -> Q_b / alpha = 1 exactly: rounding ties go to even
+    x = np.array([[127.0, 2.5, 3.5, -2.5, -0.5, 0.5, 1.5, -126.5]], np.float32)
+    q, r = oracle_mod.quant_rows(x)
+    assert q[0].tolist() == [127, 2, 4, -2, 0, 0, 2, -126]
+
+
+# ------------------------------------------------------------------------ AAPLinear (Eq. 3)
+def test_linear_accumulators_and_dequant(oracle_mod):
+    rng = np.random.default_rng(4)
+    for K, N in ((32, 96), (128, 32), (512, 128)):
+        q = rng.integers(-127, 128, (50, K)).astype(np.int8)
+        T = rng.choice(np.array([-1, 0, 1], np.int8), (K, N))
+        r = (rng.random(50) * 3).astype(np.float32)
+        b = rng.standard_normal(N).astype(np.float32)
+        s = np.float32(1 / math.sqrt(K))
+        out, acc = oracle_mod.linear_rows(q, r, T, s, b)
+        assert (acc == q.astype(np.int64) @ T.astype(np.int64)).all()
+        ref = acc.astype(np.float64) * (float(s) * r[:, None].astype(np.float64) / 127) + b.astype(np.float64)
+        assert np.allclose(out, ref, rtol=4e-7, atol=4e-7)
+        out0, acc0 = oracle_mod.linear_rows(q, r, np.zeros_like(T), s, b)
+        assert (acc0 == 0).all() and (out0 == b[None, :]).all()      # zero weights: output = bias
+
+
+# ------------------------------------------------------------------------ LayerNorm
+def test_layernorm_against_torch_fp64(oracle_mod):
+    rng = np.random.default_rng(5)
+    for d in (32, 64, 128):
+        R = (rng.standard_normal((300, d)) * 3 + rng.standard_normal((300, 1))).astype(np.float32)
+        g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+        b = (0.1 * rng.standard_normal(d)).astype(np.float32)
+        out = oracle_mod.layernorm_rows(R, g, b, 1e-5)
+        ref = torch.nn.functional.layer_norm(torch.tensor(R, dtype=torch.float64), (d,),
+                                             torch.tensor(g, dtype=torch.float64),
+                                             torch.tensor(b, dtype=torch.float64), eps=1e-5).numpy()
+        assert np.abs(out - ref).max() <= 1e-5
+
+
+# ------------------------------------------------------------------------ HPSA attention
+def _sdpa_reference(H, w, qkv):
+    """torch fp64 scaled-dot-product attention per head with boolean masks from H."""
+    m, n = H.shape
+    L = n + m
+    A = np.zeros((L, L), np.int64)
+    A[:n, n:] = H.T
+    A[n:, :n] = H
+    M1 = torch.tensor(A != 0)
+    M2 = torch.tensor((A @ A) != 0)
+    d, h = w.d, w.heads
+    dh = d // h
+    t = torch.tensor(qkv, dtype=torch.float64)
+    Q, K, V = t[:, :d], t[:, d:2 * d], t[:, 2 * d:]
+    out = torch.zeros(L, d, dtype=torch.float64)
+    for hh in range(h):
+        sl = slice(hh * dh, (hh + 1) * dh)
+        mask = M1 if hh < w.first_ring_heads else M2
+        out[:, sl] = torch.nn.functional.scaled_dot_product_attention(
+            Q[None, None, :, sl], K[None, None, :, sl].contiguous(), V[None, None, :, sl], attn_mask=mask,
+            scale=1.0 / math.sqrt(dh))[0, 0]
+    return out.numpy()
+
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_attention_against_fp64_sdpa(oracle_mod, c):
+    cfg, H, G, w, y, x = build_workload(c, batch=1)
+    om = oracle_mod.OracleModel(H, w)
+    rng = np.random.default_rng(6)
+    qkv = (rng.standard_normal((om.L, 3 * w.d)) * 2).astype(np.float32)
+    o = om.attention(qkv)
+    ref = _sdpa_reference(H, w, qkv)
+    assert np.abs(o - ref).max() <= 1e-6 * max(1.0, np.abs(ref).max())
+    o64 = om.attention_dense_f64(qkv)                       # the oracle's own dense fp64 mode
+    assert np.abs(o64 - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max())
+
+
+def test_attention_single_neighbour_rows_exact(oracle_mod):
+    """Hamming variables 4, 5, 6 have one check each: their first-ring rows copy that check's V."""
+    cfg, H, G, w, y, x = build_workload(1, batch=1)
+    om = oracle_mod.OracleModel(H, w)
+    rng = np.random.default_rng(7)
+    qkv = rng.standard_normal((om.L, 3 * w.d)).astype(np.float32)
+    o = om.attention(qkv)
+    d, dh, n = w.d, w.d // w.heads, H.shape[1]
+    for v in (4, 5, 6):
+        (chk,) = np.nonzero(H[:, v])[0]
+        for hh in range(w.first_ring_heads):
+            sl = slice(hh * dh, (hh + 1) * dh)
+            assert (o[v, sl] == qkv[n + chk, 2 * d:][sl]).all()
+
+
+# ------------------------------------------------------------------------ head
+def test_head_against_fp64(oracle_mod):
+    cfg, H, G, w, y, x = build_workload(2, batch=4)
+    om = oracle_mod.OracleModel(H, w)
+    rng = np.random.default_rng(8)
+    X = rng.standard_normal((om.L, w.d)).astype(np.float32)
+    f, bits, z = om.head(X, y[0])
+    z64 = X.astype(np.float64) @ w.head_w1.astype(np.float64) + w.head_b1
+    f64 = z64 @ w.head_wo.astype(np.float64) + w.head_bo
+    assert np.abs(z - z64).max() <= 1e-5 and np.abs(f - f64).max() <= 1e-5
+    assert (bits == ((y[0] * f) < 0)).all()                 # bin(y * f)
