@@ -145,15 +145,16 @@ void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float
 /*
  * AAPLinear at inference, Eq. 3: integer product of the int8 activations and
  * the ternary weights (additions and subtractions only), dequantised by
- * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  The dequant
- * and bias are one fused multiply-add: out = fma(acc, (s*alpha)/127, b).
+ * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  The scale is
+ * evaluated as alpha * (s / 127) with s = gamma*delta, and dequant plus bias is
+ * one fused multiply-add: out = fma(acc, alpha * (s / 127), b).
  * Pin: accumulators equal an int64 library matmul; zero weights give the bias.
  */
 void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int8_t *T, int32_t K,
                         int32_t n_out, float s, const float *b, float *out, int32_t *acc) {
   for (int64_t i = 0; i < rows; ++i) {
     const int8_t *qi = q + i * K;
-    float sc = (s * r[i]) / 127.0f;
+    float sc = r[i] * (s / 127.0f);
     for (int32_t o = 0; o < n_out; ++o) {
       int32_t a = 0;
       for (int32_t c = 0; c < K; ++c) a += (int32_t)qi[c] * (int32_t)T[(int64_t)c * n_out + o];
@@ -200,7 +201,7 @@ static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_
  * and head h the softmax of the scaled dot products over the allowed keys j
  * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.
  * Score s_j = TREE(q*k, d_h) * kappa; mu = max s_j; e_j = EXP(s_j - mu);
- * S = SEQ sum e_j; o = (SEQ fma(e_j, v_j, acc)) / S.  Returns 0, or -1 for a
+ * S = SEQ sum e_j; o = (SEQ fma(e_j, v_j, acc)) * (1 / S).  Returns 0, or -1 for a
  * row with no allowed key.
  * Pin: within 1e-6 relative of the fp64 dense (-inf)-masked softmax; a row
  * with one allowed key returns that value row exactly.
@@ -230,7 +231,8 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
           const float *vj = qkv + (int64_t)j * 3 * d + 2 * d + h * dh;
           for (int32_t t = 0; t < dh; ++t) acc[t] = fmaf(e, vj[t], acc[t]);
         }
-      for (int32_t t = 0; t < dh; ++t) o[(int64_t)i * d + h * dh + t] = acc[t] / S;
+      const float rS = 1.0f / S;
+      for (int32_t t = 0; t < dh; ++t) o[(int64_t)i * d + h * dh + t] = acc[t] * rS;
     }
   return 0;
 }
