@@ -1,0 +1,187 @@
+"""Throughput of the AECCT decode on one MI355X.
+
+Workload: BCH(31,16) (cyclic H from the t = 3 generator polynomial), d = 32, N = 6 layers,
+8 heads (4 first-ring, 4 second-ring), ternary weights with P(0) = 0.5, a batch of 65536
+BPSK/AWGN words at Eb/N0 in {4, 5, 6, 7} dB, seeded synthetic data and random weights.
+One step = one aecct_decode of the whole batch (pre-processing, every layer, head and hard
+decision); y is resident in device memory before timing starts.
+
+Prints one JSON line: words/s, the roofline of the dominant kernel (algorithmic fp32 ALU
+operations per launch over its HIP-event duration, against one fp32 VALU operation per lane
+per clock), and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = 2                      # BCH(31,16), batch 65536
+PEAK_ALU_OPS = 256 * 4 * 16 * 2.4e9   # CUs x SIMDs x lanes x clock: fp32 VALU ops/s, non-packed
+PEAK_INT8 = 5.0e15                # dense int8 MFMA ops/s
+PEAK_HBM = 8.0e12
+
+
+def algorithmic_counts(H, w):
+    """Per-word work of the method as defined (not as executed): fp32 ALU operations, int8
+    MACs and HBM bytes.  Each scalar arithmetic operation of the definition counts once (an
+    FMA once, exp once, a division or square root once); the int8 x ternary products are
+    MFMA work and counted separately."""
+    m, n = H.shape
+    L, d, N, dff, heads = n + m, w.d, w.n_layers, w.d_ff, w.heads
+    dh, hf = d // heads, w.first_ring_heads
+    A = np.zeros((L, L), np.int64)
+    A[:n, n:] = H.T
+    A[n:, :n] = H
+    nnz1 = int((A != 0).sum())
+    nnz2 = int(((A @ A) != 0).sum())
+    quant = lambda K: 4 * K + 1                 # max|x|, 127/alpha, x*inv, rint, to-int
+    token_layer = (3 * quant(d) + quant(dff)    # inputs of QKV, O, FF1 and FF2
+                   + 2 * (3 * d + d + dff + d) + 4   # int->fp32 + fma dequant, 4 row scales
+                   + 2 * d                      # residual adds
+                   + 2 * (6 * d + 3)            # two LayerNorms
+                   + dff)                       # ReLU
+    pair = 3 * dh + 4                           # dot (dh mul, dh-1 add), scale, max, sub, exp, sum, dh fma
+    row_head = dh + 1                           # 1/S and dh products
+    pairs = hf * nnz1 + (heads - hf) * nnz2
+    layer = L * token_layer + pairs * pair + L * heads * row_head
+    embed = L * (d + 1) + int(H.sum())          # t*E rows, |y| / syndrome XORs
+    head = L * 2 * d + n * (L + 1) + 2 * n
+    alu = embed + N * layer + head
+    macs = N * L * (3 * d * d + d * d + 2 * d * dff)
+    hbm = 4 * n + n + 4 * n                     # y in, bits out, logits out
+    return dict(alu_ops=alu, int8_macs=macs, hbm_bytes=hbm, pairs_per_layer=pairs)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2410_05911_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
+    on the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", f"{kernel}__{workload}__pmc.json")
+    if not os.path.exists(p):
+        return None
+    rec = json.load(open(p))
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(H, w, y, budget_s=12.0):
+    import oracle
+    threads = min(os.cpu_count() or 1, 16)
+    om = oracle.OracleModel(H, w)
+    probe = 512
+    t0 = time.perf_counter()
+    om.decode(y[:probe], n_threads=threads)
+    t1 = time.perf_counter() - t0
+    k = int(min(y.shape[0], max(probe, probe * budget_s / max(t1, 1e-6))))
+    t0 = time.perf_counter()
+    om.decode(y[:k], n_threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": k / dt, "unit": "codewords/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {k} of {y.shape[0]} words of the same workload, canonical fp32 oracle, "
+                      f"{threads} OpenMP threads, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--path", type=int, default=0, help="0 auto, 1 layered, 2 fused")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", type=int, default=WORKLOAD)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the decode shards over words with no exchange); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2410_05911_amd as P
+    from workloads import build_workload
+
+    cfg, H, G, w, y, x = build_workload(args.workload)
+    B = cfg.batch
+    dev = torch.device("cuda:0")
+    dec = P.Decoder(H, w, path=args.path)
+    yd = torch.from_numpy(y).to(dev)
+    bits = torch.empty((B, cfg.n), dtype=torch.uint8, device=dev)
+    logits = torch.empty((B, cfg.n), dtype=torch.float32, device=dev)
+    ws = dec.workspace(B, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        dec.decode(yd, bits, logits, ws, stream)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dec.decode(yd, bits, logits, ws, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = ev0.elapsed_time(ev1) / args.steps
+    value = B / (ms * 1e-3)
+
+    cnt = algorithmic_counts(H, w)
+    path = "fused" if dec.path == P.PATH_FUSED else "layered"
+    kernel = "k_fused_decode" if path == "fused" else "layered_decode"
+    launch_s = ms * 1e-3                        # fused: one launch per step
+    achieved = cnt["alu_ops"] * B / launch_s
+    roofline = {
+        "bound": "alu",
+        "kernel": kernel,
+        "achieved": achieved / 1e12,
+        "peak": PEAK_ALU_OPS / 1e12,
+        "unit": "Top/s (fp32 VALU ops, one per lane per clock)",
+        "frac": achieved / PEAK_ALU_OPS,
+        "traffic": measured_traffic(kernel, cfg.name),
+        "alu_ops_per_word": cnt["alu_ops"],
+        "int8_mfma_frac": 2 * cnt["int8_macs"] * B / launch_s / PEAK_INT8,
+        "hbm_alg_frac": cnt["hbm_bytes"] * B / launch_s / PEAK_HBM,
+    }
+    out = {
+        "metric": "decoded codewords/sec (1 GPU) + % of int8-MFMA/HBM roofline",
+        "value": value,
+        "unit": "codewords/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8xternary->int32, fp32",
+        "data": "synthetic: seeded BPSK/AWGN words, random ternary weights",
+        "config": {"workload": cfg.name, "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
+                   "n": cfg.n, "tokens": dec.L, "d": cfg.d, "layers": cfg.n_layers, "heads": cfg.heads,
+                   "first_ring_heads": w.first_ring_heads, "batch": B, "path": path,
+                   "wall_s_timed": t_wall},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(H, w, y)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+/*
+ * aecct.h -- C ABI of the MI355X (gfx950) AECCT inference library.
+ *
+ * AECCT (Levy, Choukroun, Wolf, "Accelerating Error Correction Code
+ * Transformers") decodes a binary linear code with a transformer encoder.
+ * This library runs its batched inference forward pass: channel words y in,
+ * bit decisions out.
+ *
+ * What one decode computes, per received word (Section 3, "Problem Settings"
+ * and "Error Correction Code Transformer"; Section 4; Section 6):
+ *   1. h(y) = [|y|, 1 - 2 s(y)] with s(y) = H bin(y) mod 2: 2n-k tokens, the n
+ *      variable nodes first, then the n-k check nodes of the Tanner graph;
+ *   2. each token scalar times its row of the embedding table (plus an
+ *      optional fixed positional table, the inference form of the spectral
+ *      positional encoding of Section 4.3);
+ *   3. N Post-LN encoder blocks (Section 6).  Each block applies head
+ *      partitioned self-attention (Section 4.2: the first h_f heads attend
+ *      over Tanner neighbours, the rest over nodes two steps away, self
+ *      included), then a ReLU feed-forward block (Section 4, item 4); every
+ *      in-block linear map is an AAP linear layer (Section 4.1, Eq. 2-3):
+ *      per-token absmax int8 activations times ternary weights, int32
+ *      accumulation, dequantised by (weight scale) * alpha / 127 before the
+ *      fp32 bias;
+ *   4. the output head of Section 3: z = W_{d->1} x + b1 per token, then
+ *      f = W_o^T z + b_o over tokens, and the hard decision
+ *      bit = bin(y * f) = [y < 0] xor [f < 0].
+ * The fp32 arithmetic follows one fixed evaluation order, so results are
+ * reproducible bit for bit between runs, batch sizes and kernel paths.
+ *
+ * Conventions for every entry point:
+ *   - The return value is the only error channel; no global state is kept.
+ *   - "device" pointers are HIP device memory (or managed memory) of the GPU
+ *     that was current at aecct_create; "host" pointers are ordinary memory.
+ *   - stream is a hipStream_t passed as void* (NULL = the default stream).
+ *     Entry points that take a stream only enqueue work on it; they neither
+ *     allocate nor synchronise.  Results are ready once the stream is.
+ *   - A model is immutable after create: concurrent calls with the same model
+ *     on different streams are safe if their outputs and workspaces differ.
+ */
+#ifndef AECCT_H
+#define AECCT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum aecct_status {
+  AECCT_OK = 0,
+  AECCT_ERR_INVALID_ARG = 1,          /* null pointer, bad size, non-ternary weight, bad H ... */
+  AECCT_ERR_UNSUPPORTED = 2,          /* valid model outside the shapes the kernels implement */
+  AECCT_ERR_OUT_OF_MEMORY = 3,        /* host or device allocation failed */
+  AECCT_ERR_DEVICE = 4,               /* a HIP call or kernel launch failed */
+  AECCT_ERR_WORKSPACE_TOO_SMALL = 5
+} aecct_status;
+
+/* Kernel path.  Both give identical results (same evaluation order). */
+typedef enum aecct_path {
+  AECCT_PATH_AUTO = 0,     /* fused when a word fits in on-chip memory, else layered */
+  AECCT_PATH_LAYERED = 1,  /* one kernel per stage, intermediates in device memory */
+  AECCT_PATH_FUSED = 2     /* whole words resident in LDS, all layers in one launch */
+} aecct_path;
+
+/* The six in-block linear maps, in the order used by `scale` and `aecct_ternary_gemm`. */
+typedef enum aecct_linear {
+  AECCT_LIN_Q = 0, AECCT_LIN_K = 1, AECCT_LIN_V = 2, AECCT_LIN_O = 3, AECCT_LIN_FF1 = 4,
+  AECCT_LIN_FF2 = 5
+} aecct_linear;
+
+/*
+ * Model parameters, all HOST pointers, row-major, read (and copied) by
+ * aecct_create only; the caller keeps ownership.  L = n + m tokens.
+ * Linear weights are stored [in][out] (x W, Section 4.1) with entries in
+ * {-1, 0, +1}; scale[l][k] is the per-matrix weight scale gamma*delta of Eq. 3.
+ */
+typedef struct aecct_weights {
+  const float *embed;                         /* [L][d] token embedding rows */
+  const float *pos;                           /* [L][d] fixed positional rows, or NULL */
+  const int8_t *w_q, *w_k, *w_v, *w_o;        /* [N][d][d] */
+  const int8_t *w_ff1;                        /* [N][d][d_ff] */
+  const int8_t *w_ff2;                        /* [N][d_ff][d] */
+  const float *scale;                         /* [N][6] in aecct_linear order */
+  const float *b_q, *b_k, *b_v, *b_o;         /* [N][d] */
+  const float *b_ff1;                         /* [N][d_ff] */
+  const float *b_ff2;                         /* [N][d] */
+  const float *ln1_g, *ln1_b, *ln2_g, *ln2_b; /* [N][d] LayerNorm gain / offset */
+  const float *head_w1;                       /* [d]   W_{d->1} */
+  float head_b1;
+  const float *head_wo;                       /* [L][n] W_o */
+  const float *head_bo;                       /* [n] */
+} aecct_weights;
+
+typedef struct aecct_options {
+  int32_t first_ring_heads;  /* h_f, 0..heads; -1 = heads / 2 (the paper's default split) */
+  int32_t d_ff;              /* feed-forward width; -1 = 4 d */
+  float ln_eps;              /* LayerNorm epsilon; <= 0 = 1e-5 */
+  int32_t path;              /* aecct_path */
+} aecct_options;
+
+typedef struct aecct_model aecct_model;   /* opaque */
+
+/*
+ * Build a model on the current HIP device.
+ *   H    host [m][n] parity-check matrix (Section 3), entries 0/1, no
+ *        all-zero row or column (such a node would have an empty attention
+ *        row); the HPSA masks of Section 4.2 are derived from it here;
+ *   w    parameters as above; d model width, n_layers >= 1, heads >= 1;
+ *   opt  may be NULL (defaults).
+ * Supported shapes: d in {32, 64, 128}, d / heads in {4, 8, 16}, d_ff = 4 d,
+ * n + m <= 4096; anything else valid returns AECCT_ERR_UNSUPPORTED.
+ * All arguments are validated before any HIP call.  On success *out owns
+ * device memory until aecct_destroy.  Errors: INVALID_ARG, UNSUPPORTED,
+ * OUT_OF_MEMORY, DEVICE (no GPU, or a HIP allocation or copy failed).
+ */
+aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_weights *w, int32_t d,
+                          int32_t n_layers, int32_t heads, const aecct_options *opt, aecct_model **out);
+
+/* Release a model (NULL is a no-op).  No call may still be running on it. */
+void aecct_destroy(aecct_model *model);
+
+/* Static description of a built model (host call, no GPU work). */
+typedef struct aecct_model_info {
+  int32_t n, m, L, d, n_layers, heads, first_ring_heads, d_ff;
+  int32_t path;              /* resolved aecct_path (never AUTO) */
+  int64_t nnz_first_ring;    /* allowed (query, key) pairs of the first-ring mask */
+  int64_t nnz_second_ring;   /* same for the second-ring mask (diagonal included) */
+  size_t device_bytes;       /* device memory held by the model */
+} aecct_model_info;
+aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info);
+
+/*
+ * Bytes of device workspace aecct_decode needs for `batch` words (host call).
+ * The fused path needs none (0).  Errors: INVALID_ARG.
+ */
+aecct_status aecct_workspace_size(const aecct_model *model, int64_t batch, size_t *bytes);
+
+/*
+ * Decode `batch` received words.
+ *   y          device fp32 [batch][n], channel output y = x_s + noise (Section 3);
+ *   bits       device uint8 [batch][n], 0/1 hard decisions bin(y * f);
+ *   logits     device fp32 [batch][n] noise estimate f = f_theta(h(y)), or NULL;
+ *   workspace  device scratch of at least aecct_workspace_size bytes (may be
+ *              NULL when that size is 0); 256-byte aligned.
+ * batch == 0 is a no-op.  Non-finite y is not checked.  Errors: INVALID_ARG,
+ * WORKSPACE_TOO_SMALL, DEVICE (launch failure reported by HIP).
+ */
+aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits,
+                          float *logits, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Human-readable name of a status code (static string). */
+const char *aecct_status_string(aecct_status status);
+
+/* ------------------------------------------------------------------------------------------
+ * Stage entry points: the steps of the layered path, one launch each, on
+ * caller-provided device buffers of `words` whole words (rows = words * L).
+ * aecct_decode(path = LAYERED) is exactly embed, then per layer qkv ->
+ * attention -> oproj_ln -> ffn1 -> ffn2_ln, then head.  They let a caller run, time or
+ * check one step on inputs of its choice.  Layout of every activation: row r
+ * of word b at index b * L + r, features contiguous.  Errors: INVALID_ARG.
+ * ---------------------------------------------------------------------------------------- */
+
+/* Section 3 pre-processing + embedding + Eq. 2 quantisation of layer 0's input.
+ * y [words][n] -> x fp32 [rows][d], xq int8 [rows][d], ax fp32 [rows]. */
+aecct_status aecct_stage_embed(const aecct_model *model, const float *y, int64_t words, float *x,
+                               int8_t *xq, float *ax, void *stream);
+
+/* Eq. 3 for the query, key and value maps of `layer`:
+ * xq, ax -> qkv fp32 [rows][3d] (Q | K | V per row). */
+aecct_status aecct_stage_qkv(const aecct_model *model, int32_t layer, const int8_t *xq,
+                             const float *ax, int64_t words, float *qkv, void *stream);
+
+/* Section 4.2 head-partitioned attention and Eq. 2 quantisation of its output:
+ * qkv -> oq int8 [rows][d], ao fp32 [rows]; o fp32 [rows][d] also written when non-NULL. */
+aecct_status aecct_stage_attention(const aecct_model *model, const float *qkv, int64_t words,
+                                   float *o, int8_t *oq, float *ao, void *stream);
+
+/* Output projection (Eq. 3), residual and LN1 (Post-LN, Section 6), then Eq. 2:
+ * oq, ao, x -> x1 fp32 [rows][d], x1q int8 [rows][d], a1 fp32 [rows]. */
+aecct_status aecct_stage_oproj_ln(const aecct_model *model, int32_t layer, const int8_t *oq,
+                                  const float *ao, const float *x, int64_t words, float *x1,
+                                  int8_t *x1q, float *a1, void *stream);
+
+/* First feed-forward map (Eq. 3), ReLU (Section 4, item 4) and Eq. 2 on the hidden row:
+ * x1q, a1 -> gq int8 [rows][d_ff], ag fp32 [rows]. */
+aecct_status aecct_stage_ffn1(const aecct_model *model, int32_t layer, const int8_t *x1q, const float *a1,
+                              int64_t words, int8_t *gq, float *ag, void *stream);
+
+/* Second feed-forward map (Eq. 3), residual and LN2 (Post-LN, Section 6), then Eq. 2:
+ * gq, ag, x1 -> x fp32 [rows][d], xq int8 [rows][d], ax fp32 [rows]. */
+aecct_status aecct_stage_ffn2_ln(const aecct_model *model, int32_t layer, const int8_t *gq, const float *ag,
+                                 const float *x1, int64_t words, float *x, int8_t *xq, float *ax,
+                                 void *stream);
+
+/* Output head and hard decision (Section 3): x [rows][d], y [words][n] ->
+ * bits uint8 [words][n], logits fp32 [words][n] (may be NULL). */
+aecct_status aecct_stage_head(const aecct_model *model, const float *x, const float *y, int64_t words,
+                              uint8_t *bits, float *logits, void *stream);
+
+/* The int8 x ternary product of one AAP linear map alone (Eq. 3 before the
+ * dequantisation): a int8 [rows][in] -> acc int32 [rows][out] exactly, for
+ * matrix `kind` (aecct_linear) of `layer`.  Any rows >= 0. */
+aecct_status aecct_ternary_gemm(const aecct_model *model, int32_t layer, int32_t kind, const int8_t *a,
+                                int64_t rows, int32_t *acc, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,472 @@
+// Host side of the C ABI: argument validation, Tanner-graph neighbour lists, packing
+// of the ternary weights into MFMA B fragments, the single device allocation of a
+// model, workspace layout, and the launch sequence of a decode.
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/aecct.h"
+#include "aecct_internal.h"
+
+using aecct::Model;
+
+struct aecct_model {
+  Model M;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kChunkCapBytes = size_t(4) << 30;   // layered workspace per chunk of words
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool finite_all(const float *p, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (!std::isfinite(p[i])) return false;
+  return true;
+}
+
+bool ternary_all(const int8_t *p, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (p[i] < -1 || p[i] > 1) return false;
+  return true;
+}
+
+// 2-bit code of a ternary value: 00 -> 0, 01 -> +1, 11 -> -1.
+inline uint16_t code2(int8_t v) { return v == 1 ? 1u : (v == -1 ? 3u : 0u); }
+
+// Packs a [K][N] ternary map given by get(k, j) into 16x32 MFMA B-fragment blocks:
+// block (t, s) at index t * (K/32) + s, lane l holds column 16t + (l & 15) and inputs
+// 32s + 8(l >> 4) + e in bits 2e..2e+1.
+template <class Get>
+void pack_map(int K, int N, Get get, uint16_t *out) {
+  const int S = K / 32, T = N / 16;
+  for (int t = 0; t < T; ++t)
+    for (int s = 0; s < S; ++s)
+      for (int l = 0; l < 64; ++l) {
+        uint16_t v = 0;
+        const int j = 16 * t + (l & 15);
+        for (int e = 0; e < 8; ++e) v |= (uint16_t)(code2(get(32 * s + 8 * (l >> 4) + e, j)) << (2 * e));
+        out[((size_t)t * S + s) * 64 + l] = v;
+      }
+}
+
+size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
+
+// Device memory plan: byte offsets inside the model's single allocation.
+struct Plan {
+  size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
+  struct Layer { size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b; };
+  std::vector<Layer> layer;
+};
+
+Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_t nnz2, bool has_pos) {
+  const int L = n + m;
+  Plan p{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  p.chk_ptr = take(sizeof(int32_t) * (m + 1));
+  p.chk_idx = take(sizeof(int32_t) * E);
+  p.m1_ptr = take(sizeof(int32_t) * (L + 1));
+  p.m1_idx = take(sizeof(int32_t) * nnz1);
+  p.m2_ptr = take(sizeof(int32_t) * (L + 1));
+  p.m2_idx = take(sizeof(int32_t) * nnz2);
+  p.embed = take(sizeof(float) * L * d);
+  p.pos = has_pos ? take(sizeof(float) * L * d) : 0;
+  p.w1 = take(sizeof(float) * d);
+  p.wo = take(sizeof(float) * (size_t)L * n);
+  p.bo = take(sizeof(float) * n);
+  p.layer.resize(N);
+  for (int l = 0; l < N; ++l) {
+    auto &q = p.layer[l];
+    q.qkv = take(2 * packed_words(d, 3 * d));
+    q.o = take(2 * packed_words(d, d));
+    q.ff1 = take(2 * packed_words(d, dff));
+    q.ff2 = take(2 * packed_words(dff, d));
+    q.b_qkv = take(sizeof(float) * 3 * d);
+    q.b_o = take(sizeof(float) * d);
+    q.b_ff1 = take(sizeof(float) * dff);
+    q.b_ff2 = take(sizeof(float) * d);
+    q.ln1_g = take(sizeof(float) * d);
+    q.ln1_b = take(sizeof(float) * d);
+    q.ln2_g = take(sizeof(float) * d);
+    q.ln2_b = take(sizeof(float) * d);
+  }
+  p.total = off;
+  return p;
+}
+
+// Layered-path workspace for `words` words: region offsets.
+struct WsPlan {
+  size_t x, xq, ax, qkv, oq, ao, x1, x1q, a1, gq, ag, total;
+};
+
+WsPlan ws_plan(const Model &M, int64_t words) {
+  const size_t R = (size_t)words * M.L, d = M.d, dff = M.dff;
+  WsPlan w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  w.x = take(4 * R * d);
+  w.xq = take(R * d);
+  w.ax = take(4 * R);
+  w.qkv = take(4 * R * 3 * d);
+  w.oq = take(R * d);
+  w.ao = take(4 * R);
+  w.x1 = take(4 * R * d);
+  w.x1q = take(R * d);
+  w.a1 = take(4 * R);
+  w.gq = take(R * dff);
+  w.ag = take(4 * R);
+  w.total = off;
+  return w;
+}
+
+int64_t chunk_words(const Model &M, int64_t batch) {
+  const size_t per_word = ws_plan(M, 1).total;
+  int64_t c = (int64_t)(kChunkCapBytes / (per_word ? per_word : 1));
+  if (c < 1) c = 1;
+  return batch < c ? batch : c;
+}
+
+aecct_status from_hip(hipError_t e) {
+  if (e == hipSuccess) return AECCT_OK;
+  return e == hipErrorOutOfMemory ? AECCT_ERR_OUT_OF_MEMORY : AECCT_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *aecct_status_string(aecct_status s) {
+  switch (s) {
+    case AECCT_OK: return "ok";
+    case AECCT_ERR_INVALID_ARG: return "invalid argument";
+    case AECCT_ERR_UNSUPPORTED: return "unsupported model shape";
+    case AECCT_ERR_OUT_OF_MEMORY: return "out of memory";
+    case AECCT_ERR_DEVICE: return "device error";
+    case AECCT_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_weights *w, int32_t d,
+                          int32_t n_layers, int32_t heads, const aecct_options *opt, aecct_model **out) {
+  if (!out) return AECCT_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!H || !w || m <= 0 || n <= 0 || d <= 0 || n_layers <= 0 || heads <= 0 || d % heads) return AECCT_ERR_INVALID_ARG;
+  const int hf = (opt && opt->first_ring_heads >= 0) ? opt->first_ring_heads : heads / 2;
+  if (opt && opt->first_ring_heads < -1) return AECCT_ERR_INVALID_ARG;
+  if (hf > heads) return AECCT_ERR_INVALID_ARG;
+  const int dff = (opt && opt->d_ff > 0) ? opt->d_ff : 4 * d;
+  if (opt && opt->d_ff < -1) return AECCT_ERR_INVALID_ARG;
+  const float eps = (opt && opt->ln_eps > 0.0f) ? opt->ln_eps : 1e-5f;
+  if (opt && !std::isfinite(opt->ln_eps)) return AECCT_ERR_INVALID_ARG;
+  const int path_req = opt ? opt->path : AECCT_PATH_AUTO;
+  if (path_req < AECCT_PATH_AUTO || path_req > AECCT_PATH_FUSED) return AECCT_ERR_INVALID_ARG;
+  const int64_t L64 = (int64_t)n + m;
+  if (L64 > (1 << 20)) return AECCT_ERR_UNSUPPORTED;
+  const int L = (int)L64;
+  // parity-check matrix: 0/1, no empty row or column
+  std::vector<int> rowdeg(m, 0), coldeg(n, 0);
+  size_t E = 0;
+  for (int j = 0; j < m; ++j)
+    for (int i = 0; i < n; ++i) {
+      const uint8_t h = H[(size_t)j * n + i];
+      if (h > 1) return AECCT_ERR_INVALID_ARG;
+      if (h) { ++rowdeg[j]; ++coldeg[i]; ++E; }
+    }
+  for (int j = 0; j < m; ++j) if (!rowdeg[j]) return AECCT_ERR_INVALID_ARG;
+  for (int i = 0; i < n; ++i) if (!coldeg[i]) return AECCT_ERR_INVALID_ARG;
+  // weights
+  const size_t N = (size_t)n_layers, D = (size_t)d, F = (size_t)dff;
+  const int8_t *wts[6] = {w->w_q, w->w_k, w->w_v, w->w_o, w->w_ff1, w->w_ff2};
+  const float *bs[6] = {w->b_q, w->b_k, w->b_v, w->b_o, w->b_ff1, w->b_ff2};
+  const size_t wsz[6] = {D * D, D * D, D * D, D * D, D * F, F * D};
+  const size_t bsz[6] = {D, D, D, D, F, D};
+  if (!w->embed || !w->scale || !w->ln1_g || !w->ln1_b || !w->ln2_g || !w->ln2_b || !w->head_w1 || !w->head_wo ||
+      !w->head_bo)
+    return AECCT_ERR_INVALID_ARG;
+  for (int k = 0; k < 6; ++k) {
+    if (!wts[k] || !bs[k]) return AECCT_ERR_INVALID_ARG;
+    if (!ternary_all(wts[k], N * wsz[k])) return AECCT_ERR_INVALID_ARG;
+    if (!finite_all(bs[k], N * bsz[k])) return AECCT_ERR_INVALID_ARG;
+  }
+  if (!finite_all(w->embed, (size_t)L * D) || (w->pos && !finite_all(w->pos, (size_t)L * D)) ||
+      !finite_all(w->scale, N * 6) || !finite_all(w->ln1_g, N * D) || !finite_all(w->ln1_b, N * D) ||
+      !finite_all(w->ln2_g, N * D) || !finite_all(w->ln2_b, N * D) || !finite_all(w->head_w1, D) ||
+      !std::isfinite(w->head_b1) || !finite_all(w->head_wo, (size_t)L * n) || !finite_all(w->head_bo, (size_t)n))
+    return AECCT_ERR_INVALID_ARG;
+  // shapes the kernels implement
+  const int dh = d / heads;
+  if (!(d == 32 || d == 64 || d == 128) || !(dh == 4 || dh == 8 || dh == 16) || dff != 4 * d || L > 4096 ||
+      n_layers > aecct::kMaxLayers)
+    return AECCT_ERR_UNSUPPORTED;
+
+  // Tanner graph lists and HPSA masks (Section 4.2): M1 = neighbours, M2 = nodes two
+  // steps away plus the node itself; each list ascending.
+  std::vector<std::vector<int>> adj(L);
+  std::vector<int32_t> chk_ptr(m + 1, 0), chk_idx;
+  chk_idx.reserve(E);
+  for (int j = 0; j < m; ++j) {
+    for (int i = 0; i < n; ++i)
+      if (H[(size_t)j * n + i]) {
+        chk_idx.push_back(i);
+        adj[i].push_back(n + j);
+        adj[n + j].push_back(i);
+      }
+    chk_ptr[j + 1] = (int32_t)chk_idx.size();
+  }
+  std::vector<int32_t> m1_ptr(L + 1, 0), m1_idx, m2_ptr(L + 1, 0), m2_idx;
+  std::vector<int> mark(L, -1);
+  for (int a = 0; a < L; ++a) {
+    std::vector<int> nb = adj[a];
+    std::sort(nb.begin(), nb.end());
+    for (int v : nb) m1_idx.push_back(v);
+    m1_ptr[a + 1] = (int32_t)m1_idx.size();
+    for (int k : adj[a])
+      for (int b : adj[k]) mark[b] = a;
+    for (int b = 0; b < L; ++b)
+      if (mark[b] == a) m2_idx.push_back(b);
+    m2_ptr[a + 1] = (int32_t)m2_idx.size();
+  }
+
+  Model M{};
+  M.n = n; M.m = m; M.L = L; M.d = d; M.n_layers = n_layers; M.heads = heads; M.hf = hf; M.dff = dff;
+  M.dh = dh; M.eps = eps;
+  M.kappa = (float)(1.0 / std::sqrt((double)dh));
+  M.nnz1 = (int64_t)m1_idx.size();
+  M.nnz2 = (int64_t)m2_idx.size();
+  M.head_b1 = w->head_b1;
+  for (int l = 0; l < n_layers; ++l)
+    for (int k = 0; k < 6; ++k) M.layer[l].sq[k] = w->scale[(size_t)l * 6 + k] / 127.0f;
+  M.path = path_req;
+  if (M.path == AECCT_PATH_AUTO) M.path = aecct::fused_supported(M) ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
+  if (M.path == AECCT_PATH_FUSED && !aecct::fused_supported(M)) return AECCT_ERR_UNSUPPORTED;
+
+  // host image of the device block
+  const Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
+  std::vector<unsigned char> img;
+  try {
+    img.assign(P.total, 0);
+  } catch (const std::bad_alloc &) {
+    return AECCT_ERR_OUT_OF_MEMORY;
+  }
+  auto put = [&](size_t off, const void *src, size_t bytes) { if (bytes) std::memcpy(img.data() + off, src, bytes); };
+  put(P.chk_ptr, chk_ptr.data(), 4 * chk_ptr.size());
+  put(P.chk_idx, chk_idx.data(), 4 * chk_idx.size());
+  put(P.m1_ptr, m1_ptr.data(), 4 * m1_ptr.size());
+  put(P.m1_idx, m1_idx.data(), 4 * m1_idx.size());
+  put(P.m2_ptr, m2_ptr.data(), 4 * m2_ptr.size());
+  put(P.m2_idx, m2_idx.data(), 4 * m2_idx.size());
+  put(P.embed, w->embed, 4 * (size_t)L * D);
+  if (w->pos) put(P.pos, w->pos, 4 * (size_t)L * D);
+  put(P.w1, w->head_w1, 4 * D);
+  put(P.wo, w->head_wo, 4 * (size_t)L * n);
+  put(P.bo, w->head_bo, 4 * (size_t)n);
+  for (int l = 0; l < n_layers; ++l) {
+    const auto &q = P.layer[l];
+    const int8_t *Wq = w->w_q + l * D * D, *Wk = w->w_k + l * D * D, *Wv = w->w_v + l * D * D;
+    const int8_t *Wo = w->w_o + l * D * D, *W1 = w->w_ff1 + l * D * F, *W2 = w->w_ff2 + l * F * D;
+    pack_map(d, 3 * d, [&](int k, int j) {
+      const int8_t *src = j < d ? Wq : (j < 2 * d ? Wk : Wv);
+      return src[(size_t)k * D + (j % d)];
+    }, (uint16_t *)(img.data() + q.qkv));
+    pack_map(d, d, [&](int k, int j) { return Wo[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.o));
+    pack_map(d, dff, [&](int k, int j) { return W1[(size_t)k * F + j]; }, (uint16_t *)(img.data() + q.ff1));
+    pack_map(dff, d, [&](int k, int j) { return W2[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.ff2));
+    put(q.b_qkv, w->b_q + l * D, 4 * D);
+    put(q.b_qkv + 4 * D, w->b_k + l * D, 4 * D);
+    put(q.b_qkv + 8 * D, w->b_v + l * D, 4 * D);
+    put(q.b_o, w->b_o + l * D, 4 * D);
+    put(q.b_ff1, w->b_ff1 + l * F, 4 * F);
+    put(q.b_ff2, w->b_ff2 + l * D, 4 * D);
+    put(q.ln1_g, w->ln1_g + l * D, 4 * D);
+    put(q.ln1_b, w->ln1_b + l * D, 4 * D);
+    put(q.ln2_g, w->ln2_g + l * D, 4 * D);
+    put(q.ln2_b, w->ln2_b + l * D, 4 * D);
+  }
+
+  // device
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return AECCT_ERR_DEVICE;
+  void *blk = nullptr;
+  hipError_t e = hipMalloc(&blk, P.total);
+  if (e != hipSuccess) return from_hip(e);
+  e = hipMemcpy(blk, img.data(), P.total, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(blk);
+    return AECCT_ERR_DEVICE;
+  }
+  aecct_model *am = new (std::nothrow) aecct_model;
+  if (!am) {
+    (void)hipFree(blk);
+    return AECCT_ERR_OUT_OF_MEMORY;
+  }
+  unsigned char *b = (unsigned char *)blk;
+  M.device = dev;
+  M.dev_block = blk;
+  M.device_bytes = P.total;
+  M.chk_ptr = (const int32_t *)(b + P.chk_ptr);
+  M.chk_idx = (const int32_t *)(b + P.chk_idx);
+  M.m1_ptr = (const int32_t *)(b + P.m1_ptr);
+  M.m1_idx = (const int32_t *)(b + P.m1_idx);
+  M.m2_ptr = (const int32_t *)(b + P.m2_ptr);
+  M.m2_idx = (const int32_t *)(b + P.m2_idx);
+  M.embed = (const float *)(b + P.embed);
+  M.pos = w->pos ? (const float *)(b + P.pos) : nullptr;
+  M.head_w1 = (const float *)(b + P.w1);
+  M.head_wo = (const float *)(b + P.wo);
+  M.head_bo = (const float *)(b + P.bo);
+  for (int l = 0; l < n_layers; ++l) {
+    const auto &q = P.layer[l];
+    auto &Lw = M.layer[l];
+    Lw.qkv = (const uint16_t *)(b + q.qkv);
+    Lw.o = (const uint16_t *)(b + q.o);
+    Lw.ff1 = (const uint16_t *)(b + q.ff1);
+    Lw.ff2 = (const uint16_t *)(b + q.ff2);
+    Lw.b_qkv = (const float *)(b + q.b_qkv);
+    Lw.b_o = (const float *)(b + q.b_o);
+    Lw.b_ff1 = (const float *)(b + q.b_ff1);
+    Lw.b_ff2 = (const float *)(b + q.b_ff2);
+    Lw.ln1_g = (const float *)(b + q.ln1_g);
+    Lw.ln1_b = (const float *)(b + q.ln1_b);
+    Lw.ln2_g = (const float *)(b + q.ln2_g);
+    Lw.ln2_b = (const float *)(b + q.ln2_b);
+  }
+  am->M = M;
+  *out = am;
+  return AECCT_OK;
+}
+
+void aecct_destroy(aecct_model *model) {
+  if (!model) return;
+  if (model->M.dev_block) (void)hipFree(model->M.dev_block);
+  delete model;
+}
+
+aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
+  if (!model || !info) return AECCT_ERR_INVALID_ARG;
+  const Model &M = model->M;
+  info->n = M.n; info->m = M.m; info->L = M.L; info->d = M.d; info->n_layers = M.n_layers;
+  info->heads = M.heads; info->first_ring_heads = M.hf; info->d_ff = M.dff; info->path = M.path;
+  info->nnz_first_ring = M.nnz1; info->nnz_second_ring = M.nnz2; info->device_bytes = M.device_bytes;
+  return AECCT_OK;
+}
+
+aecct_status aecct_workspace_size(const aecct_model *model, int64_t batch, size_t *bytes) {
+  if (!model || !bytes || batch < 0) return AECCT_ERR_INVALID_ARG;
+  if (model->M.path == AECCT_PATH_FUSED || batch == 0) {
+    *bytes = 0;
+    return AECCT_OK;
+  }
+  *bytes = ws_plan(model->M, chunk_words(model->M, batch)).total;
+  return AECCT_OK;
+}
+
+aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits, float *logits,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+  if (!model || batch < 0) return AECCT_ERR_INVALID_ARG;
+  if (batch == 0) return AECCT_OK;
+  if (!y || !bits) return AECCT_ERR_INVALID_ARG;
+  const Model &M = model->M;
+  hipStream_t s = (hipStream_t)stream;
+  size_t need = 0;
+  aecct_workspace_size(model, batch, &need);
+  if (workspace_bytes < need) return AECCT_ERR_WORKSPACE_TOO_SMALL;
+  if (need && !workspace) return AECCT_ERR_INVALID_ARG;
+  if (M.path == AECCT_PATH_FUSED) return from_hip(aecct::launch_fused(M, y, batch, bits, logits, s)) == AECCT_OK
+                                             ? AECCT_OK : AECCT_ERR_DEVICE;
+  const int64_t cw = chunk_words(M, batch);
+  const WsPlan W = ws_plan(M, cw);
+  unsigned char *ws = (unsigned char *)workspace;
+  float *x = (float *)(ws + W.x), *qkv = (float *)(ws + W.qkv), *x1 = (float *)(ws + W.x1);
+  int8_t *xq = (int8_t *)(ws + W.xq), *oq = (int8_t *)(ws + W.oq), *x1q = (int8_t *)(ws + W.x1q);
+  int8_t *gq = (int8_t *)(ws + W.gq);
+  float *ax = (float *)(ws + W.ax), *ao = (float *)(ws + W.ao), *a1 = (float *)(ws + W.a1), *ag = (float *)(ws + W.ag);
+  for (int64_t w0 = 0; w0 < batch; w0 += cw) {
+    const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
+    const int64_t rows = nw * M.L;
+    hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, s);
+    for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
+      e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
+      if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
+      if (e == hipSuccess) e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
+      if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
+      if (e == hipSuccess) e = aecct::launch_ffn2_ln(M, l, gq, ag, x1, rows, x, xq, ax, s);
+    }
+    if (e == hipSuccess)
+      e = aecct::launch_head(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, s);
+    if (e != hipSuccess) return AECCT_ERR_DEVICE;
+  }
+  return AECCT_OK;
+}
+
+// ---- stage entry points --------------------------------------------------------------------
+
+#define AECCT_STAGE_CHECK(cond) \
+  do {                          \
+    if (!(cond)) return AECCT_ERR_INVALID_ARG; \
+  } while (0)
+
+static inline aecct_status launched(hipError_t e) { return e == hipSuccess ? AECCT_OK : AECCT_ERR_DEVICE; }
+
+aecct_status aecct_stage_embed(const aecct_model *model, const float *y, int64_t words, float *x, int8_t *xq,
+                               float *ax, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (y && x && xq && ax)));
+  return launched(aecct::launch_embed(model->M, y, words, x, xq, ax, (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_qkv(const aecct_model *model, int32_t layer, const int8_t *xq, const float *ax,
+                             int64_t words, float *qkv, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers && (words == 0 || (xq && ax && qkv)));
+  return launched(aecct::launch_qkv(model->M, layer, xq, ax, words * model->M.L, qkv, (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_attention(const aecct_model *model, const float *qkv, int64_t words, float *o, int8_t *oq,
+                                   float *ao, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (qkv && oq && ao)));
+  return launched(aecct::launch_attention(model->M, qkv, words, o, oq, ao, (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_oproj_ln(const aecct_model *model, int32_t layer, const int8_t *oq, const float *ao,
+                                  const float *x, int64_t words, float *x1, int8_t *x1q, float *a1, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers &&
+                    (words == 0 || (oq && ao && x && x1 && x1q && a1)));
+  return launched(aecct::launch_oproj_ln(model->M, layer, oq, ao, x, words * model->M.L, x1, x1q, a1,
+                                         (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_ffn1(const aecct_model *model, int32_t layer, const int8_t *x1q, const float *a1,
+                              int64_t words, int8_t *gq, float *ag, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers && (words == 0 || (x1q && a1 && gq && ag)));
+  return launched(aecct::launch_ffn1(model->M, layer, x1q, a1, words * model->M.L, gq, ag, (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_ffn2_ln(const aecct_model *model, int32_t layer, const int8_t *gq, const float *ag,
+                                 const float *x1, int64_t words, float *x, int8_t *xq, float *ax, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers &&
+                    (words == 0 || (gq && ag && x1 && x && xq && ax)));
+  return launched(aecct::launch_ffn2_ln(model->M, layer, gq, ag, x1, words * model->M.L, x, xq, ax,
+                                        (hipStream_t)stream));
+}
+
+aecct_status aecct_stage_head(const aecct_model *model, const float *x, const float *y, int64_t words, uint8_t *bits,
+                              float *logits, void *stream) {
+  AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (x && y && bits)));
+  return launched(aecct::launch_head(model->M, x, y, words, bits, logits, (hipStream_t)stream));
+}
+
+aecct_status aecct_ternary_gemm(const aecct_model *model, int32_t layer, int32_t kind, const int8_t *a, int64_t rows,
+                                int32_t *acc, void *stream) {
+  AECCT_STAGE_CHECK(model && rows >= 0 && layer >= 0 && layer < model->M.n_layers && kind >= 0 && kind < 6 &&
+                    (rows == 0 || (a && acc)));
+  return launched(aecct::launch_ternary_gemm(model->M, layer, kind, a, rows, acc, (hipStream_t)stream));
+}
+
+}  // extern "C"

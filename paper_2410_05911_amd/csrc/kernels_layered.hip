@@ -1,0 +1,509 @@
+// Layered path: one kernel per stage of the AECCT forward pass, activations in
+// device memory between stages.  Used for any code length; the fused path covers
+// short codes in a single launch.
+//
+// Row layout of every activation: row b * L + r for token r of word b, features
+// contiguous.  Tokens 0..n-1 are variable nodes, n..n+m-1 check nodes (Section 3).
+#include <hip/hip_runtime.h>
+
+#include "aecct_internal.h"
+#include "device_common.h"
+
+namespace aecct {
+
+// ------------------------------------------------------------------------------------------
+// Embedding: pre-processing h(y) (Section 3), X = t * E (+ P), and the Eq. 2 code of X.
+// 16 lanes per row; lane c holds features c + 16 t, t < D / 16.
+// ------------------------------------------------------------------------------------------
+struct EmbedArgs {
+  const float *y;
+  int64_t rows;
+  int n, L;
+  const int32_t *chk_ptr, *chk_idx;
+  const float *embed, *pos;
+  float *x;
+  int8_t *xq;
+  float *ax;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
+  constexpr int T = D / 16;
+  const int c = threadIdx.x & 15;
+  const int64_t g = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (g >= p.rows) return;  // uniform over the 16 lanes of a row
+  const int64_t w = g / p.L;
+  const int i = (int)(g - w * p.L);
+  const float *yw = p.y + w * p.n;
+  float t;
+  if (i < p.n) {
+    t = fabsf(yw[i]);
+  } else {
+    int s = 0;
+    for (int e = p.chk_ptr[i - p.n]; e < p.chk_ptr[i - p.n + 1]; ++e) s ^= (yw[p.chk_idx[e]] < 0.0f) ? 1 : 0;
+    t = s ? -1.0f : 1.0f;
+  }
+  float v[T];
+  float amax = 0.0f;
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    const int col = 16 * tt + c;
+    v[tt] = __builtin_fmaf(t, p.embed[(int64_t)i * D + col], p.pos ? p.pos[(int64_t)i * D + col] : 0.0f);
+    p.x[g * D + col] = v[tt];
+    amax = fmaxf(amax, fabsf(v[tt]));
+  }
+  amax = row16_max(amax);
+  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) p.xq[g * D + 16 * tt + c] = (int8_t)quant_code(v[tt], inv);
+  if (c == 0) p.ax[g] = amax;
+}
+
+// ------------------------------------------------------------------------------------------
+// Ternary x int8 GEMM on int8 MFMA (Eq. 3) with fused epilogues.
+// A block stages its packed weights once into LDS as int8 B fragments, then its four
+// waves walk 16-row strips: one wave owns all output columns of its 16 rows, so the
+// row-wise LayerNorm and absmax reductions stay inside the wave (intra-lane over the
+// column tiles, then a 16-lane DPP reduction).
+// ------------------------------------------------------------------------------------------
+enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3 };
+
+struct GemmArgs {
+  const int8_t *a;        // [rows][K]
+  const float *alpha;     // [rows] Eq. 2 scale of each A row
+  const uint16_t *bpack;  // packed B blocks of the whole map
+  int tile0;              // first 16-column tile of the map this launch computes
+  int64_t rows;
+  float sq[3];            // per 1/3 of the columns (QKV) or sq[0] for all: fp32(scale / 127)
+  const float *bias;      // [NOUT]
+  const float *resid;     // [rows][NOUT] (LN)
+  const float *ln_g, *ln_b;
+  float eps;
+  float *out_f;           // fp32 output (QKV, LN)
+  int8_t *out_q;          // int8 output (LN, RELU_QUANT)
+  float *out_a;           // [rows] scale of out_q rows
+  int32_t *out_acc;       // raw accumulators (RAW)
+};
+
+constexpr int kGemmWaves = 4;
+
+template <int K, int NOUT, int EPI>
+__global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
+  constexpr int S = K / 32;
+  constexpr int T = NOUT / 16;
+  constexpr bool kQuantOut = (EPI == EPI_LN || EPI == EPI_RELU_QUANT);
+  __shared__ uint64_t bsm[T * S * 64];
+  __shared__ __attribute__((aligned(16))) int8_t qstage[kQuantOut ? kGemmWaves : 1][kQuantOut ? 16 * NOUT : 16];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  {
+    const uint16_t *src = p.bpack + (size_t)p.tile0 * S * 64;
+    for (int u = tid; u < T * S * 64; u += kGemmWaves * 64) bsm[u] = unpack_ternary8(src[u]);
+  }
+  __syncthreads();
+
+  const int64_t nstrips = (p.rows + 15) / 16;
+  const int64_t ngroups = (nstrips + kGemmWaves - 1) / kGemmWaves;
+  const int col = lane & 15, rg = lane >> 4;
+  for (int64_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+    const int64_t row0 = (grp * kGemmWaves + wave) * 16;
+    long afr[S];
+    {
+      const int64_t ar = row0 + col;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        afr[s] = ar < p.rows ? *(const long *)(p.a + ar * K + 32 * s + 8 * rg) : 0;
+    }
+    v4i acc[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      acc[t] = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < S; ++s) acc[t] = mfma_i8_16x16x32(afr[s], (long)bsm[(t * S + s) * 64 + lane], acc[t]);
+    }
+
+    int64_t r[4];
+    bool ok[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[i] = row0 + 4 * rg + i;
+      ok[i] = r[i] < p.rows;
+    }
+
+    if constexpr (EPI == EPI_RAW) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (ok[i]) p.out_acc[r[i] * NOUT + 16 * t + col] = acc[t][i];
+    } else {
+      float al[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) al[i] = ok[i] ? p.alpha[r[i]] : 0.0f;
+      if constexpr (EPI == EPI_QKV) {
+        constexpr int TB = T / 3;  // tiles per map
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          const float sq = p.sq[t / TB];
+          const float b = p.bias[j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (ok[i]) p.out_f[r[i] * NOUT + j] = __builtin_fmaf((float)acc[t][i], al[i] * sq, b);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float sc = al[i] * p.sq[0];
+          float v[T];
+          if constexpr (EPI == EPI_LN) {
+            // residual + LayerNorm over the NOUT (= d) features of row r[i]
+            float e[T], sq[T], tmp[T];
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              const int j = 16 * t + col;
+              const float y = __builtin_fmaf((float)acc[t][i], sc, p.bias[j]);
+              const float res = ok[i] ? p.resid[r[i] * NOUT + j] : 0.0f;
+              v[t] = res + y;
+              tmp[t] = v[t];
+            }
+            const float mean = row16_sum(lane_tree<T>(tmp)) / (float)NOUT;
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              e[t] = v[t] - mean;
+              sq[t] = e[t] * e[t];
+            }
+            const float var = row16_sum(lane_tree<T>(sq)) / (float)NOUT;
+            const float rho = 1.0f / __builtin_sqrtf(var + p.eps);
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              const int j = 16 * t + col;
+              v[t] = __builtin_fmaf(e[t] * rho, p.ln_g[j], p.ln_b[j]);
+              if (ok[i]) p.out_f[r[i] * NOUT + j] = v[t];
+            }
+          } else {  // EPI_RELU_QUANT
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              const float f = __builtin_fmaf((float)acc[t][i], sc, p.bias[16 * t + col]);
+              v[t] = f > 0.0f ? f : 0.0f;
+            }
+          }
+          // Eq. 2 on the finished row
+          float amax = 0.0f;
+#pragma unroll
+          for (int t = 0; t < T; ++t) amax = fmaxf(amax, fabsf(v[t]));
+          amax = row16_max(amax);
+          const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+          for (int t = 0; t < T; ++t) qstage[wave][(4 * rg + i) * NOUT + 16 * t + col] = (int8_t)quant_code(v[t], inv);
+          if (col == 0 && ok[i]) p.out_a[r[i]] = amax;
+        }
+      }
+    }
+    if constexpr (kQuantOut) {
+      __syncthreads();
+      const int64_t valid = p.rows - row0 < 16 ? (p.rows - row0 > 0 ? p.rows - row0 : 0) : 16;
+      const int chunks = (int)(valid * NOUT / 16);
+      const uint4 *src = (const uint4 *)qstage[wave];
+      uint4 *dst = (uint4 *)(p.out_q + row0 * NOUT);
+      for (int cidx = lane; cidx < chunks; cidx += 64) dst[cidx] = src[cidx];
+      __syncthreads();
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Head-partitioned attention (Section 4.2): one lane per (row, head); heads 0..hf-1 read
+// the first-ring neighbour list of the row, the others the second-ring list.  Two passes
+// over the neighbours (ascending): the running maximum of the scaled scores, then the
+// exponentials, their sum and the weighted value sum.  The heads of a row sit in adjacent
+// lanes, so the row's Eq. 2 scale is a shuffle reduction.
+// ------------------------------------------------------------------------------------------
+struct AttnArgs {
+  const float *qkv;
+  int64_t rows;
+  int L, d, heads, hf;
+  float kappa;
+  const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
+  float *o;
+  int8_t *oq;
+  float *ao;
+};
+
+template <int DH>
+__device__ __forceinline__ float head_score(const float (&q)[DH], const float *k, float kappa) {
+  float pr[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) pr[t] = q[t] * k[t];
+  return lane_tree<DH>(pr) * kappa;
+}
+
+template <int DH>
+__global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
+  const int heads = p.heads;
+  const int rpb = 256 / heads;
+  const int h = threadIdx.x % heads;
+  const int64_t g = (int64_t)blockIdx.x * rpb + threadIdx.x / heads;
+  const bool valid = g < p.rows;
+  const int d = p.d, d3 = 3 * p.d;
+  const int64_t w = valid ? g / p.L : 0;
+  const int i = valid ? (int)(g - w * p.L) : 0;
+  const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr;
+  const int32_t *idx = h < p.hf ? p.m1_idx : p.m2_idx;
+  const int beg = valid ? ptr[i] : 0, end = valid ? ptr[i + 1] : 0;
+  const float *base = p.qkv + w * p.L * d3;
+  float q[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) q[t] = valid ? base[(int64_t)i * d3 + h * DH + t] : 0.0f;
+
+  float mu = -INFINITY;
+  for (int e = beg; e < end; ++e) {
+    const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
+    mu = fmaxf(mu, head_score<DH>(q, kr, p.kappa));
+  }
+  float S = 0.0f, acc[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+  for (int e = beg; e < end; ++e) {
+    const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
+    const float ex = softmax_exp(head_score<DH>(q, kr, p.kappa) - mu);
+    S = S + ex;
+    const float *vr = kr + d;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+  }
+  const float rS = valid ? 1.0f / S : 0.0f;
+  float amax = 0.0f;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) {
+    acc[t] = acc[t] * rS;
+    amax = fmaxf(amax, fabsf(acc[t]));
+  }
+  for (int off = 1; off < heads; off <<= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  if (!valid) return;
+  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+  int8_t qv[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) qv[t] = (int8_t)quant_code(acc[t], inv);
+  int8_t *dq = p.oq + g * d + h * DH;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) dq[t] = qv[t];
+  if (p.o) {
+#pragma unroll
+    for (int t = 0; t < DH; ++t) p.o[g * d + h * DH + t] = acc[t];
+  }
+  if (h == 0) p.ao[g] = amax;
+}
+
+// ------------------------------------------------------------------------------------------
+// Output head and hard decision (Section 3): one block per word.  z_i = W_{d->1} x_i + b1
+// (16 lanes per token, pairwise over features), then f_o = sum_i z_i W_o[i][o] + b_o in
+// ascending token order, bit = [y < 0] xor [f < 0].
+// ------------------------------------------------------------------------------------------
+struct HeadArgs {
+  const float *x, *y;
+  int n, L;
+  const float *w1, *wo, *bo;
+  float b1;
+  uint8_t *bits;
+  float *logits;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void k_head(HeadArgs p) {
+  constexpr int T = D / 16;
+  extern __shared__ float zs[];
+  const int64_t w = blockIdx.x;
+  const int c = threadIdx.x & 15;
+  for (int i = threadIdx.x >> 4; i < p.L; i += 16) {
+    const float *xr = p.x + (w * p.L + i) * D;
+    float v[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) v[t] = xr[16 * t + c] * p.w1[16 * t + c];
+    const float z = row16_sum(lane_tree<T>(v)) + p.b1;
+    if (c == 0) zs[i] = z;
+  }
+  __syncthreads();
+  for (int o = threadIdx.x; o < p.n; o += 256) {
+    float acc = 0.0f;
+    for (int i = 0; i < p.L; ++i) acc = __builtin_fmaf(zs[i], p.wo[(int64_t)i * p.n + o], acc);
+    const float f = acc + p.bo[o];
+    const float yv = p.y[w * p.n + o];
+    p.bits[w * p.n + o] = (uint8_t)((yv < 0.0f) != (f < 0.0f));
+    if (p.logits) p.logits[w * p.n + o] = f;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// launchers
+// ------------------------------------------------------------------------------------------
+namespace {
+
+int gemm_grid(int64_t rows) {
+  const int64_t groups = ((rows + 15) / 16 + kGemmWaves - 1) / kGemmWaves;
+  const int64_t g = groups < 2048 ? groups : 2048;
+  return (int)(g > 0 ? g : 1);
+}
+
+template <int K, int NOUT, int EPI>
+hipError_t run_gemm(const GemmArgs &a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm<K, NOUT, EPI>), dim3(gemm_grid(a.rows)), dim3(kGemmWaves * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+GemmArgs gemm_base(const int8_t *a, const float *alpha, const uint16_t *bpack, int64_t rows) {
+  GemmArgs g{};
+  g.a = a;
+  g.alpha = alpha;
+  g.bpack = bpack;
+  g.rows = rows;
+  return g;
+}
+
+}  // namespace
+
+hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
+                        hipStream_t s) {
+  EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax};
+  if (a.rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.rows + 15) / 16));
+  switch (M.d) {
+    case 32: hipLaunchKernelGGL(k_embed<32>, grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL(k_embed<64>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(k_embed<128>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t rows, float *qkv,
+                      hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  GemmArgs a = gemm_base(xq, ax, W.qkv, rows);
+  a.sq[0] = W.sq[0];
+  a.sq[1] = W.sq[1];
+  a.sq[2] = W.sq[2];
+  a.bias = W.b_qkv;
+  a.out_f = qkv;
+  switch (M.d) {
+    case 32: return run_gemm<32, 96, EPI_QKV>(a, s);
+    case 64: return run_gemm<64, 192, EPI_QKV>(a, s);
+    case 128: return run_gemm<128, 384, EPI_QKV>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,
+                           int64_t rows, float *x1, int8_t *x1q, float *a1, hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  GemmArgs a = gemm_base(oq, ao, W.o, rows);
+  a.sq[0] = W.sq[3];
+  a.bias = W.b_o;
+  a.resid = x;
+  a.ln_g = W.ln1_g;
+  a.ln_b = W.ln1_b;
+  a.eps = M.eps;
+  a.out_f = x1;
+  a.out_q = x1q;
+  a.out_a = a1;
+  switch (M.d) {
+    case 32: return run_gemm<32, 32, EPI_LN>(a, s);
+    case 64: return run_gemm<64, 64, EPI_LN>(a, s);
+    case 128: return run_gemm<128, 128, EPI_LN>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, int8_t *gq,
+                      float *ag, hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  GemmArgs a = gemm_base(x1q, a1, W.ff1, rows);
+  a.sq[0] = W.sq[4];
+  a.bias = W.b_ff1;
+  a.out_q = gq;
+  a.out_a = ag;
+  switch (M.d) {
+    case 32: return run_gemm<32, 128, EPI_RELU_QUANT>(a, s);
+    case 64: return run_gemm<64, 256, EPI_RELU_QUANT>(a, s);
+    case 128: return run_gemm<128, 512, EPI_RELU_QUANT>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_ffn2_ln(const Model &M, int layer, const int8_t *gq, const float *ag, const float *x1,
+                          int64_t rows, float *x, int8_t *xq, float *ax, hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  GemmArgs a = gemm_base(gq, ag, W.ff2, rows);
+  a.sq[0] = W.sq[5];
+  a.bias = W.b_ff2;
+  a.resid = x1;
+  a.ln_g = W.ln2_g;
+  a.ln_b = W.ln2_b;
+  a.eps = M.eps;
+  a.out_f = x;
+  a.out_q = xq;
+  a.out_a = ax;
+  switch (M.d) {
+    case 32: return run_gemm<128, 32, EPI_LN>(a, s);
+    case 64: return run_gemm<256, 64, EPI_LN>(a, s);
+    case 128: return run_gemm<512, 128, EPI_LN>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a_in, int64_t rows,
+                               int32_t *acc, hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  const uint16_t *bp = kind <= 2 ? W.qkv : kind == 3 ? W.o : kind == 4 ? W.ff1 : W.ff2;
+  GemmArgs a = gemm_base(a_in, nullptr, bp, rows);
+  a.tile0 = kind <= 2 ? kind * (M.d / 16) : 0;
+  a.out_acc = acc;
+  const int d = M.d;
+  if (kind <= 3) {
+    if (d == 32) return run_gemm<32, 32, EPI_RAW>(a, s);
+    if (d == 64) return run_gemm<64, 64, EPI_RAW>(a, s);
+    if (d == 128) return run_gemm<128, 128, EPI_RAW>(a, s);
+  } else if (kind == 4) {
+    if (d == 32) return run_gemm<32, 128, EPI_RAW>(a, s);
+    if (d == 64) return run_gemm<64, 256, EPI_RAW>(a, s);
+    if (d == 128) return run_gemm<128, 512, EPI_RAW>(a, s);
+  } else {
+    if (d == 32) return run_gemm<128, 32, EPI_RAW>(a, s);
+    if (d == 64) return run_gemm<256, 64, EPI_RAW>(a, s);
+    if (d == 128) return run_gemm<512, 128, EPI_RAW>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
+                            hipStream_t s) {
+  AttnArgs a{qkv, words * M.L, M.L, M.d, M.heads, M.hf, M.kappa, M.m1_ptr, M.m1_idx, M.m2_ptr, M.m2_idx,
+             o, oq, ao};
+  if (a.rows <= 0) return hipSuccess;
+  const int rpb = 256 / M.heads;
+  const dim3 grid((unsigned)((a.rows + rpb - 1) / rpb));
+  switch (M.dh) {
+    case 4: hipLaunchKernelGGL(k_attention<4>, grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL(k_attention<8>, grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL(k_attention<16>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
+                       float *logits, hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  HeadArgs a{x, y, M.n, M.L, M.head_w1, M.head_wo, M.head_bo, M.head_b1, bits, logits};
+  const size_t shm = sizeof(float) * (size_t)M.L;
+  switch (M.d) {
+    case 32: hipLaunchKernelGGL(k_head<32>, dim3((unsigned)words), dim3(256), shm, s, a); break;
+    case 64: hipLaunchKernelGGL(k_head<64>, dim3((unsigned)words), dim3(256), shm, s, a); break;
+    case 128: hipLaunchKernelGGL(k_head<128>, dim3((unsigned)words), dim3(256), shm, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace aecct

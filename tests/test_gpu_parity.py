@@ -1,0 +1,201 @@
+"""GPU parity: the HIP path against the CPU oracle, through the C ABI.
+
+Every floating-point value is compared bit for bit: both sides follow the same
+evaluation order (pairwise feature sums, ascending neighbour and token sums, the same
+exp), so the required tolerance (1e-3 on logits, identical bits where |logit| > 1e-3)
+is met with margin 0.  Integer work (syndromes, int8 codes, int32 accumulators) is
+compared exactly.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from workloads import CONFIGS, build_workload  # noqa: E402
+
+LOGIT_TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def P():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2410_05911_amd as P
+    P.lib()
+    return P
+
+
+_cache = {}
+
+
+def _setup(P, c, batch, path):
+    key = (c, batch, path)
+    if key not in _cache:
+        cfg, H, G, w, y, x = build_workload(c, batch=batch)
+        dec = P.Decoder(H, w, path=path)
+        _cache[key] = (cfg, H, G, w, y, x, dec)
+    return _cache[key]
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _assert_logits(f_gpu, f_ref, bits_gpu, bits_ref, y):
+    """Bit-exact expectation, with the tolerance rule checked explicitly as well."""
+    diff = np.abs(f_gpu.astype(np.float64) - f_ref.astype(np.float64))
+    assert diff.max() <= LOGIT_TOL, diff.max()
+    sure = np.abs(f_ref) > LOGIT_TOL
+    assert (bits_gpu[sure] == bits_ref[sure]).all()
+    nbad = int((f_gpu != f_ref).sum())
+    assert nbad == 0, f"{nbad} logits differ (max |diff| {diff.max():.3g})"
+    assert (bits_gpu == bits_ref).all()
+
+
+# ------------------------------------------------------------------------------ ternary GEMM
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
+def test_ternary_gemm_teacher_forced(P, c):
+    """int8 x ternary accumulators (Eq. 3) exactly equal an int64 matmul, for every map,
+    with a ragged number of rows (not a multiple of the 16-row MFMA tile)."""
+    print(f"[gemm] config {c}", flush=True)
+    cfg, H, G, w, y, x, dec = _setup(P, c, 4, P.PATH_LAYERED)
+    rng = np.random.default_rng(100 + c)
+    rows = 16 * 37 + 5
+    for layer in sorted({0, w.n_layers - 1}):
+        for kind, name in enumerate(("q", "k", "v", "o", "ff1", "ff2")):
+            T = w.w[name][layer]
+            a = rng.integers(-127, 128, (rows, T.shape[0])).astype(np.int8)
+            a[3] = 127
+            a[4] = -127
+            acc = _np(dec.ternary_gemm(layer, kind, _dev(a)))
+            ref = a.astype(np.int64) @ T.astype(np.int64)
+            assert (acc == ref).all(), (layer, name)
+    assert _np(dec.ternary_gemm(0, 0, _dev(np.zeros((0, w.d), np.int8)))).shape == (0, w.d)
+
+
+# ------------------------------------------------------------------------------ stages
+def _oracle_taps(om, ys):
+    taps = []
+    for yw in ys:
+        bits, f, t = om.decode_taps(yw)
+        t["bits"], t["f"] = bits, f
+        taps.append(t)
+    return {k: np.stack([t[k] for t in taps]) for k in taps[0]}
+
+
+@pytest.mark.parametrize("c,words", [(1, 5), (2, 3), (3, 2), (4, 1), (5, 1)])
+def test_stages_teacher_forced(P, oracle_mod, c, words):
+    """Each layered-path stage, fed the oracle's own inputs for that stage, reproduces the
+    oracle's outputs bit for bit (fp32 values, int8 codes and per-row scales)."""
+    print(f"[stages] config {c} words {words}", flush=True)
+    cfg, H, G, w, y, x, dec = _setup(P, c, 8, P.PATH_LAYERED)
+    om = oracle_mod.OracleModel(H, w)
+    ys = y[:words]
+    T = _oracle_taps(om, ys)
+    L, d, N = om.L, w.d, w.n_layers
+
+    def rows(a):          # [words, N?, L, ...] per-layer slice -> [words*L, ...]
+        return np.ascontiguousarray(a.reshape((words * L,) + a.shape[2:]))
+
+    xg, xqg, axg = dec.stage_embed(_dev(ys))
+    assert (_np(xg) == rows(T["x_in"][:, 0])).all()
+    assert (_np(xqg) == rows(T["xq"][:, 0])).all()
+    assert (_np(axg) == rows(T["ax"][:, 0])).all()
+    for l in range(N):
+        qkv = dec.stage_qkv(l, _dev(rows(T["xq"][:, l])), _dev(rows(T["ax"][:, l])))
+        assert (_np(qkv) == rows(T["qkv"][:, l])).all(), ("qkv", l)
+        o, oq, ao = dec.stage_attention(_dev(rows(T["qkv"][:, l])))
+        assert (_np(o) == rows(T["o"][:, l])).all(), ("o", l)
+        assert (_np(oq) == rows(T["oq"][:, l])).all(), ("oq", l)
+        assert (_np(ao) == rows(T["ao"][:, l])).all(), ("ao", l)
+        x1, x1q, a1 = dec.stage_oproj_ln(l, _dev(rows(T["oq"][:, l])), _dev(rows(T["ao"][:, l])),
+                                         _dev(rows(T["x_in"][:, l])))
+        assert (_np(x1) == rows(T["x1"][:, l])).all(), ("x1", l)
+        assert (_np(x1q) == rows(T["x1q"][:, l])).all(), ("x1q", l)
+        assert (_np(a1) == rows(T["a1"][:, l])).all(), ("a1", l)
+        gq, ag = dec.stage_ffn1(l, _dev(rows(T["x1q"][:, l])), _dev(rows(T["a1"][:, l])))
+        assert (_np(gq) == rows(T["gq"][:, l])).all(), ("gq", l)
+        assert (_np(ag) == rows(T["ag"][:, l])).all(), ("ag", l)
+        xo, xoq, axo = dec.stage_ffn2_ln(l, _dev(rows(T["gq"][:, l])), _dev(rows(T["ag"][:, l])),
+                                         _dev(rows(T["x1"][:, l])))
+        assert (_np(xo) == rows(T["x_out"][:, l])).all(), ("x_out", l)
+        if l + 1 < N:
+            assert (_np(xoq) == rows(T["xq"][:, l + 1])).all(), ("xq", l + 1)
+            assert (_np(axo) == rows(T["ax"][:, l + 1])).all(), ("ax", l + 1)
+    bits, logits = dec.stage_head(_dev(rows(T["x_out"][:, N - 1])), _dev(ys))
+    assert (_np(logits) == T["f"]).all()
+    assert (_np(bits) == T["bits"]).all()
+
+
+# ------------------------------------------------------------------------------ end to end
+# oracle sample sizes per workload (whole words the CPU oracle decodes in seconds)
+_SAMPLE = {1: 1024, 2: 768, 3: 48, 4: 6, 5: 2}
+
+
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
+def test_decode_full_batch_against_oracle(P, oracle_mod, c):
+    """Full configured batch through aecct_decode; the oracle recomputes a spread sample of
+    the words (all of them for Hamming(7,4))."""
+    cfg = CONFIGS[c]
+    print(f"[e2e] config {c} batch {cfg.batch}", flush=True)
+    cfg, H, G, w, y, x, dec = _setup(P, c, cfg.batch, P.PATH_AUTO)
+    bits, logits = dec.decode(_dev(y))
+    bits, logits = _np(bits), _np(logits)
+    k = min(_SAMPLE[c], cfg.batch)
+    idx = np.unique(np.linspace(0, cfg.batch - 1, k).astype(np.int64))
+    om = oracle_mod.OracleModel(H, w)
+    bo, fo = om.decode(y[idx], n_threads=16)
+    _assert_logits(logits[idx], fo, bits[idx], bo, y[idx])
+
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_decode_edge_batches(P, oracle_mod, c):
+    """batch 0 (no-op), 1, and ragged batches; per-word results do not depend on the batch."""
+    print(f"[edge] config {c}", flush=True)
+    cfg, H, G, w, y, x, dec = _setup(P, c, 67, P.PATH_AUTO)
+    om = oracle_mod.OracleModel(H, w)
+    bo, fo = om.decode(y, n_threads=16)
+    for B in (1, 2, 3, 17, 67):
+        bits, logits = dec.decode(_dev(y[:B]))
+        _assert_logits(_np(logits), fo[:B], _np(bits), bo[:B], y[:B])
+    e = torch.empty((0, cfg.n), dtype=torch.float32, device="cuda")
+    b0, l0 = dec.decode(e)
+    assert b0.shape == (0, cfg.n)
+    # noiseless all-zero codeword: |y| = 1 and zero syndrome; y = -0.0 counts as bit 0
+    z = np.ones((2, cfg.n), np.float32)
+    z[1] = -0.0
+    bits, logits = dec.decode(_dev(z))
+    bo, fo = om.decode(z)
+    _assert_logits(_np(logits), fo, _np(bits), bo, z)
+
+
+def test_workspace_too_small_and_bad_args(P):
+    cfg, H, G, w, y, x, dec = _setup(P, 3, 4, P.PATH_LAYERED)
+    yd = _dev(y)
+    need = dec.workspace_size(4)
+    assert need > 0
+    ws = torch.empty(need - 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(P.AecctError) as ei:
+        dec.decode(yd, workspace=ws)
+    assert ei.value.status == P.ERR_WORKSPACE_TOO_SMALL
+    with pytest.raises(P.AecctError) as ei:
+        dec.stage_qkv(w.n_layers, torch.zeros((dec.L * 4, w.d), dtype=torch.int8, device="cuda"),
+                      torch.zeros(dec.L * 4, device="cuda"))
+    assert ei.value.status == P.ERR_INVALID_ARG
+
+
+def test_deterministic_and_stream(P):
+    cfg, H, G, w, y, x, dec = _setup(P, 2, 2048, P.PATH_AUTO)
+    yd = _dev(y)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        b1, l1 = dec.decode(yd, stream=s)
+    s.synchronize()
+    b2, l2 = dec.decode(yd)
+    assert torch.equal(l1, l2) and torch.equal(b1, b2)
