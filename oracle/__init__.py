@@ -46,8 +46,12 @@ def lib():
         L = C.CDLL(LIB)
         L.oracle_tree_sum.restype = C.c_float
         L.oracle_tree_sum.argtypes = [_f32p, C.c_int32]
-        L.oracle_exp.restype = C.c_float
-        L.oracle_exp.argtypes = [C.c_float]
+        L.oracle_exp2.restype = C.c_float
+        L.oracle_exp2.argtypes = [C.c_float]
+        L.oracle_rsqrt.restype = C.c_float
+        L.oracle_rsqrt.argtypes = [C.c_float]
+        L.oracle_query_scale.restype = C.c_float
+        L.oracle_query_scale.argtypes = [C.c_int32]
         L.oracle_masks.argtypes = [_u8p, C.c_int32, C.c_int32, _u8p, _u8p]
         L.oracle_preprocess.argtypes = [_u8p, C.c_int32, C.c_int32, _f32p, _f32p]
         L.oracle_quant_rows.argtypes = [_f32p, C.c_int64, C.c_int32, _i8p, _f32p]
@@ -57,7 +61,7 @@ def lib():
         L.oracle_attention_word.restype = C.c_int
         L.oracle_attention_word.argtypes = [C.POINTER(_Model), _u8p, _u8p, _f32p, _f32p]
         L.oracle_attention_dense_f64.restype = C.c_int
-        L.oracle_attention_dense_f64.argtypes = [C.POINTER(_Model), _u8p, _u8p, _f64p, _f64p]
+        L.oracle_attention_dense_f64.argtypes = [C.POINTER(_Model), _u8p, _u8p, _f64p, C.c_double, _f64p]
         L.oracle_head_word.argtypes = [C.POINTER(_Model), _f32p, _f32p, _f32p, _u8p, _f32p]
         L.oracle_decode.restype = C.c_int
         L.oracle_decode.argtypes = [C.POINTER(_Model), _f32p, C.c_int64, _u8p, _f32p, C.c_int32]
@@ -172,13 +176,14 @@ class OracleModel:
             raise RuntimeError("empty attention row")
         return o
 
-    def attention_dense_f64(self, qkv, M1=None, M2=None):
+    def attention_dense_f64(self, qkv, score_scale, M1=None, M2=None):
+        """softmax(score_scale * q.k) attention in fp64 over the dense masks."""
         if M1 is None:
             M1, M2 = masks(self.H)
         qkv = _c(qkv, np.float64)
         o = np.zeros((self.L, self.d), np.float64)
         if lib().oracle_attention_dense_f64(C.byref(self.st), _p(M1, _u8p), _p(M2, _u8p), _p(qkv, _f64p),
-                                            _p(o, _f64p)):
+                                            float(score_scale), _p(o, _f64p)):
             raise RuntimeError("empty attention row")
         return o
 
@@ -200,8 +205,16 @@ def tree_sum(v) -> np.float32:
     return np.float32(lib().oracle_tree_sum(_p(v, _f32p), v.size))
 
 
-def exp(x) -> np.float32:
-    return np.float32(lib().oracle_exp(float(np.float32(x))))
+def exp2(x) -> np.float32:
+    return np.float32(lib().oracle_exp2(float(np.float32(x))))
+
+
+def rsqrt(v) -> np.float32:
+    return np.float32(lib().oracle_rsqrt(float(np.float32(v))))
+
+
+def query_scale(dh: int) -> np.float32:
+    return np.float32(lib().oracle_query_scale(int(dh)))
 
 
 def masks(H):
@@ -233,6 +246,7 @@ def quant_rows(x):
 
 
 def linear_rows(q, r, T, s, b):
+    """AAP linear rows with weight scale s (gamma*delta); the oracle takes fp32(s / 127)."""
     q = _c(q, np.int8)
     r = _c(r, np.float32)
     T = _c(T, np.int8)
@@ -241,7 +255,8 @@ def linear_rows(q, r, T, s, b):
     n_out = T.shape[1]
     out = np.zeros((rows, n_out), np.float32)
     acc = np.zeros((rows, n_out), np.int32)
-    lib().oracle_linear_rows(_p(q, _i8p), _p(r, _f32p), rows, _p(T, _i8p), K, n_out, float(np.float32(s)),
+    sq = np.float32(s) / np.float32(127.0)
+    lib().oracle_linear_rows(_p(q, _i8p), _p(r, _f32p), rows, _p(T, _i8p), K, n_out, float(sq),
                              _p(b, _f32p), _p(out, _f32p), _p(acc, _i32p))
     return out, acc
 

@@ -10,7 +10,10 @@
  *   TREE(v, w)  pairwise sum: v[t] += v[t + w/2] for t < w/2, then recurse on
  *               the first half (w a power of two);
  *   SEQ         left-to-right from 0 in ascending index;
- *   EXP         oracle_exp below (Cody-Waite reduction + degree-7 Taylor).
+ *   DOT         q.k as a multiply followed by fused multiply-adds in ascending
+ *               index order;
+ *   EXP2        oracle_exp2 below (2^x, degree-7 Taylor series);
+ *   RSQRT       oracle_rsqrt below (three Newton steps from a bit-level seed).
  */
 #include "aecct_oracle.h"
 
@@ -43,31 +46,59 @@ float oracle_tree_sum(const float *v, int32_t w) {
 }
 
 /*
- * exp(x) for x <= 0, as used by the softmax of Section 3 (CASA) / Section 4.2
- * (HPSA).  Cody & Waite (1980) argument reduction x = k ln2 + r with ln2 split
- * into a 16-bit head (so k * LN2_HI is exact for |k| < 2^7) and its fp32
- * remainder, then the degree-7 Taylor polynomial of e^r by Horner, then the
- * exact scaling by 2^k.  Results below exp(-80) are flushed to 0; they are
- * negligible next to the largest softmax term, which is exactly 1.
- * Pin: within 2 ulp of libm exp over [-80, 0]; EXP(0) == 1 exactly.
+ * 2^x for x <= 0, the exponential of the attention softmax (Section 3, CASA;
+ * Section 4.2, HPSA) taken in base 2: softmax(s) = 2^(s log2 e - max) / sum,
+ * with log2 e folded into the scores.  x is clamped to >= -125 (so the result
+ * stays a normal number; such terms are below 2^-124 of the largest, which is
+ * exactly 1), split exactly into k = rint(x) and r = x - k in [-1/2, 1/2],
+ * 2^r = sum_j (r ln 2)^j / j! to degree 7 by Horner with fp32-rounded
+ * coefficients, then scaled exactly by 2^k.
+ * Pin: within 2 ulp of 2^x over [-125, 0]; exact at integers.
  */
-float oracle_exp(float x) {
-  const float LOG2E = 1.44269502163f;          /* fp32(log2 e) */
-  const float LN2_HI = 0.693145751953125f;     /* 45426 * 2^-16 */
-  const float LN2_LO = 1.428606765330187e-6f; /* fp32(ln 2 - LN2_HI) */
-  if (x < -80.0f) return 0.0f;
-  float k = rintf(x * LOG2E);
-  float r = fmaf(-k, LN2_HI, x);
-  r = fmaf(-k, LN2_LO, r);
-  float p = 1.0f / 5040.0f;
-  p = fmaf(p, r, 1.0f / 720.0f);
-  p = fmaf(p, r, 1.0f / 120.0f);
-  p = fmaf(p, r, 1.0f / 24.0f);
-  p = fmaf(p, r, 1.0f / 6.0f);
-  p = fmaf(p, r, 0.5f);
-  p = fmaf(p, r, 1.0f);
-  p = fmaf(p, r, 1.0f);
+#define ORC_LN2 0.69314718055994530942
+static const float exp2_coef[8] = {
+    1.0f,
+    (float)(ORC_LN2),
+    (float)(ORC_LN2 * ORC_LN2 / 2.0),
+    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 / 6.0),
+    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 24.0),
+    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 120.0),
+    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 720.0),
+    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 5040.0)};
+
+float oracle_exp2(float x) {
+  if (x < -125.0f) x = -125.0f;
+  const float k = rintf(x);
+  const float r = x - k;
+  float p = exp2_coef[7];
+  for (int j = 6; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
   return ldexpf(p, (int)k);
+}
+
+/*
+ * 1/sqrt(v) for v > 0, the normaliser of LayerNorm: the bit-level seed
+ * 0x5F3759DF - (bits(v) >> 1) (Lomont, "Fast inverse square root", 2003),
+ * then three Newton steps y <- y (3/2 - (v/2) y^2).
+ * Pin: within 4 ulp of 1/sqrt(v) in double over the LayerNorm range.
+ */
+float oracle_rsqrt(float v) {
+  const float h = 0.5f * v;
+  uint32_t bits;
+  memcpy(&bits, &v, sizeof bits);
+  bits = 0x5F3759DFu - (bits >> 1);
+  float y;
+  memcpy(&y, &bits, sizeof y);
+  for (int it = 0; it < 3; ++it) {
+    float t = y * y;
+    t = fmaf(-h, t, 1.5f);
+    y = y * t;
+  }
+  return y;
+}
+
+/* Score scale of the scaled queries: fp32(log2(e) / sqrt(d_h)). */
+float oracle_query_scale(int32_t dh) {
+  return (float)(1.4426950408889634074 / sqrt((double)dh));
 }
 
 /*
@@ -114,7 +145,9 @@ void oracle_preprocess(const uint8_t *H, int32_t m, int32_t n, const float *y, f
 /*
  * Absmax int8 activation quantisation, Eq. 2 with Q_b = 127, applied per token
  * row: alpha = max|x|, q = RoundClip(x * (Q_b / alpha), -Q_b, Q_b) with
- * round-half-to-even.  An all-zero row gives q = 0 and alpha = 0.
+ * Q_b / alpha rounded to fp32 and the product x * (Q_b / alpha) rounded once,
+ * half to even, straight to an integer (the product of two floats is exact in
+ * double).  An all-zero row gives q = 0 and alpha = 0.
  * Pin: |q| <= 127, the argmax maps to +-127, sign kept, monotone, error bound.
  */
 void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float *r) {
@@ -133,9 +166,9 @@ void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float
     }
     float inv = 127.0f / a;
     for (int32_t c = 0; c < K; ++c) {
-      float v = rintf(xi[c] * inv);
-      if (v > 127.0f) v = 127.0f;
-      if (v < -127.0f) v = -127.0f;
+      double v = rint((double)xi[c] * (double)inv);
+      if (v > 127.0) v = 127.0;
+      if (v < -127.0) v = -127.0;
       qi[c] = (int8_t)v;
     }
     r[i] = a;
@@ -145,16 +178,17 @@ void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float
 /*
  * AAPLinear at inference, Eq. 3: integer product of the int8 activations and
  * the ternary weights (additions and subtractions only), dequantised by
- * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  The scale is
- * evaluated as alpha * (s / 127) with s = gamma*delta, and dequant plus bias is
- * one fused multiply-add: out = fma(acc, alpha * (s / 127), b).
+ * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  With
+ * sq = s / 127 (s = gamma*delta, the caller rounds it to fp32) the scale is
+ * alpha * sq and dequant plus bias is one fused multiply-add:
+ * out = fma(acc, alpha * sq, b).
  * Pin: accumulators equal an int64 library matmul; zero weights give the bias.
  */
 void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int8_t *T, int32_t K,
-                        int32_t n_out, float s, const float *b, float *out, int32_t *acc) {
+                        int32_t n_out, float sq, const float *b, float *out, int32_t *acc) {
   for (int64_t i = 0; i < rows; ++i) {
     const int8_t *qi = q + i * K;
-    float sc = r[i] * (s / 127.0f);
+    float sc = r[i] * sq;
     for (int32_t o = 0; o < n_out; ++o) {
       int32_t a = 0;
       for (int32_t c = 0; c < K; ++c) a += (int32_t)qi[c] * (int32_t)T[(int64_t)c * n_out + o];
@@ -167,7 +201,7 @@ void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int
 /*
  * LayerNorm of the Post-LN block (Section 6): mean and biased variance over
  * the d features (TREE sums), out = (x - mean) / sqrt(var + eps) * g + b,
- * evaluated as fma((x - mean) * (1 / sqrtf(var + eps)), g, b).
+ * evaluated as fma((x - mean) * RSQRT(var + eps), g, b).
  * Pin: within 1e-5 of the fp64 library layer_norm.
  */
 void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float *g, const float *b,
@@ -181,35 +215,36 @@ void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float 
       sq[c] = e[c] * e[c];
     }
     float var = oracle_tree_sum(sq, d) / (float)d;
-    float rho = 1.0f / sqrtf(var + eps);
+    float rho = oracle_rsqrt(var + eps);
     for (int32_t c = 0; c < d; ++c) out[i * d + c] = fmaf(e[c] * rho, g[c], b[c]);
   }
 }
 
-static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_t h, int32_t dh,
-                       float kappa) {
-  float p[ORC_MAX_TREE];
+/* DOT of a scaled query row segment with a key row segment (ascending dims). */
+static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_t h, int32_t dh) {
   const float *qi = qkv + (int64_t)i * 3 * d + h * dh;
   const float *kj = qkv + (int64_t)j * 3 * d + d + h * dh;
-  for (int32_t t = 0; t < dh; ++t) p[t] = qi[t] * kj[t];
-  return oracle_tree_sum(p, dh) * kappa;
+  float s = qi[0] * kj[0];
+  for (int32_t t = 1; t < dh; ++t) s = fmaf(qi[t], kj[t], s);
+  return s;
 }
 
 /*
  * Head-partitioned self-attention (Section 4.2): heads 0..h_f-1 attend over
  * the first-ring mask M1, the others over the second-ring mask M2.  Per row i
  * and head h the softmax of the scaled dot products over the allowed keys j
- * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.
- * Score s_j = TREE(q*k, d_h) * kappa; mu = max s_j; e_j = EXP(s_j - mu);
- * S = SEQ sum e_j; o = (SEQ fma(e_j, v_j, acc)) * (1 / S).  Returns 0, or -1 for a
- * row with no allowed key.
+ * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.  The
+ * query rows arrive already multiplied by log2(e)/sqrt(d_h) (folded into the
+ * query map, see oracle_query_scale), so the softmax is taken in base 2:
+ * s_j = DOT(q', k_j); mu = max s_j; e_j = EXP2(s_j - mu); S = SEQ sum e_j;
+ * o = (SEQ fma(e_j, v_j, acc)) * (1 / S).  Returns 0, or -1 for a row with no
+ * allowed key.
  * Pin: within 1e-6 relative of the fp64 dense (-inf)-masked softmax; a row
  * with one allowed key returns that value row exactly.
  */
 int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
                           const float *qkv, float *o) {
   const int32_t L = M->n + M->m, d = M->d, dh = M->d / M->heads;
-  const float kappa = (float)(1.0 / sqrt((double)dh));
   for (int32_t i = 0; i < L; ++i)
     for (int32_t h = 0; h < M->heads; ++h) {
       const uint8_t *row = (h < M->first_ring_heads ? M1 : M2) + (int64_t)i * L;
@@ -217,7 +252,7 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
       int cnt = 0;
       for (int32_t j = 0; j < L; ++j)
         if (row[j]) {
-          float s = score_f32(qkv, d, i, j, h, dh, kappa);
+          float s = score_f32(qkv, d, i, j, h, dh);
           if (s > mu) mu = s;
           ++cnt;
         }
@@ -226,7 +261,7 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
       for (int32_t t = 0; t < dh; ++t) acc[t] = 0.0f;
       for (int32_t j = 0; j < L; ++j)
         if (row[j]) {
-          float e = oracle_exp(score_f32(qkv, d, i, j, h, dh, kappa) - mu);
+          float e = oracle_exp2(score_f32(qkv, d, i, j, h, dh) - mu);
           S = S + e;
           const float *vj = qkv + (int64_t)j * 3 * d + 2 * d + h * dh;
           for (int32_t t = 0; t < dh; ++t) acc[t] = fmaf(e, vj[t], acc[t]);
@@ -264,7 +299,7 @@ void oracle_head_word(const oracle_model *M, const float *X, const float *y, flo
 /* ------------------------------------------------------------------ whole decode */
 
 typedef struct {
-  float *t, *X, *qkv, *O, *X1, *F, *Y, *R;
+  float *t, *X, *qkv, *O, *X1, *F, *Y, *R, *bq;
   int8_t *q, *gq;
   float *r, *rg;
   int32_t *acc, *accf;
@@ -280,19 +315,20 @@ static int alloc_buf(const oracle_model *M, word_buf *w) {
   w->F = malloc(sizeof(float) * L * dff);
   w->Y = malloc(sizeof(float) * L * (dff > 3 * d ? dff : 3 * d));
   w->R = malloc(sizeof(float) * L * d);
+  w->bq = malloc(sizeof(float) * d);
   w->q = malloc((size_t)(L * (dff > d ? dff : d)));
   w->gq = malloc((size_t)(L * dff));
   w->r = malloc(sizeof(float) * L);
   w->rg = malloc(sizeof(float) * L);
   w->acc = malloc(sizeof(int32_t) * L * d);
   w->accf = malloc(sizeof(int32_t) * L * dff);
-  return (w->t && w->X && w->qkv && w->O && w->X1 && w->F && w->Y && w->R && w->q && w->gq &&
+  return (w->t && w->X && w->qkv && w->O && w->X1 && w->F && w->Y && w->R && w->bq && w->q && w->gq &&
           w->r && w->rg && w->acc && w->accf) ? 0 : -1;
 }
 
 static void free_buf(word_buf *w) {
   free(w->t); free(w->X); free(w->qkv); free(w->O); free(w->X1); free(w->F); free(w->Y);
-  free(w->R); free(w->q); free(w->gq); free(w->r); free(w->rg); free(w->acc); free(w->accf);
+  free(w->R); free(w->bq); free(w->q); free(w->gq); free(w->r); free(w->rg); free(w->acc); free(w->accf);
 }
 
 static const int8_t *wmat(const oracle_model *M, int kind, int layer) {
@@ -312,17 +348,23 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     for (int64_t c = 0; c < d; ++c)
       w->X[i * d + c] = fmaf(w->t[i], M->embed[i * d + c], M->pos ? M->pos[i * d + c] : 0.0f);
 
+  const float kq = oracle_query_scale(M->d / M->heads);
   for (int32_t l = 0; l < M->n_layers; ++l) {
     const float *sc = M->scale + (int64_t)l * 6;
+    float sq[6];
+    for (int k = 0; k < 6; ++k) sq[k] = sc[k] / 127.0f;
     const int64_t LD = L * d;
     if (tp && tp->x_in) memcpy(tp->x_in + l * LD, w->X, sizeof(float) * LD);
     /* a. Q, K, V from the int8 input */
     oracle_quant_rows(w->X, L, (int32_t)d, w->q, w->r);
     if (tp && tp->xq) memcpy(tp->xq + l * LD, w->q, (size_t)LD);
     if (tp && tp->ax) memcpy(tp->ax + l * L, w->r, sizeof(float) * L);
+    /* the query map carries the score scale log2(e)/sqrt(d_h) in its dequant scale and bias */
+    for (int64_t c = 0; c < d; ++c) w->bq[c] = bvec(M, ORC_Q, l)[c] * kq;
     for (int kind = ORC_Q; kind <= ORC_V; ++kind) {
-      oracle_linear_rows(w->q, w->r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d, sc[kind],
-                         bvec(M, kind, l), w->Y, NULL);
+      oracle_linear_rows(w->q, w->r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d,
+                         kind == ORC_Q ? sq[kind] * kq : sq[kind], kind == ORC_Q ? w->bq : bvec(M, kind, l),
+                         w->Y, NULL);
       for (int64_t i = 0; i < L; ++i)
         memcpy(w->qkv + i * 3 * d + kind * d, w->Y + i * d, sizeof(float) * d);
     }
@@ -334,7 +376,7 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     oracle_quant_rows(w->O, L, (int32_t)d, w->q, w->r);
     if (tp && tp->oq) memcpy(tp->oq + l * LD, w->q, (size_t)LD);
     if (tp && tp->ao) memcpy(tp->ao + l * L, w->r, sizeof(float) * L);
-    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O],
+    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sq[ORC_O],
                        bvec(M, ORC_O, l), w->Y, w->acc);
     if (tp && tp->acc_o) memcpy(tp->acc_o + l * LD, w->acc, sizeof(int32_t) * LD);
     for (int64_t e = 0; e < LD; ++e) w->R[e] = w->X[e] + w->Y[e];
@@ -344,14 +386,14 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     oracle_quant_rows(w->X1, L, (int32_t)d, w->q, w->r);
     if (tp && tp->x1q) memcpy(tp->x1q + l * LD, w->q, (size_t)LD);
     if (tp && tp->a1) memcpy(tp->a1 + l * L, w->r, sizeof(float) * L);
-    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sc[ORC_FF1],
+    oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sq[ORC_FF1],
                        bvec(M, ORC_FF1, l), w->F, w->accf);
     if (tp && tp->acc_ff1) memcpy(tp->acc_ff1 + l * L * dff, w->accf, sizeof(int32_t) * L * dff);
     for (int64_t e = 0; e < L * dff; ++e) w->F[e] = w->F[e] > 0.0f ? w->F[e] : 0.0f;
     oracle_quant_rows(w->F, L, (int32_t)dff, w->gq, w->rg);
     if (tp && tp->gq) memcpy(tp->gq + l * L * dff, w->gq, (size_t)(L * dff));
     if (tp && tp->ag) memcpy(tp->ag + l * L, w->rg, sizeof(float) * L);
-    oracle_linear_rows(w->gq, w->rg, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sc[ORC_FF2],
+    oracle_linear_rows(w->gq, w->rg, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sq[ORC_FF2],
                        bvec(M, ORC_FF2, l), w->Y, w->acc);
     if (tp && tp->acc_ff2) memcpy(tp->acc_ff2 + l * LD, w->acc, sizeof(int32_t) * LD);
     for (int64_t e = 0; e < LD; ++e) w->R[e] = w->X1[e] + w->Y[e];
@@ -453,9 +495,10 @@ static void layernorm_f64(double *R, int64_t rows, int32_t d, const float *g, co
   }
 }
 
-/* Dense attention: softmax over all L keys with the masked scores set to -inf. */
+/* Dense attention: softmax(score_scale * q.k) over all L keys with the masked
+ * scores set to -inf, libm exp. */
 int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
-                               const double *qkv, double *o) {
+                               const double *qkv, double score_scale, double *o) {
   const int32_t L = M->n + M->m, d = M->d, dh = M->d / M->heads;
   double *s = malloc(sizeof(double) * L);
   if (!s) return -1;
@@ -467,7 +510,7 @@ int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const u
         double dot = 0.0;
         for (int32_t t = 0; t < dh; ++t)
           dot += qkv[(int64_t)i * 3 * d + h * dh + t] * qkv[(int64_t)j * 3 * d + d + h * dh + t];
-        s[j] = row[j] ? dot / sqrt((double)dh) : -INFINITY;
+        s[j] = row[j] ? dot * score_scale : -INFINITY;
         if (s[j] > mx) mx = s[j];
       }
       if (mx == -INFINITY) { free(s); return -1; }
@@ -517,7 +560,7 @@ int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, ui
           for (int64_t i = 0; i < L; ++i)
             for (int64_t c = 0; c < d; ++c) qkv[i * 3 * d + kind * d + c] = Y[i * d + c];
         }
-        if (oracle_attention_dense_f64(M, M1, M2, qkv, O)) { err |= 1; break; }
+        if (oracle_attention_dense_f64(M, M1, M2, qkv, 1.0 / sqrt((double)(d / M->heads)), O)) { err |= 1; break; }
         quant_rows_f64(O, L, (int32_t)d, q, r);
         linear_rows_f64(q, r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O], bvec(M, ORC_O, l), Y);
         for (int64_t e = 0; e < L * d; ++e) X1[e] = X[e] + Y[e];

@@ -12,7 +12,8 @@
  *                     biases and scales are fp32 in Section 4.1), in a fixed,
  *                     stated evaluation order so that any correct
  *                     implementation that keeps the same order reproduces
- *                     every value bit for bit;
+ *                     every value bit for bit (the qkv tap holds the query
+ *                     rows scaled by log2(e)/sqrt(d_h), see oracle_query_scale);
  *   reference fp64 -- the same model in double precision with dense
  *                     (-inf)-masked softmax attention and libm exp; the
  *                     semantic check of the canonical mode.
@@ -67,12 +68,14 @@ typedef struct oracle_taps {
 
 /* ---- building blocks (canonical fp32) ---- */
 float oracle_tree_sum(const float *v, int32_t w);
-float oracle_exp(float x);
+float oracle_exp2(float x);
+float oracle_rsqrt(float v);
+float oracle_query_scale(int32_t dh);
 void oracle_masks(const uint8_t *H, int32_t m, int32_t n, uint8_t *M1, uint8_t *M2);
 void oracle_preprocess(const uint8_t *H, int32_t m, int32_t n, const float *y, float *t);
 void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float *r);
 void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int8_t *T, int32_t K,
-                        int32_t n_out, float s, const float *b, float *out, int32_t *acc);
+                        int32_t n_out, float sq, const float *b, float *out, int32_t *acc);
 void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float *g, const float *b,
                            float eps, float *out);
 int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
@@ -89,7 +92,7 @@ int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, ui
                         double *f, int32_t n_threads);
 /* fp64 dense masked softmax attention of one word (reference for the sparse canonical one). */
 int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
-                               const double *qkv, double *o);
+                               const double *qkv, double score_scale, double *o);
 
 #ifdef __cplusplus
 }

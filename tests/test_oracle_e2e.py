@@ -106,6 +106,7 @@ def test_taps_stagewise_against_fp64(oracle_mod, c):
         assert (a64 == t["ax"][l]).all()
         qkv = np.concatenate([lin(t["xq"][l], t["ax"][l], w.w[k][l], sc[i], w.b[k][l])
                               for i, k in enumerate(("q", "k", "v"))], 1)
+        qkv[:, :d] *= math.log2(math.e) / math.sqrt(d // w.heads)      # scaled queries
         close(t["qkv"][l], qkv, 1e-6)
         close(t["o"][l], _sdpa_reference(H, w, t["qkv"][l]), 2e-6)
         q64, a64 = _q64(t["o"][l].astype(np.float64))

@@ -36,19 +36,36 @@ def test_tree_sum_pairs_stride_halving(oracle_mod):
         assert abs(float(oracle_mod.tree_sum(x)) - exact) <= bound + 1e-30
 
 
-# ------------------------------------------------------------------------ EXP
-def test_exp_close_to_libm_and_exact_at_zero(oracle_mod):
-    assert oracle_mod.exp(0.0) == np.float32(1.0)
-    assert oracle_mod.exp(-0.0) == np.float32(1.0)
-    assert oracle_mod.exp(-80.5) == 0.0 and oracle_mod.exp(-1e4) == 0.0
-    xs = np.concatenate([-np.linspace(0, 80, 40001, dtype=np.float32),
-                         -np.random.default_rng(1).random(20000).astype(np.float32) * 80])
+# ------------------------------------------------------------------------ EXP2, RSQRT
+def test_exp2_close_to_pow_and_exact_at_integers(oracle_mod):
+    for k in range(0, 126):
+        assert oracle_mod.exp2(-float(k)) == np.float32(2.0 ** -k)
+    assert oracle_mod.exp2(-0.0) == np.float32(1.0)
+    assert oracle_mod.exp2(-200.0) == np.float32(2.0 ** -125)      # clamped: stays a normal number
+    xs = np.concatenate([-np.linspace(0, 125, 50001, dtype=np.float32),
+                         -np.random.default_rng(1).random(20000).astype(np.float32) * 125])
     worst = 0.0
     for x in xs:
-        e = float(oracle_mod.exp(x))
-        ref = math.exp(float(x))
+        e = float(oracle_mod.exp2(x))
+        ref = 2.0 ** float(x)
         worst = max(worst, abs(e - ref) / float(_ulp(ref)))
+    assert worst <= 1.0, worst
+
+
+def test_rsqrt_close_to_exact(oracle_mod):
+    rng = np.random.default_rng(2)
+    vs = np.concatenate([np.exp(rng.uniform(math.log(1e-5), math.log(1e4), 20000)),
+                         [1e-5, 0.25, 1.0, 2.0, 3.0, 4.0, 1e4]]).astype(np.float32)
+    worst = 0.0
+    for v in vs:
+        ref = 1.0 / math.sqrt(float(v))
+        worst = max(worst, abs(float(oracle_mod.rsqrt(v)) - ref) / float(_ulp(ref)))
     assert worst <= 2.0, worst
+
+
+def test_query_scale(oracle_mod):
+    for dh in (4, 8, 16):
+        assert oracle_mod.query_scale(dh) == np.float32(1.0 / (math.log(2.0) * math.sqrt(dh)))
 
 
 # ------------------------------------------------------------------------ pre-processing
@@ -139,8 +156,9 @@ def test_layernorm_against_torch_fp64(oracle_mod):
 
 
 # ------------------------------------------------------------------------ HPSA attention
-def _sdpa_reference(H, w, qkv):
-    """torch fp64 scaled-dot-product attention per head with boolean masks from H."""
+def _sdpa_reference(H, w, qkv, scale=math.log(2.0)):
+    """torch fp64 scaled-dot-product attention per head with boolean masks from H.  The oracle's
+    query rows carry log2(e)/sqrt(d_h), so softmax(ln2 * q'.k) is the base-e softmax of q.k/sqrt(d_h)."""
     m, n = H.shape
     L = n + m
     A = np.zeros((L, L), np.int64)
@@ -158,7 +176,7 @@ def _sdpa_reference(H, w, qkv):
         mask = M1 if hh < w.first_ring_heads else M2
         out[:, sl] = torch.nn.functional.scaled_dot_product_attention(
             Q[None, None, :, sl], K[None, None, :, sl].contiguous(), V[None, None, :, sl], attn_mask=mask,
-            scale=1.0 / math.sqrt(dh))[0, 0]
+            scale=scale)[0, 0]
     return out.numpy()
 
 
@@ -171,7 +189,7 @@ def test_attention_against_fp64_sdpa(oracle_mod, c):
     o = om.attention(qkv)
     ref = _sdpa_reference(H, w, qkv)
     assert np.abs(o - ref).max() <= 1e-6 * max(1.0, np.abs(ref).max())
-    o64 = om.attention_dense_f64(qkv)                       # the oracle's own dense fp64 mode
+    o64 = om.attention_dense_f64(qkv, math.log(2.0))        # the oracle's own dense fp64 mode
     assert np.abs(o64 - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max())
 
 
