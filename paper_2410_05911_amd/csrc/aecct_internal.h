@@ -21,16 +21,17 @@ struct LayerWeights {
   const uint16_t *o;     // [d][d]
   const uint16_t *ff1;   // [d][d_ff]
   const uint16_t *ff2;   // [d_ff][d]
-  const float *b_qkv;    // [3d]
+  const float *b_qkv;    // [3d]; the query third pre-multiplied by the score scale (see Model::kq)
   const float *b_o, *b_ff1, *b_ff2;
   const float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
   float sq[6];           // fp32(scale / 127) per map, aecct_linear order
+  float sq_qs;           // fp32(sq[0] * kq): dequant scale of the scaled queries
 };
 
 struct Model {
   int n, m, L, d, n_layers, heads, hf, dff, dh;
   float eps;
-  float kappa;           // fp32(1 / sqrt(d_h))
+  float kq;              // fp32(log2(e) / sqrt(d_h)): score scale folded into the query map
   int path;              // resolved aecct_path
   int device;
   int64_t nnz1, nnz2;

@@ -6,8 +6,10 @@
 //   - sums over features are pairwise with stride halving: element c is first
 //     added to element c + w/2, then the first half is reduced the same way;
 //   - sums over attention neighbours and over tokens run in ascending index;
+//   - a head's dot product is a multiply then fused multiply-adds, ascending;
+//   - the softmax is taken in base 2 on query rows pre-scaled by log2(e)/sqrt(d_h);
 //   - only the multiply-adds written as fmaf are fused (built with
-//     -ffp-contract=off), division and square root are correctly rounded.
+//     -ffp-contract=off), division is correctly rounded.
 #pragma once
 
 #include <cstdint>
@@ -62,29 +64,57 @@ __device__ __forceinline__ float lane_tree(float (&v)[T]) {
   return v[0];
 }
 
-// Eq. 2 code of one value: round-half-even(x * (127 / alpha)).  With alpha = max|x| the
-// product is at most 127 (1 + 2^-23) in magnitude, so the code is already within
-// [-127, 127] and the clip of Eq. 2 never changes it.
-__device__ __forceinline__ int quant_code(float x, float inv) { return (int)__builtin_rintf(x * inv); }
+// Eq. 2 code of one value: the exact product x * inv rounded once, half to even, to an
+// integer.  fma(x, inv, 1.5 * 2^23) performs that rounding (the sum lies in [2^23, 2^24),
+// where the fp32 spacing is 1, and 1.5 * 2^23 is even), and the code sits in the low
+// bits: the low byte of the result's bit pattern is the int8 code.  With alpha = max|x|
+// and inv = fp32(127 / alpha) the product is at most 127 (1 + 2^-23) in magnitude, so the
+// code is already within [-127, 127] and the clip of Eq. 2 never changes it.
+__device__ __forceinline__ uint32_t quant_bits(float x, float inv) {
+  return __builtin_bit_cast(uint32_t, __builtin_fmaf(x, inv, 0x1.8p23f));
+}
+__device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_t)quant_bits(x, inv); }
 
-// exp(x), x <= 0, for the attention softmax: Cody & Waite reduction x = k ln2 + r with
-// ln2 split into a 16-bit head (k * head exact for |k| < 128) and an fp32 tail, the
-// degree-7 Taylor polynomial of e^r (coefficients fp32(1/j!)) by Horner, and an exact
-// scaling by 2^k.  Arguments below -80 give 0.
-__device__ __forceinline__ float softmax_exp(float x) {
-  if (x < -80.0f) return 0.0f;
-  const float k = __builtin_rintf(x * 0x1.715476p+0f);
-  float r = __builtin_fmaf(-k, 0x1.62e4p-1f, x);
-  r = __builtin_fmaf(-k, 0x1.7f7d1cp-20f, r);
-  float p = 0x1.a01a02p-13f;
-  p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);
-  p = __builtin_fmaf(p, r, 0x1.111112p-7f);
-  p = __builtin_fmaf(p, r, 0x1.555556p-5f);
-  p = __builtin_fmaf(p, r, 0x1.555556p-3f);
-  p = __builtin_fmaf(p, r, 0.5f);
-  p = __builtin_fmaf(p, r, 1.0f);
+// 2^x, x <= 0, for the base-2 attention softmax: clamp to -125 (the result stays a normal
+// number), exact split x = k + r with k = rint(x), r in [-1/2, 1/2], the degree-7 Taylor
+// series of 2^r = e^(r ln 2) by Horner with coefficients fp32((ln 2)^j / j!), and an exact
+// scaling by 2^k.
+__device__ __forceinline__ float softmax_exp2(float x) {
+  x = fmaxf(x, -125.0f);
+  const float k = __builtin_rintf(x);
+  const float r = x - k;
+  float p = 0x1.ffcbfcp-17f;
+  p = __builtin_fmaf(p, r, 0x1.430912p-13f);
+  p = __builtin_fmaf(p, r, 0x1.5d87fep-10f);
+  p = __builtin_fmaf(p, r, 0x1.3b2ab6p-7f);
+  p = __builtin_fmaf(p, r, 0x1.c6b08ep-5f);
+  p = __builtin_fmaf(p, r, 0x1.ebfbe0p-3f);
+  p = __builtin_fmaf(p, r, 0x1.62e430p-1f);
   p = __builtin_fmaf(p, r, 1.0f);
   return __builtin_ldexpf(p, (int)k);
+}
+
+// 1/sqrt(v), v > 0, for LayerNorm: seed 0x5F3759DF - (bits(v) >> 1) (Lomont 2003), then
+// three Newton steps y <- y (3/2 - (v/2) y^2).
+__device__ __forceinline__ float ln_rsqrt(float v) {
+  const float h = 0.5f * v;
+  float y = __builtin_bit_cast(float, 0x5F3759DFu - (__builtin_bit_cast(uint32_t, v) >> 1));
+#pragma unroll
+  for (int it = 0; it < 3; ++it) {
+    float t = y * y;
+    t = __builtin_fmaf(-h, t, 1.5f);
+    y = y * t;
+  }
+  return y;
+}
+
+// A head's dot product: q[0] k[0], then fused multiply-adds in ascending order.
+template <int DH>
+__device__ __forceinline__ float head_dot(const float (&q)[DH], const float *k) {
+  float s = q[0] * k[0];
+#pragma unroll
+  for (int t = 1; t < DH; ++t) s = __builtin_fmaf(q[t], k[t], s);
+  return s;
 }
 
 // 8 ternary codes (2 bits each, 00 -> 0, 01 -> +1, 11 -> -1, code e in bits 2e..2e+1)

@@ -239,12 +239,14 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   Model M{};
   M.n = n; M.m = m; M.L = L; M.d = d; M.n_layers = n_layers; M.heads = heads; M.hf = hf; M.dff = dff;
   M.dh = dh; M.eps = eps;
-  M.kappa = (float)(1.0 / std::sqrt((double)dh));
+  M.kq = (float)(1.4426950408889634074 / std::sqrt((double)dh));
   M.nnz1 = (int64_t)m1_idx.size();
   M.nnz2 = (int64_t)m2_idx.size();
   M.head_b1 = w->head_b1;
-  for (int l = 0; l < n_layers; ++l)
+  for (int l = 0; l < n_layers; ++l) {
     for (int k = 0; k < 6; ++k) M.layer[l].sq[k] = w->scale[(size_t)l * 6 + k] / 127.0f;
+    M.layer[l].sq_qs = M.layer[l].sq[0] * M.kq;
+  }
   M.path = path_req;
   if (M.path == AECCT_PATH_AUTO) M.path = aecct::fused_supported(M) ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
   if (M.path == AECCT_PATH_FUSED && !aecct::fused_supported(M)) return AECCT_ERR_UNSUPPORTED;
@@ -280,7 +282,11 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     pack_map(d, d, [&](int k, int j) { return Wo[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.o));
     pack_map(d, dff, [&](int k, int j) { return W1[(size_t)k * F + j]; }, (uint16_t *)(img.data() + q.ff1));
     pack_map(dff, d, [&](int k, int j) { return W2[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.ff2));
-    put(q.b_qkv, w->b_q + l * D, 4 * D);
+    {
+      std::vector<float> bqs(D);
+      for (size_t c = 0; c < D; ++c) bqs[c] = w->b_q[l * D + c] * M.kq;   // scaled query bias
+      put(q.b_qkv, bqs.data(), 4 * D);
+    }
     put(q.b_qkv + 4 * D, w->b_k + l * D, 4 * D);
     put(q.b_qkv + 8 * D, w->b_v + l * D, 4 * D);
     put(q.b_o, w->b_o + l * D, 4 * D);

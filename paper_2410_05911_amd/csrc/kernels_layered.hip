@@ -55,7 +55,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   amax = row16_max(amax);
   const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
 #pragma unroll
-  for (int tt = 0; tt < T; ++tt) p.xq[g * D + 16 * tt + c] = (int8_t)quant_code(v[tt], inv);
+  for (int tt = 0; tt < T; ++tt) p.xq[g * D + 16 * tt + c] = quant_code(v[tt], inv);
   if (c == 0) p.ax[g] = amax;
 }
 
@@ -75,7 +75,7 @@ struct GemmArgs {
   int tile0;              // first 16-column tile of the map this launch computes
   int64_t rows;
   float sq[3];            // per 1/3 of the columns (QKV) or sq[0] for all: fp32(scale / 127)
-  const float *bias;      // [NOUT]
+  const float *bias;      // [NOUT] (QKV: the query third already scaled like sq[0])
   const float *resid;     // [rows][NOUT] (LN)
   const float *ln_g, *ln_b;
   float eps;
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
               sq[t] = e[t] * e[t];
             }
             const float var = row16_sum(lane_tree<T>(sq)) / (float)NOUT;
-            const float rho = 1.0f / __builtin_sqrtf(var + p.eps);
+            const float rho = ln_rsqrt(var + p.eps);
 #pragma unroll
             for (int t = 0; t < T; ++t) {
               const int j = 16 * t + col;
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
           amax = row16_max(amax);
           const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
 #pragma unroll
-          for (int t = 0; t < T; ++t) qstage[wave][(4 * rg + i) * NOUT + 16 * t + col] = (int8_t)quant_code(v[t], inv);
+          for (int t = 0; t < T; ++t) qstage[wave][(4 * rg + i) * NOUT + 16 * t + col] = quant_code(v[t], inv);
           if (col == 0 && ok[i]) p.out_a[r[i]] = amax;
         }
       }
@@ -215,28 +215,19 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
 // ------------------------------------------------------------------------------------------
 // Head-partitioned attention (Section 4.2): one lane per (row, head); heads 0..hf-1 read
 // the first-ring neighbour list of the row, the others the second-ring list.  Two passes
-// over the neighbours (ascending): the running maximum of the scaled scores, then the
-// exponentials, their sum and the weighted value sum.  The heads of a row sit in adjacent
-// lanes, so the row's Eq. 2 scale is a shuffle reduction.
+// over the neighbours (ascending): the maximum of the scores (query rows arrive scaled by
+// log2(e)/sqrt(d_h)), then the base-2 exponentials, their sum and the weighted value sum.
+// The heads of a row sit in adjacent lanes, so the row's Eq. 2 scale is a shuffle reduction.
 // ------------------------------------------------------------------------------------------
 struct AttnArgs {
   const float *qkv;
   int64_t rows;
   int L, d, heads, hf;
-  float kappa;
   const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
   float *o;
   int8_t *oq;
   float *ao;
 };
-
-template <int DH>
-__device__ __forceinline__ float head_score(const float (&q)[DH], const float *k, float kappa) {
-  float pr[DH];
-#pragma unroll
-  for (int t = 0; t < DH; ++t) pr[t] = q[t] * k[t];
-  return lane_tree<DH>(pr) * kappa;
-}
 
 template <int DH>
 __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
@@ -259,14 +250,14 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
   float mu = -INFINITY;
   for (int e = beg; e < end; ++e) {
     const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
-    mu = fmaxf(mu, head_score<DH>(q, kr, p.kappa));
+    mu = fmaxf(mu, head_dot<DH>(q, kr));
   }
   float S = 0.0f, acc[DH];
 #pragma unroll
   for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
   for (int e = beg; e < end; ++e) {
     const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
-    const float ex = softmax_exp(head_score<DH>(q, kr, p.kappa) - mu);
+    const float ex = softmax_exp2(head_dot<DH>(q, kr) - mu);
     S = S + ex;
     const float *vr = kr + d;
 #pragma unroll
@@ -284,7 +275,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
   const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
   int8_t qv[DH];
 #pragma unroll
-  for (int t = 0; t < DH; ++t) qv[t] = (int8_t)quant_code(acc[t], inv);
+  for (int t = 0; t < DH; ++t) qv[t] = quant_code(acc[t], inv);
   int8_t *dq = p.oq + g * d + h * DH;
 #pragma unroll
   for (int t = 0; t < DH; ++t) dq[t] = qv[t];
@@ -381,7 +372,7 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
                       hipStream_t s) {
   const LayerWeights &W = M.layer[layer];
   GemmArgs a = gemm_base(xq, ax, W.qkv, rows);
-  a.sq[0] = W.sq[0];
+  a.sq[0] = W.sq_qs;
   a.sq[1] = W.sq[1];
   a.sq[2] = W.sq[2];
   a.bias = W.b_qkv;
@@ -478,8 +469,7 @@ hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t
 
 hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
                             hipStream_t s) {
-  AttnArgs a{qkv, words * M.L, M.L, M.d, M.heads, M.hf, M.kappa, M.m1_ptr, M.m1_idx, M.m2_ptr, M.m2_idx,
-             o, oq, ao};
+  AttnArgs a{qkv, words * M.L, M.L, M.d, M.heads, M.hf, M.m1_ptr, M.m1_idx, M.m2_ptr, M.m2_idx, o, oq, ao};
   if (a.rows <= 0) return hipSuccess;
   const int rpb = 256 / M.heads;
   const dim3 grid((unsigned)((a.rows + rpb - 1) / rpb));
