@@ -62,6 +62,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 // Device memory plan: byte offsets inside the model's single allocation.
 struct Plan {
   size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
+  size_t f_frag, f_vec, f_nbr, f_slot, f_chk, f_tok, f_e, f_p, f_w1;
   struct Layer { size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b; };
   std::vector<Layer> layer;
 };
@@ -132,6 +133,143 @@ int64_t chunk_words(const Model &M, int64_t batch) {
   int64_t c = (int64_t)(kChunkCapBytes / (per_word ? per_word : 1));
   if (c < 1) c = 1;
   return batch < c ? batch : c;
+}
+
+// Host image of the fused path's tables.  Lane layout (see kernel_fused.hip): lane group g
+// of token slot c holds, for maps feeding a LayerNorm, feature 16 o + 4 i + g in register
+// v = 4 o + i; the query / key / value maps are unpermuted (row r of output tile o is
+// feature 16 o + r); an input step's slot 8 g + e carries the feature the producing lane
+// group g keeps in its register e.
+struct FusedImage {
+  std::vector<uint16_t> frag;
+  std::vector<float> vec;
+  std::vector<uint16_t> nbr;
+  std::vector<uint32_t> slot_tab;
+  std::vector<uint64_t> chk;
+  std::vector<int32_t> slot_token;
+  std::vector<float> eperm, pperm, w1perm;
+};
+
+void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const std::vector<int32_t> &m1_ptr,
+                 const std::vector<int32_t> &m1_idx, const std::vector<int32_t> &m2_ptr,
+                 const std::vector<int32_t> &m2_idx, FusedImage &F) {
+  using namespace aecct;
+  const int L = M.L, n = M.n, m = M.m, NT = (L + 15) / 16, S = 16 * NT, N = M.n_layers;
+  const size_t D = fz::D, FF = fz::DFF;
+  auto len = [&](int mask, int tok) {
+    return mask == 0 ? m1_ptr[tok + 1] - m1_ptr[tok] : m2_ptr[tok + 1] - m2_ptr[tok];
+  };
+  auto mask_of = [&](int head) { return head < M.hf ? 0 : 1; };
+  // token slots: longest second-group lists first, then longest first-group lists
+  std::vector<int> order(L);
+  for (int t = 0; t < L; ++t) order[t] = t;
+  auto work = [&](int tok, int grp) {
+    int mx = 0;
+    for (int g = 0; g < 4; ++g) mx = std::max(mx, len(mask_of(4 * grp + g), tok));
+    return mx;
+  };
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    const int a2 = work(a, 1), b2 = work(b, 1);
+    if (a2 != b2) return a2 > b2;
+    return work(a, 0) > work(b, 0);
+  });
+  F.slot_token.assign(S, -1);
+  std::vector<int> slot_of(L);
+  for (int sl = 0; sl < L; ++sl) {
+    F.slot_token[sl] = order[sl];
+    slot_of[order[sl]] = sl;
+  }
+  // neighbour lists: byte offsets of the neighbours' 64-byte key rows, ascending token order
+  F.slot_tab.assign(2 * S, 0);
+  for (int sl = 0; sl < S; ++sl)
+    for (int mask = 0; mask < 2; ++mask) {
+      const int tok = F.slot_token[sl];
+      const uint32_t start = (uint32_t)F.nbr.size();
+      uint32_t cnt = 0;
+      if (tok >= 0) {
+        const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
+        const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
+        for (int e = ptr[tok]; e < ptr[tok + 1]; ++e) F.nbr.push_back((uint16_t)(slot_of[idx[e]] * 64));
+        cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
+      }
+      F.slot_tab[2 * sl + mask] = start | (cnt << 16);
+    }
+  while (F.nbr.size() % 8) F.nbr.push_back(0);
+  F.chk.assign(m, 0);
+  for (int j = 0; j < m; ++j)
+    for (int i = 0; i < n; ++i)
+      if (H[(size_t)j * n + i]) F.chk[j] |= (uint64_t)1 << i;
+  F.eperm.assign((size_t)S * 32, 0.0f);
+  if (w->pos) F.pperm.assign((size_t)S * 32, 0.0f);
+  for (int sl = 0; sl < L; ++sl)
+    for (int g = 0; g < 4; ++g)
+      for (int v = 0; v < 8; ++v) {
+        const size_t src = (size_t)F.slot_token[sl] * D + 4 * v + g, dst = ((size_t)sl * 4 + g) * 8 + v;
+        F.eperm[dst] = w->embed[src];
+        if (w->pos) F.pperm[dst] = w->pos[src];
+      }
+  F.w1perm.resize(32);
+  for (int g = 0; g < 4; ++g)
+    for (int v = 0; v < 8; ++v) F.w1perm[8 * g + v] = w->head_w1[4 * v + g];
+
+  // input slot e of lane group g -> feature, per producer layout
+  auto in_x = [](int g, int e) { return 4 * e + g; };                                   // LN outputs, embedding
+  auto in_o = [](int g, int e) { return e < 4 ? 4 * g + e : 16 + 4 * g + (e - 4); };   // attention output
+  auto in_g = [](int s, int g, int e) { return 16 * (2 * s + (e >> 2)) + 4 * g + (e & 3); };  // ReLU hidden
+  // output row r of tile o -> feature
+  auto out_ln = [](int o, int r) { return 16 * o + 4 * (r & 3) + (r >> 2); };
+  F.frag.assign((size_t)N * fz::FRAGS * 64, 0);
+  F.vec.assign((size_t)N * fz::VEC, 0.0f);
+  for (int l = 0; l < N; ++l) {
+    const int8_t *Wq = w->w_q + l * D * D, *Wk = w->w_k + l * D * D, *Wv = w->w_v + l * D * D;
+    const int8_t *Wo = w->w_o + l * D * D, *W1 = w->w_ff1 + l * D * FF, *W2 = w->w_ff2 + l * FF * D;
+    uint16_t *fr = F.frag.data() + (size_t)l * fz::FRAGS * 64;
+    auto put_frag = [&](int idx, auto value) {   // value(lane row r, lane group g, slot e) -> ternary
+      for (int lane = 0; lane < 64; ++lane) {
+        uint16_t v = 0;
+        for (int e = 0; e < 8; ++e) v |= (uint16_t)(code2(value(lane & 15, lane >> 4, e)) << (2 * e));
+        fr[(size_t)idx * 64 + lane] = v;
+      }
+    };
+    for (int o = 0; o < 6; ++o)
+      put_frag(o, [&](int r, int g, int e) {
+        const int col = 16 * o + r, mat = col / 32, j = col % 32;
+        const int8_t *W = mat == 0 ? Wq : (mat == 1 ? Wk : Wv);
+        return W[(size_t)in_x(g, e) * D + j];
+      });
+    for (int o = 0; o < 2; ++o)
+      put_frag(fz::F_O + o, [&](int r, int g, int e) { return Wo[(size_t)in_o(g, e) * D + out_ln(o, r)]; });
+    for (int o = 0; o < 8; ++o)
+      put_frag(fz::F_FF1 + o, [&](int r, int g, int e) { return W1[(size_t)in_x(g, e) * FF + 16 * o + r]; });
+    for (int o = 0; o < 2; ++o)
+      for (int st = 0; st < 4; ++st)
+        put_frag(fz::F_FF2 + 4 * o + st,
+                 [&](int r, int g, int e) { return W2[(size_t)in_g(st, g, e) * D + out_ln(o, r)]; });
+    float *V = F.vec.data() + (size_t)l * fz::VEC;
+    for (size_t j = 0; j < D; ++j) {
+      V[fz::V_BQKV + j] = w->b_q[l * D + j] * M.kq;
+      V[fz::V_BQKV + 32 + j] = w->b_k[l * D + j];
+      V[fz::V_BQKV + 64 + j] = w->b_v[l * D + j];
+    }
+    for (size_t j = 0; j < FF; ++j) V[fz::V_BFF1 + j] = w->b_ff1[l * FF + j];
+    for (int o = 0; o < 2; ++o)
+      for (int g = 0; g < 4; ++g)
+        for (int i = 0; i < 4; ++i) {
+          const int f = 16 * o + 4 * i + g, at = 16 * o + 4 * g + i;
+          V[fz::V_BO + at] = w->b_o[l * D + f];
+          V[fz::V_BFF2 + at] = w->b_ff2[l * D + f];
+        }
+    for (int g = 0; g < 4; ++g)
+      for (int v = 0; v < 8; ++v) {
+        const int f = 4 * v + g, at = 8 * g + v;
+        V[fz::V_LN1G + at] = w->ln1_g[l * D + f];
+        V[fz::V_LN1B + at] = w->ln1_b[l * D + f];
+        V[fz::V_LN2G + at] = w->ln2_g[l * D + f];
+        V[fz::V_LN2B + at] = w->ln2_b[l * D + f];
+      }
+    V[fz::V_SQ + 0] = M.layer[l].sq_qs;
+    for (int k = 1; k < 6; ++k) V[fz::V_SQ + k] = M.layer[l].sq[k];
+  }
 }
 
 aecct_status from_hip(hipError_t e) {
@@ -251,8 +389,26 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   if (M.path == AECCT_PATH_AUTO) M.path = aecct::fused_supported(M) ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
   if (M.path == AECCT_PATH_FUSED && !aecct::fused_supported(M)) return AECCT_ERR_UNSUPPORTED;
 
+  // fused-path tables (built whenever the shape allows the fused kernel)
+  FusedImage FI;
+  if (aecct::fused_supported(M)) build_fused(M, H, w, m1_ptr, m1_idx, m2_ptr, m2_idx, FI);
+
   // host image of the device block
-  const Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
+  Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
+  {
+    size_t off = P.total;
+    auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+    P.f_frag = take(2 * FI.frag.size());
+    P.f_vec = take(4 * FI.vec.size());
+    P.f_nbr = take(2 * FI.nbr.size());
+    P.f_slot = take(4 * FI.slot_tab.size());
+    P.f_chk = take(8 * FI.chk.size());
+    P.f_tok = take(4 * FI.slot_token.size());
+    P.f_e = take(4 * FI.eperm.size());
+    P.f_p = take(4 * FI.pperm.size());
+    P.f_w1 = take(4 * FI.w1perm.size());
+    P.total = off;
+  }
   std::vector<unsigned char> img;
   try {
     img.assign(P.total, 0);
@@ -271,6 +427,15 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   put(P.w1, w->head_w1, 4 * D);
   put(P.wo, w->head_wo, 4 * (size_t)L * n);
   put(P.bo, w->head_bo, 4 * (size_t)n);
+  put(P.f_frag, FI.frag.data(), 2 * FI.frag.size());
+  put(P.f_vec, FI.vec.data(), 4 * FI.vec.size());
+  put(P.f_nbr, FI.nbr.data(), 2 * FI.nbr.size());
+  put(P.f_slot, FI.slot_tab.data(), 4 * FI.slot_tab.size());
+  put(P.f_chk, FI.chk.data(), 8 * FI.chk.size());
+  put(P.f_tok, FI.slot_token.data(), 4 * FI.slot_token.size());
+  put(P.f_e, FI.eperm.data(), 4 * FI.eperm.size());
+  put(P.f_p, FI.pperm.data(), 4 * FI.pperm.size());
+  put(P.f_w1, FI.w1perm.data(), 4 * FI.w1perm.size());
   for (int l = 0; l < n_layers; ++l) {
     const auto &q = P.layer[l];
     const int8_t *Wq = w->w_q + l * D * D, *Wk = w->w_k + l * D * D, *Wv = w->w_v + l * D * D;
@@ -344,6 +509,20 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     Lw.ln1_b = (const float *)(b + q.ln1_b);
     Lw.ln2_g = (const float *)(b + q.ln2_g);
     Lw.ln2_b = (const float *)(b + q.ln2_b);
+  }
+  if (!FI.frag.empty()) {
+    aecct::FusedTables &T = M.fused;
+    T.ready = true;
+    T.frag = (const uint16_t *)(b + P.f_frag);
+    T.vec = (const float *)(b + P.f_vec);
+    T.nbr = (const uint32_t *)(b + P.f_nbr);
+    T.nbr_words = (int)(FI.nbr.size() / 2);
+    T.slot_tab = (const uint32_t *)(b + P.f_slot);
+    T.chk = (const uint64_t *)(b + P.f_chk);
+    T.slot_token = (const int32_t *)(b + P.f_tok);
+    T.eperm = (const float *)(b + P.f_e);
+    T.pperm = FI.pperm.empty() ? nullptr : (const float *)(b + P.f_p);
+    T.w1perm = (const float *)(b + P.f_w1);
   }
   am->M = M;
   *out = am;

@@ -1,4 +1,23 @@
-// Fused path: whole words resident in LDS, every layer in one launch.
+// Fused path: one wavefront decodes one whole word, every layer, in one launch.
+//
+// Shapes: d = 32, 8 heads of 4, d_ff = 128, L = n + m <= 64 tokens, n <= 64.  A word's
+// tokens fill NT = ceil(L / 16) tiles of 16 token "slots"; the host orders tokens by
+// attention work so that the 16 lanes of a tile run neighbour loops of similar length.
+//
+// The linear maps run transposed on v_mfma_i32_16x16x32_i8: the ternary weights are the A
+// operand (16 output features x 32 inputs) and 16 tokens are the columns, so lane
+// (c = lane & 15, g = lane >> 4) owns token slot c of a tile and, for every map, a fixed
+// set of 4 (per 16-feature output tile) of that token's features.  The host permutes the
+// rows and input slots of every packed weight fragment so that
+//   - the outputs feeding a LayerNorm (attention output projection, second FFN map) land
+//     with feature 4 v + g in register v (v = 0..7): the pairwise feature sum is three
+//     in-lane levels (v strides 4, 2, 1) then lane xor 32 and lane xor 16;
+//   - the int8 codes a lane produces are exactly the B-operand bytes of the next map
+//     (input slot 8 g + e of a 32-input step), so activations never leave registers;
+//   - the query, key and value outputs of lane group g are the 4 dims of head g (first
+//     16 features) or head 4 + g (second 16).
+// Queries stay in registers; keys and values of one head group (4 heads) at a time go to
+// a per-wave LDS buffer that the neighbour loops gather from.
 #include <hip/hip_runtime.h>
 
 #include "aecct_internal.h"
@@ -6,10 +25,436 @@
 
 namespace aecct {
 
-bool fused_supported(const Model &) { return false; }
 
-hipError_t launch_fused(const Model &, const float *, int64_t, uint8_t *, float *, hipStream_t) {
-  return hipErrorNotSupported;
+
+struct FusedArgs {
+  const uint16_t *frag;        // [N][FRAGS][64] 2-bit codes
+  const float *vec;            // [N][VEC]
+  const uint32_t *nbr;         // neighbour entries, uint16 byte offsets, two per word
+  int nbr_words;
+  const uint32_t *slot_tab;    // [16 NT][2]: start | count << 16, first / second ring
+  const uint64_t *chk;         // [m] variable bitmask of each check
+  const int32_t *slot_token;   // [16 NT] token of each slot or -1
+  const float *eperm, *pperm;  // [16 NT][4][8] embedding (and positional) rows in lane order
+  const float *w1perm;         // [4][8]
+  float b1;
+  const float *wo, *bo;        // [L][n], [n]
+  const float *y;
+  uint8_t *bits;
+  float *logits;
+  int64_t words;
+  int n, m, L, N, hf;
+  float eps;
+  int off_vec, off_nbr, off_slot, off_chk, off_tok, off_kv, kv_bytes;
+};
+
+namespace {
+
+__device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32); }
+__device__ __forceinline__ float xor16(float v) { return __shfl_xor(v, 16); }
+
+// Pairwise sum over a token's 32 features held as x[v] = feature 4 v + g.
+__device__ __forceinline__ float token_sum(const float (&x)[8]) {
+  float u[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) u[v] = x[v];
+  float s = lane_tree<8>(u);
+  s = s + xor32(s);
+  s = s + xor16(s);
+  return s;
+}
+
+__device__ __forceinline__ float token_max_abs(const float (&x)[8]) {
+  float a = fabsf(x[0]);
+#pragma unroll
+  for (int v = 1; v < 8; ++v) a = fmaxf(a, fabsf(x[v]));
+  a = fmaxf(a, xor32(a));
+  a = fmaxf(a, xor16(a));
+  return a;
+}
+
+// Byte 0 of four Eq. 2 code patterns into one dword (byte i from b[i]).
+__device__ __forceinline__ uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  const uint32_t lo = __builtin_amdgcn_perm(b1, b0, 0x0c0c0400u);
+  const uint32_t hi = __builtin_amdgcn_perm(b3, b2, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+}
+
+// Eq. 2 over a token's 32 values held 8 per lane; returns alpha, writes the 8 codes
+// (value v in byte v) to two dwords.
+__device__ __forceinline__ float quant8(const float (&x)[8], uint32_t &lo, uint32_t &hi) {
+  const float a = token_max_abs(x);
+  const float inv = a == 0.0f ? 0.0f : 127.0f / a;
+  lo = pack4(quant_bits(x[0], inv), quant_bits(x[1], inv), quant_bits(x[2], inv), quant_bits(x[3], inv));
+  hi = pack4(quant_bits(x[4], inv), quant_bits(x[5], inv), quant_bits(x[6], inv), quant_bits(x[7], inv));
+  return a;
+}
+
+// LayerNorm of a token's 32 features (x[v] = feature 4 v + g), gain / offset in lane order.
+__device__ __forceinline__ void token_layernorm(float (&x)[8], const float *gp, const float *bp, float eps) {
+  const float mean = token_sum(x) / 32.0f;
+  float e[8], sq[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    e[v] = x[v] - mean;
+    sq[v] = e[v] * e[v];
+  }
+  const float var = token_sum(sq) / 32.0f;
+  const float rho = ln_rsqrt(var + eps);
+#pragma unroll
+  for (int v = 0; v < 8; ++v) x[v] = __builtin_fmaf(e[v] * rho, gp[v], bp[v]);
+}
+
+__device__ __forceinline__ long as_long(uint32_t lo, uint32_t hi) { return (long)(((uint64_t)hi << 32) | lo); }
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One (token slot, head) softmax row: q is the scaled query, entries are byte offsets of
+// the neighbours' key rows in the head group buffer (ascending token order), kbase points
+// at this lane's head in that buffer, values sit vofs bytes after the keys.
+__device__ __forceinline__ void attend(const float (&q)[4], const uint16_t *ent, int cnt, const unsigned char *kbase,
+                                       int vofs, float (&o)[4]) {
+  float mu = -INFINITY;
+  for (int e = 0; e < cnt; ++e) {
+    const float4 k = *(const float4 *)(kbase + ent[e]);
+    const float kk[4] = {k.x, k.y, k.z, k.w};
+    mu = fmaxf(mu, head_dot<4>(q, kk));
+  }
+  float S = 0.0f, acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int e = 0; e < cnt; ++e) {
+    const unsigned char *kp = kbase + ent[e];
+    const float4 k = *(const float4 *)kp;
+    const float kk[4] = {k.x, k.y, k.z, k.w};
+    const float ex = softmax_exp2(head_dot<4>(q, kk) - mu);
+    S = S + ex;
+    const float4 vv = *(const float4 *)(kp + vofs);
+    acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
+    acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
+    acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
+    acc[3] = __builtin_fmaf(ex, vv.w, acc[3]);
+  }
+  const float rS = cnt > 0 ? 1.0f / S : 0.0f;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) o[t] = acc[t] * rS;
+}
+
+}  // namespace
+
+template <int NT>
+__global__ __launch_bounds__(fz::kMaxWaves * 64, 1) void k_fused_decode(FusedArgs p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  // ---- one-time staging: packed ternary fragments -> int8, per-layer vectors, tables ----
+  {
+    uint64_t *sf = (uint64_t *)smem;
+    const int nf = p.N * fz::FRAGS * 64;
+    for (int u = tid; u < nf; u += nthr) sf[u] = unpack_ternary8(p.frag[u]);
+    float *sv = (float *)(smem + p.off_vec);
+    for (int u = tid; u < p.N * fz::VEC; u += nthr) sv[u] = p.vec[u];
+    uint32_t *sn = (uint32_t *)(smem + p.off_nbr);
+    for (int u = tid; u < p.nbr_words; u += nthr) sn[u] = p.nbr[u];
+    uint32_t *ss = (uint32_t *)(smem + p.off_slot);
+    for (int u = tid; u < 32 * NT; u += nthr) ss[u] = p.slot_tab[u];
+    uint64_t *sc = (uint64_t *)(smem + p.off_chk);
+    for (int u = tid; u < p.m; u += nthr) sc[u] = p.chk[u];
+    int32_t *st = (int32_t *)(smem + p.off_tok);
+    for (int u = tid; u < 16 * NT; u += nthr) st[u] = p.slot_token[u];
+  }
+  __syncthreads();
+
+  const int lane = tid & 63, c = lane & 15, g = lane >> 4;
+  const int wave = tid >> 6, nw = nthr >> 6;
+  const uint64_t *sfrag = (const uint64_t *)smem;
+  const float *svec = (const float *)(smem + p.off_vec);
+  const uint16_t *snbr = (const uint16_t *)(smem + p.off_nbr);
+  const uint32_t *sslot = (const uint32_t *)(smem + p.off_slot);
+  const uint64_t *schk = (const uint64_t *)(smem + p.off_chk);
+  const int32_t *stok = (const int32_t *)(smem + p.off_tok);
+  unsigned char *kv = smem + p.off_kv + wave * p.kv_bytes;
+  const int vofs = 16 * NT * 64;           // values follow the keys of all slots
+  unsigned char *kbase = kv + 16 * g;      // this lane's head inside a slot's 64-byte key row
+  const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
+
+  int tok[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) tok[t] = stok[16 * t + c];
+
+  for (int64_t w = (int64_t)blockIdx.x * nw + wave; w < p.words; w += (int64_t)gridDim.x * nw) {
+    // ---- pre-processing h(y) (Section 3) and embedding ----
+    const float *yw = p.y + w * p.n;
+    const float ylane = lane < p.n ? yw[lane] : 0.0f;
+    const uint64_t neg = __ballot(ylane < 0.0f);
+    float X[NT][8], al[NT];
+    uint32_t xb[NT][2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int tk = tok[t];
+      const float yv = __shfl(ylane, (tk >= 0 && tk < p.n) ? tk : 0);
+      float tv = 0.0f;
+      if (tk >= 0) {
+        if (tk < p.n) {
+          tv = fabsf(yv);
+        } else {
+          const int s = __builtin_popcountll(neg & schk[tk - p.n]) & 1;
+          tv = s ? -1.0f : 1.0f;
+        }
+      }
+      const float4 *er = (const float4 *)(p.eperm + ((16 * t + c) * 4 + g) * 8);
+      const float4 e0 = er[0], e1 = er[1];
+      const float ev[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+      float pv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (p.pperm) {
+        const float4 *pr = (const float4 *)(p.pperm + ((16 * t + c) * 4 + g) * 8);
+        const float4 p0 = pr[0], p1 = pr[1];
+        pv[0] = p0.x; pv[1] = p0.y; pv[2] = p0.z; pv[3] = p0.w;
+        pv[4] = p1.x; pv[5] = p1.y; pv[6] = p1.z; pv[7] = p1.w;
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) X[t][v] = __builtin_fmaf(tv, ev[v], pv[v]);
+      al[t] = quant8(X[t], xb[t][0], xb[t][1]);
+    }
+
+    for (int l = 0; l < p.N; ++l) {
+      const uint64_t *F = sfrag + l * fz::FRAGS * 64 + lane;
+      const float *V = svec + l * fz::VEC;
+      const float sq_q = V[fz::V_SQ + 0], sq_k = V[fz::V_SQ + 1], sq_v = V[fz::V_SQ + 2];
+      const float sq_o = V[fz::V_SQ + 3], sq_1 = V[fz::V_SQ + 4], sq_2 = V[fz::V_SQ + 5];
+      // ---- per head group (heads g, then 4 + g): queries, keys, values (Eq. 3) of that
+      // group, keys and values to LDS, then head-partitioned attention (Section 4.2) ----
+      float ob[NT][8];
+#pragma unroll
+      for (int grp = 0; grp < 2; ++grp) {
+        float q[NT][4];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const long bop = as_long(xb[t][0], xb[t][1]);
+          const v4i aq = mfma_i8_16x16x32((long)F[(0 + grp) * 64], bop, v4i{0, 0, 0, 0});
+          const v4i ak = mfma_i8_16x16x32((long)F[(2 + grp) * 64], bop, v4i{0, 0, 0, 0});
+          const v4i av = mfma_i8_16x16x32((long)F[(4 + grp) * 64], bop, v4i{0, 0, 0, 0});
+          const float scq = al[t] * sq_q, sck = al[t] * sq_k, scv = al[t] * sq_v;
+          const float *bq = V + fz::V_BQKV + 16 * grp + 4 * g;
+          float kk[4], vv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            q[t][i] = __builtin_fmaf((float)aq[i], scq, bq[i]);
+            kk[i] = __builtin_fmaf((float)ak[i], sck, bq[32 + i]);
+            vv[i] = __builtin_fmaf((float)av[i], scv, bq[64 + i]);
+          }
+          *(float4 *)(kbase + (16 * t + c) * 64) = make_float4(kk[0], kk[1], kk[2], kk[3]);
+          *(float4 *)(kbase + vofs + (16 * t + c) * 64) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+        }
+        wave_sync_lds();
+        const int mask = grp == 0 ? mask1 : mask2;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const uint32_t st = sslot[(16 * t + c) * 2 + mask];
+          float o[4];
+          attend(q[t], snbr + (st & 0xffff), (int)(st >> 16), kbase, vofs, o);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ob[t][4 * grp + i] = o[i];
+        }
+        wave_sync_lds();
+      }
+      // ---- output projection, residual, LN1 (Section 6), Eq. 2 ----
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        uint32_t lo, hi;
+        const float ao = quant8(ob[t], lo, hi);
+        const long bop = as_long(lo, hi);
+        const v4i a0 = mfma_i8_16x16x32((long)F[fz::F_O * 64], bop, v4i{0, 0, 0, 0});
+        const v4i a1 = mfma_i8_16x16x32((long)F[(fz::F_O + 1) * 64], bop, v4i{0, 0, 0, 0});
+        const float sc = ao * sq_o;
+        const float *bo = V + fz::V_BO + 4 * g;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          X[t][i] = X[t][i] + __builtin_fmaf((float)a0[i], sc, bo[i]);
+          X[t][4 + i] = X[t][4 + i] + __builtin_fmaf((float)a1[i], sc, bo[16 + i]);
+        }
+        token_layernorm(X[t], V + fz::V_LN1G + 8 * g, V + fz::V_LN1B + 8 * g, p.eps);
+        al[t] = quant8(X[t], xb[t][0], xb[t][1]);
+      }
+      // ---- feed-forward block with ReLU, residual, LN2, Eq. 2 ----
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const long bop = as_long(xb[t][0], xb[t][1]);
+        v4i acc[8];
+#pragma unroll
+        for (int o = 0; o < 8; ++o) acc[o] = mfma_i8_16x16x32((long)F[(fz::F_FF1 + o) * 64], bop, v4i{0, 0, 0, 0});
+        const float sc = al[t] * sq_1;
+        float G[8][4];
+        float amax = 0.0f;
+#pragma unroll
+        for (int o = 0; o < 8; ++o)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float f = __builtin_fmaf((float)acc[o][i], sc, V[fz::V_BFF1 + 16 * o + 4 * g + i]);
+            G[o][i] = f > 0.0f ? f : 0.0f;
+            amax = fmaxf(amax, G[o][i]);
+          }
+        amax = fmaxf(amax, xor32(amax));
+        amax = fmaxf(amax, xor16(amax));
+        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+        uint32_t gb[8];
+#pragma unroll
+        for (int o = 0; o < 8; ++o)
+          gb[o] = pack4(quant_bits(G[o][0], inv), quant_bits(G[o][1], inv), quant_bits(G[o][2], inv),
+                        quant_bits(G[o][3], inv));
+        v4i b0 = v4i{0, 0, 0, 0}, b1 = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const long gop = as_long(gb[2 * s], gb[2 * s + 1]);
+          b0 = mfma_i8_16x16x32((long)F[(fz::F_FF2 + s) * 64], gop, b0);
+          b1 = mfma_i8_16x16x32((long)F[(fz::F_FF2 + 4 + s) * 64], gop, b1);
+        }
+        const float sc2 = amax * sq_2;
+        const float *b2 = V + fz::V_BFF2 + 4 * g;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          X[t][i] = X[t][i] + __builtin_fmaf((float)b0[i], sc2, b2[i]);
+          X[t][4 + i] = X[t][4 + i] + __builtin_fmaf((float)b1[i], sc2, b2[16 + i]);
+        }
+        token_layernorm(X[t], V + fz::V_LN2G + 8 * g, V + fz::V_LN2B + 8 * g, p.eps);
+        al[t] = quant8(X[t], xb[t][0], xb[t][1]);
+      }
+    }
+
+    // ---- output head and hard decision (Section 3) ----
+    float *zbuf = (float *)kv;
+    {
+      const float4 *wr = (const float4 *)(p.w1perm + 8 * g);
+      const float4 w0 = wr[0], w1 = wr[1];
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        float pr[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) pr[v] = X[t][v] * wv[v];
+        const float z = token_sum(pr) + p.b1;
+        if (g == 0 && tok[t] >= 0) zbuf[tok[t]] = z;
+      }
+    }
+    wave_sync_lds();
+    if (lane < p.n) {
+      float acc = 0.0f;
+      for (int i = 0; i < p.L; ++i) acc = __builtin_fmaf(zbuf[i], p.wo[(int64_t)i * p.n + lane], acc);
+      const float f = acc + p.bo[lane];
+      p.bits[w * p.n + lane] = (uint8_t)((ylane < 0.0f) != (f < 0.0f));
+      if (p.logits) p.logits[w * p.n + lane] = f;
+    }
+    wave_sync_lds();
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// host-side launcher
+// ------------------------------------------------------------------------------------------
+
+int fused_tiles(const Model &M) { return (M.L + 15) / 16; }
+
+// LDS layout of one block: fragments, vectors, neighbour entries, slot table, check
+// masks, slot tokens (all shared), then one key/value buffer per wave.
+struct FusedLds {
+  int off_vec, off_nbr, off_slot, off_chk, off_tok, off_kv, kv_bytes;
+};
+
+FusedLds fused_lds(const Model &M, int nbr_words) {
+  const int NT = fused_tiles(M);
+  FusedLds L{};
+  size_t off = (size_t)M.n_layers * fz::FRAGS * 64 * 8;
+  L.off_vec = (int)off;
+  off += (size_t)M.n_layers * fz::VEC * 4;
+  L.off_nbr = (int)off;
+  off += (size_t)nbr_words * 4;
+  L.off_slot = (int)off;
+  off += (size_t)32 * NT * 4;
+  off = (off + 7) / 8 * 8;
+  L.off_chk = (int)off;
+  off += (size_t)M.m * 8;
+  L.off_tok = (int)off;
+  off += (size_t)16 * NT * 4;
+  off = (off + 15) / 16 * 16;
+  L.off_kv = (int)off;
+  L.kv_bytes = NT * 2048;
+  return L;
+}
+
+bool fused_supported(const Model &M) {
+  if (M.d != 32 || M.heads != 8 || M.dff != 128 || M.L > 64 || M.n > 64) return false;
+  const int nbr_words = (int)(((M.nnz1 + M.nnz2) + 7) / 8 * 4);
+  const FusedLds L = fused_lds(M, nbr_words);
+  return (size_t)L.off_kv + 4 * (size_t)L.kv_bytes <= (size_t)fz::kLdsMax;   // room for four waves
+}
+
+template <int NT>
+static hipError_t launch_nt(const FusedArgs &a, int waves, size_t lds, int grid, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       fz::kLdsMax);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(k_fused_decode<NT>, dim3(grid), dim3(waves * 64), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
+                        hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  const FusedTables &T = M.fused;
+  const int NT = fused_tiles(M);
+  FusedArgs a{};
+  a.frag = T.frag;
+  a.vec = T.vec;
+  a.nbr = T.nbr;
+  a.nbr_words = T.nbr_words;
+  a.slot_tab = T.slot_tab;
+  a.chk = T.chk;
+  a.slot_token = T.slot_token;
+  a.eperm = T.eperm;
+  a.pperm = T.pperm;
+  a.w1perm = T.w1perm;
+  a.b1 = M.head_b1;
+  a.wo = M.head_wo;
+  a.bo = M.head_bo;
+  a.y = y;
+  a.bits = bits;
+  a.logits = logits;
+  a.words = words;
+  a.n = M.n;
+  a.m = M.m;
+  a.L = M.L;
+  a.N = M.n_layers;
+  a.hf = M.hf;
+  a.eps = M.eps;
+  const FusedLds Ld = fused_lds(M, T.nbr_words);
+  a.off_vec = Ld.off_vec;
+  a.off_nbr = Ld.off_nbr;
+  a.off_slot = Ld.off_slot;
+  a.off_chk = Ld.off_chk;
+  a.off_tok = Ld.off_tok;
+  a.off_kv = Ld.off_kv;
+  a.kv_bytes = Ld.kv_bytes;
+  const size_t off = (size_t)Ld.off_kv;
+  int waves = (int)((fz::kLdsMax - off) / a.kv_bytes);
+  if (waves > fz::kMaxWaves) waves = fz::kMaxWaves;
+  if (waves < 1) return hipErrorInvalidConfiguration;
+  const size_t lds = off + (size_t)waves * a.kv_bytes;
+  int64_t blocks = (words + waves - 1) / waves;
+  const int64_t per_cu = (int64_t)(fz::kLdsMax / lds) > 0 ? (int64_t)(fz::kLdsMax / lds) : 1;
+  const int64_t cap = 256 * per_cu;
+  const int grid = (int)(blocks < cap ? blocks : cap);
+  switch (NT) {
+    case 1: return launch_nt<1>(a, waves, lds, grid, s);
+    case 2: return launch_nt<2>(a, waves, lds, grid, s);
+    case 3: return launch_nt<3>(a, waves, lds, grid, s);
+    case 4: return launch_nt<4>(a, waves, lds, grid, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace aecct

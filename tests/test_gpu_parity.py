@@ -199,3 +199,40 @@ def test_deterministic_and_stream(P):
     s.synchronize()
     b2, l2 = dec.decode(yd)
     assert torch.equal(l1, l2) and torch.equal(b1, b2)
+
+
+# ------------------------------------------------------------------------------ fused path
+@pytest.mark.parametrize("c", [1, 2])
+def test_fused_and_layered_paths_agree(P, c):
+    """The single-launch fused kernel and the per-stage layered kernels give identical bits
+    and logits (same evaluation order), on a ragged batch."""
+    print(f"[paths] config {c}", flush=True)
+    cfg, H, G, w, y, x = build_workload(c, batch=4099)
+    fused = P.Decoder(H, w, path=P.PATH_FUSED)
+    layered = P.Decoder(H, w, path=P.PATH_LAYERED)
+    assert fused.path == P.PATH_FUSED and layered.path == P.PATH_LAYERED
+    yd = _dev(y)
+    bf, lf = fused.decode(yd)
+    bl, ll = layered.decode(yd)
+    assert torch.equal(lf, ll) and torch.equal(bf, bl)
+
+
+@pytest.mark.parametrize("hf,with_pos", [(2, False), (6, True), (0, False), (8, True)])
+def test_fused_head_split_and_positional_table(P, oracle_mod, hf, with_pos):
+    """Other first/second-ring head splits (Table 4 of the paper ablates 2/6, 4/4, 6/2) and
+    a fixed positional table (the inference form of the spectral encoding) on BCH(31,16)."""
+    from workloads import random_weights
+    from workloads.configs import parity_check
+    from workloads.channel import awgn_words
+    from workloads.codes import generator_from_parity
+    print(f"[variants] hf {hf} pos {with_pos}", flush=True)
+    H = parity_check(CONFIGS[2])
+    m, n = H.shape
+    w = random_weights(n, m, 32, 3, 8, seed=40 + hf, first_ring_heads=hf, with_pos=with_pos)
+    y, x, _ = awgn_words(generator_from_parity(H), 333, (3.0, 5.0), seed=7)
+    om = oracle_mod.OracleModel(H, w)
+    bo, fo = om.decode(y, n_threads=16)
+    for path in (P.PATH_FUSED, P.PATH_LAYERED):
+        dec = P.Decoder(H, w, path=path)
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
