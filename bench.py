@@ -31,10 +31,19 @@ PEAK_HBM = 8.0e12
 
 
 def algorithmic_counts(H, w):
-    """Per-word work of the method as defined (not as executed): fp32 ALU operations, int8
-    MACs and HBM bytes.  Each scalar arithmetic operation of the definition counts once (an
-    FMA once, exp once, a division or square root once); the int8 x ternary products are
-    MFMA work and counted separately."""
+    """Per-word work of the method as the paper writes it (not as executed).
+
+    fp32/ALU operations: every scalar operation of Sections 3-4 counts once, with each
+    multiply-accumulate of a dot product, of the attention-weighted value sum, of the
+    dequantisation plus bias and of the LayerNorm affine map counted as one operation (one
+    fused instruction); exp, division, square root and rounding count once each.  The
+    ternary x int8 products are MFMA work, counted separately as int8 MACs.
+      quantisation of a K-wide row (Eq. 2): max|x|, multiply, round per value + Q_b/alpha
+      dequant (Eq. 3): one multiply-add per output + alpha * scale per row and map
+      LayerNorm: sum, subtract, square-accumulate, normalise, affine per value + 5 per row
+      attention pair: d_h multiply-adds (q.k), scale, max, subtract, exp, sum, d_h (p v)
+      attention row and head: 1/S and d_h products
+    """
     m, n = H.shape
     L, d, N, dff, heads = n + m, w.d, w.n_layers, w.d_ff, w.heads
     dh, hf = d // heads, w.first_ring_heads
@@ -43,21 +52,21 @@ def algorithmic_counts(H, w):
     A[n:, :n] = H
     nnz1 = int((A != 0).sum())
     nnz2 = int(((A @ A) != 0).sum())
-    quant = lambda K: 4 * K + 1                 # max|x|, 127/alpha, x*inv, rint, to-int
-    token_layer = (3 * quant(d) + quant(dff)    # inputs of QKV, O, FF1 and FF2
-                   + 2 * (3 * d + d + dff + d) + 4   # int->fp32 + fma dequant, 4 row scales
-                   + 2 * d                      # residual adds
-                   + 2 * (6 * d + 3)            # two LayerNorms
-                   + dff)                       # ReLU
-    pair = 3 * dh + 4                           # dot (dh mul, dh-1 add), scale, max, sub, exp, sum, dh fma
-    row_head = dh + 1                           # 1/S and dh products
+    quant = lambda K: 3 * K + 1
+    token_layer = (3 * quant(d) + quant(dff)          # inputs of the QKV, O, FF1, FF2 maps
+                   + (3 * d + d + dff + d) + 4        # dequant + bias, 4 row scales
+                   + 2 * d                            # two residual adds
+                   + 2 * (5 * d + 5)                  # two LayerNorms
+                   + dff)                             # ReLU
+    pair = 2 * dh + 5
+    row_head = dh + 1
     pairs = hf * nnz1 + (heads - hf) * nnz2
     layer = L * token_layer + pairs * pair + L * heads * row_head
-    embed = L * (d + 1) + int(H.sum())          # t*E rows, |y| / syndrome XORs
-    head = L * 2 * d + n * (L + 1) + 2 * n
+    embed = L * (d + 1) + int(H.sum())                # t * E_i rows, |y| / sign, syndrome XORs
+    head = L * (d + 1) + n * (L + 1 + 2)              # z_i, f_o, hard decision
     alu = embed + N * layer + head
     macs = N * L * (3 * d * d + d * d + 2 * d * dff)
-    hbm = 4 * n + n + 4 * n                     # y in, bits out, logits out
+    hbm = 4 * n + n + 4 * n                           # y in, bits and logits out
     return dict(alu_ops=alu, int8_macs=macs, hbm_bytes=hbm, pairs_per_layer=pairs)
 
 
@@ -71,15 +80,33 @@ def kernel_source_hash():
 
 
 def measured_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
-    on the current kernel sources."""
-    p = os.path.join(ROOT, "profiles", f"{kernel}__{workload}__pmc.json")
+    """HBM bytes per launch from the committed rocprofv3 counter summary (lines
+    `source_hash: ...` and `hbm_bytes_per_launch: ...`), if it was taken on the current
+    kernel sources; otherwise None."""
+    p = os.path.join(ROOT, "profiles", f"{kernel}__{workload}__hbm_counters.md")
     if not os.path.exists(p):
         return None
-    rec = json.load(open(p))
+    rec = {}
+    for ln in open(p):
+        if ":" in ln and ln.strip().startswith(("source_hash", "hbm_bytes_per_launch")):
+            k, v = ln.split(":", 1)
+            rec[k.strip()] = v.strip().strip("`")
     if rec.get("source_hash") != kernel_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return float(rec["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in rec else None
+
+
+def copy_calibration(mib: int = 512):
+    """A plain device-to-device copy of a known size (the scale for the HBM counters)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4}))
 
 
 def cpu_baseline(H, w, y, budget_s=12.0):
@@ -107,7 +134,12 @@ def main():
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 layered, 2 fused")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 512 MiB device copy (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the decode shards over words with no exchange); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)

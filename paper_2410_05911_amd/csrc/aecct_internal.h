@@ -20,7 +20,7 @@ constexpr int F_O = 6, F_FF1 = 8, F_FF2 = 16;
 constexpr int VEC = 424;       // floats per layer
 constexpr int V_BQKV = 0, V_BO = 96, V_BFF1 = 128, V_BFF2 = 256, V_LN1G = 288, V_LN1B = 320, V_LN2G = 352,
               V_LN2B = 384, V_SQ = 416;
-constexpr int kMaxWaves = 12;
+constexpr int kWaves = 12;     // wavefronts (words in flight) per block
 constexpr int kLdsMax = 160 * 1024;
 }  // namespace fz
 
@@ -50,6 +50,8 @@ struct FusedTables {
   const uint32_t *nbr;         // neighbour entries (uint16 byte offsets into a wave's key buffer)
   int nbr_words;               // 32-bit words of nbr (a multiple of 4)
   const uint32_t *slot_tab;    // [16 NT][2] start | count << 16 per slot, first / second ring
+  const uint32_t *tile_tab;    // [NT][2] padded list length T | shortest real length << 16 per head group
+  int maxt;                    // largest T
   const uint64_t *chk;         // [m] bitmask of the variables of each check
   const int32_t *slot_token;   // [16 NT] token in each slot, -1 for padding
   const float *eperm, *pperm;  // [16 NT][4][8] embedding / positional rows in lane order
@@ -95,7 +97,8 @@ hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t w
 hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a, int64_t rows, int32_t *acc,
                                hipStream_t s);
 // ---- fused path (kernel_fused.hip) -----------------------------------------------------
-bool fused_supported(const Model &M);
+bool fused_supported(const Model &M);                 // shape check
+bool fused_fits(const Model &M, int nbr_words);       // LDS check with the built neighbour table
 hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
                         hipStream_t s);
 

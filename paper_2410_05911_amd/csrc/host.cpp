@@ -62,7 +62,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 // Device memory plan: byte offsets inside the model's single allocation.
 struct Plan {
   size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
-  size_t f_frag, f_vec, f_nbr, f_slot, f_chk, f_tok, f_e, f_p, f_w1;
+  size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
   struct Layer { size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b; };
   std::vector<Layer> layer;
 };
@@ -145,6 +145,8 @@ struct FusedImage {
   std::vector<float> vec;
   std::vector<uint16_t> nbr;
   std::vector<uint32_t> slot_tab;
+  std::vector<uint32_t> tile_tab;
+  int maxt = 0;
   std::vector<uint64_t> chk;
   std::vector<int32_t> slot_token;
   std::vector<float> eperm, pperm, w1perm;
@@ -179,7 +181,29 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
     F.slot_token[sl] = order[sl];
     slot_of[order[sl]] = sl;
   }
-  // neighbour lists: byte offsets of the neighbours' 64-byte key rows, ascending token order
+  // Per tile and head group the neighbour loop runs T = the longest list among the tile's
+  // lanes; cmin = the shortest real list (padding slots excluded).
+  F.tile_tab.assign(2 * NT, 0);
+  std::vector<int> padT(NT, 1);
+  for (int t = 0; t < NT; ++t)
+    for (int grp = 0; grp < 2; ++grp) {
+      int T = 1, cmin = 1 << 15;
+      for (int c = 0; c < 16; ++c) {
+        const int tok = F.slot_token[16 * t + c];
+        if (tok < 0) continue;
+        for (int g = 0; g < 4; ++g) {
+          const int l = len(mask_of(4 * grp + g), tok);
+          T = std::max(T, l);
+          cmin = std::min(cmin, l);
+        }
+      }
+      if (cmin > T) cmin = T;
+      F.tile_tab[2 * t + grp] = (uint32_t)T | ((uint32_t)cmin << 16);
+      padT[t] = std::max(padT[t], T);
+      F.maxt = std::max(F.maxt, T);
+    }
+  // neighbour lists: byte offsets of the neighbours' 64-byte key rows, ascending token order,
+  // padded to the tile's longest list with copies of the first entry
   F.slot_tab.assign(2 * S, 0);
   for (int sl = 0; sl < S; ++sl)
     for (int mask = 0; mask < 2; ++mask) {
@@ -192,6 +216,8 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
         for (int e = ptr[tok]; e < ptr[tok + 1]; ++e) F.nbr.push_back((uint16_t)(slot_of[idx[e]] * 64));
         cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
       }
+      const uint16_t first = cnt ? F.nbr[start] : 0;
+      while (F.nbr.size() < start + (size_t)padT[sl / 16]) F.nbr.push_back(first);
       F.slot_tab[2 * sl + mask] = start | (cnt << 16);
     }
   while (F.nbr.size() % 8) F.nbr.push_back(0);
@@ -386,12 +412,17 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     M.layer[l].sq_qs = M.layer[l].sq[0] * M.kq;
   }
   M.path = path_req;
-  if (M.path == AECCT_PATH_AUTO) M.path = aecct::fused_supported(M) ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
-  if (M.path == AECCT_PATH_FUSED && !aecct::fused_supported(M)) return AECCT_ERR_UNSUPPORTED;
 
   // fused-path tables (built whenever the shape allows the fused kernel)
   FusedImage FI;
-  if (aecct::fused_supported(M)) build_fused(M, H, w, m1_ptr, m1_idx, m2_ptr, m2_idx, FI);
+  bool fused_ok = path_req != AECCT_PATH_LAYERED && aecct::fused_supported(M);
+  if (fused_ok) {
+    build_fused(M, H, w, m1_ptr, m1_idx, m2_ptr, m2_idx, FI);
+    fused_ok = aecct::fused_fits(M, (int)(FI.nbr.size() / 2));
+    if (!fused_ok) FI = FusedImage();
+  }
+  if (M.path == AECCT_PATH_AUTO) M.path = fused_ok ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
+  if (M.path == AECCT_PATH_FUSED && !fused_ok) return AECCT_ERR_UNSUPPORTED;
 
   // host image of the device block
   Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
@@ -402,6 +433,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     P.f_vec = take(4 * FI.vec.size());
     P.f_nbr = take(2 * FI.nbr.size());
     P.f_slot = take(4 * FI.slot_tab.size());
+    P.f_tile = take(4 * FI.tile_tab.size());
     P.f_chk = take(8 * FI.chk.size());
     P.f_tok = take(4 * FI.slot_token.size());
     P.f_e = take(4 * FI.eperm.size());
@@ -431,6 +463,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   put(P.f_vec, FI.vec.data(), 4 * FI.vec.size());
   put(P.f_nbr, FI.nbr.data(), 2 * FI.nbr.size());
   put(P.f_slot, FI.slot_tab.data(), 4 * FI.slot_tab.size());
+  put(P.f_tile, FI.tile_tab.data(), 4 * FI.tile_tab.size());
   put(P.f_chk, FI.chk.data(), 8 * FI.chk.size());
   put(P.f_tok, FI.slot_token.data(), 4 * FI.slot_token.size());
   put(P.f_e, FI.eperm.data(), 4 * FI.eperm.size());
@@ -518,6 +551,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     T.nbr = (const uint32_t *)(b + P.f_nbr);
     T.nbr_words = (int)(FI.nbr.size() / 2);
     T.slot_tab = (const uint32_t *)(b + P.f_slot);
+    T.tile_tab = (const uint32_t *)(b + P.f_tile);
+    T.maxt = FI.maxt;
     T.chk = (const uint64_t *)(b + P.f_chk);
     T.slot_token = (const int32_t *)(b + P.f_tok);
     T.eperm = (const float *)(b + P.f_e);

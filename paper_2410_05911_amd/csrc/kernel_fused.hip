@@ -33,6 +33,7 @@ struct FusedArgs {
   const uint32_t *nbr;         // neighbour entries, uint16 byte offsets, two per word
   int nbr_words;
   const uint32_t *slot_tab;    // [16 NT][2]: start | count << 16, first / second ring
+  const uint32_t *tile_tab;    // [NT][2]: padded length T | shortest real length << 16, per head group
   const uint64_t *chk;         // [m] variable bitmask of each check
   const int32_t *slot_token;   // [16 NT] token of each slot or -1
   const float *eperm, *pperm;  // [16 NT][4][8] embedding (and positional) rows in lane order
@@ -64,13 +65,20 @@ __device__ __forceinline__ float token_sum(const float (&x)[8]) {
   return s;
 }
 
+// Maximum of non-negative values across lane xor 32 and lane xor 16: for non-negative
+// floats the bit patterns order like unsigned integers.
+__device__ __forceinline__ float cross_max_nonneg(float a) {
+  uint32_t u = __builtin_bit_cast(uint32_t, a);
+  u = max(u, (uint32_t)__shfl_xor((int)u, 32));
+  u = max(u, (uint32_t)__shfl_xor((int)u, 16));
+  return __builtin_bit_cast(float, u);
+}
+
 __device__ __forceinline__ float token_max_abs(const float (&x)[8]) {
   float a = fabsf(x[0]);
 #pragma unroll
   for (int v = 1; v < 8; ++v) a = fmaxf(a, fabsf(x[v]));
-  a = fmaxf(a, xor32(a));
-  a = fmaxf(a, xor16(a));
-  return a;
+  return cross_max_nonneg(a);
 }
 
 // Byte 0 of four Eq. 2 code patterns into one dword (byte i from b[i]).
@@ -113,29 +121,40 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// One (token slot, head) softmax row: q is the scaled query, entries are byte offsets of
-// the neighbours' key rows in the head group buffer (ascending token order), kbase points
-// at this lane's head in that buffer, values sit vofs bytes after the keys.
-__device__ __forceinline__ void attend(const float (&q)[4], const uint16_t *ent, int cnt, const unsigned char *kbase,
-                                       int vofs, float (&o)[4]) {
+// One (token slot, head) softmax row.  The lists of a tile are padded to a common length T
+// (uniform over the wave): entries past a lane's own count cnt repeat its first entry, so
+// the maximum is unchanged, and their weights are zeroed in the second pass (only needed
+// from the tile's shortest list length cmin on).  Scores stay in registers between the
+// passes.  q is the scaled query, ent the lane's entries (byte offsets of the neighbours'
+// key rows in ascending token order), kbase this lane's head in the key buffer, values
+// vofs bytes after the keys.
+template <int MAXT>
+__device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t *ent, int cnt, int T, int cmin,
+                                            const unsigned char *kbase, int vofs, float (&o)[4]) {
+  float s[MAXT];
   float mu = -INFINITY;
-  for (int e = 0; e < cnt; ++e) {
-    const float4 k = *(const float4 *)(kbase + ent[e]);
-    const float kk[4] = {k.x, k.y, k.z, k.w};
-    mu = fmaxf(mu, head_dot<4>(q, kk));
+#pragma unroll
+  for (int j = 0; j < MAXT; ++j) {
+    if (j < T) {
+      const float4 k = *(const float4 *)(kbase + ent[j]);
+      const float kk[4] = {k.x, k.y, k.z, k.w};
+      s[j] = head_dot<4>(q, kk);
+      mu = j == 0 ? s[j] : fmaxf(mu, s[j]);
+    }
   }
   float S = 0.0f, acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int e = 0; e < cnt; ++e) {
-    const unsigned char *kp = kbase + ent[e];
-    const float4 k = *(const float4 *)kp;
-    const float kk[4] = {k.x, k.y, k.z, k.w};
-    const float ex = softmax_exp2(head_dot<4>(q, kk) - mu);
-    S = S + ex;
-    const float4 vv = *(const float4 *)(kp + vofs);
-    acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
-    acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
-    acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
-    acc[3] = __builtin_fmaf(ex, vv.w, acc[3]);
+#pragma unroll
+  for (int j = 0; j < MAXT; ++j) {
+    if (j < T) {
+      float ex = softmax_exp2(s[j] - mu);
+      if (j >= cmin) ex = j < cnt ? ex : 0.0f;
+      S = S + ex;
+      const float4 vv = *(const float4 *)(kbase + vofs + ent[j]);
+      acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
+      acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
+      acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
+      acc[3] = __builtin_fmaf(ex, vv.w, acc[3]);
+    }
   }
   const float rS = cnt > 0 ? 1.0f / S : 0.0f;
 #pragma unroll
@@ -144,8 +163,8 @@ __device__ __forceinline__ void attend(const float (&q)[4], const uint16_t *ent,
 
 }  // namespace
 
-template <int NT>
-__global__ __launch_bounds__(fz::kMaxWaves * 64, 1) void k_fused_decode(FusedArgs p) {
+template <int NT, int MAXT, int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
   // ---- one-time staging: packed ternary fragments -> int8, per-layer vectors, tables ----
@@ -228,19 +247,17 @@ __global__ __launch_bounds__(fz::kMaxWaves * 64, 1) void k_fused_decode(FusedArg
       float ob[NT][8];
 #pragma unroll
       for (int grp = 0; grp < 2; ++grp) {
-        float q[NT][4];
+        // keys and values of every tile to LDS; queries are made per tile just before use
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           const long bop = as_long(xb[t][0], xb[t][1]);
-          const v4i aq = mfma_i8_16x16x32((long)F[(0 + grp) * 64], bop, v4i{0, 0, 0, 0});
           const v4i ak = mfma_i8_16x16x32((long)F[(2 + grp) * 64], bop, v4i{0, 0, 0, 0});
           const v4i av = mfma_i8_16x16x32((long)F[(4 + grp) * 64], bop, v4i{0, 0, 0, 0});
-          const float scq = al[t] * sq_q, sck = al[t] * sq_k, scv = al[t] * sq_v;
+          const float sck = al[t] * sq_k, scv = al[t] * sq_v;
           const float *bq = V + fz::V_BQKV + 16 * grp + 4 * g;
           float kk[4], vv[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            q[t][i] = __builtin_fmaf((float)aq[i], scq, bq[i]);
             kk[i] = __builtin_fmaf((float)ak[i], sck, bq[32 + i]);
             vv[i] = __builtin_fmaf((float)av[i], scv, bq[64 + i]);
           }
@@ -251,9 +268,18 @@ __global__ __launch_bounds__(fz::kMaxWaves * 64, 1) void k_fused_decode(FusedArg
         const int mask = grp == 0 ? mask1 : mask2;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
+          const v4i aq =
+              mfma_i8_16x16x32((long)F[(0 + grp) * 64], as_long(xb[t][0], xb[t][1]), v4i{0, 0, 0, 0});
+          const float scq = al[t] * sq_q;
+          const float *bq = V + fz::V_BQKV + 16 * grp + 4 * g;
+          float q[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) q[i] = __builtin_fmaf((float)aq[i], scq, bq[i]);
           const uint32_t st = sslot[(16 * t + c) * 2 + mask];
+          const uint32_t tt = __builtin_amdgcn_readfirstlane(p.tile_tab[2 * t + grp]);
           float o[4];
-          attend(q[t], snbr + (st & 0xffff), (int)(st >> 16), kbase, vofs, o);
+          attend_tile<MAXT>(q, snbr + (st & 0xffff), (int)(st >> 16), (int)(tt & 0xffff), (int)(tt >> 16), kbase,
+                            vofs, o);
 #pragma unroll
           for (int i = 0; i < 4; ++i) ob[t][4 * grp + i] = o[i];
         }
@@ -295,8 +321,7 @@ __global__ __launch_bounds__(fz::kMaxWaves * 64, 1) void k_fused_decode(FusedArg
             G[o][i] = f > 0.0f ? f : 0.0f;
             amax = fmaxf(amax, G[o][i]);
           }
-        amax = fmaxf(amax, xor32(amax));
-        amax = fmaxf(amax, xor16(amax));
+        amax = cross_max_nonneg(amax);
         const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
         uint32_t gb[8];
 #pragma unroll
@@ -383,23 +408,34 @@ FusedLds fused_lds(const Model &M, int nbr_words) {
 }
 
 bool fused_supported(const Model &M) {
-  if (M.d != 32 || M.heads != 8 || M.dff != 128 || M.L > 64 || M.n > 64) return false;
-  const int nbr_words = (int)(((M.nnz1 + M.nnz2) + 7) / 8 * 4);
-  const FusedLds L = fused_lds(M, nbr_words);
-  return (size_t)L.off_kv + 4 * (size_t)L.kv_bytes <= (size_t)fz::kLdsMax;   // room for four waves
+  return M.d == 32 && M.heads == 8 && M.dff == 128 && M.L <= 64 && M.n <= 64;
 }
 
-template <int NT>
-static hipError_t launch_nt(const FusedArgs &a, int waves, size_t lds, int grid, hipStream_t s) {
+bool fused_fits(const Model &M, int nbr_words) {
+  const FusedLds L = fused_lds(M, nbr_words);
+  return (size_t)L.off_kv + fz::kWaves * (size_t)L.kv_bytes <= (size_t)fz::kLdsMax;
+}
+
+template <int NT, int MAXT, int WAVES>
+static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       fz::kLdsMax);
+    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT, MAXT, WAVES>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, fz::kLdsMax);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(k_fused_decode<NT>, dim3(grid), dim3(waves * 64), lds, s, a);
+  hipLaunchKernelGGL((k_fused_decode<NT, MAXT, WAVES>), dim3(grid), dim3(WAVES * 64), lds, s, a);
   return hipGetLastError();
+}
+
+template <int NT>
+static hipError_t launch_maxt(const FusedArgs &a, int maxt, size_t lds, int grid, hipStream_t s) {
+  if (maxt <= 8) return launch_nt<NT, 8, fz::kWaves>(a, lds, grid, s);
+  if (maxt <= 16) return launch_nt<NT, 16, fz::kWaves>(a, lds, grid, s);
+  if (maxt <= 28) return launch_nt<NT, 28, fz::kWaves>(a, lds, grid, s);
+  if (maxt <= 32) return launch_nt<NT, 32, fz::kWaves>(a, lds, grid, s);
+  return launch_nt<NT, 64, fz::kWaves>(a, lds, grid, s);
 }
 
 hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
@@ -413,6 +449,7 @@ hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *
   a.nbr = T.nbr;
   a.nbr_words = T.nbr_words;
   a.slot_tab = T.slot_tab;
+  a.tile_tab = T.tile_tab;
   a.chk = T.chk;
   a.slot_token = T.slot_token;
   a.eperm = T.eperm;
@@ -440,19 +477,18 @@ hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *
   a.off_kv = Ld.off_kv;
   a.kv_bytes = Ld.kv_bytes;
   const size_t off = (size_t)Ld.off_kv;
-  int waves = (int)((fz::kLdsMax - off) / a.kv_bytes);
-  if (waves > fz::kMaxWaves) waves = fz::kMaxWaves;
-  if (waves < 1) return hipErrorInvalidConfiguration;
+  const int waves = fz::kWaves;
+  if (off + (size_t)waves * a.kv_bytes > (size_t)fz::kLdsMax) return hipErrorInvalidConfiguration;
   const size_t lds = off + (size_t)waves * a.kv_bytes;
   int64_t blocks = (words + waves - 1) / waves;
   const int64_t per_cu = (int64_t)(fz::kLdsMax / lds) > 0 ? (int64_t)(fz::kLdsMax / lds) : 1;
   const int64_t cap = 256 * per_cu;
   const int grid = (int)(blocks < cap ? blocks : cap);
   switch (NT) {
-    case 1: return launch_nt<1>(a, waves, lds, grid, s);
-    case 2: return launch_nt<2>(a, waves, lds, grid, s);
-    case 3: return launch_nt<3>(a, waves, lds, grid, s);
-    case 4: return launch_nt<4>(a, waves, lds, grid, s);
+    case 1: return launch_maxt<1>(a, T.maxt, lds, grid, s);
+    case 2: return launch_maxt<2>(a, T.maxt, lds, grid, s);
+    case 3: return launch_maxt<3>(a, T.maxt, lds, grid, s);
+    case 4: return launch_maxt<4>(a, T.maxt, lds, grid, s);
   }
   return hipErrorInvalidValue;
 }
