@@ -202,7 +202,7 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
       padT[t] = std::max(padT[t], T);
       F.maxt = std::max(F.maxt, T);
     }
-  // neighbour lists: byte offsets of the neighbours' 64-byte key rows, ascending token order,
+  // neighbour lists: byte offsets of the neighbours' 16-byte key rows, ascending token order,
   // padded to the tile's longest list with copies of the first entry
   F.slot_tab.assign(2 * S, 0);
   for (int sl = 0; sl < S; ++sl)
@@ -213,7 +213,7 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
       if (tok >= 0) {
         const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
         const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
-        for (int e = ptr[tok]; e < ptr[tok + 1]; ++e) F.nbr.push_back((uint16_t)(slot_of[idx[e]] * 64));
+        for (int e = ptr[tok]; e < ptr[tok + 1]; ++e) F.nbr.push_back((uint16_t)(slot_of[idx[e]] * 16));
         cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
       }
       const uint16_t first = cnt ? F.nbr[start] : 0;

@@ -51,27 +51,47 @@ struct FusedArgs {
 
 namespace {
 
-__device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32); }
-__device__ __forceinline__ float xor16(float v) { return __shfl_xor(v, 16); }
+// Butterfly steps across lane xor 32 and lane xor 16 with the gfx950 lane-swap
+// instructions: swapping v with a copy of itself leaves, in the two results, v of the lane
+// and of its partner (in an order that depends on the half); sum and maximum commute, so
+// every lane gets the same bits.  The copy goes through an opaque move so that the compiler
+// cannot treat the two swap results as the same value.
+__device__ __forceinline__ uint32_t opaque_copy(uint32_t v) {
+  uint32_t w;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(w) : "v"(v));
+  return w;
+}
+__device__ __forceinline__ float pair_sum32(float v) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+__device__ __forceinline__ float pair_sum16(float v) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+__device__ __forceinline__ uint32_t pair_max32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, opaque_copy(v), false, false);
+  return max((uint32_t)r[0], (uint32_t)r[1]);
+}
+__device__ __forceinline__ uint32_t pair_max16(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, opaque_copy(v), false, false);
+  return max((uint32_t)r[0], (uint32_t)r[1]);
+}
 
 // Pairwise sum over a token's 32 features held as x[v] = feature 4 v + g.
 __device__ __forceinline__ float token_sum(const float (&x)[8]) {
   float u[8];
 #pragma unroll
   for (int v = 0; v < 8; ++v) u[v] = x[v];
-  float s = lane_tree<8>(u);
-  s = s + xor32(s);
-  s = s + xor16(s);
-  return s;
+  return pair_sum16(pair_sum32(lane_tree<8>(u)));
 }
 
 // Maximum of non-negative values across lane xor 32 and lane xor 16: for non-negative
 // floats the bit patterns order like unsigned integers.
 __device__ __forceinline__ float cross_max_nonneg(float a) {
-  uint32_t u = __builtin_bit_cast(uint32_t, a);
-  u = max(u, (uint32_t)__shfl_xor((int)u, 32));
-  u = max(u, (uint32_t)__shfl_xor((int)u, 16));
-  return __builtin_bit_cast(float, u);
+  return __builtin_bit_cast(float, pair_max16(pair_max32(__builtin_bit_cast(uint32_t, a))));
 }
 
 __device__ __forceinline__ float token_max_abs(const float (&x)[8]) {
@@ -193,9 +213,11 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   const uint32_t *sslot = (const uint32_t *)(smem + p.off_slot);
   const uint64_t *schk = (const uint64_t *)(smem + p.off_chk);
   const int32_t *stok = (const int32_t *)(smem + p.off_tok);
+  // Keys (then values) of the current head group, head-major: head h of slot s at
+  // (h * 16 NT + s) * 16 bytes, so the 16 lanes of one head gather from all banks.
   unsigned char *kv = smem + p.off_kv + wave * p.kv_bytes;
-  const int vofs = 16 * NT * 64;           // values follow the keys of all slots
-  unsigned char *kbase = kv + 16 * g;      // this lane's head inside a slot's 64-byte key row
+  const int vofs = 16 * NT * 64;           // values follow the keys of all four heads
+  unsigned char *kbase = kv + g * (16 * NT * 16);
   const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
 
   int tok[NT];
@@ -261,8 +283,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
             kk[i] = __builtin_fmaf((float)ak[i], sck, bq[32 + i]);
             vv[i] = __builtin_fmaf((float)av[i], scv, bq[64 + i]);
           }
-          *(float4 *)(kbase + (16 * t + c) * 64) = make_float4(kk[0], kk[1], kk[2], kk[3]);
-          *(float4 *)(kbase + vofs + (16 * t + c) * 64) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+          *(float4 *)(kbase + (16 * t + c) * 16) = make_float4(kk[0], kk[1], kk[2], kk[3]);
+          *(float4 *)(kbase + vofs + (16 * t + c) * 16) = make_float4(vv[0], vv[1], vv[2], vv[3]);
         }
         wave_sync_lds();
         const int mask = grp == 0 ? mask1 : mask2;
