@@ -12,7 +12,7 @@
  *   SEQ         left-to-right from 0 in ascending index;
  *   DOT         q.k as a multiply followed by fused multiply-adds in ascending
  *               index order;
- *   EXP2        oracle_exp2 below (2^x, degree-7 Taylor series);
+ *   EXP2        oracle_exp2 below (2^x, economised degree-6 series);
  *   RSQRT       oracle_rsqrt below (three Newton steps from a bit-level seed).
  */
 #include "aecct_oracle.h"
@@ -50,28 +50,39 @@ float oracle_tree_sum(const float *v, int32_t w) {
  * Section 4.2, HPSA) taken in base 2: softmax(s) = 2^(s log2 e - max) / sum,
  * with log2 e folded into the scores.  x is clamped to >= -125 (so the result
  * stays a normal number; such terms are below 2^-124 of the largest, which is
- * exactly 1), split exactly into k = rint(x) and r = x - k in [-1/2, 1/2],
- * 2^r = sum_j (r ln 2)^j / j! to degree 7 by Horner with fp32-rounded
- * coefficients, then scaled exactly by 2^k.
- * Pin: within 2 ulp of 2^x over [-125, 0]; exact at integers.
+ * exactly 1), split exactly into k = rint(x) and r = x - k in [-1/2, 1/2];
+ * 2^r = e^(r ln 2) is the degree-7 Taylor series economised to degree 6 by
+ * Chebyshev's method (Lanczos): subtracting c7 T7(2r) / 8192, with
+ * T7(u) = 64u^7 - 112u^5 + 56u^3 - 7u, cancels the r^7 term and moves
+ * c7 * 3584/8192 into c5, -c7 * 448/8192 into c3 and c7 * 14/8192 into c1
+ * (added error below 2e-9); Horner with fp32-rounded coefficients, then the
+ * exact scaling by 2^k.
+ * Pin: within 1 ulp of 2^x over [-125, 0]; exact at integers.
  */
 #define ORC_LN2 0.69314718055994530942
-static const float exp2_coef[8] = {
+#define ORC_T(j) ORC_T##j
+#define ORC_T1 (ORC_LN2)
+#define ORC_T2 (ORC_LN2 * ORC_LN2 / 2.0)
+#define ORC_T3 (ORC_LN2 * ORC_LN2 * ORC_LN2 / 6.0)
+#define ORC_T4 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 24.0)
+#define ORC_T5 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 120.0)
+#define ORC_T6 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 720.0)
+#define ORC_T7 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 5040.0)
+static const float exp2_coef[7] = {
     1.0f,
-    (float)(ORC_LN2),
-    (float)(ORC_LN2 * ORC_LN2 / 2.0),
-    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 / 6.0),
-    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 24.0),
-    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 120.0),
-    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 720.0),
-    (float)(ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 5040.0)};
+    (float)(ORC_T1 + ORC_T7 * 14.0 / 8192.0),
+    (float)(ORC_T2),
+    (float)(ORC_T3 - ORC_T7 * 448.0 / 8192.0),
+    (float)(ORC_T4),
+    (float)(ORC_T5 + ORC_T7 * 3584.0 / 8192.0),
+    (float)(ORC_T6)};
 
 float oracle_exp2(float x) {
   if (x < -125.0f) x = -125.0f;
   const float k = rintf(x);
   const float r = x - k;
-  float p = exp2_coef[7];
-  for (int j = 6; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
+  float p = exp2_coef[6];
+  for (int j = 5; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
   return ldexpf(p, (int)k);
 }
 
