@@ -76,18 +76,19 @@ __device__ __forceinline__ uint32_t quant_bits(float x, float inv) {
 __device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_t)quant_bits(x, inv); }
 
 // 2^x, x <= 0, for the base-2 attention softmax: clamp to -125 (the result stays a normal
-// number), exact split x = k + r with k = rint(x), r in [-1/2, 1/2], the degree-7 Taylor
-// series of 2^r = e^(r ln 2) by Horner with coefficients fp32((ln 2)^j / j!), and an exact
+// number), exact split x = k + r with k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its
+// degree-7 Taylor series economised to degree 6 with the Chebyshev polynomial T7(2r) / 8192
+// (coefficients fp32 of: 1, ln2 + c7*14/8192, (ln2)^2/2, (ln2)^3/6 - c7*448/8192, (ln2)^4/24,
+// (ln2)^5/120 + c7*3584/8192, (ln2)^6/720 with c7 = (ln2)^7/5040), Horner, then an exact
 // scaling by 2^k.
 __device__ __forceinline__ float softmax_exp2(float x) {
   x = fmaxf(x, -125.0f);
   const float k = __builtin_rintf(x);
   const float r = x - k;
-  float p = 0x1.ffcbfcp-17f;
-  p = __builtin_fmaf(p, r, 0x1.430912p-13f);
-  p = __builtin_fmaf(p, r, 0x1.5d87fep-10f);
+  float p = 0x1.430912p-13f;
+  p = __builtin_fmaf(p, r, 0x1.5f47d0p-10f);
   p = __builtin_fmaf(p, r, 0x1.3b2ab6p-7f);
-  p = __builtin_fmaf(p, r, 0x1.c6b08ep-5f);
+  p = __builtin_fmaf(p, r, 0x1.c6aecep-5f);
   p = __builtin_fmaf(p, r, 0x1.ebfbe0p-3f);
   p = __builtin_fmaf(p, r, 0x1.62e430p-1f);
   p = __builtin_fmaf(p, r, 1.0f);

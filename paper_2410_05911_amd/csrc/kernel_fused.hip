@@ -51,7 +51,8 @@ struct FusedArgs {
 
 namespace {
 
-// Butterfly steps across lane xor 32 and lane xor 16 with the gfx950 lane-swap
+// Butterfly steps across lane xor 32 and lane xor 16: ds_bpermute through the LDS crossbar
+// (default, measured faster here), or, with AECCT_XLANE_SWAP, the gfx950 lane-swap
 // instructions: swapping v with a copy of itself leaves, in the two results, v of the lane
 // and of its partner (in an order that depends on the half); sum and maximum commute, so
 // every lane gets the same bits.  The copy goes through an opaque move so that the compiler
@@ -61,6 +62,12 @@ __device__ __forceinline__ uint32_t opaque_copy(uint32_t v) {
   asm volatile("v_mov_b32 %0, %1" : "=v"(w) : "v"(v));
   return w;
 }
+#if !defined(AECCT_XLANE_SWAP)
+__device__ __forceinline__ float pair_sum32(float v) { return v + __shfl_xor(v, 32); }
+__device__ __forceinline__ float pair_sum16(float v) { return v + __shfl_xor(v, 16); }
+__device__ __forceinline__ uint32_t pair_max32(uint32_t v) { return max(v, (uint32_t)__shfl_xor((int)v, 32)); }
+__device__ __forceinline__ uint32_t pair_max16(uint32_t v) { return max(v, (uint32_t)__shfl_xor((int)v, 16)); }
+#else
 __device__ __forceinline__ float pair_sum32(float v) {
   const uint32_t u = __builtin_bit_cast(uint32_t, v);
   const auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
@@ -79,6 +86,7 @@ __device__ __forceinline__ uint32_t pair_max16(uint32_t v) {
   const auto r = __builtin_amdgcn_permlane16_swap(v, opaque_copy(v), false, false);
   return max((uint32_t)r[0], (uint32_t)r[1]);
 }
+#endif
 
 // Pairwise sum over a token's 32 features held as x[v] = feature 4 v + g.
 __device__ __forceinline__ float token_sum(const float (&x)[8]) {
