@@ -46,18 +46,18 @@ float oracle_tree_sum(const float *v, int32_t w) {
 }
 
 /*
- * 2^x for x <= 0, the exponential of the attention softmax (Section 3, CASA;
- * Section 4.2, HPSA) taken in base 2: softmax(s) = 2^(s log2 e - max) / sum,
- * with log2 e folded into the scores.  x is clamped to >= -125 (so the result
- * stays a normal number; such terms are below 2^-124 of the largest, which is
- * exactly 1), split exactly into k = rint(x) and r = x - k in [-1/2, 1/2];
+ * 2^x, the exponential of the attention softmax (Section 3, CASA; Section 4.2,
+ * HPSA) taken in base 2: softmax(s) = 2^(s log2 e) / sum, with log2 e folded
+ * into the scores.  x is clamped to [-125, 128] (the result stays a normal
+ * number or becomes +inf from 2^128 on, and k below fits an int), split
+ * exactly into k = rint(x) and r = x - k in [-1/2, 1/2];
  * 2^r = e^(r ln 2) is the degree-7 Taylor series economised to degree 6 by
  * Chebyshev's method (Lanczos): subtracting c7 T7(2r) / 8192, with
  * T7(u) = 64u^7 - 112u^5 + 56u^3 - 7u, cancels the r^7 term and moves
  * c7 * 3584/8192 into c5, -c7 * 448/8192 into c3 and c7 * 14/8192 into c1
  * (added error below 2e-9); Horner with fp32-rounded coefficients, then the
  * exact scaling by 2^k.
- * Pin: within 1 ulp of 2^x over [-125, 0]; exact at integers.
+ * Pin: within 1 ulp of 2^x over [-125, 64]; exact at integers; +inf from 128.
  */
 #define ORC_LN2 0.69314718055994530942
 #define ORC_T(j) ORC_T##j
@@ -79,6 +79,7 @@ static const float exp2_coef[7] = {
 
 float oracle_exp2(float x) {
   if (x < -125.0f) x = -125.0f;
+  if (x > 128.0f) x = 128.0f;
   const float k = rintf(x);
   const float r = x - k;
   float p = exp2_coef[6];
@@ -247,11 +248,15 @@ static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_
  * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.  The
  * query rows arrive already multiplied by log2(e)/sqrt(d_h) (folded into the
  * query map, see oracle_query_scale), so the softmax is taken in base 2:
- * s_j = DOT(q', k_j); mu = max s_j; e_j = EXP2(s_j - mu); S = SEQ sum e_j;
- * o = (SEQ fma(e_j, v_j, acc)) * (1 / S).  Returns 0, or -1 for a row with no
+ * s_j = DOT(q', k_j); the weights are the plain definition e_j = EXP2(s_j)
+ * with S = SEQ sum e_j and acc = SEQ fma(e_j, v_j, acc), kept when
+ * 2^-64 <= S <= 2^64 (no overflow; every weight clamped at 2^-125 then lies
+ * below 2^-61 S); otherwise the row is redone with the usual stabilising
+ * shift, e_j = EXP2(s_j - mu), mu = max s_j.  o = acc * (1 / S).  Both forms
+ * are the same softmax up to rounding.  Returns 0, or -1 for a row with no
  * allowed key.
- * Pin: within 1e-6 relative of the fp64 dense (-inf)-masked softmax; a row
- * with one allowed key returns that value row exactly.
+ * Pin: within 1e-6 relative of the fp64 dense (-inf)-masked softmax, on rows
+ * of either form; a row with one allowed key returns that value row to 3 ulp.
  */
 int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
                           const float *qkv, float *o) {
@@ -269,14 +274,20 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
         }
       if (cnt == 0) return -1;
       float S = 0.0f, acc[ORC_MAX_TREE];
-      for (int32_t t = 0; t < dh; ++t) acc[t] = 0.0f;
-      for (int32_t j = 0; j < L; ++j)
-        if (row[j]) {
-          float e = oracle_exp2(score_f32(qkv, d, i, j, h, dh) - mu);
-          S = S + e;
-          const float *vj = qkv + (int64_t)j * 3 * d + 2 * d + h * dh;
-          for (int32_t t = 0; t < dh; ++t) acc[t] = fmaf(e, vj[t], acc[t]);
-        }
+      for (int pass = 0; pass < 2; ++pass) {
+        const float shift = pass == 0 ? 0.0f : mu;
+        S = 0.0f;
+        for (int32_t t = 0; t < dh; ++t) acc[t] = 0.0f;
+        for (int32_t j = 0; j < L; ++j)
+          if (row[j]) {
+            float s = score_f32(qkv, d, i, j, h, dh);
+            float e = oracle_exp2(pass == 0 ? s : s - shift);
+            S = S + e;
+            const float *vj = qkv + (int64_t)j * 3 * d + 2 * d + h * dh;
+            for (int32_t t = 0; t < dh; ++t) acc[t] = fmaf(e, vj[t], acc[t]);
+          }
+        if (S >= 0x1p-64f && S <= 0x1p64f) break;
+      }
       const float rS = 1.0f / S;
       for (int32_t t = 0; t < dh; ++t) o[(int64_t)i * d + h * dh + t] = acc[t] * rS;
     }

@@ -41,8 +41,14 @@ def test_exp2_close_to_pow_and_exact_at_integers(oracle_mod):
     for k in range(0, 126):
         assert oracle_mod.exp2(-float(k)) == np.float32(2.0 ** -k)
     assert oracle_mod.exp2(-0.0) == np.float32(1.0)
+    for k in range(1, 128):
+        assert oracle_mod.exp2(float(k)) == np.float32(2.0 ** k)
     assert oracle_mod.exp2(-200.0) == np.float32(2.0 ** -125)      # clamped: stays a normal number
-    xs = np.concatenate([-np.linspace(0, 125, 50001, dtype=np.float32),
+    for x in (128.0, 1e30):                                          # clamped at 128: 2^128 is +inf
+        assert np.isinf(oracle_mod.exp2(x)) and oracle_mod.exp2(x) > 0
+    for x in (np.float32(127.4), np.float32(127.75)):               # still finite below 2^128
+        assert abs(float(oracle_mod.exp2(x)) - 2.0 ** float(x)) <= float(_ulp(2.0 ** float(x)))
+    xs = np.concatenate([np.linspace(-125, 64, 50001, dtype=np.float32),
                          -np.random.default_rng(1).random(20000).astype(np.float32) * 125])
     worst = 0.0
     for x in xs:
@@ -193,8 +199,34 @@ def test_attention_against_fp64_sdpa(oracle_mod, c):
     assert np.abs(o64 - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max())
 
 
-def test_attention_single_neighbour_rows_exact(oracle_mod):
-    """Hamming variables 4, 5, 6 have one check each: their first-ring rows copy that check's V."""
+@pytest.mark.parametrize("regime", ["overflow", "underflow", "mixed"])
+def test_attention_shifted_fallback_against_fp64_sdpa(oracle_mod, regime):
+    """Rows whose unshifted weight sum leaves [2^-64, 2^64] take the max-shifted form: scores of
+    a few hundred overflow 2^s, scores below -125 would all clamp to the same weight."""
+    cfg, H, G, w, y, x = build_workload(2, batch=1)
+    om = oracle_mod.OracleModel(H, w)
+    rng = np.random.default_rng(9)
+    qkv = rng.standard_normal((om.L, 3 * w.d))
+    d = w.d
+    if regime == "overflow":
+        qkv[:, :d] *= 40.0
+    elif regime == "underflow":
+        qkv[:, :d] = np.abs(qkv[:, :d]) * 20.0 + 5.0
+        qkv[:, d:2 * d] = -np.abs(qkv[:, d:2 * d]) - 4.0
+    else:                                   # half the tokens in each regime, the rest plain
+        qkv[::3, :d] *= 40.0
+        qkv[1::3, :d] = np.abs(qkv[1::3, :d]) * 20.0 + 5.0
+        qkv[1::3, d:2 * d] = -np.abs(qkv[1::3, d:2 * d]) - 4.0
+    qkv = qkv.astype(np.float32)
+    o = om.attention(qkv)
+    ref = _sdpa_reference(H, w, qkv)
+    assert np.isfinite(o).all()
+    assert np.abs(o - ref).max() <= 1e-5 * max(1.0, np.abs(ref).max())
+
+
+def test_attention_single_neighbour_rows_copy_value(oracle_mod):
+    """Hamming variables 4, 5, 6 have one check each: their first-ring rows are that check's V,
+    up to the three roundings of (e v) * (1 / e)."""
     cfg, H, G, w, y, x = build_workload(1, batch=1)
     om = oracle_mod.OracleModel(H, w)
     rng = np.random.default_rng(7)
@@ -205,7 +237,8 @@ def test_attention_single_neighbour_rows_exact(oracle_mod):
         (chk,) = np.nonzero(H[:, v])[0]
         for hh in range(w.first_ring_heads):
             sl = slice(hh * dh, (hh + 1) * dh)
-            assert (o[v, sl] == qkv[n + chk, 2 * d:][sl]).all()
+            ref = qkv[n + chk, 2 * d:][sl].astype(np.float64)
+            assert (np.abs(o[v, sl] - ref) <= 3 * 2.0 ** -24 * np.abs(ref)).all()
 
 
 # ------------------------------------------------------------------------ head
