@@ -53,8 +53,7 @@ struct FusedTables {
   const uint32_t *nbr;         // neighbour entries (uint16 byte offsets into a wave's key buffer)
   int nbr_words;               // 32-bit words of nbr (a multiple of 4)
   const uint32_t *slot_tab;    // [16 NT][2] start | count << 16 per slot, first / second ring
-  const uint32_t *tile_tab;    // [NT][2] padded list length T | shortest real length << 16 per head group
-  int maxt;                    // largest T
+  const uint32_t *tile_tab;    // [NT][2] longest list T of the tile, per head group
   const uint64_t *chk;         // [m] bitmask of the variables of each check
   const int32_t *slot_token;   // [16 NT] token in each slot, -1 for padding
   const float *eperm, *pperm;  // [16 NT][4][8] embedding / positional rows in lane order

@@ -75,14 +75,16 @@ __device__ __forceinline__ uint32_t quant_bits(float x, float inv) {
 }
 __device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_t)quant_bits(x, inv); }
 
-// 2^x, x <= 0, for the base-2 attention softmax: clamp to -125 (the result stays a normal
-// number), exact split x = k + r with k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its
+// 2^x for the base-2 attention softmax: clamp to [-125, 128] (the result stays a normal
+// number, or is +inf from 2^128 on; a NaN argument gives 2^-125, since the median of three
+// with a NaN operand is the minimum of the other two), exact split x = k + r with
+// k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its
 // degree-7 Taylor series economised to degree 6 with the Chebyshev polynomial T7(2r) / 8192
 // (coefficients fp32 of: 1, ln2 + c7*14/8192, (ln2)^2/2, (ln2)^3/6 - c7*448/8192, (ln2)^4/24,
 // (ln2)^5/120 + c7*3584/8192, (ln2)^6/720 with c7 = (ln2)^7/5040), Horner, then an exact
 // scaling by 2^k.
 __device__ __forceinline__ float softmax_exp2(float x) {
-  x = fmaxf(x, -125.0f);
+  x = __builtin_amdgcn_fmed3f(x, -125.0f, 128.0f);
   const float k = __builtin_rintf(x);
   const float r = x - k;
   float p = 0x1.430912p-13f;

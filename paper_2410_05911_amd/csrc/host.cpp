@@ -146,7 +146,6 @@ struct FusedImage {
   std::vector<uint16_t> nbr;
   std::vector<uint32_t> slot_tab;
   std::vector<uint32_t> tile_tab;
-  int maxt = 0;
   std::vector<uint64_t> chk;
   std::vector<int32_t> slot_token;
   std::vector<float> eperm, pperm, w1perm;
@@ -162,7 +161,8 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
     return mask == 0 ? m1_ptr[tok + 1] - m1_ptr[tok] : m2_ptr[tok + 1] - m2_ptr[tok];
   };
   auto mask_of = [&](int head) { return head < M.hf ? 0 : 1; };
-  // token slots: longest second-group lists first, then longest first-group lists
+  // token slots: tiles of 16 tokens taken in order of longest second-group lists first, then
+  // longest first-group lists (similar loop lengths within a tile)
   std::vector<int> order(L);
   for (int t = 0; t < L; ++t) order[t] = t;
   auto work = [&](int tok, int grp) {
@@ -176,50 +176,126 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
     return work(a, 0) > work(b, 0);
   });
   F.slot_token.assign(S, -1);
-  std::vector<int> slot_of(L);
-  for (int sl = 0; sl < L; ++sl) {
-    F.slot_token[sl] = order[sl];
-    slot_of[order[sl]] = sl;
-  }
+  for (int sl = 0; sl < L; ++sl) F.slot_token[sl] = order[sl];
   // Per tile and head group the neighbour loop runs T = the longest list among the tile's
-  // lanes; cmin = the shortest real list (padding slots excluded).
+  // lanes (padding slots have none).
   F.tile_tab.assign(2 * NT, 0);
   std::vector<int> padT(NT, 1);
   for (int t = 0; t < NT; ++t)
     for (int grp = 0; grp < 2; ++grp) {
-      int T = 1, cmin = 1 << 15;
+      int T = 1;
       for (int c = 0; c < 16; ++c) {
         const int tok = F.slot_token[16 * t + c];
         if (tok < 0) continue;
-        for (int g = 0; g < 4; ++g) {
-          const int l = len(mask_of(4 * grp + g), tok);
-          T = std::max(T, l);
-          cmin = std::min(cmin, l);
-        }
+        for (int g = 0; g < 4; ++g) T = std::max(T, len(mask_of(4 * grp + g), tok));
       }
-      if (cmin > T) cmin = T;
-      F.tile_tab[2 * t + grp] = (uint32_t)T | ((uint32_t)cmin << 16);
+      F.tile_tab[2 * t + grp] = (uint32_t)T;
       padT[t] = std::max(padT[t], T);
-      F.maxt = std::max(F.maxt, T);
     }
-  // neighbour lists: byte offsets of the neighbours' 16-byte key rows, ascending token order,
-  // padded to the tile's longest list with copies of the first entry
-  F.slot_tab.assign(2 * S, 0);
-  for (int sl = 0; sl < S; ++sl)
-    for (int mask = 0; mask < 2; ++mask) {
-      const int tok = F.slot_token[sl];
-      const uint32_t start = (uint32_t)F.nbr.size();
-      uint32_t cnt = 0;
-      if (tok >= 0) {
-        const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
-        const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
-        for (int e = ptr[tok]; e < ptr[tok + 1]; ++e) F.nbr.push_back((uint16_t)(slot_of[idx[e]] * 16));
-        cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
+  // every list of the tile is stored, also those of a mask no head uses: pad to the longest
+  for (int t = 0; t < NT; ++t)
+    for (int c = 0; c < 16; ++c) {
+      const int tok = F.slot_token[16 * t + c];
+      if (tok >= 0) padT[t] = std::max(padT[t], std::max(len(0, tok), len(1, tok)));
+    }
+  // Columns within a tile: a seeded local search over swaps of two columns of one tile that
+  // lowers the LDS bank collisions of the key/value gathers (the 16 lanes of one head read the
+  // rows of their e-th neighbours; rows of slots with equal column mod 16 (or mod 8 within a
+  // half of the lanes) share banks).  Tile membership, hence every loop length, is unchanged.
+  {
+    auto nb = [&](int mask, int tok, int e) {
+      const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
+      const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
+      const int cnt = ptr[tok + 1] - ptr[tok];
+      return e < cnt ? idx[ptr[tok] + e] : L;      // entries past the list read the pad row
+    };
+    std::vector<int> col(L + 1, 0);                // the pad row (index L) sits in column 0
+    auto refresh = [&]() {
+      for (int sl = 0; sl < S; ++sl)
+        if (F.slot_token[sl] >= 0) col[F.slot_token[sl]] = sl % 16;
+    };
+    auto cost = [&]() {
+      long total = 0;
+      for (int t = 0; t < NT; ++t)
+        for (int grp = 0; grp < 2; ++grp) {
+          const int T = (int)F.tile_tab[2 * t + grp];
+          int weight[2] = {0, 0};                  // lane groups reading each mask
+          for (int g = 0; g < 4; ++g) ++weight[mask_of(4 * grp + g)];
+          for (int mask = 0; mask < 2; ++mask) {
+            if (!weight[mask]) continue;
+            for (int e = 0; e < T; ++e) {
+              int seen_tok[16], cnt16[16] = {0}, cnt8a[8] = {0}, cnt8b[8] = {0}, ns = 0;
+              for (int c = 0; c < 16; ++c) {
+                const int tok = F.slot_token[16 * t + c];
+                if (tok < 0) continue;
+                const int j = nb(mask, tok, e);
+                bool dup = false;
+                for (int q = 0; q < ns; ++q) dup |= seen_tok[q] == j;
+                if (dup) continue;
+                seen_tok[ns++] = j;
+                ++cnt16[col[j]];
+                if (c < 8) ++cnt8a[col[j] % 8]; else ++cnt8b[col[j] % 8];
+              }
+              int m16 = 0, m8 = 0;
+              for (int b = 0; b < 16; ++b) m16 = std::max(m16, cnt16[b]);
+              for (int b = 0; b < 8; ++b) m8 = std::max(m8, std::max(cnt8a[b], cnt8b[b]));
+              total += (long)weight[mask] * (m16 + m8);
+            }
+          }
+        }
+      return total;
+    };
+    refresh();
+    long best = cost();
+    uint64_t rng = 0x9E3779B97F4A7C15ull;
+    auto next = [&]() { rng ^= rng << 13; rng ^= rng >> 7; rng ^= rng << 17; return rng; };
+    const int iters = 2000;
+    for (int it = 0; it < iters; ++it) {
+      const int t = (int)(next() % NT);
+      const int a = 16 * t + (int)(next() % 16), b = 16 * t + (int)(next() % 16);
+      if (a == b || (F.slot_token[a] < 0 && F.slot_token[b] < 0)) continue;
+      std::swap(F.slot_token[a], F.slot_token[b]);
+      refresh();
+      const long cst = cost();
+      if (cst <= best) {
+        best = cst;
+      } else {
+        std::swap(F.slot_token[a], F.slot_token[b]);
+        refresh();
       }
-      const uint16_t first = cnt ? F.nbr[start] : 0;
-      while (F.nbr.size() < start + (size_t)padT[sl / 16]) F.nbr.push_back(first);
-      F.slot_tab[2 * sl + mask] = start | (cnt << 16);
     }
+  }
+  std::vector<int> slot_of(L);
+  for (int sl = 0; sl < S; ++sl)
+    if (F.slot_token[sl] >= 0) slot_of[F.slot_token[sl]] = sl;
+  // neighbour lists: byte offsets of the neighbours' 16-byte key rows in ascending token order,
+  // padded to the tile's longest list with the offset of the pad row (row 16 NT of a head),
+  // and stored entry-major per (tile, mask): entry e of column c at tbase + e * 16 + c.
+  F.slot_tab.assign(2 * S, 0);
+  {
+    std::vector<size_t> tbase(2 * NT);
+    size_t total = 0;
+    for (int t = 0; t < NT; ++t)
+      for (int mask = 0; mask < 2; ++mask) {
+        tbase[2 * t + mask] = total;
+        total += (size_t)padT[t] * 16;
+      }
+    F.nbr.assign(total, 0);
+    for (int sl = 0; sl < S; ++sl)
+      for (int mask = 0; mask < 2; ++mask) {
+        const int t = sl / 16, c = sl % 16, tok = F.slot_token[sl];
+        const size_t base = tbase[2 * t + mask] + c;
+        uint32_t cnt = 0;
+        if (tok >= 0) {
+          const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
+          const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
+          cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
+          for (uint32_t e = 0; e < cnt; ++e) F.nbr[base + 16 * e] = (uint16_t)(slot_of[idx[ptr[tok] + e]] * 16);
+        }
+        for (int e = (int)cnt; e < padT[t]; ++e) F.nbr[base + 16 * (size_t)e] = (uint16_t)(S * 16);
+        F.slot_tab[2 * sl + mask] = (uint32_t)base | (cnt << 16);
+      }
+  }
   while (F.nbr.size() % 8) F.nbr.push_back(0);
   F.chk.assign(m, 0);
   for (int j = 0; j < m; ++j)
@@ -227,9 +303,10 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
       if (H[(size_t)j * n + i]) F.chk[j] |= (uint64_t)1 << i;
   F.eperm.assign((size_t)S * 32, 0.0f);
   if (w->pos) F.pperm.assign((size_t)S * 32, 0.0f);
-  for (int sl = 0; sl < L; ++sl)
+  for (int sl = 0; sl < S; ++sl)
     for (int g = 0; g < 4; ++g)
       for (int v = 0; v < 8; ++v) {
+        if (F.slot_token[sl] < 0) continue;   // padding slots keep zero rows
         const size_t src = (size_t)F.slot_token[sl] * D + 4 * v + g, dst = ((size_t)sl * 4 + g) * 8 + v;
         F.eperm[dst] = w->embed[src];
         if (w->pos) F.pperm[dst] = w->pos[src];
@@ -552,7 +629,6 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     T.nbr_words = (int)(FI.nbr.size() / 2);
     T.slot_tab = (const uint32_t *)(b + P.f_slot);
     T.tile_tab = (const uint32_t *)(b + P.f_tile);
-    T.maxt = FI.maxt;
     T.chk = (const uint64_t *)(b + P.f_chk);
     T.slot_token = (const int32_t *)(b + P.f_tok);
     T.eperm = (const float *)(b + P.f_e);

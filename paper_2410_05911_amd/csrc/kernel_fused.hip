@@ -33,7 +33,7 @@ struct FusedArgs {
   const uint32_t *nbr;         // neighbour entries, uint16 byte offsets, two per word
   int nbr_words;
   const uint32_t *slot_tab;    // [16 NT][2]: start | count << 16, first / second ring
-  const uint32_t *tile_tab;    // [NT][2]: padded length T | shortest real length << 16, per head group
+  const uint32_t *tile_tab;    // [NT][2]: longest list T of the tile, per head group
   const uint64_t *chk;         // [m] variable bitmask of each check
   const int32_t *slot_token;   // [16 NT] token of each slot or -1
   const float *eperm, *pperm;  // [16 NT][4][8] embedding (and positional) rows in lane order
@@ -149,40 +149,54 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// One (token slot, head) softmax row.  The lists of a tile are padded to a common length T
-// (uniform over the wave): entries past a lane's own count cnt repeat its first entry, so
-// the maximum is unchanged, and their weights are zeroed in the second pass (only needed
-// from the tile's shortest list length cmin on).  Scores stay in registers between the
-// passes.  q is the scaled query, ent the lane's entries (byte offsets of the neighbours'
-// key rows in ascending token order), kbase this lane's head in the key buffer, values
-// vofs bytes after the keys.
-template <int MAXT>
-__device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t *ent, int cnt, int T, int cmin,
+// Neighbour lists: q is the lane's scaled query, ent its entries (byte offsets of the
+// neighbours' key rows in ascending token order, 16 apart: a tile's lists are stored
+// entry-major so the 16 lanes of a head read consecutive words), kbase this lane's head in
+// the key buffer, values vofs bytes after the keys.
+// One neighbour of the base-2 softmax (Section 4.2): score DOT(q', k) of the key row at
+// byte offset e, its weight 2^s, and the running sums S and acc (ascending neighbours).
+__device__ __forceinline__ void attend_step(const float (&q)[4], const unsigned char *kbase, int vofs,
+                                            uint32_t e, float shift, float &S, float (&acc)[4]) {
+  const float4 k = *(const float4 *)(kbase + e);
+  const float kk[4] = {k.x, k.y, k.z, k.w};
+  const float ex = softmax_exp2(head_dot<4>(q, kk) - shift);
+  S = S + ex;
+  const float4 vv = *(const float4 *)(kbase + vofs + e);
+  acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
+  acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
+  acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
+  acc[3] = __builtin_fmaf(ex, vv.w, acc[3]);
+}
+
+// Attention of one lane's (token, head) row over its cnt neighbours, all lanes of the tile
+// running T (the tile's longest list) steps.  Entries past a lane's list point at the
+// head's pad row (key NaN, value 0): its weight is 2^-125 (the clamp maps the NaN score to
+// -125) and its value 0, so acc is unchanged and S too whenever S >= 2^-64, the only case in
+// which the unshifted sums are kept; a row whose sum leaves [2^-64, 2^64] is redone over its
+// real entries with the scores shifted by their maximum.
+__device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t *ent, int cnt, int T,
                                             const unsigned char *kbase, int vofs, float (&o)[4]) {
-  float s[MAXT];
-  float mu = -INFINITY;
-#pragma unroll
-  for (int j = 0; j < MAXT; ++j) {
-    if (j < T) {
-      const float4 k = *(const float4 *)(kbase + ent[j]);
-      const float kk[4] = {k.x, k.y, k.z, k.w};
-      s[j] = head_dot<4>(q, kk);
-      mu = j == 0 ? s[j] : fmaxf(mu, s[j]);
-    }
-  }
   float S = 0.0f, acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-  for (int j = 0; j < MAXT; ++j) {
-    if (j < T) {
-      float ex = softmax_exp2(s[j] - mu);
-      if (j >= cmin) ex = j < cnt ? ex : 0.0f;
-      S = S + ex;
-      const float4 vv = *(const float4 *)(kbase + vofs + ent[j]);
-      acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
-      acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
-      acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
-      acc[3] = __builtin_fmaf(ex, vv.w, acc[3]);
+  int j = 0;
+  for (; j + 4 <= T; j += 4) {
+    const uint16_t *e = ent + 16 * j;
+    attend_step(q, kbase, vofs, e[0], 0.0f, S, acc);
+    attend_step(q, kbase, vofs, e[16], 0.0f, S, acc);
+    attend_step(q, kbase, vofs, e[32], 0.0f, S, acc);
+    attend_step(q, kbase, vofs, e[48], 0.0f, S, acc);
+  }
+  for (; j < T; ++j) attend_step(q, kbase, vofs, ent[16 * j], 0.0f, S, acc);
+  if (cnt > 0 && !(S >= 0x1p-64f && S <= 0x1p64f)) {
+    float mu = -INFINITY;
+    for (int i = 0; i < cnt; ++i) {
+      const float4 k = *(const float4 *)(kbase + ent[16 * i]);
+      const float kk[4] = {k.x, k.y, k.z, k.w};
+      mu = fmaxf(mu, head_dot<4>(q, kk));
     }
+    S = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = 0.0f;
+    for (int i = 0; i < cnt; ++i) attend_step(q, kbase, vofs, ent[16 * i], mu, S, acc);
   }
   const float rS = cnt > 0 ? 1.0f / S : 0.0f;
 #pragma unroll
@@ -191,7 +205,7 @@ __device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t 
 
 }  // namespace
 
-template <int NT, int MAXT, int WAVES>
+template <int NT, int WAVES>
 __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
@@ -224,8 +238,14 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   // Keys (then values) of the current head group, head-major: head h of slot s at
   // (h * 16 NT + s) * 16 bytes, so the 16 lanes of one head gather from all banks.
   unsigned char *kv = smem + p.off_kv + wave * p.kv_bytes;
-  const int vofs = 16 * NT * 64;           // values follow the keys of all four heads
-  unsigned char *kbase = kv + g * (16 * NT * 16);
+  constexpr int HS = (16 * NT + 1) * 16;   // one head: 16 NT slot rows and the pad row
+  const int vofs = 4 * HS;                 // values follow the keys of all four heads
+  unsigned char *kbase = kv + g * HS;
+  if (lane < 4) {                          // pad rows of the four heads: key NaN, value 0
+    *(float4 *)(kv + lane * HS + 16 * NT * 16) = make_float4(__builtin_nanf(""), __builtin_nanf(""),
+                                                             __builtin_nanf(""), __builtin_nanf(""));
+    *(float4 *)(kv + vofs + lane * HS + 16 * NT * 16) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
   const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
 
   int tok[NT];
@@ -306,10 +326,9 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) q[i] = __builtin_fmaf((float)aq[i], scq, bq[i]);
           const uint32_t st = sslot[(16 * t + c) * 2 + mask];
-          const uint32_t tt = __builtin_amdgcn_readfirstlane(p.tile_tab[2 * t + grp]);
+          const int T = (int)__builtin_amdgcn_readfirstlane(p.tile_tab[2 * t + grp]);
           float o[4];
-          attend_tile<MAXT>(q, snbr + (st & 0xffff), (int)(st >> 16), (int)(tt & 0xffff), (int)(tt >> 16), kbase,
-                            vofs, o);
+          attend_tile(q, snbr + (st & 0xffff), (int)(st >> 16), T, kbase, vofs, o);
 #pragma unroll
           for (int i = 0; i < 4; ++i) ob[t][4 * grp + i] = o[i];
         }
@@ -433,7 +452,7 @@ FusedLds fused_lds(const Model &M, int nbr_words) {
   off += (size_t)16 * NT * 4;
   off = (off + 15) / 16 * 16;
   L.off_kv = (int)off;
-  L.kv_bytes = NT * 2048;
+  L.kv_bytes = 2 * 4 * (16 * NT + 1) * 16;   // keys and values, 4 heads, 16 NT slots + pad row
   return L;
 }
 
@@ -446,26 +465,17 @@ bool fused_fits(const Model &M, int nbr_words) {
   return (size_t)L.off_kv + fz::kWaves * (size_t)L.kv_bytes <= (size_t)fz::kLdsMax;
 }
 
-template <int NT, int MAXT, int WAVES>
+template <int NT, int WAVES>
 static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT, MAXT, WAVES>,
+    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT, WAVES>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, fz::kLdsMax);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((k_fused_decode<NT, MAXT, WAVES>), dim3(grid), dim3(WAVES * 64), lds, s, a);
+  hipLaunchKernelGGL((k_fused_decode<NT, WAVES>), dim3(grid), dim3(WAVES * 64), lds, s, a);
   return hipGetLastError();
-}
-
-template <int NT>
-static hipError_t launch_maxt(const FusedArgs &a, int maxt, size_t lds, int grid, hipStream_t s) {
-  if (maxt <= 8) return launch_nt<NT, 8, fz::kWaves>(a, lds, grid, s);
-  if (maxt <= 16) return launch_nt<NT, 16, fz::kWaves>(a, lds, grid, s);
-  if (maxt <= 28) return launch_nt<NT, 28, fz::kWaves>(a, lds, grid, s);
-  if (maxt <= 32) return launch_nt<NT, 32, fz::kWaves>(a, lds, grid, s);
-  return launch_nt<NT, 64, fz::kWaves>(a, lds, grid, s);
 }
 
 hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
@@ -515,10 +525,10 @@ hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *
   const int64_t cap = 256 * per_cu;
   const int grid = (int)(blocks < cap ? blocks : cap);
   switch (NT) {
-    case 1: return launch_maxt<1>(a, T.maxt, lds, grid, s);
-    case 2: return launch_maxt<2>(a, T.maxt, lds, grid, s);
-    case 3: return launch_maxt<3>(a, T.maxt, lds, grid, s);
-    case 4: return launch_maxt<4>(a, T.maxt, lds, grid, s);
+    case 1: return launch_nt<1, fz::kWaves>(a, lds, grid, s);
+    case 2: return launch_nt<2, fz::kWaves>(a, lds, grid, s);
+    case 3: return launch_nt<3, fz::kWaves>(a, lds, grid, s);
+    case 4: return launch_nt<4, fz::kWaves>(a, lds, grid, s);
   }
   return hipErrorInvalidValue;
 }

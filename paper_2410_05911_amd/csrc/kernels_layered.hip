@@ -214,10 +214,11 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
 
 // ------------------------------------------------------------------------------------------
 // Head-partitioned attention (Section 4.2): one lane per (row, head); heads 0..hf-1 read
-// the first-ring neighbour list of the row, the others the second-ring list.  Two passes
-// over the neighbours (ascending): the maximum of the scores (query rows arrive scaled by
-// log2(e)/sqrt(d_h)), then the base-2 exponentials, their sum and the weighted value sum.
-// The heads of a row sit in adjacent lanes, so the row's Eq. 2 scale is a shuffle reduction.
+// the first-ring neighbour list of the row, the others the second-ring list.  One pass over
+// the neighbours (ascending) sums the base-2 exponentials of the scores (query rows arrive
+// scaled by log2(e)/sqrt(d_h)) and the weighted values; a row whose sum falls outside
+// [2^-64, 2^64] is redone with the scores shifted by their maximum.  The heads of a row sit
+// in adjacent lanes, so the row's Eq. 2 scale is a shuffle reduction.
 // ------------------------------------------------------------------------------------------
 struct AttnArgs {
   const float *qkv;
@@ -247,21 +248,35 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
 #pragma unroll
   for (int t = 0; t < DH; ++t) q[t] = valid ? base[(int64_t)i * d3 + h * DH + t] : 0.0f;
 
-  float mu = -INFINITY;
-  for (int e = beg; e < end; ++e) {
-    const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
-    mu = fmaxf(mu, head_dot<DH>(q, kr));
-  }
+  // weights 2^s unshifted; rows whose sum leaves [2^-64, 2^64] are redone shifted by max s
   float S = 0.0f, acc[DH];
 #pragma unroll
   for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
   for (int e = beg; e < end; ++e) {
     const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
-    const float ex = softmax_exp2(head_dot<DH>(q, kr) - mu);
+    const float ex = softmax_exp2(head_dot<DH>(q, kr));
     S = S + ex;
     const float *vr = kr + d;
 #pragma unroll
     for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+  }
+  if (end > beg && !(S >= 0x1p-64f && S <= 0x1p64f)) {
+    float mu = -INFINITY;
+    for (int e = beg; e < end; ++e) {
+      const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
+      mu = fmaxf(mu, head_dot<DH>(q, kr));
+    }
+    S = 0.0f;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+    for (int e = beg; e < end; ++e) {
+      const float *kr = base + (int64_t)idx[e] * d3 + d + h * DH;
+      const float ex = softmax_exp2(head_dot<DH>(q, kr) - mu);
+      S = S + ex;
+      const float *vr = kr + d;
+#pragma unroll
+      for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+    }
   }
   const float rS = valid ? 1.0f / S : 0.0f;
   float amax = 0.0f;

@@ -236,3 +236,33 @@ def test_fused_head_split_and_positional_table(P, oracle_mod, hf, with_pos):
         dec = P.Decoder(H, w, path=path)
         bits, logits = dec.decode(_dev(y))
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+@pytest.mark.parametrize("regime", ["mixed", "overflow", "underflow"])
+def test_softmax_shifted_rows(P, oracle_mod, regime):
+    """Attention rows whose unshifted weight sum leaves [2^-64, 2^64] take the max-shifted
+    form on both paths: query/key scales blown up (scores of hundreds: some or all rows
+    overflow), or query and key biases of opposite sign (every score far below -64)."""
+    from workloads import random_weights
+    from workloads.configs import parity_check
+    from workloads.channel import awgn_words
+    from workloads.codes import generator_from_parity
+    print(f"[softmax] regime {regime}", flush=True)
+    H = parity_check(CONFIGS[2])
+    m, n = H.shape
+    w = random_weights(n, m, 32, 2, 8, seed=77)
+    if regime == "mixed":
+        w.scale[:, 0:2] *= np.float32(5.0)
+    elif regime == "overflow":
+        w.scale[:, 0:2] *= np.float32(40.0)
+    else:
+        w.b["q"][:] = np.float32(6.0)
+        w.b["k"][:] = np.float32(-6.0)
+    y, x, _ = awgn_words(generator_from_parity(H), 129, (3.0, 5.0), seed=8)
+    om = oracle_mod.OracleModel(H, w)
+    bo, fo = om.decode(y, n_threads=16)
+    assert np.isfinite(fo).all()
+    for path in (P.PATH_FUSED, P.PATH_LAYERED):
+        dec = P.Decoder(H, w, path=path)
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
