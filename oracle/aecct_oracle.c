@@ -12,7 +12,7 @@
  *   SEQ         left-to-right from 0 in ascending index;
  *   DOT         q.k as a multiply followed by fused multiply-adds in ascending
  *               index order;
- *   EXP2        oracle_exp2 below (2^x, economised degree-6 series);
+ *   EXP2        oracle_exp2 below (2^x, economised degree-5 series);
  *   RSQRT       oracle_rsqrt below (three Newton steps from a bit-level seed).
  */
 #include "aecct_oracle.h"
@@ -51,13 +51,17 @@ float oracle_tree_sum(const float *v, int32_t w) {
  * into the scores.  x is clamped to [-125, 128] (the result stays a normal
  * number or becomes +inf from 2^128 on, and k below fits an int), split
  * exactly into k = rint(x) and r = x - k in [-1/2, 1/2];
- * 2^r = e^(r ln 2) is the degree-7 Taylor series economised to degree 6 by
- * Chebyshev's method (Lanczos): subtracting c7 T7(2r) / 8192, with
- * T7(u) = 64u^7 - 112u^5 + 56u^3 - 7u, cancels the r^7 term and moves
- * c7 * 3584/8192 into c5, -c7 * 448/8192 into c3 and c7 * 14/8192 into c1
- * (added error below 2e-9); Horner with fp32-rounded coefficients, then the
- * exact scaling by 2^k.
- * Pin: within 1 ulp of 2^x over [-125, 64]; exact at integers; +inf from 128.
+ * 2^r = e^(r ln 2) is its degree-7 Taylor series (c_j = (ln 2)^j / j!)
+ * economised to degree 5 by Chebyshev's method (Lanczos), |2r| <= 1:
+ * subtracting c7 T7(2r) / 8192, T7(u) = 64u^7 - 112u^5 + 56u^3 - 7u, cancels
+ * r^7 and moves c7 * 3584/8192 into c5, -c7 * 448/8192 into c3 and
+ * c7 * 14/8192 into c1; subtracting c6 T6(2r) / 2048, T6(u) = 32u^6 - 48u^4
+ * + 18u^2 - 1, cancels r^6 and moves c6 * 768/2048 into c4 and
+ * -c6 * 72/2048 into c2 (its constant c6 / 2048 is left out so that 2^0 is
+ * exactly 1).  Added error below c6/1024 + c7/8192 < 1.6e-7; Horner with
+ * fp32-rounded coefficients, then the exact scaling by 2^k.
+ * Pin: relative error below 3e-7 over [-125, 64]; exact at integers; +inf
+ * from 128.
  */
 #define ORC_LN2 0.69314718055994530942
 #define ORC_T(j) ORC_T##j
@@ -68,22 +72,21 @@ float oracle_tree_sum(const float *v, int32_t w) {
 #define ORC_T5 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 120.0)
 #define ORC_T6 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 720.0)
 #define ORC_T7 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 5040.0)
-static const float exp2_coef[7] = {
+static const float exp2_coef[6] = {
     1.0f,
     (float)(ORC_T1 + ORC_T7 * 14.0 / 8192.0),
-    (float)(ORC_T2),
+    (float)(ORC_T2 - ORC_T6 * 72.0 / 2048.0),
     (float)(ORC_T3 - ORC_T7 * 448.0 / 8192.0),
-    (float)(ORC_T4),
-    (float)(ORC_T5 + ORC_T7 * 3584.0 / 8192.0),
-    (float)(ORC_T6)};
+    (float)(ORC_T4 + ORC_T6 * 768.0 / 2048.0),
+    (float)(ORC_T5 + ORC_T7 * 3584.0 / 8192.0)};
 
 float oracle_exp2(float x) {
   if (x < -125.0f) x = -125.0f;
   if (x > 128.0f) x = 128.0f;
   const float k = rintf(x);
   const float r = x - k;
-  float p = exp2_coef[6];
-  for (int j = 5; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
+  float p = exp2_coef[5];
+  for (int j = 4; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
   return ldexpf(p, (int)k);
 }
 

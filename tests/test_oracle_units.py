@@ -47,15 +47,15 @@ def test_exp2_close_to_pow_and_exact_at_integers(oracle_mod):
     for x in (128.0, 1e30):                                          # clamped at 128: 2^128 is +inf
         assert np.isinf(oracle_mod.exp2(x)) and oracle_mod.exp2(x) > 0
     for x in (np.float32(127.4), np.float32(127.75)):               # still finite below 2^128
-        assert abs(float(oracle_mod.exp2(x)) - 2.0 ** float(x)) <= float(_ulp(2.0 ** float(x)))
+        assert abs(float(oracle_mod.exp2(x)) - 2.0 ** float(x)) <= 3e-7 * 2.0 ** float(x)
     xs = np.concatenate([np.linspace(-125, 64, 50001, dtype=np.float32),
                          -np.random.default_rng(1).random(20000).astype(np.float32) * 125])
     worst = 0.0
     for x in xs:
         e = float(oracle_mod.exp2(x))
         ref = 2.0 ** float(x)
-        worst = max(worst, abs(e - ref) / float(_ulp(ref)))
-    assert worst <= 1.0, worst
+        worst = max(worst, abs(e - ref) / ref)
+    assert worst <= 3e-7, worst
 
 
 def test_rsqrt_close_to_exact(oracle_mod):
