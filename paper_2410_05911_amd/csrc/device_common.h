@@ -78,20 +78,19 @@ __device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_
 // 2^x for the base-2 attention softmax: clamp to [-125, 128] (the result stays a normal
 // number, or is +inf from 2^128 on; a NaN argument gives 2^-125, since the median of three
 // with a NaN operand is the minimum of the other two), exact split x = k + r with
-// k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its
-// degree-7 Taylor series economised to degree 6 with the Chebyshev polynomial T7(2r) / 8192
-// (coefficients fp32 of: 1, ln2 + c7*14/8192, (ln2)^2/2, (ln2)^3/6 - c7*448/8192, (ln2)^4/24,
-// (ln2)^5/120 + c7*3584/8192, (ln2)^6/720 with c7 = (ln2)^7/5040), Horner, then an exact
-// scaling by 2^k.
+// k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its degree-7 Taylor series
+// (c_j = (ln2)^j / j!) economised to degree 5 with the Chebyshev polynomials T7(2r) / 8192
+// and T6(2r) / 2048, the constant term kept at 1 (coefficients fp32 of: 1,
+// c1 + c7*14/8192, c2 - c6*72/2048, c3 - c7*448/8192, c4 + c6*768/2048,
+// c5 + c7*3584/8192), Horner, then an exact scaling by 2^k.  Relative error below 3e-7.
 __device__ __forceinline__ float softmax_exp2(float x) {
   x = __builtin_amdgcn_fmed3f(x, -125.0f, 128.0f);
   const float k = __builtin_rintf(x);
   const float r = x - k;
-  float p = 0x1.430912p-13f;
-  p = __builtin_fmaf(p, r, 0x1.5f47d0p-10f);
-  p = __builtin_fmaf(p, r, 0x1.3b2ab6p-7f);
+  float p = 0x1.5f47d0p-10f;
+  p = __builtin_fmaf(p, r, 0x1.3d0f44p-7f);
   p = __builtin_fmaf(p, r, 0x1.c6aecep-5f);
-  p = __builtin_fmaf(p, r, 0x1.ebfbe0p-3f);
+  p = __builtin_fmaf(p, r, 0x1.ebf90ap-3f);
   p = __builtin_fmaf(p, r, 0x1.62e430p-1f);
   p = __builtin_fmaf(p, r, 1.0f);
   return __builtin_ldexpf(p, (int)k);

@@ -180,7 +180,6 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
   // Per tile and head group the neighbour loop runs T = the longest list among the tile's
   // lanes (padding slots have none).
   F.tile_tab.assign(2 * NT, 0);
-  std::vector<int> padT(NT, 1);
   for (int t = 0; t < NT; ++t)
     for (int grp = 0; grp < 2; ++grp) {
       int T = 1;
@@ -190,14 +189,22 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
         for (int g = 0; g < 4; ++g) T = std::max(T, len(mask_of(4 * grp + g), tok));
       }
       F.tile_tab[2 * t + grp] = (uint32_t)T;
-      padT[t] = std::max(padT[t], T);
     }
-  // every list of the tile is stored, also those of a mask no head uses: pad to the longest
-  for (int t = 0; t < NT; ++t)
+  // Stored length of the (tile, mask) lists: every list of the mask in the tile (also of a
+  // mask no head uses), and T of every head group that reads the mask.
+  std::vector<int> padT(2 * NT, 1);
+  for (int t = 0; t < NT; ++t) {
     for (int c = 0; c < 16; ++c) {
       const int tok = F.slot_token[16 * t + c];
-      if (tok >= 0) padT[t] = std::max(padT[t], std::max(len(0, tok), len(1, tok)));
+      if (tok < 0) continue;
+      for (int mask = 0; mask < 2; ++mask) padT[2 * t + mask] = std::max(padT[2 * t + mask], len(mask, tok));
     }
+    for (int grp = 0; grp < 2; ++grp)
+      for (int g = 0; g < 4; ++g) {
+        const int mask = mask_of(4 * grp + g);
+        padT[2 * t + mask] = std::max(padT[2 * t + mask], (int)F.tile_tab[2 * t + grp]);
+      }
+  }
   // Columns within a tile: a seeded local search over swaps of two columns of one tile that
   // lowers the LDS bank collisions of the key/value gathers (the 16 lanes of one head read the
   // rows of their e-th neighbours; rows of slots with equal column mod 16 (or mod 8 within a
@@ -269,30 +276,31 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
   for (int sl = 0; sl < S; ++sl)
     if (F.slot_token[sl] >= 0) slot_of[F.slot_token[sl]] = sl;
   // neighbour lists: byte offsets of the neighbours' 16-byte key rows in ascending token order,
-  // padded to the tile's longest list with the offset of the pad row (row 16 NT of a head),
-  // and stored entry-major per (tile, mask): entry e of column c at tbase + e * 16 + c.
+  // padded with the offset of the pad row (row 16 NT of a head), in groups of four entries
+  // per column: entry e of column c at tbase + 64 (e / 4) + 4 c + e % 4.  A (tile, mask)
+  // region holds floor(padT / 4) + 1 groups, one more than the full groups of any loop over
+  // it, so the kernel may always read the group after the last full one.
   F.slot_tab.assign(2 * S, 0);
   {
     std::vector<size_t> tbase(2 * NT);
     size_t total = 0;
-    for (int t = 0; t < NT; ++t)
-      for (int mask = 0; mask < 2; ++mask) {
-        tbase[2 * t + mask] = total;
-        total += (size_t)padT[t] * 16;
-      }
-    F.nbr.assign(total, 0);
+    for (int tm = 0; tm < 2 * NT; ++tm) {
+      tbase[tm] = total;
+      total += (size_t)(padT[tm] / 4 + 1) * 64;
+    }
+    F.nbr.assign(total, (uint16_t)(S * 16));
     for (int sl = 0; sl < S; ++sl)
       for (int mask = 0; mask < 2; ++mask) {
         const int t = sl / 16, c = sl % 16, tok = F.slot_token[sl];
-        const size_t base = tbase[2 * t + mask] + c;
+        const size_t base = tbase[2 * t + mask] + 4 * (size_t)c;
         uint32_t cnt = 0;
         if (tok >= 0) {
           const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
           const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
           cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
-          for (uint32_t e = 0; e < cnt; ++e) F.nbr[base + 16 * e] = (uint16_t)(slot_of[idx[ptr[tok] + e]] * 16);
+          for (uint32_t e = 0; e < cnt; ++e)
+            F.nbr[base + 64 * (e / 4) + e % 4] = (uint16_t)(slot_of[idx[ptr[tok] + e]] * 16);
         }
-        for (int e = (int)cnt; e < padT[t]; ++e) F.nbr[base + 16 * (size_t)e] = (uint16_t)(S * 16);
         F.slot_tab[2 * sl + mask] = (uint32_t)base | (cnt << 16);
       }
   }
@@ -495,7 +503,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   bool fused_ok = path_req != AECCT_PATH_LAYERED && aecct::fused_supported(M);
   if (fused_ok) {
     build_fused(M, H, w, m1_ptr, m1_idx, m2_ptr, m2_idx, FI);
-    fused_ok = aecct::fused_fits(M, (int)(FI.nbr.size() / 2));
+    // list starts are 16-bit entry indices
+    fused_ok = FI.nbr.size() <= 65536 && aecct::fused_fits(M, (int)(FI.nbr.size() / 2));
     if (!fused_ok) FI = FusedImage();
   }
   if (M.path == AECCT_PATH_AUTO) M.path = fused_ok ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;

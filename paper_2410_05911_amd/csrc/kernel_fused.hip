@@ -30,7 +30,7 @@ namespace aecct {
 struct FusedArgs {
   const uint16_t *frag;        // [N][FRAGS][64] 2-bit codes
   const float *vec;            // [N][VEC]
-  const uint32_t *nbr;         // neighbour entries, uint16 byte offsets, two per word
+  const uint32_t *nbr;         // neighbour entries, uint16 byte offsets, four per lane and group
   int nbr_words;
   const uint32_t *slot_tab;    // [16 NT][2]: start | count << 16, first / second ring
   const uint32_t *tile_tab;    // [NT][2]: longest list T of the tile, per head group
@@ -149,19 +149,19 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Neighbour lists: q is the lane's scaled query, ent its entries (byte offsets of the
-// neighbours' key rows in ascending token order, 16 apart: a tile's lists are stored
-// entry-major so the 16 lanes of a head read consecutive words), kbase this lane's head in
-// the key buffer, values vofs bytes after the keys.
-// One neighbour of the base-2 softmax (Section 4.2): score DOT(q', k) of the key row at
-// byte offset e, its weight 2^s, and the running sums S and acc (ascending neighbours).
-__device__ __forceinline__ void attend_step(const float (&q)[4], const unsigned char *kbase, int vofs,
-                                            uint32_t e, float shift, float &S, float (&acc)[4]) {
-  const float4 k = *(const float4 *)(kbase + e);
+// Neighbour lists: q is the lane's scaled query; ent its entries (byte offsets of the
+// neighbours' key rows in ascending token order), four to a lane per 8-byte group: entry e
+// at ent[64 (e / 4) + e % 4], so the 16 lanes of a head read 128 consecutive bytes per
+// group; kbase is this lane's head in the key buffer, values vofs bytes after the keys.
+__device__ __forceinline__ float4 lds_row(const unsigned char *p) { return *(const float4 *)p; }
+
+// One neighbour of the base-2 softmax (Section 4.2): score DOT(q', k), its weight
+// 2^(s - shift), and the running sums S and acc (ascending neighbours).
+__device__ __forceinline__ void attend_step(const float (&q)[4], float4 k, float4 vv, float shift, float &S,
+                                            float (&acc)[4]) {
   const float kk[4] = {k.x, k.y, k.z, k.w};
   const float ex = softmax_exp2(head_dot<4>(q, kk) - shift);
   S = S + ex;
-  const float4 vv = *(const float4 *)(kbase + vofs + e);
   acc[0] = __builtin_fmaf(ex, vv.x, acc[0]);
   acc[1] = __builtin_fmaf(ex, vv.y, acc[1]);
   acc[2] = __builtin_fmaf(ex, vv.z, acc[2]);
@@ -169,34 +169,57 @@ __device__ __forceinline__ void attend_step(const float (&q)[4], const unsigned 
 }
 
 // Attention of one lane's (token, head) row over its cnt neighbours, all lanes of the tile
-// running T (the tile's longest list) steps.  Entries past a lane's list point at the
-// head's pad row (key NaN, value 0): its weight is 2^-125 (the clamp maps the NaN score to
-// -125) and its value 0, so acc is unchanged and S too whenever S >= 2^-64, the only case in
-// which the unshifted sums are kept; a row whose sum leaves [2^-64, 2^64] is redone over its
-// real entries with the scores shifted by their maximum.
+// running T (the tile's longest list) steps, a group of four entries at a time with the
+// next group's entries read ahead.  Entries past a lane's list point at the head's pad row
+// (key NaN, value 0): its weight is 2^-125 (the clamp maps the NaN score to -125) and its
+// value 0, so acc is unchanged and S too whenever S >= 2^-64, the only case in which the
+// unshifted sums are kept; a row whose sum leaves [2^-64, 2^64] is redone over its real
+// entries with the scores shifted by their maximum.
 __device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t *ent, int cnt, int T,
                                             const unsigned char *kbase, int vofs, float (&o)[4]) {
   float S = 0.0f, acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  int j = 0;
-  for (; j + 4 <= T; j += 4) {
-    const uint16_t *e = ent + 16 * j;
-    attend_step(q, kbase, vofs, e[0], 0.0f, S, acc);
-    attend_step(q, kbase, vofs, e[16], 0.0f, S, acc);
-    attend_step(q, kbase, vofs, e[32], 0.0f, S, acc);
-    attend_step(q, kbase, vofs, e[48], 0.0f, S, acc);
+  const uint2 *eg = (const uint2 *)ent;
+  const int G = T >> 2;
+  uint2 nx = eg[0];
+  for (int u = 0; u < G; ++u) {
+    const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+    const float4 k0 = lds_row(kbase + e0), v0 = lds_row(kbase + vofs + e0);
+    const float4 k1 = lds_row(kbase + e1), v1 = lds_row(kbase + vofs + e1);
+    const float4 k2 = lds_row(kbase + e2), v2 = lds_row(kbase + vofs + e2);
+    const float4 k3 = lds_row(kbase + e3), v3 = lds_row(kbase + vofs + e3);
+    nx = eg[16 * (u + 1)];          // in the table: every list has a group past its end
+    attend_step(q, k0, v0, 0.0f, S, acc);
+    attend_step(q, k1, v1, 0.0f, S, acc);
+    attend_step(q, k2, v2, 0.0f, S, acc);
+    attend_step(q, k3, v3, 0.0f, S, acc);
   }
-  for (; j < T; ++j) attend_step(q, kbase, vofs, ent[16 * j], 0.0f, S, acc);
+  const int rem = T & 3;              // the last, partial group is already in nx
+  if (rem > 0) {
+    const uint32_t e0 = nx.x & 0xffffu;
+    attend_step(q, lds_row(kbase + e0), lds_row(kbase + vofs + e0), 0.0f, S, acc);
+  }
+  if (rem > 1) {
+    const uint32_t e1 = nx.x >> 16;
+    attend_step(q, lds_row(kbase + e1), lds_row(kbase + vofs + e1), 0.0f, S, acc);
+  }
+  if (rem > 2) {
+    const uint32_t e2 = nx.y & 0xffffu;
+    attend_step(q, lds_row(kbase + e2), lds_row(kbase + vofs + e2), 0.0f, S, acc);
+  }
   if (cnt > 0 && !(S >= 0x1p-64f && S <= 0x1p64f)) {
     float mu = -INFINITY;
     for (int i = 0; i < cnt; ++i) {
-      const float4 k = *(const float4 *)(kbase + ent[16 * i]);
+      const float4 k = lds_row(kbase + ent[64 * (i >> 2) + (i & 3)]);
       const float kk[4] = {k.x, k.y, k.z, k.w};
       mu = fmaxf(mu, head_dot<4>(q, kk));
     }
     S = 0.0f;
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[t] = 0.0f;
-    for (int i = 0; i < cnt; ++i) attend_step(q, kbase, vofs, ent[16 * i], mu, S, acc);
+    for (int i = 0; i < cnt; ++i) {
+      const uint32_t e = ent[64 * (i >> 2) + (i & 3)];
+      attend_step(q, lds_row(kbase + e), lds_row(kbase + vofs + e), mu, S, acc);
+    }
   }
   const float rS = cnt > 0 ? 1.0f / S : 0.0f;
 #pragma unroll
@@ -441,6 +464,7 @@ FusedLds fused_lds(const Model &M, int nbr_words) {
   size_t off = (size_t)M.n_layers * fz::FRAGS * 64 * 8;
   L.off_vec = (int)off;
   off += (size_t)M.n_layers * fz::VEC * 4;
+  off = (off + 7) / 8 * 8;                    // 8-byte entry groups
   L.off_nbr = (int)off;
   off += (size_t)nbr_words * 4;
   L.off_slot = (int)off;

@@ -211,6 +211,7 @@ def test_fused_and_layered_paths_agree(P, c):
     fused = P.Decoder(H, w, path=P.PATH_FUSED)
     layered = P.Decoder(H, w, path=P.PATH_LAYERED)
     assert fused.path == P.PATH_FUSED and layered.path == P.PATH_LAYERED
+    assert P.Decoder(H, w).path == P.PATH_FUSED       # the automatic choice takes the fused kernel
     yd = _dev(y)
     bf, lf = fused.decode(yd)
     bl, ll = layered.decode(yd)
