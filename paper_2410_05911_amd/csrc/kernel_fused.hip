@@ -63,10 +63,19 @@ __device__ __forceinline__ uint32_t opaque_copy(uint32_t v) {
   return w;
 }
 #if !defined(AECCT_XLANE_SWAP)
-__device__ __forceinline__ float pair_sum32(float v) { return v + __shfl_xor(v, 32); }
-__device__ __forceinline__ float pair_sum16(float v) { return v + __shfl_xor(v, 16); }
-__device__ __forceinline__ uint32_t pair_max32(uint32_t v) { return max(v, (uint32_t)__shfl_xor((int)v, 32)); }
-__device__ __forceinline__ uint32_t pair_max16(uint32_t v) { return max(v, (uint32_t)__shfl_xor((int)v, 16)); }
+// v of lane (this lane xor m), m = 16 or 32: a whole-wave permute, byte address 4 (lane ^ m)
+template <int M>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((__builtin_amdgcn_workitem_id_x() & 63u) ^ M) << 2), (int)v);
+}
+__device__ __forceinline__ float pair_sum32(float v) {
+  return v + __builtin_bit_cast(float, lane_xor<32>(__builtin_bit_cast(uint32_t, v)));
+}
+__device__ __forceinline__ float pair_sum16(float v) {
+  return v + __builtin_bit_cast(float, lane_xor<16>(__builtin_bit_cast(uint32_t, v)));
+}
+__device__ __forceinline__ uint32_t pair_max32(uint32_t v) { return max(v, lane_xor<32>(v)); }
+__device__ __forceinline__ uint32_t pair_max16(uint32_t v) { return max(v, lane_xor<16>(v)); }
 #else
 __device__ __forceinline__ float pair_sum32(float v) {
   const uint32_t u = __builtin_bit_cast(uint32_t, v);
@@ -251,7 +260,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   __syncthreads();
 
   const int lane = tid & 63, c = lane & 15, g = lane >> 4;
-  const int wave = tid >> 6, nw = nthr >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = nthr >> 6;   // uniform: scalar
   const uint64_t *sfrag = (const uint64_t *)smem;
   const float *svec = (const float *)(smem + p.off_vec);
   const uint16_t *snbr = (const uint16_t *)(smem + p.off_nbr);
@@ -271,21 +280,26 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   }
   const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
 
-  int tok[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) tok[t] = stok[16 * t + c];
-
   for (int64_t w = (int64_t)blockIdx.x * nw + wave; w < p.words; w += (int64_t)gridDim.x * nw) {
+    // Per-word copy of the lane index: the addresses of the embedding and head steps derive
+    // from it, so they are recomputed per word rather than held through the layers.
+    int lw = lane;
+    asm volatile("" : "+v"(lw));
+    const int cw = lw & 15, gw = lw >> 4;
+    int tok[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) tok[t] = stok[16 * t + cw];
     // ---- pre-processing h(y) (Section 3) and embedding ----
     const float *yw = p.y + w * p.n;
-    const float ylane = lane < p.n ? yw[lane] : 0.0f;
+    const float ylane = lw < p.n ? yw[lw] : 0.0f;
     const uint64_t neg = __ballot(ylane < 0.0f);
     float X[NT][8], al[NT];
     uint32_t xb[NT][2];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int tk = tok[t];
-      const float yv = __shfl(ylane, (tk >= 0 && tk < p.n) ? tk : 0);
+      const float yv = __builtin_bit_cast(
+          float, __builtin_amdgcn_ds_bpermute(((tk >= 0 && tk < p.n) ? tk : 0) << 2, __builtin_bit_cast(int, ylane)));
       float tv = 0.0f;
       if (tk >= 0) {
         if (tk < p.n) {
@@ -295,12 +309,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
           tv = s ? -1.0f : 1.0f;
         }
       }
-      const float4 *er = (const float4 *)(p.eperm + ((16 * t + c) * 4 + g) * 8);
+      const float4 *er = (const float4 *)(p.eperm + ((16 * t + cw) * 4 + gw) * 8);
       const float4 e0 = er[0], e1 = er[1];
       const float ev[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
       float pv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
       if (p.pperm) {
-        const float4 *pr = (const float4 *)(p.pperm + ((16 * t + c) * 4 + g) * 8);
+        const float4 *pr = (const float4 *)(p.pperm + ((16 * t + cw) * 4 + gw) * 8);
         const float4 p0 = pr[0], p1 = pr[1];
         pv[0] = p0.x; pv[1] = p0.y; pv[2] = p0.z; pv[3] = p0.w;
         pv[4] = p1.x; pv[5] = p1.y; pv[6] = p1.z; pv[7] = p1.w;
@@ -421,8 +435,10 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
 
     // ---- output head and hard decision (Section 3) ----
     float *zbuf = (float *)kv;
+    int lh = lane;
+    asm volatile("" : "+v"(lh));
     {
-      const float4 *wr = (const float4 *)(p.w1perm + 8 * g);
+      const float4 *wr = (const float4 *)(p.w1perm + 8 * (lh >> 4));
       const float4 w0 = wr[0], w1 = wr[1];
       const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
 #pragma unroll
@@ -431,16 +447,17 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
 #pragma unroll
         for (int v = 0; v < 8; ++v) pr[v] = X[t][v] * wv[v];
         const float z = token_sum(pr) + p.b1;
-        if (g == 0 && tok[t] >= 0) zbuf[tok[t]] = z;
+        const int tk = stok[16 * t + (lh & 15)];
+        if (lh < 16 && tk >= 0) zbuf[tk] = z;
       }
     }
     wave_sync_lds();
-    if (lane < p.n) {
+    if (lh < p.n) {
       float acc = 0.0f;
-      for (int i = 0; i < p.L; ++i) acc = __builtin_fmaf(zbuf[i], p.wo[(int64_t)i * p.n + lane], acc);
-      const float f = acc + p.bo[lane];
-      p.bits[w * p.n + lane] = (uint8_t)((ylane < 0.0f) != (f < 0.0f));
-      if (p.logits) p.logits[w * p.n + lane] = f;
+      for (int i = 0; i < p.L; ++i) acc = __builtin_fmaf(zbuf[i], p.wo[(int64_t)i * p.n + lh], acc);
+      const float f = acc + p.bo[lh];
+      p.bits[w * p.n + lh] = (uint8_t)((ylane < 0.0f) != (f < 0.0f));
+      if (p.logits) p.logits[w * p.n + lh] = f;
     }
     wave_sync_lds();
   }
