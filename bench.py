@@ -126,6 +126,39 @@ def cpu_baseline(H, w, y, budget_s=12.0):
                       f"{threads} OpenMP threads, {dt:.1f} s"}
 
 
+def aap_import_bench(repeats: int = 5):
+    """AAP weight import (Eq. 1, a host step of model creation) for every in-block map of a
+    d = 128, 10-layer model (the LDPC(256,128) shape): 60 fp32 matrices, 1.97 M weights."""
+    import paper_2410_05911_amd as P
+    rng = np.random.default_rng(4242)
+    d, N = 128, 10
+    mats = []
+    for _ in range(N):
+        mats += [rng.standard_normal((d, d)).astype(np.float32) * 0.05 for _ in range(4)]
+        mats += [rng.standard_normal((d, 4 * d)).astype(np.float32) * 0.05,
+                 rng.standard_normal((4 * d, d)).astype(np.float32) * 0.05]
+    total = sum(m.size for m in mats)
+    P.aap_ternarize(mats[0])
+    best = float("inf")
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        for m in mats:
+            P.aap_ternarize(m)
+        best = min(best, time.perf_counter() - t0)
+    out = {"metric": "AAP weight import (Eq. 1) throughput, host", "value": total / best, "unit": "weights/s",
+           "higher_is_better": True, "ms_per_model": best * 1e3,
+           "config": {"workload": "aap_import_d128_N10", "matrices": len(mats), "weights": total,
+                      "percentile": 0.5, "delta": 1.0, "eps": 1e-8}}
+    import oracle
+    t0 = time.perf_counter()
+    for m in mats:
+        oracle.aap_ternarize(m)
+    dt = time.perf_counter() - t0
+    out["cpu_baseline"] = {"value": total / dt, "unit": "weights/s", "cores": 1, "kind": "oracle",
+                           "sample": "the same 60 matrices, one pass, full sort per matrix"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,9 +169,14 @@ def main():
     ap.add_argument("--workload", type=int, default=WORKLOAD)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (HBM counter calibration)")
+    ap.add_argument("--aap-import", action="store_true",
+                    help="only time the AAP weight import (Eq. 1) of a d = 128, 10-layer model")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.aap_import:
+        aap_import_bench()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the decode shards over words with no exchange); "

@@ -117,6 +117,31 @@ typedef struct aecct_model aecct_model;   /* opaque */
 aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_weights *w, int32_t d,
                           int32_t n_layers, int32_t heads, const aecct_options *opt, aecct_model **out);
 
+/*
+ * Ternary weights and weight scale of one AAP linear layer from its trained
+ * fp32 weights (Section 4.1, Eq. 1): the step that turns a checkpoint into
+ * the `aecct_weights` above.  Host call, no GPU work.
+ *   gamma    = Percentile(|W|, p): the p-quantile of the `count` absolute
+ *              values, interpolated linearly between the order statistics
+ *              floor(pos) and floor(pos) + 1 at pos = p (count - 1) (zero
+ *              based), evaluated in double and rounded once to fp32; the
+ *              paper's p is 0.5, the median;
+ *   *scale   = fp32(gamma * delta), the matrix scale gamma*delta of Eq. 3;
+ *   ternary  = RoundClip(W / (scale + eps), -1, 1): the fp32 quotient by
+ *              fp32(scale + eps), rounded to the nearest integer (ties to
+ *              even) and clipped; if scale + eps is 0 the quotient of a
+ *              nonzero weight counts as +-infinity (ternary = its sign) and a
+ *              zero weight gives 0.
+ *   w          host fp32 [count], any layout (only the multiset of |w|
+ *              matters for gamma); must be finite;
+ *   percentile p in [0, 1]; delta the learned factor, finite and > 0;
+ *   eps        the paper's epsilon, finite and >= 0 (1e-8 is usual);
+ *   ternary    host int8 [count] out, entry i from w[i]; scale host fp32 out.
+ * count >= 1.  Errors: INVALID_ARG (and OUT_OF_MEMORY for the copy of |w|).
+ */
+aecct_status aecct_aap_ternarize(const float *w, int64_t count, float percentile, float delta, float eps,
+                                 int8_t *ternary, float *scale);
+
 /* Release a model (NULL is a no-op).  No call may still be running on it. */
 void aecct_destroy(aecct_model *model);
 

@@ -67,6 +67,8 @@ def lib():
         L.oracle_decode.argtypes = [C.POINTER(_Model), _f32p, C.c_int64, _u8p, _f32p, C.c_int32]
         L.oracle_decode_taps.restype = C.c_int
         L.oracle_decode_taps.argtypes = [C.POINTER(_Model), _f32p, _u8p, _f32p, C.POINTER(_Taps)]
+        L.oracle_aap_ternarize.restype = C.c_int
+        L.oracle_aap_ternarize.argtypes = [_f32p, C.c_int64, C.c_float, C.c_float, C.c_float, _i8p, _f32p]
         L.oracle_decode_ref64.restype = C.c_int
         L.oracle_decode_ref64.argtypes = [C.POINTER(_Model), _f32p, C.c_int64, _u8p, _f64p, C.c_int32]
         _lib = L
@@ -268,3 +270,15 @@ def layernorm_rows(R, g, b, eps=1e-5):
     lib().oracle_layernorm_rows(_p(R, _f32p), rows, d, _p(_c(g, np.float32), _f32p), _p(_c(b, np.float32), _f32p),
                                 float(np.float32(eps)), _p(out, _f32p))
     return out
+
+
+def aap_ternarize(w, p=0.5, delta=1.0, eps=1e-8):
+    """AAP import of one fp32 weight matrix (Eq. 1): (ternary int8 of w's shape, scale gamma*delta)."""
+    w = _c(w, np.float32)
+    t = np.zeros(w.shape, np.int8)
+    sc = np.zeros(1, np.float32)
+    rc = lib().oracle_aap_ternarize(_p(w, _f32p), w.size, float(np.float32(p)), float(np.float32(delta)),
+                                    float(np.float32(eps)), _p(t, _i8p), _p(sc, _f32p))
+    if rc:
+        raise ValueError("oracle_aap_ternarize: invalid arguments")
+    return t, sc[0]

@@ -321,6 +321,57 @@ void oracle_head_word(const oracle_model *M, const float *X, const float *y, flo
   }
 }
 
+/* ------------------------------------------------------------------ AAP import */
+
+static int cmp_float(const void *a, const void *b) {
+  const float x = *(const float *)a, y = *(const float *)b;
+  return (x > y) - (x < y);
+}
+
+/*
+ * Adaptive Absolute Percentile ternarisation of one weight matrix (Section 4.1,
+ * Eq. 1): gamma = Percentile(Abs(W), p) with the paper's p = 0.5; the scale of
+ * Eq. 3 is gamma * delta; Ternary(W) = RoundClip(W / (gamma delta + eps), -1, 1)
+ * with RoundClip(x, a, b) = max(a, min(b, round(x))).
+ * Readings: the percentile is the p-quantile with linear interpolation between
+ * the order statistics around p (count - 1) (zero based), computed in double
+ * and rounded once to fp32; round is to nearest, ties to even; the quotient is
+ * the correctly rounded fp32 division by fp32(fp32(gamma delta) + eps); when
+ * that denominator is 0, nonzero weights map to their sign.
+ * Pin: gamma equals numpy's median of |W| (p = 0.5) and its linear-method
+ * quantile otherwise; the ternary entries equal numpy's float32 division
+ * rounded half to even and clipped; zeros / signs / clipping invariants.
+ */
+int oracle_aap_ternarize(const float *w, int64_t count, float p, float delta, float eps, int8_t *t,
+                         float *scale) {
+  if (count < 1 || !(p >= 0.0f && p <= 1.0f) || !(delta > 0.0f) || !(eps >= 0.0f)) return -1;
+  float *a = (float *)malloc(sizeof(float) * (size_t)count);
+  if (!a) return -1;
+  for (int64_t i = 0; i < count; ++i) a[i] = fabsf(w[i]);
+  qsort(a, (size_t)count, sizeof(float), cmp_float);
+  const double pos = (double)p * (double)(count - 1);
+  int64_t lo = (int64_t)floor(pos);
+  if (lo > count - 1) lo = count - 1;
+  const int64_t hi = lo + 1 < count ? lo + 1 : lo;
+  const double frac = pos - (double)lo;
+  const float gamma = (float)((double)a[lo] + frac * ((double)a[hi] - (double)a[lo]));
+  free(a);
+  const float s = gamma * delta;
+  const float den = s + eps;
+  for (int64_t i = 0; i < count; ++i) {
+    float r;
+    if (den == 0.0f)
+      r = w[i] > 0.0f ? 1.0f : (w[i] < 0.0f ? -1.0f : 0.0f);
+    else
+      r = rintf(w[i] / den);
+    if (r > 1.0f) r = 1.0f;
+    if (r < -1.0f) r = -1.0f;
+    t[i] = (int8_t)r;
+  }
+  *scale = s;
+  return 0;
+}
+
 /* ------------------------------------------------------------------ whole decode */
 
 typedef struct {

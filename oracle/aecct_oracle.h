@@ -90,6 +90,11 @@ int oracle_decode_taps(const oracle_model *M, const float *y, uint8_t *bits, flo
                        const oracle_taps *taps);
 int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, uint8_t *bits,
                         double *f, int32_t n_threads);
+/* AAP weight import (Section 4.1, Eq. 1): gamma = p-quantile of |w| (linear interpolation,
+ * double, rounded to fp32), *scale = fp32(gamma * delta), t = RoundClip(w / fp32(scale + eps)).
+ * Returns 0, or -1 for invalid arguments. */
+int oracle_aap_ternarize(const float *w, int64_t count, float p, float delta, float eps, int8_t *t,
+                         float *scale);
 /* fp64 dense masked softmax attention of one word (reference for the sparse canonical one). */
 int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const uint8_t *M2,
                                const double *qkv, double score_scale, double *o);

@@ -88,8 +88,22 @@ def lib():
         L.aecct_stage_head.argtypes = [_vp, _vp, _vp, C.c_int64, _vp, _vp, _vp]
         L.aecct_ternary_gemm.restype = C.c_int
         L.aecct_ternary_gemm.argtypes = [_vp, C.c_int32, C.c_int32, _vp, C.c_int64, _vp, _vp]
+        L.aecct_aap_ternarize.restype = C.c_int
+        L.aecct_aap_ternarize.argtypes = [_f32p, C.c_int64, C.c_float, C.c_float, C.c_float, _i8p, _f32p]
         _lib = L
     return _lib
+
+
+def aap_ternarize(w, percentile: float = 0.5, delta: float = 1.0, eps: float = 1e-8):
+    """AAP import of one trained fp32 weight matrix (Section 4.1, Eq. 1) by the library:
+    returns (ternary int8 array of w's shape, weight scale gamma*delta as np.float32)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    t = np.zeros(w.shape, np.int8)
+    sc = C.c_float(0.0)
+    _check(lib().aecct_aap_ternarize(w.ctypes.data_as(_f32p), w.size, float(np.float32(percentile)),
+                                     float(np.float32(delta)), float(np.float32(eps)), t.ctypes.data_as(_i8p),
+                                     C.byref(sc)), "aecct_aap_ternarize")
+    return t, np.float32(sc.value)
 
 
 def _check(status: int, what: str):

@@ -267,3 +267,31 @@ def test_softmax_shifted_rows(P, oracle_mod, regime):
         dec = P.Decoder(H, w, path=path)
         bits, logits = dec.decode(_dev(y))
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+def test_decode_with_aap_imported_weights(P, oracle_mod):
+    """A model whose six in-block maps come from fp32 matrices through the library's AAP import
+    (Eq. 1) decodes like the oracle model whose maps come from the oracle's import."""
+    import copy
+    from workloads import random_weights
+    from workloads.configs import parity_check
+    from workloads.channel import awgn_words
+    from workloads.codes import generator_from_parity
+    H = parity_check(CONFIGS[2])
+    m, n = H.shape
+    base = random_weights(n, m, 32, 2, 8, seed=91)
+    rng = np.random.default_rng(92)
+    w_lib, w_orc = copy.deepcopy(base), copy.deepcopy(base)
+    for kind_i, kind in enumerate(("q", "k", "v", "o", "ff1", "ff2")):
+        for layer in range(base.n_layers):
+            W = rng.standard_normal(base.w[kind][layer].shape).astype(np.float32) * 0.05
+            delta = np.float32(1.0 + 0.1 * layer + 0.05 * kind_i)
+            t_l, s_l = P.aap_ternarize(W, 0.5, delta, 1e-8)
+            t_o, s_o = oracle_mod.aap_ternarize(W, p=0.5, delta=delta, eps=1e-8)
+            w_lib.w[kind][layer], w_lib.scale[layer, kind_i] = t_l, s_l
+            w_orc.w[kind][layer], w_orc.scale[layer, kind_i] = t_o, s_o
+    y, x, _ = awgn_words(generator_from_parity(H), 200, (3.0, 5.0), seed=93)
+    bo, fo = oracle_mod.OracleModel(H, w_orc).decode(y, n_threads=16)
+    for path in (P.PATH_FUSED, P.PATH_LAYERED):
+        bits, logits = P.Decoder(H, w_lib, path=path).decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
