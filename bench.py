@@ -30,7 +30,7 @@ PEAK_INT8 = 5.0e15                # dense int8 MFMA ops/s
 PEAK_HBM = 8.0e12
 
 
-def algorithmic_counts(H, w):
+def algorithmic_counts(H, w, attention: str = "hpsa"):
     """Per-word work of the method as the paper writes it (not as executed).
 
     fp32/ALU operations: every scalar operation of Sections 3-4 counts once, with each
@@ -60,7 +60,8 @@ def algorithmic_counts(H, w):
                    + dff)                             # ReLU
     pair = 2 * dh + 5
     row_head = dh + 1
-    pairs = hf * nnz1 + (heads - hf) * nnz2
+    # HPSA: h_f heads over the first ring, the rest over the second; CASA: every head over both
+    pairs = heads * (nnz1 + nnz2) if attention == "casa" else hf * nnz1 + (heads - hf) * nnz2
     layer = L * token_layer + pairs * pair + L * heads * row_head
     embed = L * (d + 1) + int(H.sum())                # t * E_i rows, |y| / sign, syndrome XORs
     head = L * (d + 1) + n * (L + 1 + 2)              # z_i, f_o, hard decision
@@ -167,6 +168,8 @@ def main():
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 layered, 2 fused")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD)
+    ap.add_argument("--attention", choices=("hpsa", "casa"), default="hpsa",
+                    help="head-partitioned masks (the method) or the ECCT mask on every head")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (HBM counter calibration)")
     ap.add_argument("--aap-import", action="store_true",
@@ -187,7 +190,7 @@ def main():
     import paper_2410_05911_amd as P
     from workloads import build_workload
 
-    cfg, H, G, w, y, x = build_workload(args.workload)
+    cfg, H, G, w, y, x = build_workload(args.workload, attention=args.attention)
     B = cfg.batch
     dev = torch.device("cuda:0")
     dec = P.Decoder(H, w, path=args.path)
@@ -212,7 +215,7 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     value = B / (ms * 1e-3)
 
-    cnt = algorithmic_counts(H, w)
+    cnt = algorithmic_counts(H, w, args.attention)
     path = "fused" if dec.path == P.PATH_FUSED else "layered"
     kernel = "k_fused_decode" if path == "fused" else "layered_decode"
     launch_s = ms * 1e-3                        # fused: one launch per step
@@ -224,7 +227,7 @@ def main():
         "peak": PEAK_ALU_OPS / 1e12,
         "unit": "Top/s (fp32 VALU ops, one per lane per clock)",
         "frac": achieved / PEAK_ALU_OPS,
-        "traffic": measured_traffic(kernel, cfg.name),
+        "traffic": measured_traffic(kernel, cfg.name) if args.attention == "hpsa" else None,
         "alu_ops_per_word": cnt["alu_ops"],
         "int8_mfma_frac": 2 * cnt["int8_macs"] * B / launch_s / PEAK_INT8,
         "hbm_alg_frac": cnt["hbm_bytes"] * B / launch_s / PEAK_HBM,
@@ -242,9 +245,10 @@ def main():
         "vs_baseline": None,
         "dtype": "int8xternary->int32, fp32",
         "data": "synthetic: seeded BPSK/AWGN words, random ternary weights",
-        "config": {"workload": cfg.name, "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
+        "config": {"workload": cfg.name if args.attention == "hpsa" else cfg.name + "_casa", "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
                    "n": cfg.n, "tokens": dec.L, "d": cfg.d, "layers": cfg.n_layers, "heads": cfg.heads,
-                   "first_ring_heads": w.first_ring_heads, "batch": B, "path": path,
+                   "first_ring_heads": w.first_ring_heads if args.attention == "hpsa" else None,
+                   "attention": args.attention, "batch": B, "path": path,
                    "wall_s_timed": t_wall},
         "roofline": roofline,
     }

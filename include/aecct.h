@@ -92,11 +92,21 @@ typedef struct aecct_weights {
   const float *head_bo;                       /* [n] */
 } aecct_weights;
 
+/* Attention masks of the heads. */
+typedef enum aecct_attention {
+  AECCT_ATTN_HPSA = 0,  /* head partitioning (Section 4.2): heads 0..h_f-1 over the first-ring
+                           mask (Tanner neighbours), the rest over the second-ring mask (nodes two
+                           steps away, the node itself included) */
+  AECCT_ATTN_CASA = 1   /* the ECCT mask for every head (Section 3, code-aware self attention): the
+                           union of the two rings, nodes at most two steps away; h_f is ignored */
+} aecct_attention;
+
 typedef struct aecct_options {
   int32_t first_ring_heads;  /* h_f, 0..heads; -1 = heads / 2 (the paper's default split) */
   int32_t d_ff;              /* feed-forward width; -1 = 4 d */
   float ln_eps;              /* LayerNorm epsilon; <= 0 = 1e-5 */
   int32_t path;              /* aecct_path */
+  int32_t attention;         /* aecct_attention */
 } aecct_options;
 
 typedef struct aecct_model aecct_model;   /* opaque */
@@ -152,6 +162,7 @@ typedef struct aecct_model_info {
   int64_t nnz_first_ring;    /* allowed (query, key) pairs of the first-ring mask */
   int64_t nnz_second_ring;   /* same for the second-ring mask (diagonal included) */
   size_t device_bytes;       /* device memory held by the model */
+  int32_t attention;         /* aecct_attention (first_ring_heads reads 0 under CASA) */
 } aecct_model_info;
 aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info);
 

@@ -28,7 +28,8 @@ class _Model(C.Structure):
                 ("ln_eps", C.c_float), ("H", _u8p), ("embed", _f32p), ("pos", _f32p),
                 ("w", _i8p * 6), ("scale", _f32p), ("bias", _f32p * 6),
                 ("ln1_g", _f32p), ("ln1_b", _f32p), ("ln2_g", _f32p), ("ln2_b", _f32p),
-                ("head_w1", _f32p), ("head_b1", C.c_float), ("head_wo", _f32p), ("head_bo", _f32p)]
+                ("head_w1", _f32p), ("head_b1", C.c_float), ("head_wo", _f32p), ("head_bo", _f32p),
+                ("attention", C.c_int32)]
 
 
 class _Taps(C.Structure):
@@ -84,6 +85,7 @@ def _c(a, dtype):
 
 
 KINDS = ("q", "k", "v", "o", "ff1", "ff2")
+ATTENTION = {"hpsa": 0, "casa": 1}
 
 
 class OracleModel:
@@ -118,6 +120,7 @@ class OracleModel:
         st.head_b1 = w.head_b1
         st.head_wo = _p(keep(w.head_wo, np.float32), _f32p)
         st.head_bo = _p(keep(w.head_bo, np.float32), _f32p)
+        st.attention = ATTENTION[getattr(w, "attention", "hpsa")]
         self.st = st
 
     # ------------------------------------------------------------ whole decode

@@ -236,6 +236,16 @@ void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float 
 }
 
 /* DOT of a scaled query row segment with a key row segment (ascending dims). */
+/* Whether key j is allowed for row i of head h: HPSA (Section 4.2) gives heads below h_f the
+ * first-ring mask and the others the second-ring mask; CASA (Section 3, the ECCT mask) gives
+ * every head their union, the nodes at most two steps away including the node itself. */
+static int key_allowed(const oracle_model *M, const uint8_t *M1, const uint8_t *M2, int32_t h, int32_t i,
+                       int32_t j) {
+  const int64_t e = (int64_t)i * (M->n + M->m) + j;
+  if (M->attention == 1) return M1[e] || M2[e];
+  return h < M->first_ring_heads ? M1[e] : M2[e];
+}
+
 static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_t h, int32_t dh) {
   const float *qi = qkv + (int64_t)i * 3 * d + h * dh;
   const float *kj = qkv + (int64_t)j * 3 * d + d + h * dh;
@@ -246,7 +256,8 @@ static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_
 
 /*
  * Head-partitioned self-attention (Section 4.2): heads 0..h_f-1 attend over
- * the first-ring mask M1, the others over the second-ring mask M2.  Per row i
+ * the first-ring mask M1, the others over the second-ring mask M2 (with
+ * attention = 1, the CASA variant of Section 3: every head over M1 | M2).  Per row i
  * and head h the softmax of the scaled dot products over the allowed keys j
  * (ascending) weighs the value rows; the scale is 1/sqrt(d_h) per head.  The
  * query rows arrive already multiplied by log2(e)/sqrt(d_h) (folded into the
@@ -266,11 +277,10 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
   const int32_t L = M->n + M->m, d = M->d, dh = M->d / M->heads;
   for (int32_t i = 0; i < L; ++i)
     for (int32_t h = 0; h < M->heads; ++h) {
-      const uint8_t *row = (h < M->first_ring_heads ? M1 : M2) + (int64_t)i * L;
       float mu = -INFINITY;
       int cnt = 0;
       for (int32_t j = 0; j < L; ++j)
-        if (row[j]) {
+        if (key_allowed(M, M1, M2, h, i, j)) {
           float s = score_f32(qkv, d, i, j, h, dh);
           if (s > mu) mu = s;
           ++cnt;
@@ -282,7 +292,7 @@ int oracle_attention_word(const oracle_model *M, const uint8_t *M1, const uint8_
         S = 0.0f;
         for (int32_t t = 0; t < dh; ++t) acc[t] = 0.0f;
         for (int32_t j = 0; j < L; ++j)
-          if (row[j]) {
+          if (key_allowed(M, M1, M2, h, i, j)) {
             float s = score_f32(qkv, d, i, j, h, dh);
             float e = oracle_exp2(pass == 0 ? s : s - shift);
             S = S + e;
@@ -580,13 +590,12 @@ int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const u
   if (!s) return -1;
   for (int32_t i = 0; i < L; ++i)
     for (int32_t h = 0; h < M->heads; ++h) {
-      const uint8_t *row = (h < M->first_ring_heads ? M1 : M2) + (int64_t)i * L;
       double mx = -INFINITY;
       for (int32_t j = 0; j < L; ++j) {
         double dot = 0.0;
         for (int32_t t = 0; t < dh; ++t)
           dot += qkv[(int64_t)i * 3 * d + h * dh + t] * qkv[(int64_t)j * 3 * d + d + h * dh + t];
-        s[j] = row[j] ? dot * score_scale : -INFINITY;
+        s[j] = key_allowed(M, M1, M2, h, i, j) ? dot * score_scale : -INFINITY;
         if (s[j] > mx) mx = s[j];
       }
       if (mx == -INFINITY) { free(s); return -1; }

@@ -50,6 +50,8 @@ typedef struct oracle_model {
   float head_b1;
   const float *head_wo;       /* [L][n] (W_o) */
   const float *head_bo;       /* [n] */
+  int32_t attention;          /* 0: HPSA head partitioning (Section 4.2); 1: CASA, every head
+                                 over the ECCT mask M1 | M2 (Section 3) */
 } oracle_model;
 
 /* Per-layer intermediate values of one word (each pointer may be NULL). */

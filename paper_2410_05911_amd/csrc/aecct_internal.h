@@ -65,6 +65,7 @@ struct Model {
   float eps;
   float kq;              // fp32(log2(e) / sqrt(d_h)): score scale folded into the query map
   int path;              // resolved aecct_path
+  int attention;         // aecct_attention; under CASA the second-ring lists hold the union, hf = 0
   int device;
   int64_t nnz1, nnz2;
   size_t device_bytes;
@@ -72,7 +73,8 @@ struct Model {
 
   // Tanner graph: check j's variables chk_idx[chk_ptr[j] .. chk_ptr[j+1]) ascending
   const int32_t *chk_ptr, *chk_idx;
-  // attention neighbour lists per token, ascending: first ring (M1) and second ring (M2)
+  // attention neighbour lists per token, ascending: first ring (M1) and second ring (M2, or
+  // M1 | M2 under CASA)
   const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;

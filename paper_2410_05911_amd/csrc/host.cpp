@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <iterator>
 #include <new>
 #include <vector>
 
@@ -190,14 +191,18 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
       }
       F.tile_tab[2 * t + grp] = (uint32_t)T;
     }
-  // Stored length of the (tile, mask) lists: every list of the mask in the tile (also of a
-  // mask no head uses), and T of every head group that reads the mask.
-  std::vector<int> padT(2 * NT, 1);
+  // Stored length of the (tile, mask) lists of a mask some head reads: every list of the mask
+  // in the tile, and T of every head group that reads the mask.  A mask no head reads gets an
+  // empty region (its lists are never stored or read).
+  bool used[2] = {false, false};
+  for (int h = 0; h < 8; ++h) used[mask_of(h)] = true;
+  std::vector<int> padT(2 * NT, 0);
   for (int t = 0; t < NT; ++t) {
     for (int c = 0; c < 16; ++c) {
       const int tok = F.slot_token[16 * t + c];
       if (tok < 0) continue;
-      for (int mask = 0; mask < 2; ++mask) padT[2 * t + mask] = std::max(padT[2 * t + mask], len(mask, tok));
+      for (int mask = 0; mask < 2; ++mask)
+        if (used[mask]) padT[2 * t + mask] = std::max(padT[2 * t + mask], len(mask, tok));
     }
     for (int grp = 0; grp < 2; ++grp)
       for (int g = 0; g < 4; ++g) {
@@ -294,7 +299,7 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
         const int t = sl / 16, c = sl % 16, tok = F.slot_token[sl];
         const size_t base = tbase[2 * t + mask] + 4 * (size_t)c;
         uint32_t cnt = 0;
-        if (tok >= 0) {
+        if (tok >= 0 && used[mask]) {
           const std::vector<int32_t> &ptr = mask == 0 ? m1_ptr : m2_ptr;
           const std::vector<int32_t> &idx = mask == 0 ? m1_idx : m2_idx;
           cnt = (uint32_t)(ptr[tok + 1] - ptr[tok]);
@@ -418,6 +423,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   if (opt && !std::isfinite(opt->ln_eps)) return AECCT_ERR_INVALID_ARG;
   const int path_req = opt ? opt->path : AECCT_PATH_AUTO;
   if (path_req < AECCT_PATH_AUTO || path_req > AECCT_PATH_FUSED) return AECCT_ERR_INVALID_ARG;
+  const int attention = opt ? opt->attention : AECCT_ATTN_HPSA;
+  if (attention != AECCT_ATTN_HPSA && attention != AECCT_ATTN_CASA) return AECCT_ERR_INVALID_ARG;
   const int64_t L64 = (int64_t)n + m;
   if (L64 > (1 << 20)) return AECCT_ERR_UNSUPPORTED;
   const int L = (int)L64;
@@ -491,6 +498,20 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.kq = (float)(1.4426950408889634074 / std::sqrt((double)dh));
   M.nnz1 = (int64_t)m1_idx.size();
   M.nnz2 = (int64_t)m2_idx.size();
+  M.attention = attention;
+  if (attention == AECCT_ATTN_CASA) {
+    // every head reads the union of the two rings: it takes the second-ring list slot, h_f = 0
+    std::vector<int32_t> u_ptr(L + 1, 0), u_idx;
+    u_idx.reserve(m1_idx.size() + m2_idx.size());
+    for (int a = 0; a < L; ++a) {
+      std::merge(m1_idx.begin() + m1_ptr[a], m1_idx.begin() + m1_ptr[a + 1], m2_idx.begin() + m2_ptr[a],
+                 m2_idx.begin() + m2_ptr[a + 1], std::back_inserter(u_idx));
+      u_ptr[a + 1] = (int32_t)u_idx.size();
+    }
+    m2_ptr.swap(u_ptr);
+    m2_idx.swap(u_idx);
+    M.hf = 0;
+  }
   M.head_b1 = w->head_b1;
   for (int l = 0; l < n_layers; ++l) {
     for (int k = 0; k < 6; ++k) M.layer[l].sq[k] = w->scale[(size_t)l * 6 + k] / 127.0f;
@@ -661,6 +682,7 @@ aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
   info->n = M.n; info->m = M.m; info->L = M.L; info->d = M.d; info->n_layers = M.n_layers;
   info->heads = M.heads; info->first_ring_heads = M.hf; info->d_ff = M.dff; info->path = M.path;
   info->nnz_first_ring = M.nnz1; info->nnz_second_ring = M.nnz2; info->device_bytes = M.device_bytes;
+  info->attention = M.attention;
   return AECCT_OK;
 }
 

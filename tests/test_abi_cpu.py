@@ -41,7 +41,7 @@ def test_status_strings(P):
     assert P.lib().aecct_status_string(99) == b"unknown status"
 
 
-def _create(P, H, w, d=None, n_layers=None, heads=None, path=0, hf=None, dff=None, eps=None):
+def _create(P, H, w, d=None, n_layers=None, heads=None, path=0, hf=None, dff=None, eps=None, attention=0):
     H = np.ascontiguousarray(H, np.uint8)
     m, n = H.shape
     keep = []
@@ -68,7 +68,7 @@ def _create(P, H, w, d=None, n_layers=None, heads=None, path=0, hf=None, dff=Non
     st.head_w1, st.head_b1 = f32(w.head_w1), float(w.head_b1)
     st.head_wo, st.head_bo = f32(w.head_wo), f32(w.head_bo)
     opt = P.Options(w.first_ring_heads if hf is None else hf, w.d_ff if dff is None else dff,
-                    w.ln_eps if eps is None else eps, path)
+                    w.ln_eps if eps is None else eps, path, attention)
     h = C.c_void_p()
     rc = P.lib().aecct_create(H.ctypes.data_as(C.POINTER(C.c_uint8)), m, n, C.byref(st),
                               w.d if d is None else d, w.n_layers if n_layers is None else n_layers,
@@ -106,6 +106,7 @@ def test_create_validation_before_device(P):
     assert _create(P, H, w, heads=5) == INV                # d % heads != 0
     assert _create(P, H, w, hf=9) == INV                   # more first-ring heads than heads
     assert _create(P, H, w, path=7) == INV
+    assert _create(P, H, w, attention=2) == INV            # neither HPSA nor CASA
     w4 = random_weights(7, 3, 32, 2, 4, seed=1)            # d_h = 8: supported
     w5 = random_weights(7, 3, 32, 2, 1, seed=1)            # d_h = 32: not supported
     assert _create(P, H, w5) == UNS

@@ -295,3 +295,20 @@ def test_decode_with_aap_imported_weights(P, oracle_mod):
     for path in (P.PATH_FUSED, P.PATH_LAYERED):
         bits, logits = P.Decoder(H, w_lib, path=path).decode(_dev(y))
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_casa_decode_against_oracle(P, oracle_mod, c):
+    """The CASA variant (Section 3: the ECCT mask on every head) on every path that takes the
+    shape, against the oracle on a sample of a ragged batch."""
+    print(f"[casa] config {c}", flush=True)
+    cfg, H, G, w, y, x = build_workload(c, batch=1027, attention="casa")
+    k = {1: 1027, 2: 256, 3: 24}[c]
+    idx = np.unique(np.linspace(0, 1026, k).astype(np.int64))
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y[idx], n_threads=16)
+    paths = (P.PATH_FUSED, P.PATH_LAYERED) if c in (1, 2) else (P.PATH_LAYERED,)
+    for path in paths:
+        dec = P.Decoder(H, w, path=path)
+        assert dec.info.attention == P.ATTN_CASA and dec.path == path
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits)[idx], fo, _np(bits)[idx], bo, y[idx])

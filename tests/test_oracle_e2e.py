@@ -54,11 +54,12 @@ def test_zero_weight_closed_form(oracle_mod):
         assert np.abs(f[bi] - fr).max() <= 2e-5
 
 
-def test_fp32_canonical_close_to_fp64_reference(oracle_mod):
-    """The canonical fp32 decode against the oracle's fp64 dense mode on Hamming(7,4).
-    Differences come only from fp32 rounding and the rare int8 code that sits on a rounding
-    boundary; most words agree to ~1e-6."""
-    cfg, H, G, w, y, x = build_workload(1, batch=1024)
+@pytest.mark.parametrize("attention", ["hpsa", "casa"])
+def test_fp32_canonical_close_to_fp64_reference(oracle_mod, attention):
+    """The canonical fp32 decode against the oracle's fp64 dense mode on Hamming(7,4), with the
+    head-partitioned masks and with the ECCT mask on every head.  Differences come only from fp32
+    rounding and the rare int8 code that sits on a rounding boundary; most words agree to ~1e-6."""
+    cfg, H, G, w, y, x = build_workload(1, batch=1024, attention=attention)
     om = oracle_mod.OracleModel(H, w)
     bits, f = om.decode(y, n_threads=8)
     bits64, f64 = om.decode_ref64(y, n_threads=8)

@@ -179,16 +179,20 @@ def _sdpa_reference(H, w, qkv, scale=math.log(2.0)):
     out = torch.zeros(L, d, dtype=torch.float64)
     for hh in range(h):
         sl = slice(hh * dh, (hh + 1) * dh)
-        mask = M1 if hh < w.first_ring_heads else M2
+        if getattr(w, "attention", "hpsa") == "casa":
+            mask = M1 | M2                          # the ECCT mask for every head
+        else:
+            mask = M1 if hh < w.first_ring_heads else M2
         out[:, sl] = torch.nn.functional.scaled_dot_product_attention(
             Q[None, None, :, sl], K[None, None, :, sl].contiguous(), V[None, None, :, sl], attn_mask=mask,
             scale=scale)[0, 0]
     return out.numpy()
 
 
+@pytest.mark.parametrize("attention", ["hpsa", "casa"])
 @pytest.mark.parametrize("c", [1, 2, 3])
-def test_attention_against_fp64_sdpa(oracle_mod, c):
-    cfg, H, G, w, y, x = build_workload(c, batch=1)
+def test_attention_against_fp64_sdpa(oracle_mod, c, attention):
+    cfg, H, G, w, y, x = build_workload(c, batch=1, attention=attention)
     om = oracle_mod.OracleModel(H, w)
     rng = np.random.default_rng(6)
     qkv = (rng.standard_normal((om.L, 3 * w.d)) * 2).astype(np.float32)
@@ -252,3 +256,21 @@ def test_head_against_fp64(oracle_mod):
     f64 = z64 @ w.head_wo.astype(np.float64) + w.head_bo
     assert np.abs(z - z64).max() <= 1e-5 and np.abs(f - f64).max() <= 1e-5
     assert (bits == ((y[0] * f) < 0)).all()                 # bin(y * f)
+
+
+def test_casa_mask_is_ecct_mask_and_doubles_pairs(oracle_mod):
+    """CASA (Section 3) lets every head see the nodes at most two Tanner steps away: its per-head
+    pair count is |M1| + |M2|, twice HPSA's total over 8 heads when h_f = h_s (Section 4.2)."""
+    cfg, H, G, w, y, x = build_workload(2, batch=1)
+    M1, M2 = oracle_mod.masks(H)
+    m, n = H.shape
+    L = n + m
+    # BFS distance <= 2 in the Tanner graph, self included
+    A = np.zeros((L, L), bool)
+    A[:n, n:] = H.T.astype(bool)
+    A[n:, :n] = H.astype(bool)
+    reach = np.eye(L, dtype=bool) | A | ((A.astype(int) @ A.astype(int)) > 0)
+    assert ((M1.astype(bool) | M2.astype(bool)) == reach).all()
+    hp = 4 * M1.sum() + 4 * M2.sum()
+    ca = 8 * (M1.astype(bool) | M2.astype(bool)).sum()
+    assert ca == 2 * hp

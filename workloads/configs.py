@@ -56,13 +56,16 @@ def parity_check(cfg: WorkloadConfig) -> np.ndarray:
     return _H_CACHE[key].copy()
 
 
-def build_workload(index: int, batch: int | None = None, *, data_seed: int | None = None):
-    """(cfg, H, G, weights, y, x) for workload `index`; `batch` overrides the configured batch."""
+def build_workload(index: int, batch: int | None = None, *, data_seed: int | None = None,
+                   attention: str = "hpsa"):
+    """(cfg, H, G, weights, y, x) for workload `index`; `batch` overrides the configured batch,
+    `attention` picks the head-partitioned ("hpsa") or all-heads-ECCT-mask ("casa") model."""
     cfg = CONFIGS[index]
     H = parity_check(cfg)
     G = generator_from_parity(H)
     m, n = H.shape
-    w = random_weights(n, m, cfg.d, cfg.n_layers, cfg.heads, p_zero=cfg.p_zero, seed=cfg.seeds[1])
+    w = random_weights(n, m, cfg.d, cfg.n_layers, cfg.heads, p_zero=cfg.p_zero, seed=cfg.seeds[1],
+                       attention=attention)
     B = cfg.batch if batch is None else batch
     y, x, _ = awgn_words(G, B, cfg.ebn0, seed=cfg.seeds[2] if data_seed is None else data_seed)
     return cfg, H, G, w, y, x
