@@ -90,6 +90,11 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
                       hipStream_t s);
 hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
                             hipStream_t s);
+// Q/K/V projection and attention fused per (word, 16-dimension head group), then Eq. 2 per
+// token of O: the layered decode's path for d = 64, 128 when L tokens' Q, K, V of a group fit LDS.
+bool qkv_attention_supported(const Model &M);
+hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                float *o, int8_t *oq, float *ao, hipStream_t s);
 hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,
                            int64_t rows, float *x1, int8_t *x1q, float *a1, hipStream_t s);
 hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, int8_t *gq,

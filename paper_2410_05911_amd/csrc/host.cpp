@@ -721,8 +721,12 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
     const int64_t rows = nw * M.L;
     hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
-      e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
-      if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
+      if (aecct::qkv_attention_supported(M)) {
+        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, oq, ao, s);   // O (fp32) in the QKV space
+      } else {
+        e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
+        if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
+      }
       if (e == hipSuccess) e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
       if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
       if (e == hipSuccess) e = aecct::launch_ffn2_ln(M, l, gq, ag, x1, rows, x, xq, ax, s);

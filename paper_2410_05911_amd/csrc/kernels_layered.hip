@@ -6,6 +6,8 @@
 // contiguous.  Tokens 0..n-1 are variable nodes, n..n+m-1 check nodes (Section 3).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "aecct_internal.h"
 #include "device_common.h"
 
@@ -66,7 +68,9 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
 // row-wise LayerNorm and absmax reductions stay inside the wave (intra-lane over the
 // column tiles, then a 16-lane DPP reduction).
 // ------------------------------------------------------------------------------------------
-enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3 };
+// EPI_QKV_MAP: one of the three maps of EPI_QKV per launch (out_f and bias pointing at the map's
+// columns, rows 3 NOUT apart, scale sq[0]), a third of the accumulators of the fused launch.
+enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3, EPI_QKV_MAP = 4 };
 
 struct GemmArgs {
   const int8_t *a;        // [rows][K]
@@ -140,7 +144,16 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
       float al[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) al[i] = ok[i] ? p.alpha[r[i]] : 0.0f;
-      if constexpr (EPI == EPI_QKV) {
+      if constexpr (EPI == EPI_QKV_MAP) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          const float b = p.bias[j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (ok[i]) p.out_f[r[i] * (3 * NOUT) + j] = __builtin_fmaf((float)acc[t][i], al[i] * p.sq[0], b);
+        }
+      } else if constexpr (EPI == EPI_QKV) {
         constexpr int TB = T / 3;  // tiles per map
 #pragma unroll
         for (int t = 0; t < T; ++t) {
@@ -302,6 +315,152 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
 }
 
 // ------------------------------------------------------------------------------------------
+// Query/key/value projection and attention of one 16-dimension head group of one word
+// (d = 64 or 128).  The group's three 16-column tiles of the packed QKV map (Eq. 3) are
+// multiplied for all L tokens on v_mfma_i32_16x16x32_i8 and dequantised into LDS (fp32,
+// [L][16] each for Q, K, V), then the group's attention rows (Section 4.2, the same
+// single-pass base-2 softmax and the same evaluation order as k_attention) gather their
+// neighbours' keys and values from LDS.  Blocks are persistent over the words and keep one
+// head group, whose weight tiles they stage once.  Writes the attention output O (fp32
+// [rows][d]) of the group's columns; k_quant_rows then applies Eq. 2 per token.
+// ------------------------------------------------------------------------------------------
+struct QkvAttnArgs {
+  const int8_t *xq;       // [rows][d] Eq. 2 codes of the layer input
+  const float *ax;        // [rows] their scales
+  const uint16_t *bpack;  // packed QKV map ([d][3d])
+  const float *bias;      // [3d]; the query third pre-scaled like sq[0]
+  float sq[3];            // dequant scale of Q (with log2(e)/sqrt(d_h)), K, V
+  int64_t words;
+  int L, hf;
+  const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
+  float *o;               // [rows][d]
+};
+
+template <int D, int DH>
+__global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
+  const int L = p.L;
+  float *qs = (float *)(smem + 3 * S * 64 * 8), *ks = qs + (size_t)L * 16, *vs = ks + (size_t)L * 16;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
+  const int hg = blockIdx.x % G;
+  for (int u = tid; u < 3 * S * 64; u += 256) {
+    const int m = u / (S * 64), rest = u - m * (S * 64);
+    bf[u] = unpack_ternary8(p.bpack[(size_t)(m * G + hg) * S * 64 + rest]);
+  }
+  const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+  __syncthreads();
+  const int64_t wstride = gridDim.x / G;
+  for (int64_t w = blockIdx.x / G; w < p.words; w += wstride) {
+    const int8_t *xw = p.xq + w * L * D;
+    const float *aw = p.ax + w * L;
+    for (int tt = wave; tt < (L + 15) / 16; tt += 4) {
+      const int ra = 16 * tt + col;
+      long afr[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) afr[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * rg) : 0;
+      v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        aq = mfma_i8_16x16x32(afr[s], (long)bf[(0 * S + s) * 64 + lane], aq);
+        ak = mfma_i8_16x16x32(afr[s], (long)bf[(1 * S + s) * 64 + lane], ak);
+        av = mfma_i8_16x16x32(afr[s], (long)bf[(2 * S + s) * 64 + lane], av);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 16 * tt + 4 * rg + i;
+        if (tok < L) {
+          const float al = aw[tok];
+          qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al * p.sq[0], bq);
+          ks[tok * 16 + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
+          vs[tok * 16 + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
+        }
+      }
+    }
+    __syncthreads();
+    for (int r = tid; r < L * HPG; r += 256) {
+      const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
+      const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr;
+      const int32_t *idx = h < p.hf ? p.m1_idx : p.m2_idx;
+      const int beg = ptr[i], end = ptr[i + 1];
+      float q[DH];
+#pragma unroll
+      for (int t = 0; t < DH; ++t) q[t] = qs[i * 16 + hh * DH + t];
+      float S_ = 0.0f, acc[DH];
+#pragma unroll
+      for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+      for (int e = beg; e < end; ++e) {
+        const int j = idx[e];
+        const float ex = softmax_exp2(head_dot<DH>(q, ks + j * 16 + hh * DH));
+        S_ = S_ + ex;
+        const float *vr = vs + j * 16 + hh * DH;
+#pragma unroll
+        for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+      }
+      if (end > beg && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
+        float mu = -INFINITY;
+        for (int e = beg; e < end; ++e) mu = fmaxf(mu, head_dot<DH>(q, ks + idx[e] * 16 + hh * DH));
+        S_ = 0.0f;
+#pragma unroll
+        for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+        for (int e = beg; e < end; ++e) {
+          const int j = idx[e];
+          const float ex = softmax_exp2(head_dot<DH>(q, ks + j * 16 + hh * DH) - mu);
+          S_ = S_ + ex;
+          const float *vr = vs + j * 16 + hh * DH;
+#pragma unroll
+          for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+        }
+      }
+      const float rS = end > beg ? 1.0f / S_ : 0.0f;
+      float *orow = p.o + (w * L + i) * D + h * DH;
+#pragma unroll
+      for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
+    }
+    __syncthreads();
+  }
+}
+
+// Eq. 2 per row of an fp32 [rows][D] matrix: 16 lanes per row, lane c holding the D / 16
+// consecutive features from c D / 16; alpha = max |x| (order-free), codes as everywhere.
+template <int D>
+__global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows, int8_t *q, float *a) {
+  constexpr int V = D / 16;
+  const int64_t r = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int c = threadIdx.x & 15;
+  float v[V];
+  if (r < rows) {
+#pragma unroll
+    for (int u = 0; u < V; u += 4) {
+      const float4 f = *(const float4 *)(x + r * D + c * V + u);
+      v[u] = f.x; v[u + 1] = f.y; v[u + 2] = f.z; v[u + 3] = f.w;
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < V; ++u) v[u] = 0.0f;
+  }
+  float amax = 0.0f;
+#pragma unroll
+  for (int u = 0; u < V; ++u) amax = fmaxf(amax, fabsf(v[u]));
+  amax = row16_max(amax);
+  if (r >= rows) return;
+  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+  uint32_t pk[V / 4];
+#pragma unroll
+  for (int u = 0; u < V / 4; ++u)
+    pk[u] = (uint32_t)(uint8_t)quant_code(v[4 * u], inv) | (uint32_t)(uint8_t)quant_code(v[4 * u + 1], inv) << 8 |
+            (uint32_t)(uint8_t)quant_code(v[4 * u + 2], inv) << 16 |
+            (uint32_t)(uint8_t)quant_code(v[4 * u + 3], inv) << 24;
+  if constexpr (V == 8) {
+    *(uint2 *)(q + r * D + c * V) = make_uint2(pk[0], pk[1]);
+  } else {
+    *(uint32_t *)(q + r * D + c * V) = pk[0];
+  }
+  if (c == 0) a[r] = amax;
+}
+
+// ------------------------------------------------------------------------------------------
 // Output head and hard decision (Section 3): one block per word.  z_i = W_{d->1} x_i + b1
 // (16 lanes per token, pairwise over features), then f_o = sum_i z_i W_o[i][o] + b_o in
 // ascending token order, bit = [y < 0] xor [f < 0].
@@ -395,7 +554,18 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
   switch (M.d) {
     case 32: return run_gemm<32, 96, EPI_QKV>(a, s);
     case 64: return run_gemm<64, 192, EPI_QKV>(a, s);
-    case 128: return run_gemm<128, 384, EPI_QKV>(a, s);
+    case 128:
+      // one launch per map: 8 output tiles per wave instead of 24
+      for (int m = 0; m < 3; ++m) {
+        GemmArgs b = a;
+        b.tile0 = 8 * m;
+        b.sq[0] = a.sq[m];
+        b.bias = a.bias + 128 * m;
+        b.out_f = a.out_f + 128 * m;
+        const hipError_t e = run_gemm<128, 128, EPI_QKV_MAP>(b, s);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
   }
   return hipErrorInvalidValue;
 }
@@ -494,6 +664,60 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
     case 16: hipLaunchKernelGGL(k_attention<16>, grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+size_t qkv_attention_lds(const Model &M) { return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)3 * M.L * 16 * 4; }
+
+bool qkv_attention_supported(const Model &M) {
+  return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && qkv_attention_lds(M) <= 160 * 1024;
+}
+
+template <int D, int DH>
+static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention<D, DH>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  constexpr int G = D / 16;
+  const int per_cu = (int)((160 * 1024) / lds) > 0 ? (int)((160 * 1024) / lds) : 1;
+  const int64_t blocks_per_group = std::min<int64_t>(a.words, (int64_t)256 * per_cu / G > 0 ? (int64_t)256 * per_cu / G : 1);
+  hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)(G * blocks_per_group)), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                float *o, int8_t *oq, float *ao, hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  if (!qkv_attention_supported(M)) return hipErrorInvalidValue;
+  const LayerWeights &W = M.layer[layer];
+  QkvAttnArgs a{};
+  a.xq = xq;
+  a.ax = ax;
+  a.bpack = W.qkv;
+  a.bias = W.b_qkv;
+  a.sq[0] = W.sq_qs;
+  a.sq[1] = W.sq[1];
+  a.sq[2] = W.sq[2];
+  a.words = words;
+  a.L = M.L;
+  a.hf = M.hf;
+  a.m1_ptr = M.m1_ptr; a.m1_idx = M.m1_idx; a.m2_ptr = M.m2_ptr; a.m2_idx = M.m2_idx;
+  a.o = o;
+  const size_t lds = qkv_attention_lds(M);
+  hipError_t e = hipErrorInvalidValue;
+  if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
+  else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
+  else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(a, lds, s);
+  else if (M.d == 64 && M.dh == 16) e = run_qkv_attention<64, 16>(a, lds, s);
+  if (e != hipSuccess) return e;
+  const int64_t rows = words * M.L;
+  const dim3 grid((unsigned)((rows + 15) / 16));
+  if (M.d == 64) hipLaunchKernelGGL(k_quant_rows<64>, grid, dim3(256), 0, s, o, rows, oq, ao);
+  else hipLaunchKernelGGL(k_quant_rows<128>, grid, dim3(256), 0, s, o, rows, oq, ao);
   return hipGetLastError();
 }
 
