@@ -336,8 +336,10 @@ struct QkvAttnArgs {
   float *o;               // [rows][d]
 };
 
+constexpr int kQaThreads = 512;
+
 template <int D, int DH>
-__global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
+__global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
   constexpr int S = D / 32, G = D / 16, HPG = 16 / DH;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
@@ -345,7 +347,7 @@ __global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
   float *qs = (float *)(smem + 3 * S * 64 * 8), *ks = qs + (size_t)L * 16, *vs = ks + (size_t)L * 16;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
   const int hg = blockIdx.x % G;
-  for (int u = tid; u < 3 * S * 64; u += 256) {
+  for (int u = tid; u < 3 * S * 64; u += kQaThreads) {
     const int m = u / (S * 64), rest = u - m * (S * 64);
     bf[u] = unpack_ternary8(p.bpack[(size_t)(m * G + hg) * S * 64 + rest]);
   }
@@ -355,7 +357,7 @@ __global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
   for (int64_t w = blockIdx.x / G; w < p.words; w += wstride) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
-    for (int tt = wave; tt < (L + 15) / 16; tt += 4) {
+    for (int tt = wave; tt < (L + 15) / 16; tt += kQaThreads / 64) {
       const int ra = 16 * tt + col;
       long afr[S];
 #pragma unroll
@@ -379,7 +381,7 @@ __global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
       }
     }
     __syncthreads();
-    for (int r = tid; r < L * HPG; r += 256) {
+    for (int r = tid; r < L * HPG; r += kQaThreads) {
       const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
       const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr;
       const int32_t *idx = h < p.hf ? p.m1_idx : p.m2_idx;
@@ -390,6 +392,7 @@ __global__ __launch_bounds__(256) void k_qkv_attention(QkvAttnArgs p) {
       float S_ = 0.0f, acc[DH];
 #pragma unroll
       for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+#pragma unroll 4
       for (int e = beg; e < end; ++e) {
         const int j = idx[e];
         const float ex = softmax_exp2(head_dot<DH>(q, ks + j * 16 + hh * DH));
@@ -685,7 +688,7 @@ static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_
   constexpr int G = D / 16;
   const int per_cu = (int)((160 * 1024) / lds) > 0 ? (int)((160 * 1024) / lds) : 1;
   const int64_t blocks_per_group = std::min<int64_t>(a.words, (int64_t)256 * per_cu / G > 0 ? (int64_t)256 * per_cu / G : 1);
-  hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)(G * blocks_per_group)), dim3(256), lds, s, a);
+  hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)(G * blocks_per_group)), dim3(kQaThreads), lds, s, a);
   return hipGetLastError();
 }
 
