@@ -312,3 +312,34 @@ def test_casa_decode_against_oracle(P, oracle_mod, c):
         assert dec.info.attention == P.ATTN_CASA and dec.path == path
         bits, logits = dec.decode(_dev(y))
         _assert_logits(_np(logits)[idx], fo, _np(bits)[idx], bo, y[idx])
+
+
+def _random_parity_check(m, n, seed, col_weight=3):
+    """A random 0/1 parity-check matrix with no empty row or column (not a designed code)."""
+    rng = np.random.default_rng(seed)
+    H = np.zeros((m, n), np.uint8)
+    for i in range(n):
+        H[rng.choice(m, size=col_weight, replace=False), i] = 1
+    for j in range(m):
+        if not H[j].any():
+            H[j, rng.integers(n)] = 1
+    return H
+
+
+@pytest.mark.parametrize("d,m,n,hf,attention", [(64, 21, 47, 4, "hpsa"), (64, 13, 30, 2, "hpsa"),
+                                                 (128, 25, 51, 4, "hpsa"), (128, 9, 20, 6, "casa"),
+                                                 (64, 40, 90, 0, "hpsa"), (128, 37, 70, 8, "hpsa")])
+def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attention):
+    """d = 64 and 128 on token counts L = n + m that are not multiples of 16 (partial token
+    tiles in the fused projection/attention kernel), several head splits and CASA."""
+    from workloads import random_weights
+    print(f"[wide] d {d} m {m} n {n} hf {hf} {attention}", flush=True)
+    H = _random_parity_check(m, n, seed=m * 131 + n)
+    w = random_weights(n, m, d, 2, 8, seed=d + m + n, first_ring_heads=hf, attention=attention)
+    rng = np.random.default_rng(5)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (37, n)) + 0.6 * rng.standard_normal((37, n))).astype(np.float32)
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.path == P.PATH_LAYERED
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits), fo, _np(bits), bo, y)
