@@ -89,7 +89,7 @@ struct GemmArgs {
   int32_t *out_acc;       // raw accumulators (RAW)
 };
 
-constexpr int kGemmWaves = 4;
+constexpr int kGemmWaves = 8;
 
 template <int K, int NOUT, int EPI>
 __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
@@ -507,16 +507,21 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs p) {
 // ------------------------------------------------------------------------------------------
 namespace {
 
-int gemm_grid(int64_t rows) {
+// Persistent grid: as many blocks as stay resident (LDS-limited), each staging its map's
+// weights once and striding over the 16-row strips.
+int gemm_grid(int64_t rows, size_t lds_bytes) {
   const int64_t groups = ((rows + 15) / 16 + kGemmWaves - 1) / kGemmWaves;
-  const int64_t g = groups < 2048 ? groups : 2048;
+  const int64_t per_cu = lds_bytes ? std::max<int64_t>(1, (int64_t)(160 * 1024 / lds_bytes)) : 8;
+  const int64_t g = std::min<int64_t>(groups, 256 * std::min<int64_t>(per_cu, 8));
   return (int)(g > 0 ? g : 1);
 }
 
 template <int K, int NOUT, int EPI>
 hipError_t run_gemm(const GemmArgs &a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm<K, NOUT, EPI>), dim3(gemm_grid(a.rows)), dim3(kGemmWaves * 64), 0, s, a);
+  constexpr bool kQuantOut = (EPI == EPI_LN || EPI == EPI_RELU_QUANT);
+  constexpr size_t lds = (size_t)(NOUT / 16) * (K / 32) * 64 * 8 + (kQuantOut ? (size_t)kGemmWaves * 16 * NOUT : 16);
+  hipLaunchKernelGGL((k_gemm<K, NOUT, EPI>), dim3(gemm_grid(a.rows, lds)), dim3(kGemmWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
