@@ -342,9 +342,13 @@ template <int D, int DH>
 __global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
   constexpr int S = D / 32, G = D / 16, HPG = 16 / DH;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  // Q rows 16 floats apart; K and V rows KVS = 20 floats apart, so that the 64-byte rows start
+  // on 16 different LDS banks (at 16 apart every row starts on one of 4) and random neighbour
+  // gathers collide less.
+  constexpr int KVS = 20;
   uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
   const int L = p.L;
-  float *qs = (float *)(smem + 3 * S * 64 * 8), *ks = qs + (size_t)L * 16, *vs = ks + (size_t)L * 16;
+  float *qs = (float *)(smem + 3 * S * 64 * 8), *ks = qs + (size_t)L * 16, *vs = ks + (size_t)L * KVS;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
   const int hg = blockIdx.x % G;
   for (int u = tid; u < 3 * S * 64; u += kQaThreads) {
@@ -375,8 +379,8 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
         if (tok < L) {
           const float al = aw[tok];
           qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al * p.sq[0], bq);
-          ks[tok * 16 + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
-          vs[tok * 16 + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
+          ks[tok * KVS + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
+          vs[tok * KVS + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
         }
       }
     }
@@ -395,23 +399,23 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
 #pragma unroll 4
       for (int e = beg; e < end; ++e) {
         const int j = idx[e];
-        const float ex = softmax_exp2(head_dot<DH>(q, ks + j * 16 + hh * DH));
+        const float ex = softmax_exp2(head_dot<DH>(q, ks + j * KVS + hh * DH));
         S_ = S_ + ex;
-        const float *vr = vs + j * 16 + hh * DH;
+        const float *vr = vs + j * KVS + hh * DH;
 #pragma unroll
         for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
       }
       if (end > beg && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
         float mu = -INFINITY;
-        for (int e = beg; e < end; ++e) mu = fmaxf(mu, head_dot<DH>(q, ks + idx[e] * 16 + hh * DH));
+        for (int e = beg; e < end; ++e) mu = fmaxf(mu, head_dot<DH>(q, ks + idx[e] * KVS + hh * DH));
         S_ = 0.0f;
 #pragma unroll
         for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
         for (int e = beg; e < end; ++e) {
           const int j = idx[e];
-          const float ex = softmax_exp2(head_dot<DH>(q, ks + j * 16 + hh * DH) - mu);
+          const float ex = softmax_exp2(head_dot<DH>(q, ks + j * KVS + hh * DH) - mu);
           S_ = S_ + ex;
-          const float *vr = vs + j * 16 + hh * DH;
+          const float *vr = vs + j * KVS + hh * DH;
 #pragma unroll
           for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
         }
@@ -675,7 +679,7 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
   return hipGetLastError();
 }
 
-size_t qkv_attention_lds(const Model &M) { return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)3 * M.L * 16 * 4; }
+size_t qkv_attention_lds(const Model &M) { return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + 2 * 20) * 4; }
 
 bool qkv_attention_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && qkv_attention_lds(M) <= 160 * 1024;
