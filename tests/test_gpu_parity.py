@@ -343,3 +343,30 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
     assert dec.path == P.PATH_LAYERED
     bits, logits = dec.decode(_dev(y))
     _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+@pytest.mark.parametrize("m,n,hf,attention,with_pos", [
+    (6, 14, 4, "hpsa", False),     # L = 20: two token tiles
+    (9, 23, 2, "hpsa", True),      # L = 32: two full tiles
+    (11, 22, 4, "casa", False),    # L = 33: three tiles, one token in the last
+    (20, 40, 6, "hpsa", False),    # L = 60: four tiles
+    (22, 42, 4, "hpsa", True),     # L = 64: four full tiles, the largest the kernel takes
+    (30, 34, 0, "hpsa", False),    # L = 64, n = 34 variables, all heads second-ring
+    (3, 5, 8, "hpsa", False),      # L = 8: one partial tile, all heads first-ring
+])
+def test_fused_kernel_tile_counts(P, oracle_mod, m, n, hf, attention, with_pos):
+    """The single-wave kernel at every token-tile count it instantiates (1 to 4 tiles of 16),
+    on random parity-check matrices, against the oracle; the layered path must agree too."""
+    from workloads import random_weights
+    print(f"[tiles] m {m} n {n} hf {hf} {attention} pos {with_pos}", flush=True)
+    H = _random_parity_check(m, n, seed=7 * m + n, col_weight=min(3, m))
+    w = random_weights(n, m, 32, 3, 8, seed=m + 3 * n, first_ring_heads=hf, attention=attention,
+                       with_pos=with_pos)
+    rng = np.random.default_rng(m * n)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (301, n)) + 0.7 * rng.standard_normal((301, n))).astype(np.float32)
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
+    fused = P.Decoder(H, w, path=P.PATH_FUSED)
+    assert fused.path == P.PATH_FUSED
+    for dec in (fused, P.Decoder(H, w, path=P.PATH_LAYERED)):
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
