@@ -64,7 +64,10 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 struct Plan {
   size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
-  struct Layer { size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b; };
+  struct Layer {
+    size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b;
+    size_t o8, ff1_8, ff2_8;   // the same O, FF1, FF2 fragments unpacked to int8 (token block), or 0
+  };
   std::vector<Layer> layer;
 };
 
@@ -99,6 +102,11 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
     q.ln1_b = take(sizeof(float) * d);
     q.ln2_g = take(sizeof(float) * d);
     q.ln2_b = take(sizeof(float) * d);
+    if (d == 64) {   // the token block's int8 fragments
+      q.o8 = take(8 * packed_words(d, d));
+      q.ff1_8 = take(8 * packed_words(d, dff));
+      q.ff2_8 = take(8 * packed_words(dff, d));
+    }
   }
   p.total = off;
   return p;
@@ -587,6 +595,20 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     pack_map(d, d, [&](int k, int j) { return Wo[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.o));
     pack_map(d, dff, [&](int k, int j) { return W1[(size_t)k * F + j]; }, (uint16_t *)(img.data() + q.ff1));
     pack_map(dff, d, [&](int k, int j) { return W2[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.ff2));
+    if (q.o8) {   // unpacked copies: 8 int8 bytes per lane and block, byte e = code e
+      auto unpack = [&](size_t src, size_t dst, size_t words) {
+        const uint16_t *in = (const uint16_t *)(img.data() + src);
+        int8_t *outb = (int8_t *)(img.data() + dst);
+        for (size_t u = 0; u < words; ++u)
+          for (int e = 0; e < 8; ++e) {
+            const int c = (in[u] >> (2 * e)) & 3;
+            outb[8 * u + e] = (int8_t)(c == 1 ? 1 : (c == 3 ? -1 : 0));
+          }
+      };
+      unpack(q.o, q.o8, packed_words(d, d));
+      unpack(q.ff1, q.ff1_8, packed_words(d, dff));
+      unpack(q.ff2, q.ff2_8, packed_words(dff, d));
+    }
     {
       std::vector<float> bqs(D);
       for (size_t c = 0; c < D; ++c) bqs[c] = w->b_q[l * D + c] * M.kq;   // scaled query bias
@@ -649,6 +671,9 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     Lw.ln1_b = (const float *)(b + q.ln1_b);
     Lw.ln2_g = (const float *)(b + q.ln2_g);
     Lw.ln2_b = (const float *)(b + q.ln2_b);
+    Lw.o8 = q.o8 ? (const uint64_t *)(b + q.o8) : nullptr;
+    Lw.ff1_8 = q.ff1_8 ? (const uint64_t *)(b + q.ff1_8) : nullptr;
+    Lw.ff2_8 = q.ff2_8 ? (const uint64_t *)(b + q.ff2_8) : nullptr;
   }
   if (!FI.frag.empty()) {
     aecct::FusedTables &T = M.fused;
@@ -727,9 +752,14 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
         e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
         if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
       }
-      if (e == hipSuccess) e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
-      if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
-      if (e == hipSuccess) e = aecct::launch_ffn2_ln(M, l, gq, ag, x1, rows, x, xq, ax, s);
+      if (e != hipSuccess) break;
+      if (aecct::token_block_supported(M)) {
+        e = aecct::launch_token_block(M, l, oq, ao, x, rows, xq, ax, s);
+      } else {
+        e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
+        if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
+        if (e == hipSuccess) e = aecct::launch_ffn2_ln(M, l, gq, ag, x1, rows, x, xq, ax, s);
+      }
     }
     if (e == hipSuccess)
       e = aecct::launch_head(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, s);

@@ -70,6 +70,13 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
 // ------------------------------------------------------------------------------------------
 // EPI_QKV_MAP: one of the three maps of EPI_QKV per launch (out_f and bias pointing at the map's
 // columns, rows 3 NOUT apart, scale sq[0]), a third of the accumulators of the fused launch.
+// Orders this wavefront's LDS writes before its following LDS reads (and the reverse).
+__device__ __forceinline__ void wave_barrier_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3, EPI_QKV_MAP = 4 };
 
 struct GemmArgs {
@@ -468,6 +475,212 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
 }
 
 // ------------------------------------------------------------------------------------------
+// The token-local half of a layer in one kernel (d = 64): output projection, residual, LN1
+// (Eq. 3, Section 6), Eq. 2, FFN1 with ReLU, Eq. 2, FFN2, residual, LN2 and Eq. 2 of the next
+// layer's input.  One wavefront per 16-row strip, each map on v_mfma_i32_16x16x32_i8 with the
+// activations as the A operand and int8 weight fragments (staged in LDS once per block) as B, with the
+// same epilogues and evaluation order as k_gemm's EPI_LN / EPI_RELU_QUANT; between maps the
+// int8 codes go through a per-wavefront LDS transpose.  The FFN1 scale needs a row's 4 d ReLU
+// outputs, so that map runs twice: once for the row maxima, once (recomputed, identical) to
+// quantise.  No block barrier: wavefronts are independent.
+// ------------------------------------------------------------------------------------------
+struct TokenBlockArgs {
+  const int8_t *oq;             // [rows][d] Eq. 2 codes of the attention output
+  const float *ao;              // [rows]
+  float *x;                     // [rows][d] layer input (residual); overwritten with the output
+  const uint64_t *bo, *b1, *b2; // int8 B fragments of O [d][d], FF1 [d][4d], FF2 [4d][d]
+  const float *bias_o, *bias_1, *bias_2, *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  float sq_o, sq_1, sq_2, eps;
+  int64_t rows;
+  int8_t *xq;                   // [rows][d] Eq. 2 codes of the output
+  float *ax;                    // [rows]
+};
+
+constexpr int kTbWaves = 8;
+
+// Dynamic LDS: the three maps' int8 fragments (staged once per block; 36 KB at d = 64), then
+// one 16 x 4d byte transpose stage per wavefront.
+template <int D>
+constexpr size_t token_block_lds() {
+  return (size_t)(D * D + 2 * D * 4 * D) + (size_t)kTbWaves * 16 * 4 * D;
+}
+
+template <int D>
+__global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
+  constexpr int S = D / 32, T = D / 16, S4 = 4 * D / 32, T4 = 4 * D / 16;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint64_t *lbo = (uint64_t *)smem, *lb1 = lbo + D * D / 8, *lb2 = lb1 + 4 * D * D / 8;
+  for (int u = threadIdx.x; u < D * D / 8; u += kTbWaves * 64) lbo[u] = p.bo[u];
+  for (int u = threadIdx.x; u < 4 * D * D / 8; u += kTbWaves * 64) {
+    lb1[u] = p.b1[u];
+    lb2[u] = p.b2[u];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, rg = lane >> 4;
+  int8_t *stg = (int8_t *)(smem + (size_t)(D * D + 2 * D * 4 * D) + (size_t)wave * 16 * 4 * D);
+  const int64_t nstrips = (p.rows + 15) / 16;
+  for (int64_t strip = (int64_t)blockIdx.x * kTbWaves + wave; strip < nstrips;
+       strip += (int64_t)gridDim.x * kTbWaves) {
+    const int64_t row0 = strip * 16;
+    int64_t r[4];
+    bool ok[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[i] = row0 + 4 * rg + i;
+      ok[i] = r[i] < p.rows;
+    }
+    // ---- output projection, residual, LN1 ----
+    float x1[T][4], a1[4];
+    {
+      long afr[S];
+      const int64_t ra = row0 + col;
+#pragma unroll
+      for (int s = 0; s < S; ++s) afr[s] = ra < p.rows ? *(const long *)(p.oq + ra * D + 32 * s + 8 * rg) : 0;
+      v4i acc[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        acc[t] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc[t] = mfma_i8_16x16x32(afr[s], (long)lbo[(t * S + s) * 64 + lane], acc[t]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sc = (ok[i] ? p.ao[r[i]] : 0.0f) * p.sq_o;
+        float v[T], e[T], sq[T], tmp[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          const float y = __builtin_fmaf((float)acc[t][i], sc, p.bias_o[j]);
+          const float res = ok[i] ? p.x[r[i] * D + j] : 0.0f;
+          v[t] = res + y;
+          tmp[t] = v[t];
+        }
+        const float mean = row16_sum(lane_tree<T>(tmp)) / (float)D;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          e[t] = v[t] - mean;
+          sq[t] = e[t] * e[t];
+        }
+        const float var = row16_sum(lane_tree<T>(sq)) / (float)D;
+        const float rho = ln_rsqrt(var + p.eps);
+        float amax = 0.0f;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          x1[t][i] = __builtin_fmaf(e[t] * rho, p.ln1_g[j], p.ln1_b[j]);
+          amax = fmaxf(amax, fabsf(x1[t][i]));
+        }
+        amax = row16_max(amax);
+        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+        for (int t = 0; t < T; ++t) stg[(4 * rg + i) * D + 16 * t + col] = quant_code(x1[t][i], inv);
+        a1[i] = amax;
+      }
+    }
+    wave_barrier_lds();
+    // ---- FFN1 with ReLU; Eq. 2 over the 4 d outputs of a row ----
+    float ag[4];
+    {
+      long afr[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) afr[s] = *(const long *)(stg + col * D + 32 * s + 8 * rg);
+      wave_barrier_lds();
+      float sc[4], am[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sc[i] = a1[i] * p.sq_1;
+#pragma unroll 2
+      for (int t = 0; t < T4; ++t) {                       // pass 1: row maxima
+        v4i acc = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32(afr[s], (long)lb1[(t * S + s) * 64 + lane], acc);
+        const float b = p.bias_1[16 * t + col];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float f = __builtin_fmaf((float)acc[i], sc[i], b);
+          am[i] = fmaxf(am[i], f > 0.0f ? f : 0.0f);
+        }
+      }
+      float inv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        am[i] = row16_max(am[i]);
+        inv[i] = am[i] == 0.0f ? 0.0f : 127.0f / am[i];
+        ag[i] = am[i];
+      }
+#pragma unroll 2
+      for (int t = 0; t < T4; ++t) {                       // pass 2: the same values, quantised
+        v4i acc = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32(afr[s], (long)lb1[(t * S + s) * 64 + lane], acc);
+        const float b = p.bias_1[16 * t + col];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float f = __builtin_fmaf((float)acc[i], sc[i], b);
+          stg[(4 * rg + i) * (4 * D) + 16 * t + col] = quant_code(f > 0.0f ? f : 0.0f, inv[i]);
+        }
+      }
+    }
+    wave_barrier_lds();
+    // ---- FFN2, residual, LN2, Eq. 2 of the next layer's input ----
+    {
+      v4i acc[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t] = v4i{0, 0, 0, 0};
+#pragma unroll 1
+      for (int s = 0; s < S4; ++s) {        // k-steps outermost: one A fragment live at a time
+        const long af = *(const long *)(stg + col * (4 * D) + 32 * s + 8 * rg);
+#pragma unroll
+        for (int t = 0; t < T; ++t) acc[t] = mfma_i8_16x16x32(af, (long)lb2[(t * S4 + s) * 64 + lane], acc[t]);
+      }
+      wave_barrier_lds();
+      float amx[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sc = ag[i] * p.sq_2;
+        float v[T], e[T], sq[T], tmp[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const float y = __builtin_fmaf((float)acc[t][i], sc, p.bias_2[16 * t + col]);
+          v[t] = x1[t][i] + y;
+          tmp[t] = v[t];
+        }
+        const float mean = row16_sum(lane_tree<T>(tmp)) / (float)D;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          e[t] = v[t] - mean;
+          sq[t] = e[t] * e[t];
+        }
+        const float var = row16_sum(lane_tree<T>(sq)) / (float)D;
+        const float rho = ln_rsqrt(var + p.eps);
+        float amax = 0.0f;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          v[t] = __builtin_fmaf(e[t] * rho, p.ln2_g[j], p.ln2_b[j]);
+          if (ok[i]) p.x[r[i] * D + j] = v[t];
+          amax = fmaxf(amax, fabsf(v[t]));
+        }
+        amax = row16_max(amax);
+        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+        for (int t = 0; t < T; ++t) stg[(4 * rg + i) * D + 16 * t + col] = quant_code(v[t], inv);
+        amx[i] = amax;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (col == 0 && ok[i]) p.ax[r[i]] = amx[i];
+      wave_barrier_lds();
+      const int64_t valid = p.rows - row0 < 16 ? p.rows - row0 : 16;
+      const int chunks = (int)(valid * D / 16);
+      const uint4 *src = (const uint4 *)stg;
+      uint4 *dst = (uint4 *)(p.xq + row0 * D);
+      for (int c = lane; c < chunks; c += 64) dst[c] = src[c];
+      wave_barrier_lds();
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // Output head and hard decision (Section 3): one block per word.  z_i = W_{d->1} x_i + b1
 // (16 lanes per token, pairwise over features), then f_o = sum_i z_i W_o[i][o] + b_o in
 // ascending token order, bit = [y < 0] xor [f < 0].
@@ -730,6 +943,53 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   const dim3 grid((unsigned)((rows + 15) / 16));
   if (M.d == 64) hipLaunchKernelGGL(k_quant_rows<64>, grid, dim3(256), 0, s, o, rows, oq, ao);
   else hipLaunchKernelGGL(k_quant_rows<128>, grid, dim3(256), 0, s, o, rows, oq, ao);
+  return hipGetLastError();
+}
+
+// d = 64 only: there the three maps (36 KB of int8) stay in LDS; at d = 128 (144 KB) they would
+// stream from L2 for every strip, which measured slower than the separate GEMMs.
+bool token_block_supported(const Model &M) {
+  return M.d == 64 && M.dff == 4 * M.d && M.layer[0].o8 != nullptr;
+}
+
+hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const float *ao, float *x,
+                              int64_t rows, int8_t *xq, float *ax, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (!token_block_supported(M)) return hipErrorInvalidValue;
+  const LayerWeights &W = M.layer[layer];
+  TokenBlockArgs a{};
+  a.oq = oq;
+  a.ao = ao;
+  a.x = x;
+  a.bo = W.o8;
+  a.b1 = W.ff1_8;
+  a.b2 = W.ff2_8;
+  a.bias_o = W.b_o;
+  a.bias_1 = W.b_ff1;
+  a.bias_2 = W.b_ff2;
+  a.ln1_g = W.ln1_g;
+  a.ln1_b = W.ln1_b;
+  a.ln2_g = W.ln2_g;
+  a.ln2_b = W.ln2_b;
+  a.sq_o = W.sq[3];    // aecct_linear order: q, k, v, o, ff1, ff2
+  a.sq_1 = W.sq[4];
+  a.sq_2 = W.sq[5];
+  a.eps = M.eps;
+  a.rows = rows;
+  a.xq = xq;
+  a.ax = ax;
+  const int64_t strips = (rows + 15) / 16;
+  constexpr size_t lds = token_block_lds<64>();
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_token_block<64>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, 256 * per_cu);
+  hipLaunchKernelGGL(k_token_block<64>, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
   return hipGetLastError();
 }
 
