@@ -51,19 +51,10 @@ struct FusedArgs {
 
 namespace {
 
-// Butterfly steps across lane xor 32 and lane xor 16: ds_bpermute through the LDS crossbar
-// (default, measured faster here), or, with AECCT_XLANE_SWAP, the gfx950 lane-swap
-// instructions: swapping v with a copy of itself leaves, in the two results, v of the lane
-// and of its partner (in an order that depends on the half); sum and maximum commute, so
-// every lane gets the same bits.  The copy goes through an opaque move so that the compiler
-// cannot treat the two swap results as the same value.
-__device__ __forceinline__ uint32_t opaque_copy(uint32_t v) {
-  uint32_t w;
-  asm volatile("v_mov_b32 %0, %1" : "=v"(w) : "v"(v));
-  return w;
-}
-#if !defined(AECCT_XLANE_SWAP)
-// v of lane (this lane xor m), m = 16 or 32: a whole-wave permute, byte address 4 (lane ^ m)
+// Butterfly steps across lane xor 32 and lane xor 16 through ds_bpermute (the LDS crossbar;
+// measured faster here than the gfx950 lane-swap instructions).  Sum and maximum commute, so
+// both lanes of a pair get the same bits.
+// v of lane (this lane xor M), M = 16 or 32: a whole-wave permute, byte address 4 (lane ^ M)
 template <int M>
 __device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((__builtin_amdgcn_workitem_id_x() & 63u) ^ M) << 2), (int)v);
@@ -76,26 +67,6 @@ __device__ __forceinline__ float pair_sum16(float v) {
 }
 __device__ __forceinline__ uint32_t pair_max32(uint32_t v) { return max(v, lane_xor<32>(v)); }
 __device__ __forceinline__ uint32_t pair_max16(uint32_t v) { return max(v, lane_xor<16>(v)); }
-#else
-__device__ __forceinline__ float pair_sum32(float v) {
-  const uint32_t u = __builtin_bit_cast(uint32_t, v);
-  const auto r = __builtin_amdgcn_permlane32_swap(u, opaque_copy(u), false, false);
-  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
-}
-__device__ __forceinline__ float pair_sum16(float v) {
-  const uint32_t u = __builtin_bit_cast(uint32_t, v);
-  const auto r = __builtin_amdgcn_permlane16_swap(u, opaque_copy(u), false, false);
-  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
-}
-__device__ __forceinline__ uint32_t pair_max32(uint32_t v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(v, opaque_copy(v), false, false);
-  return max((uint32_t)r[0], (uint32_t)r[1]);
-}
-__device__ __forceinline__ uint32_t pair_max16(uint32_t v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(v, opaque_copy(v), false, false);
-  return max((uint32_t)r[0], (uint32_t)r[1]);
-}
-#endif
 
 // Pairwise sum over a token's 32 features held as x[v] = feature 4 v + g.
 __device__ __forceinline__ float token_sum(const float (&x)[8]) {
