@@ -37,7 +37,10 @@ struct LayerWeights {
   const uint16_t *o;     // [d][d]
   const uint16_t *ff1;   // [d][d_ff]
   const uint16_t *ff2;   // [d_ff][d]
-  const uint64_t *o8, *ff1_8, *ff2_8;   // O, FF1, FF2 blocks unpacked to int8 (d = 64), else null
+  // token block (d = 64, 128): O, FF1, FF2 as permuted int8 A fragments and six d-vectors
+  // (b_o, ln1_g, ln1_b, b_ff2, ln2_g, ln2_b) in lane order; null otherwise
+  const uint64_t *tb_o, *tb_1, *tb_2;
+  const float *tb_vec;
   const float *b_qkv;    // [3d]; the query third pre-multiplied by the score scale (see Model::kq)
   const float *b_o, *b_ff1, *b_ff2;
   const float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
@@ -97,7 +100,7 @@ bool qkv_attention_supported(const Model &M);
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                 float *o, int8_t *oq, float *ao, hipStream_t s);
 // O-projection, residual, LN1, FFN with ReLU, residual, LN2 and Eq. 2 of the next layer's
-// input in one kernel (d = 64): one wavefront per 16-token strip, activations between
+// input in one kernel (d = 64, 128): one wavefront per 16-token strip, activations between
 // the maps only in registers and a per-wavefront LDS transpose.
 bool token_block_supported(const Model &M);
 hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const float *ao, float *x,

@@ -66,7 +66,7 @@ struct Plan {
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
   struct Layer {
     size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b;
-    size_t o8, ff1_8, ff2_8;   // the same O, FF1, FF2 fragments unpacked to int8 (token block), or 0
+    size_t tb_o, tb_1, tb_2, tb_vec;   // token-block fragments and lane-order vectors (d = 64, 128), or 0
   };
   std::vector<Layer> layer;
 };
@@ -102,10 +102,11 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
     q.ln1_b = take(sizeof(float) * d);
     q.ln2_g = take(sizeof(float) * d);
     q.ln2_b = take(sizeof(float) * d);
-    if (d == 64) {   // the token block's int8 fragments
-      q.o8 = take(8 * packed_words(d, d));
-      q.ff1_8 = take(8 * packed_words(d, dff));
-      q.ff2_8 = take(8 * packed_words(dff, d));
+    if ((d == 64 || d == 128) && dff == 4 * d) {   // the token block's int8 A fragments
+      q.tb_o = take((size_t)d * d);
+      q.tb_1 = take((size_t)d * dff);
+      q.tb_2 = take((size_t)dff * d);
+      q.tb_vec = take(sizeof(float) * 6 * d);
     }
   }
   p.total = off;
@@ -595,19 +596,35 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     pack_map(d, d, [&](int k, int j) { return Wo[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.o));
     pack_map(d, dff, [&](int k, int j) { return W1[(size_t)k * F + j]; }, (uint16_t *)(img.data() + q.ff1));
     pack_map(dff, d, [&](int k, int j) { return W2[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.ff2));
-    if (q.o8) {   // unpacked copies: 8 int8 bytes per lane and block, byte e = code e
-      auto unpack = [&](size_t src, size_t dst, size_t words) {
-        const uint16_t *in = (const uint16_t *)(img.data() + src);
-        int8_t *outb = (int8_t *)(img.data() + dst);
-        for (size_t u = 0; u < words; ++u)
-          for (int e = 0; e < 8; ++e) {
-            const int c = (in[u] >> (2 * e)) & 3;
-            outb[8 * u + e] = (int8_t)(c == 1 ? 1 : (c == 3 ? -1 : 0));
-          }
+    if (q.tb_o) {
+      // Token block (transposed products: weights are the A operand, 16 tokens the columns).
+      // A fragment (tile t, step s): lane l holds output row l & 15 and k-slots 8 (l >> 4) + e
+      // in byte e.  Lane layout of d-wide activations: lane group g holds feature 4 v + g in
+      // register v.  O and FF2 output row r of tile t is feature 16 t + 4 (r & 3) + (r >> 2)
+      // (lane group g then holds v = 4 t + i); FF1 reads slot k of step s as feature
+      // 32 s + 4 (k & 7) + (k >> 3) (the 8 codes lane group g packs for step s); FF1's outputs
+      // keep their order and FF2 reads slot k of step s as hidden feature
+      // 16 (2 s + ((k & 7) >> 2)) + 4 (k >> 3) + (k & 3).
+      auto pack_a = [&](size_t dst, int T, int S, auto get) {
+        int8_t *o8 = (int8_t *)(img.data() + dst);
+        for (int t = 0; t < T; ++t)
+          for (int st = 0; st < S; ++st)
+            for (int l = 0; l < 64; ++l)
+              for (int e = 0; e < 8; ++e) o8[(((size_t)t * S + st) * 64 + l) * 8 + e] = get(t, st, l & 15, 8 * (l >> 4) + e);
       };
-      unpack(q.o, q.o8, packed_words(d, d));
-      unpack(q.ff1, q.ff1_8, packed_words(d, dff));
-      unpack(q.ff2, q.ff2_8, packed_words(dff, d));
+      auto out_x = [](int t, int r) { return 16 * t + 4 * (r & 3) + (r >> 2); };
+      auto in_x = [](int st, int k) { return 32 * st + 4 * (k & 7) + (k >> 3); };
+      auto in_h = [](int st, int k) { return 16 * (2 * st + ((k & 7) >> 2)) + 4 * (k >> 3) + (k & 3); };
+      pack_a(q.tb_o, d / 16, d / 32, [&](int t, int st, int r, int k) { return Wo[(size_t)(32 * st + k) * D + out_x(t, r)]; });
+      pack_a(q.tb_1, dff / 16, d / 32, [&](int t, int st, int r, int k) { return W1[(size_t)in_x(st, k) * F + 16 * t + r]; });
+      pack_a(q.tb_2, d / 16, dff / 32, [&](int t, int st, int r, int k) { return W2[(size_t)in_h(st, k) * D + out_x(t, r)]; });
+      // b_o, ln1_g, ln1_b, b_ff2, ln2_g, ln2_b in lane order: [vector][g][v] = vector[4 v + g]
+      float *vx = (float *)(img.data() + q.tb_vec);
+      const float *srcs[6] = {w->b_o + l * D, w->ln1_g + l * D, w->ln1_b + l * D, w->b_ff2 + l * D,
+                              w->ln2_g + l * D, w->ln2_b + l * D};
+      for (int k = 0; k < 6; ++k)
+        for (int g = 0; g < 4; ++g)
+          for (int v = 0; v < d / 4; ++v) vx[(size_t)k * d + g * (d / 4) + v] = srcs[k][4 * v + g];
     }
     {
       std::vector<float> bqs(D);
@@ -671,9 +688,10 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     Lw.ln1_b = (const float *)(b + q.ln1_b);
     Lw.ln2_g = (const float *)(b + q.ln2_g);
     Lw.ln2_b = (const float *)(b + q.ln2_b);
-    Lw.o8 = q.o8 ? (const uint64_t *)(b + q.o8) : nullptr;
-    Lw.ff1_8 = q.ff1_8 ? (const uint64_t *)(b + q.ff1_8) : nullptr;
-    Lw.ff2_8 = q.ff2_8 ? (const uint64_t *)(b + q.ff2_8) : nullptr;
+    Lw.tb_o = q.tb_o ? (const uint64_t *)(b + q.tb_o) : nullptr;
+    Lw.tb_1 = q.tb_1 ? (const uint64_t *)(b + q.tb_1) : nullptr;
+    Lw.tb_2 = q.tb_2 ? (const uint64_t *)(b + q.tb_2) : nullptr;
+    Lw.tb_vec = q.tb_vec ? (const float *)(b + q.tb_vec) : nullptr;
   }
   if (!FI.frag.empty()) {
     aecct::FusedTables &T = M.fused;

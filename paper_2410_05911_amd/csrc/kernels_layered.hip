@@ -475,21 +475,28 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
 }
 
 // ------------------------------------------------------------------------------------------
-// The token-local half of a layer in one kernel (d = 64): output projection, residual, LN1
-// (Eq. 3, Section 6), Eq. 2, FFN1 with ReLU, Eq. 2, FFN2, residual, LN2 and Eq. 2 of the next
-// layer's input.  One wavefront per 16-row strip, each map on v_mfma_i32_16x16x32_i8 with the
-// activations as the A operand and int8 weight fragments (staged in LDS once per block) as B, with the
-// same epilogues and evaluation order as k_gemm's EPI_LN / EPI_RELU_QUANT; between maps the
-// int8 codes go through a per-wavefront LDS transpose.  The FFN1 scale needs a row's 4 d ReLU
-// outputs, so that map runs twice: once for the row maxima, once (recomputed, identical) to
-// quantise.  No block barrier: wavefronts are independent.
+// The token-local half of a layer in one kernel (d = 64, 128): output projection, residual,
+// LN1 (Eq. 3, Section 6), Eq. 2, FFN1 with ReLU, Eq. 2, FFN2, residual, LN2 and Eq. 2 of the
+// next layer's input.  One wavefront per 16-token strip.  The products run transposed on
+// v_mfma_i32_16x16x32_i8 (weights are the A operand, from LDS; the strip's 16 tokens are the
+// columns), so lane (c, g) = (lane & 15, lane >> 4) holds, for token c, the d-wide activations
+// as register v = feature 4 v + g.  The host permutes the fragments' rows and k-slots so that
+// (a) the O and FF2 outputs land in that layout, (b) the 8 codes a lane quantises for k-step s
+// are exactly its B-operand bytes for FF1, and (c) two FF1 output tiles give exactly the
+// B-operand bytes of one FF2 k-step: no activation leaves registers between the maps.  FF1 runs
+// twice: once for the rows' ReLU maxima (the Eq. 2 scale of the hidden row), once (identical
+// values) to quantise, each pair of tiles feeding FF2 at once.  LayerNorm sums are the
+// pairwise order (in-lane over v, then lanes xor 32, xor 16); epilogues and evaluation order
+// are those of k_gemm's EPI_LN / EPI_RELU_QUANT.  Only the next layer's codes go through LDS,
+// to be written in row order.  No block barrier after the weight staging.
 // ------------------------------------------------------------------------------------------
 struct TokenBlockArgs {
   const int8_t *oq;             // [rows][d] Eq. 2 codes of the attention output
   const float *ao;              // [rows]
   float *x;                     // [rows][d] layer input (residual); overwritten with the output
-  const uint64_t *bo, *b1, *b2; // int8 B fragments of O [d][d], FF1 [d][4d], FF2 [4d][d]
-  const float *bias_o, *bias_1, *bias_2, *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  const uint64_t *fo, *f1, *f2; // permuted A fragments of O, FF1, FF2
+  const float *vec;             // [6][4][d/4] b_o, ln1_g, ln1_b, b_ff2, ln2_g, ln2_b in lane order
+  const float *b1;              // [4d] FF1 bias
   float sq_o, sq_1, sq_2, eps;
   int64_t rows;
   int8_t *xq;                   // [rows][d] Eq. 2 codes of the output
@@ -498,185 +505,199 @@ struct TokenBlockArgs {
 
 constexpr int kTbWaves = 8;
 
-// Dynamic LDS: the three maps' int8 fragments (staged once per block; 36 KB at d = 64), then
-// one 16 x 4d byte transpose stage per wavefront.
+// d = 64 also keeps the six d-vectors and the FF1 bias in LDS (at d = 128 the fragments fill it).
 template <int D>
-constexpr size_t token_block_lds() {
-  return (size_t)(D * D + 2 * D * 4 * D) + (size_t)kTbWaves * 16 * 4 * D;
+constexpr bool tb_lds_vectors() { return D == 64; }
+
+template <int D>
+constexpr size_t token_block_lds() {   // fragments, per-wave 16 x d stages, [vectors, FF1 bias]
+  return (size_t)9 * D * D + (size_t)kTbWaves * 16 * D + (tb_lds_vectors<D>() ? (size_t)10 * D * 4 : 0);
+}
+
+// v of lane (this lane xor M), M = 16 or 32
+template <int M>
+__device__ __forceinline__ uint32_t tb_lane_xor(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((__builtin_amdgcn_workitem_id_x() & 63u) ^ M) << 2), (int)v);
+}
+// Pairwise sum of a token's d features held as x[v] = feature 4 v + g.
+template <int V>
+__device__ __forceinline__ float tb_token_sum(const float (&x)[V]) {
+  float u[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) u[v] = x[v];
+  float t = lane_tree<V>(u);
+  t = t + __builtin_bit_cast(float, tb_lane_xor<32>(__builtin_bit_cast(uint32_t, t)));
+  return t + __builtin_bit_cast(float, tb_lane_xor<16>(__builtin_bit_cast(uint32_t, t)));
+}
+// Maximum over the four lanes of a token (non-negative floats order like their bit patterns).
+__device__ __forceinline__ float tb_token_max(float a) {
+  uint32_t u = __builtin_bit_cast(uint32_t, a);
+  u = max(u, tb_lane_xor<32>(u));
+  u = max(u, tb_lane_xor<16>(u));
+  return __builtin_bit_cast(float, u);
+}
+// Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
+__device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
+  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
+  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
+  return (long)(((uint64_t)hi << 32) | lo);
 }
 
 template <int D>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
-  constexpr int S = D / 32, T = D / 16, S4 = 4 * D / 32, T4 = 4 * D / 16;
+  constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint64_t *lbo = (uint64_t *)smem, *lb1 = lbo + D * D / 8, *lb2 = lb1 + 4 * D * D / 8;
-  for (int u = threadIdx.x; u < D * D / 8; u += kTbWaves * 64) lbo[u] = p.bo[u];
-  for (int u = threadIdx.x; u < 4 * D * D / 8; u += kTbWaves * 64) {
-    lb1[u] = p.b1[u];
-    lb2[u] = p.b2[u];
+  uint64_t *fo = (uint64_t *)smem, *f1 = fo + (size_t)TO * S * 64, *f2 = f1 + (size_t)TH * S * 64;
+  for (int u = threadIdx.x; u < TO * S * 64; u += kTbWaves * 64) fo[u] = p.fo[u];
+  for (int u = threadIdx.x; u < TH * S * 64; u += kTbWaves * 64) f1[u] = p.f1[u];
+  for (int u = threadIdx.x; u < TO * SH * 64; u += kTbWaves * 64) f2[u] = p.f2[u];
+  const float *vec = p.vec, *bias1 = p.b1;
+  if constexpr (tb_lds_vectors<D>()) {
+    float *lv = (float *)(smem + (size_t)9 * D * D + (size_t)kTbWaves * 16 * D);
+    for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
+    for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
+    vec = lv;
+    bias1 = lv + 6 * D;
   }
   __syncthreads();
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, rg = lane >> 4;
-  int8_t *stg = (int8_t *)(smem + (size_t)(D * D + 2 * D * 4 * D) + (size_t)wave * 16 * 4 * D);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
+  int8_t *stg = (int8_t *)(smem + (size_t)9 * D * D) + (size_t)wave * 16 * D;
+  const float *vb_o = vec + 0 * D + g * V, *vg1 = vec + 1 * D + g * V, *vb1 = vec + 2 * D + g * V;
+  const float *vb_2 = vec + 3 * D + g * V, *vg2 = vec + 4 * D + g * V, *vbb2 = vec + 5 * D + g * V;
   const int64_t nstrips = (p.rows + 15) / 16;
   for (int64_t strip = (int64_t)blockIdx.x * kTbWaves + wave; strip < nstrips;
        strip += (int64_t)gridDim.x * kTbWaves) {
-    const int64_t row0 = strip * 16;
-    int64_t r[4];
-    bool ok[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      r[i] = row0 + 4 * rg + i;
-      ok[i] = r[i] < p.rows;
-    }
-    // ---- output projection, residual, LN1 ----
-    float x1[T][4], a1[4];
+    const int64_t row0 = strip * 16, tok = row0 + c;
+    const bool ok = tok < p.rows;
+    // ---- output projection, residual, LN1, Eq. 2 ----
+    float x1[V];
+    long xb[S];
+    float a1;
     {
-      long afr[S];
-      const int64_t ra = row0 + col;
+      long bq[S];
 #pragma unroll
-      for (int s = 0; s < S; ++s) afr[s] = ra < p.rows ? *(const long *)(p.oq + ra * D + 32 * s + 8 * rg) : 0;
-      v4i acc[T];
+      for (int s = 0; s < S; ++s) bq[s] = ok ? *(const long *)(p.oq + tok * D + 32 * s + 8 * g) : 0;
+      const float sc = (ok ? p.ao[tok] : 0.0f) * p.sq_o;
 #pragma unroll
-      for (int t = 0; t < T; ++t) {
-        acc[t] = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) acc[t] = mfma_i8_16x16x32(afr[s], (long)lbo[(t * S + s) * 64 + lane], acc[t]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float sc = (ok[i] ? p.ao[r[i]] : 0.0f) * p.sq_o;
-        float v[T], e[T], sq[T], tmp[T];
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          const int j = 16 * t + col;
-          const float y = __builtin_fmaf((float)acc[t][i], sc, p.bias_o[j]);
-          const float res = ok[i] ? p.x[r[i] * D + j] : 0.0f;
-          v[t] = res + y;
-          tmp[t] = v[t];
-        }
-        const float mean = row16_sum(lane_tree<T>(tmp)) / (float)D;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          e[t] = v[t] - mean;
-          sq[t] = e[t] * e[t];
-        }
-        const float var = row16_sum(lane_tree<T>(sq)) / (float)D;
-        const float rho = ln_rsqrt(var + p.eps);
-        float amax = 0.0f;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          const int j = 16 * t + col;
-          x1[t][i] = __builtin_fmaf(e[t] * rho, p.ln1_g[j], p.ln1_b[j]);
-          amax = fmaxf(amax, fabsf(x1[t][i]));
-        }
-        amax = row16_max(amax);
-        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
-#pragma unroll
-        for (int t = 0; t < T; ++t) stg[(4 * rg + i) * D + 16 * t + col] = quant_code(x1[t][i], inv);
-        a1[i] = amax;
-      }
-    }
-    wave_barrier_lds();
-    // ---- FFN1 with ReLU; Eq. 2 over the 4 d outputs of a row ----
-    float ag[4];
-    {
-      long afr[S];
-#pragma unroll
-      for (int s = 0; s < S; ++s) afr[s] = *(const long *)(stg + col * D + 32 * s + 8 * rg);
-      wave_barrier_lds();
-      float sc[4], am[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sc[i] = a1[i] * p.sq_1;
-#pragma unroll 2
-      for (int t = 0; t < T4; ++t) {                       // pass 1: row maxima
+      for (int o = 0; o < TO; ++o) {
         v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
-        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32(afr[s], (long)lb1[(t * S + s) * 64 + lane], acc);
-        const float b = p.bias_1[16 * t + col];
+        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)fo[(o * S + s) * 64 + lane], bq[s], acc);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float f = __builtin_fmaf((float)acc[i], sc[i], b);
-          am[i] = fmaxf(am[i], f > 0.0f ? f : 0.0f);
+          const int v = 4 * o + i;
+          const float y = __builtin_fmaf((float)acc[i], sc, vb_o[v]);
+          const float res = ok ? p.x[tok * D + 4 * v + g] : 0.0f;
+          x1[v] = res + y;
         }
       }
-      float inv[4];
+      const float mean = tb_token_sum<V>(x1) / (float)D;
+      float e[V], sq[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        e[v] = x1[v] - mean;
+        sq[v] = e[v] * e[v];
+      }
+      const float var = tb_token_sum<V>(sq) / (float)D;
+      const float rho = ln_rsqrt(var + p.eps);
+      float amax = 0.0f;
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        x1[v] = __builtin_fmaf(e[v] * rho, vg1[v], vb1[v]);
+        amax = fmaxf(amax, fabsf(x1[v]));
+      }
+      amax = tb_token_max(amax);
+      const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        uint32_t b[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) b[k] = quant_bits(x1[8 * s + k], inv);
+        xb[s] = tb_pack8(b);
+      }
+      a1 = amax;
+    }
+    // ---- FFN1 with ReLU (twice) feeding FFN2 ----
+    const float sc1 = a1 * p.sq_1;
+    float am = 0.0f;
+#pragma unroll 2
+    for (int o = 0; o < TH; ++o) {                          // pass 1: the row's ReLU maximum
+      v4i acc = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)f1[(o * S + s) * 64 + lane], xb[s], acc);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        am[i] = row16_max(am[i]);
-        inv[i] = am[i] == 0.0f ? 0.0f : 127.0f / am[i];
-        ag[i] = am[i];
-      }
-#pragma unroll 2
-      for (int t = 0; t < T4; ++t) {                       // pass 2: the same values, quantised
-        v4i acc = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32(afr[s], (long)lb1[(t * S + s) * 64 + lane], acc);
-        const float b = p.bias_1[16 * t + col];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float f = __builtin_fmaf((float)acc[i], sc[i], b);
-          stg[(4 * rg + i) * (4 * D) + 16 * t + col] = quant_code(f > 0.0f ? f : 0.0f, inv[i]);
-        }
+        const float f = __builtin_fmaf((float)acc[i], sc1, bias1[16 * o + 4 * g + i]);
+        am = fmaxf(am, f > 0.0f ? f : 0.0f);
       }
     }
-    wave_barrier_lds();
-    // ---- FFN2, residual, LN2, Eq. 2 of the next layer's input ----
-    {
-      v4i acc[T];
+    am = tb_token_max(am);
+    const float inv1 = am == 0.0f ? 0.0f : 127.0f / am;
+    v4i acc2[TO];
 #pragma unroll
-      for (int t = 0; t < T; ++t) acc[t] = v4i{0, 0, 0, 0};
+    for (int o = 0; o < TO; ++o) acc2[o] = v4i{0, 0, 0, 0};
 #pragma unroll 1
-      for (int s = 0; s < S4; ++s) {        // k-steps outermost: one A fragment live at a time
-        const long af = *(const long *)(stg + col * (4 * D) + 32 * s + 8 * rg);
+    for (int s2 = 0; s2 < SH; ++s2) {                       // pass 2: tiles 2 s2, 2 s2 + 1 -> FF2 step s2
+      v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
 #pragma unroll
-        for (int t = 0; t < T; ++t) acc[t] = mfma_i8_16x16x32(af, (long)lb2[(t * S4 + s) * 64 + lane], acc[t]);
+      for (int s = 0; s < S; ++s) {
+        h0 = mfma_i8_16x16x32((long)f1[((2 * s2) * S + s) * 64 + lane], xb[s], h0);
+        h1 = mfma_i8_16x16x32((long)f1[((2 * s2 + 1) * S + s) * 64 + lane], xb[s], h1);
       }
-      wave_barrier_lds();
-      float amx[4];
+      uint32_t b[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float sc = ag[i] * p.sq_2;
-        float v[T], e[T], sq[T], tmp[T];
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          const float y = __builtin_fmaf((float)acc[t][i], sc, p.bias_2[16 * t + col]);
-          v[t] = x1[t][i] + y;
-          tmp[t] = v[t];
-        }
-        const float mean = row16_sum(lane_tree<T>(tmp)) / (float)D;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          e[t] = v[t] - mean;
-          sq[t] = e[t] * e[t];
-        }
-        const float var = row16_sum(lane_tree<T>(sq)) / (float)D;
-        const float rho = ln_rsqrt(var + p.eps);
-        float amax = 0.0f;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          const int j = 16 * t + col;
-          v[t] = __builtin_fmaf(e[t] * rho, p.ln2_g[j], p.ln2_b[j]);
-          if (ok[i]) p.x[r[i] * D + j] = v[t];
-          amax = fmaxf(amax, fabsf(v[t]));
-        }
-        amax = row16_max(amax);
-        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
-#pragma unroll
-        for (int t = 0; t < T; ++t) stg[(4 * rg + i) * D + 16 * t + col] = quant_code(v[t], inv);
-        amx[i] = amax;
+        const float f0 = __builtin_fmaf((float)h0[i], sc1, bias1[16 * (2 * s2) + 4 * g + i]);
+        const float f1v = __builtin_fmaf((float)h1[i], sc1, bias1[16 * (2 * s2 + 1) + 4 * g + i]);
+        b[i] = quant_bits(f0 > 0.0f ? f0 : 0.0f, inv1);
+        b[4 + i] = quant_bits(f1v > 0.0f ? f1v : 0.0f, inv1);
       }
+      const long gb = tb_pack8(b);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (col == 0 && ok[i]) p.ax[r[i]] = amx[i];
-      wave_barrier_lds();
-      const int64_t valid = p.rows - row0 < 16 ? p.rows - row0 : 16;
-      const int chunks = (int)(valid * D / 16);
-      const uint4 *src = (const uint4 *)stg;
-      uint4 *dst = (uint4 *)(p.xq + row0 * D);
-      for (int c = lane; c < chunks; c += 64) dst[c] = src[c];
-      wave_barrier_lds();
+      for (int o = 0; o < TO; ++o) acc2[o] = mfma_i8_16x16x32((long)f2[(o * SH + s2) * 64 + lane], gb, acc2[o]);
     }
+    // ---- FFN2 epilogue: residual, LN2, Eq. 2 of the next layer's input ----
+    {
+      const float sc2 = am * p.sq_2;
+      float v2[V];
+#pragma unroll
+      for (int o = 0; o < TO; ++o)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int v = 4 * o + i;
+          v2[v] = x1[v] + __builtin_fmaf((float)acc2[o][i], sc2, vb_2[v]);
+        }
+      const float mean = tb_token_sum<V>(v2) / (float)D;
+      float e[V], sq[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        e[v] = v2[v] - mean;
+        sq[v] = e[v] * e[v];
+      }
+      const float var = tb_token_sum<V>(sq) / (float)D;
+      const float rho = ln_rsqrt(var + p.eps);
+      float amax = 0.0f;
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        v2[v] = __builtin_fmaf(e[v] * rho, vg2[v], vbb2[v]);
+        if (ok) p.x[tok * D + 4 * v + g] = v2[v];
+        amax = fmaxf(amax, fabsf(v2[v]));
+      }
+      amax = tb_token_max(amax);
+      const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+#pragma unroll
+      for (int v = 0; v < V; ++v) stg[c * D + 4 * v + g] = quant_code(v2[v], inv);
+      if (g == 0 && ok) p.ax[tok] = amax;
+    }
+    wave_barrier_lds();
+    const int64_t valid = p.rows - row0 < 16 ? p.rows - row0 : 16;
+    const int chunks = (int)(valid * D / 16);
+    const uint4 *src = (const uint4 *)stg;
+    uint4 *dst = (uint4 *)(p.xq + row0 * D);
+    for (int k = lane; k < chunks; k += 64) dst[k] = src[k];
+    wave_barrier_lds();
   }
 }
 
@@ -946,10 +967,25 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   return hipGetLastError();
 }
 
-// d = 64 only: there the three maps (36 KB of int8) stay in LDS; at d = 128 (144 KB) they would
-// stream from L2 for every strip, which measured slower than the separate GEMMs.
 bool token_block_supported(const Model &M) {
-  return M.d == 64 && M.dff == 4 * M.d && M.layer[0].o8 != nullptr;
+  return (M.d == 64 || M.d == 128) && M.dff == 4 * M.d && M.layer[0].tb_o != nullptr;
+}
+
+template <int D>
+static hipError_t run_token_block(const TokenBlockArgs &a, hipStream_t s) {
+  constexpr size_t lds = token_block_lds<D>();
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e =
+        hipFuncSetAttribute((const void *)k_token_block<D>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int64_t strips = (a.rows + 15) / 16;
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, 256 * per_cu);
+  hipLaunchKernelGGL(k_token_block<D>, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const float *ao, float *x,
@@ -961,16 +997,11 @@ hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const
   a.oq = oq;
   a.ao = ao;
   a.x = x;
-  a.bo = W.o8;
-  a.b1 = W.ff1_8;
-  a.b2 = W.ff2_8;
-  a.bias_o = W.b_o;
-  a.bias_1 = W.b_ff1;
-  a.bias_2 = W.b_ff2;
-  a.ln1_g = W.ln1_g;
-  a.ln1_b = W.ln1_b;
-  a.ln2_g = W.ln2_g;
-  a.ln2_b = W.ln2_b;
+  a.fo = W.tb_o;
+  a.f1 = W.tb_1;
+  a.f2 = W.tb_2;
+  a.vec = W.tb_vec;
+  a.b1 = W.b_ff1;
   a.sq_o = W.sq[3];    // aecct_linear order: q, k, v, o, ff1, ff2
   a.sq_1 = W.sq[4];
   a.sq_2 = W.sq[5];
@@ -978,19 +1009,7 @@ hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const
   a.rows = rows;
   a.xq = xq;
   a.ax = ax;
-  const int64_t strips = (rows + 15) / 16;
-  constexpr size_t lds = token_block_lds<64>();
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_token_block<64>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, 256 * per_cu);
-  hipLaunchKernelGGL(k_token_block<64>, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
-  return hipGetLastError();
+  return M.d == 64 ? run_token_block<64>(a, s) : run_token_block<128>(a, s);
 }
 
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
