@@ -505,13 +505,15 @@ struct TokenBlockArgs {
 
 constexpr int kTbWaves = 8;
 
-// d = 64 also keeps the six d-vectors and the FF1 bias in LDS (at d = 128 the fragments fill it).
+// LDS: the FF1 and FF2 fragments (8 d^2 bytes), the O fragments (d^2; at d = 128 they are read
+// from memory instead, once per strip, to leave room), per-wave 16 x d stages, then the six
+// d-vectors and the FF1 bias.
 template <int D>
-constexpr bool tb_lds_vectors() { return D == 64; }
+constexpr bool tb_lds_o() { return D == 64; }
 
 template <int D>
-constexpr size_t token_block_lds() {   // fragments, per-wave 16 x d stages, [vectors, FF1 bias]
-  return (size_t)9 * D * D + (size_t)kTbWaves * 16 * D + (tb_lds_vectors<D>() ? (size_t)10 * D * 4 : 0);
+constexpr size_t token_block_lds() {
+  return (size_t)(tb_lds_o<D>() ? 9 : 8) * D * D + (size_t)kTbWaves * 16 * D + (size_t)10 * D * 4;
 }
 
 // v of lane (this lane xor M), M = 16 or 32
@@ -549,21 +551,23 @@ template <int D>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
   constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint64_t *fo = (uint64_t *)smem, *f1 = fo + (size_t)TO * S * 64, *f2 = f1 + (size_t)TH * S * 64;
-  for (int u = threadIdx.x; u < TO * S * 64; u += kTbWaves * 64) fo[u] = p.fo[u];
+  constexpr size_t frag_bytes = (size_t)(tb_lds_o<D>() ? 9 : 8) * D * D;
+  uint64_t *f1 = (uint64_t *)smem, *f2 = f1 + (size_t)TH * S * 64;
+  const uint64_t *fo = p.fo;
   for (int u = threadIdx.x; u < TH * S * 64; u += kTbWaves * 64) f1[u] = p.f1[u];
   for (int u = threadIdx.x; u < TO * SH * 64; u += kTbWaves * 64) f2[u] = p.f2[u];
-  const float *vec = p.vec, *bias1 = p.b1;
-  if constexpr (tb_lds_vectors<D>()) {
-    float *lv = (float *)(smem + (size_t)9 * D * D + (size_t)kTbWaves * 16 * D);
-    for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
-    for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
-    vec = lv;
-    bias1 = lv + 6 * D;
+  if constexpr (tb_lds_o<D>()) {
+    uint64_t *lo = f2 + (size_t)TO * SH * 64;
+    for (int u = threadIdx.x; u < TO * S * 64; u += kTbWaves * 64) lo[u] = p.fo[u];
+    fo = lo;
   }
+  float *lv = (float *)(smem + frag_bytes + (size_t)kTbWaves * 16 * D);
+  for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
+  for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
+  const float *vec = lv, *bias1 = lv + 6 * D;
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
-  int8_t *stg = (int8_t *)(smem + (size_t)9 * D * D) + (size_t)wave * 16 * D;
+  int8_t *stg = (int8_t *)(smem + frag_bytes) + (size_t)wave * 16 * D;
   const float *vb_o = vec + 0 * D + g * V, *vg1 = vec + 1 * D + g * V, *vb1 = vec + 2 * D + g * V;
   const float *vb_2 = vec + 3 * D + g * V, *vg2 = vec + 4 * D + g * V, *vbb2 = vec + 5 * D + g * V;
   const int64_t nstrips = (p.rows + 15) / 16;
