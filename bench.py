@@ -170,6 +170,8 @@ def main():
     ap.add_argument("--workload", type=int, default=WORKLOAD)
     ap.add_argument("--attention", choices=("hpsa", "casa"), default="hpsa",
                     help="head-partitioned masks (the method) or the ECCT mask on every head")
+    ap.add_argument("--first-ring-heads", type=int, default=None,
+                    help="h_f, heads on the first-ring mask (default heads / 2; HPSA only)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (HBM counter calibration)")
     ap.add_argument("--aap-import", action="store_true",
@@ -190,7 +192,14 @@ def main():
     import paper_2410_05911_amd as P
     from workloads import build_workload
 
-    cfg, H, G, w, y, x = build_workload(args.workload, attention=args.attention)
+    if args.first_ring_heads is not None and args.attention != "hpsa":
+        print("--first-ring-heads applies to the head-partitioned masks only", file=sys.stderr)
+        sys.exit(2)
+    cfg, H, G, w, y, x = build_workload(args.workload, attention=args.attention,
+                                        first_ring_heads=args.first_ring_heads)
+    default_split = args.attention == "hpsa" and w.first_ring_heads == cfg.heads // 2
+    wl_name = cfg.name if default_split else (cfg.name + "_casa" if args.attention == "casa"
+                                              else f"{cfg.name}_hf{w.first_ring_heads}")
     B = cfg.batch
     dev = torch.device("cuda:0")
     dec = P.Decoder(H, w, path=args.path)
@@ -227,7 +236,7 @@ def main():
         "peak": PEAK_ALU_OPS / 1e12,
         "unit": "Top/s (fp32 VALU ops, one per lane per clock)",
         "frac": achieved / PEAK_ALU_OPS,
-        "traffic": measured_traffic(kernel, cfg.name) if args.attention == "hpsa" else None,
+        "traffic": measured_traffic(kernel, cfg.name) if default_split else None,
         "alu_ops_per_word": cnt["alu_ops"],
         "int8_mfma_frac": 2 * cnt["int8_macs"] * B / launch_s / PEAK_INT8,
         "hbm_alg_frac": cnt["hbm_bytes"] * B / launch_s / PEAK_HBM,
@@ -245,7 +254,7 @@ def main():
         "vs_baseline": None,
         "dtype": "int8xternary->int32, fp32",
         "data": "synthetic: seeded BPSK/AWGN words, random ternary weights",
-        "config": {"workload": cfg.name if args.attention == "hpsa" else cfg.name + "_casa", "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
+        "config": {"workload": wl_name, "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
                    "n": cfg.n, "tokens": dec.L, "d": cfg.d, "layers": cfg.n_layers, "heads": cfg.heads,
                    "first_ring_heads": w.first_ring_heads if args.attention == "hpsa" else None,
                    "attention": args.attention, "batch": B, "path": path,

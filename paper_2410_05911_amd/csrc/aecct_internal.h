@@ -80,6 +80,11 @@ struct Model {
   // attention neighbour lists per token, ascending: first ring (M1) and second ring (M2, or
   // M1 | M2 under CASA)
   const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
+  // the same lists in groups of four 16-bit token indices (built when L < 2^16): token a's list
+  // starts at group meta[2a] and has meta[2a + 1] entries, followed by at least one more group
+  bool grouped;
+  const int32_t *g1_meta, *g2_meta;
+  const uint16_t *g1_tab, *g2_tab;
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;
   float head_b1;
@@ -94,17 +99,19 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
                       hipStream_t s);
 hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
                             hipStream_t s);
-// Q/K/V projection and attention fused per (word, 16-dimension head group), then Eq. 2 per
-// token of O: the layered decode's path for d = 64, 128 when L tokens' Q, K, V of a group fit LDS.
+// Q/K/V projection and attention fused per word, one 16-dimension head group at a time, into
+// fp32 O, then (when oq is not null) Eq. 2 per token of O: the layered decode's path for
+// d = 64, 128 when L tokens' Q, K, V of a group fit LDS.
 bool qkv_attention_supported(const Model &M);
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                 float *o, int8_t *oq, float *ao, hipStream_t s);
-// O-projection, residual, LN1, FFN with ReLU, residual, LN2 and Eq. 2 of the next layer's
-// input in one kernel (d = 64, 128): one wavefront per 16-token strip, activations between
-// the maps only in registers and a per-wavefront LDS transpose.
+// Eq. 2 of the attention output (given as fp32 o, or already as codes oq with scales ao: exactly
+// one of o and oq is not null), O-projection, residual, LN1, FFN with ReLU, residual, LN2 and
+// Eq. 2 of the next layer's input in one kernel (d = 64, 128): one wavefront per 16-token strip,
+// activations between the maps only in registers and a per-wavefront LDS transpose.
 bool token_block_supported(const Model &M);
-hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const float *ao, float *x,
-                              int64_t rows, int8_t *xq, float *ax, hipStream_t s);
+hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s);
 hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,
                            int64_t rows, float *x1, int8_t *x1q, float *a1, hipStream_t s);
 hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, int8_t *gq,

@@ -63,6 +63,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 // Device memory plan: byte offsets inside the model's single allocation.
 struct Plan {
   size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
+  size_t g1_meta, g1_tab, g2_meta, g2_tab;   // grouped neighbour lists (layered attention)
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
   struct Layer {
     size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b;
@@ -540,6 +541,27 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   if (M.path == AECCT_PATH_AUTO) M.path = fused_ok ? AECCT_PATH_FUSED : AECCT_PATH_LAYERED;
   if (M.path == AECCT_PATH_FUSED && !fused_ok) return AECCT_ERR_UNSUPPORTED;
 
+  // Neighbour lists in groups of four 16-bit token indices for the layered attention: token a's
+  // list starts at group meta[2a] and has meta[2a + 1] entries; floor(cnt / 4) + 1 groups are
+  // stored, so the group after the last full one can always be read (its unused slots hold 0).
+  std::vector<int32_t> G1m, G2m;
+  std::vector<uint16_t> G1, G2;
+  auto group_lists = [&](const std::vector<int32_t> &ptr, const std::vector<int32_t> &idx,
+                         std::vector<int32_t> &meta, std::vector<uint16_t> &tab) {
+    meta.assign(2 * (size_t)L, 0);
+    for (int a = 0; a < L; ++a) {
+      const int cnt = ptr[a + 1] - ptr[a];
+      meta[2 * a] = (int32_t)(tab.size() / 4);
+      meta[2 * a + 1] = cnt;
+      const int slots = 4 * (cnt / 4 + 1);
+      for (int e = 0; e < slots; ++e) tab.push_back(e < cnt ? (uint16_t)idx[ptr[a] + e] : 0);
+    }
+  };
+  if (L <= 65535) {
+    group_lists(m1_ptr, m1_idx, G1m, G1);
+    group_lists(m2_ptr, m2_idx, G2m, G2);
+  }
+
   // host image of the device block
   Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
   {
@@ -555,6 +577,10 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     P.f_e = take(4 * FI.eperm.size());
     P.f_p = take(4 * FI.pperm.size());
     P.f_w1 = take(4 * FI.w1perm.size());
+    P.g1_meta = take(8 * (size_t)L);
+    P.g1_tab = take(2 * G1.size());
+    P.g2_meta = take(8 * (size_t)L);
+    P.g2_tab = take(2 * G2.size());
     P.total = off;
   }
   std::vector<unsigned char> img;
@@ -585,6 +611,10 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   put(P.f_e, FI.eperm.data(), 4 * FI.eperm.size());
   put(P.f_p, FI.pperm.data(), 4 * FI.pperm.size());
   put(P.f_w1, FI.w1perm.data(), 4 * FI.w1perm.size());
+  put(P.g1_meta, G1m.data(), 4 * G1m.size());
+  put(P.g1_tab, G1.data(), 2 * G1.size());
+  put(P.g2_meta, G2m.data(), 4 * G2m.size());
+  put(P.g2_tab, G2.data(), 2 * G2.size());
   for (int l = 0; l < n_layers; ++l) {
     const auto &q = P.layer[l];
     const int8_t *Wq = w->w_q + l * D * D, *Wk = w->w_k + l * D * D, *Wv = w->w_v + l * D * D;
@@ -668,6 +698,11 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.m1_idx = (const int32_t *)(b + P.m1_idx);
   M.m2_ptr = (const int32_t *)(b + P.m2_ptr);
   M.m2_idx = (const int32_t *)(b + P.m2_idx);
+  M.grouped = !G1.empty();
+  M.g1_meta = (const int32_t *)(b + P.g1_meta);
+  M.g1_tab = (const uint16_t *)(b + P.g1_tab);
+  M.g2_meta = (const int32_t *)(b + P.g2_meta);
+  M.g2_tab = (const uint16_t *)(b + P.g2_tab);
   M.embed = (const float *)(b + P.embed);
   M.pos = w->pos ? (const float *)(b + P.pos) : nullptr;
   M.head_w1 = (const float *)(b + P.w1);
@@ -763,16 +798,21 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
     hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, s);
+    // The fused projection + attention leaves O in fp32 (in the QKV space); the token block then
+    // applies Eq. 2 itself. The unfused attention quantises O as it writes it (a quarter of the
+    // bytes).
+    const bool tb = aecct::token_block_supported(M), qa = aecct::qkv_attention_supported(M);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
-      if (aecct::qkv_attention_supported(M)) {
-        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, oq, ao, s);   // O (fp32) in the QKV space
+      if (qa) {
+        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, s);
       } else {
         e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
         if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
       }
       if (e != hipSuccess) break;
-      if (aecct::token_block_supported(M)) {
-        e = aecct::launch_token_block(M, l, oq, ao, x, rows, xq, ax, s);
+      if (tb) {
+        e = qa ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
+               : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
         if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);

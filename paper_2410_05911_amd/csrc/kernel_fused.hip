@@ -472,13 +472,21 @@ bool fused_supported(const Model &M) {
   return M.d == 32 && M.heads == 8 && M.dff == 128 && M.L <= 64 && M.n <= 64;
 }
 
-bool fused_fits(const Model &M, int nbr_words) {
+// Words in flight per block: kWaves, or as many as the LDS holds when the tables are larger
+// (at least 4, one per SIMD); 0 if not even that fits.  The kernel is compiled for kWaves
+// wavefronts (its register budget), and runs with any smaller count.
+int fused_waves(const Model &M, int nbr_words) {
   const FusedLds L = fused_lds(M, nbr_words);
-  return (size_t)L.off_kv + fz::kWaves * (size_t)L.kv_bytes <= (size_t)fz::kLdsMax;
+  if ((size_t)L.off_kv >= (size_t)fz::kLdsMax) return 0;
+  const int fit = (int)(((size_t)fz::kLdsMax - (size_t)L.off_kv) / (size_t)L.kv_bytes);
+  const int w = fit < fz::kWaves ? fit : fz::kWaves;
+  return w >= 4 ? w : 0;
 }
 
+bool fused_fits(const Model &M, int nbr_words) { return fused_waves(M, nbr_words) > 0; }
+
 template <int NT, int WAVES>
-static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, hipStream_t s) {
+static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, int waves, hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT, WAVES>,
@@ -486,7 +494,7 @@ static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, hipStream_
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((k_fused_decode<NT, WAVES>), dim3(grid), dim3(WAVES * 64), lds, s, a);
+  hipLaunchKernelGGL((k_fused_decode<NT, WAVES>), dim3(grid), dim3(waves * 64), lds, s, a);
   return hipGetLastError();
 }
 
@@ -529,18 +537,19 @@ hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *
   a.off_kv = Ld.off_kv;
   a.kv_bytes = Ld.kv_bytes;
   const size_t off = (size_t)Ld.off_kv;
-  const int waves = fz::kWaves;
-  if (off + (size_t)waves * a.kv_bytes > (size_t)fz::kLdsMax) return hipErrorInvalidConfiguration;
+  const int waves = fused_waves(M, T.nbr_words);
+  if (waves < 1 || waves > fz::kWaves || off + (size_t)waves * a.kv_bytes > (size_t)fz::kLdsMax)
+    return hipErrorInvalidConfiguration;
   const size_t lds = off + (size_t)waves * a.kv_bytes;
   int64_t blocks = (words + waves - 1) / waves;
   const int64_t per_cu = (int64_t)(fz::kLdsMax / lds) > 0 ? (int64_t)(fz::kLdsMax / lds) : 1;
   const int64_t cap = 256 * per_cu;
   const int grid = (int)(blocks < cap ? blocks : cap);
   switch (NT) {
-    case 1: return launch_nt<1, fz::kWaves>(a, lds, grid, s);
-    case 2: return launch_nt<2, fz::kWaves>(a, lds, grid, s);
-    case 3: return launch_nt<3, fz::kWaves>(a, lds, grid, s);
-    case 4: return launch_nt<4, fz::kWaves>(a, lds, grid, s);
+    case 1: return launch_nt<1, fz::kWaves>(a, lds, grid, waves, s);
+    case 2: return launch_nt<2, fz::kWaves>(a, lds, grid, waves, s);
+    case 3: return launch_nt<3, fz::kWaves>(a, lds, grid, waves, s);
+    case 4: return launch_nt<4, fz::kWaves>(a, lds, grid, waves, s);
   }
   return hipErrorInvalidValue;
 }

@@ -322,14 +322,18 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
 }
 
 // ------------------------------------------------------------------------------------------
-// Query/key/value projection and attention of one 16-dimension head group of one word
+// Query/key/value projection and attention of one word, one 16-dimension head group at a time
 // (d = 64 or 128).  The group's three 16-column tiles of the packed QKV map (Eq. 3) are
-// multiplied for all L tokens on v_mfma_i32_16x16x32_i8 and dequantised into LDS (fp32,
-// [L][16] each for Q, K, V), then the group's attention rows (Section 4.2, the same
-// single-pass base-2 softmax and the same evaluation order as k_attention) gather their
-// neighbours' keys and values from LDS.  Blocks are persistent over the words and keep one
-// head group, whose weight tiles they stage once.  Writes the attention output O (fp32
-// [rows][d]) of the group's columns; k_quant_rows then applies Eq. 2 per token.
+// multiplied for all L tokens on v_mfma_i32_16x16x32_i8 and dequantised into LDS (fp32: Q as
+// [L][16], K and V of a token side by side in one 144-byte row), then the group's attention
+// rows (Section 4.2, the same single-pass base-2 softmax and the same evaluation order as
+// k_attention) gather their neighbours' keys and values from LDS.  A row's neighbour indices
+// come four to an 8-byte group, the next group read while the current one's rows are gathered.
+// Blocks are persistent over the words and take every head group of a word in turn, so
+// first-ring groups (short neighbour lists) and second-ring groups (long ones) share each
+// block's time; the next group's weight tiles are unpacked into a second LDS buffer while the
+// current group's rows run.  Writes the attention output O (fp32 [rows][d]); Eq. 2 of O runs
+// in the token block (or in k_quant_rows).
 // ------------------------------------------------------------------------------------------
 struct QkvAttnArgs {
   const int8_t *xq;       // [rows][d] Eq. 2 codes of the layer input
@@ -339,100 +343,150 @@ struct QkvAttnArgs {
   float sq[3];            // dequant scale of Q (with log2(e)/sqrt(d_h)), K, V
   int64_t words;
   int L, hf;
-  const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
-  float *o;               // [rows][d]
+  const int2 *meta1, *meta2;   // per token: first group, entry count (first ring, second ring)
+  const uint2 *tab1, *tab2;    // four 16-bit token indices per group
+  float *o;                    // [rows][d]
 };
 
 constexpr int kQaThreads = 512;
+// K (16 floats) and V (16 floats) of a token in one row of kQaRow floats: 144 bytes apart, rows
+// start on 16 different 16-byte bank groups, so random neighbour gathers collide less, and a
+// value sits at a fixed 64-byte offset from its key.
+constexpr int kQaRow = 36;
+
+template <int D>
+constexpr size_t qa_frag_bytes() { return (size_t)3 * (D / 32) * 64 * 8; }
+
+// Unpacks head group hg's three weight tiles (2-bit codes in HBM) into int8 fragments in LDS.
+template <int D>
+__device__ __forceinline__ void qa_stage_group(const uint16_t *bpack, int hg, uint64_t *bf, int tid) {
+  constexpr int S = D / 32, G = D / 16;
+  for (int u = tid; u < 3 * S * 64; u += kQaThreads) {
+    const int m = u / (S * 64), rest = u - m * (S * 64);
+    bf[u] = unpack_ternary8(bpack[(size_t)(m * G + hg) * S * 64 + rest]);
+  }
+}
+
+// One neighbour of the base-2 softmax: kr points at the neighbour's key (d_h floats, 16-byte
+// aligned), its value 16 floats further.
+template <int DH>
+__device__ __forceinline__ void qa_step(const float (&q)[DH], const float *kr, float shift, float &S,
+                                        float (&acc)[DH]) {
+  float k[DH], v[DH];
+#pragma unroll
+  for (int t = 0; t < DH; t += 4) {
+    const float4 a = *(const float4 *)(kr + t), b = *(const float4 *)(kr + 16 + t);
+    k[t] = a.x; k[t + 1] = a.y; k[t + 2] = a.z; k[t + 3] = a.w;
+    v[t] = b.x; v[t + 1] = b.y; v[t + 2] = b.z; v[t + 3] = b.w;
+  }
+  const float ex = softmax_exp2(head_dot<DH>(q, k) - shift);
+  S = S + ex;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+}
+
+__device__ __forceinline__ uint32_t qa_entry(const uint2 *eg, int e) {
+  const uint2 gq = eg[e >> 2];
+  const uint32_t w = (e & 2) ? gq.y : gq.x;
+  return (e & 1) ? w >> 16 : w & 0xffffu;
+}
 
 template <int D, int DH>
 __global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
-  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH;
+  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, R = kQaRow;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  // Q rows 16 floats apart; K and V rows KVS = 20 floats apart, so that the 64-byte rows start
-  // on 16 different LDS banks (at 16 apart every row starts on one of 4) and random neighbour
-  // gathers collide less.
-  constexpr int KVS = 20;
-  uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
   const int L = p.L;
-  float *qs = (float *)(smem + 3 * S * 64 * 8), *ks = qs + (size_t)L * 16, *vs = ks + (size_t)L * KVS;
+  uint64_t *bfb = (uint64_t *)smem;                          // [2][3][S][64] weight fragments
+  float *qs = (float *)(smem + 2 * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
-  const int hg = blockIdx.x % G;
-  for (int u = tid; u < 3 * S * 64; u += kQaThreads) {
-    const int m = u / (S * 64), rest = u - m * (S * 64);
-    bf[u] = unpack_ternary8(p.bpack[(size_t)(m * G + hg) * S * 64 + rest]);
-  }
-  const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+  if (blockIdx.x >= p.words) return;
+  qa_stage_group<D>(p.bpack, 0, bfb, tid);
   __syncthreads();
-  const int64_t wstride = gridDim.x / G;
-  for (int64_t w = blockIdx.x / G; w < p.words; w += wstride) {
+  int buf = 0;
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
-    for (int tt = wave; tt < (L + 15) / 16; tt += kQaThreads / 64) {
-      const int ra = 16 * tt + col;
-      long afr[S];
+    for (int hg = 0; hg < G; ++hg) {
+      const uint64_t *bf = bfb + (size_t)buf * 3 * S * 64;
+      const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+      for (int tt = wave; tt < (L + 15) / 16; tt += kQaThreads / 64) {
+        const int ra = 16 * tt + col;
+        long afr[S];
 #pragma unroll
-      for (int s = 0; s < S; ++s) afr[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * rg) : 0;
-      v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+        for (int s = 0; s < S; ++s) afr[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * rg) : 0;
+        v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
 #pragma unroll
-      for (int s = 0; s < S; ++s) {
-        aq = mfma_i8_16x16x32(afr[s], (long)bf[(0 * S + s) * 64 + lane], aq);
-        ak = mfma_i8_16x16x32(afr[s], (long)bf[(1 * S + s) * 64 + lane], ak);
-        av = mfma_i8_16x16x32(afr[s], (long)bf[(2 * S + s) * 64 + lane], av);
-      }
+        for (int s = 0; s < S; ++s) {
+          aq = mfma_i8_16x16x32(afr[s], (long)bf[(0 * S + s) * 64 + lane], aq);
+          ak = mfma_i8_16x16x32(afr[s], (long)bf[(1 * S + s) * 64 + lane], ak);
+          av = mfma_i8_16x16x32(afr[s], (long)bf[(2 * S + s) * 64 + lane], av);
+        }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = 16 * tt + 4 * rg + i;
-        if (tok < L) {
-          const float al = aw[tok];
-          qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al * p.sq[0], bq);
-          ks[tok * KVS + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
-          vs[tok * KVS + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * tt + 4 * rg + i;
+          if (tok < L) {
+            const float al = aw[tok];
+            qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al * p.sq[0], bq);
+            kv[tok * R + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
+            kv[tok * R + 16 + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
+          }
         }
       }
-    }
-    __syncthreads();
-    for (int r = tid; r < L * HPG; r += kQaThreads) {
-      const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
-      const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr;
-      const int32_t *idx = h < p.hf ? p.m1_idx : p.m2_idx;
-      const int beg = ptr[i], end = ptr[i + 1];
-      float q[DH];
+      __syncthreads();
+      // the other buffer was last read before the barrier above: fill it with the next group
+      if (hg + 1 < G || w + gridDim.x < p.words)
+        qa_stage_group<D>(p.bpack, hg + 1 < G ? hg + 1 : 0, bfb + (size_t)(buf ^ 1) * 3 * S * 64, tid);
+      for (int r = tid; r < L * HPG; r += kQaThreads) {
+        const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
+        const bool first = h < p.hf;
+        const int2 mt = (first ? p.meta1 : p.meta2)[i];
+        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
+        const int cnt = mt.y;
+        const float *kb = kv + hh * DH;
+        float q[DH];
 #pragma unroll
-      for (int t = 0; t < DH; ++t) q[t] = qs[i * 16 + hh * DH + t];
-      float S_ = 0.0f, acc[DH];
-#pragma unroll
-      for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-#pragma unroll 4
-      for (int e = beg; e < end; ++e) {
-        const int j = idx[e];
-        const float ex = softmax_exp2(head_dot<DH>(q, ks + j * KVS + hh * DH));
-        S_ = S_ + ex;
-        const float *vr = vs + j * KVS + hh * DH;
-#pragma unroll
-        for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
-      }
-      if (end > beg && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
-        float mu = -INFINITY;
-        for (int e = beg; e < end; ++e) mu = fmaxf(mu, head_dot<DH>(q, ks + idx[e] * KVS + hh * DH));
-        S_ = 0.0f;
+        for (int t = 0; t < DH; t += 4) {
+          const float4 a = *(const float4 *)(qs + i * 16 + hh * DH + t);
+          q[t] = a.x; q[t + 1] = a.y; q[t + 2] = a.z; q[t + 3] = a.w;
+        }
+        float S_ = 0.0f, acc[DH];
 #pragma unroll
         for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-        for (int e = beg; e < end; ++e) {
-          const int j = idx[e];
-          const float ex = softmax_exp2(head_dot<DH>(q, ks + j * KVS + hh * DH) - mu);
-          S_ = S_ + ex;
-          const float *vr = vs + j * KVS + hh * DH;
-#pragma unroll
-          for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
+        uint2 nx = eg[0];
+        for (int u = 0; u < (cnt >> 2); ++u) {
+          const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+          nx = eg[u + 1];             // stored: every list has a group after its last full one
+          qa_step<DH>(q, kb + e0 * R, 0.0f, S_, acc);
+          qa_step<DH>(q, kb + e1 * R, 0.0f, S_, acc);
+          qa_step<DH>(q, kb + e2 * R, 0.0f, S_, acc);
+          qa_step<DH>(q, kb + e3 * R, 0.0f, S_, acc);
         }
-      }
-      const float rS = end > beg ? 1.0f / S_ : 0.0f;
-      float *orow = p.o + (w * L + i) * D + h * DH;
+        const int rem = cnt & 3;      // the last, partial group is already in nx
+        if (rem > 0) qa_step<DH>(q, kb + (nx.x & 0xffffu) * R, 0.0f, S_, acc);
+        if (rem > 1) qa_step<DH>(q, kb + (nx.x >> 16) * R, 0.0f, S_, acc);
+        if (rem > 2) qa_step<DH>(q, kb + (nx.y & 0xffffu) * R, 0.0f, S_, acc);
+        if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
+          float mu = -INFINITY;
+          for (int e = 0; e < cnt; ++e) {
+            const float *kr = kb + qa_entry(eg, e) * R;
+            float k[DH];
 #pragma unroll
-      for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
+            for (int t = 0; t < DH; ++t) k[t] = kr[t];
+            mu = fmaxf(mu, head_dot<DH>(q, k));
+          }
+          S_ = 0.0f;
+#pragma unroll
+          for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+          for (int e = 0; e < cnt; ++e) qa_step<DH>(q, kb + qa_entry(eg, e) * R, mu, S_, acc);
+        }
+        const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
+        float *orow = p.o + (w * L + i) * D + h * DH;
+#pragma unroll
+        for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
+      }
+      __syncthreads();
+      buf ^= 1;
     }
-    __syncthreads();
   }
 }
 
@@ -491,8 +545,9 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
 // to be written in row order.  No block barrier after the weight staging.
 // ------------------------------------------------------------------------------------------
 struct TokenBlockArgs {
-  const int8_t *oq;             // [rows][d] Eq. 2 codes of the attention output
-  const float *ao;              // [rows]
+  const float *o;               // [rows][d] attention output (fp32), or
+  const int8_t *oq;             // [rows][d] its Eq. 2 codes and
+  const float *ao;              // [rows] their scales
   float *x;                     // [rows][d] layer input (residual); overwritten with the output
   const uint64_t *fo, *f1, *f2; // permuted A fragments of O, FF1, FF2
   const float *vec;             // [6][4][d/4] b_o, ln1_g, ln1_b, b_ff2, ln2_g, ln2_b in lane order
@@ -547,7 +602,7 @@ __device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
   return (long)(((uint64_t)hi << 32) | lo);
 }
 
-template <int D>
+template <int D, bool OQ>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
   constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -580,10 +635,38 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     long xb[S];
     float a1;
     {
+      // Eq. 2 of the token's attention output: the lane's B-operand features 32 s + 8 g + k,
+      // alpha = max |O| over the four lanes of the token
       long bq[S];
+      float sc;
+      if constexpr (OQ) {
 #pragma unroll
-      for (int s = 0; s < S; ++s) bq[s] = ok ? *(const long *)(p.oq + tok * D + 32 * s + 8 * g) : 0;
-      const float sc = (ok ? p.ao[tok] : 0.0f) * p.sq_o;
+        for (int s = 0; s < S; ++s) bq[s] = ok ? *(const long *)(p.oq + tok * D + 32 * s + 8 * g) : 0;
+        sc = (ok ? p.ao[tok] : 0.0f) * p.sq_o;
+      } else {
+        float ov[S][8];
+        float om = 0.0f;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+#pragma unroll
+          for (int k = 0; k < 8; k += 4) {
+            const float4 f = ok ? *(const float4 *)(p.o + tok * D + 32 * s + 8 * g + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+            ov[s][k] = f.x; ov[s][k + 1] = f.y; ov[s][k + 2] = f.z; ov[s][k + 3] = f.w;
+          }
+#pragma unroll
+          for (int k = 0; k < 8; ++k) om = fmaxf(om, fabsf(ov[s][k]));
+        }
+        om = tb_token_max(om);
+        const float oinv = om == 0.0f ? 0.0f : 127.0f / om;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          uint32_t b[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) b[k] = quant_bits(ov[s][k], oinv);
+          bq[s] = tb_pack8(b);
+        }
+        sc = om * p.sq_o;
+      }
 #pragma unroll
       for (int o = 0; o < TO; ++o) {
         v4i acc = v4i{0, 0, 0, 0};
@@ -917,10 +1000,13 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
   return hipGetLastError();
 }
 
-size_t qkv_attention_lds(const Model &M) { return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + 2 * 20) * 4; }
+size_t qkv_attention_lds(const Model &M) {
+  return (size_t)2 * 3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
+}
 
 bool qkv_attention_supported(const Model &M) {
-  return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && qkv_attention_lds(M) <= 160 * 1024;
+  return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped &&
+         qkv_attention_lds(M) <= 160 * 1024;
 }
 
 template <int D, int DH>
@@ -932,10 +1018,9 @@ static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  constexpr int G = D / 16;
-  const int per_cu = (int)((160 * 1024) / lds) > 0 ? (int)((160 * 1024) / lds) : 1;
-  const int64_t blocks_per_group = std::min<int64_t>(a.words, (int64_t)256 * per_cu / G > 0 ? (int64_t)256 * per_cu / G : 1);
-  hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)(G * blocks_per_group)), dim3(kQaThreads), lds, s, a);
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+  hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)blocks), dim3(kQaThreads), lds, s, a);
   return hipGetLastError();
 }
 
@@ -955,7 +1040,8 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.words = words;
   a.L = M.L;
   a.hf = M.hf;
-  a.m1_ptr = M.m1_ptr; a.m1_idx = M.m1_idx; a.m2_ptr = M.m2_ptr; a.m2_idx = M.m2_idx;
+  a.meta1 = (const int2 *)M.g1_meta; a.meta2 = (const int2 *)M.g2_meta;
+  a.tab1 = (const uint2 *)M.g1_tab; a.tab2 = (const uint2 *)M.g2_tab;
   a.o = o;
   const size_t lds = qkv_attention_lds(M);
   hipError_t e = hipErrorInvalidValue;
@@ -963,7 +1049,7 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
   else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(a, lds, s);
   else if (M.d == 64 && M.dh == 16) e = run_qkv_attention<64, 16>(a, lds, s);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !oq) return e;
   const int64_t rows = words * M.L;
   const dim3 grid((unsigned)((rows + 15) / 16));
   if (M.d == 64) hipLaunchKernelGGL(k_quant_rows<64>, grid, dim3(256), 0, s, o, rows, oq, ao);
@@ -975,29 +1061,30 @@ bool token_block_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && M.dff == 4 * M.d && M.layer[0].tb_o != nullptr;
 }
 
-template <int D>
+template <int D, bool OQ>
 static hipError_t run_token_block(const TokenBlockArgs &a, hipStream_t s) {
   constexpr size_t lds = token_block_lds<D>();
   static bool attr_set = false;
   if (!attr_set) {
     const hipError_t e =
-        hipFuncSetAttribute((const void *)k_token_block<D>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipFuncSetAttribute((const void *)k_token_block<D, OQ>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int64_t strips = (a.rows + 15) / 16;
   const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
   const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, 256 * per_cu);
-  hipLaunchKernelGGL(k_token_block<D>, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
+  hipLaunchKernelGGL((k_token_block<D, OQ>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const float *ao, float *x,
-                              int64_t rows, int8_t *xq, float *ax, hipStream_t s) {
+hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (!token_block_supported(M)) return hipErrorInvalidValue;
   const LayerWeights &W = M.layer[layer];
   TokenBlockArgs a{};
+  a.o = o;
   a.oq = oq;
   a.ao = ao;
   a.x = x;
@@ -1013,7 +1100,9 @@ hipError_t launch_token_block(const Model &M, int layer, const int8_t *oq, const
   a.rows = rows;
   a.xq = xq;
   a.ax = ax;
-  return M.d == 64 ? run_token_block<64>(a, s) : run_token_block<128>(a, s);
+  if (!oq == !o) return hipErrorInvalidValue;
+  if (oq) return M.d == 64 ? run_token_block<64, true>(a, s) : run_token_block<128, true>(a, s);
+  return M.d == 64 ? run_token_block<64, false>(a, s) : run_token_block<128, false>(a, s);
 }
 
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,

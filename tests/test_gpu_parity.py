@@ -239,31 +239,54 @@ def test_fused_head_split_and_positional_table(P, oracle_mod, hf, with_pos):
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
-@pytest.mark.parametrize("regime", ["mixed", "overflow", "underflow"])
-def test_softmax_shifted_rows(P, oracle_mod, regime):
+@pytest.mark.parametrize("hf", [2, 6])
+def test_fused_with_fewer_words_in_flight(P, oracle_mod, hf):
+    """BCH(31,16), 6 layers, with a head group that mixes both rings: its neighbour tables are
+    padded to the group's longest list and leave LDS for 11 words per block instead of 12; the
+    automatic choice must still be the fused kernel, run with fewer wavefronts."""
+    from workloads import build_workload
+    print(f"[waves] hf {hf}", flush=True)
+    cfg, H, G, w, y, x = build_workload(2, batch=517, first_ring_heads=hf)
+    om = oracle_mod.OracleModel(H, w)
+    bo, fo = om.decode(y, n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.path == P.PATH_FUSED
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("regime", ["mixed", "overflow", "underflow", "zero_values"])
+def test_softmax_shifted_rows(P, oracle_mod, regime, d):
     """Attention rows whose unshifted weight sum leaves [2^-64, 2^64] take the max-shifted
-    form on both paths: query/key scales blown up (scores of hundreds: some or all rows
-    overflow), or query and key biases of opposite sign (every score far below -64)."""
+    form on every path (d = 32: fused and layered; d = 64: the layered projection + attention
+    kernel): query/key scales blown up (scores of hundreds: about 5 % of the rows, or nearly
+    all, overflow), or query and key biases of opposite sign (every score far below -64).
+    "zero_values": a zero value map makes every attention output row 0, so its Eq. 2 scale is 0
+    (codes 0, dequantisation scale 0)."""
     from workloads import random_weights
     from workloads.configs import parity_check
     from workloads.channel import awgn_words
     from workloads.codes import generator_from_parity
-    print(f"[softmax] regime {regime}", flush=True)
+    print(f"[softmax] regime {regime} d {d}", flush=True)
     H = parity_check(CONFIGS[2])
     m, n = H.shape
-    w = random_weights(n, m, 32, 2, 8, seed=77)
+    w = random_weights(n, m, d, 2, 8, seed=77)
     if regime == "mixed":
         w.scale[:, 0:2] *= np.float32(5.0)
     elif regime == "overflow":
         w.scale[:, 0:2] *= np.float32(40.0)
-    else:
+    elif regime == "underflow":
         w.b["q"][:] = np.float32(6.0)
         w.b["k"][:] = np.float32(-6.0)
+    else:
+        w.scale[:, 2] = np.float32(0.0)
+        w.b["v"][:] = np.float32(0.0)
     y, x, _ = awgn_words(generator_from_parity(H), 129, (3.0, 5.0), seed=8)
     om = oracle_mod.OracleModel(H, w)
     bo, fo = om.decode(y, n_threads=16)
     assert np.isfinite(fo).all()
-    for path in (P.PATH_FUSED, P.PATH_LAYERED):
+    for path in ((P.PATH_FUSED, P.PATH_LAYERED) if d == 32 else (P.PATH_LAYERED,)):
         dec = P.Decoder(H, w, path=path)
         bits, logits = dec.decode(_dev(y))
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
