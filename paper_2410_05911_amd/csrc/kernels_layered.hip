@@ -356,16 +356,32 @@ constexpr int kQaRow = 36;
 
 template <int D>
 constexpr size_t qa_frag_bytes() { return (size_t)3 * (D / 32) * 64 * 8; }
+// Token tiles a wavefront keeps in registers across a word's head groups (L <= 16 x 8 x 4).
+constexpr int kQaTilesPerWave = 4;
 
-// Unpacks head group hg's three weight tiles (2-bit codes in HBM) into int8 fragments in LDS.
+// Head group hg's three weight tiles, 2-bit codes from HBM: the loads are issued early (into
+// registers) and unpacked into int8 fragments in LDS later, so their latency overlaps the rows.
 template <int D>
-__device__ __forceinline__ void qa_stage_group(const uint16_t *bpack, int hg, uint64_t *bf, int tid) {
-  constexpr int S = D / 32, G = D / 16;
-  for (int u = tid; u < 3 * S * 64; u += kQaThreads) {
-    const int m = u / (S * 64), rest = u - m * (S * 64);
-    bf[u] = unpack_ternary8(bpack[(size_t)(m * G + hg) * S * 64 + rest]);
+struct QaStage {
+  static constexpr int kWords = 3 * (D / 32) * 64, kPer = (kWords + kQaThreads - 1) / kQaThreads;
+  uint32_t pk[kPer];
+  __device__ __forceinline__ void load(const uint16_t *bpack, int hg, int tid) {
+    constexpr int S = D / 32, G = D / 16;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int u = tid + k * kQaThreads;
+      const int m = u / (S * 64), rest = u - m * (S * 64);
+      pk[k] = u < kWords ? bpack[(size_t)(m * G + hg) * S * 64 + rest] : 0u;
+    }
   }
-}
+  __device__ __forceinline__ void store(uint64_t *bf, int tid) const {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int u = tid + k * kQaThreads;
+      if (u < kWords) bf[u] = unpack_ternary8(pk[k]);
+    }
+  }
+};
 
 // One neighbour of the base-2 softmax: kr points at the neighbour's key (d_h floats, 16-byte
 // aligned), its value 16 floats further.
@@ -391,99 +407,161 @@ __device__ __forceinline__ uint32_t qa_entry(const uint2 *eg, int e) {
   return (e & 1) ? w >> 16 : w & 0xffffu;
 }
 
+// Attention of one (token, head) row over its cnt neighbours (ascending), entries from eg with
+// the first group already in g0; writes the row's d_h outputs.
+template <int DH>
+__device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
+                                       float *orow) {
+  constexpr int R = kQaRow;
+  float q[DH];
+#pragma unroll
+  for (int t = 0; t < DH; t += 4) {
+    const float4 a = *(const float4 *)(qrow + t);
+    q[t] = a.x; q[t + 1] = a.y; q[t + 2] = a.z; q[t + 3] = a.w;
+  }
+  float S_ = 0.0f, acc[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+  uint2 nx = g0;
+  for (int u = 0; u < (cnt >> 2); ++u) {
+    const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+    nx = eg[u + 1];             // stored: every list has a group after its last full one
+    qa_step<DH>(q, kb + e0 * R, 0.0f, S_, acc);
+    qa_step<DH>(q, kb + e1 * R, 0.0f, S_, acc);
+    qa_step<DH>(q, kb + e2 * R, 0.0f, S_, acc);
+    qa_step<DH>(q, kb + e3 * R, 0.0f, S_, acc);
+  }
+  const int rem = cnt & 3;      // the last, partial group is already in nx
+  if (rem > 0) qa_step<DH>(q, kb + (nx.x & 0xffffu) * R, 0.0f, S_, acc);
+  if (rem > 1) qa_step<DH>(q, kb + (nx.x >> 16) * R, 0.0f, S_, acc);
+  if (rem > 2) qa_step<DH>(q, kb + (nx.y & 0xffffu) * R, 0.0f, S_, acc);
+  if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
+    float mu = -INFINITY;
+    for (int e = 0; e < cnt; ++e) {
+      const float *kr = kb + qa_entry(eg, e) * R;
+      float k[DH];
+#pragma unroll
+      for (int t = 0; t < DH; ++t) k[t] = kr[t];
+      mu = fmaxf(mu, head_dot<DH>(q, k));
+    }
+    S_ = 0.0f;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+    for (int e = 0; e < cnt; ++e) qa_step<DH>(q, kb + qa_entry(eg, e) * R, mu, S_, acc);
+  }
+  const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
+}
+
+// d = 128: one block per CU (its LDS), so 2 wavefronts per SIMD and room for the word's token
+// tiles in registers across the head groups; d = 64: three blocks per CU, tiles reloaded per
+// group (from L1/L2) to stay within the register budget of 6 wavefronts per SIMD.
+template <int D>
+constexpr bool qa_keep_tiles() { return D == 128; }
+template <int D>
+constexpr int qa_waves_per_simd() { return D == 128 ? 2 : 6; }
+
+// Q, K, V of token tile tt (16 tokens) for the head group whose fragments are bf: the A
+// fragments a (the tile's Eq. 2 codes) and the four token scales al of this lane's outputs.
+template <int D>
+__device__ __forceinline__ void qa_project(const uint64_t *bf, const long (&a)[D / 32], const float (&al)[4],
+                                           int tt, int L, int lane, float bq, float bk, float bv, const float (&sq)[3],
+                                           float *qs, float *kv) {
+  constexpr int S = D / 32, R = kQaRow;
+  const int col = lane & 15, rg = lane >> 4;
+  v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    aq = mfma_i8_16x16x32(a[s], (long)bf[(0 * S + s) * 64 + lane], aq);
+    ak = mfma_i8_16x16x32(a[s], (long)bf[(1 * S + s) * 64 + lane], ak);
+    av = mfma_i8_16x16x32(a[s], (long)bf[(2 * S + s) * 64 + lane], av);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = 16 * tt + 4 * rg + i;
+    if (tok < L) {
+      qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al[i] * sq[0], bq);
+      kv[tok * R + col] = __builtin_fmaf((float)ak[i], al[i] * sq[1], bk);
+      kv[tok * R + 16 + col] = __builtin_fmaf((float)av[i], al[i] * sq[2], bv);
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void qa_load_tile(const int8_t *xw, const float *aw, int tt, int L, int lane,
+                                             long (&a)[D / 32], float (&al)[4]) {
+  const int col = lane & 15, rg = lane >> 4, ra = 16 * tt + col;
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) a[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * rg) : 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = 16 * tt + 4 * rg + i;
+    al[i] = tok < L ? aw[tok] : 0.0f;
+  }
+}
+
 template <int D, int DH>
-__global__ __launch_bounds__(kQaThreads) void k_qkv_attention(QkvAttnArgs p) {
-  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, R = kQaRow;
+__global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_attention(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, TW = qa_keep_tiles<D>() ? kQaTilesPerWave : 1;
+  constexpr int NWV = kQaThreads / 64;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int L = p.L;
+  const int L = p.L, ntiles = (L + 15) / 16;
   uint64_t *bfb = (uint64_t *)smem;                          // [2][3][S][64] weight fragments
   float *qs = (float *)(smem + 2 * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15;
   if (blockIdx.x >= p.words) return;
-  qa_stage_group<D>(p.bpack, 0, bfb, tid);
+  {
+    QaStage<D> st;
+    st.load(p.bpack, 0, tid);
+    st.store(bfb, tid);
+  }
+  // the thread's row (token i0, head hh0 of the group; L d / (16 d_h) <= kQaThreads rows): its
+  // list metadata and first entry group for both masks stay in registers for the whole kernel
+  const bool row0 = tid < L * HPG;
+  const int hh0 = row0 ? tid / L : 0, i0 = row0 ? tid - hh0 * L : 0;
+  const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
+  const uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
   __syncthreads();
   int buf = 0;
+  const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
+  long afr[TW][S];
+  float alw[TW][4];
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
+    if constexpr (qa_keep_tiles<D>()) {
+      // the wave's token tiles, used by all head groups of the word
+#pragma unroll
+      for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wave + NWV * k, L, lane, afr[k], alw[k]);
+    }
     for (int hg = 0; hg < G; ++hg) {
       const uint64_t *bf = bfb + (size_t)buf * 3 * S * 64;
       const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
-      for (int tt = wave; tt < (L + 15) / 16; tt += kQaThreads / 64) {
-        const int ra = 16 * tt + col;
-        long afr[S];
+      if constexpr (qa_keep_tiles<D>()) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) afr[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * rg) : 0;
-        v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-          aq = mfma_i8_16x16x32(afr[s], (long)bf[(0 * S + s) * 64 + lane], aq);
-          ak = mfma_i8_16x16x32(afr[s], (long)bf[(1 * S + s) * 64 + lane], ak);
-          av = mfma_i8_16x16x32(afr[s], (long)bf[(2 * S + s) * 64 + lane], av);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int tok = 16 * tt + 4 * rg + i;
-          if (tok < L) {
-            const float al = aw[tok];
-            qs[tok * 16 + col] = __builtin_fmaf((float)aq[i], al * p.sq[0], bq);
-            kv[tok * R + col] = __builtin_fmaf((float)ak[i], al * p.sq[1], bk);
-            kv[tok * R + 16 + col] = __builtin_fmaf((float)av[i], al * p.sq[2], bv);
-          }
+        for (int k = 0; k < TW; ++k)
+          if (wave + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wave + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
+      } else {
+        for (int tt = wave; tt < ntiles; tt += NWV) {
+          qa_load_tile<D>(xw, aw, tt, L, lane, afr[0], alw[0]);
+          qa_project<D>(bf, afr[0], alw[0], tt, L, lane, bq, bk, bv, sq, qs, kv);
         }
       }
       __syncthreads();
-      // the other buffer was last read before the barrier above: fill it with the next group
-      if (hg + 1 < G || w + gridDim.x < p.words)
-        qa_stage_group<D>(p.bpack, hg + 1 < G ? hg + 1 : 0, bfb + (size_t)(buf ^ 1) * 3 * S * 64, tid);
-      for (int r = tid; r < L * HPG; r += kQaThreads) {
-        const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
+      // the other buffer was last read before the barrier above: the next group's weights are
+      // loaded now and written there after the rows
+      const bool more = hg + 1 < G || w + gridDim.x < p.words;
+      QaStage<D> st;
+      if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
+      if (row0) {
+        const int h = hg * HPG + hh0;
         const bool first = h < p.hf;
-        const int2 mt = (first ? p.meta1 : p.meta2)[i];
-        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
-        const int cnt = mt.y;
-        const float *kb = kv + hh * DH;
-        float q[DH];
-#pragma unroll
-        for (int t = 0; t < DH; t += 4) {
-          const float4 a = *(const float4 *)(qs + i * 16 + hh * DH + t);
-          q[t] = a.x; q[t + 1] = a.y; q[t + 2] = a.z; q[t + 3] = a.w;
-        }
-        float S_ = 0.0f, acc[DH];
-#pragma unroll
-        for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-        uint2 nx = eg[0];
-        for (int u = 0; u < (cnt >> 2); ++u) {
-          const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
-          nx = eg[u + 1];             // stored: every list has a group after its last full one
-          qa_step<DH>(q, kb + e0 * R, 0.0f, S_, acc);
-          qa_step<DH>(q, kb + e1 * R, 0.0f, S_, acc);
-          qa_step<DH>(q, kb + e2 * R, 0.0f, S_, acc);
-          qa_step<DH>(q, kb + e3 * R, 0.0f, S_, acc);
-        }
-        const int rem = cnt & 3;      // the last, partial group is already in nx
-        if (rem > 0) qa_step<DH>(q, kb + (nx.x & 0xffffu) * R, 0.0f, S_, acc);
-        if (rem > 1) qa_step<DH>(q, kb + (nx.x >> 16) * R, 0.0f, S_, acc);
-        if (rem > 2) qa_step<DH>(q, kb + (nx.y & 0xffffu) * R, 0.0f, S_, acc);
-        if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
-          float mu = -INFINITY;
-          for (int e = 0; e < cnt; ++e) {
-            const float *kr = kb + qa_entry(eg, e) * R;
-            float k[DH];
-#pragma unroll
-            for (int t = 0; t < DH; ++t) k[t] = kr[t];
-            mu = fmaxf(mu, head_dot<DH>(q, k));
-          }
-          S_ = 0.0f;
-#pragma unroll
-          for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-          for (int e = 0; e < cnt; ++e) qa_step<DH>(q, kb + qa_entry(eg, e) * R, mu, S_, acc);
-        }
-        const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
-        float *orow = p.o + (w * L + i) * D + h * DH;
-#pragma unroll
-        for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
+        const int2 mt = first ? mt1 : mt2;
+        qa_row<DH>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
+                   mt.y, p.o + (w * L + i0) * D + h * DH);
       }
+      if (more) st.store(bfb + (size_t)(buf ^ 1) * 3 * S * 64, tid);
       __syncthreads();
       buf ^= 1;
     }
@@ -1006,6 +1084,7 @@ size_t qkv_attention_lds(const Model &M) {
 
 bool qkv_attention_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped &&
+         M.L <= 16 * (kQaThreads / 64) * kQaTilesPerWave && M.L * (16 / M.dh) <= kQaThreads &&
          qkv_attention_lds(M) <= 160 * 1024;
 }
 
