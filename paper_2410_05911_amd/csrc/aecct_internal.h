@@ -34,6 +34,7 @@ constexpr int kLdsMax = 160 * 1024;
 // one [d][3d] map.
 struct LayerWeights {
   const uint16_t *qkv;   // blocks of the [d][3d] map
+  const uint16_t *qkv_tb;  // the same map reading its inputs in lane order (d = 64, 128), or null
   const uint16_t *o;     // [d][d]
   const uint16_t *ff1;   // [d][d_ff]
   const uint16_t *ff2;   // [d_ff][d]
@@ -93,10 +94,16 @@ struct Model {
 };
 
 // ---- launchers (kernels_layered.hip) ---------------------------------------------------
+// Activation layouts.  Natural: X [rows][d] fp32 and its codes Xq [rows][d] by feature.  Lane
+// order (the decode with the token block, d = 64, 128): the token block holds feature 4 v + g
+// of a token in register v of lane group g, so X stores feature f at (f % 4) (d / 4) + f / 4
+// (a lane's d / 4 values contiguous) and Xq stores feature 32 s + 4 k + g (k < 8, g < 4) at
+// byte 32 s + 8 g + k (a lane's eight codes of step s as one 8-byte word); the Q/K/V map is
+// packed a second time to read its inputs in that byte order.
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
-                        hipStream_t s);
+                        bool lane_order, hipStream_t s);
 hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t rows, float *qkv,
-                      hipStream_t s);
+                      bool lane_order, hipStream_t s);
 hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
                             hipStream_t s);
 // Q/K/V projection and attention fused per word, one 16-dimension head group at a time, into
@@ -104,11 +111,11 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
 // d = 64, 128 when L tokens' Q, K, V of a group fit LDS.
 bool qkv_attention_supported(const Model &M);
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
-                                float *o, int8_t *oq, float *ao, hipStream_t s);
+                                float *o, int8_t *oq, float *ao, bool lane_order, hipStream_t s);
 // Eq. 2 of the attention output (given as fp32 o, or already as codes oq with scales ao: exactly
-// one of o and oq is not null), O-projection, residual, LN1, FFN with ReLU, residual, LN2 and
-// Eq. 2 of the next layer's input in one kernel (d = 64, 128): one wavefront per 16-token strip,
-// activations between the maps only in registers and a per-wavefront LDS transpose.
+// one of o and oq is not null; natural layout), O-projection, residual, LN1, FFN with ReLU,
+// residual, LN2 and Eq. 2 of the next layer's input in one kernel (d = 64, 128): one wavefront
+// per 16-token strip, activations between the maps only in registers; X and Xq in lane order.
 bool token_block_supported(const Model &M);
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
                               float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s);
@@ -119,7 +126,7 @@ hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float
 hipError_t launch_ffn2_ln(const Model &M, int layer, const int8_t *gq, const float *ag, const float *x1,
                           int64_t rows, float *x, int8_t *xq, float *ax, hipStream_t s);
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
-                       float *logits, hipStream_t s);
+                       float *logits, bool lane_order, hipStream_t s);
 hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a, int64_t rows, int32_t *acc,
                                hipStream_t s);
 // ---- fused path (kernel_fused.hip) -----------------------------------------------------

@@ -68,6 +68,7 @@ struct Plan {
   struct Layer {
     size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b;
     size_t tb_o, tb_1, tb_2, tb_vec;   // token-block fragments and lane-order vectors (d = 64, 128), or 0
+    size_t qkv_tb;                     // the QKV map reading lane-order codes (d = 64, 128), or 0
   };
   std::vector<Layer> layer;
 };
@@ -108,6 +109,7 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
       q.tb_1 = take((size_t)d * dff);
       q.tb_2 = take((size_t)dff * d);
       q.tb_vec = take(sizeof(float) * 6 * d);
+      q.qkv_tb = take(2 * packed_words(d, 3 * d));
     }
   }
   p.total = off;
@@ -626,6 +628,15 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     pack_map(d, d, [&](int k, int j) { return Wo[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.o));
     pack_map(d, dff, [&](int k, int j) { return W1[(size_t)k * F + j]; }, (uint16_t *)(img.data() + q.ff1));
     pack_map(dff, d, [&](int k, int j) { return W2[(size_t)k * D + j]; }, (uint16_t *)(img.data() + q.ff2));
+    if (q.qkv_tb) {
+      // input slot k of step k / 32 reads the code of feature 32 (k / 32) + 4 (k % 8) + (k % 32) / 8,
+      // the byte order in which the token block writes the next layer's codes
+      pack_map(d, 3 * d, [&](int k, int j) {
+        const int8_t *src = j < d ? Wq : (j < 2 * d ? Wk : Wv);
+        const int f = 32 * (k >> 5) + 4 * (k & 7) + ((k & 31) >> 3);
+        return src[(size_t)f * D + (j % d)];
+      }, (uint16_t *)(img.data() + q.qkv_tb));
+    }
     if (q.tb_o) {
       // Token block (transposed products: weights are the A operand, 16 tokens the columns).
       // A fragment (tile t, step s): lane l holds output row l & 15 and k-slots 8 (l >> 4) + e
@@ -727,6 +738,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     Lw.tb_1 = q.tb_1 ? (const uint64_t *)(b + q.tb_1) : nullptr;
     Lw.tb_2 = q.tb_2 ? (const uint64_t *)(b + q.tb_2) : nullptr;
     Lw.tb_vec = q.tb_vec ? (const float *)(b + q.tb_vec) : nullptr;
+    Lw.qkv_tb = q.qkv_tb ? (const uint16_t *)(b + q.qkv_tb) : nullptr;
   }
   if (!FI.frag.empty()) {
     aecct::FusedTables &T = M.fused;
@@ -797,16 +809,17 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
   for (int64_t w0 = 0; w0 < batch; w0 += cw) {
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
-    hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, s);
+    // With the token block, X and Xq are kept in its lane order from the embedding to the head.
     // The fused projection + attention leaves O in fp32 (in the QKV space); the token block then
     // applies Eq. 2 itself. The unfused attention quantises O as it writes it (a quarter of the
     // bytes).
     const bool tb = aecct::token_block_supported(M), qa = aecct::qkv_attention_supported(M);
+    hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, tb, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
       if (qa) {
-        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, s);
+        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, tb, s);
       } else {
-        e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, s);
+        e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, tb, s);
         if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
       }
       if (e != hipSuccess) break;
@@ -820,7 +833,7 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
       }
     }
     if (e == hipSuccess)
-      e = aecct::launch_head(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, s);
+      e = aecct::launch_head(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, tb, s);
     if (e != hipSuccess) return AECCT_ERR_DEVICE;
   }
   return AECCT_OK;
@@ -838,13 +851,13 @@ static inline aecct_status launched(hipError_t e) { return e == hipSuccess ? AEC
 aecct_status aecct_stage_embed(const aecct_model *model, const float *y, int64_t words, float *x, int8_t *xq,
                                float *ax, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (y && x && xq && ax)));
-  return launched(aecct::launch_embed(model->M, y, words, x, xq, ax, (hipStream_t)stream));
+  return launched(aecct::launch_embed(model->M, y, words, x, xq, ax, false, (hipStream_t)stream));
 }
 
 aecct_status aecct_stage_qkv(const aecct_model *model, int32_t layer, const int8_t *xq, const float *ax,
                              int64_t words, float *qkv, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers && (words == 0 || (xq && ax && qkv)));
-  return launched(aecct::launch_qkv(model->M, layer, xq, ax, words * model->M.L, qkv, (hipStream_t)stream));
+  return launched(aecct::launch_qkv(model->M, layer, xq, ax, words * model->M.L, qkv, false, (hipStream_t)stream));
 }
 
 aecct_status aecct_stage_attention(const aecct_model *model, const float *qkv, int64_t words, float *o, int8_t *oq,
@@ -878,7 +891,7 @@ aecct_status aecct_stage_ffn2_ln(const aecct_model *model, int32_t layer, const 
 aecct_status aecct_stage_head(const aecct_model *model, const float *x, const float *y, int64_t words, uint8_t *bits,
                               float *logits, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (x && y && bits)));
-  return launched(aecct::launch_head(model->M, x, y, words, bits, logits, (hipStream_t)stream));
+  return launched(aecct::launch_head(model->M, x, y, words, bits, logits, false, (hipStream_t)stream));
 }
 
 aecct_status aecct_ternary_gemm(const aecct_model *model, int32_t layer, int32_t kind, const int8_t *a, int64_t rows,

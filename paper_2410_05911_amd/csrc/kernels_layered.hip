@@ -13,9 +13,15 @@
 
 namespace aecct {
 
+// Positions of feature f of a d-wide row in the lane-order layouts (the token block's register
+// layout): X (fp32) and Xq (codes).
+template <int D>
+__device__ __forceinline__ int lane_order_x(int f) { return (f & 3) * (D / 4) + (f >> 2); }
+__device__ __forceinline__ int lane_order_q(int f) { return (f & ~31) + 8 * (f & 3) + ((f >> 2) & 7); }
+
 // ------------------------------------------------------------------------------------------
 // Embedding: pre-processing h(y) (Section 3), X = t * E (+ P), and the Eq. 2 code of X.
-// 16 lanes per row; lane c holds features c + 16 t, t < D / 16.
+// 16 lanes per row; lane c holds features c + 16 t, t < D / 16.  LO: X and Xq in lane order.
 // ------------------------------------------------------------------------------------------
 struct EmbedArgs {
   const float *y;
@@ -28,7 +34,7 @@ struct EmbedArgs {
   float *ax;
 };
 
-template <int D>
+template <int D, bool LO>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   constexpr int T = D / 16;
   const int c = threadIdx.x & 15;
@@ -51,13 +57,13 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   for (int tt = 0; tt < T; ++tt) {
     const int col = 16 * tt + c;
     v[tt] = __builtin_fmaf(t, p.embed[(int64_t)i * D + col], p.pos ? p.pos[(int64_t)i * D + col] : 0.0f);
-    p.x[g * D + col] = v[tt];
+    p.x[g * D + (LO ? lane_order_x<D>(col) : col)] = v[tt];
     amax = fmaxf(amax, fabsf(v[tt]));
   }
   amax = row16_max(amax);
   const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
 #pragma unroll
-  for (int tt = 0; tt < T; ++tt) p.xq[g * D + 16 * tt + c] = quant_code(v[tt], inv);
+  for (int tt = 0; tt < T; ++tt) p.xq[g * D + (LO ? lane_order_q(16 * tt + c) : 16 * tt + c)] = quant_code(v[tt], inv);
   if (c == 0) p.ax[g] = amax;
 }
 
@@ -619,8 +625,9 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
 // twice: once for the rows' ReLU maxima (the Eq. 2 scale of the hidden row), once (identical
 // values) to quantise, each pair of tiles feeding FF2 at once.  LayerNorm sums are the
 // pairwise order (in-lane over v, then lanes xor 32, xor 16); epilogues and evaluation order
-// are those of k_gemm's EPI_LN / EPI_RELU_QUANT.  Only the next layer's codes go through LDS,
-// to be written in row order.  No block barrier after the weight staging.
+// are those of k_gemm's EPI_LN / EPI_RELU_QUANT.  X and the next layer's codes are kept in that
+// lane order in memory too, so every lane reads and writes contiguous words.  No block barrier
+// after the weight staging.
 // ------------------------------------------------------------------------------------------
 struct TokenBlockArgs {
   const float *o;               // [rows][d] attention output (fp32), or
@@ -638,15 +645,10 @@ struct TokenBlockArgs {
 
 constexpr int kTbWaves = 8;
 
-// LDS: the FF1 and FF2 fragments (8 d^2 bytes), the O fragments (d^2; at d = 128 they are read
-// from memory instead, once per strip, to leave room), per-wave 16 x d stages, then the six
-// d-vectors and the FF1 bias.
-template <int D>
-constexpr bool tb_lds_o() { return D == 64; }
-
+// LDS: the FF1, FF2 and O fragments (9 d^2 bytes), then the six d-vectors and the FF1 bias.
 template <int D>
 constexpr size_t token_block_lds() {
-  return (size_t)(tb_lds_o<D>() ? 9 : 8) * D * D + (size_t)kTbWaves * 16 * D + (size_t)10 * D * 4;
+  return (size_t)9 * D * D + (size_t)10 * D * 4;
 }
 
 // v of lane (this lane xor M), M = 16 or 32
@@ -684,23 +686,17 @@ template <int D, bool OQ>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
   constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  constexpr size_t frag_bytes = (size_t)(tb_lds_o<D>() ? 9 : 8) * D * D;
-  uint64_t *f1 = (uint64_t *)smem, *f2 = f1 + (size_t)TH * S * 64;
-  const uint64_t *fo = p.fo;
+  constexpr size_t frag_bytes = (size_t)9 * D * D;
+  uint64_t *f1 = (uint64_t *)smem, *f2 = f1 + (size_t)TH * S * 64, *fo = f2 + (size_t)TO * SH * 64;
   for (int u = threadIdx.x; u < TH * S * 64; u += kTbWaves * 64) f1[u] = p.f1[u];
   for (int u = threadIdx.x; u < TO * SH * 64; u += kTbWaves * 64) f2[u] = p.f2[u];
-  if constexpr (tb_lds_o<D>()) {
-    uint64_t *lo = f2 + (size_t)TO * SH * 64;
-    for (int u = threadIdx.x; u < TO * S * 64; u += kTbWaves * 64) lo[u] = p.fo[u];
-    fo = lo;
-  }
-  float *lv = (float *)(smem + frag_bytes + (size_t)kTbWaves * 16 * D);
+  for (int u = threadIdx.x; u < TO * S * 64; u += kTbWaves * 64) fo[u] = p.fo[u];
+  float *lv = (float *)(smem + frag_bytes);
   for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
   for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
   const float *vec = lv, *bias1 = lv + 6 * D;
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
-  int8_t *stg = (int8_t *)(smem + frag_bytes) + (size_t)wave * 16 * D;
   const float *vb_o = vec + 0 * D + g * V, *vg1 = vec + 1 * D + g * V, *vb1 = vec + 2 * D + g * V;
   const float *vb_2 = vec + 3 * D + g * V, *vg2 = vec + 4 * D + g * V, *vbb2 = vec + 5 * D + g * V;
   const int64_t nstrips = (p.rows + 15) / 16;
@@ -750,12 +746,14 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)fo[(o * S + s) * 64 + lane], bq[s], acc);
+        // the residual: four consecutive values of X in lane order
+        const float4 r = ok ? *(const float4 *)(p.x + tok * D + g * V + 4 * o) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float res[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int v = 4 * o + i;
           const float y = __builtin_fmaf((float)acc[i], sc, vb_o[v]);
-          const float res = ok ? p.x[tok * D + 4 * v + g] : 0.0f;
-          x1[v] = res + y;
+          x1[v] = res[i] + y;
         }
       }
       const float mean = tb_token_sum<V>(x1) / (float)D;
@@ -847,22 +845,29 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
       for (int v = 0; v < V; ++v) {
         v2[v] = __builtin_fmaf(e[v] * rho, vg2[v], vbb2[v]);
-        if (ok) p.x[tok * D + 4 * v + g] = v2[v];
         amax = fmaxf(amax, fabsf(v2[v]));
+      }
+      if (ok) {
+#pragma unroll
+        for (int u = 0; u < V; u += 4)
+          *(float4 *)(p.x + tok * D + g * V + u) = make_float4(v2[u], v2[u + 1], v2[u + 2], v2[u + 3]);
       }
       amax = tb_token_max(amax);
       const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+      if (ok) {
+        // the next layer's codes in lane order: step s's eight codes of this lane as one word
 #pragma unroll
-      for (int v = 0; v < V; ++v) stg[c * D + 4 * v + g] = quant_code(v2[v], inv);
-      if (g == 0 && ok) p.ax[tok] = amax;
+        for (int s = 0; s < S; ++s) {
+          uint32_t b[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) b[k] = quant_bits(v2[8 * s + k], inv);
+          *(long *)(p.xq + tok * D + 32 * s + 8 * g) = tb_pack8(b);
+        }
+        if (g == 0) p.ax[tok] = amax;
+      }
     }
-    wave_barrier_lds();
-    const int64_t valid = p.rows - row0 < 16 ? p.rows - row0 : 16;
-    const int chunks = (int)(valid * D / 16);
-    const uint4 *src = (const uint4 *)stg;
-    uint4 *dst = (uint4 *)(p.xq + row0 * D);
-    for (int k = lane; k < chunks; k += 64) dst[k] = src[k];
-    wave_barrier_lds();
+    // keeps the scheduler from overlapping strips (their live ranges would not fit the registers)
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -880,7 +885,7 @@ struct HeadArgs {
   float *logits;
 };
 
-template <int D>
+template <int D, bool LO>
 __global__ __launch_bounds__(256) void k_head(HeadArgs p) {
   constexpr int T = D / 16;
   extern __shared__ float zs[];
@@ -890,7 +895,7 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs p) {
     const float *xr = p.x + (w * p.L + i) * D;
     float v[T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) v[t] = xr[16 * t + c] * p.w1[16 * t + c];
+    for (int t = 0; t < T; ++t) v[t] = xr[LO ? lane_order_x<D>(16 * t + c) : 16 * t + c] * p.w1[16 * t + c];
     const float z = row16_sum(lane_tree<T>(v)) + p.b1;
     if (c == 0) zs[i] = z;
   }
@@ -940,23 +945,31 @@ GemmArgs gemm_base(const int8_t *a, const float *alpha, const uint16_t *bpack, i
 }  // namespace
 
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
-                        hipStream_t s) {
+                        bool lane_order, hipStream_t s) {
   EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax};
   if (a.rows <= 0) return hipSuccess;
+  if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((a.rows + 15) / 16));
   switch (M.d) {
-    case 32: hipLaunchKernelGGL(k_embed<32>, grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL(k_embed<64>, grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL(k_embed<128>, grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_embed<32, false>), grid, dim3(256), 0, s, a); break;
+    case 64:
+      if (lane_order) hipLaunchKernelGGL((k_embed<64, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_embed<64, false>), grid, dim3(256), 0, s, a);
+      break;
+    case 128:
+      if (lane_order) hipLaunchKernelGGL((k_embed<128, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_embed<128, false>), grid, dim3(256), 0, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t rows, float *qkv,
-                      hipStream_t s) {
+                      bool lane_order, hipStream_t s) {
   const LayerWeights &W = M.layer[layer];
-  GemmArgs a = gemm_base(xq, ax, W.qkv, rows);
+  if (lane_order && !W.qkv_tb) return hipErrorInvalidValue;
+  GemmArgs a = gemm_base(xq, ax, lane_order ? W.qkv_tb : W.qkv, rows);
   a.sq[0] = W.sq_qs;
   a.sq[1] = W.sq[1];
   a.sq[2] = W.sq[2];
@@ -1104,14 +1117,15 @@ static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_
 }
 
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
-                                float *o, int8_t *oq, float *ao, hipStream_t s) {
+                                float *o, int8_t *oq, float *ao, bool lane_order, hipStream_t s) {
   if (words <= 0) return hipSuccess;
   if (!qkv_attention_supported(M)) return hipErrorInvalidValue;
   const LayerWeights &W = M.layer[layer];
+  if (lane_order && !W.qkv_tb) return hipErrorInvalidValue;
   QkvAttnArgs a{};
   a.xq = xq;
   a.ax = ax;
-  a.bpack = W.qkv;
+  a.bpack = lane_order ? W.qkv_tb : W.qkv;
   a.bias = W.b_qkv;
   a.sq[0] = W.sq_qs;
   a.sq[1] = W.sq[1];
@@ -1185,14 +1199,22 @@ hipError_t launch_token_block(const Model &M, int layer, const float *o, const i
 }
 
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
-                       float *logits, hipStream_t s) {
+                       float *logits, bool lane_order, hipStream_t s) {
   if (words <= 0) return hipSuccess;
+  if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
   HeadArgs a{x, y, M.n, M.L, M.head_w1, M.head_wo, M.head_bo, M.head_b1, bits, logits};
   const size_t shm = sizeof(float) * (size_t)M.L;
+  const dim3 grid((unsigned)words);
   switch (M.d) {
-    case 32: hipLaunchKernelGGL(k_head<32>, dim3((unsigned)words), dim3(256), shm, s, a); break;
-    case 64: hipLaunchKernelGGL(k_head<64>, dim3((unsigned)words), dim3(256), shm, s, a); break;
-    case 128: hipLaunchKernelGGL(k_head<128>, dim3((unsigned)words), dim3(256), shm, s, a); break;
+    case 32: hipLaunchKernelGGL((k_head<32, false>), grid, dim3(256), shm, s, a); break;
+    case 64:
+      if (lane_order) hipLaunchKernelGGL((k_head<64, true>), grid, dim3(256), shm, s, a);
+      else hipLaunchKernelGGL((k_head<64, false>), grid, dim3(256), shm, s, a);
+      break;
+    case 128:
+      if (lane_order) hipLaunchKernelGGL((k_head<128, true>), grid, dim3(256), shm, s, a);
+      else hipLaunchKernelGGL((k_head<128, false>), grid, dim3(256), shm, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
