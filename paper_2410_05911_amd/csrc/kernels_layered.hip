@@ -643,7 +643,7 @@ struct TokenBlockArgs {
   float *ax;                    // [rows]
 };
 
-constexpr int kTbWaves = 8;
+constexpr int kTbWaves = 16;
 
 // LDS: the FF1, FF2 and O fragments (9 d^2 bytes), then the six d-vectors and the FF1 bias.
 template <int D>
