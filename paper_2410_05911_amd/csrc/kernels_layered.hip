@@ -337,9 +337,11 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
 // come four to an 8-byte group, the next group read while the current one's rows are gathered.
 // Blocks are persistent over the words and take every head group of a word in turn, so
 // first-ring groups (short neighbour lists) and second-ring groups (long ones) share each
-// block's time; the next group's weight tiles are unpacked into a second LDS buffer while the
-// current group's rows run.  Writes the attention output O (fp32 [rows][d]); Eq. 2 of O runs
-// in the token block (or in k_quant_rows).
+// block's time; the next group's weight tiles are loaded while the current group's rows run.
+// Writes the attention output O (fp32 [rows][d]); Eq. 2 of O runs in the token block (or in
+// k_quant_rows).  A head's keys are gathered by neighbour index: the 144-byte row stride puts
+// rows on 16 different 16-byte bank groups (at 128 bytes random gathers collide far more, and
+// the kernel ran about 30 % slower).
 // ------------------------------------------------------------------------------------------
 struct QkvAttnArgs {
   const int8_t *xq;       // [rows][d] Eq. 2 codes of the layer input
@@ -461,12 +463,12 @@ __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const
 }
 
 // d = 128: one block per CU (its LDS), so 2 wavefronts per SIMD and room for the word's token
-// tiles in registers across the head groups; d = 64: three blocks per CU, tiles reloaded per
-// group (from L1/L2) to stay within the register budget of 6 wavefronts per SIMD.
+// tiles in registers across the head groups; d = 64: three blocks per CU (d_h = 8), tiles
+// reloaded per group (from L1/L2) to stay within the register budget of 6 wavefronts per SIMD.
 template <int D>
 constexpr bool qa_keep_tiles() { return D == 128; }
-template <int D>
-constexpr int qa_waves_per_simd() { return D == 128 ? 2 : 6; }
+template <int D, int DH>
+constexpr int qa_waves_per_simd() { return D == 128 ? 2 : (DH == 8 ? 6 : 4); }
 
 // Q, K, V of token tile tt (16 tokens) for the head group whose fragments are bf: the A
 // fragments a (the tile's Eq. 2 codes) and the four token scales al of this lane's outputs.
@@ -508,19 +510,19 @@ __device__ __forceinline__ void qa_load_tile(const int8_t *xw, const float *aw, 
 }
 
 template <int D, int DH>
-__global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_attention(QkvAttnArgs p) {
+__global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qkv_attention(QkvAttnArgs p) {
   constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, TW = qa_keep_tiles<D>() ? kQaTilesPerWave : 1;
   constexpr int NWV = kQaThreads / 64;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int L = p.L, ntiles = (L + 15) / 16;
-  uint64_t *bfb = (uint64_t *)smem;                          // [2][3][S][64] weight fragments
-  float *qs = (float *)(smem + 2 * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
+  uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
+  float *qs = (float *)(smem + qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15;
   if (blockIdx.x >= p.words) return;
   {
     QaStage<D> st;
     st.load(p.bpack, 0, tid);
-    st.store(bfb, tid);
+    st.store(bf, tid);
   }
   // the thread's row (token i0, head hh0 of the group; L d / (16 d_h) <= kQaThreads rows): its
   // list metadata and first entry group for both masks stay in registers for the whole kernel
@@ -529,7 +531,6 @@ __global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_atte
   const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
   const uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
   __syncthreads();
-  int buf = 0;
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
@@ -542,7 +543,6 @@ __global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_atte
       for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wave + NWV * k, L, lane, afr[k], alw[k]);
     }
     for (int hg = 0; hg < G; ++hg) {
-      const uint64_t *bf = bfb + (size_t)buf * 3 * S * 64;
       const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
       if constexpr (qa_keep_tiles<D>()) {
 #pragma unroll
@@ -555,8 +555,8 @@ __global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_atte
         }
       }
       __syncthreads();
-      // the other buffer was last read before the barrier above: the next group's weights are
-      // loaded now and written there after the rows
+      // the fragments were last read before the barrier above: the next group's weights are
+      // loaded now and written after the rows
       const bool more = hg + 1 < G || w + gridDim.x < p.words;
       QaStage<D> st;
       if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
@@ -567,9 +567,8 @@ __global__ __launch_bounds__(kQaThreads, qa_waves_per_simd<D>()) void k_qkv_atte
         qa_row<DH>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
                    mt.y, p.o + (w * L + i0) * D + h * DH);
       }
-      if (more) st.store(bfb + (size_t)(buf ^ 1) * 3 * S * 64, tid);
+      if (more) st.store(bf, tid);
       __syncthreads();
-      buf ^= 1;
     }
   }
 }
@@ -1092,7 +1091,7 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
 }
 
 size_t qkv_attention_lds(const Model &M) {
-  return (size_t)2 * 3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
+  return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
 }
 
 bool qkv_attention_supported(const Model &M) {
