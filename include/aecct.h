@@ -101,6 +101,16 @@ typedef enum aecct_attention {
                            union of the two rings, nodes at most two steps away; h_f is ignored */
 } aecct_attention;
 
+/* How the layered path computes a layer's queries, keys, values (Eq. 3) and attention
+   (Section 4.2); every form gives the same results bit for bit. */
+typedef enum aecct_layered_attention {
+  AECCT_LAYERED_ATTN_UNFUSED = 0,  /* ternary GEMM to Q, K, V in device memory, then attention */
+  AECCT_LAYERED_ATTN_LDS_F32 = 1,  /* fused per word and 16-dimension head group, K and V in
+                                      LDS as fp32 (d = 64, 128, short words) */
+  AECCT_LAYERED_ATTN_LDS_I16 = 2   /* fused, K and V in LDS as their int16 accumulators with
+                                      per-token scales (d = 64, 128, longer words) */
+} aecct_layered_attention;
+
 typedef struct aecct_options {
   int32_t first_ring_heads;  /* h_f, 0..heads; -1 = heads / 2 (the paper's default split) */
   int32_t d_ff;              /* feed-forward width; -1 = 4 d */
@@ -163,6 +173,8 @@ typedef struct aecct_model_info {
   int64_t nnz_second_ring;   /* same for the second-ring mask (diagonal included) */
   size_t device_bytes;       /* device memory held by the model */
   int32_t attention;         /* aecct_attention (first_ring_heads reads 0 under CASA) */
+  int32_t layered_attention; /* aecct_layered_attention: how the layered path runs a layer's
+                                projection and attention (reported whatever path resolved) */
 } aecct_model_info;
 aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info);
 

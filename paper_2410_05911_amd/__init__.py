@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libaecct.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_WORKSPACE_TOO_SMALL = range(6)
 PATH_AUTO, PATH_LAYERED, PATH_FUSED = 0, 1, 2
 ATTN_HPSA, ATTN_CASA = 0, 1
+LAYERED_ATTN_UNFUSED, LAYERED_ATTN_LDS_F32, LAYERED_ATTN_LDS_I16 = 0, 1, 2
 LIN_Q, LIN_K, LIN_V, LIN_O, LIN_FF1, LIN_FF2 = range(6)
 
 _vp = C.c_void_p
@@ -35,14 +36,14 @@ class Weights(C.Structure):
 
 class Options(C.Structure):
     _fields_ = [("first_ring_heads", C.c_int32), ("d_ff", C.c_int32), ("ln_eps", C.c_float), ("path", C.c_int32),
-                ("attention", C.c_int32)]
+                ("attention", C.c_int32), ("layered_attention", C.c_int32)]
 
 
 class ModelInfo(C.Structure):
     _fields_ = [("n", C.c_int32), ("m", C.c_int32), ("L", C.c_int32), ("d", C.c_int32), ("n_layers", C.c_int32),
                 ("heads", C.c_int32), ("first_ring_heads", C.c_int32), ("d_ff", C.c_int32), ("path", C.c_int32),
                 ("nnz_first_ring", C.c_int64), ("nnz_second_ring", C.c_int64), ("device_bytes", C.c_size_t),
-                ("attention", C.c_int32)]
+                ("attention", C.c_int32), ("layered_attention", C.c_int32)]
 
 
 class AecctError(RuntimeError):

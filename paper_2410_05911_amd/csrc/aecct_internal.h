@@ -112,6 +112,11 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
 bool qkv_attention_supported(const Model &M);
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                 float *o, int8_t *oq, float *ao, bool lane_order, hipStream_t s);
+// The same with keys and values kept in LDS as int16 accumulators (words too long for the fp32
+// form, up to about 1800 tokens): writes O in fp32 only.
+bool qkv_attention_i16_supported(const Model &M);
+hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                    float *o, bool lane_order, hipStream_t s);
 // Eq. 2 of the attention output (given as fp32 o, or already as codes oq with scales ao: exactly
 // one of o and oq is not null; natural layout), O-projection, residual, LN1, FFN with ReLU,
 // residual, LN2 and Eq. 2 of the next layer's input in one kernel (d = 64, 128): one wavefront

@@ -766,6 +766,15 @@ void aecct_destroy(aecct_model *model) {
   delete model;
 }
 
+// The layered decode's projection + attention form: fused with fp32 keys and values in LDS when
+// they fit, else (with the token block, which takes O in fp32) with int16 accumulators, else the
+// separate GEMM and attention kernels.
+static int32_t layered_attention_form(const Model &M) {
+  if (aecct::qkv_attention_supported(M)) return AECCT_LAYERED_ATTN_LDS_F32;
+  if (aecct::token_block_supported(M) && aecct::qkv_attention_i16_supported(M)) return AECCT_LAYERED_ATTN_LDS_I16;
+  return AECCT_LAYERED_ATTN_UNFUSED;
+}
+
 aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
   if (!model || !info) return AECCT_ERR_INVALID_ARG;
   const Model &M = model->M;
@@ -773,6 +782,7 @@ aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
   info->heads = M.heads; info->first_ring_heads = M.hf; info->d_ff = M.dff; info->path = M.path;
   info->nnz_first_ring = M.nnz1; info->nnz_second_ring = M.nnz2; info->device_bytes = M.device_bytes;
   info->attention = M.attention;
+  info->layered_attention = layered_attention_form(M);
   return AECCT_OK;
 }
 
@@ -810,22 +820,26 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
     // With the token block, X and Xq are kept in its lane order from the embedding to the head.
-    // The fused projection + attention leaves O in fp32 (in the QKV space); the token block then
-    // applies Eq. 2 itself. The unfused attention quantises O as it writes it (a quarter of the
-    // bytes).
-    const bool tb = aecct::token_block_supported(M), qa = aecct::qkv_attention_supported(M);
+    // The fused projection + attention (keys and values in LDS as fp32, or as int16 accumulators
+    // for long words) leaves O in fp32 (in the QKV space); the token block then applies Eq. 2
+    // itself. The unfused attention quantises O as it writes it (a quarter of the bytes).
+    const bool tb = aecct::token_block_supported(M);
+    const int32_t form = layered_attention_form(M);
+    const bool qa = form == AECCT_LAYERED_ATTN_LDS_F32, qw = form == AECCT_LAYERED_ATTN_LDS_I16;
     hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, tb, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
       if (qa) {
         e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, tb, s);
+      } else if (qw) {
+        e = aecct::launch_qkv_attention_i16(M, l, xq, ax, nw, qkv, tb, s);
       } else {
         e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, tb, s);
         if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
       }
       if (e != hipSuccess) break;
       if (tb) {
-        e = qa ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
-               : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
+        e = qa || qw ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
+                     : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
         if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);

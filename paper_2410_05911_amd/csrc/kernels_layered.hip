@@ -573,6 +573,158 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// The same projection and attention for words whose keys and values of a head group do not fit
+// LDS in fp32 (d = 64, 128 with up to about 1800 tokens).  Keys and values stay in LDS as their
+// exact int32 accumulators, which fit int16 (|acc| <= 127 d < 2^15), with each token's two
+// dequantisation scales (alpha * s_k / 127, alpha * s_v / 127); every gather rebuilds the fp32
+// key and value with the same fma(acc, scale, bias) the projection would have applied, so the
+// results are those of k_attention bit for bit.  Queries go through the output rows in memory:
+// the projection writes the group's queries where the group's attention outputs will go, and
+// each row's thread reads its query there before overwriting it with the output.
+// ------------------------------------------------------------------------------------------
+constexpr int kQwRow = 40;   // int16 per token: key (16), value (16), pad; 80 bytes apart
+
+template <int D>
+size_t qkv_attention_i16_lds_bytes(int L) {
+  return qa_frag_bytes<D>() + (size_t)L * (kQwRow * 2 + 8);
+}
+
+// One neighbour: kw points at the neighbour's key accumulators (d_h int16, 16-byte aligned), its
+// value accumulators 16 int16 further; c = its (key, value) scales; bk, bv the head's biases.
+template <int DH>
+__device__ __forceinline__ void qw_step(const float (&q)[DH], const int16_t *kw, float2 c, const float (&bk)[DH],
+                                        const float (&bv)[DH], float shift, float &S, float (&acc)[DH]) {
+  float k[DH], v[DH];
+#pragma unroll
+  for (int t = 0; t < DH; t += 8) {
+    const uint4 a = *(const uint4 *)(kw + t), b = *(const uint4 *)(kw + 16 + t);
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      k[t + 2 * u] = __builtin_fmaf((float)(int)(short)(aw[u] & 0xffffu), c.x, bk[t + 2 * u]);
+      k[t + 2 * u + 1] = __builtin_fmaf((float)((int)aw[u] >> 16), c.x, bk[t + 2 * u + 1]);
+      v[t + 2 * u] = __builtin_fmaf((float)(int)(short)(bw[u] & 0xffffu), c.y, bv[t + 2 * u]);
+      v[t + 2 * u + 1] = __builtin_fmaf((float)((int)bw[u] >> 16), c.y, bv[t + 2 * u + 1]);
+    }
+  }
+  const float ex = softmax_exp2(head_dot<DH>(q, k) - shift);
+  S = S + ex;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+}
+
+template <int D, int DH>
+__global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, R = kQwRow, NWV = kQaThreads / 64;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int L = p.L, ntiles = (L + 15) / 16;
+  uint64_t *bf = (uint64_t *)smem;                                   // [3][S][64] weight fragments
+  int16_t *kvw = (int16_t *)(smem + qa_frag_bytes<D>());             // [L][R] key, value accumulators
+  float2 *cs = (float2 *)(kvw + (size_t)L * R);                      // [L] key, value scales
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
+  if (blockIdx.x >= p.words) return;
+  {
+    QaStage<D> st;
+    st.load(p.bpack, 0, tid);
+    st.store(bf, tid);
+  }
+  __syncthreads();
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    const int8_t *xw = p.xq + w * L * D;
+    const float *aw = p.ax + w * L;
+    float *ow = p.o + w * L * D;
+    for (int hg = 0; hg < G; ++hg) {
+      const float bq = p.bias[16 * hg + col];
+      for (int tt = wave; tt < ntiles; tt += NWV) {
+        long a[S];
+        float al[4];
+        qa_load_tile<D>(xw, aw, tt, L, lane, a, al);
+        v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          aq = mfma_i8_16x16x32(a[s], (long)bf[(0 * S + s) * 64 + lane], aq);
+          ak = mfma_i8_16x16x32(a[s], (long)bf[(1 * S + s) * 64 + lane], ak);
+          av = mfma_i8_16x16x32(a[s], (long)bf[(2 * S + s) * 64 + lane], av);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * tt + 4 * rg + i;
+          if (tok < L) {
+            ow[(size_t)tok * D + 16 * hg + col] = __builtin_fmaf((float)aq[i], al[i] * p.sq[0], bq);
+            kvw[tok * R + col] = (int16_t)ak[i];
+            kvw[tok * R + 16 + col] = (int16_t)av[i];
+            if (hg == 0 && col == 0) cs[tok] = make_float2(al[i] * p.sq[1], al[i] * p.sq[2]);
+          }
+        }
+      }
+      __syncthreads();   // also orders the queries written to memory before their rows read them
+      const bool more = hg + 1 < G || w + gridDim.x < p.words;
+      QaStage<D> st;
+      if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
+      for (int r = tid; r < L * HPG; r += kQaThreads) {
+        const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
+        const bool first = h < p.hf;
+        const int2 mt = (first ? p.meta1 : p.meta2)[i];
+        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
+        const int cnt = mt.y;
+        float *orow = ow + (size_t)i * D + h * DH;
+        float q[DH], bk[DH], bv[DH];
+#pragma unroll
+        for (int t = 0; t < DH; t += 4) {
+          const float4 a = *(const float4 *)(orow + t);
+          const float4 b = *(const float4 *)(p.bias + D + h * DH + t);
+          const float4 c = *(const float4 *)(p.bias + 2 * D + h * DH + t);
+          q[t] = a.x; q[t + 1] = a.y; q[t + 2] = a.z; q[t + 3] = a.w;
+          bk[t] = b.x; bk[t + 1] = b.y; bk[t + 2] = b.z; bk[t + 3] = b.w;
+          bv[t] = c.x; bv[t + 1] = c.y; bv[t + 2] = c.z; bv[t + 3] = c.w;
+        }
+        const int16_t *kb = kvw + hh * DH;
+        float S_ = 0.0f, acc[DH];
+#pragma unroll
+        for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+        uint2 nx = eg[0];
+        for (int u = 0; u < (cnt >> 2); ++u) {
+          const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+          nx = eg[u + 1];             // stored: every list has a group after its last full one
+          qw_step<DH>(q, kb + e0 * R, cs[e0], bk, bv, 0.0f, S_, acc);
+          qw_step<DH>(q, kb + e1 * R, cs[e1], bk, bv, 0.0f, S_, acc);
+          qw_step<DH>(q, kb + e2 * R, cs[e2], bk, bv, 0.0f, S_, acc);
+          qw_step<DH>(q, kb + e3 * R, cs[e3], bk, bv, 0.0f, S_, acc);
+        }
+        const int rem = cnt & 3;
+        if (rem > 0) { const uint32_t e = nx.x & 0xffffu; qw_step<DH>(q, kb + e * R, cs[e], bk, bv, 0.0f, S_, acc); }
+        if (rem > 1) { const uint32_t e = nx.x >> 16; qw_step<DH>(q, kb + e * R, cs[e], bk, bv, 0.0f, S_, acc); }
+        if (rem > 2) { const uint32_t e = nx.y & 0xffffu; qw_step<DH>(q, kb + e * R, cs[e], bk, bv, 0.0f, S_, acc); }
+        if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
+          float mu = -INFINITY;
+          for (int e = 0; e < cnt; ++e) {
+            const uint32_t j = qa_entry(eg, e);
+            const float cx = cs[j].x;
+            float k[DH];
+#pragma unroll
+            for (int t = 0; t < DH; ++t) k[t] = __builtin_fmaf((float)kb[j * R + t], cx, bk[t]);
+            mu = fmaxf(mu, head_dot<DH>(q, k));
+          }
+          S_ = 0.0f;
+#pragma unroll
+          for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
+          for (int e = 0; e < cnt; ++e) {
+            const uint32_t j = qa_entry(eg, e);
+            qw_step<DH>(q, kb + j * R, cs[j], bk, bv, mu, S_, acc);
+          }
+        }
+        const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
+#pragma unroll
+        for (int t = 0; t < DH; t += 4)
+          *(float4 *)(orow + t) = make_float4(acc[t] * rS, acc[t + 1] * rS, acc[t + 2] * rS, acc[t + 3] * rS);
+      }
+      if (more) st.store(bf, tid);
+      __syncthreads();
+    }
+  }
+}
+
 // Eq. 2 per row of an fp32 [rows][D] matrix: 16 lanes per row, lane c holding the D / 16
 // consecutive features from c D / 16; alpha = max |x| (order-free), codes as everywhere.
 template <int D>
@@ -1147,6 +1299,55 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   if (M.d == 64) hipLaunchKernelGGL(k_quant_rows<64>, grid, dim3(256), 0, s, o, rows, oq, ao);
   else hipLaunchKernelGGL(k_quant_rows<128>, grid, dim3(256), 0, s, o, rows, oq, ao);
   return hipGetLastError();
+}
+
+bool qkv_attention_i16_supported(const Model &M) {
+  if (!((M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped)) return false;
+  const size_t lds = M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L);
+  return lds <= 160 * 1024;
+}
+
+template <int D, int DH>
+static hipError_t run_qkv_attention_i16(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_i16<D, DH>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+  hipLaunchKernelGGL((k_qkv_attention_i16<D, DH>), dim3((unsigned)blocks), dim3(kQaThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                    float *o, bool lane_order, hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  if (!qkv_attention_i16_supported(M)) return hipErrorInvalidValue;
+  const LayerWeights &W = M.layer[layer];
+  if (lane_order && !W.qkv_tb) return hipErrorInvalidValue;
+  QkvAttnArgs a{};
+  a.xq = xq;
+  a.ax = ax;
+  a.bpack = lane_order ? W.qkv_tb : W.qkv;
+  a.bias = W.b_qkv;
+  a.sq[0] = W.sq_qs;
+  a.sq[1] = W.sq[1];
+  a.sq[2] = W.sq[2];
+  a.words = words;
+  a.L = M.L;
+  a.hf = M.hf;
+  a.meta1 = (const int2 *)M.g1_meta; a.meta2 = (const int2 *)M.g2_meta;
+  a.tab1 = (const uint2 *)M.g1_tab; a.tab2 = (const uint2 *)M.g2_tab;
+  a.o = o;
+  const size_t lds = M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L);
+  if (M.d == 64 && M.dh == 8) return run_qkv_attention_i16<64, 8>(a, lds, s);
+  if (M.d == 128 && M.dh == 16) return run_qkv_attention_i16<128, 16>(a, lds, s);
+  if (M.d == 128 && M.dh == 8) return run_qkv_attention_i16<128, 8>(a, lds, s);
+  if (M.d == 64 && M.dh == 16) return run_qkv_attention_i16<64, 16>(a, lds, s);
+  return hipErrorInvalidValue;
 }
 
 bool token_block_supported(const Model &M) {

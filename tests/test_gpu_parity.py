@@ -351,10 +351,14 @@ def _random_parity_check(m, n, seed, col_weight=3):
 
 @pytest.mark.parametrize("d,m,n,hf,attention", [(64, 21, 47, 4, "hpsa"), (64, 13, 30, 2, "hpsa"),
                                                  (128, 25, 51, 4, "hpsa"), (128, 9, 20, 6, "casa"),
-                                                 (64, 40, 90, 0, "hpsa"), (128, 37, 70, 8, "hpsa")])
+                                                 (64, 40, 90, 0, "hpsa"), (128, 37, 70, 8, "hpsa"),
+                                                 (64, 100, 201, 4, "hpsa"), (64, 131, 263, 2, "casa"),
+                                                 (128, 200, 401, 4, "hpsa"), (128, 255, 510, 6, "hpsa")])
 def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attention):
     """d = 64 and 128 on token counts L = n + m that are not multiples of 16 (partial token
-    tiles in the fused projection/attention kernel), several head splits and CASA."""
+    tiles in the fused projection/attention kernels), several head splits and CASA.  Words of up
+    to 256 (d = 64) or 512 (d = 128) tokens keep keys and values in LDS as fp32; the longer ones
+    (L = 301, 394, 601, 765) as int16 accumulators."""
     from workloads import random_weights
     print(f"[wide] d {d} m {m} n {n} hf {hf} {attention}", flush=True)
     H = _random_parity_check(m, n, seed=m * 131 + n)
@@ -364,8 +368,46 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
     bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
     dec = P.Decoder(H, w)
     assert dec.path == P.PATH_LAYERED
+    long_word = m + n > (256 if d == 64 else 512)
+    assert dec.info.layered_attention == (P.LAYERED_ATTN_LDS_I16 if long_word else P.LAYERED_ATTN_LDS_F32)
     bits, logits = dec.decode(_dev(y))
     _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("regime", ["mixed", "underflow", "zero_values"])
+def test_long_words_shifted_softmax(P, oracle_mod, regime, d):
+    """The int16 key/value form on long words (L = 601) with rows that take the max-shifted
+    softmax (some or all), and with a zero value map (O = 0, Eq. 2 scale 0)."""
+    from workloads import random_weights
+    print(f"[long softmax] d {d} {regime}", flush=True)
+    m, n = 200, 401
+    H = _random_parity_check(m, n, seed=17)
+    w = random_weights(n, m, d, 2, 8, seed=23)
+    if regime == "mixed":
+        w.scale[:, 0:2] *= np.float32(5.0)
+    elif regime == "underflow":
+        w.b["q"][:] = np.float32(6.0)
+        w.b["k"][:] = np.float32(-6.0)
+    else:
+        w.scale[:, 2] = np.float32(0.0)
+        w.b["v"][:] = np.float32(0.0)
+    rng = np.random.default_rng(6)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (21, n)) + 0.6 * rng.standard_normal((21, n))).astype(np.float32)
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
+    assert np.isfinite(fo).all()
+    dec = P.Decoder(H, w)
+    assert dec.info.layered_attention == P.LAYERED_ATTN_LDS_I16
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+def test_layered_attention_forms_of_the_workloads(P):
+    """LDPC(128,64) and LDPC(256,128) run keys and values in LDS as fp32, LDPC(1024,512) (1536
+    tokens) as int16 accumulators."""
+    for c, form in ((3, P.LAYERED_ATTN_LDS_F32), (4, P.LAYERED_ATTN_LDS_F32), (5, P.LAYERED_ATTN_LDS_I16)):
+        cfg, H, G, w, y, x, dec = _setup(P, c, 4, P.PATH_LAYERED)
+        assert dec.info.layered_attention == form, c
 
 
 @pytest.mark.parametrize("m,n,hf,attention,with_pos", [
