@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <iterator>
 #include <new>
 #include <vector>
@@ -148,6 +149,125 @@ int64_t chunk_words(const Model &M, int64_t batch) {
   return batch < c ? batch : c;
 }
 
+// Token tiles of the fused path.  In tile t the neighbour loop of head group grp runs
+// T(t, grp) = the longest list of that group among the tile's tokens, so a decode costs
+// sum over tiles of T(t, 0) + T(t, 1) steps.  Given per-token loop lengths w0, w1, this picks
+// NT tiles of at most 16 tokens minimising that sum: a depth-first search over the tiles'
+// (T0, T1) caps, taken as pairs of attained lengths in non-increasing order, pruned by the best
+// cost so far, by tokens no chosen or later cap can cover, and by capacity; a full set of caps
+// is accepted when a token-to-tile assignment within 16 per tile exists (augmenting paths).
+// The search stops after a fixed number of nodes and keeps the best partition found; it
+// starts from tiles filled in order of longest lists.  Returns the token of each slot (-1 for
+// padding).
+std::vector<int32_t> fused_tile_partition(int L, int NT, const std::vector<int> &w0, const std::vector<int> &w1) {
+  struct Cap { int a, b; };
+  auto cost_of = [&](const std::vector<int32_t> &slots) {
+    long c = 0;
+    for (int t = 0; t < NT; ++t) {
+      int a = 0, b = 0;
+      for (int k = 0; k < 16; ++k) {
+        const int tok = slots[16 * t + k];
+        if (tok >= 0) { a = std::max(a, w0[tok]); b = std::max(b, w1[tok]); }
+      }
+      c += a + b;
+    }
+    return c;
+  };
+  auto fill = [&](std::vector<int> order) {
+    std::vector<int32_t> slots(16 * NT, -1);
+    for (int i = 0; i < L; ++i) slots[i] = order[i];
+    return slots;
+  };
+  std::vector<int> order(L);
+  for (int t = 0; t < L; ++t) order[t] = t;
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+    if (w1[x] != w1[y]) return w1[x] > w1[y];
+    return w0[x] > w0[y];
+  });
+  std::vector<int32_t> best = fill(order);
+  long best_cost = cost_of(best);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return w0[x] + w1[x] > w0[y] + w1[y]; });
+  {
+    std::vector<int32_t> s2 = fill(order);
+    const long c2 = cost_of(s2);
+    if (c2 < best_cost) { best = s2; best_cost = c2; }
+  }
+  std::vector<int> va(w0.begin(), w0.end()), vb(w1.begin(), w1.end());
+  std::sort(va.begin(), va.end());
+  va.erase(std::unique(va.begin(), va.end()), va.end());
+  std::sort(vb.begin(), vb.end());
+  vb.erase(std::unique(vb.begin(), vb.end()), vb.end());
+  std::vector<Cap> caps;
+  for (int b : vb)
+    for (int a : va) caps.push_back({a, b});
+  std::sort(caps.begin(), caps.end(), [](const Cap &x, const Cap &y) { return x.b != y.b ? x.b > y.b : x.a > y.a; });
+  const int nc = (int)caps.size();
+  // assignment of every token to one of the chosen caps, at most 16 per tile
+  std::vector<int> assign(L), load(NT);
+  auto feasible = [&](const std::vector<Cap> &cs) {
+    std::vector<std::vector<int>> opts(L);
+    for (int t = 0; t < L; ++t)
+      for (int k = 0; k < NT; ++k)
+        if (w0[t] <= cs[k].a && w1[t] <= cs[k].b) opts[t].push_back(k);
+    std::fill(assign.begin(), assign.end(), -1);
+    std::fill(load.begin(), load.end(), 0);
+    std::vector<char> seen(NT);
+    std::function<bool(int)> aug = [&](int t) -> bool {
+      for (int k : opts[t]) {
+        if (seen[k]) continue;
+        seen[k] = 1;
+        if (load[k] < 16) { ++load[k]; assign[t] = k; return true; }
+        for (int u = 0; u < L; ++u)
+          if (assign[u] == k && aug(u)) { assign[t] = k; return true; }
+      }
+      return false;
+    };
+    std::vector<int> ord(L);
+    for (int t = 0; t < L; ++t) ord[t] = t;
+    std::sort(ord.begin(), ord.end(), [&](int x, int y) { return opts[x].size() < opts[y].size(); });
+    for (int t : ord) {
+      std::fill(seen.begin(), seen.end(), 0);
+      if (!aug(t)) return false;
+    }
+    return true;
+  };
+  std::vector<Cap> chosen;
+  std::vector<int> cover(L, 0);                // chosen caps covering each token
+  long nodes = 0;
+  const long kMaxNodes = 20000;
+  std::function<void(int, long)> dfs = [&](int j, long sum) {
+    if (++nodes > kMaxNodes) return;
+    const int k = (int)chosen.size();
+    // tokens no chosen cap covers: later caps (b no larger than caps[j].b) must take them
+    int unc = 0, unc_b = -1, unc_lb = 0;
+    for (int t = 0; t < L; ++t)
+      if (!cover[t]) { ++unc; unc_b = std::max(unc_b, w1[t]); unc_lb = std::max(unc_lb, w0[t] + w1[t]); }
+    if (k == NT) {
+      if (unc == 0 && sum < best_cost && feasible(chosen)) {
+        std::vector<int32_t> slots(16 * NT, -1);
+        std::vector<int> fillk(NT, 0);
+        for (int t = 0; t < L; ++t) slots[16 * assign[t] + fillk[assign[t]]++] = t;
+        const long c = cost_of(slots);
+        if (c < best_cost) { best = slots; best_cost = c; }
+      }
+      return;
+    }
+    if (unc > 16 * (NT - k) || sum + unc_lb >= best_cost) return;
+    for (int i = j; i < nc; ++i) {
+      if (caps[i].b < unc_b) break;            // caps are ordered by b: none later covers them
+      if (sum + caps[i].a + caps[i].b >= best_cost) continue;
+      chosen.push_back(caps[i]);
+      for (int t = 0; t < L; ++t) cover[t] += w0[t] <= caps[i].a && w1[t] <= caps[i].b;
+      dfs(i, sum + caps[i].a + caps[i].b);
+      for (int t = 0; t < L; ++t) cover[t] -= w0[t] <= caps[i].a && w1[t] <= caps[i].b;
+      chosen.pop_back();
+      if (nodes > kMaxNodes) return;
+    }
+  };
+  dfs(0, 0);
+  return best;
+}
+
 // Host image of the fused path's tables.  Lane layout (see kernel_fused.hip): lane group g
 // of token slot c holds, for maps feeding a LayerNorm, feature 16 o + 4 i + g in register
 // v = 4 o + i; the query / key / value maps are unpermuted (row r of output tile o is
@@ -174,22 +294,17 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
     return mask == 0 ? m1_ptr[tok + 1] - m1_ptr[tok] : m2_ptr[tok + 1] - m2_ptr[tok];
   };
   auto mask_of = [&](int head) { return head < M.hf ? 0 : 1; };
-  // token slots: tiles of 16 tokens taken in order of longest second-group lists first, then
-  // longest first-group lists (similar loop lengths within a tile)
-  std::vector<int> order(L);
-  for (int t = 0; t < L; ++t) order[t] = t;
   auto work = [&](int tok, int grp) {
     int mx = 0;
     for (int g = 0; g < 4; ++g) mx = std::max(mx, len(mask_of(4 * grp + g), tok));
     return mx;
   };
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
-    const int a2 = work(a, 1), b2 = work(b, 1);
-    if (a2 != b2) return a2 > b2;
-    return work(a, 0) > work(b, 0);
-  });
-  F.slot_token.assign(S, -1);
-  for (int sl = 0; sl < L; ++sl) F.slot_token[sl] = order[sl];
+  // token slots: tiles chosen to minimise the padded neighbour-loop steps
+  {
+    std::vector<int> w0(L), w1(L);
+    for (int t = 0; t < L; ++t) { w0[t] = work(t, 0); w1[t] = work(t, 1); }
+    F.slot_token = fused_tile_partition(L, NT, w0, w1);
+  }
   // Per tile and head group the neighbour loop runs T = the longest list among the tile's
   // lanes (padding slots have none).
   F.tile_tab.assign(2 * NT, 0);
