@@ -12,7 +12,7 @@
  *   SEQ         left-to-right from 0 in ascending index;
  *   DOT         q.k as a multiply followed by fused multiply-adds in ascending
  *               index order;
- *   EXP2        oracle_exp2 below (2^x, economised degree-5 series);
+ *   EXP2        oracle_exp2 below (2^x, floor split, minimax degree-5 polynomial);
  *   RSQRT       oracle_rsqrt below (three Newton steps from a bit-level seed).
  */
 #include "aecct_oracle.h"
@@ -49,42 +49,28 @@ float oracle_tree_sum(const float *v, int32_t w) {
  * 2^x, the exponential of the attention softmax (Section 3, CASA; Section 4.2,
  * HPSA) taken in base 2: softmax(s) = 2^(s log2 e) / sum, with log2 e folded
  * into the scores.  x is clamped to [-125, 128] (the result stays a normal
- * number or becomes +inf from 2^128 on, and k below fits an int), split
- * exactly into k = rint(x) and r = x - k in [-1/2, 1/2];
- * 2^r = e^(r ln 2) is its degree-7 Taylor series (c_j = (ln 2)^j / j!)
- * economised to degree 5 by Chebyshev's method (Lanczos), |2r| <= 1:
- * subtracting c7 T7(2r) / 8192, T7(u) = 64u^7 - 112u^5 + 56u^3 - 7u, cancels
- * r^7 and moves c7 * 3584/8192 into c5, -c7 * 448/8192 into c3 and
- * c7 * 14/8192 into c1; subtracting c6 T6(2r) / 2048, T6(u) = 32u^6 - 48u^4
- * + 18u^2 - 1, cancels r^6 and moves c6 * 768/2048 into c4 and
- * -c6 * 72/2048 into c2 (its constant c6 / 2048 is left out so that 2^0 is
- * exactly 1).  Added error below c6/1024 + c7/8192 < 1.6e-7; Horner with
- * fp32-rounded coefficients, then the exact scaling by 2^k.
+ * number or becomes +inf from 2^128 on, and k below fits an int), split into
+ * k = floor(x) and r = min(x - k, 1 - 2^-24) in [0, 1) (x - k is exact except
+ * for x in (-1, 0), where it is rounded once and can round up to 1; the min
+ * keeps r below 1 then), and 2^x = 2^k p(r) with
+ *   p(r) = 1 + a1 r + a2 r^2 + a3 r^3 + a4 r^4 + a5 r^5,
+ * the degree-5 polynomial with constant term 1 (so that 2^x is exact at
+ * integers) whose maximum relative error against 2^r on [0, 1] is least
+ * (5.2e-8, found by linear programming over 20000 points of the interval),
+ * coefficients rounded to fp32.  Horner with fmaf, then the exact scaling by
+ * 2^k.
  * Pin: relative error below 3e-7 over [-125, 64]; exact at integers; +inf
  * from 128.
  */
-#define ORC_LN2 0.69314718055994530942
-#define ORC_T(j) ORC_T##j
-#define ORC_T1 (ORC_LN2)
-#define ORC_T2 (ORC_LN2 * ORC_LN2 / 2.0)
-#define ORC_T3 (ORC_LN2 * ORC_LN2 * ORC_LN2 / 6.0)
-#define ORC_T4 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 24.0)
-#define ORC_T5 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 120.0)
-#define ORC_T6 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 720.0)
-#define ORC_T7 (ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 * ORC_LN2 / 5040.0)
-static const float exp2_coef[6] = {
-    1.0f,
-    (float)(ORC_T1 + ORC_T7 * 14.0 / 8192.0),
-    (float)(ORC_T2 - ORC_T6 * 72.0 / 2048.0),
-    (float)(ORC_T3 - ORC_T7 * 448.0 / 8192.0),
-    (float)(ORC_T4 + ORC_T6 * 768.0 / 2048.0),
-    (float)(ORC_T5 + ORC_T7 * 3584.0 / 8192.0)};
+static const float exp2_coef[6] = {1.0f,           0x1.62e4f0p-1f, 0x1.ebd24ep-3f,
+                                   0x1.c98e60p-5f, 0x1.2552ccp-7f, 0x1.f08ff4p-10f};
 
 float oracle_exp2(float x) {
   if (x < -125.0f) x = -125.0f;
   if (x > 128.0f) x = 128.0f;
-  const float k = rintf(x);
-  const float r = x - k;
+  const float k = floorf(x);
+  float r = x - k;
+  if (r > 0x1.fffffep-1f) r = 0x1.fffffep-1f;
   float p = exp2_coef[5];
   for (int j = 4; j >= 0; --j) p = fmaf(p, r, exp2_coef[j]);
   return ldexpf(p, (int)k);

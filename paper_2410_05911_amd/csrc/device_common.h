@@ -77,23 +77,24 @@ __device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_
 
 // 2^x for the base-2 attention softmax: clamp to [-125, 128] (the result stays a normal
 // number, or is +inf from 2^128 on; a NaN argument gives 2^-125, since the median of three
-// with a NaN operand is the minimum of the other two), exact split x = k + r with
-// k = rint(x), r in [-1/2, 1/2], 2^r = e^(r ln 2) by its degree-7 Taylor series
-// (c_j = (ln2)^j / j!) economised to degree 5 with the Chebyshev polynomials T7(2r) / 8192
-// and T6(2r) / 2048, the constant term kept at 1 (coefficients fp32 of: 1,
-// c1 + c7*14/8192, c2 - c6*72/2048, c3 - c7*448/8192, c4 + c6*768/2048,
-// c5 + c7*3584/8192), Horner, then an exact scaling by 2^k.  Relative error below 3e-7.
+// with a NaN operand is the minimum of the other two), split x = k + r with k = floor(x)
+// and r = fract(x) = min(x - floor(x), 1 - 2^-24) in [0, 1) (v_fract_f32; v_cvt_flr_i32_f32
+// gives k as an integer in one instruction), 2^r by p(r) = 1 + a1 r + ... + a5 r^5, the
+// degree-5 polynomial with constant term 1 of least maximum relative error against 2^r on
+// [0, 1] (5.2e-8 before rounding its coefficients to fp32), Horner, then an exact scaling by
+// 2^k.  Relative error below 3e-7; exact at integers.
 __device__ __forceinline__ float softmax_exp2(float x) {
   x = __builtin_amdgcn_fmed3f(x, -125.0f, 128.0f);
-  const float k = __builtin_rintf(x);
-  const float r = x - k;
-  float p = 0x1.5f47d0p-10f;
-  p = __builtin_fmaf(p, r, 0x1.3d0f44p-7f);
-  p = __builtin_fmaf(p, r, 0x1.c6aecep-5f);
-  p = __builtin_fmaf(p, r, 0x1.ebf90ap-3f);
-  p = __builtin_fmaf(p, r, 0x1.62e430p-1f);
+  const float r = __builtin_amdgcn_fractf(x);
+  int k;
+  asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(k) : "v"(x));
+  float p = 0x1.f08ff4p-10f;
+  p = __builtin_fmaf(p, r, 0x1.2552ccp-7f);
+  p = __builtin_fmaf(p, r, 0x1.c98e60p-5f);
+  p = __builtin_fmaf(p, r, 0x1.ebd24ep-3f);
+  p = __builtin_fmaf(p, r, 0x1.62e4f0p-1f);
   p = __builtin_fmaf(p, r, 1.0f);
-  return __builtin_ldexpf(p, (int)k);
+  return __builtin_ldexpf(p, k);
 }
 
 // 1/sqrt(v), v > 0, for LayerNorm: seed 0x5F3759DF - (bits(v) >> 1) (Lomont 2003), then
