@@ -855,6 +855,9 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
        strip += (int64_t)gridDim.x * kTbWaves) {
     const int64_t row0 = strip * 16, tok = row0 + c;
     const bool ok = tok < p.rows;
+    // loads of a padding column read the last row instead: each column's results depend on
+    // that column alone and padding columns are never stored
+    const int64_t tl = ok ? tok : p.rows - 1;
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
@@ -866,8 +869,8 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       float sc;
       if constexpr (OQ) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) bq[s] = ok ? *(const long *)(p.oq + tok * D + 32 * s + 8 * g) : 0;
-        sc = (ok ? p.ao[tok] : 0.0f) * p.sq_o;
+        for (int s = 0; s < S; ++s) bq[s] = *(const long *)(p.oq + tl * D + 32 * s + 8 * g);
+        sc = p.ao[tl] * p.sq_o;
       } else {
         float ov[S][8];
         float om = 0.0f;
@@ -875,7 +878,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         for (int s = 0; s < S; ++s) {
 #pragma unroll
           for (int k = 0; k < 8; k += 4) {
-            const float4 f = ok ? *(const float4 *)(p.o + tok * D + 32 * s + 8 * g + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
             ov[s][k] = f.x; ov[s][k + 1] = f.y; ov[s][k + 2] = f.z; ov[s][k + 3] = f.w;
           }
 #pragma unroll
@@ -898,7 +901,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
         for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)fo[(o * S + s) * 64 + lane], bq[s], acc);
         // the residual: four consecutive values of X in lane order
-        const float4 r = ok ? *(const float4 *)(p.x + tok * D + g * V + 4 * o) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 r = *(const float4 *)(p.x + tl * D + g * V + 4 * o);
         const float res[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -935,19 +938,18 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     }
     // ---- FFN1 with ReLU (twice) feeding FFN2 ----
     const float sc1 = a1 * p.sq_1;
+    // pass 1: the row's ReLU maximum, max(0, F_0, F_1, ...) = max over ReLU(F); adding +0
+    // turns a -0 result into +0, so the cross-lane maximum may compare bit patterns
     float am = 0.0f;
 #pragma unroll 2
-    for (int o = 0; o < TH; ++o) {                          // pass 1: the row's ReLU maximum
+    for (int o = 0; o < TH; ++o) {
       v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
       for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)f1[(o * S + s) * 64 + lane], xb[s], acc);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float f = __builtin_fmaf((float)acc[i], sc1, bias1[16 * o + 4 * g + i]);
-        am = fmaxf(am, f > 0.0f ? f : 0.0f);
-      }
+      for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, bias1[16 * o + 4 * g + i]));
     }
-    am = tb_token_max(am);
+    am = tb_token_max(am + 0.0f);
     const float inv1 = am == 0.0f ? 0.0f : 127.0f / am;
     v4i acc2[TO];
 #pragma unroll
