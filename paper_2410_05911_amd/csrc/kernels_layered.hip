@@ -794,7 +794,32 @@ struct TokenBlockArgs {
   float *ax;                    // [rows]
 };
 
-constexpr int kTbWaves = 16;
+constexpr int kTbWaves = 8;
+// Whether a wavefront reads the next strip's attention output and residual while it runs the
+// current strip's feed-forward block (fp32 O input only).
+constexpr bool kTbPrefetch = true;
+
+// A strip's fp32 inputs as one lane holds them: O features 32 s + 8 g + k (its B-operand
+// slots) and the residual X in lane order (register v = feature 4 v + g).
+template <int D>
+struct TbIn {
+  float o[D / 32][8];
+  float x[D / 4];
+  __device__ __forceinline__ void load(const TokenBlockArgs &p, int64_t tl, int g) {
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s)
+#pragma unroll
+      for (int k = 0; k < 8; k += 4) {
+        const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
+        o[s][k] = f.x; o[s][k + 1] = f.y; o[s][k + 2] = f.z; o[s][k + 3] = f.w;
+      }
+#pragma unroll
+    for (int u = 0; u < D / 4; u += 4) {
+      const float4 r = *(const float4 *)(p.x + tl * D + g * (D / 4) + u);
+      x[u] = r.x; x[u + 1] = r.y; x[u + 2] = r.z; x[u + 3] = r.w;
+    }
+  }
+};
 
 // LDS: the FF1, FF2 and O fragments (9 d^2 bytes), then the six d-vectors and the FF1 bias.
 template <int D>
@@ -850,14 +875,20 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
   const float *vb_o = vec + 0 * D + g * V, *vg1 = vec + 1 * D + g * V, *vb1 = vec + 2 * D + g * V;
   const float *vb_2 = vec + 3 * D + g * V, *vg2 = vec + 4 * D + g * V, *vbb2 = vec + 5 * D + g * V;
-  const int64_t nstrips = (p.rows + 15) / 16;
-  for (int64_t strip = (int64_t)blockIdx.x * kTbWaves + wave; strip < nstrips;
-       strip += (int64_t)gridDim.x * kTbWaves) {
+  const int64_t nstrips = (p.rows + 15) / 16, sstride = (int64_t)gridDim.x * kTbWaves;
+  // loads of a padding column read the last row instead: each column's results depend on
+  // that column alone and padding columns are never stored
+  auto load_row = [&](int64_t st) { const int64_t t = st * 16 + c; return t < p.rows ? t : p.rows - 1; };
+  constexpr bool PF = kTbPrefetch && !OQ;
+  TbIn<D> cur;
+  if constexpr (PF) {
+    if ((int64_t)blockIdx.x * kTbWaves + wave < nstrips) cur.load(p, load_row((int64_t)blockIdx.x * kTbWaves + wave), g);
+  }
+  for (int64_t strip = (int64_t)blockIdx.x * kTbWaves + wave; strip < nstrips; strip += sstride) {
     const int64_t row0 = strip * 16, tok = row0 + c;
     const bool ok = tok < p.rows;
-    // loads of a padding column read the last row instead: each column's results depend on
-    // that column alone and padding columns are never stored
-    const int64_t tl = ok ? tok : p.rows - 1;
+    const int64_t tl = load_row(strip);
+    if constexpr (!PF && !OQ) cur.load(p, tl, g);
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
@@ -872,18 +903,12 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         for (int s = 0; s < S; ++s) bq[s] = *(const long *)(p.oq + tl * D + 32 * s + 8 * g);
         sc = p.ao[tl] * p.sq_o;
       } else {
-        float ov[S][8];
+        const float (&ov)[S][8] = cur.o;
         float om = 0.0f;
 #pragma unroll
-        for (int s = 0; s < S; ++s) {
-#pragma unroll
-          for (int k = 0; k < 8; k += 4) {
-            const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
-            ov[s][k] = f.x; ov[s][k + 1] = f.y; ov[s][k + 2] = f.z; ov[s][k + 3] = f.w;
-          }
+        for (int s = 0; s < S; ++s)
 #pragma unroll
           for (int k = 0; k < 8; ++k) om = fmaxf(om, fabsf(ov[s][k]));
-        }
         om = tb_token_max(om);
         const float oinv = om == 0.0f ? 0.0f : 127.0f / om;
 #pragma unroll
@@ -901,8 +926,14 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
         for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)fo[(o * S + s) * 64 + lane], bq[s], acc);
         // the residual: four consecutive values of X in lane order
-        const float4 r = *(const float4 *)(p.x + tl * D + g * V + 4 * o);
-        const float res[4] = {r.x, r.y, r.z, r.w};
+        float res[4];
+        if constexpr (OQ) {
+          const float4 r = *(const float4 *)(p.x + tl * D + g * V + 4 * o);
+          res[0] = r.x; res[1] = r.y; res[2] = r.z; res[3] = r.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) res[i] = cur.x[4 * o + i];
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int v = 4 * o + i;
@@ -950,6 +981,10 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, bias1[16 * o + 4 * g + i]));
     }
     am = tb_token_max(am + 0.0f);
+    if constexpr (PF) {                                     // the next strip's inputs
+      const int64_t ns = strip + sstride;
+      cur.load(p, load_row(ns < nstrips ? ns : strip), g);
+    }
     const float inv1 = am == 0.0f ? 0.0f : 127.0f / am;
     v4i acc2[TO];
 #pragma unroll
