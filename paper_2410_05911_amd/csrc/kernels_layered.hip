@@ -391,8 +391,27 @@ struct QaStage {
   }
 };
 
-// One neighbour of the base-2 softmax: kr points at the neighbour's key (d_h floats, 16-byte
-// aligned), its value 16 floats further.
+// d_h consecutive floats of LDS (16-byte aligned) into registers.
+template <int DH>
+__device__ __forceinline__ void qa_load(float (&x)[DH], const float *p) {
+#pragma unroll
+  for (int t = 0; t < DH; t += 4) {
+    const float4 a = *(const float4 *)(p + t);
+    x[t] = a.x; x[t + 1] = a.y; x[t + 2] = a.z; x[t + 3] = a.w;
+  }
+}
+
+// One neighbour of the base-2 softmax: score DOT(q', k), weight 2^(s - shift), and the running
+// sums S and acc (ascending neighbours).
+template <int DH>
+__device__ __forceinline__ void qa_step(const float (&q)[DH], const float (&k)[DH], const float (&v)[DH], float shift,
+                                        float &S, float (&acc)[DH]) {
+  const float ex = softmax_exp2(head_dot<DH>(q, k) - shift);
+  S = S + ex;
+#pragma unroll
+  for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+}
+// kr points at the neighbour's key, its value 16 floats further.
 template <int DH>
 __device__ __forceinline__ void qa_step(const float (&q)[DH], const float *kr, float shift, float &S,
                                         float (&acc)[DH]) {
@@ -403,10 +422,7 @@ __device__ __forceinline__ void qa_step(const float (&q)[DH], const float *kr, f
     k[t] = a.x; k[t + 1] = a.y; k[t + 2] = a.z; k[t + 3] = a.w;
     v[t] = b.x; v[t + 1] = b.y; v[t + 2] = b.z; v[t + 3] = b.w;
   }
-  const float ex = softmax_exp2(head_dot<DH>(q, k) - shift);
-  S = S + ex;
-#pragma unroll
-  for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+  qa_step<DH>(q, k, v, shift, S, acc);
 }
 
 __device__ __forceinline__ uint32_t qa_entry(const uint2 *eg, int e) {
@@ -417,7 +433,7 @@ __device__ __forceinline__ uint32_t qa_entry(const uint2 *eg, int e) {
 
 // Attention of one (token, head) row over its cnt neighbours (ascending), entries from eg with
 // the first group already in g0; writes the row's d_h outputs.
-template <int DH>
+template <int DH, bool PIPE>
 __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
                                        float *orow) {
   constexpr int R = kQaRow;
@@ -430,19 +446,48 @@ __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const
   float S_ = 0.0f, acc[DH];
 #pragma unroll
   for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-  uint2 nx = g0;
-  for (int u = 0; u < (cnt >> 2); ++u) {
-    const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
-    nx = eg[u + 1];             // stored: every list has a group after its last full one
-    qa_step<DH>(q, kb + e0 * R, 0.0f, S_, acc);
-    qa_step<DH>(q, kb + e1 * R, 0.0f, S_, acc);
-    qa_step<DH>(q, kb + e2 * R, 0.0f, S_, acc);
-    qa_step<DH>(q, kb + e3 * R, 0.0f, S_, acc);
+  // Software pipelined (PIPE): a neighbour's value and the next neighbour's key are read
+  // before the neighbour's score is computed.  Every list stores a group after its last full
+  // one (unused slots hold token 0), so each look-ahead read stays within the word's rows.
+  // The scheduling barriers keep the compiler from hoisting further reads (their registers
+  // would spill).
+  if constexpr (PIPE) {
+    uint2 gc = g0;
+    float ka[DH], kb_[DH], v[DH];
+    qa_load<DH>(ka, kb + (gc.x & 0xffffu) * R);
+    auto stage = [&](uint32_t cur, uint32_t nxt, float (&kc)[DH], float (&kn)[DH]) {
+      qa_load<DH>(v, kb + cur * R + 16);
+      qa_load<DH>(kn, kb + nxt * R);
+      qa_step<DH>(q, kc, v, 0.0f, S_, acc);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    for (int u = 0; u < (cnt >> 2); ++u) {
+      const uint2 gn = eg[u + 1];
+      stage(gc.x & 0xffffu, gc.x >> 16, ka, kb_);
+      stage(gc.x >> 16, gc.y & 0xffffu, kb_, ka);
+      stage(gc.y & 0xffffu, gc.y >> 16, ka, kb_);
+      stage(gc.y >> 16, gn.x & 0xffffu, kb_, ka);
+      gc = gn;
+    }
+    const int rem = cnt & 3;    // the last, partial group is in gc, its first key in ka
+    if (rem > 0) stage(gc.x & 0xffffu, gc.x >> 16, ka, kb_);
+    if (rem > 1) stage(gc.x >> 16, gc.y & 0xffffu, kb_, ka);
+    if (rem > 2) stage(gc.y & 0xffffu, gc.y >> 16, ka, kb_);
+  } else {
+    uint2 nx = g0;
+    for (int u = 0; u < (cnt >> 2); ++u) {
+      const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+      nx = eg[u + 1];           // stored: every list has a group after its last full one
+      qa_step<DH>(q, kb + e0 * R, 0.0f, S_, acc);
+      qa_step<DH>(q, kb + e1 * R, 0.0f, S_, acc);
+      qa_step<DH>(q, kb + e2 * R, 0.0f, S_, acc);
+      qa_step<DH>(q, kb + e3 * R, 0.0f, S_, acc);
+    }
+    const int rem = cnt & 3;    // the last, partial group is already in nx
+    if (rem > 0) qa_step<DH>(q, kb + (nx.x & 0xffffu) * R, 0.0f, S_, acc);
+    if (rem > 1) qa_step<DH>(q, kb + (nx.x >> 16) * R, 0.0f, S_, acc);
+    if (rem > 2) qa_step<DH>(q, kb + (nx.y & 0xffffu) * R, 0.0f, S_, acc);
   }
-  const int rem = cnt & 3;      // the last, partial group is already in nx
-  if (rem > 0) qa_step<DH>(q, kb + (nx.x & 0xffffu) * R, 0.0f, S_, acc);
-  if (rem > 1) qa_step<DH>(q, kb + (nx.x >> 16) * R, 0.0f, S_, acc);
-  if (rem > 2) qa_step<DH>(q, kb + (nx.y & 0xffffu) * R, 0.0f, S_, acc);
   if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {
     float mu = -INFINITY;
     for (int e = 0; e < cnt; ++e) {
@@ -564,7 +609,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         const int h = hg * HPG + hh0;
         const bool first = h < p.hf;
         const int2 mt = first ? mt1 : mt2;
-        qa_row<DH>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
+        qa_row<DH, D == 128>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
                    mt.y, p.o + (w * L + i0) * D + h * DH);
       }
       if (more) st.store(bf, tid);
