@@ -362,6 +362,14 @@ constexpr int kQaThreads = 512;
 // value sits at a fixed 64-byte offset from its key.
 constexpr int kQaRow = 36;
 
+// Block barrier that orders LDS accesses only: waits for this wave's LDS operations, not for
+// its global stores or loads in flight (the attention outputs and the next weight tiles).
+__device__ __forceinline__ void block_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int D>
 constexpr size_t qa_frag_bytes() { return (size_t)3 * (D / 32) * 64 * 8; }
 // Token tiles a wavefront keeps in registers across a word's head groups (L <= 16 x 8 x 4).
@@ -599,7 +607,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
           qa_project<D>(bf, afr[0], alw[0], tt, L, lane, bq, bk, bv, sq, qs, kv);
         }
       }
-      __syncthreads();
+      block_sync_lds();
       // the fragments were last read before the barrier above: the next group's weights are
       // loaded now and written after the rows
       const bool more = hg + 1 < G || w + gridDim.x < p.words;
@@ -613,7 +621,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
                    mt.y, p.o + (w * L + i0) * D + h * DH);
       }
       if (more) st.store(bf, tid);
-      __syncthreads();
+      block_sync_lds();
     }
   }
 }
@@ -765,7 +773,7 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
           *(float4 *)(orow + t) = make_float4(acc[t] * rS, acc[t + 1] * rS, acc[t + 2] * rS, acc[t + 3] * rS);
       }
       if (more) st.store(bf, tid);
-      __syncthreads();
+      block_sync_lds();            // the next group's projection overwrites keys and values
     }
   }
 }
