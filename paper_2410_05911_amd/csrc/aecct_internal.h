@@ -130,6 +130,9 @@ hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float
                       float *ag, hipStream_t s);
 hipError_t launch_ffn2_ln(const Model &M, int layer, const int8_t *gq, const float *ag, const float *x1,
                           int64_t rows, float *x, int8_t *xq, float *ax, hipStream_t s);
+// The head of a decode: z per token into zbuf (words * L floats), then the word-tiled product.
+hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
+                             float *logits, bool lane_order, float *zbuf, hipStream_t s);
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
                        float *logits, bool lane_order, hipStream_t s);
 hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a, int64_t rows, int32_t *acc,

@@ -962,7 +962,8 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
       }
     }
     if (e == hipSuccess)
-      e = aecct::launch_head(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, tb, s);
+      e = aecct::launch_head_tiled(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, tb,
+                                   a1, s);   // a1 (rows floats) is free once the layers are done
     if (e != hipSuccess) return AECCT_ERR_DEVICE;
   }
   return AECCT_OK;

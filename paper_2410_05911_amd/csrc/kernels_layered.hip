@@ -1151,6 +1151,72 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs p) {
   }
 }
 
+// The same head for a batch of words in two kernels: z per token into a buffer, then
+// f = W_o^T z + b_o as a product tiled over words and outputs, so that each block reads a
+// 64-output strip of W_o once for 16 words instead of once per word.  Every f_o is still the
+// ascending chain acc = fma(z_i, W_o[i][o], acc) from 0 over i = 0 .. L-1, then + b_o.
+template <int D, bool LO>
+__global__ __launch_bounds__(256) void k_head_z(HeadArgs p, int64_t rows, float *z) {
+  constexpr int T = D / 16;
+  const int c = threadIdx.x & 15;
+  for (int64_t r = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4; r < rows; r += (int64_t)gridDim.x * 16) {
+    const float *xr = p.x + r * D;
+    float v[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) v[t] = xr[LO ? lane_order_x<D>(16 * t + c) : 16 * t + c] * p.w1[16 * t + c];
+    const float zr = row16_sum(lane_tree<T>(v)) + p.b1;
+    if (c == 0) z[r] = zr;
+  }
+}
+
+constexpr int kHeadWords = 16, kHeadOuts = 64, kHeadK = 32;
+
+// Block (word tile, output tile): thread (w = tid / 16, j = tid % 16) owns word w and outputs
+// 4 j .. 4 j + 3 of the tile.  Per chunk of 32 tokens the tile's z values and W_o rows are
+// staged in LDS; the chunk length is the same for every thread (the order of the chains).
+__global__ __launch_bounds__(256) void k_head_gemm(HeadArgs p, int64_t words, const float *z) {
+  __shared__ float zs[kHeadK][kHeadWords];
+  __shared__ __attribute__((aligned(16))) float ws[kHeadK][kHeadOuts];
+  const int tid = threadIdx.x, wl = tid >> 4, j = tid & 15;
+  const int64_t w0 = (int64_t)blockIdx.x * kHeadWords;
+  const int o0 = blockIdx.y * kHeadOuts;
+  const int n = p.n, L = p.L;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i0 = 0; i0 < L; i0 += kHeadK) {
+    const int kc = min(kHeadK, L - i0);
+    for (int u = tid; u < kHeadK * kHeadWords; u += 256) {      // z of the tile's words
+      const int k = u / kHeadWords, w = u % kHeadWords;
+      const int64_t wg = w0 + w;
+      zs[k][w] = (k < kc && wg < words) ? z[wg * L + i0 + k] : 0.0f;
+    }
+    for (int u = tid; u < kHeadK * kHeadOuts; u += 256) {       // rows i0 .. i0 + kc - 1 of W_o
+      const int k = u / kHeadOuts, o = u % kHeadOuts;
+      ws[k][o] = (k < kc && o0 + o < n) ? p.wo[(int64_t)(i0 + k) * n + o0 + o] : 0.0f;
+    }
+    __syncthreads();
+    for (int k = 0; k < kc; ++k) {
+      const float zv = zs[k][wl];
+      const float4 wv = *(const float4 *)&ws[k][4 * j];
+      acc[0] = __builtin_fmaf(zv, wv.x, acc[0]);
+      acc[1] = __builtin_fmaf(zv, wv.y, acc[1]);
+      acc[2] = __builtin_fmaf(zv, wv.z, acc[2]);
+      acc[3] = __builtin_fmaf(zv, wv.w, acc[3]);
+    }
+    __syncthreads();
+  }
+  const int64_t w = w0 + wl;
+  if (w >= words) return;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int o = o0 + 4 * j + u;
+    if (o >= n) break;
+    const float f = acc[u] + p.bo[o];
+    const float yv = p.y[w * n + o];
+    p.bits[w * n + o] = (uint8_t)((yv < 0.0f) != (f < 0.0f));
+    if (p.logits) p.logits[w * n + o] = f;
+  }
+}
+
 // ------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------
@@ -1486,6 +1552,30 @@ hipError_t launch_token_block(const Model &M, int layer, const float *o, const i
   if (!oq == !o) return hipErrorInvalidValue;
   if (oq) return M.d == 64 ? run_token_block<64, true>(a, s) : run_token_block<128, true>(a, s);
   return M.d == 64 ? run_token_block<64, false>(a, s) : run_token_block<128, false>(a, s);
+}
+
+hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
+                             float *logits, bool lane_order, float *zbuf, hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
+  HeadArgs a{x, y, M.n, M.L, M.head_w1, M.head_wo, M.head_bo, M.head_b1, bits, logits};
+  const int64_t rows = words * M.L;
+  const unsigned zgrid = (unsigned)std::min<int64_t>((rows + 15) / 16, 256 * 64);
+  switch (M.d) {
+    case 32: hipLaunchKernelGGL((k_head_z<32, false>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf); break;
+    case 64:
+      if (lane_order) hipLaunchKernelGGL((k_head_z<64, true>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf);
+      else hipLaunchKernelGGL((k_head_z<64, false>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf);
+      break;
+    case 128:
+      if (lane_order) hipLaunchKernelGGL((k_head_z<128, true>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf);
+      else hipLaunchKernelGGL((k_head_z<128, false>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  const dim3 grid((unsigned)((words + kHeadWords - 1) / kHeadWords), (unsigned)((M.n + kHeadOuts - 1) / kHeadOuts));
+  hipLaunchKernelGGL(k_head_gemm, grid, dim3(256), 0, s, a, words, (const float *)zbuf);
+  return hipGetLastError();
 }
 
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
