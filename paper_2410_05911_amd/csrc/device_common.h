@@ -75,6 +75,19 @@ __device__ __forceinline__ uint32_t quant_bits(float x, float inv) {
 }
 __device__ __forceinline__ int8_t quant_code(float x, float inv) { return (int8_t)quant_bits(x, inv); }
 
+// Eq. 2 codes of four ReLU outputs from the code patterns of the pre-activations: the low 16
+// bits of a quant_bits pattern are the code as an int16 (1.5 * 2^23 + c for |c| <= 127), so
+// max(code, 0) on two codes at a time (v_pk_max_i16) equals the code of max(x, 0) (inv >= 0, and
+// rounding is monotone); returns the four codes as bytes 0..3.
+typedef short short2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack4_relu(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  short2_t lo = __builtin_bit_cast(short2_t, __builtin_amdgcn_perm(b1, b0, 0x05040100u));
+  short2_t hi = __builtin_bit_cast(short2_t, __builtin_amdgcn_perm(b3, b2, 0x05040100u));
+  lo = __builtin_elementwise_max(lo, (short2_t){0, 0});
+  hi = __builtin_elementwise_max(hi, (short2_t){0, 0});
+  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo), 0x06040200u);
+}
+
 // 2^x for the base-2 attention softmax: clamp to [-125, 128] (the result stays a normal
 // number, or is +inf from 2^128 on; a NaN argument gives 2^-125, since the median of three
 // with a NaN operand is the minimum of the other two), split x = k + r with k = floor(x)

@@ -368,23 +368,23 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
 #pragma unroll
         for (int o = 0; o < 8; ++o) acc[o] = mfma_i8_16x16x32((long)F[(fz::F_FF1 + o) * 64], bop, v4i{0, 0, 0, 0});
         const float sc = al[t] * sq_1;
+        // F1 pre-activations; the ReLU is applied to the maximum (max(0, F...)) and to the codes
         float G[8][4];
         float amax = 0.0f;
 #pragma unroll
         for (int o = 0; o < 8; ++o)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float f = __builtin_fmaf((float)acc[o][i], sc, V[fz::V_BFF1 + 16 * o + 4 * g + i]);
-            G[o][i] = f > 0.0f ? f : 0.0f;
+            G[o][i] = __builtin_fmaf((float)acc[o][i], sc, V[fz::V_BFF1 + 16 * o + 4 * g + i]);
             amax = fmaxf(amax, G[o][i]);
           }
-        amax = cross_max_nonneg(amax);
+        amax = cross_max_nonneg(amax + 0.0f);   // + 0 turns a -0 maximum into +0
         const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
         uint32_t gb[8];
 #pragma unroll
         for (int o = 0; o < 8; ++o)
-          gb[o] = pack4(quant_bits(G[o][0], inv), quant_bits(G[o][1], inv), quant_bits(G[o][2], inv),
-                        quant_bits(G[o][3], inv));
+          gb[o] = pack4_relu(quant_bits(G[o][0], inv), quant_bits(G[o][1], inv), quant_bits(G[o][2], inv),
+                             quant_bits(G[o][3], inv));
         v4i b0 = v4i{0, 0, 0, 0}, b1 = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < 4; ++s) {

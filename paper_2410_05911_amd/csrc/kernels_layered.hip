@@ -1053,12 +1053,11 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       uint32_t b[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float f0 = __builtin_fmaf((float)h0[i], sc1, bias1[16 * (2 * s2) + 4 * g + i]);
-        const float f1v = __builtin_fmaf((float)h1[i], sc1, bias1[16 * (2 * s2 + 1) + 4 * g + i]);
-        b[i] = quant_bits(f0 > 0.0f ? f0 : 0.0f, inv1);
-        b[4 + i] = quant_bits(f1v > 0.0f ? f1v : 0.0f, inv1);
+        b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, bias1[16 * (2 * s2) + 4 * g + i]), inv1);
+        b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, bias1[16 * (2 * s2 + 1) + 4 * g + i]), inv1);
       }
-      const long gb = tb_pack8(b);
+      // ReLU on the codes: the code of max(F, 0) is max(code of F, 0)
+      const long gb = (long)(((uint64_t)pack4_relu(b[4], b[5], b[6], b[7]) << 32) | pack4_relu(b[0], b[1], b[2], b[3]));
 #pragma unroll
       for (int o = 0; o < TO; ++o) acc2[o] = mfma_i8_16x16x32((long)f2[(o * SH + s2) * 64 + lane], gb, acc2[o]);
     }
