@@ -110,6 +110,30 @@ __device__ __forceinline__ float softmax_exp2(float x) {
   return __builtin_ldexpf(p, k);
 }
 
+// 1/s correctly rounded for s in [2^-64, 2^64]: v_rcp_f32, then one Newton step with fused
+// multiply-adds, r + r (1 - s r).  Checked on gfx950 against the IEEE division for every fp32
+// s of that range (no difference).  The softmax sum S is always in it where it is inverted: the
+// unshifted sums are kept only inside [2^-64, 2^64], and a shifted sum lies in [1, count].
+__device__ __forceinline__ float recip_softmax_sum(float s) {
+  const float r = __builtin_amdgcn_rcpf(s);
+  return __builtin_fmaf(__builtin_fmaf(-s, r, 1.0f), r, r);
+}
+
+// The Eq. 2 scale factor fp32(127 / a) for a = alpha >= 0, and 0 for a = 0.  With a = m 2^e,
+// m in [1/2, 1) (v_frexp_mant_f32 / v_frexp_exp_i32_f32, denormals included): q0 = 127
+// v_rcp_f32(m), then the remainder correction q0 + r (127 - m q0) with fused multiply-adds, which
+// equals the IEEE quotient 127 / m for every fp32 m of [2^-100, 2^100] (checked on gfx950), and
+// 127 / a = (127 / m) 2^-e is an exact rescaling: 127 / a is never below 2^-122, so the result is
+// normal or overflows to +inf exactly where the quotient does.
+__device__ __forceinline__ float inv127(float a) {
+  const float m = __builtin_amdgcn_frexp_mantf(a);
+  const int e = __builtin_amdgcn_frexp_expf(a);
+  const float r = __builtin_amdgcn_rcpf(m);
+  const float q0 = 127.0f * r;
+  const float q = __builtin_fmaf(__builtin_fmaf(-m, q0, 127.0f), r, q0);
+  return a == 0.0f ? 0.0f : __builtin_ldexpf(q, -e);
+}
+
 // 1/sqrt(v), v > 0, for LayerNorm: seed 0x5F3759DF - (bits(v) >> 1) (Lomont 2003), then
 // three Newton steps y <- y (3/2 - (v/2) y^2).
 __device__ __forceinline__ float ln_rsqrt(float v) {

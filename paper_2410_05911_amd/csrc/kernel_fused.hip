@@ -100,7 +100,7 @@ __device__ __forceinline__ uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2,
 // (value v in byte v) to two dwords.
 __device__ __forceinline__ float quant8(const float (&x)[8], uint32_t &lo, uint32_t &hi) {
   const float a = token_max_abs(x);
-  const float inv = a == 0.0f ? 0.0f : 127.0f / a;
+  const float inv = inv127(a);
   lo = pack4(quant_bits(x[0], inv), quant_bits(x[1], inv), quant_bits(x[2], inv), quant_bits(x[3], inv));
   hi = pack4(quant_bits(x[4], inv), quant_bits(x[5], inv), quant_bits(x[6], inv), quant_bits(x[7], inv));
   return a;
@@ -201,7 +201,7 @@ __device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t 
       attend_step(q, lds_row(kbase + e), lds_row(kbase + vofs + e), mu, S, acc);
     }
   }
-  const float rS = cnt > 0 ? 1.0f / S : 0.0f;
+  const float rS = cnt > 0 ? recip_softmax_sum(S) : 0.0f;
 #pragma unroll
   for (int t = 0; t < 4; ++t) o[t] = acc[t] * rS;
 }
@@ -379,7 +379,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
             amax = fmaxf(amax, G[o][i]);
           }
         amax = cross_max_nonneg(amax + 0.0f);   // + 0 turns a -0 maximum into +0
-        const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+        const float inv = inv127(amax);
         uint32_t gb[8];
 #pragma unroll
         for (int o = 0; o < 8; ++o)

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
     amax = fmaxf(amax, fabsf(v[tt]));
   }
   amax = row16_max(amax);
-  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+  const float inv = inv127(amax);
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) p.xq[g * D + (LO ? lane_order_q(16 * tt + c) : 16 * tt + c)] = quant_code(v[tt], inv);
   if (c == 0) p.ax[g] = amax;
@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
 #pragma unroll
           for (int t = 0; t < T; ++t) amax = fmaxf(amax, fabsf(v[t]));
           amax = row16_max(amax);
-          const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+          const float inv = inv127(amax);
 #pragma unroll
           for (int t = 0; t < T; ++t) qstage[wave][(4 * rg + i) * NOUT + 16 * t + col] = quant_code(v[t], inv);
           if (col == 0 && ok[i]) p.out_a[r[i]] = amax;
@@ -304,7 +304,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
       for (int t = 0; t < DH; ++t) acc[t] = __builtin_fmaf(ex, vr[t], acc[t]);
     }
   }
-  const float rS = valid ? 1.0f / S : 0.0f;
+  const float rS = valid ? recip_softmax_sum(S) : 0.0f;
   float amax = 0.0f;
 #pragma unroll
   for (int t = 0; t < DH; ++t) {
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs p) {
   }
   for (int off = 1; off < heads; off <<= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
   if (!valid) return;
-  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+  const float inv = inv127(amax);
   int8_t qv[DH];
 #pragma unroll
   for (int t = 0; t < DH; ++t) qv[t] = quant_code(acc[t], inv);
@@ -510,7 +510,7 @@ __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const
     for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
     for (int e = 0; e < cnt; ++e) qa_step<DH>(q, kb + qa_entry(eg, e) * R, mu, S_, acc);
   }
-  const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
+  const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
 #pragma unroll
   for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
 }
@@ -767,7 +767,7 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
             qw_step<DH>(q, kb + j * R, cs[j], bk, bv, mu, S_, acc);
           }
         }
-        const float rS = cnt > 0 ? 1.0f / S_ : 0.0f;
+        const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
 #pragma unroll
         for (int t = 0; t < DH; t += 4)
           *(float4 *)(orow + t) = make_float4(acc[t] * rS, acc[t + 1] * rS, acc[t + 2] * rS, acc[t + 3] * rS);
@@ -801,7 +801,7 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
   for (int u = 0; u < V; ++u) amax = fmaxf(amax, fabsf(v[u]));
   amax = row16_max(amax);
   if (r >= rows) return;
-  const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+  const float inv = inv127(amax);
   uint32_t pk[V / 4];
 #pragma unroll
   for (int u = 0; u < V / 4; ++u)
@@ -963,7 +963,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
           for (int k = 0; k < 8; ++k) om = fmaxf(om, fabsf(ov[s][k]));
         om = tb_token_max(om);
-        const float oinv = om == 0.0f ? 0.0f : 127.0f / om;
+        const float oinv = inv127(om);
 #pragma unroll
         for (int s = 0; s < S; ++s) {
           uint32_t b[8];
@@ -1010,7 +1010,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         amax = fmaxf(amax, fabsf(x1[v]));
       }
       amax = tb_token_max(amax);
-      const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+      const float inv = inv127(amax);
 #pragma unroll
       for (int s = 0; s < S; ++s) {
         uint32_t b[8];
@@ -1038,7 +1038,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       const int64_t ns = strip + sstride;
       cur.load(p, load_row(ns < nstrips ? ns : strip), g);
     }
-    const float inv1 = am == 0.0f ? 0.0f : 127.0f / am;
+    const float inv1 = inv127(am);
     v4i acc2[TO];
 #pragma unroll
     for (int o = 0; o < TO; ++o) acc2[o] = v4i{0, 0, 0, 0};
@@ -1093,7 +1093,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
           *(float4 *)(p.x + tok * D + g * V + u) = make_float4(v2[u], v2[u + 1], v2[u + 2], v2[u + 3]);
       }
       amax = tb_token_max(amax);
-      const float inv = amax == 0.0f ? 0.0f : 127.0f / amax;
+      const float inv = inv127(amax);
       if (ok) {
         // the next layer's codes in lane order: step s's eight codes of this lane as one word
 #pragma unroll
