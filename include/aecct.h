@@ -197,6 +197,24 @@ aecct_status aecct_workspace_size(const aecct_model *model, int64_t batch, size_
 aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits,
                           float *logits, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Device arithmetic self-check (for tests and bring-up; decoding does not need it).  The kernels
+ * compute three quantities with gfx950 instructions whose results the oracle states in IEEE
+ * terms; this compares the two on the current device over every fp32 operand of the ranges the
+ * kernels use and writes, per quantity, the number of operands that differ (0 on a conforming
+ * device):
+ *   counts[0]  the split of 2^x (softmax, Sections 3 and 4.2): v_fract_f32(x) against
+ *              min(x - floor(x), 1 - 2^-24) and v_cvt_flr_i32_f32(x) against floor(x), for x in
+ *              [-126, 129];
+ *   counts[1]  the softmax normaliser: reciprocal plus one fused correction against the IEEE
+ *              quotient 1 / s, for s in [2^-64, 2^64];
+ *   counts[2]  the Eq. 2 scale 127 / alpha (0 for alpha = 0) against the IEEE quotient, for every
+ *              finite alpha >= 0, denormals included.
+ * counts: host uint64_t[3].  Allocates a few bytes of device memory and synchronises the device
+ * (about a second of GPU time).  Errors: INVALID_ARG (NULL counts), DEVICE (no GPU, HIP failure).
+ */
+aecct_status aecct_check_device_arith(uint64_t *counts);
+
 /* Human-readable name of a status code (static string). */
 const char *aecct_status_string(aecct_status status);
 

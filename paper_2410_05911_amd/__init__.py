@@ -94,6 +94,8 @@ def lib():
         L.aecct_ternary_gemm.argtypes = [_vp, C.c_int32, C.c_int32, _vp, C.c_int64, _vp, _vp]
         L.aecct_aap_ternarize.restype = C.c_int
         L.aecct_aap_ternarize.argtypes = [_f32p, C.c_int64, C.c_float, C.c_float, C.c_float, _i8p, _f32p]
+        L.aecct_check_device_arith.restype = C.c_int
+        L.aecct_check_device_arith.argtypes = [C.POINTER(C.c_uint64)]
         _lib = L
     return _lib
 
@@ -108,6 +110,14 @@ def aap_ternarize(w, percentile: float = 0.5, delta: float = 1.0, eps: float = 1
                                      float(np.float32(delta)), float(np.float32(eps)), t.ctypes.data_as(_i8p),
                                      C.byref(sc)), "aecct_aap_ternarize")
     return t, np.float32(sc.value)
+
+
+def check_device_arith():
+    """Counts of fp32 operands where the device's fract/floor split, softmax reciprocal and
+    127/alpha differ from their IEEE definitions (all 0 on a conforming GPU)."""
+    counts = (C.c_uint64 * 3)()
+    _check(lib().aecct_check_device_arith(counts), "aecct_check_device_arith")
+    return tuple(int(c) for c in counts)
 
 
 def _check(status: int, what: str):

@@ -435,3 +435,11 @@ def test_fused_kernel_tile_counts(P, oracle_mod, m, n, hf, attention, with_pos):
     for dec in (fused, P.Decoder(H, w, path=P.PATH_LAYERED)):
         bits, logits = dec.decode(_dev(y))
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
+def test_device_arithmetic_matches_ieee_definitions(P):
+    """The fract/floor split of 2^x, the softmax reciprocal and 127/alpha, computed with gfx950
+    instructions, equal their IEEE definitions (the oracle's) on every fp32 operand of the ranges
+    the kernels use."""
+    fract_floor, recip, inv127 = P.check_device_arith()
+    assert (fract_floor, recip, inv127) == (0, 0, 0)
