@@ -354,6 +354,7 @@ struct QkvAttnArgs {
   const int2 *meta1, *meta2;   // per token: first group, entry count (first ring, second ring)
   const uint2 *tab1, *tab2;    // four 16-bit token indices per group
   float *o;                    // [rows][d]
+  int resident;                // k_qkv_attention: every head group's weight tiles stay in LDS
 };
 
 constexpr int kQaThreads = 512;
@@ -568,14 +569,18 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   constexpr int NWV = kQaThreads / 64;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int L = p.L, ntiles = (L + 15) / 16;
-  uint64_t *bf = (uint64_t *)smem;                           // [3][S][64] weight fragments
-  float *qs = (float *)(smem + qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
+  // weight fragments: [G][3][S][64] when resident (staged once per block), else one group's
+  // [3][S][64], restaged per group
+  constexpr int FW = 3 * S * 64;
+  const bool resident = p.resident != 0;
+  uint64_t *bfa = (uint64_t *)smem;
+  float *qs = (float *)(smem + (resident ? G : 1) * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15;
   if (blockIdx.x >= p.words) return;
-  {
+  for (int hg = 0; hg < (resident ? G : 1); ++hg) {
     QaStage<D> st;
-    st.load(p.bpack, 0, tid);
-    st.store(bf, tid);
+    st.load(p.bpack, hg, tid);
+    st.store(bfa + hg * FW, tid);
   }
   // the thread's row (token i0, head hh0 of the group; L d / (16 d_h) <= kQaThreads rows): its
   // list metadata and first entry group for both masks stay in registers for the whole kernel
@@ -596,6 +601,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
       for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wave + NWV * k, L, lane, afr[k], alw[k]);
     }
     for (int hg = 0; hg < G; ++hg) {
+      const uint64_t *bf = resident ? bfa + hg * FW : bfa;
       const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
       if constexpr (qa_keep_tiles<D>()) {
 #pragma unroll
@@ -608,9 +614,9 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         }
       }
       block_sync_lds();
-      // the fragments were last read before the barrier above: the next group's weights are
-      // loaded now and written after the rows
-      const bool more = hg + 1 < G || w + gridDim.x < p.words;
+      // not resident: the fragments were last read before the barrier above, so the next group's
+      // weights are loaded now and written after the rows
+      const bool more = !resident && (hg + 1 < G || w + gridDim.x < p.words);
       QaStage<D> st;
       if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
       if (row0) {
@@ -620,7 +626,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         qa_row<DH, D == 128>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
                    mt.y, p.o + (w * L + i0) * D + h * DH);
       }
-      if (more) st.store(bf, tid);
+      if (more) st.store(bfa, tid);
       block_sync_lds();
     }
   }
@@ -1397,8 +1403,14 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
   return hipGetLastError();
 }
 
-size_t qkv_attention_lds(const Model &M) {
-  return (size_t)3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
+size_t qkv_attention_lds(const Model &M, bool resident = false) {
+  return (size_t)(resident ? M.d / 16 : 1) * 3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
+}
+
+// Keep every head group's weight tiles in LDS when that does not lower the blocks per CU.
+bool qkv_attention_resident(const Model &M) {
+  const size_t one = qkv_attention_lds(M, false), all = qkv_attention_lds(M, true);
+  return all <= 160 * 1024 && (160 * 1024 / all) >= (160 * 1024 / one);
 }
 
 bool qkv_attention_supported(const Model &M) {
@@ -1442,7 +1454,8 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.meta1 = (const int2 *)M.g1_meta; a.meta2 = (const int2 *)M.g2_meta;
   a.tab1 = (const uint2 *)M.g1_tab; a.tab2 = (const uint2 *)M.g2_tab;
   a.o = o;
-  const size_t lds = qkv_attention_lds(M);
+  a.resident = qkv_attention_resident(M) ? 1 : 0;
+  const size_t lds = qkv_attention_lds(M, a.resident != 0);
   hipError_t e = hipErrorInvalidValue;
   if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
   else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
