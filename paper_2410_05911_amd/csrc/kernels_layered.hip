@@ -592,14 +592,16 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
+  if constexpr (qa_keep_tiles<D>()) {
+    // the wave's token tiles of its first word, used by all head groups of the word; the next
+    // word's are read during the last group's rows
+    const int64_t w = blockIdx.x;
+#pragma unroll
+    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+  }
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
-    if constexpr (qa_keep_tiles<D>()) {
-      // the wave's token tiles, used by all head groups of the word
-#pragma unroll
-      for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wave + NWV * k, L, lane, afr[k], alw[k]);
-    }
     for (int hg = 0; hg < G; ++hg) {
       const uint64_t *bf = resident ? bfa + hg * FW : bfa;
       const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
@@ -614,6 +616,14 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         }
       }
       block_sync_lds();
+      if constexpr (qa_keep_tiles<D>()) {
+        const int64_t wn = w + gridDim.x;
+        if (hg == G - 1 && wn < p.words) {
+#pragma unroll
+          for (int k = 0; k < TW; ++k)
+            qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+        }
+      }
       // not resident: the fragments were last read before the barrier above, so the next group's
       // weights are loaded now and written after the rows
       const bool more = !resident && (hg + 1 < G || w + gridDim.x < p.words);
