@@ -981,11 +981,19 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
   float *lv = (float *)(smem + frag_bytes);
   for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
   for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
-  const float *vec = lv, *bias1 = lv + 6 * D;
+  const float *vec = lv;
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
   const float *vb_o = vec + 0 * D + g * V, *vg1 = vec + 1 * D + g * V, *vb1 = vec + 2 * D + g * V;
   const float *vb_2 = vec + 3 * D + g * V, *vg2 = vec + 4 * D + g * V, *vbb2 = vec + 5 * D + g * V;
+  // Per-lane bases of the FF1 / FF2 fragments and the FF1 bias as opaque byte offsets: each loop
+  // then keeps one running address per array and reaches the rest through the 16-bit immediate
+  // offset of the LDS reads (rather than an add per read past the first 64 KB).
+  uint32_t o_f1 = (uint32_t)lane * 8u, o_f2 = (uint32_t)(TH * S * 64 + lane) * 8u,
+           o_b1 = (uint32_t)(frag_bytes + (size_t)6 * D * 4) + 16u * (uint32_t)g;
+  asm volatile("" : "+v"(o_f1), "+v"(o_f2), "+v"(o_b1));
+  const uint64_t *f1l = (const uint64_t *)(smem + o_f1), *f2l = (const uint64_t *)(smem + o_f2);
+  const float *b1l = (const float *)(smem + o_b1);        // b1l[16 o + i] = FF1 bias 16 o + 4 g + i
   const int64_t nstrips = (p.rows + 15) / 16, sstride = (int64_t)gridDim.x * kTbWaves;
   // loads of a padding column read the last row instead: each column's results depend on
   // that column alone and padding columns are never stored
@@ -1087,9 +1095,9 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     for (int o = 0; o < TH; ++o) {
       v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
-      for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)f1[(o * S + s) * 64 + lane], xb[s], acc);
+      for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)f1l[(o * S + s) * 64], xb[s], acc);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, bias1[16 * o + 4 * g + i]));
+      for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]));
     }
     am = tb_token_max(am + 0.0f);
     if constexpr (PF) {                                     // the next strip's inputs
@@ -1105,19 +1113,19 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
 #pragma unroll
       for (int s = 0; s < S; ++s) {
-        h0 = mfma_i8_16x16x32((long)f1[((2 * s2) * S + s) * 64 + lane], xb[s], h0);
-        h1 = mfma_i8_16x16x32((long)f1[((2 * s2 + 1) * S + s) * 64 + lane], xb[s], h1);
+        h0 = mfma_i8_16x16x32((long)f1l[((2 * s2) * S + s) * 64], xb[s], h0);
+        h1 = mfma_i8_16x16x32((long)f1l[((2 * s2 + 1) * S + s) * 64], xb[s], h1);
       }
       uint32_t b[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, bias1[16 * (2 * s2) + 4 * g + i]), inv1);
-        b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, bias1[16 * (2 * s2 + 1) + 4 * g + i]), inv1);
+        b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, b1l[16 * (2 * s2) + i]), inv1);
+        b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, b1l[16 * (2 * s2 + 1) + i]), inv1);
       }
       // ReLU on the codes: the code of max(F, 0) is max(code of F, 0)
       const long gb = (long)(((uint64_t)pack4_relu(b[4], b[5], b[6], b[7]) << 32) | pack4_relu(b[0], b[1], b[2], b[3]));
 #pragma unroll
-      for (int o = 0; o < TO; ++o) acc2[o] = mfma_i8_16x16x32((long)f2[(o * SH + s2) * 64 + lane], gb, acc2[o]);
+      for (int o = 0; o < TO; ++o) acc2[o] = mfma_i8_16x16x32((long)f2l[(o * SH + s2) * 64], gb, acc2[o]);
     }
     // ---- FFN2 epilogue: residual, LN2, Eq. 2 of the next layer's input ----
     {
