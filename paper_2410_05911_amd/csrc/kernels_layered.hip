@@ -653,7 +653,6 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
 // each row's thread reads its query there before overwriting it with the output.
 // ------------------------------------------------------------------------------------------
 constexpr int kQwRow = 40;   // int16 per token: key (16), value (16), pad; 80 bytes apart
-constexpr int kQwPre = 4;    // rows per thread whose list metadata stay in registers (even)
 
 template <int D>
 size_t qkv_attention_i16_lds_bytes(int L) {
@@ -699,18 +698,6 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
     st.load(p.bpack, 0, tid);
     st.store(bf, tid);
   }
-  // list metadata and first entry group, both masks, of the thread's first kQwPre rows (token
-  // i = r mod L of row r = tid + 512 k); the same for every word and head group
-  int2 pm1[kQwPre], pm2[kQwPre];
-  uint2 pg1[kQwPre], pg2[kQwPre];
-#pragma unroll
-  for (int k = 0; k < kQwPre; ++k) {
-    const int r = tid + k * kQaThreads, i = r < L * HPG ? r % L : 0;
-    pm1[k] = p.meta1[i];
-    pm2[k] = p.meta2[i];
-    pg1[k] = p.tab1[pm1[k].x];
-    pg2[k] = p.tab2[pm2[k].x];
-  }
   __syncthreads();
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
@@ -744,12 +731,14 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
       const bool more = hg + 1 < G || w + gridDim.x < p.words;
       QaStage<D> st;
       if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
-      // Rows r = tid + 512 k of this thread.  The first kQwPre rows' list metadata were read once
-      // per kernel; each row's query (in the output row) and key / value biases are read while
-      // the previous row of the thread runs.
-      auto row_in = [&](int r, float (&q)[DH], float (&bk)[DH], float (&bv)[DH]) {
+      for (int r = tid; r < L * HPG; r += kQaThreads) {
         const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
-        const float *orow = ow + (size_t)i * D + h * DH;
+        const bool first = h < p.hf;
+        const int2 mt = (first ? p.meta1 : p.meta2)[i];
+        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
+        const int cnt = mt.y;
+        float *orow = ow + (size_t)i * D + h * DH;
+        float q[DH], bk[DH], bv[DH];
 #pragma unroll
         for (int t = 0; t < DH; t += 4) {
           const float4 a = *(const float4 *)(orow + t);
@@ -759,18 +748,11 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
           bk[t] = b.x; bk[t + 1] = b.y; bk[t + 2] = b.z; bk[t + 3] = b.w;
           bv[t] = c.x; bv[t + 1] = c.y; bv[t + 2] = c.z; bv[t + 3] = c.w;
         }
-      };
-      auto row = [&](int r, const float (&q)[DH], const float (&bk)[DH], const float (&bv)[DH], int2 mt, uint2 g0) {
-        const int hh = r / L, i = r - hh * L, h = hg * HPG + hh;
-        const bool first = h < p.hf;
-        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
-        const int cnt = mt.y;
-        float *orow = ow + (size_t)i * D + h * DH;
         const int16_t *kb = kvw + hh * DH;
         float S_ = 0.0f, acc[DH];
 #pragma unroll
         for (int t = 0; t < DH; ++t) acc[t] = 0.0f;
-        uint2 nx = g0;
+        uint2 nx = eg[0];
         for (int u = 0; u < (cnt >> 2); ++u) {
           const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
           nx = eg[u + 1];             // stored: every list has a group after its last full one
@@ -805,30 +787,6 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
 #pragma unroll
         for (int t = 0; t < DH; t += 4)
           *(float4 *)(orow + t) = make_float4(acc[t] * rS, acc[t + 1] * rS, acc[t + 2] * rS, acc[t + 3] * rS);
-      };
-      const int nrows = L * HPG;
-      float qa[DH], bka[DH], bva[DH], qb[DH], bkb[DH], bvb[DH];
-      if (tid < nrows) row_in(tid, qa, bka, bva);
-#pragma unroll
-      for (int k = 0; k < kQwPre; k += 2) {
-        const int r0 = tid + k * kQaThreads, r1 = r0 + kQaThreads;
-        if (r1 < nrows) row_in(r1, qb, bkb, bvb);
-        if (r0 < nrows) {
-          const bool first = (hg * HPG + r0 / L) < p.hf;
-          row(r0, qa, bka, bva, first ? pm1[k] : pm2[k], first ? pg1[k] : pg2[k]);
-        }
-        if (r1 + kQaThreads < nrows) row_in(r1 + kQaThreads, qa, bka, bva);
-        if (r1 < nrows) {
-          const bool first = (hg * HPG + r1 / L) < p.hf;
-          row(r1, qb, bkb, bvb, first ? pm1[k + 1] : pm2[k + 1], first ? pg1[k + 1] : pg2[k + 1]);
-        }
-      }
-      for (int r = tid + kQwPre * kQaThreads; r < nrows; r += kQaThreads) {   // rows past the first kQwPre
-        const int hh = r / L, i = r - hh * L;
-        const bool first = (hg * HPG + hh) < p.hf;
-        const int2 mt = (first ? p.meta1 : p.meta2)[i];
-        row_in(r, qa, bka, bva);
-        row(r, qa, bka, bva, mt, (first ? p.tab1 : p.tab2)[mt.x]);
       }
       if (more) st.store(bf, tid);
       block_sync_lds();            // the next group's projection overwrites keys and values
