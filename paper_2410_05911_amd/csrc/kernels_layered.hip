@@ -705,10 +705,12 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
     float *ow = p.o + w * L * D;
     for (int hg = 0; hg < G; ++hg) {
       const float bq = p.bias[16 * hg + col];
+      // the wave's next tile is read while the current one is projected
+      long a[S], an[S];
+      float al[4], aln[4];
+      if (wave < ntiles) qa_load_tile<D>(xw, aw, wave, L, lane, a, al);
       for (int tt = wave; tt < ntiles; tt += NWV) {
-        long a[S];
-        float al[4];
-        qa_load_tile<D>(xw, aw, tt, L, lane, a, al);
+        if (tt + NWV < ntiles) qa_load_tile<D>(xw, aw, tt + NWV, L, lane, an, aln);
         v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < S; ++s) {
@@ -726,6 +728,10 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
             if (hg == 0 && col == 0) cs[tok] = make_float2(al[i] * p.sq[1], al[i] * p.sq[2]);
           }
         }
+#pragma unroll
+        for (int u = 0; u < S; ++u) a[u] = an[u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) al[u] = aln[u];
       }
       __syncthreads();   // also orders the queries written to memory before their rows read them
       const bool more = hg + 1 < G || w + gridDim.x < p.words;
