@@ -155,13 +155,40 @@ __device__ __forceinline__ void attend_step(const float (&q)[4], float4 k, float
 // value 0, so acc is unchanged and S too whenever S >= 2^-64, the only case in which the
 // unshifted sums are kept; a row whose sum leaves [2^-64, 2^64] is redone over its real
 // entries with the scores shifted by their maximum.
+// The first neighbour starts the sums: S = e and acc = e v (the same values as 0 + e and
+// fma(e, v, 0), up to the sign of a zero acc, which no later step or Eq. 2 code can observe).
+__device__ __forceinline__ void attend_first(const float (&q)[4], float4 k, float4 vv, float &S, float (&acc)[4]) {
+  const float kk[4] = {k.x, k.y, k.z, k.w};
+  const float ex = softmax_exp2(head_dot<4>(q, kk));
+  S = ex;
+  acc[0] = ex * vv.x;
+  acc[1] = ex * vv.y;
+  acc[2] = ex * vv.z;
+  acc[3] = ex * vv.w;
+}
+
 __device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t *ent, int cnt, int T,
                                             const unsigned char *kbase, int vofs, float (&o)[4]) {
-  float S = 0.0f, acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  float S, acc[4];
   const uint2 *eg = (const uint2 *)ent;
   const int G = T >> 2;
   uint2 nx = eg[0];
-  for (int u = 0; u < G; ++u) {
+  if (G > 0) {                        // the first group, its first entry starting the sums
+    const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
+    const float4 k0 = lds_row(kbase + e0), v0 = lds_row(kbase + vofs + e0);
+    const float4 k1 = lds_row(kbase + e1), v1 = lds_row(kbase + vofs + e1);
+    const float4 k2 = lds_row(kbase + e2), v2 = lds_row(kbase + vofs + e2);
+    const float4 k3 = lds_row(kbase + e3), v3 = lds_row(kbase + vofs + e3);
+    nx = eg[16];
+    attend_first(q, k0, v0, S, acc);
+    attend_step(q, k1, v1, 0.0f, S, acc);
+    attend_step(q, k2, v2, 0.0f, S, acc);
+    attend_step(q, k3, v3, 0.0f, S, acc);
+  } else {                            // T = 1..3 (T >= 1): the first remainder entry starts them
+    const uint32_t e0 = nx.x & 0xffffu;
+    attend_first(q, lds_row(kbase + e0), lds_row(kbase + vofs + e0), S, acc);
+  }
+  for (int u = 1; u < G; ++u) {
     const uint32_t e0 = nx.x & 0xffffu, e1 = nx.x >> 16, e2 = nx.y & 0xffffu, e3 = nx.y >> 16;
     const float4 k0 = lds_row(kbase + e0), v0 = lds_row(kbase + vofs + e0);
     const float4 k1 = lds_row(kbase + e1), v1 = lds_row(kbase + vofs + e1);
@@ -174,7 +201,7 @@ __device__ __forceinline__ void attend_tile(const float (&q)[4], const uint16_t 
     attend_step(q, k3, v3, 0.0f, S, acc);
   }
   const int rem = T & 3;              // the last, partial group is already in nx
-  if (rem > 0) {
+  if (rem > 0 && G > 0) {             // (with no full group, its first entry started the sums)
     const uint32_t e0 = nx.x & 0xffffu;
     attend_step(q, lds_row(kbase + e0), lds_row(kbase + vofs + e0), 0.0f, S, acc);
   }
