@@ -20,10 +20,9 @@ constexpr int F_O = 6, F_FF1 = 8, F_FF2 = 16;
 constexpr int VEC = 424;       // floats per layer
 constexpr int V_BQKV = 0, V_BO = 96, V_BFF1 = 128, V_BFF2 = 256, V_LN1G = 288, V_LN1B = 320, V_LN2G = 352,
               V_LN2B = 384, V_SQ = 416;
-#ifndef AECCT_FUSED_WAVES
-#define AECCT_FUSED_WAVES 12
-#endif
-constexpr int kWaves = AECCT_FUSED_WAVES;   // wavefronts (words in flight) per block
+// wavefronts (words in flight) per block: 12 of 168 registers each fill the register file; blocks
+// of 8 or 10 waves were measured 18 % slower on BCH(31,16)
+constexpr int kWaves = 12;
 constexpr int kLdsMax = 160 * 1024;
 }  // namespace fz
 
