@@ -443,3 +443,21 @@ def test_device_arithmetic_matches_ieee_definitions(P):
     the kernels use."""
     fract_floor, recip, inv127 = P.check_device_arith()
     assert (fract_floor, recip, inv127) == (0, 0, 0)
+
+
+@pytest.mark.parametrize("d,m,n,layers", [(64, 700, 1301, 2), (128, 700, 1301, 1), (64, 1365, 2731, 1)])
+def test_layered_unfused_attention_long_words(P, oracle_mod, d, m, n, layers):
+    """Words too long for a head group's keys and values in LDS (L = 2001, and L = 4096, the
+    largest token count the library accepts): the Q/K/V GEMM, attention rows gathered from device
+    memory with Eq. 2 of O on the way out, then the token block reading the int8 codes of O."""
+    from workloads import random_weights
+    print(f"[unfused long] d {d} L {m + n}", flush=True)
+    H = _random_parity_check(m, n, seed=29)
+    w = random_weights(n, m, d, layers, 8, seed=31)
+    rng = np.random.default_rng(8)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (3, n)) + 0.7 * rng.standard_normal((3, n))).astype(np.float32)
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.info.layered_attention == P.LAYERED_ATTN_UNFUSED
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits), fo, _np(bits), bo, y)
