@@ -11,7 +11,8 @@
  *               the first half (w a power of two);
  *   SEQ         left-to-right from 0 in ascending index;
  *   DOT         q.k as a multiply followed by fused multiply-adds in ascending
- *               index order;
+ *               index order; a head of 16 dimensions forms its two 8-dimension
+ *               halves that way and adds them (low half + high half);
  *   EXP2        oracle_exp2 below (2^x, floor split, minimax degree-5 polynomial);
  *   RSQRT       oracle_rsqrt below (three Newton steps from a bit-level seed).
  */
@@ -221,7 +222,6 @@ void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float 
   }
 }
 
-/* DOT of a scaled query row segment with a key row segment (ascending dims). */
 /* Whether key j is allowed for row i of head h: HPSA (Section 4.2) gives heads below h_f the
  * first-ring mask and the others the second-ring mask; CASA (Section 3, the ECCT mask) gives
  * every head their union, the nodes at most two steps away including the node itself. */
@@ -232,12 +232,19 @@ static int key_allowed(const oracle_model *M, const uint8_t *M1, const uint8_t *
   return h < M->first_ring_heads ? M1[e] : M2[e];
 }
 
+/* DOT of the scaled query of row i with the key of token j, head h (d_h dims): a multiply then
+ * fused multiply-adds in ascending dims; with d_h = 16 the two 8-dim halves separately, then
+ * their sum. */
+static float dot_seq(const float *q, const float *k, int32_t w) {
+  float s = q[0] * k[0];
+  for (int32_t t = 1; t < w; ++t) s = fmaf(q[t], k[t], s);
+  return s;
+}
 static float score_f32(const float *qkv, int32_t d, int32_t i, int32_t j, int32_t h, int32_t dh) {
   const float *qi = qkv + (int64_t)i * 3 * d + h * dh;
   const float *kj = qkv + (int64_t)j * 3 * d + d + h * dh;
-  float s = qi[0] * kj[0];
-  for (int32_t t = 1; t < dh; ++t) s = fmaf(qi[t], kj[t], s);
-  return s;
+  if (dh == 16) return dot_seq(qi, kj, 8) + dot_seq(qi + 8, kj + 8, 8);
+  return dot_seq(qi, kj, dh);
 }
 
 /*

@@ -148,13 +148,20 @@ __device__ __forceinline__ float ln_rsqrt(float v) {
   return y;
 }
 
-// A head's dot product: q[0] k[0], then fused multiply-adds in ascending order.
-template <int DH>
-__device__ __forceinline__ float head_dot(const float (&q)[DH], const float *k) {
+// A head's dot product: q[0] k[0], then fused multiply-adds in ascending order; a head of 16
+// dimensions takes its two 8-dimension halves that way and adds them (low + high), the order
+// in which two lanes that each hold one half combine them.
+template <int W>
+__device__ __forceinline__ float dot_seq(const float *q, const float *k) {
   float s = q[0] * k[0];
 #pragma unroll
-  for (int t = 1; t < DH; ++t) s = __builtin_fmaf(q[t], k[t], s);
+  for (int t = 1; t < W; ++t) s = __builtin_fmaf(q[t], k[t], s);
   return s;
+}
+template <int DH>
+__device__ __forceinline__ float head_dot(const float (&q)[DH], const float *k) {
+  if constexpr (DH == 16) return dot_seq<8>(q, k) + dot_seq<8>(q + 8, k + 8);
+  else return dot_seq<DH>(q, k);
 }
 
 // 8 ternary codes (2 bits each, 00 -> 0, 01 -> +1, 11 -> -1, code e in bits 2e..2e+1)
