@@ -643,6 +643,149 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
 }
 
 // ------------------------------------------------------------------------------------------
+// The same projection and attention for 16-dimension heads (d = 128) with every attention row
+// split over a lane pair: lane 2 r + h of the block takes dimensions 8 h .. 8 h + 7 of row r (its
+// query, key, value halves), forms its half of the score, and the pair adds the two halves with
+// one DPP exchange (the canonical order: low half + high half, so both lanes hold the same
+// bits); both lanes then compute the same weight and sums, each for its own 8 output
+// dimensions.  Blocks of 12 wavefronts, so that a word of up to 384 tokens fills every lane
+// and three wavefronts per SIMD have rows in flight; every head group's weight tiles resident in
+// LDS.
+// ------------------------------------------------------------------------------------------
+constexpr int kQpThreads = 768;
+constexpr int kQpTilesPerWave = 3;
+
+// the partner lane's value (lane ^ 1) within the quad
+__device__ __forceinline__ float pair_other(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, true));
+}
+
+// One neighbour of a half row: kr points at the neighbour's key half (8 floats), its value half
+// 16 floats further.
+__device__ __forceinline__ void qp_step(const float (&q)[8], const float (&k)[8], const float (&v)[8], float shift,
+                                        float &S, float (&acc)[8]) {
+  const float h = dot_seq<8>(q, k);
+  const float ex = softmax_exp2(h + pair_other(h) - shift);
+  S = S + ex;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+}
+
+// Attention of one half row: qrow, kb and orow already offset to this lane's half; entries as in
+// qa_row, the first group in g0.  Both lanes of a pair run it with the same row.
+__device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
+                                       float *orow) {
+  constexpr int R = kQaRow;
+  float q[8];
+  qa_load<8>(q, qrow);
+  float S_ = 0.0f, acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
+  // a neighbour's value half and the next neighbour's key half are read before the neighbour's
+  // score (every list stores a group after its last full one; unused slots hold token 0)
+  uint2 gc = g0;
+  float ka[8], kb_[8], v[8];
+  qa_load<8>(ka, kb + (gc.x & 0xffffu) * R);
+  auto stage = [&](uint32_t cur, uint32_t nxt, float (&kc)[8], float (&kn)[8]) {
+    qa_load<8>(v, kb + cur * R + 16);
+    qa_load<8>(kn, kb + nxt * R);
+    qp_step(q, kc, v, 0.0f, S_, acc);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int u = 0; u < (cnt >> 2); ++u) {
+    const uint2 gn = eg[u + 1];
+    stage(gc.x & 0xffffu, gc.x >> 16, ka, kb_);
+    stage(gc.x >> 16, gc.y & 0xffffu, kb_, ka);
+    stage(gc.y & 0xffffu, gc.y >> 16, ka, kb_);
+    stage(gc.y >> 16, gn.x & 0xffffu, kb_, ka);
+    gc = gn;
+  }
+  const int rem = cnt & 3;
+  if (rem > 0) stage(gc.x & 0xffffu, gc.x >> 16, ka, kb_);
+  if (rem > 1) stage(gc.x >> 16, gc.y & 0xffffu, kb_, ka);
+  if (rem > 2) stage(gc.y & 0xffffu, gc.y >> 16, ka, kb_);
+  if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {     // the same decision in both lanes
+    float mu = -INFINITY;
+    for (int e = 0; e < cnt; ++e) {
+      float k[8];
+      qa_load<8>(k, kb + qa_entry(eg, e) * R);
+      const float h = dot_seq<8>(q, k);
+      mu = fmaxf(mu, h + pair_other(h));
+    }
+    S_ = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
+    for (int e = 0; e < cnt; ++e) {
+      const float *kr = kb + qa_entry(eg, e) * R;
+      float k[8], vv[8];
+      qa_load<8>(k, kr);
+      qa_load<8>(vv, kr + 16);
+      qp_step(q, k, vv, mu, S_, acc);
+    }
+  }
+  const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
+  *(float4 *)orow = make_float4(acc[0] * rS, acc[1] * rS, acc[2] * rS, acc[3] * rS);
+  *(float4 *)(orow + 4) = make_float4(acc[4] * rS, acc[5] * rS, acc[6] * rS, acc[7] * rS);
+}
+
+template <int D>
+__global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, TW = kQpTilesPerWave, NWV = kQpThreads / 64, FW = 3 * S * 64;
+  static_assert(D == 128, "16-dimension heads, one per head group");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int L = p.L, ntiles = (L + 15) / 16;
+  uint64_t *bfa = (uint64_t *)smem;                                  // [G][3][S][64] weight fragments
+  float *qs = (float *)(smem + G * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, half = tid & 1;
+  if (blockIdx.x >= p.words) return;
+  for (int hg = 0; hg < G; ++hg) {
+    QaStage<D> st;
+    st.load(p.bpack, hg, tid);
+    st.store(bfa + hg * FW, tid);
+  }
+  // this pair's first row (token tid / 2): list metadata of both masks held for the kernel
+  const int r0 = tid >> 1, i0 = r0 < L ? r0 : 0;
+  const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
+  const uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
+  __syncthreads();
+  const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
+  long afr[TW][S];
+  float alw[TW][4];
+  {
+    const int64_t w = blockIdx.x;
+#pragma unroll
+    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+  }
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    for (int hg = 0; hg < G; ++hg) {
+      const uint64_t *bf = bfa + hg * FW;
+      const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+#pragma unroll
+      for (int k = 0; k < TW; ++k)
+        if (wave + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wave + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
+      block_sync_lds();
+      const int64_t wn = w + gridDim.x;
+      if (hg == G - 1 && wn < p.words) {                   // the next word's tiles, read during these rows
+#pragma unroll
+        for (int k = 0; k < TW; ++k)
+          qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+      }
+      const bool first = hg < p.hf;
+      float *ow = p.o + w * L * D + hg * 16 + 8 * half;
+      if (r0 < L)
+        qp_row(qs + r0 * 16 + 8 * half, kv + 8 * half, (first ? p.tab1 : p.tab2) + (first ? mt1.x : mt2.x),
+               first ? g01 : g02, first ? mt1.y : mt2.y, ow + (size_t)r0 * D);
+      for (int r = r0 + kQpThreads / 2; r < L; r += kQpThreads / 2) {   // words of more than 384 tokens
+        const int2 mt = (first ? p.meta1 : p.meta2)[r];
+        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
+        qp_row(qs + r * 16 + 8 * half, kv + 8 * half, eg, eg[0], mt.y, ow + (size_t)r * D);
+      }
+      block_sync_lds();
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // The same projection and attention for words whose keys and values of a head group do not fit
 // LDS in fp32 (d = 64, 128 with up to about 1800 tokens).  Keys and values stay in LDS as their
 // exact int32 accumulators, which fit int16 (|acc| <= 127 d < 2^15), with each token's two
@@ -1458,6 +1601,27 @@ static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_
   return hipGetLastError();
 }
 
+// The lane-pair form (16-dimension heads): every group's weights resident, up to 36 token tiles.
+bool qkv_attention_pair_supported(const Model &M) {
+  return M.d == 128 && M.dh == 16 && M.grouped && M.L <= 16 * (kQpThreads / 64) * kQpTilesPerWave &&
+         qkv_attention_lds(M, true) <= 160 * 1024;
+}
+
+template <int D>
+static hipError_t run_qkv_attention_pair(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_pair<D>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+  hipLaunchKernelGGL((k_qkv_attention_pair<D>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                 float *o, int8_t *oq, float *ao, bool lane_order, hipStream_t s) {
   if (words <= 0) return hipSuccess;
@@ -1481,7 +1645,8 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.resident = qkv_attention_resident(M) ? 1 : 0;
   const size_t lds = qkv_attention_lds(M, a.resident != 0);
   hipError_t e = hipErrorInvalidValue;
-  if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
+  if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(a, qkv_attention_lds(M, true), s);
+  else if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
   else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
   else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(a, lds, s);
   else if (M.d == 64 && M.dh == 16) e = run_qkv_attention<64, 16>(a, lds, s);
