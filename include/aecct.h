@@ -107,8 +107,9 @@ typedef enum aecct_layered_attention {
   AECCT_LAYERED_ATTN_UNFUSED = 0,  /* ternary GEMM to Q, K, V in device memory, then attention */
   AECCT_LAYERED_ATTN_LDS_F32 = 1,  /* fused per word and 16-dimension head group, K and V in
                                       LDS as fp32 (d = 64, 128, short words) */
-  AECCT_LAYERED_ATTN_LDS_I16 = 2   /* fused, K and V in LDS as their int16 accumulators with
-                                      per-token scales (d = 64, 128, longer words) */
+  AECCT_LAYERED_ATTN_LDS_I16 = 2   /* fused, V (and, on the longest words or with 8-dimension
+                                      heads, K too) in LDS as int16 accumulators with per-token
+                                      scales, the rest as fp32 (d = 64, 128, longer words) */
 } aecct_layered_attention;
 
 typedef struct aecct_options {

@@ -378,15 +378,15 @@ constexpr int kQaTilesPerWave = 4;
 
 // Head group hg's three weight tiles, 2-bit codes from HBM: the loads are issued early (into
 // registers) and unpacked into int8 fragments in LDS later, so their latency overlaps the rows.
-template <int D>
+template <int D, int NT = kQaThreads>
 struct QaStage {
-  static constexpr int kWords = 3 * (D / 32) * 64, kPer = (kWords + kQaThreads - 1) / kQaThreads;
+  static constexpr int kWords = 3 * (D / 32) * 64, kPer = (kWords + NT - 1) / NT;
   uint32_t pk[kPer];
   __device__ __forceinline__ void load(const uint16_t *bpack, int hg, int tid) {
     constexpr int S = D / 32, G = D / 16;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      const int u = tid + k * kQaThreads;
+      const int u = tid + k * NT;
       const int m = u / (S * 64), rest = u - m * (S * 64);
       pk[k] = u < kWords ? bpack[(size_t)(m * G + hg) * S * 64 + rest] : 0u;
     }
@@ -394,7 +394,7 @@ struct QaStage {
   __device__ __forceinline__ void store(uint64_t *bf, int tid) const {
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      const int u = tid + k * kQaThreads;
+      const int u = tid + k * NT;
       if (u < kWords) bf[u] = unpack_ternary8(pk[k]);
     }
   }
@@ -739,7 +739,7 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, half = tid & 1;
   if (blockIdx.x >= p.words) return;
   for (int hg = 0; hg < G; ++hg) {
-    QaStage<D> st;
+    QaStage<D, kQpThreads> st;
     st.load(p.bpack, hg, tid);
     st.store(bfa + hg * FW, tid);
   }
@@ -936,6 +936,201 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
 #pragma unroll
         for (int t = 0; t < DH; t += 4)
           *(float4 *)(orow + t) = make_float4(acc[t] * rS, acc[t + 1] * rS, acc[t + 2] * rS, acc[t + 3] * rS);
+      }
+      if (more) st.store(bf, tid);
+      block_sync_lds();            // the next group's projection overwrites keys and values
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Long words with 16-dimension heads (d = 128, up to 1536 tokens): keys in LDS as fp32
+// (dequantised once, in the projection), values as their int16 accumulators, rebuilt by
+// fma(acc, alpha s_v, bias) at every gather as in k_qkv_attention_i16; every row split over a
+// lane pair as in k_qkv_attention_pair (lane 2 r + h takes dimensions 8 h .. 8 h + 7, the pair
+// adds the two score halves with one DPP exchange).  Blocks of kQvThreads, so that each SIMD has
+// four wavefronts of rows in flight.  Each wavefront keeps the int8 codes of its token tiles in
+// registers for all head groups of a word (the next word's are read during the last group's
+// rows), and the tokens' Eq. 2 scales alpha sit in LDS beside the keys and values.
+// ------------------------------------------------------------------------------------------
+constexpr int kQvThreads = 1024;
+constexpr int kQvTilesPerWave = 6;
+constexpr int kQvRow = 24;   // floats per token: key (16 fp32), value (16 int16); 96 bytes apart
+
+template <int D>
+size_t qkv_attention_v16_lds_bytes(int L) {
+  return qa_frag_bytes<D>() + (size_t)L * (kQvRow * 4 + 4);
+}
+
+// 8 int16 accumulators (raw pairs) to fp32 with the dequantisation fma(acc, c, bias).
+__device__ __forceinline__ void qv_dequant(uint4 a, float c, const float (&b)[8], float (&x)[8]) {
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    x[2 * u] = __builtin_fmaf((float)(int)(short)(w[u] & 0xffffu), c, b[2 * u]);
+    x[2 * u + 1] = __builtin_fmaf((float)((int)w[u] >> 16), c, b[2 * u + 1]);
+  }
+}
+
+// One neighbour of a half row: k this lane's key half, va its value accumulators, c their scale.
+__device__ __forceinline__ void qv_step(const float (&q)[8], const float (&k)[8], uint4 va, float c,
+                                        const float (&bv)[8], float shift, float &S, float (&acc)[8]) {
+  float v[8];
+  qv_dequant(va, c, bv, v);
+  const float h = dot_seq<8>(q, k);
+  const float ex = softmax_exp2(h + pair_other(h) - shift);
+  S = S + ex;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
+}
+
+// Attention of one half row: kb (keys) and vb (value accumulators) already offset to this lane's
+// half, orow to its 8 outputs (the query's half is read there first); a value's scale is
+// alpha sv, alpha from al.  Both lanes of a pair run it with the same row.
+__device__ __forceinline__ void qv_row(float *orow, const float *kb, const int16_t *vb, const float *al, float sv,
+                                       const float (&bv)[8], const uint2 *eg, int cnt) {
+  constexpr int R = kQvRow, RV = 2 * kQvRow;
+  float q[8];
+  {
+    const float4 a = *(const float4 *)orow, b = *(const float4 *)(orow + 4);
+    q[0] = a.x; q[1] = a.y; q[2] = a.z; q[3] = a.w; q[4] = b.x; q[5] = b.y; q[6] = b.z; q[7] = b.w;
+  }
+  float S_ = 0.0f, acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
+  // a neighbour's value half and alpha and the next neighbour's key half are read before the
+  // neighbour's score (every list stores a group after its last full one; unused slots hold
+  // token 0)
+  uint2 gc = eg[0];
+  float ka[8], kn[8];
+  qa_load<8>(ka, kb + (gc.x & 0xffffu) * R);
+  auto stage = [&](uint32_t cur, uint32_t nxt, float (&kc)[8], float (&kx)[8]) {
+    const uint4 va = *(const uint4 *)(vb + cur * RV);
+    const float c = al[cur] * sv;
+    qa_load<8>(kx, kb + nxt * R);
+    qv_step(q, kc, va, c, bv, 0.0f, S_, acc);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int u = 0; u < (cnt >> 2); ++u) {
+    const uint2 gn = eg[u + 1];
+    stage(gc.x & 0xffffu, gc.x >> 16, ka, kn);
+    stage(gc.x >> 16, gc.y & 0xffffu, kn, ka);
+    stage(gc.y & 0xffffu, gc.y >> 16, ka, kn);
+    stage(gc.y >> 16, gn.x & 0xffffu, kn, ka);
+    gc = gn;
+  }
+  const int rem = cnt & 3;
+  if (rem > 0) stage(gc.x & 0xffffu, gc.x >> 16, ka, kn);
+  if (rem > 1) stage(gc.x >> 16, gc.y & 0xffffu, kn, ka);
+  if (rem > 2) stage(gc.y & 0xffffu, gc.y >> 16, ka, kn);
+  if (cnt > 0 && !(S_ >= 0x1p-64f && S_ <= 0x1p64f)) {     // the same decision in both lanes
+    float mu = -INFINITY;
+    for (int e = 0; e < cnt; ++e) {
+      float k[8];
+      qa_load<8>(k, kb + qa_entry(eg, e) * R);
+      const float h = dot_seq<8>(q, k);
+      mu = fmaxf(mu, h + pair_other(h));
+    }
+    S_ = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
+    for (int e = 0; e < cnt; ++e) {
+      const uint32_t j = qa_entry(eg, e);
+      float k[8];
+      qa_load<8>(k, kb + j * R);
+      qv_step(q, k, *(const uint4 *)(vb + j * RV), al[j] * sv, bv, mu, S_, acc);
+    }
+  }
+  const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
+  *(float4 *)orow = make_float4(acc[0] * rS, acc[1] * rS, acc[2] * rS, acc[3] * rS);
+  *(float4 *)(orow + 4) = make_float4(acc[4] * rS, acc[5] * rS, acc[6] * rS, acc[7] * rS);
+}
+
+// The int8 codes of token tile tt of a word as the MFMA A operand (zero rows past L).
+template <int D>
+__device__ __forceinline__ void qa_load_codes(const int8_t *xw, int tt, int L, int lane, long (&a)[D / 32]) {
+  const int ra = 16 * tt + (lane & 15);
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) a[s] = ra < L ? *(const long *)(xw + (size_t)ra * D + 32 * s + 8 * (lane >> 4)) : 0;
+}
+
+template <int D>
+__global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, R = kQvRow, NT = kQvThreads, NWV = NT / 64, TW = kQvTilesPerWave;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int L = p.L, ntiles = (L + 15) / 16;
+  uint64_t *bf = (uint64_t *)smem;                                   // [3][S][64] weight fragments
+  float *kvf = (float *)(smem + qa_frag_bytes<D>());                 // [L][R] keys, value accumulators
+  int16_t *kvi = (int16_t *)kvf;
+  float *als = kvf + (size_t)L * R;                                  // [L] the word's alpha per token
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4, half = tid & 1;
+  if (blockIdx.x >= p.words) return;
+  {
+    QaStage<D, NT> st;
+    st.load(p.bpack, 0, tid);
+    st.store(bf, tid);
+  }
+  long afr[TW][S];
+#pragma unroll
+  for (int k = 0; k < TW; ++k) qa_load_codes<D>(p.xq + (int64_t)blockIdx.x * L * D, wave + NWV * k, L, lane, afr[k]);
+  __syncthreads();
+  const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    const float *aw = p.ax + w * L;
+    float *ow = p.o + w * L * D;
+    for (int hg = 0; hg < G; ++hg) {
+      const float bq = p.bias[16 * hg + col], bkc = p.bias[D + 16 * hg + col];
+#pragma unroll
+      for (int k = 0; k < TW; ++k) {
+        // opaque tile index: keeps the per-tile addresses from being hoisted out of the word and
+        // group loops (held for all tiles, they would not fit the registers)
+        int tt = wave + NWV * k;
+        __asm__ volatile("" : "+v"(tt));
+        if (tt >= ntiles) continue;
+        float alv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * tt + 4 * rg + i;
+          alv[i] = tok < L ? (hg == 0 ? aw[tok] : als[tok]) : 0.0f;
+        }
+        v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          aq = mfma_i8_16x16x32(afr[k][s], (long)bf[(0 * S + s) * 64 + lane], aq);
+          ak = mfma_i8_16x16x32(afr[k][s], (long)bf[(1 * S + s) * 64 + lane], ak);
+          av = mfma_i8_16x16x32(afr[k][s], (long)bf[(2 * S + s) * 64 + lane], av);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * tt + 4 * rg + i;
+          if (tok < L) {
+            ow[(size_t)tok * D + 16 * hg + col] = __builtin_fmaf((float)aq[i], alv[i] * sq[0], bq);
+            kvf[tok * R + col] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
+            kvi[tok * 2 * R + 32 + col] = (int16_t)av[i];
+            if (hg == 0 && col == 0) als[tok] = alv[i];
+          }
+        }
+      }
+      __syncthreads();   // also orders the queries written to memory before their rows read them
+      const int64_t wn = w + gridDim.x;
+      const bool more = hg + 1 < G || wn < p.words;
+      QaStage<D, NT> st;
+      if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
+      if (hg == G - 1 && wn < p.words) {                   // the next word's tiles, read during these rows
+#pragma unroll
+        for (int k = 0; k < TW; ++k) {
+          int tt = wave + NWV * k;
+          __asm__ volatile("" : "+v"(tt));
+          qa_load_codes<D>(p.xq + wn * L * D, tt, L, lane, afr[k]);
+        }
+      }
+      const bool first = hg < p.hf;
+      float bv[8];
+      qa_load<8>(bv, p.bias + 2 * D + 16 * hg + 8 * half);
+      for (int r = tid >> 1; r < L; r += NT / 2) {
+        const int2 mt = (first ? p.meta1 : p.meta2)[r];
+        qv_row(ow + (size_t)r * D + 16 * hg + 8 * half, kvf + 8 * half, kvi + 32 + 8 * half, als, sq[2], bv,
+               (first ? p.tab1 : p.tab2) + mt.x, mt.y);
       }
       if (more) st.store(bf, tid);
       block_sync_lds();            // the next group's projection overwrites keys and values
@@ -1679,6 +1874,29 @@ static hipError_t run_qkv_attention_i16(const QkvAttnArgs &a, size_t lds, hipStr
   return hipGetLastError();
 }
 
+// Keys in fp32, values in int16 (16-dimension heads), when that layout fits LDS.
+bool qkv_attention_v16_supported(const Model &M) {
+  if (!((M.d == 64 || M.d == 128) && M.dh == 16 && M.grouped)) return false;
+  if (M.L > 16 * (kQvThreads / 64) * kQvTilesPerWave) return false;
+  const size_t lds = M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L);
+  return lds <= 160 * 1024;
+}
+
+template <int D>
+static hipError_t run_qkv_attention_v16(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_v16<D>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+  hipLaunchKernelGGL((k_qkv_attention_v16<D>), dim3((unsigned)blocks), dim3(kQvThreads), lds, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                     float *o, bool lane_order, hipStream_t s) {
   if (words <= 0) return hipSuccess;
@@ -1699,11 +1917,15 @@ hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq,
   a.meta1 = (const int2 *)M.g1_meta; a.meta2 = (const int2 *)M.g2_meta;
   a.tab1 = (const uint2 *)M.g1_tab; a.tab2 = (const uint2 *)M.g2_tab;
   a.o = o;
+  if (qkv_attention_v16_supported(M)) {
+    const size_t lv = M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L);
+    return M.d == 64 ? run_qkv_attention_v16<64>(a, lv, s) : run_qkv_attention_v16<128>(a, lv, s);
+  }
   const size_t lds = M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L);
-  if (M.d == 64 && M.dh == 8) return run_qkv_attention_i16<64, 8>(a, lds, s);
   if (M.d == 128 && M.dh == 16) return run_qkv_attention_i16<128, 16>(a, lds, s);
-  if (M.d == 128 && M.dh == 8) return run_qkv_attention_i16<128, 8>(a, lds, s);
   if (M.d == 64 && M.dh == 16) return run_qkv_attention_i16<64, 16>(a, lds, s);
+  if (M.d == 64 && M.dh == 8) return run_qkv_attention_i16<64, 8>(a, lds, s);
+  if (M.d == 128 && M.dh == 8) return run_qkv_attention_i16<128, 8>(a, lds, s);
   return hipErrorInvalidValue;
 }
 

@@ -402,6 +402,27 @@ def test_long_words_shifted_softmax(P, oracle_mod, regime, d):
     _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
+@pytest.mark.parametrize("regime", ["plain", "mixed"])
+def test_long_words_int16_keys(P, oracle_mod, regime):
+    """d = 128 words of 1700 tokens: too long for fp32 keys beside int16 values in LDS, so keys
+    and values both stay int16 accumulators; plain rows and rows that take the max-shifted
+    softmax."""
+    from workloads import random_weights
+    print(f"[long int16 keys] {regime}", flush=True)
+    m, n = 567, 1133
+    H = _random_parity_check(m, n, seed=41)
+    w = random_weights(n, m, 128, 2, 8, seed=43)
+    if regime == "mixed":
+        w.scale[:, 0:2] *= np.float32(5.0)
+    rng = np.random.default_rng(9)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (9, n)) + 0.6 * rng.standard_normal((9, n))).astype(np.float32)
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y, n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.info.layered_attention == P.LAYERED_ATTN_LDS_I16
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits), fo, _np(bits), bo, y)
+
+
 def test_layered_attention_forms_of_the_workloads(P):
     """LDPC(128,64) and LDPC(256,128) run keys and values in LDS as fp32, LDPC(1024,512) (1536
     tokens) as int16 accumulators."""
