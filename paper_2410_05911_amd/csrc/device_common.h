@@ -27,6 +27,27 @@ __device__ __forceinline__ v4i mfma_i8_16x16x32(long a, long b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, c, 0, 0, 0);
 }
 
+// Two k-steps of mfma_i8_16x16x32 as one v_mfma_i32_16x16x64_i8 (twice the k per instruction,
+// the same issue cost): lane l passes its 8 A bytes of step 0 then those of step 1, and its B
+// bytes the same way.  The instruction pairs A and B bytes of equal position within a lane, so
+// the result is the sum of the two steps' products; int32 sums of int8 products are exact in
+// any order.
+__device__ __forceinline__ v4i mfma_i8_16x16x64(long a0, long a1, long b0, long b1, v4i c) {
+  const v4i a = v4i{(int)a0, (int)(a0 >> 32), (int)a1, (int)(a1 >> 32)};
+  const v4i b = v4i{(int)b0, (int)(b0 >> 32), (int)b1, (int)(b1 >> 32)};
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// c + the products of S k-steps, A and B fragments of step s from a(s) and b(s): pairs of steps
+// on the 64-deep instruction, an odd last step on the 32-deep one.
+template <int S, class FA, class FB>
+__device__ __forceinline__ v4i mfma_i8_steps(FA a, FB b, v4i c) {
+#pragma unroll
+  for (int s = 0; s + 1 < S; s += 2) c = mfma_i8_16x16x64(a(s), a(s + 1), b(s), b(s + 1), c);
+  if constexpr (S % 2 == 1) c = mfma_i8_16x16x32(a(S - 1), b(S - 1), c);
+  return c;
+}
+
 // Lane l of a 16-lane DPP row reads lane (l +- N) mod 16 of the same row.
 template <int N>
 __device__ __forceinline__ float row_rotate(float v) {

@@ -135,8 +135,8 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       acc[t] = v4i{0, 0, 0, 0};
-#pragma unroll
-      for (int s = 0; s < S; ++s) acc[t] = mfma_i8_16x16x32(afr[s], (long)bsm[(t * S + s) * 64 + lane], acc[t]);
+      acc[t] = mfma_i8_steps<S>([&](int s) { return afr[s]; }, [&](int s) { return (long)bsm[(t * S + s) * 64 + lane]; },
+                                acc[t]);
     }
 
     int64_t r[4];
@@ -533,12 +533,10 @@ __device__ __forceinline__ void qa_project(const uint64_t *bf, const long (&a)[D
   constexpr int S = D / 32, R = kQaRow;
   const int col = lane & 15, rg = lane >> 4;
   v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
-#pragma unroll
-  for (int s = 0; s < S; ++s) {
-    aq = mfma_i8_16x16x32(a[s], (long)bf[(0 * S + s) * 64 + lane], aq);
-    ak = mfma_i8_16x16x32(a[s], (long)bf[(1 * S + s) * 64 + lane], ak);
-    av = mfma_i8_16x16x32(a[s], (long)bf[(2 * S + s) * 64 + lane], av);
-  }
+  const auto fa = [&](int s) { return a[s]; };
+  aq = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; }, aq);
+  ak = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(1 * S + s) * 64 + lane]; }, ak);
+  av = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(2 * S + s) * 64 + lane]; }, av);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int tok = 16 * tt + 4 * rg + i;
@@ -855,12 +853,10 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
       for (int tt = wave; tt < ntiles; tt += NWV) {
         if (tt + NWV < ntiles) qa_load_tile<D>(xw, aw, tt + NWV, L, lane, an, aln);
         v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-          aq = mfma_i8_16x16x32(a[s], (long)bf[(0 * S + s) * 64 + lane], aq);
-          ak = mfma_i8_16x16x32(a[s], (long)bf[(1 * S + s) * 64 + lane], ak);
-          av = mfma_i8_16x16x32(a[s], (long)bf[(2 * S + s) * 64 + lane], av);
-        }
+        const auto fa = [&](int s) { return a[s]; };
+        aq = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; }, aq);
+        ak = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(1 * S + s) * 64 + lane]; }, ak);
+        av = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(2 * S + s) * 64 + lane]; }, av);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * tt + 4 * rg + i;
@@ -1094,12 +1090,10 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
           alv[i] = tok < L ? (hg == 0 ? aw[tok] : als[tok]) : 0.0f;
         }
         v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-          aq = mfma_i8_16x16x32(afr[k][s], (long)bf[(0 * S + s) * 64 + lane], aq);
-          ak = mfma_i8_16x16x32(afr[k][s], (long)bf[(1 * S + s) * 64 + lane], ak);
-          av = mfma_i8_16x16x32(afr[k][s], (long)bf[(2 * S + s) * 64 + lane], av);
-        }
+        const auto fa = [&](int s) { return afr[k][s]; };
+        aq = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; }, aq);
+        ak = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(1 * S + s) * 64 + lane]; }, ak);
+        av = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(2 * S + s) * 64 + lane]; }, av);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * tt + 4 * rg + i;
@@ -1344,8 +1338,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
       for (int o = 0; o < TO; ++o) {
         v4i acc = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)fo[(o * S + s) * 64 + lane], bq[s], acc);
+        acc = mfma_i8_steps<S>([&](int s) { return (long)fo[(o * S + s) * 64 + lane]; }, [&](int s) { return bq[s]; }, acc);
         // the residual: four consecutive values of X in lane order
         float res[4];
         if constexpr (OQ) {
@@ -1396,8 +1389,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll 2
     for (int o = 0; o < TH; ++o) {
       v4i acc = v4i{0, 0, 0, 0};
-#pragma unroll
-      for (int s = 0; s < S; ++s) acc = mfma_i8_16x16x32((long)f1l[(o * S + s) * 64], xb[s], acc);
+      acc = mfma_i8_steps<S>([&](int s) { return (long)f1l[(o * S + s) * 64]; }, [&](int s) { return xb[s]; }, acc);
 #pragma unroll
       for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]));
     }
@@ -1410,24 +1402,29 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     v4i acc2[TO];
 #pragma unroll
     for (int o = 0; o < TO; ++o) acc2[o] = v4i{0, 0, 0, 0};
+    static_assert(SH % 2 == 0, "FF2 k-steps taken in pairs");
 #pragma unroll 1
-    for (int s2 = 0; s2 < SH; ++s2) {                       // pass 2: tiles 2 s2, 2 s2 + 1 -> FF2 step s2
-      v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
+    for (int s2 = 0; s2 < SH; s2 += 2) {                    // pass 2: tiles 2 s2 .. 2 s2 + 3 -> FF2 steps s2, s2 + 1
+      long gb[2];
 #pragma unroll
-      for (int s = 0; s < S; ++s) {
-        h0 = mfma_i8_16x16x32((long)f1l[((2 * s2) * S + s) * 64], xb[s], h0);
-        h1 = mfma_i8_16x16x32((long)f1l[((2 * s2 + 1) * S + s) * 64], xb[s], h1);
+      for (int j = 0; j < 2; ++j) {
+        const int t0 = 2 * (s2 + j);
+        v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
+        h0 = mfma_i8_steps<S>([&](int s) { return (long)f1l[(t0 * S + s) * 64]; }, [&](int s) { return xb[s]; }, h0);
+        h1 = mfma_i8_steps<S>([&](int s) { return (long)f1l[((t0 + 1) * S + s) * 64]; }, [&](int s) { return xb[s]; },
+                              h1);
+        uint32_t b[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, b1l[16 * t0 + i]), inv1);
+          b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, b1l[16 * (t0 + 1) + i]), inv1);
+        }
+        // ReLU on the codes: the code of max(F, 0) is max(code of F, 0)
+        gb[j] = (long)(((uint64_t)pack4_relu(b[4], b[5], b[6], b[7]) << 32) | pack4_relu(b[0], b[1], b[2], b[3]));
       }
-      uint32_t b[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, b1l[16 * (2 * s2) + i]), inv1);
-        b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, b1l[16 * (2 * s2 + 1) + i]), inv1);
-      }
-      // ReLU on the codes: the code of max(F, 0) is max(code of F, 0)
-      const long gb = (long)(((uint64_t)pack4_relu(b[4], b[5], b[6], b[7]) << 32) | pack4_relu(b[0], b[1], b[2], b[3]));
-#pragma unroll
-      for (int o = 0; o < TO; ++o) acc2[o] = mfma_i8_16x16x32((long)f2l[(o * SH + s2) * 64], gb, acc2[o]);
+      for (int o = 0; o < TO; ++o)
+        acc2[o] = mfma_i8_16x16x64((long)f2l[(o * SH + s2) * 64], (long)f2l[(o * SH + s2 + 1) * 64], gb[0], gb[1], acc2[o]);
     }
     // ---- FFN2 epilogue: residual, LN2, Eq. 2 of the next layer's input ----
     {
