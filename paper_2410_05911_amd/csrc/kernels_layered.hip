@@ -516,11 +516,12 @@ __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const
   for (int t = 0; t < DH; ++t) orow[t] = acc[t] * rS;
 }
 
-// d = 128: one block per CU (its LDS), so 2 wavefronts per SIMD and room for the word's token
-// tiles in registers across the head groups; d = 64: three blocks per CU (d_h = 8), tiles
-// reloaded per group (from L1/L2) to stay within the register budget of 6 wavefronts per SIMD.
-template <int D>
-constexpr bool qa_keep_tiles() { return D == 128; }
+// The word's token tiles stay in registers across its head groups (d = 128: one block per CU,
+// 2 wavefronts per SIMD; d = 64 with 8-dimension heads: three blocks per CU, 6 wavefronts per
+// SIMD and at most two tiles per wave); d = 64 with 16-dimension heads reloads them per group
+// (up to four tiles per wave would not fit the registers of 4 wavefronts per SIMD).
+template <int D, int DH>
+constexpr bool qa_keep_tiles() { return D == 128 || DH == 8; }
 template <int D, int DH>
 constexpr int qa_waves_per_simd() { return D == 128 ? 2 : (DH == 8 ? 6 : 4); }
 
@@ -563,8 +564,10 @@ __device__ __forceinline__ void qa_load_tile(const int8_t *xw, const float *aw, 
 
 template <int D, int DH>
 __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qkv_attention(QkvAttnArgs p) {
-  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, TW = qa_keep_tiles<D>() ? kQaTilesPerWave : 1;
   constexpr int NWV = kQaThreads / 64;
+  // at most kQaThreads rows of L tokens x 16 / d_h heads: a wave holds up to TW of the L / 16 tiles
+  constexpr int S = D / 32, G = D / 16, HPG = 16 / DH, TW = qa_keep_tiles<D, DH>() ? (kQaThreads / HPG / 16 + NWV - 1) / NWV : 1;
+  static_assert(TW <= kQaTilesPerWave, "token tiles per wave");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int L = p.L, ntiles = (L + 15) / 16;
   // weight fragments: [G][3][S][64] when resident (staged once per block), else one group's
@@ -590,7 +593,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
-  if constexpr (qa_keep_tiles<D>()) {
+  if constexpr (qa_keep_tiles<D, DH>()) {
     // the wave's token tiles of its first word, used by all head groups of the word; the next
     // word's are read during the last group's rows
     const int64_t w = blockIdx.x;
@@ -603,10 +606,13 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
     for (int hg = 0; hg < G; ++hg) {
       const uint64_t *bf = resident ? bfa + hg * FW : bfa;
       const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
-      if constexpr (qa_keep_tiles<D>()) {
+      if constexpr (qa_keep_tiles<D, DH>()) {
 #pragma unroll
-        for (int k = 0; k < TW; ++k)
-          if (wave + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wave + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
+        for (int k = 0; k < TW; ++k) {
+          int tt = wave + NWV * k;
+          __asm__ volatile("" : "+v"(tt));   // per-tile addresses are not hoisted out of the loops
+          if (tt < ntiles) qa_project<D>(bf, afr[k], alw[k], tt, L, lane, bq, bk, bv, sq, qs, kv);
+        }
       } else {
         for (int tt = wave; tt < ntiles; tt += NWV) {
           qa_load_tile<D>(xw, aw, tt, L, lane, afr[0], alw[0]);
@@ -614,12 +620,15 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         }
       }
       block_sync_lds();
-      if constexpr (qa_keep_tiles<D>()) {
+      if constexpr (qa_keep_tiles<D, DH>()) {
         const int64_t wn = w + gridDim.x;
         if (hg == G - 1 && wn < p.words) {
 #pragma unroll
-          for (int k = 0; k < TW; ++k)
-            qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+          for (int k = 0; k < TW; ++k) {
+            int tt = wave + NWV * k;
+            __asm__ volatile("" : "+v"(tt));
+            qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, tt, L, lane, afr[k], alw[k]);
+          }
         }
       }
       // not resident: the fragments were last read before the barrier above, so the next group's
