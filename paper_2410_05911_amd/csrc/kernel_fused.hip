@@ -412,13 +412,9 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
         for (int o = 0; o < 8; ++o)
           gb[o] = pack4_relu(quant_bits(G[o][0], inv), quant_bits(G[o][1], inv), quant_bits(G[o][2], inv),
                              quant_bits(G[o][3], inv));
-        v4i b0 = v4i{0, 0, 0, 0}, b1 = v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const long gop = as_long(gb[2 * s], gb[2 * s + 1]);
-          b0 = mfma_i8_16x16x32((long)F[(fz::F_FF2 + s) * 64], gop, b0);
-          b1 = mfma_i8_16x16x32((long)F[(fz::F_FF2 + 4 + s) * 64], gop, b1);
-        }
+        const auto gop = [&](int s) { return as_long(gb[2 * s], gb[2 * s + 1]); };
+        const v4i b0 = mfma_i8_steps<4>([&](int s) { return (long)F[(fz::F_FF2 + s) * 64]; }, gop, v4i{0, 0, 0, 0});
+        const v4i b1 = mfma_i8_steps<4>([&](int s) { return (long)F[(fz::F_FF2 + 4 + s) * 64]; }, gop, v4i{0, 0, 0, 0});
         const float sc2 = amax * sq_2;
         const float *b2 = V + fz::V_BFF2 + 4 * g;
 #pragma unroll
