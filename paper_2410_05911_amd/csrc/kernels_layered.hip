@@ -953,13 +953,13 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
 // (dequantised once, in the projection), values as their int16 accumulators, rebuilt by
 // fma(acc, alpha s_v, bias) at every gather as in k_qkv_attention_i16; every row split over a
 // lane pair as in k_qkv_attention_pair (lane 2 r + h takes dimensions 8 h .. 8 h + 7, the pair
-// adds the two score halves with one DPP exchange).  Blocks of kQvThreads, so that each SIMD has
-// four wavefronts of rows in flight.  Each wavefront keeps the int8 codes of its token tiles in
-// registers for all head groups of a word (the next word's are read during the last group's
-// rows), and the tokens' Eq. 2 scales alpha sit in LDS beside the keys and values.
+// adds the two score halves with one DPP exchange).  Blocks of 12 wavefronts (three per SIMD
+// with rows in flight).  Each wavefront keeps the int8 codes of its token tiles in registers for
+// all head groups of a word, read at the word's start with the tokens' Eq. 2 scales alpha, which
+// sit in LDS beside the keys and values.
 // ------------------------------------------------------------------------------------------
-constexpr int kQvThreads = 1024;
-constexpr int kQvTilesPerWave = 6;
+constexpr int kQvThreads = 768;
+constexpr int kQvTilesPerWave = 8;
 constexpr int kQvRow = 24;   // floats per token: key (16 fp32), value (16 int16); 96 bytes apart
 
 template <int D>
@@ -1075,28 +1075,42 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
     st.load(p.bpack, 0, tid);
     st.store(bf, tid);
   }
-  long afr[TW][S];
-#pragma unroll
-  for (int k = 0; k < TW; ++k) qa_load_codes<D>(p.xq + (int64_t)blockIdx.x * L * D, wave + NWV * k, L, lane, afr[k]);
-  __syncthreads();
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
+  long afr[TW][S];
+  // Global loads are waited for only at the word's first barrier and after each projection (the
+  // barrier that publishes the queries): vmcnt counts stores too, so any other wait would also
+  // wait for the outputs still being written.
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
-    const float *aw = p.ax + w * L;
     float *ow = p.o + w * L * D;
+    // the word's token tiles (registers, for all head groups) and alphas (LDS); the previous word's
+    // rows are done with both
+    // an opaque copy of the wave index per word and per group: the per-tile addresses derived
+    // from it are not hoisted out of the loops (held for all tiles, they would not fit the
+    // registers)
+    int wv = wave;
+    __asm__ volatile("" : "+v"(wv));
+#pragma unroll
+    for (int k = 0; k < TW; ++k) qa_load_codes<D>(p.xq + w * L * D, wv + NWV * k, L, lane, afr[k]);
+    for (int t = tid; t < L; t += NT) als[t] = p.ax[w * L + t];
+    __syncthreads();
     for (int hg = 0; hg < G; ++hg) {
-      const float bq = p.bias[16 * hg + col], bkc = p.bias[D + 16 * hg + col];
+      // the next group's weight tiles: read now, written to LDS once this projection is done
+      const bool more = hg + 1 < G || w + gridDim.x < p.words;
+      QaStage<D, NT> st;
+      if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
+      float bq = p.bias[16 * hg + col], bkc = p.bias[D + 16 * hg + col];
+      int wg = wave;
+      // waited for here, before the first query store (not behind it)
+      __asm__ volatile("" : "+v"(wg), "+v"(bq), "+v"(bkc));
 #pragma unroll
       for (int k = 0; k < TW; ++k) {
-        // opaque tile index: keeps the per-tile addresses from being hoisted out of the word and
-        // group loops (held for all tiles, they would not fit the registers)
-        int tt = wave + NWV * k;
-        __asm__ volatile("" : "+v"(tt));
+        const int tt = wg + NWV * k;
         if (tt >= ntiles) continue;
         float alv[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * tt + 4 * rg + i;
-          alv[i] = tok < L ? (hg == 0 ? aw[tok] : als[tok]) : 0.0f;
+          alv[i] = tok < L ? als[tok] : 0.0f;
         }
         v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
         const auto fa = [&](int s) { return afr[k][s]; };
@@ -1110,23 +1124,11 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
             ow[(size_t)tok * D + 16 * hg + col] = __builtin_fmaf((float)aq[i], alv[i] * sq[0], bq);
             kvf[tok * R + col] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
             kvi[tok * 2 * R + 32 + col] = (int16_t)av[i];
-            if (hg == 0 && col == 0) als[tok] = alv[i];
           }
         }
       }
       __syncthreads();   // also orders the queries written to memory before their rows read them
-      const int64_t wn = w + gridDim.x;
-      const bool more = hg + 1 < G || wn < p.words;
-      QaStage<D, NT> st;
-      if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
-      if (hg == G - 1 && wn < p.words) {                   // the next word's tiles, read during these rows
-#pragma unroll
-        for (int k = 0; k < TW; ++k) {
-          int tt = wave + NWV * k;
-          __asm__ volatile("" : "+v"(tt));
-          qa_load_codes<D>(p.xq + wn * L * D, tt, L, lane, afr[k]);
-        }
-      }
+      if (more) st.store(bf, tid);   // no wave reads this group's fragments any more
       const bool first = hg < p.hf;
       float bv[8];
       qa_load<8>(bv, p.bias + 2 * D + 16 * hg + 8 * half);
@@ -1135,7 +1137,6 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
         qv_row(ow + (size_t)r * D + 16 * hg + 8 * half, kvf + 8 * half, kvi + 32 + 8 * half, als, sq[2], bv,
                (first ? p.tab1 : p.tab2) + mt.x, mt.y);
       }
-      if (more) st.store(bf, tid);
       block_sync_lds();            // the next group's projection overwrites keys and values
     }
   }
