@@ -1184,14 +1184,15 @@ __global__ __launch_bounds__(256) void k_quant_rows(const float *x, int64_t rows
 // The token-local half of a layer in one kernel (d = 64, 128): output projection, residual,
 // LN1 (Eq. 3, Section 6), Eq. 2, FFN1 with ReLU, Eq. 2, FFN2, residual, LN2 and Eq. 2 of the
 // next layer's input.  One wavefront per 16-token strip.  The products run transposed on
-// v_mfma_i32_16x16x32_i8 (weights are the A operand, from LDS; the strip's 16 tokens are the
+// int8 MFMA (weights are the A operand, from LDS; the strip's 16 tokens are the
 // columns), so lane (c, g) = (lane & 15, lane >> 4) holds, for token c, the d-wide activations
 // as register v = feature 4 v + g.  The host permutes the fragments' rows and k-slots so that
 // (a) the O and FF2 outputs land in that layout, (b) the 8 codes a lane quantises for k-step s
 // are exactly its B-operand bytes for FF1, and (c) two FF1 output tiles give exactly the
-// B-operand bytes of one FF2 k-step: no activation leaves registers between the maps.  FF1 runs
-// twice: once for the rows' ReLU maxima (the Eq. 2 scale of the hidden row), once (identical
-// values) to quantise, each pair of tiles feeding FF2 at once.  LayerNorm sums are the
+// B-operand bytes of one FF2 k-step: no activation leaves registers between the maps.  The
+// hidden row (4 d values per token) is computed once and held in registers while its ReLU maximum
+// (the Eq. 2 scale of the hidden row) is formed, then quantised, each pair of tiles feeding FF2 at
+// once (with kTbKeepHidden off, FF1 runs a second time instead).  LayerNorm sums are the
 // pairwise order (in-lane over v, then lanes xor 32, xor 16); epilogues and evaluation order
 // are those of k_gemm's EPI_LN / EPI_RELU_QUANT.  X and the next layer's codes are kept in that
 // lane order in memory too, so every lane reads and writes contiguous words.  No block barrier
@@ -1214,7 +1215,10 @@ struct TokenBlockArgs {
 constexpr int kTbWaves = 8;
 // Whether a wavefront reads the next strip's attention output and residual while it runs the
 // current strip's feed-forward block (fp32 O input only).
-constexpr bool kTbPrefetch = true;
+constexpr bool kTbPrefetch = false;
+// Whether pass 1 keeps the hidden row's fp32 values in registers for pass 2 (instead of pass 2
+// recomputing them).
+constexpr bool kTbKeepHidden = true;
 
 // A strip's fp32 inputs as one lane holds them: O features 32 s + 8 g + k (its B-operand
 // slots) and the residual X in lane order (register v = feature 4 v + g).
@@ -1391,17 +1395,31 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       }
       a1 = amax;
     }
-    // ---- FFN1 with ReLU (twice) feeding FFN2 ----
+    // ---- FFN1 with ReLU feeding FFN2 ----
     const float sc1 = a1 * p.sq_1;
     // pass 1: the row's ReLU maximum, max(0, F_0, F_1, ...) = max over ReLU(F); adding +0
     // turns a -0 result into +0, so the cross-lane maximum may compare bit patterns
     float am = 0.0f;
-#pragma unroll 2
-    for (int o = 0; o < TH; ++o) {
-      v4i acc = v4i{0, 0, 0, 0};
-      acc = mfma_i8_steps<S>([&](int s) { return (long)f1l[(o * S + s) * 64]; }, [&](int s) { return xb[s]; }, acc);
+    [[maybe_unused]] float hid[kTbKeepHidden ? TH : 1][4];
+    if constexpr (kTbKeepHidden) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]));
+      for (int o = 0; o < TH; ++o) {
+        v4i acc = v4i{0, 0, 0, 0};
+        acc = mfma_i8_steps<S>([&](int s) { return (long)f1l[(o * S + s) * 64]; }, [&](int s) { return xb[s]; }, acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          hid[o][i] = __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]);
+          am = fmaxf(am, hid[o][i]);
+        }
+      }
+    } else {
+#pragma unroll 2
+      for (int o = 0; o < TH; ++o) {
+        v4i acc = v4i{0, 0, 0, 0};
+        acc = mfma_i8_steps<S>([&](int s) { return (long)f1l[(o * S + s) * 64]; }, [&](int s) { return xb[s]; }, acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) am = fmaxf(am, __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]));
+      }
     }
     am = tb_token_max(am + 0.0f);
     if constexpr (PF) {                                     // the next strip's inputs
@@ -1413,21 +1431,29 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
     for (int o = 0; o < TO; ++o) acc2[o] = v4i{0, 0, 0, 0};
     static_assert(SH % 2 == 0, "FF2 k-steps taken in pairs");
-#pragma unroll 1
-    for (int s2 = 0; s2 < SH; s2 += 2) {                    // pass 2: tiles 2 s2 .. 2 s2 + 3 -> FF2 steps s2, s2 + 1
+    // pass 2: tiles 2 s2 .. 2 s2 + 3 -> FF2 steps s2, s2 + 1
+    auto pass2 = [&](int s2) {
       long gb[2];
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int t0 = 2 * (s2 + j);
-        v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
-        h0 = mfma_i8_steps<S>([&](int s) { return (long)f1l[(t0 * S + s) * 64]; }, [&](int s) { return xb[s]; }, h0);
-        h1 = mfma_i8_steps<S>([&](int s) { return (long)f1l[((t0 + 1) * S + s) * 64]; }, [&](int s) { return xb[s]; },
-                              h1);
         uint32_t b[8];
+        if constexpr (kTbKeepHidden) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, b1l[16 * t0 + i]), inv1);
-          b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, b1l[16 * (t0 + 1) + i]), inv1);
+          for (int i = 0; i < 4; ++i) {
+            b[i] = quant_bits(hid[t0][i], inv1);
+            b[4 + i] = quant_bits(hid[t0 + 1][i], inv1);
+          }
+        } else {
+          v4i h0 = v4i{0, 0, 0, 0}, h1 = v4i{0, 0, 0, 0};
+          h0 = mfma_i8_steps<S>([&](int s) { return (long)f1l[(t0 * S + s) * 64]; }, [&](int s) { return xb[s]; }, h0);
+          h1 = mfma_i8_steps<S>([&](int s) { return (long)f1l[((t0 + 1) * S + s) * 64]; }, [&](int s) { return xb[s]; },
+                                h1);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            b[i] = quant_bits(__builtin_fmaf((float)h0[i], sc1, b1l[16 * t0 + i]), inv1);
+            b[4 + i] = quant_bits(__builtin_fmaf((float)h1[i], sc1, b1l[16 * (t0 + 1) + i]), inv1);
+          }
         }
         // ReLU on the codes: the code of max(F, 0) is max(code of F, 0)
         gb[j] = (long)(((uint64_t)pack4_relu(b[4], b[5], b[6], b[7]) << 32) | pack4_relu(b[0], b[1], b[2], b[3]));
@@ -1435,6 +1461,13 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
 #pragma unroll
       for (int o = 0; o < TO; ++o)
         acc2[o] = mfma_i8_16x16x64((long)f2l[(o * SH + s2) * 64], (long)f2l[(o * SH + s2 + 1) * 64], gb[0], gb[1], acc2[o]);
+    };
+    if constexpr (kTbKeepHidden) {
+#pragma unroll
+      for (int s2 = 0; s2 < SH; s2 += 2) pass2(s2);
+    } else {
+#pragma unroll 1
+      for (int s2 = 0; s2 < SH; s2 += 2) pass2(s2);
     }
     // ---- FFN2 epilogue: residual, LN2, Eq. 2 of the next layer's input ----
     {
