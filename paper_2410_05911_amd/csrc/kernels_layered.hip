@@ -517,13 +517,15 @@ __device__ __forceinline__ void qa_row(const float *qrow, const float *kb, const
 }
 
 // The word's token tiles stay in registers across its head groups (d = 128: one block per CU,
-// 2 wavefronts per SIMD; d = 64 with 8-dimension heads: three blocks per CU, 6 wavefronts per
-// SIMD and at most two tiles per wave); d = 64 with 16-dimension heads reloads them per group
-// (up to four tiles per wave would not fit the registers of 4 wavefronts per SIMD).
+// 2 wavefronts per SIMD; d = 64 with 8-dimension heads: at most two tiles per wave, and a
+// register budget of 4 wavefronts per SIMD, two blocks per CU: at 6 the loop-invariant values
+// spill, and every reload from scratch waits for the outputs in flight); d = 64 with
+// 16-dimension heads reloads them per group (up to four tiles per wave would not fit the
+// registers of 4 wavefronts per SIMD).
 template <int D, int DH>
 constexpr bool qa_keep_tiles() { return D == 128 || DH == 8; }
 template <int D, int DH>
-constexpr int qa_waves_per_simd() { return D == 128 ? 2 : (DH == 8 ? 6 : 4); }
+constexpr int qa_waves_per_simd() { return D == 128 ? 2 : 4; }
 
 // Q, K, V of token tile tt (16 tokens) for the head group whose fragments are bf: the A
 // fragments a (the tile's Eq. 2 codes) and the four token scales al of this lane's outputs.
@@ -576,6 +578,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   const bool resident = p.resident != 0;
   uint64_t *bfa = (uint64_t *)smem;
   float *qs = (float *)(smem + (resident ? G : 1) * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
+  float *bl = kv + (size_t)L * kQaRow;                               // [3][D] Q, K, V biases
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15;
   if (blockIdx.x >= p.words) return;
   for (int hg = 0; hg < (resident ? G : 1); ++hg) {
@@ -583,6 +586,7 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
     st.load(p.bpack, hg, tid);
     st.store(bfa + hg * FW, tid);
   }
+  for (int u = tid; u < 3 * D; u += kQaThreads) bl[u] = p.bias[u];
   // the thread's row (token i0, head hh0 of the group; L d / (16 d_h) <= kQaThreads rows): its
   // list metadata and first entry group for both masks stay in registers for the whole kernel
   const bool row0 = tid < L * HPG;
@@ -593,24 +597,33 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
-  if constexpr (qa_keep_tiles<D, DH>()) {
-    // the wave's token tiles of its first word, used by all head groups of the word; the next
-    // word's are read during the last group's rows
-    const int64_t w = blockIdx.x;
-#pragma unroll
-    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wave + NWV * k, L, lane, afr[k], alw[k]);
-  }
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
+    if constexpr (qa_keep_tiles<D, DH>()) {
+      // the wave's token tiles of the word, used by all its head groups and waited for here: no
+      // global load is then outstanding inside the group loop, where a wait would also wait for
+      // the row outputs being written (vmcnt counts stores too)
+      int wv = wave;
+      __asm__ volatile("" : "+v"(wv));   // per-tile addresses are not hoisted out of the loops
+#pragma unroll
+      for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wv + NWV * k, L, lane, afr[k], alw[k]);
+#pragma unroll
+      for (int k = 0; k < TW; ++k) {
+#pragma unroll
+        for (int s2 = 0; s2 < S; ++s2) __asm__ volatile("" : "+v"(afr[k][s2]));
+        __asm__ volatile("" : "+v"(alw[k][0]), "+v"(alw[k][1]), "+v"(alw[k][2]), "+v"(alw[k][3]));
+      }
+    }
     for (int hg = 0; hg < G; ++hg) {
       const uint64_t *bf = resident ? bfa + hg * FW : bfa;
-      const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+      const float bq = bl[16 * hg + col], bk = bl[D + 16 * hg + col], bv = bl[2 * D + 16 * hg + col];
       if constexpr (qa_keep_tiles<D, DH>()) {
+        int wg = wave;
+        __asm__ volatile("" : "+v"(wg));
 #pragma unroll
         for (int k = 0; k < TW; ++k) {
-          int tt = wave + NWV * k;
-          __asm__ volatile("" : "+v"(tt));   // per-tile addresses are not hoisted out of the loops
+          const int tt = wg + NWV * k;
           if (tt < ntiles) qa_project<D>(bf, afr[k], alw[k], tt, L, lane, bq, bk, bv, sq, qs, kv);
         }
       } else {
@@ -620,17 +633,6 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         }
       }
       block_sync_lds();
-      if constexpr (qa_keep_tiles<D, DH>()) {
-        const int64_t wn = w + gridDim.x;
-        if (hg == G - 1 && wn < p.words) {
-#pragma unroll
-          for (int k = 0; k < TW; ++k) {
-            int tt = wave + NWV * k;
-            __asm__ volatile("" : "+v"(tt));
-            qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, tt, L, lane, afr[k], alw[k]);
-          }
-        }
-      }
       // not resident: the fragments were last read before the barrier above, so the next group's
       // weights are loaded now and written after the rows
       const bool more = !resident && (hg + 1 < G || w + gridDim.x < p.words);
@@ -661,6 +663,9 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
 // ------------------------------------------------------------------------------------------
 constexpr int kQpThreads = 768;
 constexpr int kQpTilesPerWave = 3;
+// Whether a word's token tiles are read at the word's start (and waited for there) rather than
+// during the previous word's last group of rows.
+constexpr bool kQpWordLoads = true;
 
 // the partner lane's value (lane ^ 1) within the quad
 __device__ __forceinline__ float pair_other(float v) {
@@ -743,6 +748,7 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
   const int L = p.L, ntiles = (L + 15) / 16;
   uint64_t *bfa = (uint64_t *)smem;                                  // [G][3][S][64] weight fragments
   float *qs = (float *)(smem + G * qa_frag_bytes<D>()), *kv = qs + (size_t)L * 16;
+  float *bl = kv + (size_t)L * kQaRow;                               // [3][D] Q, K, V biases
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, half = tid & 1;
   if (blockIdx.x >= p.words) return;
   for (int hg = 0; hg < G; ++hg) {
@@ -750,6 +756,7 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
     st.load(p.bpack, hg, tid);
     st.store(bfa + hg * FW, tid);
   }
+  for (int u = tid; u < 3 * D; u += kQpThreads) bl[u] = p.bias[u];
   // this pair's first row (token tid / 2): list metadata of both masks held for the kernel
   const int r0 = tid >> 1, i0 = r0 < L ? r0 : 0;
   const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
@@ -758,21 +765,37 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
-  {
+  if constexpr (!kQpWordLoads) {
     const int64_t w = blockIdx.x;
 #pragma unroll
     for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wave + NWV * k, L, lane, afr[k], alw[k]);
   }
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    if constexpr (kQpWordLoads) {
+      // the word's token tiles, waited for here: no global load is then outstanding inside the
+      // group loop, where a wait would also wait for the row outputs being written
+      int wv = wave;
+      __asm__ volatile("" : "+v"(wv));
+#pragma unroll
+      for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wv + NWV * k, L, lane, afr[k], alw[k]);
+#pragma unroll
+      for (int k = 0; k < TW; ++k) {
+#pragma unroll
+        for (int s2 = 0; s2 < S; ++s2) __asm__ volatile("" : "+v"(afr[k][s2]));
+        __asm__ volatile("" : "+v"(alw[k][0]), "+v"(alw[k][1]), "+v"(alw[k][2]), "+v"(alw[k][3]));
+      }
+    }
     for (int hg = 0; hg < G; ++hg) {
       const uint64_t *bf = bfa + hg * FW;
-      const float bq = p.bias[16 * hg + col], bk = p.bias[D + 16 * hg + col], bv = p.bias[2 * D + 16 * hg + col];
+      const float bq = bl[16 * hg + col], bk = bl[D + 16 * hg + col], bv = bl[2 * D + 16 * hg + col];
+      int wg = wave;
+      __asm__ volatile("" : "+v"(wg));
 #pragma unroll
       for (int k = 0; k < TW; ++k)
-        if (wave + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wave + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
+        if (wg + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wg + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
       block_sync_lds();
       const int64_t wn = w + gridDim.x;
-      if (hg == G - 1 && wn < p.words) {                   // the next word's tiles, read during these rows
+      if (!kQpWordLoads && hg == G - 1 && wn < p.words) {  // the next word's tiles, read during these rows
 #pragma unroll
         for (int k = 0; k < TW; ++k)
           qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, wave + NWV * k, L, lane, afr[k], alw[k]);
@@ -1806,7 +1829,8 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
 }
 
 size_t qkv_attention_lds(const Model &M, bool resident = false) {
-  return (size_t)(resident ? M.d / 16 : 1) * 3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4;
+  return (size_t)(resident ? M.d / 16 : 1) * 3 * (M.d / 32) * 64 * 8 + (size_t)M.L * (16 + kQaRow) * 4 +
+         (size_t)3 * M.d * 4;
 }
 
 // Keep every head group's weight tiles in LDS when that does not lower the blocks per CU.
@@ -1837,9 +1861,11 @@ static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_
 }
 
 // The lane-pair form (16-dimension heads): every group's weights resident, up to 36 token tiles.
+size_t qkv_attention_pair_lds(const Model &M) { return qkv_attention_lds(M, true); }
+
 bool qkv_attention_pair_supported(const Model &M) {
   return M.d == 128 && M.dh == 16 && M.grouped && M.L <= 16 * (kQpThreads / 64) * kQpTilesPerWave &&
-         qkv_attention_lds(M, true) <= 160 * 1024;
+         qkv_attention_pair_lds(M) <= 160 * 1024;
 }
 
 template <int D>
@@ -1880,7 +1906,7 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.resident = qkv_attention_resident(M) ? 1 : 0;
   const size_t lds = qkv_attention_lds(M, a.resident != 0);
   hipError_t e = hipErrorInvalidValue;
-  if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(a, qkv_attention_lds(M, true), s);
+  if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(a, qkv_attention_pair_lds(M), s);
   else if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
   else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
   else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(a, lds, s);
