@@ -94,3 +94,31 @@ def random_weights(n: int, m: int, d: int, n_layers: int, heads: int = 8, *, p_z
                         ln1_g=ln1_g, ln1_b=ln1_b, ln2_g=ln2_g, ln2_b=ln2_b,
                         head_w1=head_w1, head_b1=head_b1, head_wo=head_wo, head_bo=head_bo,
                         attention=attention)
+
+
+def random_spe_params(L: int, d_pe: int, heads: int, *, seed: int = 0) -> dict:
+    """Seeded parameters of the spectral positional encoding network (Section 4.3), fp32.
+
+    W_{2->d_PE} ~ N(0, 1); the attention's W_q, W_k, W_v, W_o ~ N(0, 1/d_PE), all stored
+    [in][out]; biases N(0, 0.1^2); the reduction over the L eigen-rows w_red ~ N(0, 1/L) with
+    bias b_red ~ N(0, 0.1^2).  Random: trained parameters are not available.
+    """
+    rng = np.random.default_rng(seed)
+    f = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    p = {"d_pe": int(d_pe), "heads": int(heads),
+         "w_in": f(rng.standard_normal((2, d_pe))), "b_in": f(0.1 * rng.standard_normal(d_pe))}
+    for name in ("q", "k", "v", "o"):
+        p["w_" + name] = f(rng.standard_normal((d_pe, d_pe)) / np.sqrt(d_pe))
+        p["b_" + name] = f(0.1 * rng.standard_normal(d_pe))
+    p["w_red"] = f(rng.standard_normal(L) / np.sqrt(L))
+    p["b_red"] = float(np.float32(0.1 * rng.standard_normal()))
+    return p
+
+
+def with_positional_table(w: ModelWeights, table: np.ndarray, d_pe: int) -> ModelWeights:
+    """The model with `table` as its positional table and the last d_pe embedding columns zeroed,
+    so that the embedded token is the concatenation of the scaled embedding and the table row."""
+    from dataclasses import replace
+    embed = w.embed.copy()
+    embed[:, w.d - d_pe:] = 0.0
+    return replace(w, embed=embed, pos=np.ascontiguousarray(table, dtype=np.float32))
