@@ -163,6 +163,75 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
 aecct_status aecct_aap_ternarize(const float *w, int64_t count, float percentile, float delta, float eps,
                                  int8_t *ternary, float *scale);
 
+/*
+ * Spectral positional encoding of the Tanner graph (Section 4.3, the SPE
+ * equations and Fig. 4): a create-time step whose output is the fixed
+ * positional table `aecct_weights.pos`.
+ *
+ * Graph: L = n + m nodes, variable nodes 0..n-1 then checks; node i and node
+ * n + j are joined where H[j][i] = 1.  Laplacian: D - A.
+ *
+ * Canonical eigenbasis (the paper leaves signs and bases of repeated
+ * eigenvalues open): eigenvalues ascending; consecutive ones closer than
+ * 1e-8 * max(1, max |lambda|) form one cluster; a cluster's basis is built from
+ * the columns P e_c of its eigenspace projector P in ascending c, each with the
+ * components along the vectors already taken removed, taken (normalised) when
+ * its squared norm exceeds 1e-6, until the cluster's dimension is reached.  It
+ * depends on the eigenspaces only, and gives a simple eigenvalue's vector the
+ * sign that makes its first entry of squared size above 1e-6 positive.
+ *
+ * aecct_tanner_spectrum: host call, no GPU work, float64 (Householder
+ * tridiagonalisation, then implicit QR steps with Wilkinson shifts).
+ *   H        host uint8 [m][n], 0/1 (zero rows or columns allowed);
+ *   eigvals  host double [L] out, ascending;
+ *   eigvecs  host double [L][L] out, row i = canonical unit eigenvector i.
+ * 1 <= m, 1 <= n, L <= 4096.  Errors: INVALID_ARG, OUT_OF_MEMORY,
+ * UNSUPPORTED (the iteration did not converge; not expected).
+ */
+aecct_status aecct_tanner_spectrum(const uint8_t *H, int32_t m, int32_t n, double *eigvals, double *eigvecs);
+
+/*
+ * Parameters of the SPE network, host fp32, row-major, [in][out]:
+ *   for node j, Phi_j in R^{L x 2} has row i = (lambda_i, phi_i[j]);
+ *   Z = Phi_j w_in + b_in                      (W_{2->d_PE}, [2][d_pe]);
+ *   multi-head self-attention over the L rows with Q = K = V = Z:
+ *     head h of `heads` uses columns h*dk..h*dk+dk-1, dk = d_pe / heads, of
+ *     Z w_q + b_q, Z w_k + b_k, Z w_v + b_v; softmax(Q_h K_h^T / sqrt(dk)) V_h;
+ *     heads concatenated, then w_o + b_o -> U in R^{L x d_pe};
+ *   SPE_j = w_red^T U + b_red                  (W_{(2n-k)->1} over the L rows).
+ * Bias pointers may be NULL (zero).
+ */
+typedef struct aecct_spe_params {
+  int32_t d_pe;                       /* width of the encoding */
+  int32_t heads;                      /* heads of its attention; d_pe % heads == 0 */
+  const float *w_in, *b_in;           /* [2][d_pe], [d_pe] */
+  const float *w_q, *w_k, *w_v, *w_o; /* [d_pe][d_pe] each */
+  const float *b_q, *b_k, *b_v, *b_o; /* [d_pe] each */
+  const float *w_red;                 /* [L] */
+  float b_red;
+} aecct_spe_params;
+
+/*
+ * The positional table from a given spectrum (any orthonormal eigenvectors;
+ * the table depends on the basis).  Runs the attention on the current HIP
+ * device (fp32, exp2 on the hardware unit), synchronously; the rest on the host
+ * in float64.
+ *   eigvals  host double [L]; eigvecs host double [L][L], row i = eigenvector i;
+ *   pos      host fp32 [L][d] out: row j = zeros in columns 0..d-d_pe-1, SPE_j
+ *            in the last d_pe columns, so that with an embedding whose last d_pe
+ *            columns are zero, t_j E_j + P_j is the concatenation [t_j E_j, SPE_j].
+ * 1 <= L <= 4096, 1 <= heads <= d_pe <= d, d_pe % heads == 0, every value
+ * finite.  Errors: INVALID_ARG, OUT_OF_MEMORY, DEVICE (no GPU, or a HIP
+ * allocation, copy or launch failed).
+ */
+aecct_status aecct_spe_table_from_spectrum(const double *eigvals, const double *eigvecs, int32_t L,
+                                           const aecct_spe_params *p, int32_t d, float *pos);
+
+/* aecct_tanner_spectrum followed by aecct_spe_table_from_spectrum; same
+ * arguments and errors. */
+aecct_status aecct_spe_table(const uint8_t *H, int32_t m, int32_t n, const aecct_spe_params *p, int32_t d,
+                             float *pos);
+
 /* Release a model (NULL is a no-op).  No call may still be running on it. */
 void aecct_destroy(aecct_model *model);
 

@@ -46,6 +46,13 @@ class ModelInfo(C.Structure):
                 ("attention", C.c_int32), ("layered_attention", C.c_int32)]
 
 
+class SpeParams(C.Structure):
+    _fields_ = [("d_pe", C.c_int32), ("heads", C.c_int32), ("w_in", _f32p), ("b_in", _f32p),
+                ("w_q", _f32p), ("w_k", _f32p), ("w_v", _f32p), ("w_o", _f32p),
+                ("b_q", _f32p), ("b_k", _f32p), ("b_v", _f32p), ("b_o", _f32p),
+                ("w_red", _f32p), ("b_red", C.c_float)]
+
+
 class AecctError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -94,6 +101,14 @@ def lib():
         L.aecct_ternary_gemm.argtypes = [_vp, C.c_int32, C.c_int32, _vp, C.c_int64, _vp, _vp]
         L.aecct_aap_ternarize.restype = C.c_int
         L.aecct_aap_ternarize.argtypes = [_f32p, C.c_int64, C.c_float, C.c_float, C.c_float, _i8p, _f32p]
+        _f64p = C.POINTER(C.c_double)
+        L.aecct_tanner_spectrum.restype = C.c_int
+        L.aecct_tanner_spectrum.argtypes = [_u8p, C.c_int32, C.c_int32, _f64p, _f64p]
+        L.aecct_spe_table_from_spectrum.restype = C.c_int
+        L.aecct_spe_table_from_spectrum.argtypes = [_f64p, _f64p, C.c_int32, C.POINTER(SpeParams), C.c_int32,
+                                                    _f32p]
+        L.aecct_spe_table.restype = C.c_int
+        L.aecct_spe_table.argtypes = [_u8p, C.c_int32, C.c_int32, C.POINTER(SpeParams), C.c_int32, _f32p]
         L.aecct_check_device_arith.restype = C.c_int
         L.aecct_check_device_arith.argtypes = [C.POINTER(C.c_uint64)]
         _lib = L
@@ -110,6 +125,58 @@ def aap_ternarize(w, percentile: float = 0.5, delta: float = 1.0, eps: float = 1
                                      float(np.float32(delta)), float(np.float32(eps)), t.ctypes.data_as(_i8p),
                                      C.byref(sc)), "aecct_aap_ternarize")
     return t, np.float32(sc.value)
+
+
+def tanner_spectrum(H):
+    """Laplacian spectrum of the Tanner graph of H by the library (host, float64): returns
+    (eigenvalues ascending [L], eigenvectors [L, L] with ROW i the canonical vector i)."""
+    H = np.ascontiguousarray(H, dtype=np.uint8)
+    m, n = H.shape
+    lam = np.zeros(n + m, np.float64)
+    vec = np.zeros((n + m, n + m), np.float64)
+    _check(lib().aecct_tanner_spectrum(H.ctypes.data_as(_u8p), m, n, lam.ctypes.data_as(C.POINTER(C.c_double)),
+                                       vec.ctypes.data_as(C.POINTER(C.c_double))), "aecct_tanner_spectrum")
+    return lam, vec
+
+
+def _spe_struct(p: dict, L: int):
+    keep = {k: _host(p.get(k), np.float32) for k in ("w_in", "b_in", "w_q", "w_k", "w_v", "w_o", "b_q", "b_k",
+                                                     "b_v", "b_o", "w_red")}
+    if keep["w_red"] is not None and keep["w_red"].size != L:
+        raise ValueError(f"w_red must have {L} entries")
+    s = SpeParams(d_pe=int(p["d_pe"]), heads=int(p["heads"]), b_red=float(np.float32(p.get("b_red", 0.0))))
+    for k, a in keep.items():
+        setattr(s, k, _p32(a))
+    return s, keep
+
+
+def _p32(a):
+    return a.ctypes.data_as(_f32p) if a is not None else None
+
+
+def spe_table_from_spectrum(lam, vec_rows, p: dict, d: int):
+    """Positional table [L, d] fp32 from a spectrum (ROW i of vec_rows = eigenvector i) and
+    the SPE parameters (Section 4.3); the attention runs on the current GPU."""
+    lam = np.ascontiguousarray(lam, dtype=np.float64)
+    vec = np.ascontiguousarray(vec_rows, dtype=np.float64)
+    L = lam.size
+    s, keep = _spe_struct(p, L)
+    out = np.zeros((L, d), np.float32)
+    _check(lib().aecct_spe_table_from_spectrum(lam.ctypes.data_as(C.POINTER(C.c_double)),
+                                               vec.ctypes.data_as(C.POINTER(C.c_double)), L, C.byref(s), d,
+                                               out.ctypes.data_as(_f32p)), "aecct_spe_table_from_spectrum")
+    return out
+
+
+def spe_table(H, p: dict, d: int):
+    """The whole SPE construction (spectrum, then attention) for H: positional table [L, d]."""
+    H = np.ascontiguousarray(H, dtype=np.uint8)
+    m, n = H.shape
+    s, keep = _spe_struct(p, n + m)
+    out = np.zeros((n + m, d), np.float32)
+    _check(lib().aecct_spe_table(H.ctypes.data_as(_u8p), m, n, C.byref(s), d, out.ctypes.data_as(_f32p)),
+           "aecct_spe_table")
+    return out
 
 
 def check_device_arith():
