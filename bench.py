@@ -183,11 +183,19 @@ def spe_bench(c: int, repeats: int = 3):
         P.spe_table_from_spectrum(lam, vec, p, d)
         best = min(best, time.perf_counter() - t0)
     pairs = L * heads * L * L            # (node, head, row, key)
+    import oracle.spe as ospe
+    k = 4
+    t0 = time.perf_counter()
+    ospe.spe_table_from_spectrum(lam, vec.T, p, d, nodes=list(range(k)))
+    dt = time.perf_counter() - t0
     print(json.dumps({"metric": "SPE table construction (Section 4.3), create time", "value": best * 1e3,
                       "unit": "ms (table from spectrum, incl. copies)", "higher_is_better": False,
                       "spectrum_host_s": t_spec, "score_pairs": pairs, "pairs_per_s": pairs / best,
                       "config": {"workload": f"spe_{cfg.name}", "tokens": L, "d": d, "d_pe": d_pe,
-                                 "heads": heads}}), flush=True)
+                                 "heads": heads},
+                      "cpu_baseline": {"value": dt / k * L * 1e3, "unit": "ms (table from spectrum)", "cores": 1,
+                                       "kind": "oracle", "sample": f"{k} of {L} nodes, float64 numpy, "
+                                       f"{dt:.1f} s, scaled to all nodes"}}), flush=True)
 
 
 def main():

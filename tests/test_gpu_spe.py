@@ -82,6 +82,25 @@ def test_spe_table_end_to_end(P, name):
     assert err <= _tol(n + m, ref), err
 
 
+def test_spe_largest_graph(P):
+    """L = 4096, the largest accepted: the attention from an orthonormal DCT-II basis standing in
+    for a spectrum (the table is defined for any orthonormal eigenvectors), 3 sampled nodes."""
+    L, d = 4096, 128
+    print("[spe-max] L 4096", flush=True)
+    k = np.arange(L)[:, None]
+    x = np.arange(L)[None, :]
+    V_rows = np.sqrt(2.0 / L) * np.cos(np.pi * (x + 0.5) * k / L)
+    V_rows[0] /= np.sqrt(2.0)
+    lam = np.sort(np.random.default_rng(2).uniform(0.0, 12.0, L))
+    p = random_spe_params(L, 32, 4, seed=8)
+    got = P.spe_table_from_spectrum(lam, V_rows, p, d)
+    nodes = [0, 1777, L - 1]
+    ref = spe.spe_table_from_spectrum(lam, V_rows.T, p, d, nodes=nodes)
+    err = np.abs(got[nodes].astype(np.float64) - ref).max()
+    print(f"[spe-max] max |err| {err:.3g}", flush=True)
+    assert err <= _tol(L, ref), err
+
+
 def test_spe_zero_input_map(P):
     """W_in = 0, b_in = 0: uniform attention, every node's SPE = sum(w_red)(b_v W_o + b_o) + b_red."""
     H = parity_check(CONFIGS[2])
