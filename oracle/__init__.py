@@ -29,7 +29,7 @@ class _Model(C.Structure):
                 ("w", _i8p * 6), ("scale", _f32p), ("bias", _f32p * 6),
                 ("ln1_g", _f32p), ("ln1_b", _f32p), ("ln2_g", _f32p), ("ln2_b", _f32p),
                 ("head_w1", _f32p), ("head_b1", C.c_float), ("head_wo", _f32p), ("head_bo", _f32p),
-                ("attention", C.c_int32)]
+                ("attention", C.c_int32), ("act_scale_mode", C.c_int32)]
 
 
 class _Taps(C.Structure):
@@ -56,6 +56,7 @@ def lib():
         L.oracle_masks.argtypes = [_u8p, C.c_int32, C.c_int32, _u8p, _u8p]
         L.oracle_preprocess.argtypes = [_u8p, C.c_int32, C.c_int32, _f32p, _f32p]
         L.oracle_quant_rows.argtypes = [_f32p, C.c_int64, C.c_int32, _i8p, _f32p]
+        L.oracle_quant_word.argtypes = [_f32p, C.c_int64, C.c_int32, _i8p, _f32p]
         L.oracle_linear_rows.argtypes = [_i8p, _f32p, C.c_int64, _i8p, C.c_int32, C.c_int32, C.c_float,
                                          _f32p, _f32p, _i32p]
         L.oracle_layernorm_rows.argtypes = [_f32p, C.c_int64, C.c_int32, _f32p, _f32p, C.c_float, _f32p]
@@ -72,6 +73,9 @@ def lib():
         L.oracle_aap_ternarize.argtypes = [_f32p, C.c_int64, C.c_float, C.c_float, C.c_float, _i8p, _f32p]
         L.oracle_decode_ref64.restype = C.c_int
         L.oracle_decode_ref64.argtypes = [C.POINTER(_Model), _f32p, C.c_int64, _u8p, _f64p, C.c_int32]
+        L.oracle_decode_ref64_word.restype = C.c_int
+        L.oracle_decode_ref64_word.argtypes = [C.POINTER(_Model), _f32p, _u8p, _f64p, _i8p, _i8p, C.c_double,
+                                               C.POINTER(C.c_int64)]
         _lib = L
     return _lib
 
@@ -86,6 +90,7 @@ def _c(a, dtype):
 
 KINDS = ("q", "k", "v", "o", "ff1", "ff2")
 ATTENTION = {"hpsa": 0, "casa": 1}
+ACT_SCALE = {"token": 0, "word": 1}
 
 
 class OracleModel:
@@ -121,6 +126,7 @@ class OracleModel:
         st.head_wo = _p(keep(w.head_wo, np.float32), _f32p)
         st.head_bo = _p(keep(w.head_bo, np.float32), _f32p)
         st.attention = ATTENTION[getattr(w, "attention", "hpsa")]
+        st.act_scale_mode = ACT_SCALE[getattr(w, "act_scale", "token")]
         self.st = st
 
     # ------------------------------------------------------------ whole decode
@@ -144,6 +150,33 @@ class OracleModel:
         if rc:
             raise RuntimeError("oracle_decode_ref64 failed")
         return bits, f
+
+    def decode_ref64_word(self, y_word, force=None, margin: float = 0.0):
+        """One word in the fp64 reference mode: (bits, f float64, codes dict, stats) where codes
+        holds the word's int8 activation codes per layer: xq [N, L, d], oq, x1q [N, L, d],
+        gq [N, L, d_ff] (the same quantisation points as the canonical taps).  `force`, a dict of
+        such codes (e.g. canonical taps), decides codes whose fp64 value lies within `margin` of
+        a rounding tie; stats = (codes so decided against the fp64 choice, codes of `force` that
+        differ from the fp64 choice away from a tie)."""
+        w = self.w
+        N, L, d, dff = w.n_layers, self.L, w.d, w.d_ff
+        y = _c(y_word, np.float32).reshape(-1)
+        codes = np.zeros((N, L * (3 * d + dff)), np.int8)
+        fc = None
+        if force is not None:
+            fc = np.ascontiguousarray(np.concatenate(
+                [np.asarray(force[k], np.int8).reshape(N, -1) for k in ("xq", "oq", "x1q", "gq")], 1))
+            assert fc.shape == codes.shape
+        bits = np.zeros(self.n, np.uint8)
+        f = np.zeros(self.n, np.float64)
+        stats = np.zeros(2, np.int64)
+        if lib().oracle_decode_ref64_word(C.byref(self.st), _p(y, _f32p), _p(bits, _u8p), _p(f, _f64p),
+                                          _p(codes, _i8p), _p(fc, _i8p), float(margin),
+                                          stats.ctypes.data_as(C.POINTER(C.c_int64))):
+            raise RuntimeError("oracle_decode_ref64_word failed")
+        c = {"xq": codes[:, :L * d].reshape(N, L, d), "oq": codes[:, L * d:2 * L * d].reshape(N, L, d),
+             "x1q": codes[:, 2 * L * d:3 * L * d].reshape(N, L, d), "gq": codes[:, 3 * L * d:].reshape(N, L, dff)}
+        return bits, f, c, (int(stats[0]), int(stats[1]))
 
     def decode_taps(self, y_word):
         """One word; returns (bits, f, taps dict of per-layer arrays)."""
@@ -247,6 +280,16 @@ def quant_rows(x):
     q = np.zeros((rows, K), np.int8)
     r = np.zeros(rows, np.float32)
     lib().oracle_quant_rows(_p(x, _f32p), rows, K, _p(q, _i8p), _p(r, _f32p))
+    return q, r
+
+
+def quant_word(x):
+    """Eq. 2 with one alpha over all rows of x (a word): (codes, alpha per row, all equal)."""
+    x = _c(x, np.float32)
+    rows, K = x.shape
+    q = np.zeros((rows, K), np.int8)
+    r = np.zeros(rows, np.float32)
+    lib().oracle_quant_word(_p(x, _f32p), rows, K, _p(q, _i8p), _p(r, _f32p))
     return q, r
 
 

@@ -178,6 +178,43 @@ void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float
 }
 
 /*
+ * The same quantiser with one alpha per word (Section 4.1 states alpha = ||x||_inf of the layer
+ * input x and calls every scaling factor a scalar): alpha = max |x| over all rows*K values of the
+ * word, every row's codes x * fp32(Q_b / alpha) rounded half to even, and every row's r set to
+ * that alpha (so the dequantisation of Eq. 3 is unchanged).  An all-zero word gives q = 0, r = 0.
+ * Pin: alpha equals the library maximum of |x| over the word; on a word whose rows share one
+ * maximum it equals the per-token form bit for bit; |q| <= 127, the argmax maps to +-127, the
+ * error bound of Eq. 2 with alpha of the word.
+ */
+void oracle_quant_word(const float *x, int64_t rows, int32_t K, int8_t *q, float *r) {
+  float a = 0.0f;
+  for (int64_t e = 0; e < rows * K; ++e) {
+    float v = fabsf(x[e]);
+    if (v > a) a = v;
+  }
+  for (int64_t i = 0; i < rows; ++i) r[i] = a;
+  if (a == 0.0f) {
+    memset(q, 0, (size_t)(rows * K));
+    return;
+  }
+  const float inv = 127.0f / a;
+  for (int64_t e = 0; e < rows * K; ++e) {
+    double v = rint((double)x[e] * (double)inv);
+    if (v > 127.0) v = 127.0;
+    if (v < -127.0) v = -127.0;
+    q[e] = (int8_t)v;
+  }
+}
+
+/* Eq. 2 at one quantisation point of a word: per token or per word, as the model says. */
+static void quant_act(const oracle_model *M, const float *x, int64_t rows, int32_t K, int8_t *q, float *r) {
+  if (M->act_scale_mode == 1)
+    oracle_quant_word(x, rows, K, q, r);
+  else
+    oracle_quant_rows(x, rows, K, q, r);
+}
+
+/*
  * AAPLinear at inference, Eq. 3: integer product of the int8 activations and
  * the ternary weights (additions and subtractions only), dequantised by
  * gamma*delta*alpha/Q_b before the bias is added (Section 4.1).  With
@@ -435,7 +472,7 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     const int64_t LD = L * d;
     if (tp && tp->x_in) memcpy(tp->x_in + l * LD, w->X, sizeof(float) * LD);
     /* a. Q, K, V from the int8 input */
-    oracle_quant_rows(w->X, L, (int32_t)d, w->q, w->r);
+    quant_act(M, w->X, L, (int32_t)d, w->q, w->r);
     if (tp && tp->xq) memcpy(tp->xq + l * LD, w->q, (size_t)LD);
     if (tp && tp->ax) memcpy(tp->ax + l * L, w->r, sizeof(float) * L);
     /* the query map carries the score scale log2(e)/sqrt(d_h) in its dequant scale and bias */
@@ -452,7 +489,7 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     if (oracle_attention_word(M, M1, M2, w->qkv, w->O)) return -1;
     if (tp && tp->o) memcpy(tp->o + l * LD, w->O, sizeof(float) * LD);
     /* c. output projection, residual, LN1 */
-    oracle_quant_rows(w->O, L, (int32_t)d, w->q, w->r);
+    quant_act(M, w->O, L, (int32_t)d, w->q, w->r);
     if (tp && tp->oq) memcpy(tp->oq + l * LD, w->q, (size_t)LD);
     if (tp && tp->ao) memcpy(tp->ao + l * L, w->r, sizeof(float) * L);
     oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sq[ORC_O],
@@ -462,14 +499,14 @@ static int decode_word(const oracle_model *M, const uint8_t *M1, const uint8_t *
     oracle_layernorm_rows(w->R, L, (int32_t)d, M->ln1_g + l * d, M->ln1_b + l * d, M->ln_eps, w->X1);
     if (tp && tp->x1) memcpy(tp->x1 + l * LD, w->X1, sizeof(float) * LD);
     /* d. FFN with ReLU, residual, LN2 */
-    oracle_quant_rows(w->X1, L, (int32_t)d, w->q, w->r);
+    quant_act(M, w->X1, L, (int32_t)d, w->q, w->r);
     if (tp && tp->x1q) memcpy(tp->x1q + l * LD, w->q, (size_t)LD);
     if (tp && tp->a1) memcpy(tp->a1 + l * L, w->r, sizeof(float) * L);
     oracle_linear_rows(w->q, w->r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sq[ORC_FF1],
                        bvec(M, ORC_FF1, l), w->F, w->accf);
     if (tp && tp->acc_ff1) memcpy(tp->acc_ff1 + l * L * dff, w->accf, sizeof(int32_t) * L * dff);
     for (int64_t e = 0; e < L * dff; ++e) w->F[e] = w->F[e] > 0.0f ? w->F[e] : 0.0f;
-    oracle_quant_rows(w->F, L, (int32_t)dff, w->gq, w->rg);
+    quant_act(M, w->F, L, (int32_t)dff, w->gq, w->rg);
     if (tp && tp->gq) memcpy(tp->gq + l * L * dff, w->gq, (size_t)(L * dff));
     if (tp && tp->ag) memcpy(tp->ag + l * L, w->rg, sizeof(float) * L);
     oracle_linear_rows(w->gq, w->rg, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sq[ORC_FF2],
@@ -488,6 +525,7 @@ static int check_model(const oracle_model *M) {
   int32_t dh = M->d / M->heads;
   if ((M->d & (M->d - 1)) || (dh & (dh - 1))) return -1;
   if (M->d > ORC_MAX_TREE || M->d_ff > ORC_MAX_TREE || M->n + M->m > ORC_MAX_TREE) return -1;
+  if (M->act_scale_mode != 0 && M->act_scale_mode != 1) return -1;
   return 0;
 }
 
@@ -540,14 +578,47 @@ int oracle_decode_taps(const oracle_model *M, const float *y, uint8_t *bits, flo
 
 /* ------------------------------------------------------------------ fp64 reference mode */
 
-static void quant_rows_f64(const double *x, int64_t rows, int32_t K, int32_t *q, double *r) {
+/* Decisions of near-tie codes (test support): where x * 127 / alpha lies within `margin` of a
+ * rounding tie k + 1/2 the fp64 decision and a fp32 one may both be right, so the code is taken
+ * from `force` (a code list of the same layout, e.g. the canonical mode's) when that code is one
+ * of the two neighbours of the tie; stats[0] counts such codes that differ from the fp64
+ * decision, stats[1] codes of `force` that differ from it anywhere else. */
+typedef struct {
+  const int8_t *force;
+  double margin;
+  int64_t stats[2];
+} tie_rule;
+
+/* Eq. 2 in fp64: alpha per row (act_scale_mode 0) or one alpha over all rows (1); codes as
+ * rint(x * 127 / alpha) clipped to +-127.  When codes is not NULL the int8 codes are also
+ * copied there; when ties is not NULL, near-tie codes follow it (see tie_rule). */
+static void quant_rows_f64(const double *x, int64_t rows, int32_t K, int per_word, int32_t *q, double *r,
+                           int8_t *codes, tie_rule *ties, int64_t tie_off) {
+  double aw = 0.0;
+  if (per_word)
+    for (int64_t e = 0; e < rows * K; ++e) aw = fmax(aw, fabs(x[e]));
   for (int64_t i = 0; i < rows; ++i) {
-    double a = 0.0;
-    for (int32_t c = 0; c < K; ++c) a = fmax(a, fabs(x[i * K + c]));
+    double a = aw;
+    if (!per_word)
+      for (int32_t c = 0; c < K; ++c) a = fmax(a, fabs(x[i * K + c]));
     r[i] = a;
     for (int32_t c = 0; c < K; ++c) {
-      double v = a == 0.0 ? 0.0 : rint(x[i * K + c] * (127.0 / a));
-      q[i * K + c] = (int32_t)fmin(127.0, fmax(-127.0, v));
+      const double u = a == 0.0 ? 0.0 : x[i * K + c] * (127.0 / a);
+      double v = fmin(127.0, fmax(-127.0, rint(u)));
+      if (ties && ties->force) {
+        const double fv = (double)ties->force[tie_off + i * K + c];
+        if (fv != v) {
+          const double lo = floor(u);
+          if (fabs(u - (lo + 0.5)) <= ties->margin && (fv == lo || fv == lo + 1.0)) {
+            ++ties->stats[0];
+            v = fv;
+          } else {
+            ++ties->stats[1];
+          }
+        }
+      }
+      q[i * K + c] = (int32_t)v;
+      if (codes) codes[i * K + c] = (int8_t)v;
     }
   }
 }
@@ -604,10 +675,70 @@ int oracle_attention_dense_f64(const oracle_model *M, const uint8_t *M1, const u
   return 0;
 }
 
+/* One word of the fp64 reference decode (embedding, N Post-LN blocks with dense masked
+ * attention, head); codes as described in the header, or NULL. */
+static int ref64_word(const oracle_model *M, const uint8_t *M1, const uint8_t *M2, const float *yb,
+                      uint8_t *bits, double *f, int8_t *codes, tie_rule *ties) {
+  const int64_t L = M->n + M->m, d = M->d, dff = M->d_ff, n = M->n;
+  const int pw = M->act_scale_mode == 1;
+  int err = 0;
+  double *X = malloc(sizeof(double) * L * d), *qkv = malloc(sizeof(double) * L * 3 * d);
+  double *O = malloc(sizeof(double) * L * d), *Y = malloc(sizeof(double) * L * dff);
+  double *X1 = malloc(sizeof(double) * L * d), *r = malloc(sizeof(double) * L);
+  int32_t *q = malloc(sizeof(int32_t) * L * dff);
+  float *t = malloc(sizeof(float) * L);
+  if (!X || !qkv || !O || !Y || !X1 || !r || !q || !t) {
+    err = -1;
+  } else {
+    oracle_preprocess(M->H, M->m, M->n, yb, t);
+    for (int64_t i = 0; i < L; ++i)
+      for (int64_t c = 0; c < d; ++c)
+        X[i * d + c] = (double)t[i] * M->embed[i * d + c] + (M->pos ? M->pos[i * d + c] : 0.0);
+    for (int32_t l = 0; l < M->n_layers && !err; ++l) {
+      const float *sc = M->scale + (int64_t)l * 6;
+      const int64_t lo = (int64_t)l * L * (3 * d + dff);
+      int8_t *cl = codes ? codes + lo : NULL;
+      quant_rows_f64(X, L, (int32_t)d, pw, q, r, cl, ties, lo);
+      for (int kind = ORC_Q; kind <= ORC_V; ++kind) {
+        linear_rows_f64(q, r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d, sc[kind], bvec(M, kind, l), Y);
+        for (int64_t i = 0; i < L; ++i)
+          for (int64_t c = 0; c < d; ++c) qkv[i * 3 * d + kind * d + c] = Y[i * d + c];
+      }
+      if (oracle_attention_dense_f64(M, M1, M2, qkv, 1.0 / sqrt((double)(d / M->heads)), O)) { err = -1; break; }
+      quant_rows_f64(O, L, (int32_t)d, pw, q, r, cl ? cl + L * d : NULL, ties, lo + L * d);
+      linear_rows_f64(q, r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O], bvec(M, ORC_O, l), Y);
+      for (int64_t e = 0; e < L * d; ++e) X1[e] = X[e] + Y[e];
+      layernorm_f64(X1, L, (int32_t)d, M->ln1_g + l * d, M->ln1_b + l * d, M->ln_eps);
+      quant_rows_f64(X1, L, (int32_t)d, pw, q, r, cl ? cl + 2 * L * d : NULL, ties, lo + 2 * L * d);
+      linear_rows_f64(q, r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sc[ORC_FF1], bvec(M, ORC_FF1, l), Y);
+      for (int64_t e = 0; e < L * dff; ++e) Y[e] = Y[e] > 0.0 ? Y[e] : 0.0;
+      quant_rows_f64(Y, L, (int32_t)dff, pw, q, r, cl ? cl + 3 * L * d : NULL, ties, lo + 3 * L * d);
+      linear_rows_f64(q, r, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sc[ORC_FF2], bvec(M, ORC_FF2, l), X);
+      for (int64_t e = 0; e < L * d; ++e) X[e] = X1[e] + X[e];
+      layernorm_f64(X, L, (int32_t)d, M->ln2_g + l * d, M->ln2_b + l * d, M->ln_eps);
+    }
+    if (!err) {
+      for (int64_t i = 0; i < L; ++i) {          /* z_i = W_{d->1} x_i + b1, kept in r */
+        double z = M->head_b1;
+        for (int64_t c = 0; c < d; ++c) z += X[i * d + c] * M->head_w1[c];
+        r[i] = z;
+      }
+      for (int64_t o = 0; o < n; ++o) {
+        double acc = M->head_bo[o];
+        for (int64_t i = 0; i < L; ++i) acc += r[i] * M->head_wo[i * n + o];
+        f[o] = acc;
+        bits[o] = (uint8_t)((yb[o] < 0.0f) ^ (acc < 0.0));
+      }
+    }
+  }
+  free(X); free(qkv); free(O); free(Y); free(X1); free(r); free(q); free(t);
+  return err;
+}
+
 int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, uint8_t *bits,
                         double *f, int32_t n_threads) {
   if (check_model(M)) return -1;
-  const int64_t L = M->n + M->m, d = M->d, dff = M->d_ff, n = M->n;
+  const int64_t L = M->n + M->m, n = M->n;
   uint8_t *M1 = malloc((size_t)(L * L)), *M2 = malloc((size_t)(L * L));
   if (!M1 || !M2) { free(M1); free(M2); return -1; }
   oracle_masks(M->H, M->m, M->n, M1, M2);
@@ -616,58 +747,29 @@ int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, ui
   if (n_threads < 1) n_threads = 1;
 #pragma omp parallel for num_threads(n_threads) schedule(dynamic, 1) reduction(| : err)
 #endif
-  for (int64_t b = 0; b < batch; ++b) {
-    const float *yb = y + b * n;
-    double *X = malloc(sizeof(double) * L * d), *qkv = malloc(sizeof(double) * L * 3 * d);
-    double *O = malloc(sizeof(double) * L * d), *Y = malloc(sizeof(double) * L * dff);
-    double *X1 = malloc(sizeof(double) * L * d), *r = malloc(sizeof(double) * L);
-    int32_t *q = malloc(sizeof(int32_t) * L * dff);
-    float *t = malloc(sizeof(float) * L);
-    if (!X || !qkv || !O || !Y || !X1 || !r || !q || !t) {
-      err |= 1;
-    } else {
-      oracle_preprocess(M->H, M->m, M->n, yb, t);
-      for (int64_t i = 0; i < L; ++i)
-        for (int64_t c = 0; c < d; ++c)
-          X[i * d + c] = (double)t[i] * M->embed[i * d + c] + (M->pos ? M->pos[i * d + c] : 0.0);
-      for (int32_t l = 0; l < M->n_layers && !err; ++l) {
-        const float *sc = M->scale + (int64_t)l * 6;
-        quant_rows_f64(X, L, (int32_t)d, q, r);
-        for (int kind = ORC_Q; kind <= ORC_V; ++kind) {
-          linear_rows_f64(q, r, L, wmat(M, kind, l), (int32_t)d, (int32_t)d, sc[kind], bvec(M, kind, l), Y);
-          for (int64_t i = 0; i < L; ++i)
-            for (int64_t c = 0; c < d; ++c) qkv[i * 3 * d + kind * d + c] = Y[i * d + c];
-        }
-        if (oracle_attention_dense_f64(M, M1, M2, qkv, 1.0 / sqrt((double)(d / M->heads)), O)) { err |= 1; break; }
-        quant_rows_f64(O, L, (int32_t)d, q, r);
-        linear_rows_f64(q, r, L, wmat(M, ORC_O, l), (int32_t)d, (int32_t)d, sc[ORC_O], bvec(M, ORC_O, l), Y);
-        for (int64_t e = 0; e < L * d; ++e) X1[e] = X[e] + Y[e];
-        layernorm_f64(X1, L, (int32_t)d, M->ln1_g + l * d, M->ln1_b + l * d, M->ln_eps);
-        quant_rows_f64(X1, L, (int32_t)d, q, r);
-        linear_rows_f64(q, r, L, wmat(M, ORC_FF1, l), (int32_t)d, (int32_t)dff, sc[ORC_FF1], bvec(M, ORC_FF1, l), Y);
-        for (int64_t e = 0; e < L * dff; ++e) Y[e] = Y[e] > 0.0 ? Y[e] : 0.0;
-        quant_rows_f64(Y, L, (int32_t)dff, q, r);
-        linear_rows_f64(q, r, L, wmat(M, ORC_FF2, l), (int32_t)dff, (int32_t)d, sc[ORC_FF2], bvec(M, ORC_FF2, l), X);
-        for (int64_t e = 0; e < L * d; ++e) X[e] = X1[e] + X[e];
-        layernorm_f64(X, L, (int32_t)d, M->ln2_g + l * d, M->ln2_b + l * d, M->ln_eps);
-      }
-      if (!err) {
-        for (int64_t i = 0; i < L; ++i) {          /* z_i = W_{d->1} x_i + b1, kept in r */
-          double z = M->head_b1;
-          for (int64_t c = 0; c < d; ++c) z += X[i * d + c] * M->head_w1[c];
-          r[i] = z;
-        }
-        for (int64_t o = 0; o < n; ++o) {
-          double acc = M->head_bo[o];
-          for (int64_t i = 0; i < L; ++i) acc += r[i] * M->head_wo[i * n + o];
-          f[b * n + o] = acc;
-          bits[b * n + o] = (uint8_t)((yb[o] < 0.0f) ^ (acc < 0.0));
-        }
-      }
-    }
-    free(X); free(qkv); free(O); free(Y); free(X1); free(r); free(q); free(t);
-  }
+  for (int64_t b = 0; b < batch; ++b)
+    if (ref64_word(M, M1, M2, y + b * n, bits + b * n, f + b * n, NULL, NULL)) err |= 1;
   free(M1);
   free(M2);
   return err ? -1 : 0;
+}
+
+int oracle_decode_ref64_word(const oracle_model *M, const float *y, uint8_t *bits, double *f,
+                             int8_t *codes, const int8_t *force, double margin, int64_t *stats) {
+  if (check_model(M) || (force && !(margin >= 0.0))) return -1;
+  const int64_t L = M->n + M->m;
+  uint8_t *M1 = malloc((size_t)(L * L)), *M2 = malloc((size_t)(L * L));
+  int err = (!M1 || !M2) ? -1 : 0;
+  tie_rule ties = {force, margin, {0, 0}};
+  if (!err) {
+    oracle_masks(M->H, M->m, M->n, M1, M2);
+    err = ref64_word(M, M1, M2, y, bits, f, codes, force ? &ties : NULL);
+  }
+  if (stats) {
+    stats[0] = ties.stats[0];
+    stats[1] = ties.stats[1];
+  }
+  free(M1);
+  free(M2);
+  return err;
 }

@@ -52,6 +52,8 @@ typedef struct oracle_model {
   const float *head_bo;       /* [n] */
   int32_t attention;          /* 0: HPSA head partitioning (Section 4.2); 1: CASA, every head
                                  over the ECCT mask M1 | M2 (Section 3) */
+  int32_t act_scale_mode;     /* Eq. 2 scale alpha: 0 = per token (max over the row's features),
+                                 1 = per word (max over all of the word's tokens and features) */
 } oracle_model;
 
 /* Per-layer intermediate values of one word (each pointer may be NULL). */
@@ -76,6 +78,7 @@ float oracle_query_scale(int32_t dh);
 void oracle_masks(const uint8_t *H, int32_t m, int32_t n, uint8_t *M1, uint8_t *M2);
 void oracle_preprocess(const uint8_t *H, int32_t m, int32_t n, const float *y, float *t);
 void oracle_quant_rows(const float *x, int64_t rows, int32_t K, int8_t *q, float *r);
+void oracle_quant_word(const float *x, int64_t rows, int32_t K, int8_t *q, float *r);
 void oracle_linear_rows(const int8_t *q, const float *r, int64_t rows, const int8_t *T, int32_t K,
                         int32_t n_out, float sq, const float *b, float *out, int32_t *acc);
 void oracle_layernorm_rows(const float *R, int64_t rows, int32_t d, const float *g, const float *b,
@@ -92,6 +95,14 @@ int oracle_decode_taps(const oracle_model *M, const float *y, uint8_t *bits, flo
                        const oracle_taps *taps);
 int oracle_decode_ref64(const oracle_model *M, const float *y, int64_t batch, uint8_t *bits,
                         double *f, int32_t n_threads);
+/* One word in the fp64 reference mode; codes (may be NULL) receives every int8 activation code
+ * the word's layers form, per layer l in the order Q/K/V input [L][d], attention output [L][d],
+ * LN1 output [L][d], hidden [L][d_ff] (N (3d + d_ff) L bytes in all).  With force (same layout,
+ * may be NULL): a code whose fp64 value x 127 / alpha lies within margin of a rounding tie takes
+ * force's code when that is one of the tie's two neighbours; stats[0] counts codes so taken that
+ * differ from the fp64 decision, stats[1] codes of force that differ from it elsewhere. */
+int oracle_decode_ref64_word(const oracle_model *M, const float *y, uint8_t *bits, double *f,
+                             int8_t *codes, const int8_t *force, double margin, int64_t *stats);
 /* AAP weight import (Section 4.1, Eq. 1): gamma = p-quantile of |w| (linear interpolation,
  * double, rounded to fp32), *scale = fp32(gamma * delta), t = RoundClip(w / fp32(scale + eps)).
  * Returns 0, or -1 for invalid arguments. */

@@ -11,11 +11,12 @@ from workloads.channel import awgn_words
 from workloads.codes import generator_from_parity
 
 
+@pytest.mark.parametrize("act_scale", ["token", "word"])
 @pytest.mark.parametrize("c", [1, 2, 3])
-def test_codeword_invariance(oracle_mod, c):
+def test_codeword_invariance(oracle_mod, c, act_scale):
     """h(y) depends only on |y| and the syndrome (Section 3), so decoding x_s + e and 1 + x_s e
     gives the same noise estimate bit for bit and bits that differ exactly by the codeword."""
-    cfg, H, G, w, y, x = build_workload(c, batch=64 if c < 3 else 4)
+    cfg, H, G, w, y, x = build_workload(c, batch=64 if c < 3 else 4, act_scale=act_scale)
     om = oracle_mod.OracleModel(H, w)
     xs = (1 - 2 * x.astype(np.int8)).astype(np.float32)
     y0 = (xs * y).astype(np.float32)                    # exact: multiplying by +-1
@@ -54,36 +55,88 @@ def test_zero_weight_closed_form(oracle_mod):
         assert np.abs(f[bi] - fr).max() <= 2e-5
 
 
+# Agreement of the canonical fp32 decode with the plain fp64 definition (dense masked softmax,
+# libm exp, exact division and square root).  The two take the same int8 decisions except where
+# an activation lies so close to a rounding tie k + 1/2 of Eq. 2 that fp32 and fp64 rounding both
+# decide it legitimately; such a flip changes a code by one step and can move a logit by ~1e-2.
+FLIP_FREE_TOL = 1e-5      # |f32 - f64| of a word whose every code equals the fp64 decision
+TIE_MARGIN = 1e-3         # |x 127 / alpha - (k + 1/2)| within which the canonical code is taken
+
+
+def _flips(t, codes):
+    return sum(int((t[k] != codes[k]).sum()) for k in ("xq", "oq", "x1q", "gq"))
+
+
 @pytest.mark.parametrize("attention", ["hpsa", "casa"])
-def test_fp32_canonical_close_to_fp64_reference(oracle_mod, attention):
-    """The canonical fp32 decode against the oracle's fp64 dense mode on Hamming(7,4), with the
-    head-partitioned masks and with the ECCT mask on every head.  Differences come only from fp32
-    rounding and the rare int8 code that sits on a rounding boundary; most words agree to ~1e-6."""
-    cfg, H, G, w, y, x = build_workload(1, batch=1024, attention=attention)
+@pytest.mark.parametrize("c,words", [(1, 1024), (2, 128)])
+def test_fp32_canonical_close_to_fp64_reference(oracle_mod, c, words, attention):
+    """The canonical fp32 decode against the oracle's fp64 dense mode, with the head-partitioned
+    masks and with the ECCT mask on every head.  Words whose int8 codes all equal the fp64 mode's
+    agree within 1e-5 on every logit and in every bit; words with a flipped code are counted."""
+    cfg, H, G, w, y, x = build_workload(c, batch=words, attention=attention)
     om = oracle_mod.OracleModel(H, w)
-    bits, f = om.decode(y, n_threads=8)
-    bits64, f64 = om.decode_ref64(y, n_threads=8)
-    err = np.abs(f - f64).max(1)
-    assert np.median(err) < 2e-6
-    assert (err <= 1e-4).mean() >= 0.97
-    assert err.max() < 0.05
-    sure = np.abs(f64) > 0.05
-    assert (bits[sure] == bits64[sure]).all()
+    n_flip, err_free = 0, 0.0
+    for b in range(words):
+        bits, f, t = om.decode_taps(y[b])
+        b64, f64, c64, _ = om.decode_ref64_word(y[b])
+        if _flips(t, c64):
+            n_flip += 1
+            continue
+        err_free = max(err_free, float(np.abs(f.astype(np.float64) - f64).max()))
+        assert (bits == b64).all()
+    print(f"config {c} {attention}: {n_flip} of {words} words with an int8 flip, flip-free max |df| {err_free:.2e}")
+    assert err_free <= FLIP_FREE_TOL
+    assert n_flip <= words // 2                 # the rule is not vacuous
 
 
-def _q64(x):
+@pytest.mark.parametrize("c,words,act_scale", [(1, 256, "token"), (1, 256, "word"), (2, 48, "token"),
+                                               (2, 48, "word"), (3, 4, "token"), (3, 4, "word"),
+                                               (4, 1, "token"), (5, 1, "token")])
+def test_canonical_equals_fp64_up_to_near_tie_codes(oracle_mod, c, words, act_scale):
+    """Survey pin P10 on every workload.  The fp64 reference decode, taking the canonical code
+    only where its own value lies within 1e-3 of a rounding tie, reproduces the canonical logits
+    within 1e-5: no canonical code differs from the fp64 decision away from a tie, so every
+    departure of the canonical fp32 order from the plain definition (folded score scale, base-2
+    softmax without shift, polynomial 2^x, Newton rsqrt, split 16-dimension dot products) stays
+    at fp32 rounding size through all N layers."""
+    from concurrent.futures import ThreadPoolExecutor
+    cfg, H, G, w, y, x = build_workload(c, batch=words, act_scale=act_scale)
+    om = oracle_mod.OracleModel(H, w)
+
+    def one(b):
+        bits, f, t = om.decode_taps(y[b])
+        b64, f64, c64, (tied, missed) = om.decode_ref64_word(y[b], force=t, margin=TIE_MARGIN)
+        err = float(np.abs(f.astype(np.float64) - f64).max())
+        sure = np.abs(f64) > 1e-3
+        return tied, missed, err, bool((bits[sure] == b64[sure]).all())
+
+    with ThreadPoolExecutor(8) as ex:
+        res = list(ex.map(one, range(words)))
+    tied = sum(r[0] for r in res)
+    print(f"config {c} alpha per {act_scale}: {tied} near-tie codes over {words} words, "
+          f"max |df| {max(r[2] for r in res):.2e}")
+    assert sum(r[1] for r in res) == 0
+    assert max(r[2] for r in res) <= FLIP_FREE_TOL
+    assert all(r[3] for r in res)
+
+
+def _q64(x, per_word=False):
     a = np.abs(x).max(1, keepdims=True)
+    if per_word:
+        a = np.full_like(a, np.abs(x).max())
     return np.clip(np.rint(x * (127.0 / np.where(a == 0, 1, a))), -127, 127), a[:, 0]
 
 
-@pytest.mark.parametrize("c", [1, 2, 3])
-def test_taps_stagewise_against_fp64(oracle_mod, c):
+@pytest.mark.parametrize("c,act_scale", [(1, "token"), (2, "token"), (3, "token"), (4, "token"), (5, "token"),
+                                         (2, "word"), (3, "word")])
+def test_taps_stagewise_against_fp64(oracle_mod, c, act_scale):
     """Every stage of the fp32 decode, fed the oracle's own int8 codes at each quantisation point,
     recomputed in fp64 with numpy/torch: QKV projections, HPSA attention, O projection + LN1,
     FFN + LN2 and the head all agree to fp32 rounding, and the int8 codes themselves differ from
     the fp64 rounding decision by at most one step on a rounding tie."""
     from test_oracle_units import _sdpa_reference
-    cfg, H, G, w, y, x = build_workload(c, batch=2)
+    cfg, H, G, w, y, x = build_workload(c, batch=2, act_scale=act_scale)
+    pw = act_scale == "word"
     om = oracle_mod.OracleModel(H, w)
     bits, f, t = om.decode_taps(y[1])
     d = w.d
@@ -101,7 +154,7 @@ def test_taps_stagewise_against_fp64(oracle_mod, c):
     flips = 0
     for l in range(w.n_layers):
         sc = w.scale[l]
-        q64, a64 = _q64(t["x_in"][l].astype(np.float64))
+        q64, a64 = _q64(t["x_in"][l].astype(np.float64), pw)
         flips += int((q64 != t["xq"][l]).sum())
         assert np.abs(q64 - t["xq"][l]).max() <= 1
         assert (a64 == t["ax"][l]).all()
@@ -110,7 +163,7 @@ def test_taps_stagewise_against_fp64(oracle_mod, c):
         qkv[:, :d] *= math.log2(math.e) / math.sqrt(d // w.heads)      # scaled queries
         close(t["qkv"][l], qkv, 1e-6)
         close(t["o"][l], _sdpa_reference(H, w, t["qkv"][l]), 2e-6)
-        q64, a64 = _q64(t["o"][l].astype(np.float64))
+        q64, a64 = _q64(t["o"][l].astype(np.float64), pw)
         flips += int((q64 != t["oq"][l]).sum())
         assert np.abs(q64 - t["oq"][l]).max() <= 1
         assert (t["acc_o"][l] == t["oq"][l].astype(np.int64) @ w.w["o"][l].astype(np.int64)).all()
@@ -118,7 +171,7 @@ def test_taps_stagewise_against_fp64(oracle_mod, c):
                 w.ln1_g[l], w.ln1_b[l])
         close(t["x1"][l], x1, 1e-5)
         F = np.maximum(lin(t["x1q"][l], t["a1"][l], w.w["ff1"][l], sc[4], w.b["ff1"][l]), 0)
-        q64, a64 = _q64(F)
+        q64, a64 = _q64(F, pw)
         flips += int((q64 != t["gq"][l]).sum())
         assert np.abs(q64 - t["gq"][l]).max() <= 1
         close(t["ag"][l], a64, 1e-6)

@@ -130,6 +130,41 @@ def test_quant_zero_row_and_half_even(oracle_mod):
     assert q[0].tolist() == [127, 2, 4, -2, 0, 0, 2, -126]
 
 
+def test_quant_word_alpha_and_invariants(oracle_mod):
+    """Eq. 2 with one alpha per word (the reading of Section 4.1 that takes alpha = ||x||_inf over
+    the whole layer input): alpha is the library maximum of |x| over every row, all rows share it,
+    the codes keep the invariants of Eq. 2 with that alpha, and a one-row word or a word whose
+    rows share one maximum is quantised exactly as the per-token form."""
+    rng = np.random.default_rng(13)
+    x = (rng.standard_normal((46, 128)) * rng.exponential(1, (46, 1))).astype(np.float32)
+    q, r = oracle_mod.quant_word(x)
+    a = np.abs(x).max()
+    assert (r == a).all()
+    assert (np.abs(q.astype(int)) <= 127).all()
+    i, j = np.unravel_index(np.abs(x).argmax(), x.shape)
+    assert abs(int(q[i, j])) == 127
+    assert ((np.sign(q) == np.sign(x)) | (q == 0)).all()
+    o = np.argsort(x.reshape(-1), kind="stable")
+    assert (np.diff(q.reshape(-1)[o].astype(int)) >= 0).all()            # monotone over the word
+    err = np.abs(x.astype(np.float64) - q * float(a) / 127)
+    assert (err <= float(a) / 254 * (1 + 2 ** -20)).all()
+    # rows of a smaller maximum use fewer code levels than their own per-token quantisation
+    qt, rt = oracle_mod.quant_rows(x)
+    small = rt < a
+    assert (np.abs(q[small]).max(1) <= np.abs(qt[small]).max(1)).all()
+    # special cases that reduce to the per-token form
+    q1, r1 = oracle_mod.quant_word(x[:1])
+    qt1, rt1 = oracle_mod.quant_rows(x[:1])
+    assert (q1 == qt1).all() and (r1 == rt1).all()
+    xs = x / np.abs(x).max(1, keepdims=True) * np.float32(3.0)             # every row's max is 3
+    xs[np.arange(46), np.abs(xs).argmax(1)] = np.float32(3.0)
+    qa, ra = oracle_mod.quant_word(xs)
+    qb, rb = oracle_mod.quant_rows(xs)
+    assert (qa == qb).all() and (ra == rb).all()
+    qz, rz = oracle_mod.quant_word(np.zeros((3, 8), np.float32))
+    assert (qz == 0).all() and (rz == 0).all()
+
+
 # ------------------------------------------------------------------------ AAPLinear (Eq. 3)
 def test_linear_accumulators_and_dequant(oracle_mod):
     rng = np.random.default_rng(4)
@@ -171,7 +206,8 @@ def _sdpa_reference(H, w, qkv, scale=math.log(2.0)):
     A[:n, n:] = H.T
     A[n:, :n] = H
     M1 = torch.tensor(A != 0)
-    M2 = torch.tensor((A @ A) != 0)
+    Af = A.astype(np.float64)                   # exact small integers; BLAS instead of an int64 loop
+    M2 = torch.tensor((Af @ Af) != 0)
     d, h = w.d, w.heads
     dh = d // h
     t = torch.tensor(qkv, dtype=torch.float64)
@@ -190,12 +226,16 @@ def _sdpa_reference(H, w, qkv, scale=math.log(2.0)):
 
 
 @pytest.mark.parametrize("attention", ["hpsa", "casa"])
-@pytest.mark.parametrize("c", [1, 2, 3])
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
 def test_attention_against_fp64_sdpa(oracle_mod, c, attention):
+    """Every workload's head width: d_h = 4 (Hamming, BCH), 8 (LDPC(128,64)) and 16 (the two
+    d = 128 LDPC codes, whose dot products the canonical order splits into two 8-term halves)."""
     cfg, H, G, w, y, x = build_workload(c, batch=1, attention=attention)
     om = oracle_mod.OracleModel(H, w)
     rng = np.random.default_rng(6)
-    qkv = (rng.standard_normal((om.L, 3 * w.d)) * 2).astype(np.float32)
+    qkv = rng.standard_normal((om.L, 3 * w.d)) * 2
+    qkv[:, :w.d] *= math.sqrt(4 / (w.d // w.heads))    # the same score spread for every head width
+    qkv = qkv.astype(np.float32)
     o = om.attention(qkv)
     ref = _sdpa_reference(H, w, qkv)
     assert np.abs(o - ref).max() <= 1e-6 * max(1.0, np.abs(ref).max())
@@ -203,25 +243,46 @@ def test_attention_against_fp64_sdpa(oracle_mod, c, attention):
     assert np.abs(o64 - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max())
 
 
+@pytest.mark.parametrize("attention", ["hpsa", "casa"])
+@pytest.mark.parametrize("c", [2, 4, 5])
 @pytest.mark.parametrize("regime", ["overflow", "underflow", "mixed"])
-def test_attention_shifted_fallback_against_fp64_sdpa(oracle_mod, regime):
+def test_attention_shifted_fallback_against_fp64_sdpa(oracle_mod, regime, c, attention):
     """Rows whose unshifted weight sum leaves [2^-64, 2^64] take the max-shifted form: scores of
-    a few hundred overflow 2^s, scores below -125 would all clamp to the same weight."""
-    cfg, H, G, w, y, x = build_workload(2, batch=1)
+    a few hundred overflow 2^s, scores below -125 would all clamp to the same weight; on d_h = 4
+    (BCH) and d_h = 16 (the d = 128 LDPC codes)."""
+    cfg, H, G, w, y, x = build_workload(c, batch=1, attention=attention)
     om = oracle_mod.OracleModel(H, w)
     rng = np.random.default_rng(9)
     qkv = rng.standard_normal((om.L, 3 * w.d))
     d = w.d
+    dh = d // w.heads
+    # Scores of about 150-200 (base-2 units) for every head width: far outside the unshifted
+    # range [2^-64, 2^64] of the weight sums, and of the same size at d_h = 4, 8 and 16 (fp32
+    # rounding of a score grows like d_h |s|).  Random products add up like sqrt(d_h), the
+    # same-sign products of the underflow rows like d_h.
+    over = 20.0 * math.sqrt(4 / dh)
     if regime == "overflow":
-        qkv[:, :d] *= 40.0
+        qkv[:, :d] *= over
     elif regime == "underflow":
-        qkv[:, :d] = np.abs(qkv[:, :d]) * 20.0 + 5.0
+        qkv[:, :d] = (np.abs(qkv[:, :d]) * 4.0 + 8.0) * (4 / dh)
         qkv[:, d:2 * d] = -np.abs(qkv[:, d:2 * d]) - 4.0
-    else:                                   # half the tokens in each regime, the rest plain
-        qkv[::3, :d] *= 40.0
-        qkv[1::3, :d] = np.abs(qkv[1::3, :d]) * 20.0 + 5.0
+    else:                                   # a third of the tokens in each regime
+        qkv[::3, :d] *= over
+        qkv[1::3, :d] = (np.abs(qkv[1::3, :d]) * 4.0 + 8.0) * (4 / dh)
         qkv[1::3, d:2 * d] = -np.abs(qkv[1::3, d:2 * d]) - 4.0
     qkv = qkv.astype(np.float32)
+    # share of (row, head) pairs whose unshifted weight sum sum_j 2^s_j leaves [2^-64, 2^64]
+    M1, M2 = oracle_mod.masks(H)
+    q64, k64 = qkv[:, :d].astype(np.float64), qkv[:, d:2 * d].astype(np.float64)
+    out_of_range = []
+    for hh in range(w.heads):
+        sl = slice(hh * dh, (hh + 1) * dh)
+        mask = (M1 | M2) if attention == "casa" else (M1 if hh < w.first_ring_heads else M2)
+        sc = np.where(mask.astype(bool), q64[:, sl] @ k64[:, sl].T, -np.inf)
+        S2 = np.log2(np.exp2(sc - sc.max(1, keepdims=True)).sum(1)) + sc.max(1)
+        out_of_range.append((S2 > 64) | (S2 < -64))
+    share = np.mean(out_of_range)
+    assert share >= {"overflow": 0.3, "underflow": 1.0, "mixed": 0.15}[regime], share
     o = om.attention(qkv)
     ref = _sdpa_reference(H, w, qkv)
     assert np.isfinite(o).all()

@@ -57,16 +57,17 @@ def parity_check(cfg: WorkloadConfig) -> np.ndarray:
 
 
 def build_workload(index: int, batch: int | None = None, *, data_seed: int | None = None,
-                   attention: str = "hpsa", first_ring_heads: int | None = None):
+                   attention: str = "hpsa", first_ring_heads: int | None = None, act_scale: str = "token"):
     """(cfg, H, G, weights, y, x) for workload `index`; `batch` overrides the configured batch,
     `attention` picks the head-partitioned ("hpsa") or all-heads-ECCT-mask ("casa") model,
-    `first_ring_heads` the number h_f of heads on the first-ring mask (default heads / 2)."""
+    `first_ring_heads` the number h_f of heads on the first-ring mask (default heads / 2),
+    `act_scale` the Eq. 2 scale granularity ("token" or "word")."""
     cfg = CONFIGS[index]
     H = parity_check(cfg)
     G = generator_from_parity(H)
     m, n = H.shape
     w = random_weights(n, m, cfg.d, cfg.n_layers, cfg.heads, p_zero=cfg.p_zero, seed=cfg.seeds[1],
-                       attention=attention, first_ring_heads=first_ring_heads)
+                       attention=attention, first_ring_heads=first_ring_heads, act_scale=act_scale)
     B = cfg.batch if batch is None else batch
     y, x, _ = awgn_words(G, B, cfg.ebn0, seed=cfg.seeds[2] if data_seed is None else data_seed)
     return cfg, H, G, w, y, x

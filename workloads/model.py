@@ -43,6 +43,7 @@ class ModelWeights:
     head_bo: np.ndarray    # [n]
     extra: dict = field(default_factory=dict)
     attention: str = "hpsa"   # "hpsa": heads split over the two rings; "casa": every head over both
+    act_scale: str = "token"  # Eq. 2 scale alpha per "token" (row) or per "word" (all of its tokens)
 
     @property
     def L(self) -> int:
@@ -59,7 +60,7 @@ class ModelWeights:
 def random_weights(n: int, m: int, d: int, n_layers: int, heads: int = 8, *, p_zero: float = 0.5,
                    seed: int = 0, first_ring_heads: int | None = None, d_ff: int | None = None,
                    ln_eps: float = 1e-5, with_pos: bool = False, zero_linear: bool = False,
-                   attention: str = "hpsa") -> ModelWeights:
+                   attention: str = "hpsa", act_scale: str = "token") -> ModelWeights:
     """Draw a model.  Ternary entries are i.i.d. with P(0) = p_zero, P(+1) = P(-1) = (1-p_zero)/2,
     every weight scale is fp32(1/sqrt(d)), embeddings are N(0,1), biases and LayerNorm offsets
     N(0, 0.1^2), LayerNorm gains 1 + N(0, 0.1^2), W_{d->1} ~ N(0, 1/d), W_o ~ N(0, 1/L).
@@ -93,7 +94,7 @@ def random_weights(n: int, m: int, d: int, n_layers: int, heads: int = 8, *, p_z
                         ln_eps=ln_eps, embed=embed, pos=pos, w=w, scale=scale, b=b,
                         ln1_g=ln1_g, ln1_b=ln1_b, ln2_g=ln2_g, ln2_b=ln2_b,
                         head_w1=head_w1, head_b1=head_b1, head_wo=head_wo, head_bo=head_bo,
-                        attention=attention)
+                        attention=attention, act_scale=act_scale)
 
 
 def random_spe_params(L: int, d_pe: int, heads: int, *, seed: int = 0) -> dict:
