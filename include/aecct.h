@@ -104,6 +104,7 @@ typedef enum aecct_attention {
 /* How the layered path computes a layer's queries, keys, values (Eq. 3) and attention
    (Section 4.2); every form gives the same results bit for bit. */
 typedef enum aecct_layered_attention {
+  AECCT_LAYERED_ATTN_AUTO = -1,    /* the fastest form the shape allows (the default) */
   AECCT_LAYERED_ATTN_UNFUSED = 0,  /* ternary GEMM to Q, K, V in device memory, then attention */
   AECCT_LAYERED_ATTN_LDS_F32 = 1,  /* fused per word and 16-dimension head group, K and V in
                                       LDS as fp32 (d = 64, 128, short words) */
@@ -112,12 +113,28 @@ typedef enum aecct_layered_attention {
                                       scales, the rest as fp32 (d = 64, 128, longer words) */
 } aecct_layered_attention;
 
+/* Granularity of the Eq. 2 activation scale alpha = ||x||_inf (Section 4.1).  The paper calls
+   every scaling factor a scalar and leaves open over which part of a layer input x it is taken. */
+typedef enum aecct_act_scale {
+  AECCT_ACT_SCALE_TOKEN = 0,  /* one alpha per token row of x (the default) */
+  AECCT_ACT_SCALE_WORD = 1    /* one alpha per received word: the maximum over all of its tokens'
+                                 features at that quantisation point (every word of a batch keeps
+                                 its own, so words stay independent) */
+} aecct_act_scale;
+
+/* Every field is read; -1 selects the default where a field allows it.  A NULL options pointer
+   is the same as { -1, -1, 0, AUTO, HPSA, AUTO, TOKEN }. */
 typedef struct aecct_options {
-  int32_t first_ring_heads;  /* h_f, 0..heads; -1 = heads / 2 (the paper's default split) */
-  int32_t d_ff;              /* feed-forward width; -1 = 4 d */
-  float ln_eps;              /* LayerNorm epsilon; <= 0 = 1e-5 */
-  int32_t path;              /* aecct_path */
-  int32_t attention;         /* aecct_attention */
+  int32_t first_ring_heads;   /* h_f, 0..heads; -1 = heads / 2 (the paper's default split) */
+  int32_t d_ff;               /* feed-forward width; -1 = 4 d */
+  float ln_eps;               /* LayerNorm epsilon; <= 0 = 1e-5 */
+  int32_t path;               /* aecct_path */
+  int32_t attention;          /* aecct_attention */
+  int32_t layered_attention;  /* aecct_layered_attention (the layered path's form); a form the
+                                 shape does not allow gives AECCT_ERR_UNSUPPORTED */
+  int32_t act_scale_mode;     /* aecct_act_scale.  WORD runs on the layered path in its unfused
+                                 form with natural activation layouts (path AUTO resolves to it;
+                                 FUSED or a fused layered form gives AECCT_ERR_UNSUPPORTED) */
 } aecct_options;
 
 typedef struct aecct_model aecct_model;   /* opaque */
@@ -131,9 +148,11 @@ typedef struct aecct_model aecct_model;   /* opaque */
  *   opt  may be NULL (defaults).
  * Supported shapes: d in {32, 64, 128}, d / heads in {4, 8, 16}, d_ff = 4 d,
  * n + m <= 4096; anything else valid returns AECCT_ERR_UNSUPPORTED.
- * All arguments are validated before any HIP call.  On success *out owns
- * device memory until aecct_destroy.  Errors: INVALID_ARG, UNSUPPORTED,
- * OUT_OF_MEMORY, DEVICE (no GPU, or a HIP allocation or copy failed).
+ * All arguments are validated before any HIP call.  The model's tables are sized
+ * for the current device's compute units and LDS per workgroup, and the kernels'
+ * launch limits are set for it.  On success *out owns device memory until
+ * aecct_destroy.  Errors: INVALID_ARG, UNSUPPORTED, OUT_OF_MEMORY, DEVICE (no
+ * GPU, or a HIP allocation, copy or attribute call failed).
  */
 aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_weights *w, int32_t d,
                           int32_t n_layers, int32_t heads, const aecct_options *opt, aecct_model **out);
@@ -243,8 +262,13 @@ typedef struct aecct_model_info {
   int64_t nnz_second_ring;   /* same for the second-ring mask (diagonal included) */
   size_t device_bytes;       /* device memory held by the model */
   int32_t attention;         /* aecct_attention (first_ring_heads reads 0 under CASA) */
-  int32_t layered_attention; /* aecct_layered_attention: how the layered path runs a layer's
-                                projection and attention (reported whatever path resolved) */
+  int32_t layered_attention; /* resolved aecct_layered_attention (never AUTO): how the layered
+                                path runs a layer's projection and attention (reported whatever
+                                path resolved) */
+  int32_t act_scale_mode;    /* aecct_act_scale */
+  int32_t device;            /* HIP device the model lives on */
+  int32_t compute_units;     /* its compute units, and the LDS bytes one workgroup may use on it: */
+  int64_t lds_bytes;         /* the persistent grids and LDS layouts are sized from these */
 } aecct_model_info;
 aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info);
 
@@ -261,8 +285,10 @@ aecct_status aecct_workspace_size(const aecct_model *model, int64_t batch, size_
  *   logits     device fp32 [batch][n] noise estimate f = f_theta(h(y)), or NULL;
  *   workspace  device scratch of at least aecct_workspace_size bytes (may be
  *              NULL when that size is 0); 256-byte aligned.
- * batch == 0 is a no-op.  Non-finite y is not checked.  Errors: INVALID_ARG,
- * WORKSPACE_TOO_SMALL, DEVICE (launch failure reported by HIP).
+ * batch == 0 is a no-op.  Non-finite y is not checked.  The current HIP device
+ * must be the one the model was created on.  Errors: INVALID_ARG (also for
+ * another current device), WORKSPACE_TOO_SMALL, DEVICE (launch failure
+ * reported by HIP).
  */
 aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits,
                           float *logits, void *workspace, size_t workspace_bytes, void *stream);
@@ -294,7 +320,10 @@ const char *aecct_status_string(aecct_status status);
  * aecct_decode(path = LAYERED) is exactly embed, then per layer qkv ->
  * attention -> oproj_ln -> ffn1 -> ffn2_ln, then head.  They let a caller run, time or
  * check one step on inputs of its choice.  Layout of every activation: row r
- * of word b at index b * L + r, features contiguous.  Errors: INVALID_ARG.
+ * of word b at index b * L + r, features contiguous.  The current device must be
+ * the model's.  Errors: INVALID_ARG; UNSUPPORTED from the steps that quantise
+ * (embed, attention, oproj_ln, ffn1, ffn2_ln) on a model with one alpha per
+ * word, where a row's codes depend on the whole word.
  * ---------------------------------------------------------------------------------------- */
 
 /* Section 3 pre-processing + embedding + Eq. 2 quantisation of layer 0's input.

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libaecct.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_WORKSPACE_TOO_SMALL = range(6)
 PATH_AUTO, PATH_LAYERED, PATH_FUSED = 0, 1, 2
 ATTN_HPSA, ATTN_CASA = 0, 1
-LAYERED_ATTN_UNFUSED, LAYERED_ATTN_LDS_F32, LAYERED_ATTN_LDS_I16 = 0, 1, 2
+LAYERED_ATTN_AUTO, LAYERED_ATTN_UNFUSED, LAYERED_ATTN_LDS_F32, LAYERED_ATTN_LDS_I16 = -1, 0, 1, 2
+ACT_SCALE_TOKEN, ACT_SCALE_WORD = 0, 1
 LIN_Q, LIN_K, LIN_V, LIN_O, LIN_FF1, LIN_FF2 = range(6)
 
 _vp = C.c_void_p
@@ -36,14 +37,15 @@ class Weights(C.Structure):
 
 class Options(C.Structure):
     _fields_ = [("first_ring_heads", C.c_int32), ("d_ff", C.c_int32), ("ln_eps", C.c_float), ("path", C.c_int32),
-                ("attention", C.c_int32), ("layered_attention", C.c_int32)]
+                ("attention", C.c_int32), ("layered_attention", C.c_int32), ("act_scale_mode", C.c_int32)]
 
 
 class ModelInfo(C.Structure):
     _fields_ = [("n", C.c_int32), ("m", C.c_int32), ("L", C.c_int32), ("d", C.c_int32), ("n_layers", C.c_int32),
                 ("heads", C.c_int32), ("first_ring_heads", C.c_int32), ("d_ff", C.c_int32), ("path", C.c_int32),
                 ("nnz_first_ring", C.c_int64), ("nnz_second_ring", C.c_int64), ("device_bytes", C.c_size_t),
-                ("attention", C.c_int32), ("layered_attention", C.c_int32)]
+                ("attention", C.c_int32), ("layered_attention", C.c_int32), ("act_scale_mode", C.c_int32),
+                ("device", C.c_int32), ("compute_units", C.c_int32), ("lds_bytes", C.c_int64)]
 
 
 class SpeParams(C.Structure):
@@ -217,10 +219,12 @@ class Decoder:
 
     `H` is the (n-k) x n parity-check matrix (0/1) and `w` carries the model parameters
     with the attribute names of `workloads.ModelWeights` (embed, pos, w[kind], b[kind], scale,
-    ln1_g, ..., head_wo, head_bo, and optionally attention = "hpsa" | "casa").
+    ln1_g, ..., head_wo, head_bo, and optionally attention = "hpsa" | "casa" and
+    act_scale = "token" | "word").  `path` and `layered_attention` choose the kernels
+    (aecct_path, aecct_layered_attention; -1 = automatic).
     """
 
-    def __init__(self, H, w, path: int = PATH_AUTO):
+    def __init__(self, H, w, path: int = PATH_AUTO, layered_attention: int = LAYERED_ATTN_AUTO):
         H = _host(H, np.uint8)
         m, n = H.shape
         self._keep = [H]
@@ -246,7 +250,9 @@ class Decoder:
         st.head_w1, st.head_b1 = f32(w.head_w1), float(np.float32(w.head_b1))
         st.head_wo, st.head_bo = f32(w.head_wo), f32(w.head_bo)
         attention = {"hpsa": ATTN_HPSA, "casa": ATTN_CASA}[getattr(w, "attention", "hpsa")]
-        opt = Options(int(w.first_ring_heads), int(w.d_ff), float(w.ln_eps), int(path), attention)
+        act = {"token": ACT_SCALE_TOKEN, "word": ACT_SCALE_WORD}[getattr(w, "act_scale", "token")]
+        opt = Options(int(w.first_ring_heads), int(w.d_ff), float(w.ln_eps), int(path), attention,
+                      int(layered_attention), act)
         h = _vp()
         _check(lib().aecct_create(H.ctypes.data_as(_u8p), m, n, C.byref(st), int(w.d), int(w.n_layers),
                                   int(w.heads), C.byref(opt), C.byref(h)), "aecct_create")

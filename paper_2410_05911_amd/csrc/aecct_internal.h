@@ -23,7 +23,7 @@ constexpr int V_BQKV = 0, V_BO = 96, V_BFF1 = 128, V_BFF2 = 256, V_LN1G = 288, V
 // wavefronts (words in flight) per block: 12 of 168 registers each fill the register file; blocks
 // of 8 or 10 waves were measured 18 % slower on BCH(31,16)
 constexpr int kWaves = 12;
-constexpr int kLdsMax = 160 * 1024;
+constexpr int kLdsMax = 160 * 1024;   // the kernel's design limit: gfx950's LDS per workgroup
 }  // namespace fz
 
 // Packed ternary weights of one layer: for every linear map, 16x32 MFMA B-operand
@@ -70,7 +70,11 @@ struct Model {
   float kq;              // fp32(log2(e) / sqrt(d_h)): score scale folded into the query map
   int path;              // resolved aecct_path
   int attention;         // aecct_attention; under CASA the second-ring lists hold the union, hf = 0
-  int device;
+  int lattn;             // resolved aecct_layered_attention: the layered decode's Q/K/V + attention form
+  int act_word;          // 1: Eq. 2 takes one alpha per word (aecct_act_scale WORD), else per token
+  int device;            // HIP device the model's memory lives on
+  int cu_count;          // compute units of that device (persistent grids)
+  size_t lds_max;        // LDS bytes one workgroup may use on it
   int64_t nnz1, nnz2;
   size_t device_bytes;
   void *dev_block;       // single device allocation holding everything below
@@ -136,6 +140,16 @@ hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t w
                        float *logits, bool lane_order, hipStream_t s);
 hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a, int64_t rows, int32_t *acc,
                                hipStream_t s);
+// Eq. 2 with one alpha per word over x [words][L][K] fp32 (of max(x, 0) when relu), natural
+// layout: codes q [words][L][K], a[row] = the word's alpha for each of its L rows.
+hipError_t launch_word_quant(const Model &M, const float *x, int64_t words, int K, bool relu, int8_t *q, float *a,
+                             hipStream_t s);
+// First feed-forward map (Eq. 3) to fp32, before the ReLU: h [rows][d_ff].
+hipError_t launch_ffn1_f32(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, float *h,
+                           hipStream_t s);
+// Dynamic-LDS limits of the kernels, set for the current device at create time.
+hipError_t set_layered_kernel_attributes(const Model &M);
+hipError_t set_fused_kernel_attributes(const Model &M);
 // ---- fused path (kernel_fused.hip) -----------------------------------------------------
 bool fused_supported(const Model &M);                 // shape check
 bool fused_fits(const Model &M, int nbr_words);       // LDS check with the built neighbour table

@@ -119,7 +119,9 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
 
 // Layered-path workspace for `words` words: region offsets.
 struct WsPlan {
-  size_t x, xq, ax, qkv, oq, ao, x1, x1q, a1, gq, ag, total;
+  size_t x, xq, ax, qkv, oq, ao, x1, x1q, a1, gq, ag;
+  size_t o32, h32;   // fp32 attention output and hidden row (one alpha per word only), or 0
+  size_t total;
 };
 
 WsPlan ws_plan(const Model &M, int64_t words) {
@@ -138,6 +140,10 @@ WsPlan ws_plan(const Model &M, int64_t words) {
   w.a1 = take(4 * R);
   w.gq = take(R * dff);
   w.ag = take(4 * R);
+  if (M.act_word) {
+    w.o32 = take(4 * R * d);
+    w.h32 = take(4 * R * dff);
+  }
   w.total = off;
   return w;
 }
@@ -515,6 +521,22 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
   }
 }
 
+// The layered decode's projection + attention form: the requested one if the shape allows it, or
+// (AUTO) fused with fp32 keys and values in LDS when they fit, else (with the token block, which
+// takes O in fp32) with int16 accumulators, else the separate GEMM and attention kernels; the
+// unfused form with one alpha per word.  -1 if the requested form does not fit the shape.
+int32_t resolve_layered_attention(const Model &M, int requested) {
+  const bool f32 = aecct::qkv_attention_supported(M);
+  const bool i16 = aecct::token_block_supported(M) && aecct::qkv_attention_i16_supported(M);
+  switch (requested) {
+    case AECCT_LAYERED_ATTN_UNFUSED: return AECCT_LAYERED_ATTN_UNFUSED;
+    case AECCT_LAYERED_ATTN_LDS_F32: return f32 && !M.act_word ? AECCT_LAYERED_ATTN_LDS_F32 : -1;
+    case AECCT_LAYERED_ATTN_LDS_I16: return i16 && !M.act_word ? AECCT_LAYERED_ATTN_LDS_I16 : -1;
+  }
+  if (M.act_word) return AECCT_LAYERED_ATTN_UNFUSED;
+  return f32 ? AECCT_LAYERED_ATTN_LDS_F32 : (i16 ? AECCT_LAYERED_ATTN_LDS_I16 : AECCT_LAYERED_ATTN_UNFUSED);
+}
+
 aecct_status from_hip(hipError_t e) {
   if (e == hipSuccess) return AECCT_OK;
   return e == hipErrorOutOfMemory ? AECCT_ERR_OUT_OF_MEMORY : AECCT_ERR_DEVICE;
@@ -552,6 +574,10 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   if (path_req < AECCT_PATH_AUTO || path_req > AECCT_PATH_FUSED) return AECCT_ERR_INVALID_ARG;
   const int attention = opt ? opt->attention : AECCT_ATTN_HPSA;
   if (attention != AECCT_ATTN_HPSA && attention != AECCT_ATTN_CASA) return AECCT_ERR_INVALID_ARG;
+  const int lattn_req = opt ? opt->layered_attention : AECCT_LAYERED_ATTN_AUTO;
+  if (lattn_req < AECCT_LAYERED_ATTN_AUTO || lattn_req > AECCT_LAYERED_ATTN_LDS_I16) return AECCT_ERR_INVALID_ARG;
+  const int act_mode = opt ? opt->act_scale_mode : AECCT_ACT_SCALE_TOKEN;
+  if (act_mode != AECCT_ACT_SCALE_TOKEN && act_mode != AECCT_ACT_SCALE_WORD) return AECCT_ERR_INVALID_ARG;
   const int64_t L64 = (int64_t)n + m;
   if (L64 > (1 << 20)) return AECCT_ERR_UNSUPPORTED;
   const int L = (int)L64;
@@ -589,6 +615,10 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   const int dh = d / heads;
   if (!(d == 32 || d == 64 || d == 128) || !(dh == 4 || dh == 8 || dh == 16) || dff != 4 * d || L > 4096 ||
       n_layers > aecct::kMaxLayers)
+    return AECCT_ERR_UNSUPPORTED;
+  // one alpha per word: the unfused layered form with natural layouts only
+  if (act_mode == AECCT_ACT_SCALE_WORD &&
+      (path_req == AECCT_PATH_FUSED || lattn_req == AECCT_LAYERED_ATTN_LDS_F32 || lattn_req == AECCT_LAYERED_ATTN_LDS_I16))
     return AECCT_ERR_UNSUPPORTED;
 
   // Tanner graph lists and HPSA masks (Section 4.2): M1 = neighbours, M2 = nodes two
@@ -645,10 +675,25 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     M.layer[l].sq_qs = M.layer[l].sq[0] * M.kq;
   }
   M.path = path_req;
+  M.act_word = act_mode == AECCT_ACT_SCALE_WORD ? 1 : 0;
+  M.grouped = L <= 65535;
+
+  // the device: every table and launch below is sized for its compute units and LDS
+  int dev = 0, cus = 0, lds = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || cus <= 0 ||
+      lds <= 0)
+    return AECCT_ERR_DEVICE;
+  M.device = dev;
+  M.cu_count = cus;
+  M.lds_max = (size_t)lds;
+  if (aecct::set_layered_kernel_attributes(M) != hipSuccess || aecct::set_fused_kernel_attributes(M) != hipSuccess)
+    return AECCT_ERR_DEVICE;
 
   // fused-path tables (built whenever the shape allows the fused kernel)
   FusedImage FI;
-  bool fused_ok = path_req != AECCT_PATH_LAYERED && aecct::fused_supported(M);
+  bool fused_ok = path_req != AECCT_PATH_LAYERED && !M.act_word && aecct::fused_supported(M);
   if (fused_ok) {
     build_fused(M, H, w, m1_ptr, m1_idx, m2_ptr, m2_idx, FI);
     // list starts are 16-bit entry indices
@@ -674,7 +719,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
       for (int e = 0; e < slots; ++e) tab.push_back(e < cnt ? (uint16_t)idx[ptr[a] + e] : 0);
     }
   };
-  if (L <= 65535) {
+  if (M.grouped) {
     group_lists(m1_ptr, m1_idx, G1m, G1);
     group_lists(m2_ptr, m2_idx, G2m, G2);
   }
@@ -799,8 +844,6 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   }
 
   // device
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return AECCT_ERR_DEVICE;
   void *blk = nullptr;
   hipError_t e = hipMalloc(&blk, P.total);
   if (e != hipSuccess) return from_hip(e);
@@ -815,7 +858,6 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     return AECCT_ERR_OUT_OF_MEMORY;
   }
   unsigned char *b = (unsigned char *)blk;
-  M.device = dev;
   M.dev_block = blk;
   M.device_bytes = P.total;
   M.chk_ptr = (const int32_t *)(b + P.chk_ptr);
@@ -824,7 +866,6 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.m1_idx = (const int32_t *)(b + P.m1_idx);
   M.m2_ptr = (const int32_t *)(b + P.m2_ptr);
   M.m2_idx = (const int32_t *)(b + P.m2_idx);
-  M.grouped = !G1.empty();
   M.g1_meta = (const int32_t *)(b + P.g1_meta);
   M.g1_tab = (const uint16_t *)(b + P.g1_tab);
   M.g2_meta = (const int32_t *)(b + P.g2_meta);
@@ -870,6 +911,14 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     T.pperm = FI.pperm.empty() ? nullptr : (const float *)(b + P.f_p);
     T.w1perm = (const float *)(b + P.f_w1);
   }
+  // the layered path's projection + attention form
+  const int lattn = resolve_layered_attention(M, lattn_req);
+  if (lattn < 0) {
+    (void)hipFree(blk);
+    delete am;
+    return AECCT_ERR_UNSUPPORTED;
+  }
+  M.lattn = lattn;
   am->M = M;
   *out = am;
   return AECCT_OK;
@@ -881,15 +930,6 @@ void aecct_destroy(aecct_model *model) {
   delete model;
 }
 
-// The layered decode's projection + attention form: fused with fp32 keys and values in LDS when
-// they fit, else (with the token block, which takes O in fp32) with int16 accumulators, else the
-// separate GEMM and attention kernels.
-static int32_t layered_attention_form(const Model &M) {
-  if (aecct::qkv_attention_supported(M)) return AECCT_LAYERED_ATTN_LDS_F32;
-  if (aecct::token_block_supported(M) && aecct::qkv_attention_i16_supported(M)) return AECCT_LAYERED_ATTN_LDS_I16;
-  return AECCT_LAYERED_ATTN_UNFUSED;
-}
-
 aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
   if (!model || !info) return AECCT_ERR_INVALID_ARG;
   const Model &M = model->M;
@@ -897,7 +937,11 @@ aecct_status aecct_get_info(const aecct_model *model, aecct_model_info *info) {
   info->heads = M.heads; info->first_ring_heads = M.hf; info->d_ff = M.dff; info->path = M.path;
   info->nnz_first_ring = M.nnz1; info->nnz_second_ring = M.nnz2; info->device_bytes = M.device_bytes;
   info->attention = M.attention;
-  info->layered_attention = layered_attention_form(M);
+  info->layered_attention = M.lattn;
+  info->act_scale_mode = M.act_word ? AECCT_ACT_SCALE_WORD : AECCT_ACT_SCALE_TOKEN;
+  info->device = M.device;
+  info->compute_units = M.cu_count;
+  info->lds_bytes = (int64_t)M.lds_max;
   return AECCT_OK;
 }
 
@@ -911,37 +955,39 @@ aecct_status aecct_workspace_size(const aecct_model *model, int64_t batch, size_
   return AECCT_OK;
 }
 
-aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits, float *logits,
-                          void *workspace, size_t workspace_bytes, void *stream) {
-  if (!model || batch < 0) return AECCT_ERR_INVALID_ARG;
-  if (batch == 0) return AECCT_OK;
-  if (!y || !bits) return AECCT_ERR_INVALID_ARG;
-  const Model &M = model->M;
-  hipStream_t s = (hipStream_t)stream;
-  size_t need = 0;
-  aecct_workspace_size(model, batch, &need);
-  if (workspace_bytes < need) return AECCT_ERR_WORKSPACE_TOO_SMALL;
-  if (need && !workspace) return AECCT_ERR_INVALID_ARG;
-  if (M.path == AECCT_PATH_FUSED) return from_hip(aecct::launch_fused(M, y, batch, bits, logits, s)) == AECCT_OK
-                                             ? AECCT_OK : AECCT_ERR_DEVICE;
-  const int64_t cw = chunk_words(M, batch);
+// The current device is the model's (every entry point that touches its memory checks this).
+static aecct_status check_device(const Model &M) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return AECCT_ERR_DEVICE;
+  return cur == M.device ? AECCT_OK : AECCT_ERR_INVALID_ARG;
+}
+
+// A decode of `batch` words in chunks of at most `cw` words, each chunk's layered activations in
+// `ws` laid out by ws_plan(M, cw) (unused on the fused path).
+static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch, uint8_t *bits, float *logits,
+                                  unsigned char *ws, int64_t cw, hipStream_t s) {
+  if (M.path == AECCT_PATH_FUSED)
+    return aecct::launch_fused(M, y, batch, bits, logits, s) == hipSuccess ? AECCT_OK : AECCT_ERR_DEVICE;
   const WsPlan W = ws_plan(M, cw);
-  unsigned char *ws = (unsigned char *)workspace;
   float *x = (float *)(ws + W.x), *qkv = (float *)(ws + W.qkv), *x1 = (float *)(ws + W.x1);
   int8_t *xq = (int8_t *)(ws + W.xq), *oq = (int8_t *)(ws + W.oq), *x1q = (int8_t *)(ws + W.x1q);
   int8_t *gq = (int8_t *)(ws + W.gq);
   float *ax = (float *)(ws + W.ax), *ao = (float *)(ws + W.ao), *a1 = (float *)(ws + W.a1), *ag = (float *)(ws + W.ag);
+  float *o32 = M.act_word ? (float *)(ws + W.o32) : nullptr, *h32 = M.act_word ? (float *)(ws + W.h32) : nullptr;
+  // With the token block, X and Xq are kept in its lane order from the embedding to the head.
+  // The fused projection + attention (keys and values in LDS as fp32, or as int16 accumulators
+  // for long words) leaves O in fp32 (in the QKV space); the token block then applies Eq. 2
+  // itself. The unfused attention quantises O as it writes it (a quarter of the bytes).  With one
+  // alpha per word every quantisation point is redone over the whole word from the fp32 values
+  // (natural layout, unfused form, no token block).
+  const bool pw = M.act_word != 0;
+  const bool tb = !pw && aecct::token_block_supported(M);
+  const bool qa = M.lattn == AECCT_LAYERED_ATTN_LDS_F32, qw = M.lattn == AECCT_LAYERED_ATTN_LDS_I16;
   for (int64_t w0 = 0; w0 < batch; w0 += cw) {
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
-    // With the token block, X and Xq are kept in its lane order from the embedding to the head.
-    // The fused projection + attention (keys and values in LDS as fp32, or as int16 accumulators
-    // for long words) leaves O in fp32 (in the QKV space); the token block then applies Eq. 2
-    // itself. The unfused attention quantises O as it writes it (a quarter of the bytes).
-    const bool tb = aecct::token_block_supported(M);
-    const int32_t form = layered_attention_form(M);
-    const bool qa = form == AECCT_LAYERED_ATTN_LDS_F32, qw = form == AECCT_LAYERED_ATTN_LDS_I16;
     hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, tb, s);
+    if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x, nw, M.d, false, xq, ax, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
       if (qa) {
         e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, tb, s);
@@ -949,7 +995,8 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
         e = aecct::launch_qkv_attention_i16(M, l, xq, ax, nw, qkv, tb, s);
       } else {
         e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, tb, s);
-        if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, nullptr, oq, ao, s);
+        if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, o32, oq, ao, s);
+        if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, o32, nw, M.d, false, oq, ao, s);
       }
       if (e != hipSuccess) break;
       if (tb) {
@@ -957,8 +1004,15 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
                      : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
-        if (e == hipSuccess) e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
+        if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x1, nw, M.d, false, x1q, a1, s);
+        if (pw) {
+          if (e == hipSuccess) e = aecct::launch_ffn1_f32(M, l, x1q, a1, rows, h32, s);
+          if (e == hipSuccess) e = aecct::launch_word_quant(M, h32, nw, M.dff, true, gq, ag, s);
+        } else if (e == hipSuccess) {
+          e = aecct::launch_ffn1(M, l, x1q, a1, rows, gq, ag, s);
+        }
         if (e == hipSuccess) e = aecct::launch_ffn2_ln(M, l, gq, ag, x1, rows, x, xq, ax, s);
+        if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x, nw, M.d, false, xq, ax, s);
       }
     }
     if (e == hipSuccess)
@@ -969,11 +1023,34 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
   return AECCT_OK;
 }
 
+aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits, float *logits,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+  if (!model || batch < 0) return AECCT_ERR_INVALID_ARG;
+  if (batch == 0) return AECCT_OK;
+  if (!y || !bits) return AECCT_ERR_INVALID_ARG;
+  const Model &M = model->M;
+  const aecct_status dv = check_device(M);
+  if (dv != AECCT_OK) return dv;
+  size_t need = 0;
+  aecct_workspace_size(model, batch, &need);
+  if (workspace_bytes < need) return AECCT_ERR_WORKSPACE_TOO_SMALL;
+  if (need && !workspace) return AECCT_ERR_INVALID_ARG;
+  return decode_chunks(M, y, batch, bits, logits, (unsigned char *)workspace, chunk_words(M, batch),
+                       (hipStream_t)stream);
+}
+
 // ---- stage entry points --------------------------------------------------------------------
 
-#define AECCT_STAGE_CHECK(cond) \
+#define AECCT_STAGE_CHECK(cond)                          \
+  do {                                                   \
+    if (!(cond)) return AECCT_ERR_INVALID_ARG;           \
+    const aecct_status dv_ = check_device(model->M);     \
+    if (dv_ != AECCT_OK) return dv_;                     \
+  } while (0)
+// steps that quantise: a row's codes depend on the whole word when alpha is per word
+#define AECCT_STAGE_PER_TOKEN() \
   do {                          \
-    if (!(cond)) return AECCT_ERR_INVALID_ARG; \
+    if (model->M.act_word) return AECCT_ERR_UNSUPPORTED; \
   } while (0)
 
 static inline aecct_status launched(hipError_t e) { return e == hipSuccess ? AECCT_OK : AECCT_ERR_DEVICE; }
@@ -981,6 +1058,7 @@ static inline aecct_status launched(hipError_t e) { return e == hipSuccess ? AEC
 aecct_status aecct_stage_embed(const aecct_model *model, const float *y, int64_t words, float *x, int8_t *xq,
                                float *ax, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (y && x && xq && ax)));
+  AECCT_STAGE_PER_TOKEN();
   return launched(aecct::launch_embed(model->M, y, words, x, xq, ax, false, (hipStream_t)stream));
 }
 
@@ -993,6 +1071,7 @@ aecct_status aecct_stage_qkv(const aecct_model *model, int32_t layer, const int8
 aecct_status aecct_stage_attention(const aecct_model *model, const float *qkv, int64_t words, float *o, int8_t *oq,
                                    float *ao, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && (words == 0 || (qkv && oq && ao)));
+  AECCT_STAGE_PER_TOKEN();
   return launched(aecct::launch_attention(model->M, qkv, words, o, oq, ao, (hipStream_t)stream));
 }
 
@@ -1000,6 +1079,7 @@ aecct_status aecct_stage_oproj_ln(const aecct_model *model, int32_t layer, const
                                   const float *x, int64_t words, float *x1, int8_t *x1q, float *a1, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers &&
                     (words == 0 || (oq && ao && x && x1 && x1q && a1)));
+  AECCT_STAGE_PER_TOKEN();
   return launched(aecct::launch_oproj_ln(model->M, layer, oq, ao, x, words * model->M.L, x1, x1q, a1,
                                          (hipStream_t)stream));
 }
@@ -1007,6 +1087,7 @@ aecct_status aecct_stage_oproj_ln(const aecct_model *model, int32_t layer, const
 aecct_status aecct_stage_ffn1(const aecct_model *model, int32_t layer, const int8_t *x1q, const float *a1,
                               int64_t words, int8_t *gq, float *ag, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers && (words == 0 || (x1q && a1 && gq && ag)));
+  AECCT_STAGE_PER_TOKEN();
   return launched(aecct::launch_ffn1(model->M, layer, x1q, a1, words * model->M.L, gq, ag, (hipStream_t)stream));
 }
 
@@ -1014,6 +1095,7 @@ aecct_status aecct_stage_ffn2_ln(const aecct_model *model, int32_t layer, const 
                                  const float *x1, int64_t words, float *x, int8_t *xq, float *ax, void *stream) {
   AECCT_STAGE_CHECK(model && words >= 0 && layer >= 0 && layer < model->M.n_layers &&
                     (words == 0 || (gq && ag && x1 && x && xq && ax)));
+  AECCT_STAGE_PER_TOKEN();
   return launched(aecct::launch_ffn2_ln(model->M, layer, gq, ag, x1, words * model->M.L, x, xq, ax,
                                         (hipStream_t)stream));
 }

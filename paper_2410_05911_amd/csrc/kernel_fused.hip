@@ -20,6 +20,8 @@
 // a per-wave LDS buffer that the neighbour loops gather from.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "aecct_internal.h"
 #include "device_common.h"
 
@@ -500,23 +502,30 @@ bool fused_supported(const Model &M) {
 // wavefronts (its register budget), and runs with any smaller count.
 int fused_waves(const Model &M, int nbr_words) {
   const FusedLds L = fused_lds(M, nbr_words);
-  if ((size_t)L.off_kv >= (size_t)fz::kLdsMax) return 0;
-  const int fit = (int)(((size_t)fz::kLdsMax - (size_t)L.off_kv) / (size_t)L.kv_bytes);
+  const size_t lds_max = std::min<size_t>(M.lds_max, fz::kLdsMax);
+  if ((size_t)L.off_kv >= lds_max) return 0;
+  const int fit = (int)((lds_max - (size_t)L.off_kv) / (size_t)L.kv_bytes);
   const int w = fit < fz::kWaves ? fit : fz::kWaves;
   return w >= 4 ? w : 0;
 }
 
 bool fused_fits(const Model &M, int nbr_words) { return fused_waves(M, nbr_words) > 0; }
 
+// The largest dynamic LDS the fused kernel may use on the model's device, set once per model at
+// create time (the launches only choose a size within it).
+hipError_t set_fused_kernel_attributes(const Model &M) {
+  const void *fns[] = {(const void *)k_fused_decode<1, fz::kWaves>, (const void *)k_fused_decode<2, fz::kWaves>,
+                       (const void *)k_fused_decode<3, fz::kWaves>, (const void *)k_fused_decode<4, fz::kWaves>};
+  const int lds = (int)std::min<size_t>(M.lds_max, fz::kLdsMax);
+  for (const void *f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 template <int NT, int WAVES>
 static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, int waves, hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_fused_decode<NT, WAVES>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, fz::kLdsMax);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
   hipLaunchKernelGGL((k_fused_decode<NT, WAVES>), dim3(grid), dim3(waves * 64), lds, s, a);
   return hipGetLastError();
 }
@@ -561,12 +570,13 @@ hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *
   a.kv_bytes = Ld.kv_bytes;
   const size_t off = (size_t)Ld.off_kv;
   const int waves = fused_waves(M, T.nbr_words);
-  if (waves < 1 || waves > fz::kWaves || off + (size_t)waves * a.kv_bytes > (size_t)fz::kLdsMax)
+  const size_t lds_max = std::min<size_t>(M.lds_max, fz::kLdsMax);
+  if (waves < 1 || waves > fz::kWaves || off + (size_t)waves * a.kv_bytes > lds_max)
     return hipErrorInvalidConfiguration;
   const size_t lds = off + (size_t)waves * a.kv_bytes;
   int64_t blocks = (words + waves - 1) / waves;
-  const int64_t per_cu = (int64_t)(fz::kLdsMax / lds) > 0 ? (int64_t)(fz::kLdsMax / lds) : 1;
-  const int64_t cap = 256 * per_cu;
+  const int64_t per_cu = (int64_t)(lds_max / lds) > 0 ? (int64_t)(lds_max / lds) : 1;
+  const int64_t cap = (int64_t)M.cu_count * per_cu;
   const int grid = (int)(blocks < cap ? blocks : cap);
   switch (NT) {
     case 1: return launch_nt<1, fz::kWaves>(a, lds, grid, waves, s);

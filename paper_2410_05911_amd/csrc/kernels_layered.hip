@@ -83,7 +83,9 @@ __device__ __forceinline__ void wave_barrier_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3, EPI_QKV_MAP = 4 };
+// EPI_F32: plain fp32 output fma(acc, alpha sq[0], bias) of every column (the feed-forward hidden
+// row before its ReLU, when Eq. 2 of the hidden row takes one alpha per word).
+enum Epi { EPI_RAW = 0, EPI_QKV = 1, EPI_LN = 2, EPI_RELU_QUANT = 3, EPI_QKV_MAP = 4, EPI_F32 = 5 };
 
 struct GemmArgs {
   const int8_t *a;        // [rows][K]
@@ -157,7 +159,16 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemmArgs p) {
       float al[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) al[i] = ok[i] ? p.alpha[r[i]] : 0.0f;
-      if constexpr (EPI == EPI_QKV_MAP) {
+      if constexpr (EPI == EPI_F32) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const int j = 16 * t + col;
+          const float b = p.bias[j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (ok[i]) p.out_f[r[i] * NOUT + j] = __builtin_fmaf((float)acc[t][i], al[i] * p.sq[0], b);
+        }
+      } else if constexpr (EPI == EPI_QKV_MAP) {
 #pragma unroll
         for (int t = 0; t < T; ++t) {
           const int j = 16 * t + col;
@@ -1648,25 +1659,75 @@ __global__ __launch_bounds__(256) void k_head_gemm(HeadArgs p, int64_t words, co
 }
 
 // ------------------------------------------------------------------------------------------
+// Eq. 2 with one alpha per word (the reading of Section 4.1 in which alpha = ||x||_inf is taken
+// over the whole layer input of a word): alpha = max |x| over the word's L rows of K values
+// (of max(x, 0) when RELU, the feed-forward hidden row), then every value's code
+// x * fp32(127 / alpha) rounded half to even, and a[row] = alpha for each of the word's rows, so
+// the dequantisation of Eq. 3 reads it like a per-token scale.  One block per word (persistent
+// over the words), natural layout, four values per lane and step.
+// ------------------------------------------------------------------------------------------
+constexpr int kWqThreads = 256;
+
+template <bool RELU>
+__global__ __launch_bounds__(kWqThreads) void k_word_quant(const float *x, int64_t words, int64_t per_word, int L,
+                                                           int8_t *q, float *a) {
+  __shared__ float red[kWqThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t n4 = per_word / 4;                       // per_word = L K, K a multiple of 32
+  for (int64_t w = blockIdx.x; w < words; w += gridDim.x) {
+    const float4 *xw = (const float4 *)(x + w * per_word);
+    float m = 0.0f;
+    for (int64_t e = tid; e < n4; e += kWqThreads) {
+      float4 v = xw[e];
+      if (RELU) {
+        v.x = v.x > 0.0f ? v.x : 0.0f; v.y = v.y > 0.0f ? v.y : 0.0f;
+        v.z = v.z > 0.0f ? v.z : 0.0f; v.w = v.w > 0.0f ? v.w : 0.0f;
+      }
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    float alpha = red[0];
+#pragma unroll
+    for (int k = 1; k < kWqThreads / 64; ++k) alpha = fmaxf(alpha, red[k]);
+    const float inv = inv127(alpha);
+    uint32_t *qw = (uint32_t *)(q + w * per_word);
+    for (int64_t e = tid; e < n4; e += kWqThreads) {
+      float4 v = xw[e];
+      if (RELU) {
+        v.x = v.x > 0.0f ? v.x : 0.0f; v.y = v.y > 0.0f ? v.y : 0.0f;
+        v.z = v.z > 0.0f ? v.z : 0.0f; v.w = v.w > 0.0f ? v.w : 0.0f;
+      }
+      qw[e] = (quant_bits(v.x, inv) & 0xffu) | (quant_bits(v.y, inv) & 0xffu) << 8 |
+              (quant_bits(v.z, inv) & 0xffu) << 16 | (quant_bits(v.w, inv) & 0xffu) << 24;
+    }
+    for (int r = tid; r < L; r += kWqThreads) a[w * L + r] = alpha;
+    __syncthreads();                                     // red[] is rewritten for the next word
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------
 namespace {
 
 // Persistent grid: as many blocks as stay resident (LDS-limited), each staging its map's
 // weights once and striding over the 16-row strips.
-int gemm_grid(int64_t rows, size_t lds_bytes) {
+int gemm_grid(const Model &M, int64_t rows, size_t lds_bytes) {
   const int64_t groups = ((rows + 15) / 16 + kGemmWaves - 1) / kGemmWaves;
-  const int64_t per_cu = lds_bytes ? std::max<int64_t>(1, (int64_t)(160 * 1024 / lds_bytes)) : 8;
-  const int64_t g = std::min<int64_t>(groups, 256 * std::min<int64_t>(per_cu, 8));
+  const int64_t per_cu = lds_bytes ? std::max<int64_t>(1, (int64_t)(M.lds_max / lds_bytes)) : 8;
+  const int64_t g = std::min<int64_t>(groups, (int64_t)M.cu_count * std::min<int64_t>(per_cu, 8));
   return (int)(g > 0 ? g : 1);
 }
 
 template <int K, int NOUT, int EPI>
-hipError_t run_gemm(const GemmArgs &a, hipStream_t s) {
+hipError_t run_gemm(const Model &M, const GemmArgs &a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   constexpr bool kQuantOut = (EPI == EPI_LN || EPI == EPI_RELU_QUANT);
   constexpr size_t lds = (size_t)(NOUT / 16) * (K / 32) * 64 * 8 + (kQuantOut ? (size_t)kGemmWaves * 16 * NOUT : 16);
-  hipLaunchKernelGGL((k_gemm<K, NOUT, EPI>), dim3(gemm_grid(a.rows, lds)), dim3(kGemmWaves * 64), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<K, NOUT, EPI>), dim3(gemm_grid(M, a.rows, lds)), dim3(kGemmWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1713,8 +1774,8 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
   a.bias = W.b_qkv;
   a.out_f = qkv;
   switch (M.d) {
-    case 32: return run_gemm<32, 96, EPI_QKV>(a, s);
-    case 64: return run_gemm<64, 192, EPI_QKV>(a, s);
+    case 32: return run_gemm<32, 96, EPI_QKV>(M, a, s);
+    case 64: return run_gemm<64, 192, EPI_QKV>(M, a, s);
     case 128:
       // one launch per map: 8 output tiles per wave instead of 24
       for (int m = 0; m < 3; ++m) {
@@ -1723,7 +1784,7 @@ hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *
         b.sq[0] = a.sq[m];
         b.bias = a.bias + 128 * m;
         b.out_f = a.out_f + 128 * m;
-        const hipError_t e = run_gemm<128, 128, EPI_QKV_MAP>(b, s);
+        const hipError_t e = run_gemm<128, 128, EPI_QKV_MAP>(M, b, s);
         if (e != hipSuccess) return e;
       }
       return hipSuccess;
@@ -1745,9 +1806,9 @@ hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const fl
   a.out_q = x1q;
   a.out_a = a1;
   switch (M.d) {
-    case 32: return run_gemm<32, 32, EPI_LN>(a, s);
-    case 64: return run_gemm<64, 64, EPI_LN>(a, s);
-    case 128: return run_gemm<128, 128, EPI_LN>(a, s);
+    case 32: return run_gemm<32, 32, EPI_LN>(M, a, s);
+    case 64: return run_gemm<64, 64, EPI_LN>(M, a, s);
+    case 128: return run_gemm<128, 128, EPI_LN>(M, a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1761,9 +1822,9 @@ hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float
   a.out_q = gq;
   a.out_a = ag;
   switch (M.d) {
-    case 32: return run_gemm<32, 128, EPI_RELU_QUANT>(a, s);
-    case 64: return run_gemm<64, 256, EPI_RELU_QUANT>(a, s);
-    case 128: return run_gemm<128, 512, EPI_RELU_QUANT>(a, s);
+    case 32: return run_gemm<32, 128, EPI_RELU_QUANT>(M, a, s);
+    case 64: return run_gemm<64, 256, EPI_RELU_QUANT>(M, a, s);
+    case 128: return run_gemm<128, 512, EPI_RELU_QUANT>(M, a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1782,9 +1843,9 @@ hipError_t launch_ffn2_ln(const Model &M, int layer, const int8_t *gq, const flo
   a.out_q = xq;
   a.out_a = ax;
   switch (M.d) {
-    case 32: return run_gemm<128, 32, EPI_LN>(a, s);
-    case 64: return run_gemm<256, 64, EPI_LN>(a, s);
-    case 128: return run_gemm<512, 128, EPI_LN>(a, s);
+    case 32: return run_gemm<128, 32, EPI_LN>(M, a, s);
+    case 64: return run_gemm<256, 64, EPI_LN>(M, a, s);
+    case 128: return run_gemm<512, 128, EPI_LN>(M, a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1798,17 +1859,17 @@ hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t
   a.out_acc = acc;
   const int d = M.d;
   if (kind <= 3) {
-    if (d == 32) return run_gemm<32, 32, EPI_RAW>(a, s);
-    if (d == 64) return run_gemm<64, 64, EPI_RAW>(a, s);
-    if (d == 128) return run_gemm<128, 128, EPI_RAW>(a, s);
+    if (d == 32) return run_gemm<32, 32, EPI_RAW>(M, a, s);
+    if (d == 64) return run_gemm<64, 64, EPI_RAW>(M, a, s);
+    if (d == 128) return run_gemm<128, 128, EPI_RAW>(M, a, s);
   } else if (kind == 4) {
-    if (d == 32) return run_gemm<32, 128, EPI_RAW>(a, s);
-    if (d == 64) return run_gemm<64, 256, EPI_RAW>(a, s);
-    if (d == 128) return run_gemm<128, 512, EPI_RAW>(a, s);
+    if (d == 32) return run_gemm<32, 128, EPI_RAW>(M, a, s);
+    if (d == 64) return run_gemm<64, 256, EPI_RAW>(M, a, s);
+    if (d == 128) return run_gemm<128, 512, EPI_RAW>(M, a, s);
   } else {
-    if (d == 32) return run_gemm<128, 32, EPI_RAW>(a, s);
-    if (d == 64) return run_gemm<256, 64, EPI_RAW>(a, s);
-    if (d == 128) return run_gemm<512, 128, EPI_RAW>(a, s);
+    if (d == 32) return run_gemm<128, 32, EPI_RAW>(M, a, s);
+    if (d == 64) return run_gemm<256, 64, EPI_RAW>(M, a, s);
+    if (d == 128) return run_gemm<512, 128, EPI_RAW>(M, a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1836,26 +1897,19 @@ size_t qkv_attention_lds(const Model &M, bool resident = false) {
 // Keep every head group's weight tiles in LDS when that does not lower the blocks per CU.
 bool qkv_attention_resident(const Model &M) {
   const size_t one = qkv_attention_lds(M, false), all = qkv_attention_lds(M, true);
-  return all <= 160 * 1024 && (160 * 1024 / all) >= (160 * 1024 / one);
+  return all <= M.lds_max && (M.lds_max / all) >= (M.lds_max / one);
 }
 
 bool qkv_attention_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped &&
          M.L <= 16 * (kQaThreads / 64) * kQaTilesPerWave && M.L * (16 / M.dh) <= kQaThreads &&
-         qkv_attention_lds(M) <= 160 * 1024;
+         qkv_attention_lds(M) <= M.lds_max;
 }
 
 template <int D, int DH>
-static hipError_t run_qkv_attention(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention<D, DH>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+static hipError_t run_qkv_attention(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
   hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)blocks), dim3(kQaThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -1865,20 +1919,13 @@ size_t qkv_attention_pair_lds(const Model &M) { return qkv_attention_lds(M, true
 
 bool qkv_attention_pair_supported(const Model &M) {
   return M.d == 128 && M.dh == 16 && M.grouped && M.L <= 16 * (kQpThreads / 64) * kQpTilesPerWave &&
-         qkv_attention_pair_lds(M) <= 160 * 1024;
+         qkv_attention_pair_lds(M) <= M.lds_max;
 }
 
 template <int D>
-static hipError_t run_qkv_attention_pair(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_pair<D>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+static hipError_t run_qkv_attention_pair(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
   hipLaunchKernelGGL((k_qkv_attention_pair<D>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -1906,11 +1953,11 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.resident = qkv_attention_resident(M) ? 1 : 0;
   const size_t lds = qkv_attention_lds(M, a.resident != 0);
   hipError_t e = hipErrorInvalidValue;
-  if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(a, qkv_attention_pair_lds(M), s);
-  else if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(a, lds, s);
-  else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(a, lds, s);
-  else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(a, lds, s);
-  else if (M.d == 64 && M.dh == 16) e = run_qkv_attention<64, 16>(a, lds, s);
+  if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M), s);
+  else if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(M, a, lds, s);
+  else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(M, a, lds, s);
+  else if (M.d == 128 && M.dh == 8) e = run_qkv_attention<128, 8>(M, a, lds, s);
+  else if (M.d == 64 && M.dh == 16) e = run_qkv_attention<64, 16>(M, a, lds, s);
   if (e != hipSuccess || !oq) return e;
   const int64_t rows = words * M.L;
   const dim3 grid((unsigned)((rows + 15) / 16));
@@ -1922,20 +1969,13 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
 bool qkv_attention_i16_supported(const Model &M) {
   if (!((M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped)) return false;
   const size_t lds = M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L);
-  return lds <= 160 * 1024;
+  return lds <= M.lds_max;
 }
 
 template <int D, int DH>
-static hipError_t run_qkv_attention_i16(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_i16<D, DH>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+static hipError_t run_qkv_attention_i16(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
   hipLaunchKernelGGL((k_qkv_attention_i16<D, DH>), dim3((unsigned)blocks), dim3(kQaThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -1945,20 +1985,13 @@ bool qkv_attention_v16_supported(const Model &M) {
   if (!((M.d == 64 || M.d == 128) && M.dh == 16 && M.grouped)) return false;
   if (M.L > 16 * (kQvThreads / 64) * kQvTilesPerWave) return false;
   const size_t lds = M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L);
-  return lds <= 160 * 1024;
+  return lds <= M.lds_max;
 }
 
 template <int D>
-static hipError_t run_qkv_attention_v16(const QkvAttnArgs &a, size_t lds, hipStream_t s) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attention_v16<D>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>(a.words, 256 * per_cu);
+static hipError_t run_qkv_attention_v16(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
   hipLaunchKernelGGL((k_qkv_attention_v16<D>), dim3((unsigned)blocks), dim3(kQvThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -1985,13 +2018,13 @@ hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq,
   a.o = o;
   if (qkv_attention_v16_supported(M)) {
     const size_t lv = M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L);
-    return M.d == 64 ? run_qkv_attention_v16<64>(a, lv, s) : run_qkv_attention_v16<128>(a, lv, s);
+    return M.d == 64 ? run_qkv_attention_v16<64>(M, a, lv, s) : run_qkv_attention_v16<128>(M, a, lv, s);
   }
   const size_t lds = M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L);
-  if (M.d == 128 && M.dh == 16) return run_qkv_attention_i16<128, 16>(a, lds, s);
-  if (M.d == 64 && M.dh == 16) return run_qkv_attention_i16<64, 16>(a, lds, s);
-  if (M.d == 64 && M.dh == 8) return run_qkv_attention_i16<64, 8>(a, lds, s);
-  if (M.d == 128 && M.dh == 8) return run_qkv_attention_i16<128, 8>(a, lds, s);
+  if (M.d == 128 && M.dh == 16) return run_qkv_attention_i16<128, 16>(M, a, lds, s);
+  if (M.d == 64 && M.dh == 16) return run_qkv_attention_i16<64, 16>(M, a, lds, s);
+  if (M.d == 64 && M.dh == 8) return run_qkv_attention_i16<64, 8>(M, a, lds, s);
+  if (M.d == 128 && M.dh == 8) return run_qkv_attention_i16<128, 8>(M, a, lds, s);
   return hipErrorInvalidValue;
 }
 
@@ -2000,18 +2033,11 @@ bool token_block_supported(const Model &M) {
 }
 
 template <int D, bool OQ>
-static hipError_t run_token_block(const TokenBlockArgs &a, hipStream_t s) {
+static hipError_t run_token_block(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
   constexpr size_t lds = token_block_lds<D>();
-  static bool attr_set = false;
-  if (!attr_set) {
-    const hipError_t e =
-        hipFuncSetAttribute((const void *)k_token_block<D, OQ>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
   const int64_t strips = (a.rows + 15) / 16;
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024 / lds));
-  const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, 256 * per_cu);
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, (int64_t)M.cu_count * per_cu);
   hipLaunchKernelGGL((k_token_block<D, OQ>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
   return hipGetLastError();
 }
@@ -2039,8 +2065,8 @@ hipError_t launch_token_block(const Model &M, int layer, const float *o, const i
   a.xq = xq;
   a.ax = ax;
   if (!oq == !o) return hipErrorInvalidValue;
-  if (oq) return M.d == 64 ? run_token_block<64, true>(a, s) : run_token_block<128, true>(a, s);
-  return M.d == 64 ? run_token_block<64, false>(a, s) : run_token_block<128, false>(a, s);
+  if (oq) return M.d == 64 ? run_token_block<64, true>(M, a, s) : run_token_block<128, true>(M, a, s);
+  return M.d == 64 ? run_token_block<64, false>(M, a, s) : run_token_block<128, false>(M, a, s);
 }
 
 hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
@@ -2049,7 +2075,7 @@ hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int
   if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
   HeadArgs a{x, y, M.n, M.L, M.head_w1, M.head_wo, M.head_bo, M.head_b1, bits, logits};
   const int64_t rows = words * M.L;
-  const unsigned zgrid = (unsigned)std::min<int64_t>((rows + 15) / 16, 256 * 64);
+  const unsigned zgrid = (unsigned)std::min<int64_t>((rows + 15) / 16, (int64_t)M.cu_count * 64);
   switch (M.d) {
     case 32: hipLaunchKernelGGL((k_head_z<32, false>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf); break;
     case 64:
@@ -2087,6 +2113,51 @@ hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t w
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// The largest dynamic LDS each kernel that takes it may use on the model's device, set once per
+// model at create time (the launches only choose a size within it).
+hipError_t set_layered_kernel_attributes(const Model &M) {
+  const void *fns[] = {
+      (const void *)k_qkv_attention<64, 8>,      (const void *)k_qkv_attention<128, 16>,
+      (const void *)k_qkv_attention<128, 8>,     (const void *)k_qkv_attention<64, 16>,
+      (const void *)k_qkv_attention_pair<128>,   (const void *)k_qkv_attention_i16<128, 16>,
+      (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
+      (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
+      (const void *)k_qkv_attention_v16<128>,    (const void *)k_token_block<64, true>,
+      (const void *)k_token_block<64, false>,    (const void *)k_token_block<128, true>,
+      (const void *)k_token_block<128, false>};
+  for (const void *f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)M.lds_max);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_word_quant(const Model &M, const float *x, int64_t words, int K, bool relu, int8_t *q, float *a,
+                             hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  if (K % 32) return hipErrorInvalidValue;
+  const int64_t per_word = (int64_t)M.L * K;
+  const unsigned grid = (unsigned)std::min<int64_t>(words, (int64_t)M.cu_count * 8);
+  if (relu) hipLaunchKernelGGL(k_word_quant<true>, dim3(grid), dim3(kWqThreads), 0, s, x, words, per_word, M.L, q, a);
+  else hipLaunchKernelGGL(k_word_quant<false>, dim3(grid), dim3(kWqThreads), 0, s, x, words, per_word, M.L, q, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ffn1_f32(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, float *h,
+                           hipStream_t s) {
+  const LayerWeights &W = M.layer[layer];
+  GemmArgs a = gemm_base(x1q, a1, W.ff1, rows);
+  a.sq[0] = W.sq[4];
+  a.bias = W.b_ff1;
+  a.out_f = h;
+  switch (M.d) {
+    case 32: return run_gemm<32, 128, EPI_F32>(M, a, s);
+    case 64: return run_gemm<64, 256, EPI_F32>(M, a, s);
+    case 128: return run_gemm<128, 512, EPI_F32>(M, a, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace aecct

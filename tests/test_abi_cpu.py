@@ -128,3 +128,30 @@ def test_null_model_calls(P):
     assert L.aecct_stage_embed(None, None, 1, None, None, None, None) == P.ERR_INVALID_ARG
     assert L.aecct_ternary_gemm(None, 0, 0, None, 1, None, None) == P.ERR_INVALID_ARG
     L.aecct_destroy(None)
+
+
+def test_struct_layouts_match_the_header(P, tmp_path):
+    """Every struct the binding mirrors has the C compiler's size and field offsets (a field the
+    header lacks, or one out of order, would pass the wrong values silently)."""
+    import subprocess
+    structs = {"aecct_weights": P.Weights, "aecct_options": P.Options, "aecct_model_info": P.ModelInfo,
+               "aecct_spe_params": P.SpeParams}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "aecct.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.splitlines():
+        cname, field, val = line.split()
+        got[(cname, field)] = int(val)
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == C.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert got[(cname, fname)] == getattr(cls, fname).offset, (cname, fname)

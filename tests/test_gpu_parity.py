@@ -134,8 +134,9 @@ def test_stages_teacher_forced(P, oracle_mod, c, words):
 
 
 # ------------------------------------------------------------------------------ end to end
-# oracle sample sizes per workload (whole words the CPU oracle decodes in seconds)
-_SAMPLE = {1: 1024, 2: 768, 3: 48, 4: 6, 5: 2}
+# oracle sample sizes per workload (whole words the CPU oracle decodes in seconds), spread over
+# the batch: every persistent block's share and every workspace chunk of the layered path
+_SAMPLE = {1: 1024, 2: 768, 3: 96, 4: 64, 5: 32}
 
 
 @pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
@@ -429,6 +430,41 @@ def test_layered_attention_forms_of_the_workloads(P):
     for c, form in ((3, P.LAYERED_ATTN_LDS_F32), (4, P.LAYERED_ATTN_LDS_F32), (5, P.LAYERED_ATTN_LDS_I16)):
         cfg, H, G, w, y, x, dec = _setup(P, c, 4, P.PATH_LAYERED)
         assert dec.info.layered_attention == form, c
+        print(f"[forms] config {c}: device {dec.info.device}, {dec.info.compute_units} CUs, "
+              f"{dec.info.lds_bytes} LDS bytes per workgroup", flush=True)
+        assert dec.info.compute_units > 0 and dec.info.lds_bytes >= 64 * 1024
+
+
+@pytest.mark.parametrize("c", [3, 4, 5])
+def test_layered_attention_forms_agree_on_the_whole_batch(P, c):
+    """The full configured batch through every Q/K/V + attention form the shape allows: the
+    production kernels (fp32 K and V in LDS with lane pairs on LDPC(256,128), fp32 keys beside
+    int16 values on LDPC(1024,512)), the int16 forms, and the unfused GEMM + attention kernels
+    that the stage entry points run; all bit-identical."""
+    cfg = CONFIGS[c]
+    print(f"[forms e2e] config {c} batch {cfg.batch}", flush=True)
+    cfg, H, G, w, y, x = build_workload(c)
+    yd = _dev(y)
+    ref = None
+    forms = {3: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_I16, P.LAYERED_ATTN_UNFUSED),
+             4: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_I16, P.LAYERED_ATTN_UNFUSED),
+             5: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_UNFUSED)}[c]
+    for form in forms:
+        dec = P.Decoder(H, w, layered_attention=form)
+        if form != P.LAYERED_ATTN_AUTO:
+            assert dec.info.layered_attention == form
+        bits, logits = dec.decode(yd)
+        torch.cuda.synchronize()
+        if ref is None:
+            ref = (bits, logits)
+        else:
+            nb = int((logits != ref[1]).sum())
+            assert nb == 0 and torch.equal(bits, ref[0]), (form, nb)
+        dec.close()
+    if c == 5:
+        with pytest.raises(P.AecctError) as ei:
+            P.Decoder(H, w, layered_attention=P.LAYERED_ATTN_LDS_F32)   # 1536 tokens: no room in LDS
+        assert ei.value.status == P.ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("m,n,hf,attention,with_pos", [
