@@ -294,6 +294,24 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
                           float *logits, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * aecct_decode without a workspace argument and without any allocation, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments and results as aecct_decode (y, bits, logits are the
+ * caller's device buffers, bits and logits bit-identical to aecct_decode's).
+ * The layered path's activations live in one static 256 MiB device array per GPU, which the
+ * library holds from its first model on that GPU until the process ends; the batch runs in
+ * chunks of as many words as the array holds (the fused path needs none).  Every call on a GPU
+ * shares that GPU's array and leaves its contents behind; no part of it has to start cleared.
+ * Calls that overlap in time on one GPU (on different streams or host threads) race on the
+ * array: the caller must order them.  Enqueues only; never allocates or synchronises.
+ * Errors: INVALID_ARG (as aecct_decode, or another current device), WORKSPACE_TOO_SMALL (one
+ * word's activations exceed 256 MiB; no shape aecct_create accepts needs that much), DEVICE
+ * (the array's address could not be obtained at create, or a launch failed).
+ */
+aecct_status aecct_decode_static(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits,
+                                 float *logits, void *stream);
+
+/*
  * Device arithmetic self-check (for tests and bring-up; decoding does not need it).  The kernels
  * compute three quantities with gfx950 instructions whose results the oracle states in IEEE
  * terms; this compares the two on the current device over every fp32 operand of the ranges the

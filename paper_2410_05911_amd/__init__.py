@@ -85,6 +85,8 @@ def lib():
         L.aecct_workspace_size.argtypes = [_vp, C.c_int64, C.POINTER(C.c_size_t)]
         L.aecct_decode.restype = C.c_int
         L.aecct_decode.argtypes = [_vp, _vp, C.c_int64, _vp, _vp, _vp, C.c_size_t, _vp]
+        L.aecct_decode_static.restype = C.c_int
+        L.aecct_decode_static.argtypes = [_vp, _vp, C.c_int64, _vp, _vp, _vp]
         L.aecct_stage_embed.restype = C.c_int
         L.aecct_stage_embed.argtypes = [_vp, _vp, C.c_int64, _vp, _vp, _vp, _vp]
         L.aecct_stage_qkv.restype = C.c_int
@@ -303,6 +305,19 @@ class Decoder:
         ws = workspace if workspace is not None else self.workspace(B, y.device)
         _check(lib().aecct_decode(self._h, _ptr(y), B, _ptr(bits), _ptr(logits), _ptr(ws),
                                   0 if ws is None else ws.numel(), _stream_ptr(stream)), "aecct_decode")
+        return bits, logits
+
+    def decode_static(self, y, bits=None, logits=None, stream=None, with_logits: bool = True):
+        """aecct_decode_static: the same decode with the library's static device scratch (no
+        workspace, no allocation by the library)."""
+        import torch
+        B = y.shape[0]
+        if bits is None:
+            bits = torch.empty((B, self.n), dtype=torch.uint8, device=y.device)
+        if logits is None and with_logits:
+            logits = torch.empty((B, self.n), dtype=torch.float32, device=y.device)
+        _check(lib().aecct_decode_static(self._h, _ptr(y), B, _ptr(bits), _ptr(logits), _stream_ptr(stream)),
+               "aecct_decode_static")
         return bits, logits
 
     # ------------------------------------------------------------------ stages

@@ -78,6 +78,7 @@ struct Model {
   int64_t nnz1, nnz2;
   size_t device_bytes;
   void *dev_block;       // single device allocation holding everything below
+  unsigned char *static_scratch;  // the device's address of the library's static scratch array
 
   // Tanner graph: check j's variables chk_idx[chk_ptr[j] .. chk_ptr[j+1]) ascending
   const int32_t *chk_ptr, *chk_idx;

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <functional>
 #include <iterator>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -20,6 +21,33 @@ using aecct::Model;
 struct aecct_model {
   Model M;
 };
+
+// ---- static scratch of aecct_decode_static -----------------------------------------------
+// The layered decode's workspace for callers that cannot allocate: one array per GPU the library
+// runs on, held until the process ends.  In host code `scratch` only names the array; its device
+// address comes from hipGetSymbolAddress, once per device (each GPU holds its own copy at its own
+// address), and is the only form in which it reaches a kernel or a copy.
+constexpr size_t kStaticScratchBytes = size_t(256) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+unsigned char *g_scratch_ptr[kMaxScratchDevices];   // per device; null until first looked up
+
+// The static scratch's address on device `dev`, which must be current.  Null if it cannot be had
+// (a device index beyond the table, or a HIP error); aecct_decode_static then refuses.
+unsigned char *static_scratch_address(int dev) {
+  if (dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = (unsigned char *)p;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
 
 namespace {
 
@@ -690,6 +718,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.lds_max = (size_t)lds;
   if (aecct::set_layered_kernel_attributes(M) != hipSuccess || aecct::set_fused_kernel_attributes(M) != hipSuccess)
     return AECCT_ERR_DEVICE;
+  M.static_scratch = static_scratch_address(dev);
 
   // fused-path tables (built whenever the shape allows the fused kernel)
   FusedImage FI;
@@ -1037,6 +1066,26 @@ aecct_status aecct_decode(const aecct_model *model, const float *y, int64_t batc
   if (need && !workspace) return AECCT_ERR_INVALID_ARG;
   return decode_chunks(M, y, batch, bits, logits, (unsigned char *)workspace, chunk_words(M, batch),
                        (hipStream_t)stream);
+}
+
+aecct_status aecct_decode_static(const aecct_model *model, const float *y, int64_t batch, uint8_t *bits,
+                                 float *logits, void *stream) {
+  if (!model || batch < 0) return AECCT_ERR_INVALID_ARG;
+  if (batch == 0) return AECCT_OK;
+  if (!y || !bits) return AECCT_ERR_INVALID_ARG;
+  const Model &M = model->M;
+  const aecct_status dv = check_device(M);
+  if (dv != AECCT_OK) return dv;
+  int64_t cw = 1;
+  if (M.path != AECCT_PATH_FUSED) {
+    if (!M.static_scratch) return AECCT_ERR_DEVICE;
+    // the most words whose workspace fits the array
+    cw = (int64_t)(kStaticScratchBytes / ws_plan(M, 1).total);
+    while (cw > 0 && ws_plan(M, cw).total > kStaticScratchBytes) --cw;
+    if (cw < 1) return AECCT_ERR_WORKSPACE_TOO_SMALL;
+    if (cw > batch) cw = batch;
+  }
+  return decode_chunks(M, y, batch, bits, logits, M.static_scratch, cw, (hipStream_t)stream);
 }
 
 // ---- stage entry points --------------------------------------------------------------------
