@@ -110,11 +110,20 @@ def copy_calibration(mib: int = 512):
     print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4}))
 
 
-def cpu_baseline(H, w, y, budget_s=12.0):
-    import oracle
-    threads = min(os.cpu_count() or 1, 16)
-    om = oracle.OracleModel(H, w)
-    probe = 512
+def cpu_model() -> str:
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_rate(om, y, threads, budget_s):
+    """Words/s of the oracle at `threads` OpenMP threads on the first k words of y, k sized from a
+    probe so that the timed run takes about budget_s."""
+    probe = 64 if threads == 1 else 512
     t0 = time.perf_counter()
     om.decode(y[:probe], n_threads=threads)
     t1 = time.perf_counter() - t0
@@ -122,9 +131,24 @@ def cpu_baseline(H, w, y, budget_s=12.0):
     t0 = time.perf_counter()
     om.decode(y[:k], n_threads=threads)
     dt = time.perf_counter() - t0
-    return {"value": k / dt, "unit": "codewords/s", "cores": threads, "kind": "oracle",
+    return k / dt, k, dt
+
+
+def cpu_baseline(H, w, y, budget_s=10.0):
+    """The oracle (canonical fp32, as committed) on the host: at the host's thread share (at most
+    16, the CPU share of one GPU on these machines) and at one thread."""
+    import oracle
+    nproc = os.cpu_count() or 1
+    threads = min(nproc, 16)
+    om = oracle.OracleModel(H, w)
+    v, k, dt = _oracle_rate(om, y, threads, budget_s)
+    v1, k1, dt1 = _oracle_rate(om, y, 1, budget_s / 2)
+    return {"value": v, "unit": "codewords/s", "cores": threads, "kind": "oracle",
             "sample": f"first {k} of {y.shape[0]} words of the same workload, canonical fp32 oracle, "
-                      f"{threads} OpenMP threads, {dt:.1f} s"}
+                      f"{threads} OpenMP threads, {dt:.1f} s",
+            "cpu_model": cpu_model(), "host_nproc": nproc,
+            "one_thread": {"value": v1, "unit": "codewords/s", "cores": 1,
+                           "sample": f"first {k1} words, 1 thread, {dt1:.1f} s"}}
 
 
 def aap_import_bench(repeats: int = 5):
@@ -210,6 +234,10 @@ def main():
                     help="head-partitioned masks (the method) or the ECCT mask on every head")
     ap.add_argument("--first-ring-heads", type=int, default=None,
                     help="h_f, heads on the first-ring mask (default heads / 2; HPSA only)")
+    ap.add_argument("--act-scale", choices=("token", "word"), default="token",
+                    help="Eq. 2 scale per token (default) or per word")
+    ap.add_argument("--layered-attention", type=int, default=-1,
+                    help="layered path's Q/K/V + attention form: -1 auto, 0 unfused, 1 fp32 in LDS, 2 int16 in LDS")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (HBM counter calibration)")
     ap.add_argument("--aap-import", action="store_true",
@@ -239,13 +267,18 @@ def main():
         print("--first-ring-heads applies to the head-partitioned masks only", file=sys.stderr)
         sys.exit(2)
     cfg, H, G, w, y, x = build_workload(args.workload, attention=args.attention,
-                                        first_ring_heads=args.first_ring_heads)
+                                        first_ring_heads=args.first_ring_heads, act_scale=args.act_scale)
     default_split = args.attention == "hpsa" and w.first_ring_heads == cfg.heads // 2
     wl_name = cfg.name if default_split else (cfg.name + "_casa" if args.attention == "casa"
                                               else f"{cfg.name}_hf{w.first_ring_heads}")
+    if args.act_scale == "word":
+        wl_name += "_alpha_per_word"
+    if args.layered_attention != -1:
+        wl_name += f"_lattn{args.layered_attention}"
+    default_split = default_split and args.act_scale == "token" and args.layered_attention == -1
     B = cfg.batch
     dev = torch.device("cuda:0")
-    dec = P.Decoder(H, w, path=args.path)
+    dec = P.Decoder(H, w, path=args.path, layered_attention=args.layered_attention)
     yd = torch.from_numpy(y).to(dev)
     bits = torch.empty((B, cfg.n), dtype=torch.uint8, device=dev)
     logits = torch.empty((B, cfg.n), dtype=torch.float32, device=dev)
@@ -300,7 +333,8 @@ def main():
         "config": {"workload": wl_name, "code": "BCH(31,16)" if cfg.code == "bch" else cfg.code,
                    "n": cfg.n, "tokens": dec.L, "d": cfg.d, "layers": cfg.n_layers, "heads": cfg.heads,
                    "first_ring_heads": w.first_ring_heads if args.attention == "hpsa" else None,
-                   "attention": args.attention, "batch": B, "path": path,
+                   "attention": args.attention, "act_scale": args.act_scale, "batch": B, "path": path,
+                   "layered_attention": dec.info.layered_attention,
                    "wall_s_timed": t_wall},
         "roofline": roofline,
     }
