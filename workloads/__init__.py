@@ -8,11 +8,11 @@ quantisation), so that the CPU oracle and the GPU path can both be fed from it
 without sharing any of the method's code.
 """
 from .codes import hamming_7_4, bch_31_16, regular_ldpc_3_6, generator_from_parity, gf2_rank
-from .model import random_weights, random_spe_params, with_positional_table, ModelWeights
+from .model import random_weights, random_spe_params, random_qat_params, with_positional_table, ModelWeights
 from .channel import awgn_words
 from .configs import CONFIGS, WorkloadConfig, build_workload
 
 __all__ = [
     "hamming_7_4", "bch_31_16", "regular_ldpc_3_6", "generator_from_parity", "gf2_rank",
-    "random_weights", "random_spe_params", "with_positional_table", "ModelWeights", "awgn_words", "CONFIGS", "WorkloadConfig", "build_workload",
+    "random_weights", "random_spe_params", "random_qat_params", "with_positional_table", "ModelWeights", "awgn_words", "CONFIGS", "WorkloadConfig", "build_workload",
 ]

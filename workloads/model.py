@@ -123,3 +123,33 @@ def with_positional_table(w: ModelWeights, table: np.ndarray, d_pe: int) -> Mode
     embed = w.embed.copy()
     embed[:, w.d - d_pe:] = 0.0
     return replace(w, embed=embed, pos=np.ascontiguousarray(table, dtype=np.float32))
+
+
+def random_qat_params(n: int, m: int, d: int, n_layers: int, *, seed: int = 0, d_ff: int | None = None,
+                      latent_std: float | None = None, delta_spread: float = 0.05) -> dict:
+    """Seeded parameters of the quantisation-aware training phase (Section 6): latent fp32 weights
+    of the six in-block maps per layer ~ N(0, latent_std^2) (default 1/d, so that Eq. 1's scale
+    gamma*delta is of the size of the inference weights' 1/sqrt(d)), the learnable factors delta
+    = 1 + N(0, delta_spread^2) (the paper initialises them to one), and the other parameters drawn
+    as in random_weights.  fp32 arrays in a dict: embed, pos (None), w[kind], delta [N, 6],
+    b[kind], ln1_g, ln1_b, ln2_g, ln2_b, head_w1, head_b1, head_wo, head_bo."""
+    rng = np.random.default_rng(seed)
+    L = n + m
+    dff = 4 * d if d_ff is None else d_ff
+    sd = (1.0 / np.sqrt(d)) if latent_std is None else latent_std
+    f = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    p = {"embed": f(rng.standard_normal((L, d))), "pos": None, "w": {}, "b": {}}
+    for kind in LINEAR_KINDS:
+        kin, kout = (d, dff) if kind == "ff1" else (dff, d) if kind == "ff2" else (d, d)
+        p["w"][kind] = f(rng.standard_normal((n_layers, kin, kout)) * sd)
+        p["b"][kind] = f(0.1 * rng.standard_normal((n_layers, kout)))
+    p["delta"] = f(1.0 + delta_spread * rng.standard_normal((n_layers, 6)))
+    p["ln1_g"] = f(1.0 + 0.1 * rng.standard_normal((n_layers, d)))
+    p["ln1_b"] = f(0.1 * rng.standard_normal((n_layers, d)))
+    p["ln2_g"] = f(1.0 + 0.1 * rng.standard_normal((n_layers, d)))
+    p["ln2_b"] = f(0.1 * rng.standard_normal((n_layers, d)))
+    p["head_w1"] = f(rng.standard_normal(d) / np.sqrt(d))
+    p["head_b1"] = float(np.float32(0.1 * rng.standard_normal()))
+    p["head_wo"] = f(rng.standard_normal((L, n)) / np.sqrt(L))
+    p["head_bo"] = f(0.1 * rng.standard_normal(n))
+    return p
