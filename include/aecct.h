@@ -329,6 +329,73 @@ aecct_status aecct_decode_static(const aecct_model *model, const float *y, int64
  */
 aecct_status aecct_check_device_arith(uint64_t *counts);
 
+/* ------------------------------------------------------------------------------------------
+ * Quantisation-aware training step (Section 6, second phase; Section 4.1 Eq. 1-3): the forward
+ * pass of a model whose in-block linear maps are AAP linear layers over latent fp32 weights, the
+ * loss of the multiplicative noise, and the gradients of every parameter.  No optimiser: the
+ * caller applies the gradients.
+ *
+ * Forward, per word: the inference model's steps, with each map's ternary weights and scale
+ * recomputed from its current latent weights W and factor delta (Eq. 1: gamma = the 0.5 quantile
+ * of |W| with linear interpolation, evaluated in double and rounded to fp32; s = fp32(gamma
+ * delta); T = RoundClip(W / fp32(s + aap_eps), -1, 1), rounding half to even), int8 absmax codes
+ * per token for every map input (Eq. 2), Y = (Xhat T) s + b with Xhat = q alpha / 127 (Eq. 3),
+ * and the natural-base softmax of q.k / sqrt(d_h) over the same masks as inference.
+ * Loss: the mean over words and bits of BCE-with-logits(-f, z), z = [y x_s < 0]: f is the logit of
+ * "the sign of y is right", as bin(y f) is the decision.
+ * Backward: Eq. 1 and Eq. 2 pass gradients straight through their rounding; alpha and gamma are
+ * constants of the step; delta receives the gradient of s and of the division inside Eq. 1:
+ *   dW = s / (s + eps) Xhat^T dY,  d delta = gamma sum(G T) - s gamma / (s + eps)^2 sum(G W),
+ * with G = Xhat^T dY; dXhat = s dY T^T.
+ * fp32 throughout, deterministic (fixed reduction order).
+ * ---------------------------------------------------------------------------------------- */
+
+/* Parameters of a training step: DEVICE fp32 pointers, the layouts of aecct_weights, latent
+ * weights in place of the ternary ones.  Read only. */
+typedef struct aecct_train_params {
+  const float *embed;                       /* [L][d] */
+  const float *pos;                         /* [L][d] fixed positional rows (not trained), or NULL */
+  const float *w_q, *w_k, *w_v, *w_o;       /* [N][d][d] latent weights */
+  const float *w_ff1, *w_ff2;               /* [N][d][d_ff], [N][d_ff][d] */
+  const float *delta;                       /* [N][6] factors of Eq. 1's scale, aecct_linear order */
+  const float *b_q, *b_k, *b_v, *b_o, *b_ff1, *b_ff2;
+  const float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  const float *head_w1;                     /* [d] */
+  const float *head_b1;                     /* [1] */
+  const float *head_wo;                     /* [L][n] */
+  const float *head_bo;                     /* [n] */
+} aecct_train_params;
+
+/* Gradients: DEVICE fp32 outputs of the same shapes (every one written; no pos). */
+typedef struct aecct_train_grads {
+  float *embed;
+  float *w_q, *w_k, *w_v, *w_o, *w_ff1, *w_ff2;
+  float *delta;
+  float *b_q, *b_k, *b_v, *b_o, *b_ff1, *b_ff2;
+  float *ln1_g, *ln1_b, *ln2_g, *ln2_b;
+  float *head_w1, *head_b1, *head_wo, *head_bo;
+} aecct_train_grads;
+
+typedef struct aecct_trainer aecct_trainer;   /* opaque: the code's masks on the current device */
+
+/* Host H [m][n] as for aecct_create; d, n_layers, heads and the options first_ring_heads, d_ff,
+ * ln_eps and attention as there (path and layered_attention are ignored); act_scale_mode must be
+ * TOKEN.  aap_eps: the epsilon of Eq. 1, finite and >= 0.  Shapes as aecct_create.  Errors:
+ * INVALID_ARG, UNSUPPORTED, OUT_OF_MEMORY, DEVICE. */
+aecct_status aecct_train_create(const uint8_t *H, int32_t m, int32_t n, int32_t d, int32_t n_layers, int32_t heads,
+                                const aecct_options *opt, float aap_eps, aecct_trainer **out);
+/* Device workspace bytes of a step on `batch` words (host call). */
+aecct_status aecct_train_workspace_size(const aecct_trainer *tr, int64_t batch, size_t *bytes);
+/* One step on `batch` >= 1 words: y device fp32 [batch][n] channel outputs; xs device fp32
+ * [batch][n] transmitted +-1 words, or NULL for the all-zero codeword (the paper's training
+ * data); loss device fp32 [1]; grads written; workspace as sized above.  Asynchronous on stream,
+ * never allocates.  The current device must be the trainer's.  Errors: INVALID_ARG,
+ * WORKSPACE_TOO_SMALL, DEVICE. */
+aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params *params, const float *y,
+                              const float *xs, int64_t batch, const aecct_train_grads *grads, float *loss,
+                              void *workspace, size_t workspace_bytes, void *stream);
+void aecct_train_destroy(aecct_trainer *tr);
+
 /* Human-readable name of a status code (static string). */
 const char *aecct_status_string(aecct_status status);
 

@@ -41,20 +41,28 @@ def head_masks(H, heads, first_ring_heads, attention="hpsa"):
     return [M1 if h < first_ring_heads else M2 for h in range(heads)]
 
 
-def aap_ternary(W, delta, eps):
+def aap_ternary(W, delta, eps, margins=None):
     """Eq. 1 on latent weights: gamma = the 0.5 quantile of |W| (linear interpolation between
-    order statistics), s = gamma * delta, T = RoundClip(W / (s + eps), -1, 1) (half to even)."""
+    order statistics), s = gamma * delta, T = RoundClip(W / (s + eps), -1, 1) (half to even).
+    margins (dict or None) keeps the least distance of |W / (s + eps)| to the tie 1/2."""
     gamma = float(np.quantile(np.abs(W), 0.5))
     s = gamma * float(delta)
-    T = np.clip(np.rint(W / (s + eps)), -1.0, 1.0)
+    u = W / (s + eps)
+    if margins is not None:
+        margins["ternary"] = min(margins.get("ternary", np.inf), float(np.abs(np.abs(u) - 0.5).min()))
+    T = np.clip(np.rint(u), -1.0, 1.0)
     return T, s, gamma
 
 
-def quant_dequant(X):
-    """Eq. 2 per token row, then back to the value it stands for: q alpha / 127 (0 for alpha 0)."""
+def quant_dequant(X, margins=None):
+    """Eq. 2 per token row, then back to the value it stands for: q alpha / 127 (0 for alpha 0).
+    margins (dict or None) keeps the least distance of a code's x 127 / alpha to a tie k + 1/2."""
     a = np.abs(X).max(-1, keepdims=True)
     safe = np.where(a == 0, 1.0, a)
-    q = np.clip(np.rint(X * (127.0 / safe)), -127, 127)
+    u = X * (127.0 / safe)
+    if margins is not None:
+        margins["act"] = min(margins.get("act", np.inf), float(np.abs(u - (np.floor(u) + 0.5)).min()))
+    q = np.clip(np.rint(u), -127, 127)
     return np.where(a == 0, 0.0, q * safe / 127.0)
 
 
@@ -87,7 +95,7 @@ def _linear_bwd(dY, Xh, W, T, s, gamma, eps):
 
 
 def forward_backward(H, p, y, xs=None, *, heads=8, first_ring_heads=None, attention="hpsa", ln_eps=1e-5,
-                     aap_eps=1e-8, with_grads=True):
+                     aap_eps=1e-8, with_grads=True, margins=None):
     """One QAT step's loss and gradients on a batch.
 
     p: dict with embed [L, d], pos [L, d] or None, w[kind] [N, in, out] latent weights, delta
@@ -95,6 +103,8 @@ def forward_backward(H, p, y, xs=None, *, heads=8, first_ring_heads=None, attent
     head_wo [L, n], head_bo [n].  y: [B, n] channel outputs; xs: [B, n] transmitted +-1 words
     (None: the all-zero codeword, x_s = +1).
     Returns (loss, f [B, n], grads dict with the keys of p except pos; None without grads).
+    margins: a dict that receives the least distance of any rounding decision to its tie:
+    "act" (Eq. 2, in code units) and "ternary" (Eq. 1, |W| / (s + eps) against 1/2).
     """
     f64 = np.float64
     H = np.asarray(H, np.int64)
@@ -123,9 +133,9 @@ def forward_backward(H, p, y, xs=None, *, heads=8, first_ring_heads=None, attent
     cache = []
     for l in range(N):
         c = {"X": X}
-        tern = [aap_ternary(W[k][l], delta[l, i], aap_eps) for i, k in enumerate(KINDS)]
+        tern = [aap_ternary(W[k][l], delta[l, i], aap_eps, margins) for i, k in enumerate(KINDS)]
         c["tern"] = tern
-        Xh = quant_dequant(X)
+        Xh = quant_dequant(X, margins)
         c["Xh"] = Xh
         QKV = [(Xh @ tern[i][0]) * tern[i][1] + bias[k][l] for i, k in enumerate(("q", "k", "v"))]
         c["QKV"] = QKV
@@ -142,17 +152,17 @@ def forward_backward(H, p, y, xs=None, *, heads=8, first_ring_heads=None, attent
             P.append(Ph)
             O[:, :, sl] = Ph @ V[:, :, sl]
         c["P"], c["O"] = P, O
-        Oh = quant_dequant(O)
+        Oh = quant_dequant(O, margins)
         c["Oh"] = Oh
         R1 = X + (Oh @ tern[3][0]) * tern[3][1] + bias["o"][l]
         X1, c["ln1"] = layernorm_fwd(R1, ln["ln1_g"][l], ln["ln1_b"][l], ln_eps)
         c["X1"] = X1
-        X1h = quant_dequant(X1)
+        X1h = quant_dequant(X1, margins)
         c["X1h"] = X1h
         F = (X1h @ tern[4][0]) * tern[4][1] + bias["ff1"][l]
         c["F"] = F
         G = np.maximum(F, 0.0)
-        Gh = quant_dequant(G)
+        Gh = quant_dequant(G, margins)
         c["Gh"] = Gh
         R2 = X1 + (Gh @ tern[5][0]) * tern[5][1] + bias["ff2"][l]
         X, c["ln2"] = layernorm_fwd(R2, ln["ln2_g"][l], ln["ln2_b"][l], ln_eps)

@@ -55,6 +55,18 @@ class SpeParams(C.Structure):
                 ("w_red", _f32p), ("b_red", C.c_float)]
 
 
+_TRAIN_FIELDS = ["embed", "pos", "w_q", "w_k", "w_v", "w_o", "w_ff1", "w_ff2", "delta", "b_q", "b_k", "b_v", "b_o",
+                 "b_ff1", "b_ff2", "ln1_g", "ln1_b", "ln2_g", "ln2_b", "head_w1", "head_b1", "head_wo", "head_bo"]
+
+
+class TrainParams(C.Structure):
+    _fields_ = [(f, _vp) for f in _TRAIN_FIELDS]
+
+
+class TrainGrads(C.Structure):
+    _fields_ = [(f, _vp) for f in _TRAIN_FIELDS if f != "pos"]
+
+
 class AecctError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -113,6 +125,16 @@ def lib():
                                                     _f32p]
         L.aecct_spe_table.restype = C.c_int
         L.aecct_spe_table.argtypes = [_u8p, C.c_int32, C.c_int32, C.POINTER(SpeParams), C.c_int32, _f32p]
+        L.aecct_train_create.restype = C.c_int
+        L.aecct_train_create.argtypes = [_u8p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                         C.POINTER(Options), C.c_float, C.POINTER(_vp)]
+        L.aecct_train_destroy.restype = None
+        L.aecct_train_destroy.argtypes = [_vp]
+        L.aecct_train_workspace_size.restype = C.c_int
+        L.aecct_train_workspace_size.argtypes = [_vp, C.c_int64, C.POINTER(C.c_size_t)]
+        L.aecct_train_grad.restype = C.c_int
+        L.aecct_train_grad.argtypes = [_vp, C.POINTER(TrainParams), _vp, _vp, C.c_int64, C.POINTER(TrainGrads), _vp,
+                                       _vp, C.c_size_t, _vp]
         L.aecct_check_device_arith.restype = C.c_int
         L.aecct_check_device_arith.argtypes = [C.POINTER(C.c_uint64)]
         _lib = L
@@ -397,3 +419,75 @@ class Decoder:
         _check(lib().aecct_ternary_gemm(self._h, layer, kind, _ptr(a), rows, _ptr(acc), _stream_ptr(stream)),
                "aecct_ternary_gemm")
         return acc
+
+
+_TRAIN_KINDS = ("q", "k", "v", "o", "ff1", "ff2")
+
+
+class Trainer:
+    """The quantisation-aware training step (Section 6, second phase) on the current GPU for the
+    code of H: forward with Eq. 1 / Eq. 2 straight-through quantisation, the loss of the
+    multiplicative noise and every parameter's gradient, in the library's kernels.
+
+    Parameters and gradients are dicts of contiguous fp32 CUDA tensors with the keys of
+    `workloads.random_qat_params` (w and b are dicts by map kind; head_b1 a one-element tensor).
+    """
+
+    def __init__(self, H, d: int, n_layers: int, heads: int = 8, first_ring_heads: int = -1,
+                 attention: str = "hpsa", ln_eps: float = 1e-5, aap_eps: float = 1e-8):
+        H = _host(H, np.uint8)
+        m, n = H.shape
+        self.n, self.m, self.L, self.d, self.n_layers = n, m, n + m, d, n_layers
+        opt = Options(int(first_ring_heads), -1, float(ln_eps), PATH_AUTO,
+                      {"hpsa": ATTN_HPSA, "casa": ATTN_CASA}[attention], LAYERED_ATTN_AUTO, ACT_SCALE_TOKEN)
+        h = _vp()
+        _check(lib().aecct_train_create(H.ctypes.data_as(_u8p), m, n, int(d), int(n_layers), int(heads), C.byref(opt),
+                                        float(np.float32(aap_eps)), C.byref(h)), "aecct_train_create")
+        self._h = h
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().aecct_train_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_size(self, batch: int) -> int:
+        sz = C.c_size_t()
+        _check(lib().aecct_train_workspace_size(self._h, int(batch), C.byref(sz)), "aecct_train_workspace_size")
+        return sz.value
+
+    @staticmethod
+    def _flat(d: dict):
+        out = {}
+        for k, v in d.items():
+            if k in ("w", "b"):
+                for kind in _TRAIN_KINDS:
+                    out[f"{k}_{kind}"] = v[kind]
+            else:
+                out[k] = v
+        return out
+
+    def grad(self, params: dict, y, xs=None, stream=None):
+        """One step on the words y [B, n] (xs: transmitted +-1 words, None = all-zero codeword).
+        Returns (loss one-element tensor, gradients dict shaped like params, without pos)."""
+        import torch
+        B = y.shape[0]
+        flat = self._flat(params)
+        tp = TrainParams(**{f: _ptr(flat.get(f)) for f in _TRAIN_FIELDS})
+        grads = {k: (torch.empty_like(v) if k not in ("w", "b") else {kk: torch.empty_like(vv) for kk, vv in v.items()})
+                 for k, v in params.items() if k != "pos" and v is not None}
+        gflat = self._flat(grads)
+        tg = TrainGrads(**{f: _ptr(gflat[f]) for f, _ in TrainGrads._fields_})
+        need = self.workspace_size(B)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=y.device)
+        loss = torch.empty(1, dtype=torch.float32, device=y.device)
+        _check(lib().aecct_train_grad(self._h, C.byref(tp), _ptr(y), _ptr(xs), B, C.byref(tg), _ptr(loss),
+                                      _ptr(self._ws), self._ws.numel(), _stream_ptr(stream)), "aecct_train_grad")
+        return loss, grads

@@ -3,6 +3,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include <hip/hip_runtime.h>
 
@@ -97,6 +98,14 @@ struct Model {
   FusedTables fused;
 };
 
+// Tanner graph lists (host.cpp): check j's variables chk_idx[chk_ptr[j] .. chk_ptr[j+1]); per token
+// its first-ring (M1) and second-ring (M2, self included) neighbours, ascending.
+struct TannerLists {
+  std::vector<int32_t> chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx;
+};
+TannerLists tanner_lists(const uint8_t *H, int m, int n);
+void casa_union(TannerLists &T);   // M2 lists := M1 | M2 (every head on the ECCT mask)
+
 // ---- launchers (kernels_layered.hip) ---------------------------------------------------
 // Activation layouts.  Natural: X [rows][d] fp32 and its codes Xq [rows][d] by feature.  Lane
 // order (the decode with the token block, d = 64, 128): the token block holds feature 4 v + g
@@ -156,5 +165,61 @@ bool fused_supported(const Model &M);                 // shape check
 bool fused_fits(const Model &M, int nbr_words);       // LDS check with the built neighbour table
 hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
                         hipStream_t s);
+
+// ---- quantisation-aware training step (train.hip) ------------------------------------------
+// Eq. 1 of one latent matrix: gamma, scale = fp32(gamma * delta) and its ternary copy t (fp32).
+struct TrainAapJob {
+  const float *w;
+  float *t;
+  int64_t count;
+  const float *delta;
+  float *gamma, *scale;
+};
+// The straight-through Eq. 1 gradients of one matrix from G = Xh^T dY held in dw.
+struct TrainDeltaJob {
+  float *dw;
+  const float *w, *t;
+  int64_t count;
+  const float *gamma, *scale;
+  float *ddelta;
+};
+struct TrainAttn {
+  const float *qkv;     // [rows][3d] Q | K | V (queries unscaled)
+  int64_t rows;
+  int L, d, heads, hf;
+  const int32_t *m1_ptr, *m1_idx, *m2_ptr, *m2_idx;
+  float *o, *lse;       // [rows][d] output, [rows][heads] log-sum-exp of the scores
+  const float *dout;    // [rows][d] gradient of O (backward)
+  float *dqkv;          // [rows][3d] gradients of Q | K | V (backward)
+  float *Dv;            // [rows][heads] dO . O (backward)
+};
+// the six maps of one layer per launch, passed by value
+struct TrainAapJobs { TrainAapJob j[6]; };
+struct TrainDeltaJobs { TrainDeltaJob j[6]; };
+hipError_t train_aap(const TrainAapJobs &jobs, float eps, hipStream_t s);
+hipError_t train_delta_grad(const TrainDeltaJobs &jobs, float eps, hipStream_t s);
+hipError_t train_embed(const float *y, int64_t rows, int n, int L, int d, const int32_t *chk_ptr,
+                       const int32_t *chk_idx, const float *E, const float *P, float *x, float *t, hipStream_t s);
+hipError_t train_quant(const float *x, int64_t rows, int K, bool relu, float *xh, hipStream_t s);
+// C[M][N] = (accumulate ? C : 0) + scale (op(A) op(B)) + bias; ta: A stored [K][M]; tb: B stored [N][K].
+// part: scratch of part_floats floats for split reductions over K.
+hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc,
+                      int64_t M, int64_t N, int64_t K, const float *scale, const float *bias, bool accumulate,
+                      float *part, int64_t part_floats, int cu_count, hipStream_t s);
+// which: 0 forward (o, lse), 1 query gradients (dqkv's Q third, Dv), 2 key and value gradients
+hipError_t train_attention(int which, int dh, const TrainAttn &a, hipStream_t s);
+hipError_t train_ln_fwd(const float *a, const float *b, int64_t rows, int d, const float *g, const float *beta, float eps,
+                        float *out, float *xn, float *rho, hipStream_t s);
+hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const float *rho, int64_t rows, int d,
+                        float *dR, hipStream_t s);
+// out[c] (+)= sum_r A[r][c] (B[r][c] if B) (w[r] if w), rows of A lda apart, B dense [rows][C]
+hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
+                        bool accumulate, float *part, int64_t part_floats, hipStream_t s);
+hipError_t train_relu_bwd(float *dg, const float *f, int64_t count, hipStream_t s);
+hipError_t train_rowdot(const float *x, int64_t rows, int d, const float *w1, const float *b1, float *z, hipStream_t s);
+hipError_t train_outer(const float *dz, int64_t rows, const float *w1, int d, float *dx, hipStream_t s);
+hipError_t train_loss(const float *f, const float *y, const float *xs, int64_t count, float *df, float *part,
+                      float *loss, hipStream_t s);
+hipError_t train_embed_grad(const float *t, const float *dx, int64_t words, int L, int d, float *de, hipStream_t s);
 
 }  // namespace aecct

@@ -572,6 +572,58 @@ aecct_status from_hip(hipError_t e) {
 
 }  // namespace
 
+namespace aecct {
+
+// Tanner graph lists and HPSA masks (Section 4.2): M1 = neighbours, M2 = nodes two steps away
+// plus the node itself; each list ascending.
+TannerLists tanner_lists(const uint8_t *H, int m, int n) {
+  const int L = n + m;
+  TannerLists T;
+  std::vector<std::vector<int>> adj(L);
+  T.chk_ptr.assign(m + 1, 0);
+  for (int j = 0; j < m; ++j) {
+    for (int i = 0; i < n; ++i)
+      if (H[(size_t)j * n + i]) {
+        T.chk_idx.push_back(i);
+        adj[i].push_back(n + j);
+        adj[n + j].push_back(i);
+      }
+    T.chk_ptr[j + 1] = (int32_t)T.chk_idx.size();
+  }
+  T.m1_ptr.assign(L + 1, 0);
+  T.m2_ptr.assign(L + 1, 0);
+  std::vector<int> mark(L, -1);
+  for (int a = 0; a < L; ++a) {
+    std::vector<int> nb = adj[a];
+    std::sort(nb.begin(), nb.end());
+    for (int v : nb) T.m1_idx.push_back(v);
+    T.m1_ptr[a + 1] = (int32_t)T.m1_idx.size();
+    for (int k : adj[a])
+      for (int b : adj[k]) mark[b] = a;
+    for (int b = 0; b < L; ++b)
+      if (mark[b] == a) T.m2_idx.push_back(b);
+    T.m2_ptr[a + 1] = (int32_t)T.m2_idx.size();
+  }
+  return T;
+}
+
+// The ECCT mask of every head under CASA (Section 3): the second-ring lists become the merged,
+// ascending union of both rings.
+void casa_union(TannerLists &T) {
+  const int L = (int)T.m1_ptr.size() - 1;
+  std::vector<int32_t> u_ptr(L + 1, 0), u_idx;
+  u_idx.reserve(T.m1_idx.size() + T.m2_idx.size());
+  for (int a = 0; a < L; ++a) {
+    std::merge(T.m1_idx.begin() + T.m1_ptr[a], T.m1_idx.begin() + T.m1_ptr[a + 1], T.m2_idx.begin() + T.m2_ptr[a],
+               T.m2_idx.begin() + T.m2_ptr[a + 1], std::back_inserter(u_idx));
+    u_ptr[a + 1] = (int32_t)u_idx.size();
+  }
+  T.m2_ptr.swap(u_ptr);
+  T.m2_idx.swap(u_idx);
+}
+
+}  // namespace aecct
+
 extern "C" {
 
 const char *aecct_status_string(aecct_status s) {
@@ -649,33 +701,9 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
       (path_req == AECCT_PATH_FUSED || lattn_req == AECCT_LAYERED_ATTN_LDS_F32 || lattn_req == AECCT_LAYERED_ATTN_LDS_I16))
     return AECCT_ERR_UNSUPPORTED;
 
-  // Tanner graph lists and HPSA masks (Section 4.2): M1 = neighbours, M2 = nodes two
-  // steps away plus the node itself; each list ascending.
-  std::vector<std::vector<int>> adj(L);
-  std::vector<int32_t> chk_ptr(m + 1, 0), chk_idx;
-  chk_idx.reserve(E);
-  for (int j = 0; j < m; ++j) {
-    for (int i = 0; i < n; ++i)
-      if (H[(size_t)j * n + i]) {
-        chk_idx.push_back(i);
-        adj[i].push_back(n + j);
-        adj[n + j].push_back(i);
-      }
-    chk_ptr[j + 1] = (int32_t)chk_idx.size();
-  }
-  std::vector<int32_t> m1_ptr(L + 1, 0), m1_idx, m2_ptr(L + 1, 0), m2_idx;
-  std::vector<int> mark(L, -1);
-  for (int a = 0; a < L; ++a) {
-    std::vector<int> nb = adj[a];
-    std::sort(nb.begin(), nb.end());
-    for (int v : nb) m1_idx.push_back(v);
-    m1_ptr[a + 1] = (int32_t)m1_idx.size();
-    for (int k : adj[a])
-      for (int b : adj[k]) mark[b] = a;
-    for (int b = 0; b < L; ++b)
-      if (mark[b] == a) m2_idx.push_back(b);
-    m2_ptr[a + 1] = (int32_t)m2_idx.size();
-  }
+  aecct::TannerLists TL = aecct::tanner_lists(H, m, n);
+  std::vector<int32_t> &chk_ptr = TL.chk_ptr, &chk_idx = TL.chk_idx, &m1_ptr = TL.m1_ptr, &m1_idx = TL.m1_idx,
+                       &m2_ptr = TL.m2_ptr, &m2_idx = TL.m2_idx;
 
   Model M{};
   M.n = n; M.m = m; M.L = L; M.d = d; M.n_layers = n_layers; M.heads = heads; M.hf = hf; M.dff = dff;
@@ -686,15 +714,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.attention = attention;
   if (attention == AECCT_ATTN_CASA) {
     // every head reads the union of the two rings: it takes the second-ring list slot, h_f = 0
-    std::vector<int32_t> u_ptr(L + 1, 0), u_idx;
-    u_idx.reserve(m1_idx.size() + m2_idx.size());
-    for (int a = 0; a < L; ++a) {
-      std::merge(m1_idx.begin() + m1_ptr[a], m1_idx.begin() + m1_ptr[a + 1], m2_idx.begin() + m2_ptr[a],
-                 m2_idx.begin() + m2_ptr[a + 1], std::back_inserter(u_idx));
-      u_ptr[a + 1] = (int32_t)u_idx.size();
-    }
-    m2_ptr.swap(u_ptr);
-    m2_idx.swap(u_idx);
+    aecct::casa_union(TL);
     M.hf = 0;
   }
   M.head_b1 = w->head_b1;

@@ -1,0 +1,688 @@
+// Quantisation-aware training step of AECCT on the GPU: the second training phase of Section 6,
+// in which the encoder's in-block linear maps are AAP linear layers (Section 4.1) over latent
+// fp32 weights.  Forward with Eq. 1 ternarisation of the current weights and Eq. 2 absmax int8
+// activations (both passing gradients straight through their rounding), the cross entropy of the
+// multiplicative noise, and the backward pass to every parameter.  fp32 throughout; every
+// reduction runs in a fixed order (split partial sums reduced in index order), so a step is
+// deterministic.
+//
+// Layouts: activations row-major [rows][features] with row b * L + r for token r of word b;
+// weights [in][out] as in the inference ABI.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "aecct_internal.h"
+#include "device_common.h"
+
+namespace aecct {
+namespace train {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// ------------------------------------------------------------------------------------------
+// Eq. 1 on the current latent weights, one block per matrix: gamma = Percentile(|W|, 0.5) (the
+// order statistics at floor(pos) and floor(pos) + 1 for pos = (count - 1) / 2, interpolated in
+// double and rounded once to fp32), s = fp32(gamma * delta), T = RoundClip(W / fp32(s + eps),
+// -1, 1) with rounding half to even (a zero denominator maps a weight to its sign).  The order
+// statistics come from a radix selection over the bit patterns of |W| (non-negative floats order
+// like their bits), one 8-bit digit per pass.
+// ------------------------------------------------------------------------------------------
+using AapJob = TrainAapJob;
+
+__device__ uint32_t radix_select(const float *w, int64_t count, uint32_t k, uint32_t *hist, uint32_t *pick) {
+  uint32_t prefix = 0, mask = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = threadIdx.x; b < 256; b += kThreads) hist[b] = 0;
+    __syncthreads();
+    for (int64_t e = threadIdx.x; e < count; e += kThreads) {
+      const uint32_t key = __float_as_uint(fabsf(w[e]));
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t b = 0, kk = k;
+      while (b < 255 && kk >= hist[b]) kk -= hist[b++];
+      pick[0] = b;
+      pick[1] = kk;
+    }
+    __syncthreads();
+    prefix |= pick[0] << shift;
+    mask |= 255u << shift;
+    k = pick[1];
+    __syncthreads();
+  }
+  return prefix;
+}
+
+__global__ __launch_bounds__(kThreads) void k_aap(TrainAapJobs jobs, float eps) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t pick[2];
+  __shared__ float sden;
+  const AapJob J = jobs.j[blockIdx.x];
+  const uint32_t lo = (uint32_t)((J.count - 1) / 2);
+  const uint32_t a_lo = radix_select(J.w, J.count, lo, hist, pick);
+  const uint32_t a_hi = (int64_t)lo + 1 < J.count ? radix_select(J.w, J.count, lo + 1, hist, pick) : a_lo;
+  if (threadIdx.x == 0) {
+    const double pos = 0.5 * (double)(J.count - 1);
+    const double frac = pos - (double)lo;
+    const double flo = (double)__uint_as_float(a_lo), fhi = (double)__uint_as_float(a_hi);
+    const float gamma = (float)(flo + frac * (fhi - flo));
+    const float s = gamma * J.delta[0];
+    *J.gamma = gamma;
+    *J.scale = s;
+    sden = s + eps;
+  }
+  __syncthreads();
+  const float den = sden;
+  for (int64_t e = threadIdx.x; e < J.count; e += kThreads) {
+    const float x = J.w[e];
+    float r = den == 0.0f ? (x > 0.0f ? 1.0f : (x < 0.0f ? -1.0f : 0.0f)) : rintf(x / den);
+    J.t[e] = fminf(1.0f, fmaxf(-1.0f, r));
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Pre-processing and embedding (Section 3): t = [|y|, 1 - 2 s(y)], X = t E (+ P); one wavefront
+// per token row.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_embed(const float *y, int64_t rows, int n, int L, int d,
+                                                    const int32_t *chk_ptr, const int32_t *chk_idx, const float *E,
+                                                    const float *P, float *x, float *tv) {
+  const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const int64_t w = r / L;
+  const int i = (int)(r - w * L);
+  const float *yw = y + w * n;
+  float t;
+  if (i < n) {
+    t = fabsf(yw[i]);
+  } else {
+    int s = 0;
+    for (int e = chk_ptr[i - n]; e < chk_ptr[i - n + 1]; ++e) s ^= yw[chk_idx[e]] < 0.0f ? 1 : 0;
+    t = s ? -1.0f : 1.0f;
+  }
+  for (int c = lane; c < d; c += 64) x[r * d + c] = fmaf(t, E[(int64_t)i * d + c], P ? P[(int64_t)i * d + c] : 0.0f);
+  if (lane == 0) tv[r] = t;
+}
+
+// Eq. 2 per token row and the value the codes stand for, q alpha / 127 (0 when alpha = 0); of
+// max(x, 0) when RELU.  One wavefront per row.
+template <bool RELU>
+__global__ __launch_bounds__(kThreads) void k_quant_dequant(const float *x, int64_t rows, int K, float *xh) {
+  const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float *xr = x + r * K;
+  float a = 0.0f;
+  for (int c = lane; c < K; c += 64) {
+    const float v = RELU ? fmaxf(xr[c], 0.0f) : xr[c];
+    a = fmaxf(a, fabsf(v));
+  }
+  a = wave_max(a);
+  const float inv = inv127(a);
+  for (int c = lane; c < K; c += 64) {
+    const float v = RELU ? fmaxf(xr[c], 0.0f) : xr[c];
+    xh[r * K + c] = a == 0.0f ? 0.0f : (float)quant_code(v, inv) * a / 127.0f;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// fp32 GEMM: C[M][N] = beta C + scale (op(A) op(B)) + bias[N], op(A) = A [M][K] (lda) or, with TA,
+// the transpose of A stored [K][M]; op(B) = B [K][N] (ldb) or, with TB, the transpose of B stored
+// [N][K].  64 x 64 output tiles, 16-deep K steps through LDS, 4 x 4 outputs per thread, FMAs in
+// ascending k.  With gridDim.z > 1 each z takes one contiguous k range and writes its raw sum to
+// part[z][M][N]; k_gemm_reduce then adds the ranges in index order and applies the epilogue.
+// ------------------------------------------------------------------------------------------
+struct GemmF32 {
+  const float *A, *B;
+  float *C;
+  int64_t M, N, K;
+  int64_t lda, ldb, ldc;
+  int64_t kchunk;
+  const float *scale;   // device scalar or null (1)
+  const float *bias;    // [N] or null
+  int beta;             // 1: accumulate into C
+  float *part;          // [splits][M][N] when split
+};
+
+template <bool TA, bool TB>
+__global__ __launch_bounds__(kThreads) void k_gemm(GemmF32 g) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const int64_t kb = (int64_t)blockIdx.z * g.kchunk, ke = std::min<int64_t>(g.K, kb + g.kchunk);
+  float acc[4][4] = {};
+  for (int64_t k0 = kb; k0 < ke; k0 += 16) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + kThreads * u;
+      int mm, kk;
+      if (TA) { kk = idx >> 6; mm = idx & 63; } else { mm = idx >> 4; kk = idx & 15; }
+      const int64_t gm = m0 + mm, gk = k0 + kk;
+      float v = 0.0f;
+      if (gm < g.M && gk < ke) v = TA ? g.A[gk * g.lda + gm] : g.A[gm * g.lda + gk];
+      As[kk][mm] = v;
+      int nn;
+      if (TB) { nn = idx >> 4; kk = idx & 15; } else { kk = idx >> 6; nn = idx & 63; }
+      const int64_t gn = n0 + nn, gk2 = k0 + kk;
+      float w = 0.0f;
+      if (gn < g.N && gk2 < ke) w = TB ? g.B[gn * g.ldb + gk2] : g.B[gk2 * g.ldb + gn];
+      Bs[kk][nn] = w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][4 * ty + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][4 * tx + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  const bool split = gridDim.z > 1;
+  const float sc = g.scale ? *g.scale : 1.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t r = m0 + 4 * ty + i;
+    if (r >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t c = n0 + 4 * tx + j;
+      if (c >= g.N) continue;
+      if (split) {
+        g.part[((int64_t)blockIdx.z * g.M + r) * g.N + c] = acc[i][j];
+      } else {
+        float v = sc * acc[i][j] + (g.bias ? g.bias[c] : 0.0f);
+        if (g.beta) v += g.C[r * g.ldc + c];
+        g.C[r * g.ldc + c] = v;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_gemm_reduce(GemmF32 g, int splits) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= g.M * g.N) return;
+  const int64_t r = e / g.N, c = e - r * g.N;
+  float s = 0.0f;
+  for (int z = 0; z < splits; ++z) s += g.part[(int64_t)z * g.M * g.N + e];
+  float v = (g.scale ? *g.scale : 1.0f) * s + (g.bias ? g.bias[c] : 0.0f);
+  if (g.beta) v += g.C[r * g.ldc + c];
+  g.C[r * g.ldc + c] = v;
+}
+
+// ------------------------------------------------------------------------------------------
+// Head-partitioned attention (Section 4.2) of the training step: one thread per (row, head) over
+// the row's neighbour list (first ring for heads below h_f, else the second-ring list, which
+// holds the union of both rings under CASA); natural-base softmax of q.k / sqrt(d_h) with the
+// maximum subtracted.  Forward stores O and the row's log-sum-exp; the backward recomputes
+// p_ij = exp(s_ij - lse_i).  The masks are symmetric, so the key and value gradients are gathered
+// per key row over its own list, without atomics.
+// ------------------------------------------------------------------------------------------
+using AttnT = TrainAttn;
+
+template <int DH>
+__device__ __forceinline__ float dot_dh(const float *a, const float *b) {
+  float s = a[0] * b[0];
+#pragma unroll
+  for (int t = 1; t < DH; ++t) s = fmaf(a[t], b[t], s);
+  return s;
+}
+
+template <int DH>
+__global__ __launch_bounds__(kThreads) void k_attn_fwd(AttnT p) {
+  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (gid >= p.rows * p.heads) return;
+  const int64_t row = gid / p.heads;
+  const int h = (int)(gid - row * p.heads);
+  const int64_t base = (row / p.L) * p.L;
+  const int i = (int)(row - base);
+  const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr, *idx = h < p.hf ? p.m1_idx : p.m2_idx;
+  const int d = p.d, ld = 3 * d;
+  const float kappa = 1.0f / sqrtf((float)DH);
+  float q[DH];
+#pragma unroll
+  for (int t = 0; t < DH; ++t) q[t] = p.qkv[row * ld + h * DH + t];
+  float mu = -INFINITY;
+  for (int e = ptr[i]; e < ptr[i + 1]; ++e)
+    mu = fmaxf(mu, dot_dh<DH>(q, p.qkv + (base + idx[e]) * ld + d + h * DH) * kappa);
+  float S = 0.0f, acc[DH] = {};
+  for (int e = ptr[i]; e < ptr[i + 1]; ++e) {
+    const int64_t j = base + idx[e];
+    const float pe = expf(dot_dh<DH>(q, p.qkv + j * ld + d + h * DH) * kappa - mu);
+    S += pe;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) acc[t] = fmaf(pe, p.qkv[j * ld + 2 * d + h * DH + t], acc[t]);
+  }
+#pragma unroll
+  for (int t = 0; t < DH; ++t) p.o[row * d + h * DH + t] = acc[t] / S;
+  p.lse[row * p.heads + h] = mu + logf(S);
+}
+
+template <int DH>
+__global__ __launch_bounds__(kThreads) void k_attn_bwd_q(AttnT p) {
+  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (gid >= p.rows * p.heads) return;
+  const int64_t row = gid / p.heads;
+  const int h = (int)(gid - row * p.heads);
+  const int64_t base = (row / p.L) * p.L;
+  const int i = (int)(row - base);
+  const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr, *idx = h < p.hf ? p.m1_idx : p.m2_idx;
+  const int d = p.d, ld = 3 * d;
+  const float kappa = 1.0f / sqrtf((float)DH);
+  float q[DH], go[DH], dq[DH] = {};
+#pragma unroll
+  for (int t = 0; t < DH; ++t) {
+    q[t] = p.qkv[row * ld + h * DH + t];
+    go[t] = p.dout[row * d + h * DH + t];
+  }
+  const float D = dot_dh<DH>(go, p.o + row * d + h * DH);
+  const float lse = p.lse[row * p.heads + h];
+  for (int e = ptr[i]; e < ptr[i + 1]; ++e) {
+    const int64_t j = base + idx[e];
+    const float *kj = p.qkv + j * ld + d + h * DH;
+    const float pij = expf(dot_dh<DH>(q, kj) * kappa - lse);
+    const float ds = pij * (dot_dh<DH>(go, p.qkv + j * ld + 2 * d + h * DH) - D) * kappa;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) dq[t] = fmaf(ds, kj[t], dq[t]);
+  }
+#pragma unroll
+  for (int t = 0; t < DH; ++t) p.dqkv[row * ld + h * DH + t] = dq[t];
+  p.Dv[row * p.heads + h] = D;
+}
+
+template <int DH>
+__global__ __launch_bounds__(kThreads) void k_attn_bwd_kv(AttnT p) {
+  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (gid >= p.rows * p.heads) return;
+  const int64_t row = gid / p.heads;   // the key / value row j
+  const int h = (int)(gid - row * p.heads);
+  const int64_t base = (row / p.L) * p.L;
+  const int j = (int)(row - base);
+  const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr, *idx = h < p.hf ? p.m1_idx : p.m2_idx;
+  const int d = p.d, ld = 3 * d;
+  const float kappa = 1.0f / sqrtf((float)DH);
+  float k[DH], v[DH], dk[DH] = {}, dv[DH] = {};
+#pragma unroll
+  for (int t = 0; t < DH; ++t) {
+    k[t] = p.qkv[row * ld + d + h * DH + t];
+    v[t] = p.qkv[row * ld + 2 * d + h * DH + t];
+  }
+  for (int e = ptr[j]; e < ptr[j + 1]; ++e) {    // rows i whose list holds j (symmetric masks)
+    const int64_t i = base + idx[e];
+    const float *qi = p.qkv + i * ld + h * DH;
+    const float *gi = p.dout + i * d + h * DH;
+    const float pij = expf(dot_dh<DH>(qi, k) * kappa - p.lse[i * p.heads + h]);
+    const float ds = pij * (dot_dh<DH>(gi, v) - p.Dv[i * p.heads + h]) * kappa;
+#pragma unroll
+    for (int t = 0; t < DH; ++t) {
+      dv[t] = fmaf(pij, gi[t], dv[t]);
+      dk[t] = fmaf(ds, qi[t], dk[t]);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < DH; ++t) {
+    p.dqkv[row * ld + d + h * DH + t] = dk[t];
+    p.dqkv[row * ld + 2 * d + h * DH + t] = dv[t];
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// LayerNorm of the Post-LN block (Section 6), one wavefront per row: forward of R = a + b, keeping
+// the normalised row xn and 1 / sqrt(var + eps); backward dR = rho (dxn - mean dxn - xn mean(dxn
+// xn)) with dxn = dy g.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_ln_fwd(const float *a, const float *b, int64_t rows, int d,
+                                                     const float *g, const float *beta, float eps, float *out,
+                                                     float *xn, float *rho) {
+  const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  float v[2], s = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    v[u] = c < d ? a[r * d + c] + b[r * d + c] : 0.0f;
+    s += v[u];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    if (c < d) q = fmaf(v[u] - mean, v[u] - mean, q);
+  }
+  const float rh = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    if (c >= d) continue;
+    const float x = (v[u] - mean) * rh;
+    xn[r * d + c] = x;
+    out[r * d + c] = fmaf(x, g[c], beta[c]);
+  }
+  if (lane == 0) rho[r] = rh;
+}
+
+__global__ __launch_bounds__(kThreads) void k_ln_bwd(const float *dy, const float *g, const float *xn,
+                                                     const float *rho, int64_t rows, int d, float *dR) {
+  const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  float dx[2], x[2], s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    dx[u] = c < d ? dy[r * d + c] * g[c] : 0.0f;
+    x[u] = c < d ? xn[r * d + c] : 0.0f;
+    s1 += dx[u];
+    s2 = fmaf(dx[u], x[u], s2);
+  }
+  const float m1 = wave_sum(s1) / (float)d, m2 = wave_sum(s2) / (float)d;
+  const float rh = rho[r];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    if (c < d) dR[r * d + c] = rh * (dx[u] - m1 - x[u] * m2);
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Column sums over rows, deterministic in two passes: out[c] (+)= sum_r A[r][c] (x B[r][c]) (x w[r]).
+// Pass one: block (chunk, column group) sums its rows in ascending order; pass two: the chunks
+// in ascending order.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_colsum_part(const float *A, const float *Bm, const float *w, int64_t rows,
+                                                          int C, int64_t lda, int64_t chunk, float *part) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  if (c >= C) return;
+  const int64_t r0 = (int64_t)blockIdx.y * chunk, r1 = std::min<int64_t>(rows, r0 + chunk);
+  float s = 0.0f;
+  for (int64_t r = r0; r < r1; ++r) {
+    float v = A[r * lda + c];
+    if (Bm) v *= Bm[r * C + c];
+    if (w) v *= w[r];
+    s += v;
+  }
+  part[(int64_t)blockIdx.y * C + c] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void k_colsum_final(const float *part, int chunks, int C, float *out, int accumulate) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  if (c >= C) return;
+  float s = 0.0f;
+  for (int z = 0; z < chunks; ++z) s += part[(int64_t)z * C + c];
+  out[c] = accumulate ? out[c] + s : s;
+}
+
+// ------------------------------------------------------------------------------------------
+// Small elementwise steps.
+// ------------------------------------------------------------------------------------------
+// ReLU backward (the Eq. 2 code of the hidden row passes the gradient straight through)
+__global__ __launch_bounds__(kThreads) void k_relu_bwd(float *dg, const float *f, int64_t count) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e < count && !(f[e] > 0.0f)) dg[e] = 0.0f;
+}
+
+// z = X w1 + b1 per row (Section 3 head, W_{d->1}); one wavefront per row
+__global__ __launch_bounds__(kThreads) void k_rowdot(const float *x, int64_t rows, int d, const float *w1,
+                                                     const float *b1, float *z) {
+  const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  float s = 0.0f;
+  for (int c = lane; c < d; c += 64) s = fmaf(x[r * d + c], w1[c], s);
+  s = wave_sum(s);
+  if (lane == 0) z[r] = s + b1[0];
+}
+
+// dX = dz w1^T (the head's W_{d->1} backward)
+__global__ __launch_bounds__(kThreads) void k_outer(const float *dz, int64_t rows, const float *w1, int d, float *dx) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= rows * d) return;
+  dx[e] = dz[e / d] * w1[e % d];
+}
+
+// Loss of the multiplicative noise (Section 6): target z = [y x_s < 0] (x_s = +1 if xs is null),
+// l = softplus(-f) + z f = BCE-with-logits(-f, z); df = (z - sigmoid(-f)) / count.  Per-block
+// sums of l in part[blockIdx].
+__global__ __launch_bounds__(kThreads) void k_loss(const float *f, const float *y, const float *xs, int64_t count,
+                                                   float inv_count, float *df, float *part) {
+  __shared__ float red[kThreads / 64];
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  float l = 0.0f;
+  if (e < count) {
+    const float fv = f[e];
+    const float sg = xs ? xs[e] : 1.0f;
+    const float z = y[e] * sg < 0.0f ? 1.0f : 0.0f;
+    const float nf = -fv;
+    l = fmaxf(nf, 0.0f) + log1pf(expf(-fabsf(nf))) + z * fv;
+    const float sig = 1.0f / (1.0f + expf(fv));          // sigmoid(-f)
+    df[e] = (z - sig) * inv_count;
+  }
+  l = wave_sum(l);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = l;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float s = 0.0f;
+    for (int k = 0; k < kThreads / 64; ++k) s += red[k];
+    part[blockIdx.x] = s;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_loss_final(const float *part, int n, float inv_count, float *loss) {
+  if (threadIdx.x != 0) return;
+  float s = 0.0f;
+  for (int k = 0; k < n; ++k) s += part[k];
+  *loss = s * inv_count;
+}
+
+// dE[i][c] = sum_b t[b L + i] dX[b L + i][c] (the embedding is t_i E_i)
+__global__ __launch_bounds__(kThreads) void k_embed_grad(const float *t, const float *dx, int64_t words, int L, int d,
+                                                         float *de) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)L * d) return;
+  const int64_t i = e / d, c = e - i * d;
+  float s = 0.0f;
+  for (int64_t b = 0; b < words; ++b) s = fmaf(t[b * L + i], dx[(b * L + i) * d + c], s);
+  de[e] = s;
+}
+
+// The straight-through Eq. 1 gradients of one matrix, one block per matrix: G = Xh^T dY arrives in
+// dW; dW = G s / (s + eps) and d delta = gamma sum(G T) - s gamma / (s + eps)^2 sum(G W).
+using DeltaJob = TrainDeltaJob;
+
+__global__ __launch_bounds__(kThreads) void k_delta_grad(TrainDeltaJobs jobs, float eps) {
+  __shared__ float r1[kThreads / 64], r2[kThreads / 64];
+  const DeltaJob J = jobs.j[blockIdx.x];
+  const float s = *J.scale, gamma = *J.gamma;
+  const float fac = s / (s + eps);
+  float a = 0.0f, b = 0.0f;
+  for (int64_t e = threadIdx.x; e < J.count; e += kThreads) {
+    const float gv = J.dw[e];
+    a = fmaf(gv, J.t[e], a);
+    b = fmaf(gv, J.w[e], b);
+    J.dw[e] = gv * fac;
+  }
+  a = wave_sum(a);
+  b = wave_sum(b);
+  if ((threadIdx.x & 63) == 0) {
+    r1[threadIdx.x >> 6] = a;
+    r2[threadIdx.x >> 6] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float sa = 0.0f, sb = 0.0f;
+    for (int k = 0; k < kThreads / 64; ++k) {
+      sa += r1[k];
+      sb += r2[k];
+    }
+    const float den = s + eps;
+    *J.ddelta = gamma * sa - s * gamma / (den * den) * sb;
+  }
+}
+
+}  // namespace train
+
+// ------------------------------------------------------------------------------------------
+// launch helpers (declared in aecct_internal.h)
+// ------------------------------------------------------------------------------------------
+namespace {
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+}
+
+hipError_t train_aap(const TrainAapJobs &jobs, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(train::k_aap, dim3(6), dim3(train::kThreads), 0, s, jobs, eps);
+  return hipGetLastError();
+}
+
+hipError_t train_delta_grad(const TrainDeltaJobs &jobs, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(train::k_delta_grad, dim3(6), dim3(train::kThreads), 0, s, jobs, eps);
+  return hipGetLastError();
+}
+
+hipError_t train_embed(const float *y, int64_t rows, int n, int L, int d, const int32_t *chk_ptr,
+                       const int32_t *chk_idx, const float *E, const float *P, float *x, float *t, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_embed, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, y, rows, n, L, d, chk_ptr,
+                     chk_idx, E, P, x, t);
+  return hipGetLastError();
+}
+
+hipError_t train_quant(const float *x, int64_t rows, int K, bool relu, float *xh, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (relu) hipLaunchKernelGGL(train::k_quant_dequant<true>, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, x, rows, K, xh);
+  else hipLaunchKernelGGL(train::k_quant_dequant<false>, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, x, rows, K, xh);
+  return hipGetLastError();
+}
+
+hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc,
+                      int64_t M, int64_t N, int64_t K, const float *scale, const float *bias, bool accumulate,
+                      float *part, int64_t part_floats, int cu_count, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  train::GemmF32 g{A, B, C, M, N, K, lda, ldb, ldc, K, scale, bias, accumulate ? 1 : 0, part};
+  const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  // split long reductions over k so that about two blocks per compute unit are busy
+  int64_t splits = std::max<int64_t>(1, std::min<int64_t>((2 * (int64_t)cu_count + tiles - 1) / tiles, (K + 255) / 256));
+  splits = std::min<int64_t>(splits, part_floats / (M * N));
+  if (splits < 1) splits = 1;
+  g.kchunk = (((K + splits - 1) / splits) + 15) / 16 * 16;
+  if (g.kchunk < 16) g.kchunk = 16;
+  splits = (K + g.kchunk - 1) / g.kchunk;
+  if (splits < 1) splits = 1;
+  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)splits);
+  if (ta && tb) hipLaunchKernelGGL((train::k_gemm<true, true>), grid, dim3(train::kThreads), 0, s, g);
+  else if (ta) hipLaunchKernelGGL((train::k_gemm<true, false>), grid, dim3(train::kThreads), 0, s, g);
+  else if (tb) hipLaunchKernelGGL((train::k_gemm<false, true>), grid, dim3(train::kThreads), 0, s, g);
+  else hipLaunchKernelGGL((train::k_gemm<false, false>), grid, dim3(train::kThreads), 0, s, g);
+  if (splits > 1)
+    hipLaunchKernelGGL(train::k_gemm_reduce, dim3(blocks_for(M * N, train::kThreads)), dim3(train::kThreads), 0, s, g,
+                       (int)splits);
+  return hipGetLastError();
+}
+
+hipError_t train_attention(int which, int dh, const TrainAttn &a, hipStream_t s) {
+  const TrainAttn &p = a;
+  if (p.rows <= 0) return hipSuccess;
+  const dim3 grid(blocks_for(p.rows * p.heads, train::kThreads));
+#define AECCT_TRAIN_ATTN(DH)                                                                                 \
+  if (which == 0) hipLaunchKernelGGL(train::k_attn_fwd<DH>, grid, dim3(train::kThreads), 0, s, p);          \
+  else if (which == 1) hipLaunchKernelGGL(train::k_attn_bwd_q<DH>, grid, dim3(train::kThreads), 0, s, p);   \
+  else hipLaunchKernelGGL(train::k_attn_bwd_kv<DH>, grid, dim3(train::kThreads), 0, s, p);
+  switch (dh) {
+    case 4: AECCT_TRAIN_ATTN(4) break;
+    case 8: AECCT_TRAIN_ATTN(8) break;
+    case 16: AECCT_TRAIN_ATTN(16) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef AECCT_TRAIN_ATTN
+  return hipGetLastError();
+}
+
+hipError_t train_ln_fwd(const float *a, const float *b, int64_t rows, int d, const float *g, const float *beta, float eps,
+                        float *out, float *xn, float *rho, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d > 128) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(train::k_ln_fwd, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, a, b, rows, d, g, beta, eps,
+                     out, xn, rho);
+  return hipGetLastError();
+}
+
+hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const float *rho, int64_t rows, int d,
+                        float *dR, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d > 128) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(train::k_ln_bwd, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, dy, g, xn, rho, rows, d, dR);
+  return hipGetLastError();
+}
+
+hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
+                        bool accumulate, float *part, int64_t part_floats, hipStream_t s) {
+  if (C <= 0) return hipSuccess;
+  int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(256, (rows + 63) / 64));
+  chunks = std::max<int64_t>(1, std::min<int64_t>(chunks, part_floats / C));
+  const int64_t chunk = std::max<int64_t>(1, (rows + chunks - 1) / chunks);
+  chunks = std::max<int64_t>(1, (rows + chunk - 1) / chunk);
+  hipLaunchKernelGGL(train::k_colsum_part, dim3(blocks_for(C, train::kThreads), (unsigned)chunks), dim3(train::kThreads),
+                     0, s, A, Bm, w, rows, C, lda, chunk, part);
+  hipLaunchKernelGGL(train::k_colsum_final, dim3(blocks_for(C, train::kThreads)), dim3(train::kThreads), 0, s, part,
+                     (int)chunks, C, out, accumulate ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t train_relu_bwd(float *dg, const float *f, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_relu_bwd, dim3(blocks_for(count, train::kThreads)), dim3(train::kThreads), 0, s, dg, f, count);
+  return hipGetLastError();
+}
+
+hipError_t train_rowdot(const float *x, int64_t rows, int d, const float *w1, const float *b1, float *z, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_rowdot, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, x, rows, d, w1, b1, z);
+  return hipGetLastError();
+}
+
+hipError_t train_outer(const float *dz, int64_t rows, const float *w1, int d, float *dx, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_outer, dim3(blocks_for(rows * d, train::kThreads)), dim3(train::kThreads), 0, s, dz, rows,
+                     w1, d, dx);
+  return hipGetLastError();
+}
+
+hipError_t train_loss(const float *f, const float *y, const float *xs, int64_t count, float *df, float *part,
+                      float *loss, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  const unsigned nb = blocks_for(count, train::kThreads);
+  const float inv = 1.0f / (float)count;
+  hipLaunchKernelGGL(train::k_loss, dim3(nb), dim3(train::kThreads), 0, s, f, y, xs, count, inv, df, part);
+  hipLaunchKernelGGL(train::k_loss_final, dim3(1), dim3(64), 0, s, part, (int)nb, inv, loss);
+  return hipGetLastError();
+}
+
+hipError_t train_embed_grad(const float *t, const float *dx, int64_t words, int L, int d, float *de, hipStream_t s) {
+  hipLaunchKernelGGL(train::k_embed_grad, dim3(blocks_for((int64_t)L * d, train::kThreads)), dim3(train::kThreads), 0, s,
+                     t, dx, words, L, d, de);
+  return hipGetLastError();
+}
+
+}  // namespace aecct

@@ -135,7 +135,8 @@ def test_struct_layouts_match_the_header(P, tmp_path):
     header lacks, or one out of order, would pass the wrong values silently)."""
     import subprocess
     structs = {"aecct_weights": P.Weights, "aecct_options": P.Options, "aecct_model_info": P.ModelInfo,
-               "aecct_spe_params": P.SpeParams}
+               "aecct_spe_params": P.SpeParams, "aecct_train_params": P.TrainParams,
+               "aecct_train_grads": P.TrainGrads}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "aecct.h"', "int main(void) {"]
     for cname, cls in structs.items():
         lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
