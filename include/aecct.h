@@ -108,9 +108,13 @@ typedef enum aecct_layered_attention {
   AECCT_LAYERED_ATTN_UNFUSED = 0,  /* ternary GEMM to Q, K, V in device memory, then attention */
   AECCT_LAYERED_ATTN_LDS_F32 = 1,  /* fused per word and 16-dimension head group, K and V in
                                       LDS as fp32 (d = 64, 128, short words) */
-  AECCT_LAYERED_ATTN_LDS_I16 = 2   /* fused, V (and, on the longest words or with 8-dimension
+  AECCT_LAYERED_ATTN_LDS_I16 = 2,  /* fused, V (and, on the longest words or with 8-dimension
                                       heads, K too) in LDS as int16 accumulators with per-token
                                       scales, the rest as fp32 (d = 64, 128, longer words) */
+  AECCT_LAYERED_ATTN_LDS_SPLIT = 3 /* fused, each head's rows one node type at a time (Section 4.2:
+                                      under head partitioning a row reads keys of one node type),
+                                      that type's keys and values in LDS as fp32 (d = 128,
+                                      16-dimension heads, HPSA, the larger node type within LDS) */
 } aecct_layered_attention;
 
 /* Granularity of the Eq. 2 activation scale alpha = ||x||_inf (Section 4.1).  The paper calls
@@ -131,7 +135,8 @@ typedef struct aecct_options {
   int32_t path;               /* aecct_path */
   int32_t attention;          /* aecct_attention */
   int32_t layered_attention;  /* aecct_layered_attention (the layered path's form); a form the
-                                 shape does not allow gives AECCT_ERR_UNSUPPORTED */
+                                 shape does not allow gives AECCT_ERR_UNSUPPORTED.  AUTO takes the
+                                 first that fits of LDS_F32, LDS_I16, LDS_SPLIT, UNFUSED */
   int32_t act_scale_mode;     /* aecct_act_scale.  WORD runs on the layered path in its unfused
                                  form with natural activation layouts (path AUTO resolves to it;
                                  FUSED or a fused layered form gives AECCT_ERR_UNSUPPORTED) */

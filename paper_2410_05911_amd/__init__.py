@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libaecct.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_WORKSPACE_TOO_SMALL = range(6)
 PATH_AUTO, PATH_LAYERED, PATH_FUSED = 0, 1, 2
 ATTN_HPSA, ATTN_CASA = 0, 1
-LAYERED_ATTN_AUTO, LAYERED_ATTN_UNFUSED, LAYERED_ATTN_LDS_F32, LAYERED_ATTN_LDS_I16 = -1, 0, 1, 2
+LAYERED_ATTN_AUTO, LAYERED_ATTN_UNFUSED, LAYERED_ATTN_LDS_F32, LAYERED_ATTN_LDS_I16, LAYERED_ATTN_LDS_SPLIT = -1, 0, 1, 2, 3
 ACT_SCALE_TOKEN, ACT_SCALE_WORD = 0, 1
 LIN_Q, LIN_K, LIN_V, LIN_O, LIN_FF1, LIN_FF2 = range(6)
 

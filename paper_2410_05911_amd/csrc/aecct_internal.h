@@ -91,6 +91,9 @@ struct Model {
   bool grouped;
   const int32_t *g1_meta, *g2_meta;
   const uint16_t *g1_tab, *g2_tab;
+  // with head partitioning every list holds one node type: the same lists with entries counted
+  // from the first token of that type (variables from 0, checks from n), or null
+  const uint16_t *g1s_tab, *g2s_tab;
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;
   float head_b1;
@@ -128,6 +131,11 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
 // The same with keys and values kept in LDS as int16 accumulators (words too long for the fp32
 // form, up to about 1800 tokens): writes O in fp32 only.
 bool qkv_attention_i16_supported(const Model &M);
+// Rows one node type at a time with the other type's keys and values in LDS as fp32 (d = 128,
+// 16-dimension heads, head partitioning): writes O in fp32 only.
+bool qkv_attention_split_supported(const Model &M);
+hipError_t launch_qkv_attention_split(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                      float *o, bool lane_order, hipStream_t s);
 hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                     float *o, bool lane_order, hipStream_t s);
 // Eq. 2 of the attention output (given as fp32 o, or already as codes oq with scales ao: exactly
@@ -135,6 +143,8 @@ hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq,
 // residual, LN2 and Eq. 2 of the next layer's input in one kernel (d = 64, 128): one wavefront
 // per 16-token strip, activations between the maps only in registers; X and Xq in lane order.
 bool token_block_supported(const Model &M);
+// words processed at once by the layered attention form `form` (aecct_layered_attention)
+int64_t attention_word_slots(const Model &M, int form);
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
                               float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s);
 hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,

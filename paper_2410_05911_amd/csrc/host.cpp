@@ -93,6 +93,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 struct Plan {
   size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
   size_t g1_meta, g1_tab, g2_meta, g2_tab;   // grouped neighbour lists (layered attention)
+  size_t g1s_tab, g2s_tab;                    // the same, counted within each node type
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
   struct Layer {
     size_t qkv, o, ff1, ff2, b_qkv, b_o, b_ff1, b_ff2, ln1_g, ln1_b, ln2_g, ln2_b;
@@ -176,12 +177,26 @@ WsPlan ws_plan(const Model &M, int64_t words) {
   return w;
 }
 
-int64_t chunk_words(const Model &M, int64_t batch) {
+// Words per chunk of a layered decode within `cap_bytes` of workspace: the batch in as few
+// chunks as fit, as even as possible, each a multiple of the words the attention kernel runs at
+// once (one word per block), so that no chunk ends in a round of mostly idle blocks.
+int64_t chunk_words_within(const Model &M, int64_t batch, size_t cap_bytes) {
   const size_t per_word = ws_plan(M, 1).total;
-  int64_t c = (int64_t)(kChunkCapBytes / (per_word ? per_word : 1));
-  if (c < 1) c = 1;
-  return batch < c ? batch : c;
+  int64_t cap = (int64_t)(cap_bytes / (per_word ? per_word : 1));
+  if (cap < 1) cap = 1;
+  while (cap > 1 && ws_plan(M, cap).total > cap_bytes) --cap;
+  if (batch <= cap) return batch;
+  const int64_t slots = aecct::attention_word_slots(M, M.lattn);
+  const int64_t nchunks = (batch + cap - 1) / cap;
+  int64_t cw = (batch + nchunks - 1) / nchunks;
+  if (slots > 1 && cw >= slots) {
+    const int64_t up = (cw + slots - 1) / slots * slots;
+    cw = up <= cap ? up : cap / slots * slots;
+  }
+  return std::max<int64_t>(1, std::min<int64_t>(cw, cap));
 }
+
+int64_t chunk_words(const Model &M, int64_t batch) { return chunk_words_within(M, batch, kChunkCapBytes); }
 
 // Token tiles of the fused path.  In tile t the neighbour loop of head group grp runs
 // T(t, grp) = the longest list of that group among the tile's tokens, so a decode costs
@@ -550,19 +565,27 @@ void build_fused(const Model &M, const uint8_t *H, const aecct_weights *w, const
 }
 
 // The layered decode's projection + attention form: the requested one if the shape allows it, or
-// (AUTO) fused with fp32 keys and values in LDS when they fit, else (with the token block, which
-// takes O in fp32) with int16 accumulators, else the separate GEMM and attention kernels; the
-// unfused form with one alpha per word.  -1 if the requested form does not fit the shape.
+// (AUTO) fused with fp32 keys and values in LDS when a word's fit, else (with the token block,
+// which takes O in fp32) int16 accumulators, else rows one node type at a time with that type's
+// keys and values in LDS as fp32 (measured no faster than the int16 form on LDPC(1024,512): its
+// two phases per head take 3 + 2 row passes of the block where one pass over all rows takes 4),
+// else the separate GEMM and attention kernels; the unfused form with one alpha per word.  -1 if
+// the requested form does not fit the shape.
 int32_t resolve_layered_attention(const Model &M, int requested) {
+  const bool tb = aecct::token_block_supported(M);
   const bool f32 = aecct::qkv_attention_supported(M);
-  const bool i16 = aecct::token_block_supported(M) && aecct::qkv_attention_i16_supported(M);
+  const bool split = tb && aecct::qkv_attention_split_supported(M);
+  const bool i16 = tb && aecct::qkv_attention_i16_supported(M);
   switch (requested) {
     case AECCT_LAYERED_ATTN_UNFUSED: return AECCT_LAYERED_ATTN_UNFUSED;
     case AECCT_LAYERED_ATTN_LDS_F32: return f32 && !M.act_word ? AECCT_LAYERED_ATTN_LDS_F32 : -1;
     case AECCT_LAYERED_ATTN_LDS_I16: return i16 && !M.act_word ? AECCT_LAYERED_ATTN_LDS_I16 : -1;
+    case AECCT_LAYERED_ATTN_LDS_SPLIT: return split && !M.act_word ? AECCT_LAYERED_ATTN_LDS_SPLIT : -1;
   }
   if (M.act_word) return AECCT_LAYERED_ATTN_UNFUSED;
-  return f32 ? AECCT_LAYERED_ATTN_LDS_F32 : (i16 ? AECCT_LAYERED_ATTN_LDS_I16 : AECCT_LAYERED_ATTN_UNFUSED);
+  if (f32) return AECCT_LAYERED_ATTN_LDS_F32;
+  if (i16) return AECCT_LAYERED_ATTN_LDS_I16;
+  return split ? AECCT_LAYERED_ATTN_LDS_SPLIT : AECCT_LAYERED_ATTN_UNFUSED;
 }
 
 aecct_status from_hip(hipError_t e) {
@@ -655,7 +678,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   const int attention = opt ? opt->attention : AECCT_ATTN_HPSA;
   if (attention != AECCT_ATTN_HPSA && attention != AECCT_ATTN_CASA) return AECCT_ERR_INVALID_ARG;
   const int lattn_req = opt ? opt->layered_attention : AECCT_LAYERED_ATTN_AUTO;
-  if (lattn_req < AECCT_LAYERED_ATTN_AUTO || lattn_req > AECCT_LAYERED_ATTN_LDS_I16) return AECCT_ERR_INVALID_ARG;
+  if (lattn_req < AECCT_LAYERED_ATTN_AUTO || lattn_req > AECCT_LAYERED_ATTN_LDS_SPLIT) return AECCT_ERR_INVALID_ARG;
   const int act_mode = opt ? opt->act_scale_mode : AECCT_ACT_SCALE_TOKEN;
   if (act_mode != AECCT_ACT_SCALE_TOKEN && act_mode != AECCT_ACT_SCALE_WORD) return AECCT_ERR_INVALID_ARG;
   const int64_t L64 = (int64_t)n + m;
@@ -698,7 +721,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     return AECCT_ERR_UNSUPPORTED;
   // one alpha per word: the unfused layered form with natural layouts only
   if (act_mode == AECCT_ACT_SCALE_WORD &&
-      (path_req == AECCT_PATH_FUSED || lattn_req == AECCT_LAYERED_ATTN_LDS_F32 || lattn_req == AECCT_LAYERED_ATTN_LDS_I16))
+      (path_req == AECCT_PATH_FUSED || lattn_req == AECCT_LAYERED_ATTN_LDS_F32 || lattn_req == AECCT_LAYERED_ATTN_LDS_I16 ||
+       lattn_req == AECCT_LAYERED_ATTN_LDS_SPLIT))
     return AECCT_ERR_UNSUPPORTED;
 
   aecct::TannerLists TL = aecct::tanner_lists(H, m, n);
@@ -772,6 +796,28 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     group_lists(m1_ptr, m1_idx, G1m, G1);
     group_lists(m2_ptr, m2_idx, G2m, G2);
   }
+  // Under head partitioning every list holds one node type (first ring: the other type; second
+  // ring: its own): the same lists counted from the first token of that type.
+  std::vector<uint16_t> G1s, G2s;
+  if (M.grouped && attention == AECCT_ATTN_HPSA) {
+    auto rebase = [&](const std::vector<uint16_t> &tab) {
+      std::vector<uint16_t> r(tab.size());
+      for (size_t e = 0; e < tab.size(); ++e) r[e] = tab[e] >= n ? (uint16_t)(tab[e] - n) : tab[e];
+      return r;
+    };
+    // every entry of a token's list must be of the node type that list reads (the Tanner graph is
+    // bipartite: first-ring neighbours are of the other type, second-ring ones of the same type)
+    bool one_type = true;
+    for (int a = 0; a < L; ++a) {
+      const bool var = a < n;
+      for (int32_t e = m1_ptr[a]; e < m1_ptr[a + 1]; ++e) one_type &= (m1_idx[e] < n) != var;
+      for (int32_t e = m2_ptr[a]; e < m2_ptr[a + 1]; ++e) one_type &= (m2_idx[e] < n) == var;
+    }
+    if (one_type) {
+      G1s = rebase(G1);
+      G2s = rebase(G2);
+    }
+  }
 
   // host image of the device block
   Plan P = make_plan(n, m, d, n_layers, dff, E, m1_idx.size(), m2_idx.size(), w->pos != nullptr);
@@ -792,6 +838,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
     P.g1_tab = take(2 * G1.size());
     P.g2_meta = take(8 * (size_t)L);
     P.g2_tab = take(2 * G2.size());
+    P.g1s_tab = take(2 * G1s.size());
+    P.g2s_tab = take(2 * G2s.size());
     P.total = off;
   }
   std::vector<unsigned char> img;
@@ -826,6 +874,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   put(P.g1_tab, G1.data(), 2 * G1.size());
   put(P.g2_meta, G2m.data(), 4 * G2m.size());
   put(P.g2_tab, G2.data(), 2 * G2.size());
+  put(P.g1s_tab, G1s.data(), 2 * G1s.size());
+  put(P.g2s_tab, G2s.data(), 2 * G2s.size());
   for (int l = 0; l < n_layers; ++l) {
     const auto &q = P.layer[l];
     const int8_t *Wq = w->w_q + l * D * D, *Wk = w->w_k + l * D * D, *Wv = w->w_v + l * D * D;
@@ -919,6 +969,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.g1_tab = (const uint16_t *)(b + P.g1_tab);
   M.g2_meta = (const int32_t *)(b + P.g2_meta);
   M.g2_tab = (const uint16_t *)(b + P.g2_tab);
+  M.g1s_tab = G1s.empty() ? nullptr : (const uint16_t *)(b + P.g1s_tab);
+  M.g2s_tab = G2s.empty() ? nullptr : (const uint16_t *)(b + P.g2s_tab);
   M.embed = (const float *)(b + P.embed);
   M.pos = w->pos ? (const float *)(b + P.pos) : nullptr;
   M.head_w1 = (const float *)(b + P.w1);
@@ -1032,6 +1084,7 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
   const bool pw = M.act_word != 0;
   const bool tb = !pw && aecct::token_block_supported(M);
   const bool qa = M.lattn == AECCT_LAYERED_ATTN_LDS_F32, qw = M.lattn == AECCT_LAYERED_ATTN_LDS_I16;
+  const bool qs = M.lattn == AECCT_LAYERED_ATTN_LDS_SPLIT;
   for (int64_t w0 = 0; w0 < batch; w0 += cw) {
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
@@ -1042,6 +1095,8 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
         e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, tb, s);
       } else if (qw) {
         e = aecct::launch_qkv_attention_i16(M, l, xq, ax, nw, qkv, tb, s);
+      } else if (qs) {
+        e = aecct::launch_qkv_attention_split(M, l, xq, ax, nw, qkv, tb, s);
       } else {
         e = aecct::launch_qkv(M, l, xq, ax, rows, qkv, tb, s);
         if (e == hipSuccess) e = aecct::launch_attention(M, qkv, nw, o32, oq, ao, s);
@@ -1049,7 +1104,7 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
       }
       if (e != hipSuccess) break;
       if (tb) {
-        e = qa || qw ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
+        e = qa || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
                      : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
@@ -1099,11 +1154,8 @@ aecct_status aecct_decode_static(const aecct_model *model, const float *y, int64
   int64_t cw = 1;
   if (M.path != AECCT_PATH_FUSED) {
     if (!M.static_scratch) return AECCT_ERR_DEVICE;
-    // the most words whose workspace fits the array
-    cw = (int64_t)(kStaticScratchBytes / ws_plan(M, 1).total);
-    while (cw > 0 && ws_plan(M, cw).total > kStaticScratchBytes) --cw;
-    if (cw < 1) return AECCT_ERR_WORKSPACE_TOO_SMALL;
-    if (cw > batch) cw = batch;
+    if (ws_plan(M, 1).total > kStaticScratchBytes) return AECCT_ERR_WORKSPACE_TOO_SMALL;
+    cw = chunk_words_within(M, batch, kStaticScratchBytes);
   }
   return decode_chunks(M, y, batch, bits, logits, M.static_scratch, cw, (hipStream_t)stream);
 }

@@ -366,6 +366,11 @@ struct QkvAttnArgs {
   const uint2 *tab1, *tab2;    // four 16-bit token indices per group
   float *o;                    // [rows][d]
   int resident;                // k_qkv_attention: every head group's weight tiles stay in LDS
+  // k_qkv_attention_split: the same lists with every entry counted from the first token of its
+  // node type (variables from 0, checks from n), the variable count n, and the LDS capacity in
+  // tokens of the larger node type
+  const uint2 *tab1s, *tab2s;
+  int n_var, kv_cap;
 };
 
 constexpr int kQaThreads = 512;
@@ -694,13 +699,12 @@ __device__ __forceinline__ void qp_step(const float (&q)[8], const float (&k)[8]
   for (int t = 0; t < 8; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
 }
 
-// Attention of one half row: qrow, kb and orow already offset to this lane's half; entries as in
-// qa_row, the first group in g0.  Both lanes of a pair run it with the same row.
-__device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
-                                       float *orow) {
+// Attention of one half row whose query half is q: kb and orow already offset to this lane's
+// half; entries as in qa_row, the first group in g0.  Both lanes of a pair run it with the same
+// row.
+__device__ __forceinline__ void qp_row_q(const float (&q)[8], const float *kb, const uint2 *eg, uint2 g0, int cnt,
+                                         float *orow) {
   constexpr int R = kQaRow;
-  float q[8];
-  qa_load<8>(q, qrow);
   float S_ = 0.0f, acc[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
@@ -749,6 +753,14 @@ __device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const
   const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
   *(float4 *)orow = make_float4(acc[0] * rS, acc[1] * rS, acc[2] * rS, acc[3] * rS);
   *(float4 *)(orow + 4) = make_float4(acc[4] * rS, acc[5] * rS, acc[6] * rS, acc[7] * rS);
+}
+
+// The same with the query half read from qrow first.
+__device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
+                                       float *orow) {
+  float q[8];
+  qa_load<8>(q, qrow);
+  qp_row_q(q, kb, eg, g0, cnt, orow);
 }
 
 template <int D>
@@ -1172,6 +1184,122 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
                (first ? p.tab1 : p.tab2) + mt.x, mt.y);
       }
       block_sync_lds();            // the next group's projection overwrites keys and values
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Long words with 16-dimension heads (d = 128, head partitioning), rows one node type at a time
+// (Section 4.2, Fig. 2): a first-ring head's variable rows read only check keys and its check
+// rows only variable keys; a second-ring head's rows read keys of their own type.  Each head
+// group therefore runs in two phases, variable rows then check rows; a phase projects the keys
+// and values of the one node type its rows read into LDS as fp32 (144-byte rows, as in
+// k_qkv_attention_pair) and the queries of its rows into the output rows in device memory.  Each
+// token's query, key and value is projected in exactly one phase of a group, so the MFMA work is
+// that of one projection; the larger node type (n = 1024 variables of the 1536 tokens of
+// LDPC(1024,512)) bounds the LDS.  Rows split over lane pairs (qp_row); blocks of 12 wavefronts,
+// each keeping its 8 token tiles' int8 codes in registers for all head groups of a word.
+// ------------------------------------------------------------------------------------------
+constexpr int kQsThreads = 768;
+constexpr int kQsTilesPerWave = 8;
+
+template <int D>
+size_t qkv_attention_split_lds_bytes(int kv_cap, int L) {
+  return qa_frag_bytes<D>() + (size_t)kv_cap * kQaRow * 4 + (size_t)L * 4;
+}
+
+template <int D>
+__global__ __launch_bounds__(kQsThreads) void k_qkv_attention_split(QkvAttnArgs p) {
+  constexpr int S = D / 32, G = D / 16, R = kQaRow, NT = kQsThreads, NWV = NT / 64, TW = kQsTilesPerWave;
+  static_assert(D == 128, "16-dimension heads, one per head group");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int L = p.L, n = p.n_var, ntiles = (L + 15) / 16;
+  uint64_t *bf = (uint64_t *)smem;                                   // [3][S][64] weight fragments
+  float *kv = (float *)(smem + qa_frag_bytes<D>());                  // [kv_cap][R] keys | values
+  float *als = kv + (size_t)p.kv_cap * R;                            // [L] the word's alpha per token
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4, half = tid & 1;
+  if (blockIdx.x >= p.words) return;
+  {
+    QaStage<D, NT> st;
+    st.load(p.bpack, 0, tid);
+    st.store(bf, tid);
+  }
+  const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
+  long afr[TW][S];
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    float *ow = p.o + w * L * D;
+    // an opaque copy of the wave index per word and per phase keeps the per-tile addresses from
+    // being hoisted out of the loops (held for all tiles, they would not fit the registers)
+    int wv = wave;
+    __asm__ volatile("" : "+v"(wv));
+#pragma unroll
+    for (int k = 0; k < TW; ++k) qa_load_codes<D>(p.xq + w * L * D, wv + NWV * k, L, lane, afr[k]);
+    for (int t = tid; t < L; t += NT) als[t] = p.ax[w * L + t];
+    __syncthreads();
+    for (int hg = 0; hg < G; ++hg) {
+      const bool first = hg < p.hf;
+      for (int ph = 0; ph < 2; ++ph) {
+        const int rlo = ph ? n : 0, rhi = ph ? L : n;                // this phase's rows
+        const bool kvar = first == (ph == 1);                        // its keys are variables
+        const int klo = kvar ? 0 : n, khi = kvar ? n : L;
+        // the next group's weight tiles: read in the group's last phase, written to LDS once its
+        // projection is done
+        const bool more = ph == 1 && (hg + 1 < G || w + gridDim.x < p.words);
+        QaStage<D, NT> st;
+        if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
+        float bq = p.bias[16 * hg + col], bkc = p.bias[D + 16 * hg + col], bvc = p.bias[2 * D + 16 * hg + col];
+        int wg = wave;
+        // waited for here, before the first query store (not behind it)
+        __asm__ volatile("" : "+v"(wg), "+v"(bq), "+v"(bkc), "+v"(bvc));
+#pragma unroll
+        for (int k = 0; k < TW; ++k) {
+          const int tt = wg + NWV * k;
+          if (tt >= ntiles) continue;
+          const int t0 = 16 * tt, t1 = t0 + 16;
+          const bool needq = t0 < rhi && t1 > rlo, needkv = t0 < khi && t1 > klo;   // uniform per wave
+          if (!needq && !needkv) continue;
+          float alv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int tok = t0 + 4 * rg + i;
+            alv[i] = tok < L ? als[tok] : 0.0f;
+          }
+          const auto fa = [&](int s) { return afr[k][s]; };
+          if (needq) {
+            v4i aq = v4i{0, 0, 0, 0};
+            aq = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; }, aq);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int tok = t0 + 4 * rg + i;
+              if (tok >= rlo && tok < rhi) ow[(size_t)tok * D + 16 * hg + col] = __builtin_fmaf((float)aq[i], alv[i] * sq[0], bq);
+            }
+          }
+          if (needkv) {
+            v4i ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+            ak = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(1 * S + s) * 64 + lane]; }, ak);
+            av = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(2 * S + s) * 64 + lane]; }, av);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int tok = t0 + 4 * rg + i;
+              if (tok >= klo && tok < khi) {
+                kv[(tok - klo) * R + col] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
+                kv[(tok - klo) * R + 16 + col] = __builtin_fmaf((float)av[i], alv[i] * sq[2], bvc);
+              }
+            }
+          }
+        }
+        __syncthreads();   // also orders the queries written to memory before their rows read them
+        if (more) st.store(bf, tid);   // no wave reads this group's fragments any more
+        const int2 *meta = first ? p.meta1 : p.meta2;
+        const uint2 *tab = first ? p.tab1s : p.tab2s;
+        for (int r = rlo + (tid >> 1); r < rhi; r += NT / 2) {
+          const int2 mt = meta[r];
+          const uint2 *eg = tab + mt.x;
+          float *orow = ow + (size_t)r * D + 16 * hg + 8 * half;
+          qp_row(orow, kv + 8 * half, eg, eg[0], mt.y, orow);
+        }
+        block_sync_lds();            // the next phase's projection overwrites keys and values
+      }
     }
   }
 }
@@ -2028,6 +2156,64 @@ hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq,
   return hipErrorInvalidValue;
 }
 
+// Rows one node type at a time: head partitioning (every list holds one node type), d = 128 with
+// 16-dimension heads, the larger node type's keys and values fit LDS.
+bool qkv_attention_split_supported(const Model &M) {
+  if (!(M.d == 128 && M.dh == 16 && M.grouped && M.g1s_tab && M.g2s_tab)) return false;   // tables: HPSA only
+  if (M.L > 16 * (kQsThreads / 64) * kQsTilesPerWave) return false;
+  return qkv_attention_split_lds_bytes<128>(std::max(M.n, M.m), M.L) <= M.lds_max;
+}
+
+hipError_t launch_qkv_attention_split(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
+                                      float *o, bool lane_order, hipStream_t s) {
+  if (words <= 0) return hipSuccess;
+  if (!qkv_attention_split_supported(M)) return hipErrorInvalidValue;
+  const LayerWeights &W = M.layer[layer];
+  if (lane_order && !W.qkv_tb) return hipErrorInvalidValue;
+  QkvAttnArgs a{};
+  a.xq = xq;
+  a.ax = ax;
+  a.bpack = lane_order ? W.qkv_tb : W.qkv;
+  a.bias = W.b_qkv;
+  a.sq[0] = W.sq_qs;
+  a.sq[1] = W.sq[1];
+  a.sq[2] = W.sq[2];
+  a.words = words;
+  a.L = M.L;
+  a.hf = M.hf;
+  a.meta1 = (const int2 *)M.g1_meta; a.meta2 = (const int2 *)M.g2_meta;
+  a.tab1s = (const uint2 *)M.g1s_tab; a.tab2s = (const uint2 *)M.g2s_tab;
+  a.n_var = M.n;
+  a.kv_cap = std::max(M.n, M.m);
+  a.o = o;
+  const size_t lds = qkv_attention_split_lds_bytes<128>(a.kv_cap, M.L);
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
+  const int64_t blocks = std::min<int64_t>(words, (int64_t)M.cu_count * per_cu);
+  hipLaunchKernelGGL((k_qkv_attention_split<128>), dim3((unsigned)blocks), dim3(kQsThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+// Words the layered decode's attention kernel processes at once (one word per block, as many
+// blocks as stay resident on the device): chunks of words are best sized in multiples of it.
+int64_t attention_word_slots(const Model &M, int form) {
+  size_t lds = 0;
+  switch (form) {
+    case 1:   // fp32 keys and values of the whole word
+      lds = qkv_attention_pair_supported(M) ? qkv_attention_pair_lds(M) : qkv_attention_lds(M, qkv_attention_resident(M));
+      break;
+    case 2:   // int16 accumulators
+      lds = qkv_attention_v16_supported(M) ? (M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L))
+                                           : (M.d == 64 ? qkv_attention_i16_lds_bytes<64>(M.L) : qkv_attention_i16_lds_bytes<128>(M.L));
+      break;
+    case 3:   // one node type's rows at a time
+      lds = qkv_attention_split_lds_bytes<128>(std::max(M.n, M.m), M.L);
+      break;
+    default:  // the unfused kernels take rows, not words
+      return 1;
+  }
+  return (int64_t)M.cu_count * std::max<int64_t>(1, (int64_t)(M.lds_max / std::max<size_t>(lds, 1)));
+}
+
 bool token_block_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && M.dff == 4 * M.d && M.layer[0].tb_o != nullptr;
 }
@@ -2124,7 +2310,8 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
       (const void *)k_qkv_attention_pair<128>,   (const void *)k_qkv_attention_i16<128, 16>,
       (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
       (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
-      (const void *)k_qkv_attention_v16<128>,    (const void *)k_token_block<64, true>,
+      (const void *)k_qkv_attention_v16<128>,    (const void *)k_qkv_attention_split<128>,
+      (const void *)k_token_block<64, true>,
       (const void *)k_token_block<64, false>,    (const void *)k_token_block<128, true>,
       (const void *)k_token_block<128, false>};
   for (const void *f : fns) {

@@ -359,7 +359,9 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
     """d = 64 and 128 on token counts L = n + m that are not multiples of 16 (partial token
     tiles in the fused projection/attention kernels), several head splits and CASA.  Words of up
     to 256 (d = 64) or 512 (d = 128) tokens keep keys and values in LDS as fp32; the longer ones
-    (L = 301, 394, 601, 765) as int16 accumulators."""
+    (L = 301, 394, 601, 765) as int16 accumulators, or (d = 128 with head partitioning) one node
+    type's rows at a time with the other type's keys and values in LDS as fp32, whose token tiles
+    straddle the variable/check boundary when n is not a multiple of 16."""
     from workloads import random_weights
     print(f"[wide] d {d} m {m} n {n} hf {hf} {attention}", flush=True)
     H = _random_parity_check(m, n, seed=m * 131 + n)
@@ -370,16 +372,22 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
     dec = P.Decoder(H, w)
     assert dec.path == P.PATH_LAYERED
     long_word = m + n > (256 if d == 64 else 512)
+    split = d == 128 and attention == "hpsa"
     assert dec.info.layered_attention == (P.LAYERED_ATTN_LDS_I16 if long_word else P.LAYERED_ATTN_LDS_F32)
     bits, logits = dec.decode(_dev(y))
     _assert_logits(_np(logits), fo, _np(bits), bo, y)
+    if long_word and split:                  # rows one node type at a time on the same words
+        dec = P.Decoder(H, w, layered_attention=P.LAYERED_ATTN_LDS_SPLIT)
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("regime", ["mixed", "underflow", "zero_values"])
 def test_long_words_shifted_softmax(P, oracle_mod, regime, d):
-    """The int16 key/value form on long words (L = 601) with rows that take the max-shifted
-    softmax (some or all), and with a zero value map (O = 0, Eq. 2 scale 0)."""
+    """The long-word forms (L = 601: int16 values, and at d = 128 rows one node type at a time) with
+    rows that take the max-shifted softmax (some or all), and with a zero value map (O = 0, Eq. 2
+    scale 0)."""
     from workloads import random_weights
     print(f"[long softmax] d {d} {regime}", flush=True)
     m, n = 200, 401
@@ -401,6 +409,10 @@ def test_long_words_shifted_softmax(P, oracle_mod, regime, d):
     assert dec.info.layered_attention == P.LAYERED_ATTN_LDS_I16
     bits, logits = dec.decode(_dev(y))
     _assert_logits(_np(logits), fo, _np(bits), bo, y)
+    if d == 128:
+        dec = P.Decoder(H, w, layered_attention=P.LAYERED_ATTN_LDS_SPLIT)
+        bits, logits = dec.decode(_dev(y))
+        _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
 @pytest.mark.parametrize("regime", ["plain", "mixed"])
@@ -439,7 +451,8 @@ def test_layered_attention_forms_of_the_workloads(P):
 def test_layered_attention_forms_agree_on_the_whole_batch(P, c):
     """The full configured batch through every Q/K/V + attention form the shape allows: the
     production kernels (fp32 K and V in LDS with lane pairs on LDPC(256,128), fp32 keys beside
-    int16 values on LDPC(1024,512)), the int16 forms, and the unfused GEMM + attention kernels
+    int16 values on LDPC(1024,512)), the int16 forms, the node-type split (one node type's rows at
+    a time, that type's keys and values in LDS as fp32), and the unfused GEMM + attention kernels
     that the stage entry points run; all bit-identical."""
     cfg = CONFIGS[c]
     print(f"[forms e2e] config {c} batch {cfg.batch}", flush=True)
@@ -447,8 +460,8 @@ def test_layered_attention_forms_agree_on_the_whole_batch(P, c):
     yd = _dev(y)
     ref = None
     forms = {3: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_I16, P.LAYERED_ATTN_UNFUSED),
-             4: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_I16, P.LAYERED_ATTN_UNFUSED),
-             5: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_UNFUSED)}[c]
+             4: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_I16, P.LAYERED_ATTN_LDS_SPLIT, P.LAYERED_ATTN_UNFUSED),
+             5: (P.LAYERED_ATTN_AUTO, P.LAYERED_ATTN_LDS_SPLIT, P.LAYERED_ATTN_UNFUSED)}[c]
     for form in forms:
         dec = P.Decoder(H, w, layered_attention=form)
         if form != P.LAYERED_ATTN_AUTO:
