@@ -222,6 +222,57 @@ def spe_bench(c: int, repeats: int = 3):
                                        f"{dt:.1f} s, scaled to all nodes"}}), flush=True)
 
 
+def train_bench(c: int, batch: int, steps: int, warmup: int):
+    """The quantisation-aware training step (Section 6, second phase) of workload c's shape on the
+    GPU: Eq. 1 on every latent matrix, forward, loss and every gradient (no optimiser update)."""
+    import torch
+    import paper_2410_05911_amd as P
+    from workloads import CONFIGS, random_qat_params
+    from workloads.configs import parity_check
+    from workloads.channel import awgn_words
+    from workloads.codes import generator_from_parity
+    cfg = CONFIGS[c]
+    H = parity_check(cfg)
+    m, n = H.shape
+    L, d, N = n + m, cfg.d, cfg.n_layers
+    p = random_qat_params(n, m, d, N, seed=7)
+    y, x, _ = awgn_words(generator_from_parity(H), batch, (3.0, 4.0, 5.0, 6.0, 7.0), seed=8)
+    y = (y * (1 - 2 * x.astype(np.float32))).astype(np.float32)       # all-zero codeword, as the paper trains
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    pd = {k: ({kk: dev(vv) for kk, vv in v.items()} if k in ("w", "b") else
+              (dev(np.array([v], np.float32)) if k == "head_b1" else (None if v is None else dev(v))))
+          for k, v in p.items()}
+    tr = P.Trainer(H, d, N)
+    yd = dev(y)
+    for _ in range(warmup):
+        tr.grad(pd, yd)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        loss, g = tr.grad(pd, yd)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    # fp32 multiply-adds of the step's GEMMs (forward, input gradients, weight gradients) and head
+    R = batch * L
+    lin = N * (4 * d * d + 2 * d * 4 * d)
+    fma = 3 * R * lin + 3 * batch * L * n
+    import oracle.qat as Q
+    k = 2
+    t0 = time.perf_counter()
+    Q.forward_backward(H, p, y[:k])
+    dt = time.perf_counter() - t0
+    print(json.dumps({"metric": "QAT training step (forward + every gradient), words/s", "value": batch / (ms * 1e-3),
+                      "unit": "codewords/s", "ms_per_step": ms, "steps": steps, "warmup": warmup,
+                      "higher_is_better": True, "loss": loss.item(),
+                      "config": {"workload": f"qat_{cfg.name}_batch{batch}", "tokens": L, "d": d, "layers": N,
+                                 "batch": batch},
+                      "gemm_fma_per_step": fma, "gemm_fma_rate_T": fma / (ms * 1e-3) / 1e12,
+                      "cpu_baseline": {"value": k / dt, "unit": "codewords/s", "cores": 1, "kind": "oracle",
+                                       "sample": f"{k} words, float64 numpy oracle, {dt:.2f} s"}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -237,7 +288,10 @@ def main():
     ap.add_argument("--act-scale", choices=("token", "word"), default="token",
                     help="Eq. 2 scale per token (default) or per word")
     ap.add_argument("--layered-attention", type=int, default=-1,
-                    help="layered path's Q/K/V + attention form: -1 auto, 0 unfused, 1 fp32 in LDS, 2 int16 in LDS")
+                    help="layered path's Q/K/V + attention form: -1 auto, 0 unfused, 1 fp32 in LDS, 2 int16 in LDS, 3 one node type at a time")
+    ap.add_argument("--train", action="store_true",
+                    help="only time the QAT training step of --workload's shape (batch --train-batch)")
+    ap.add_argument("--train-batch", type=int, default=128, help="words per training step (the paper: 128)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (HBM counter calibration)")
     ap.add_argument("--aap-import", action="store_true",
@@ -247,6 +301,9 @@ def main():
     args = ap.parse_args()
     if args.spe:
         spe_bench(args.workload)
+        return
+    if args.train:
+        train_bench(args.workload, args.train_batch, args.steps, args.warmup)
         return
     if args.copy_calibration:
         copy_calibration()
