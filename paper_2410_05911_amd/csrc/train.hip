@@ -41,23 +41,54 @@ __device__ __forceinline__ float wave_max(float v) {
 // like their bits), one 8-bit digit per pass.
 // ------------------------------------------------------------------------------------------
 using AapJob = TrainAapJob;
+constexpr int kAapThreads = 1024, kAapWaves = kAapThreads / 64;
 
-__device__ uint32_t radix_select(const float *w, int64_t count, uint32_t k, uint32_t *hist, uint32_t *pick) {
+// Bucket b's running total over the wave histograms, and the bucket holding the k-th key (k
+// counted from 0 among the keys matching the current prefix) with k's rank inside it: wave 0
+// scans the 256 buckets as four per lane.
+__device__ void select_bucket(const uint32_t (*hist)[256], uint32_t k, uint32_t *pick) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  uint32_t c[4], t = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t v = 0;
+    for (int w = 0; w < kAapWaves; ++w) v += hist[w][4 * lane + j];
+    c[j] = v;
+    t += v;
+  }
+  uint32_t incl = t;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t up = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += up;
+  }
+  const uint32_t excl = incl - t;
+  if (excl <= k && k < incl) {
+    uint32_t kk = k - excl;
+    int j = 0;
+    while (j < 3 && kk >= c[j]) kk -= c[j++];
+    pick[0] = 4 * lane + j;
+    pick[1] = kk;
+  }
+}
+
+// The k-th smallest |w| (k from 0) as a bit pattern: non-negative floats order like their bits,
+// so four passes pick its 8-bit digits from the most significant down, each pass counting the
+// keys that match the digits found so far into per-wave histograms.
+__device__ uint32_t radix_select(const float *w, int64_t count, uint32_t k, uint32_t (*hist)[256], uint32_t *pick) {
   uint32_t prefix = 0, mask = 0;
+  uint32_t *flat = &hist[0][0];
+  const int wave = threadIdx.x >> 6;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = threadIdx.x; b < 256; b += kThreads) hist[b] = 0;
+    for (int b = threadIdx.x; b < kAapWaves * 256; b += kAapThreads) flat[b] = 0;
     __syncthreads();
-    for (int64_t e = threadIdx.x; e < count; e += kThreads) {
+    for (int64_t e = threadIdx.x; e < count; e += kAapThreads) {
       const uint32_t key = __float_as_uint(fabsf(w[e]));
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      if ((key & mask) == prefix) atomicAdd(&hist[wave][(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t b = 0, kk = k;
-      while (b < 255 && kk >= hist[b]) kk -= hist[b++];
-      pick[0] = b;
-      pick[1] = kk;
-    }
+    select_bucket(hist, k, pick);
     __syncthreads();
     prefix |= pick[0] << shift;
     mask |= 255u << shift;
@@ -67,15 +98,40 @@ __device__ uint32_t radix_select(const float *w, int64_t count, uint32_t k, uint
   return prefix;
 }
 
-__global__ __launch_bounds__(kThreads) void k_aap(TrainAapJobs jobs, float eps) {
-  __shared__ uint32_t hist[256];
+__global__ __launch_bounds__(kAapThreads) void k_aap(TrainAapJobs jobs, float eps) {
+  __shared__ uint32_t hist[kAapWaves][256];
   __shared__ uint32_t pick[2];
+  __shared__ uint32_t wle[kAapWaves], wgt[kAapWaves];
   __shared__ float sden;
   const AapJob J = jobs.j[blockIdx.x];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const uint32_t lo = (uint32_t)((J.count - 1) / 2);
   const uint32_t a_lo = radix_select(J.w, J.count, lo, hist, pick);
-  const uint32_t a_hi = (int64_t)lo + 1 < J.count ? radix_select(J.w, J.count, lo + 1, hist, pick) : a_lo;
+  // the next order statistic: a_lo again if more than lo + 1 keys are <= a_lo, else the least
+  // key above it
+  uint32_t le = 0, gt = 0xffffffffu;
+  for (int64_t e = threadIdx.x; e < J.count; e += kAapThreads) {
+    const uint32_t key = __float_as_uint(fabsf(J.w[e]));
+    if (key <= a_lo) ++le;
+    else gt = min(gt, key);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    le += __shfl_xor(le, o, 64);
+    gt = min(gt, (uint32_t)__shfl_xor(gt, o, 64));
+  }
+  if (lane == 0) {
+    wle[wave] = le;
+    wgt[wave] = gt;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
+    uint32_t n_le = 0, g = 0xffffffffu;
+    for (int w = 0; w < kAapWaves; ++w) {
+      n_le += wle[w];
+      g = min(g, wgt[w]);
+    }
+    const uint32_t a_hi = ((int64_t)lo + 1 >= J.count || n_le > lo + 1) ? a_lo : g;
     const double pos = 0.5 * (double)(J.count - 1);
     const double frac = pos - (double)lo;
     const double flo = (double)__uint_as_float(a_lo), fhi = (double)__uint_as_float(a_hi);
@@ -87,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void k_aap(TrainAapJobs jobs, float eps) 
   }
   __syncthreads();
   const float den = sden;
-  for (int64_t e = threadIdx.x; e < J.count; e += kThreads) {
+  for (int64_t e = threadIdx.x; e < J.count; e += kAapThreads) {
     const float x = J.w[e];
     float r = den == 0.0f ? (x > 0.0f ? 1.0f : (x < 0.0f ? -1.0f : 0.0f)) : rintf(x / den);
     J.t[e] = fminf(1.0f, fmaxf(-1.0f, r));
@@ -409,30 +465,46 @@ __global__ __launch_bounds__(kThreads) void k_ln_bwd(const float *dy, const floa
 
 // ------------------------------------------------------------------------------------------
 // Column sums over rows, deterministic in two passes: out[c] (+)= sum_r A[r][c] (x B[r][c]) (x w[r]).
-// Pass one: block (chunk, column group) sums its rows in ascending order; pass two: the chunks
-// in ascending order.
+// A block covers cw columns (a power of two up to 64) with 256 / cw row lanes; lane l of a block
+// sums the rows l, l + lanes, ... of its chunk (four interleaved partial sums), the lanes are
+// combined by a fixed tree in LDS.  Pass one writes a partial row per chunk, pass two sums the
+// partial rows with the same kernel.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_colsum_part(const float *A, const float *Bm, const float *w, int64_t rows,
-                                                          int C, int64_t lda, int64_t chunk, float *part) {
-  const int c = blockIdx.x * kThreads + threadIdx.x;
-  if (c >= C) return;
+__global__ __launch_bounds__(kThreads) void k_colsum(const float *A, int64_t lda, const float *Bm, const float *w,
+                                                     int64_t rows, int C, int cw_log2, int64_t chunk, float *out,
+                                                     int accumulate) {
+  __shared__ float red[kThreads];
+  const int cw = 1 << cw_log2, lanes = kThreads >> cw_log2;
+  const int cl = threadIdx.x & (cw - 1), rl = threadIdx.x >> cw_log2;
+  const int c = blockIdx.x * cw + cl;
   const int64_t r0 = (int64_t)blockIdx.y * chunk, r1 = std::min<int64_t>(rows, r0 + chunk);
-  float s = 0.0f;
-  for (int64_t r = r0; r < r1; ++r) {
+  auto val = [&](int64_t r) {
     float v = A[r * lda + c];
     if (Bm) v *= Bm[r * C + c];
     if (w) v *= w[r];
-    s += v;
+    return v;
+  };
+  float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+  if (c < C) {
+    int64_t r = r0 + rl;
+    for (; r + 3 * lanes < r1; r += 4 * lanes) {
+      s0 += val(r);
+      s1 += val(r + lanes);
+      s2 += val(r + 2 * lanes);
+      s3 += val(r + 3 * lanes);
+    }
+    for (; r < r1; r += lanes) s0 += val(r);
   }
-  part[(int64_t)blockIdx.y * C + c] = s;
-}
-
-__global__ __launch_bounds__(kThreads) void k_colsum_final(const float *part, int chunks, int C, float *out, int accumulate) {
-  const int c = blockIdx.x * kThreads + threadIdx.x;
-  if (c >= C) return;
-  float s = 0.0f;
-  for (int z = 0; z < chunks; ++z) s += part[(int64_t)z * C + c];
-  out[c] = accumulate ? out[c] + s : s;
+  red[threadIdx.x] = (s0 + s1) + (s2 + s3);
+  __syncthreads();
+  for (int st = lanes >> 1; st > 0; st >>= 1) {
+    if (rl < st) red[threadIdx.x] += red[threadIdx.x + (st << cw_log2)];
+    __syncthreads();
+  }
+  if (rl == 0 && c < C) {
+    float *o = out + (int64_t)blockIdx.y * C + c;
+    *o = accumulate ? *o + red[threadIdx.x] : red[threadIdx.x];
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -512,28 +584,38 @@ __global__ __launch_bounds__(kThreads) void k_embed_grad(const float *t, const f
 // dW; dW = G s / (s + eps) and d delta = gamma sum(G T) - s gamma / (s + eps)^2 sum(G W).
 using DeltaJob = TrainDeltaJob;
 
-__global__ __launch_bounds__(kThreads) void k_delta_grad(TrainDeltaJobs jobs, float eps) {
-  __shared__ float r1[kThreads / 64], r2[kThreads / 64];
+__global__ __launch_bounds__(kAapThreads) void k_delta_grad(TrainDeltaJobs jobs, float eps) {
+  __shared__ float r1[kAapWaves], r2[kAapWaves];
   const DeltaJob J = jobs.j[blockIdx.x];
   const float s = *J.scale, gamma = *J.gamma;
   const float fac = s / (s + eps);
-  float a = 0.0f, b = 0.0f;
-  for (int64_t e = threadIdx.x; e < J.count; e += kThreads) {
+  float a[2] = {0.0f, 0.0f}, b[2] = {0.0f, 0.0f};
+  int64_t e = threadIdx.x;
+  for (; e + kAapThreads < J.count; e += 2 * kAapThreads) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t x = e + u * kAapThreads;
+      const float gv = J.dw[x];
+      a[u] = fmaf(gv, J.t[x], a[u]);
+      b[u] = fmaf(gv, J.w[x], b[u]);
+      J.dw[x] = gv * fac;
+    }
+  }
+  if (e < J.count) {
     const float gv = J.dw[e];
-    a = fmaf(gv, J.t[e], a);
-    b = fmaf(gv, J.w[e], b);
+    a[0] = fmaf(gv, J.t[e], a[0]);
+    b[0] = fmaf(gv, J.w[e], b[0]);
     J.dw[e] = gv * fac;
   }
-  a = wave_sum(a);
-  b = wave_sum(b);
+  const float sa_ = wave_sum(a[0] + a[1]), sb_ = wave_sum(b[0] + b[1]);
   if ((threadIdx.x & 63) == 0) {
-    r1[threadIdx.x >> 6] = a;
-    r2[threadIdx.x >> 6] = b;
+    r1[threadIdx.x >> 6] = sa_;
+    r2[threadIdx.x >> 6] = sb_;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     float sa = 0.0f, sb = 0.0f;
-    for (int k = 0; k < kThreads / 64; ++k) {
+    for (int k = 0; k < kAapWaves; ++k) {
       sa += r1[k];
       sb += r2[k];
     }
@@ -552,12 +634,12 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 }
 
 hipError_t train_aap(const TrainAapJobs &jobs, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(train::k_aap, dim3(6), dim3(train::kThreads), 0, s, jobs, eps);
+  hipLaunchKernelGGL(train::k_aap, dim3(6), dim3(train::kAapThreads), 0, s, jobs, eps);
   return hipGetLastError();
 }
 
 hipError_t train_delta_grad(const TrainDeltaJobs &jobs, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(train::k_delta_grad, dim3(6), dim3(train::kThreads), 0, s, jobs, eps);
+  hipLaunchKernelGGL(train::k_delta_grad, dim3(6), dim3(train::kAapThreads), 0, s, jobs, eps);
   return hipGetLastError();
 }
 
@@ -639,14 +721,24 @@ hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const 
 hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
                         bool accumulate, float *part, int64_t part_floats, hipStream_t s) {
   if (C <= 0) return hipSuccess;
-  int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(256, (rows + 63) / 64));
+  int cwl = 0;
+  while ((1 << cwl) < C && cwl < 6) ++cwl;
+  const int lanes = train::kThreads >> cwl;
+  const unsigned cblocks = blocks_for(C, 1 << cwl);
+  // about 1024 blocks in all, each lane summing at least 8 rows
+  int64_t chunks = std::min<int64_t>((rows + 8 * lanes - 1) / (8 * lanes), std::max<int64_t>(1, 1024 / cblocks));
   chunks = std::max<int64_t>(1, std::min<int64_t>(chunks, part_floats / C));
   const int64_t chunk = std::max<int64_t>(1, (rows + chunks - 1) / chunks);
   chunks = std::max<int64_t>(1, (rows + chunk - 1) / chunk);
-  hipLaunchKernelGGL(train::k_colsum_part, dim3(blocks_for(C, train::kThreads), (unsigned)chunks), dim3(train::kThreads),
-                     0, s, A, Bm, w, rows, C, lda, chunk, part);
-  hipLaunchKernelGGL(train::k_colsum_final, dim3(blocks_for(C, train::kThreads)), dim3(train::kThreads), 0, s, part,
-                     (int)chunks, C, out, accumulate ? 1 : 0);
+  if (chunks == 1) {
+    hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, 1), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows, C, cwl,
+                       chunk, out, accumulate ? 1 : 0);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, (unsigned)chunks), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows,
+                     C, cwl, chunk, part, 0);
+  hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, 1), dim3(train::kThreads), 0, s, (const float *)part, (int64_t)C,
+                     (const float *)nullptr, (const float *)nullptr, chunks, C, cwl, chunks, out, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 
