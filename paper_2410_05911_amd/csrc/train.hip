@@ -276,12 +276,167 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmF32 g) {
   }
 }
 
+// The same product on v_mfma_f32_16x16x4_f32 for operands whose contiguous dimension and leading
+// dimensions are multiples of 4 floats (16-byte loads): blocks of 128 x 128 outputs, four
+// wavefronts of 64 x 64 (4 x 4 MFMA tiles), k-steps of 32 staged through LDS, the next step's
+// operands loaded into registers while the current one is multiplied.  LDS rows of 144 floats
+// put the four k rows an MFMA fragment reads 16 banks apart.  MFMA layout (lane l): A row l & 15
+// at k = l >> 4, B column l & 15 at k = l >> 4, D rows 4 (l >> 4) + i, column l & 15.
+typedef float v4f __attribute__((ext_vector_type(4)));
+constexpr int kMfTile = 128, kMfRow = kMfTile + 16, kMfK = 32, kMfPer = kMfK * kMfTile / 4 / kThreads;
+
+__device__ __forceinline__ float4 load4_if(const float *p, bool ok) {
+  float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (ok) v = *(const float4 *)p;
+  return v;
+}
+
+template <bool TA, bool TB>
+__global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
+  __shared__ __attribute__((aligned(16))) float As[kMfK][kMfRow];
+  __shared__ __attribute__((aligned(16))) float Bs[kMfK][kMfRow];
+  const float *__restrict__ A = g.A;
+  const float *__restrict__ B = g.B;
+  const int64_t M = g.M, N = g.N, lda = g.lda, ldb = g.ldb;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int64_t m0 = (int64_t)blockIdx.y * kMfTile, n0 = (int64_t)blockIdx.x * kMfTile;
+  const int64_t kb = (int64_t)blockIdx.z * g.kchunk, ke = std::min<int64_t>(g.K, kb + g.kchunk);
+  // Thread t stages float4 number t + 256 u (u < 4) of each 32 x 128 operand tile.  Stored
+  // k-major ([k][m] or [k][n]): k row (t >> 5) + 8 u, columns 4 (t & 31) .. +3.  Stored with k
+  // contiguous: tile row (t >> 3) + 32 u, k offsets 4 (t & 7) .. +3.
+  const int km_r = tid >> 5, km_c = (tid & 31) * 4, kc_r = tid >> 3, kc_k = (tid & 7) * 4;
+  float4 ra0, ra1, ra2, ra3, rb0, rb1, rb2, rb3;
+#define AECCT_MF_LOAD(k0)                                                                          \
+  do {                                                                                             \
+    if (TA) {                                                                                      \
+      const float *p = A + ((k0) + km_r) * lda + m0 + km_c;                                       \
+      const bool okc = m0 + km_c < M;                                                              \
+      ra0 = load4_if(p, okc && (k0) + km_r < ke);                                                  \
+      ra1 = load4_if(p + 8 * lda, okc && (k0) + km_r + 8 < ke);                                    \
+      ra2 = load4_if(p + 16 * lda, okc && (k0) + km_r + 16 < ke);                                  \
+      ra3 = load4_if(p + 24 * lda, okc && (k0) + km_r + 24 < ke);                                  \
+    } else {                                                                                       \
+      const float *p = A + (m0 + kc_r) * lda + (k0) + kc_k;                                       \
+      const bool okk = (k0) + kc_k < ke;                                                           \
+      ra0 = load4_if(p, okk && m0 + kc_r < M);                                                     \
+      ra1 = load4_if(p + 32 * lda, okk && m0 + kc_r + 32 < M);                                     \
+      ra2 = load4_if(p + 64 * lda, okk && m0 + kc_r + 64 < M);                                     \
+      ra3 = load4_if(p + 96 * lda, okk && m0 + kc_r + 96 < M);                                     \
+    }                                                                                              \
+    if (TB) {                                                                                      \
+      const float *p = B + (n0 + kc_r) * ldb + (k0) + kc_k;                                       \
+      const bool okk = (k0) + kc_k < ke;                                                           \
+      rb0 = load4_if(p, okk && n0 + kc_r < N);                                                     \
+      rb1 = load4_if(p + 32 * ldb, okk && n0 + kc_r + 32 < N);                                     \
+      rb2 = load4_if(p + 64 * ldb, okk && n0 + kc_r + 64 < N);                                     \
+      rb3 = load4_if(p + 96 * ldb, okk && n0 + kc_r + 96 < N);                                     \
+    } else {                                                                                       \
+      const float *p = B + ((k0) + km_r) * ldb + n0 + km_c;                                       \
+      const bool okc = n0 + km_c < N;                                                              \
+      rb0 = load4_if(p, okc && (k0) + km_r < ke);                                                  \
+      rb1 = load4_if(p + 8 * ldb, okc && (k0) + km_r + 8 < ke);                                    \
+      rb2 = load4_if(p + 16 * ldb, okc && (k0) + km_r + 16 < ke);                                  \
+      rb3 = load4_if(p + 24 * ldb, okc && (k0) + km_r + 24 < ke);                                  \
+    }                                                                                              \
+  } while (0)
+#define AECCT_MF_PUT_KM(S, u, v) *(float4 *)&S[km_r + 8 * (u)][km_c] = v
+#define AECCT_MF_PUT_KC(S, u, v)                                                                   \
+  do {                                                                                             \
+    S[kc_k][kc_r + 32 * (u)] = v.x;                                                                \
+    S[kc_k + 1][kc_r + 32 * (u)] = v.y;                                                            \
+    S[kc_k + 2][kc_r + 32 * (u)] = v.z;                                                            \
+    S[kc_k + 3][kc_r + 32 * (u)] = v.w;                                                            \
+  } while (0)
+  v4f acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  const int fr = lane >> 4, fc = lane & 15;
+  AECCT_MF_LOAD(kb);
+  for (int64_t k0 = kb; k0 < ke; k0 += kMfK) {
+    if (TA) {
+      AECCT_MF_PUT_KM(As, 0, ra0); AECCT_MF_PUT_KM(As, 1, ra1); AECCT_MF_PUT_KM(As, 2, ra2); AECCT_MF_PUT_KM(As, 3, ra3);
+    } else {
+      AECCT_MF_PUT_KC(As, 0, ra0); AECCT_MF_PUT_KC(As, 1, ra1); AECCT_MF_PUT_KC(As, 2, ra2); AECCT_MF_PUT_KC(As, 3, ra3);
+    }
+    if (TB) {
+      AECCT_MF_PUT_KC(Bs, 0, rb0); AECCT_MF_PUT_KC(Bs, 1, rb1); AECCT_MF_PUT_KC(Bs, 2, rb2); AECCT_MF_PUT_KC(Bs, 3, rb3);
+    } else {
+      AECCT_MF_PUT_KM(Bs, 0, rb0); AECCT_MF_PUT_KM(Bs, 1, rb1); AECCT_MF_PUT_KM(Bs, 2, rb2); AECCT_MF_PUT_KM(Bs, 3, rb3);
+    }
+    __syncthreads();
+    if (k0 + kMfK < ke) AECCT_MF_LOAD(k0 + kMfK);
+#pragma unroll
+    for (int ks = 0; ks < kMfK / 4; ++ks) {
+      float a[4], b[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        a[t] = As[4 * ks + fr][wm + 16 * t + fc];
+        b[t] = Bs[4 * ks + fr][wn + 16 * t + fc];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#undef AECCT_MF_LOAD
+#undef AECCT_MF_PUT_KM
+#undef AECCT_MF_PUT_KC
+  // split partial sums raw into their slice of part, else scale, bias and the optional C
+  const bool split = gridDim.z > 1;
+  float *const P = split ? g.part + (int64_t)blockIdx.z * M * N : g.C;
+  const int64_t ld = split ? N : g.ldc;
+  const float sc = (!split && g.scale) ? *g.scale : 1.0f;
+  const bool beta = !split && g.beta;
+  const float *bias = split ? nullptr : g.bias;
+  const bool full = m0 + kMfTile <= M && n0 + kMfTile <= N;
+  float bj[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t c = n0 + wn + 16 * j + fc;
+    bj[j] = (bias && c < N) ? bias[c] : 0.0f;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t r = m0 + wm + 16 * i + 4 * fr + v;
+      if (!full && r >= M) continue;
+      float *prow = P + r * ld + n0 + wn + fc;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (!full && n0 + wn + 16 * j + fc >= N) continue;
+        float o = sc * acc[i][j][v] + bj[j];
+        if (beta) o += prow[16 * j];
+        prow[16 * j] = o;
+      }
+    }
+}
+
+// Split-k partial products summed in a fixed order: a block covers 64 outputs, its four lanes per
+// output sum the splits z = lane, lane + 4, ... and are added in lane order.
 __global__ __launch_bounds__(kThreads) void k_gemm_reduce(GemmF32 g, int splits) {
-  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (e >= g.M * g.N) return;
+  __shared__ float red[4][64];
+  const int cl = threadIdx.x & 63, rl = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + cl, MN = g.M * g.N;
+  float s0 = 0.0f, s1 = 0.0f;
+  if (e < MN) {
+    int z = rl;
+    for (; z + 4 < splits; z += 8) {
+      s0 += g.part[(int64_t)z * MN + e];
+      s1 += g.part[(int64_t)(z + 4) * MN + e];
+    }
+    if (z < splits) s0 += g.part[(int64_t)z * MN + e];
+  }
+  red[rl][cl] = s0 + s1;
+  __syncthreads();
+  if (rl != 0 || e >= MN) return;
+  const float s = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
   const int64_t r = e / g.N, c = e - r * g.N;
-  float s = 0.0f;
-  for (int z = 0; z < splits; ++z) s += g.part[(int64_t)z * g.M * g.N + e];
   float v = (g.scale ? *g.scale : 1.0f) * s + (g.bias ? g.bias[c] : 0.0f);
   if (g.beta) v += g.C[r * g.ldc + c];
   g.C[r * g.ldc + c] = v;
@@ -663,22 +818,38 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
                       float *part, int64_t part_floats, int cu_count, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   train::GemmF32 g{A, B, C, M, N, K, lda, ldb, ldc, K, scale, bias, accumulate ? 1 : 0, part};
-  const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  // the MFMA kernel reads 16-byte vectors along each operand's contiguous dimension
+  auto al16 = [](const float *p) { return ((uintptr_t)p & 15u) == 0; };
+  const bool mfma = al16(A) && al16(B) && lda % 4 == 0 && ldb % 4 == 0 && (ta ? M : K) % 4 == 0 &&
+                    (tb ? K : N) % 4 == 0;
+  const int64_t tile = mfma ? train::kMfTile : 64;
+  const int64_t tiles = ((M + tile - 1) / tile) * ((N + tile - 1) / tile);
   // split long reductions over k so that about two blocks per compute unit are busy
   int64_t splits = std::max<int64_t>(1, std::min<int64_t>((2 * (int64_t)cu_count + tiles - 1) / tiles, (K + 255) / 256));
   splits = std::min<int64_t>(splits, part_floats / (M * N));
   if (splits < 1) splits = 1;
-  g.kchunk = (((K + splits - 1) / splits) + 15) / 16 * 16;
-  if (g.kchunk < 16) g.kchunk = 16;
+  const int64_t kq = mfma ? train::kMfK : 16;
+  g.kchunk = (((K + splits - 1) / splits) + kq - 1) / kq * kq;
+  if (g.kchunk < kq) g.kchunk = kq;
   splits = (K + g.kchunk - 1) / g.kchunk;
   if (splits < 1) splits = 1;
-  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)splits);
-  if (ta && tb) hipLaunchKernelGGL((train::k_gemm<true, true>), grid, dim3(train::kThreads), 0, s, g);
-  else if (ta) hipLaunchKernelGGL((train::k_gemm<true, false>), grid, dim3(train::kThreads), 0, s, g);
-  else if (tb) hipLaunchKernelGGL((train::k_gemm<false, true>), grid, dim3(train::kThreads), 0, s, g);
-  else hipLaunchKernelGGL((train::k_gemm<false, false>), grid, dim3(train::kThreads), 0, s, g);
+  const dim3 grid((unsigned)((N + tile - 1) / tile), (unsigned)((M + tile - 1) / tile), (unsigned)splits);
+  if (mfma) {
+    if (ta && tb) hipLaunchKernelGGL((train::k_gemm_mfma<true, true>), grid, dim3(train::kThreads), 0, s, g);
+    else if (ta) hipLaunchKernelGGL((train::k_gemm_mfma<true, false>), grid, dim3(train::kThreads), 0, s, g);
+    else if (tb) hipLaunchKernelGGL((train::k_gemm_mfma<false, true>), grid, dim3(train::kThreads), 0, s, g);
+    else hipLaunchKernelGGL((train::k_gemm_mfma<false, false>), grid, dim3(train::kThreads), 0, s, g);
+  } else if (ta && tb) {
+    hipLaunchKernelGGL((train::k_gemm<true, true>), grid, dim3(train::kThreads), 0, s, g);
+  } else if (ta) {
+    hipLaunchKernelGGL((train::k_gemm<true, false>), grid, dim3(train::kThreads), 0, s, g);
+  } else if (tb) {
+    hipLaunchKernelGGL((train::k_gemm<false, true>), grid, dim3(train::kThreads), 0, s, g);
+  } else {
+    hipLaunchKernelGGL((train::k_gemm<false, false>), grid, dim3(train::kThreads), 0, s, g);
+  }
   if (splits > 1)
-    hipLaunchKernelGGL(train::k_gemm_reduce, dim3(blocks_for(M * N, train::kThreads)), dim3(train::kThreads), 0, s, g,
+    hipLaunchKernelGGL(train::k_gemm_reduce, dim3(blocks_for(M * N, 64)), dim3(train::kThreads), 0, s, g,
                        (int)splits);
   return hipGetLastError();
 }
