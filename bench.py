@@ -269,6 +269,11 @@ def train_bench(c: int, batch: int, steps: int, warmup: int):
                       "config": {"workload": f"qat_{cfg.name}_batch{batch}", "tokens": L, "d": d, "layers": N,
                                  "batch": batch},
                       "gemm_fma_per_step": fma, "gemm_fma_rate_T": fma / (ms * 1e-3) / 1e12,
+                      # fp32 MFMA roofline of the step's products: every GEMM flop over the whole
+                      # step time (a lower bound of the GEMM kernels' own rate)
+                      "roofline": {"bound": "mfma", "kernel": "k_gemm_mfma (all step GEMMs, whole-step time)",
+                                   "achieved": 2 * fma / (ms * 1e-3) / 1e12, "peak": 157.3, "unit": "TFLOP/s",
+                                   "frac": 2 * fma / (ms * 1e-3) / 1e12 / 157.3, "traffic": None},
                       "cpu_baseline": {"value": k / dt, "unit": "codewords/s", "cores": 1, "kind": "oracle",
                                        "sample": f"{k} words, float64 numpy oracle, {dt:.2f} s"}}), flush=True)
 

@@ -128,8 +128,9 @@ def with_positional_table(w: ModelWeights, table: np.ndarray, d_pe: int) -> Mode
 def random_qat_params(n: int, m: int, d: int, n_layers: int, *, seed: int = 0, d_ff: int | None = None,
                       latent_std: float | None = None, delta_spread: float = 0.05) -> dict:
     """Seeded parameters of the quantisation-aware training phase (Section 6): latent fp32 weights
-    of the six in-block maps per layer ~ N(0, latent_std^2) (default 1/d, so that Eq. 1's scale
-    gamma*delta is of the size of the inference weights' 1/sqrt(d)), the learnable factors delta
+    of the six in-block maps per layer ~ N(0, latent_std^2) (default latent_std = 1/sqrt(d), so that
+    Eq. 1's scale gamma*delta, about 0.67/sqrt(d), is of the size of the inference weights' scale),
+    the learnable factors delta
     = 1 + N(0, delta_spread^2) (the paper initialises them to one), and the other parameters drawn
     as in random_weights.  fp32 arrays in a dict: embed, pos (None), w[kind], delta [N, 6],
     b[kind], ln1_g, ln1_b, ln2_g, ln2_b, head_w1, head_b1, head_wo, head_bo."""
