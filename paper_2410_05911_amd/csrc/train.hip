@@ -277,13 +277,14 @@ __global__ __launch_bounds__(kThreads) void k_gemm(GemmF32 g) {
 }
 
 // The same product on v_mfma_f32_16x16x4_f32 for operands whose contiguous dimension and leading
-// dimensions are multiples of 4 floats (16-byte loads): blocks of 128 x 128 outputs, four
-// wavefronts of 64 x 64 (4 x 4 MFMA tiles), k-steps of 32 staged through LDS, the next step's
-// operands loaded into registers while the current one is multiplied.  LDS rows of 144 floats
-// put the four k rows an MFMA fragment reads 16 banks apart.  MFMA layout (lane l): A row l & 15
-// at k = l >> 4, B column l & 15 at k = l >> 4, D rows 4 (l >> 4) + i, column l & 15.
+// dimensions are multiples of 4 floats (16-byte loads): blocks of BM x 128 outputs (BM = 128, or 64
+// for short reductions, which then get twice the blocks), four wavefronts of BM / 2 x 64
+// (BM / 32 x 4 MFMA tiles), k-steps of 32 staged through LDS, the next step's operands loaded into
+// registers while the current one is multiplied.  LDS rows of BM + 16 and 144 floats put the four k
+// rows an MFMA fragment reads 16 banks apart.  MFMA layout (lane l): A row l & 15 at k = l >> 4,
+// B column l & 15 at k = l >> 4, D rows 4 (l >> 4) + i, column l & 15.
 typedef float v4f __attribute__((ext_vector_type(4)));
-constexpr int kMfTile = 128, kMfRow = kMfTile + 16, kMfK = 32, kMfPer = kMfK * kMfTile / 4 / kThreads;
+constexpr int kMfTile = 128, kMfK = 32;
 
 __device__ __forceinline__ float4 load4_if(const float *p, bool ok) {
   float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -291,101 +292,110 @@ __device__ __forceinline__ float4 load4_if(const float *p, bool ok) {
   return v;
 }
 
-template <bool TA, bool TB>
+template <bool TA, bool TB, int BM>
 __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
-  __shared__ __attribute__((aligned(16))) float As[kMfK][kMfRow];
-  __shared__ __attribute__((aligned(16))) float Bs[kMfK][kMfRow];
+  constexpr int BN = kMfTile, AP = BM / 32, BP = BN / 32, TM = BM / 32;
+  __shared__ __attribute__((aligned(16))) float As[kMfK][BM + 16];
+  __shared__ __attribute__((aligned(16))) float Bs[kMfK][BN + 16];
   const float *__restrict__ A = g.A;
   const float *__restrict__ B = g.B;
   const int64_t M = g.M, N = g.N, lda = g.lda, ldb = g.ldb;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
-  const int64_t m0 = (int64_t)blockIdx.y * kMfTile, n0 = (int64_t)blockIdx.x * kMfTile;
+  const int wm = (wave >> 1) * (BM / 2), wn = (wave & 1) * 64;
+  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
   const int64_t kb = (int64_t)blockIdx.z * g.kchunk, ke = std::min<int64_t>(g.K, kb + g.kchunk);
-  // Thread t stages float4 number t + 256 u (u < 4) of each 32 x 128 operand tile.  Stored
-  // k-major ([k][m] or [k][n]): k row (t >> 5) + 8 u, columns 4 (t & 31) .. +3.  Stored with k
-  // contiguous: tile row (t >> 3) + 32 u, k offsets 4 (t & 7) .. +3.
-  const int km_r = tid >> 5, km_c = (tid & 31) * 4, kc_r = tid >> 3, kc_k = (tid & 7) * 4;
-  float4 ra0, ra1, ra2, ra3, rb0, rb1, rb2, rb3;
-#define AECCT_MF_LOAD(k0)                                                                          \
-  do {                                                                                             \
-    if (TA) {                                                                                      \
-      const float *p = A + ((k0) + km_r) * lda + m0 + km_c;                                       \
-      const bool okc = m0 + km_c < M;                                                              \
-      ra0 = load4_if(p, okc && (k0) + km_r < ke);                                                  \
-      ra1 = load4_if(p + 8 * lda, okc && (k0) + km_r + 8 < ke);                                    \
-      ra2 = load4_if(p + 16 * lda, okc && (k0) + km_r + 16 < ke);                                  \
-      ra3 = load4_if(p + 24 * lda, okc && (k0) + km_r + 24 < ke);                                  \
-    } else {                                                                                       \
-      const float *p = A + (m0 + kc_r) * lda + (k0) + kc_k;                                       \
-      const bool okk = (k0) + kc_k < ke;                                                           \
-      ra0 = load4_if(p, okk && m0 + kc_r < M);                                                     \
-      ra1 = load4_if(p + 32 * lda, okk && m0 + kc_r + 32 < M);                                     \
-      ra2 = load4_if(p + 64 * lda, okk && m0 + kc_r + 64 < M);                                     \
-      ra3 = load4_if(p + 96 * lda, okk && m0 + kc_r + 96 < M);                                     \
-    }                                                                                              \
-    if (TB) {                                                                                      \
-      const float *p = B + (n0 + kc_r) * ldb + (k0) + kc_k;                                       \
-      const bool okk = (k0) + kc_k < ke;                                                           \
-      rb0 = load4_if(p, okk && n0 + kc_r < N);                                                     \
-      rb1 = load4_if(p + 32 * ldb, okk && n0 + kc_r + 32 < N);                                     \
-      rb2 = load4_if(p + 64 * ldb, okk && n0 + kc_r + 64 < N);                                     \
-      rb3 = load4_if(p + 96 * ldb, okk && n0 + kc_r + 96 < N);                                     \
-    } else {                                                                                       \
-      const float *p = B + ((k0) + km_r) * ldb + n0 + km_c;                                       \
-      const bool okc = n0 + km_c < N;                                                              \
-      rb0 = load4_if(p, okc && (k0) + km_r < ke);                                                  \
-      rb1 = load4_if(p + 8 * ldb, okc && (k0) + km_r + 8 < ke);                                    \
-      rb2 = load4_if(p + 16 * ldb, okc && (k0) + km_r + 16 < ke);                                  \
-      rb3 = load4_if(p + 24 * ldb, okc && (k0) + km_r + 24 < ke);                                  \
-    }                                                                                              \
-  } while (0)
-#define AECCT_MF_PUT_KM(S, u, v) *(float4 *)&S[km_r + 8 * (u)][km_c] = v
-#define AECCT_MF_PUT_KC(S, u, v)                                                                   \
-  do {                                                                                             \
-    S[kc_k][kc_r + 32 * (u)] = v.x;                                                                \
-    S[kc_k + 1][kc_r + 32 * (u)] = v.y;                                                            \
-    S[kc_k + 2][kc_r + 32 * (u)] = v.z;                                                            \
-    S[kc_k + 3][kc_r + 32 * (u)] = v.w;                                                            \
-  } while (0)
-  v4f acc[4][4];
+  // Thread t stages float4 number t + 256 u of each 32 x W operand tile (W = BM or 128).  Stored
+  // k-major ([k][m] or [k][n]): k row t / (W / 4) + u 1024 / W, columns 4 (t mod W / 4) .. +3.
+  // Stored with k contiguous: tile row (t >> 3) + 32 u, k offsets 4 (t & 7) .. +3.
+  const int kmA_r = tid / (BM / 4), kmA_c = (tid % (BM / 4)) * 4, kmB_r = tid >> 5, kmB_c = (tid & 31) * 4;
+  const int kc_r = tid >> 3, kc_k = (tid & 7) * 4;
+  float4 ra[AP], rb[BP];
+  v4f acc[TM][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
   const int fr = lane >> 4, fc = lane & 15;
-  AECCT_MF_LOAD(kb);
-  for (int64_t k0 = kb; k0 < ke; k0 += kMfK) {
-    if (TA) {
-      AECCT_MF_PUT_KM(As, 0, ra0); AECCT_MF_PUT_KM(As, 1, ra1); AECCT_MF_PUT_KM(As, 2, ra2); AECCT_MF_PUT_KM(As, 3, ra3);
-    } else {
-      AECCT_MF_PUT_KC(As, 0, ra0); AECCT_MF_PUT_KC(As, 1, ra1); AECCT_MF_PUT_KC(As, 2, ra2); AECCT_MF_PUT_KC(As, 3, ra3);
-    }
-    if (TB) {
-      AECCT_MF_PUT_KC(Bs, 0, rb0); AECCT_MF_PUT_KC(Bs, 1, rb1); AECCT_MF_PUT_KC(Bs, 2, rb2); AECCT_MF_PUT_KC(Bs, 3, rb3);
-    } else {
-      AECCT_MF_PUT_KM(Bs, 0, rb0); AECCT_MF_PUT_KM(Bs, 1, rb1); AECCT_MF_PUT_KM(Bs, 2, rb2); AECCT_MF_PUT_KM(Bs, 3, rb3);
-    }
-    __syncthreads();
-    if (k0 + kMfK < ke) AECCT_MF_LOAD(k0 + kMfK);
+  for (int64_t k0 = kb, first = 1; k0 < ke; k0 += kMfK, first = 0) {
+    if (first) {
+      // the first step's operands (later steps' were read during the previous step)
 #pragma unroll
-    for (int ks = 0; ks < kMfK / 4; ++ks) {
-      float a[4], b[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        a[t] = As[4 * ks + fr][wm + 16 * t + fc];
-        b[t] = Bs[4 * ks + fr][wn + 16 * t + fc];
+      for (int u = 0; u < AP; ++u) {
+        if (TA) {
+          const int64_t gk = k0 + kmA_r + u * (1024 / BM);
+          ra[u] = load4_if(A + gk * lda + m0 + kmA_c, gk < ke && m0 + kmA_c < M);
+        } else {
+          const int64_t gm = m0 + kc_r + 32 * u;
+          ra[u] = load4_if(A + gm * lda + k0 + kc_k, gm < M && k0 + kc_k < ke);
+        }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int u = 0; u < BP; ++u) {
+        if (TB) {
+          const int64_t gn = n0 + kc_r + 32 * u;
+          rb[u] = load4_if(B + gn * ldb + k0 + kc_k, gn < N && k0 + kc_k < ke);
+        } else {
+          const int64_t gk = k0 + kmB_r + 8 * u;
+          rb[u] = load4_if(B + gk * ldb + n0 + kmB_c, gk < ke && n0 + kmB_c < N);
+        }
+      }
+    }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    for (int u = 0; u < AP; ++u) {
+      if (TA) {
+        *(float4 *)&As[kmA_r + u * (1024 / BM)][kmA_c] = ra[u];
+      } else {
+        const int mm = kc_r + 32 * u;
+        As[kc_k][mm] = ra[u].x; As[kc_k + 1][mm] = ra[u].y; As[kc_k + 2][mm] = ra[u].z; As[kc_k + 3][mm] = ra[u].w;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < BP; ++u) {
+      if (TB) {
+        const int nn = kc_r + 32 * u;
+        Bs[kc_k][nn] = rb[u].x; Bs[kc_k + 1][nn] = rb[u].y; Bs[kc_k + 2][nn] = rb[u].z; Bs[kc_k + 3][nn] = rb[u].w;
+      } else {
+        *(float4 *)&Bs[kmB_r + 8 * u][kmB_c] = rb[u];
+      }
+    }
+    __syncthreads();
+    const int64_t k1 = k0 + kMfK;
+    if (k1 < ke) {
+#pragma unroll
+      for (int u = 0; u < AP; ++u) {
+        if (TA) {
+          const int64_t gk = k1 + kmA_r + u * (1024 / BM);
+          ra[u] = load4_if(A + gk * lda + m0 + kmA_c, gk < ke && m0 + kmA_c < M);
+        } else {
+          const int64_t gm = m0 + kc_r + 32 * u;
+          ra[u] = load4_if(A + gm * lda + k1 + kc_k, gm < M && k1 + kc_k < ke);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < BP; ++u) {
+        if (TB) {
+          const int64_t gn = n0 + kc_r + 32 * u;
+          rb[u] = load4_if(B + gn * ldb + k1 + kc_k, gn < N && k1 + kc_k < ke);
+        } else {
+          const int64_t gk = k1 + kmB_r + 8 * u;
+          rb[u] = load4_if(B + gk * ldb + n0 + kmB_c, gk < ke && n0 + kmB_c < N);
+        }
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < kMfK / 4; ++ks) {
+      float av[TM], bv[4];
+#pragma unroll
+      for (int t = 0; t < TM; ++t) av[t] = As[4 * ks + fr][wm + 16 * t + fc];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) bv[t] = Bs[4 * ks + fr][wn + 16 * t + fc];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
-#undef AECCT_MF_LOAD
-#undef AECCT_MF_PUT_KM
-#undef AECCT_MF_PUT_KC
   // split partial sums raw into their slice of part, else scale, bias and the optional C
   const bool split = gridDim.z > 1;
   float *const P = split ? g.part + (int64_t)blockIdx.z * M * N : g.C;
@@ -393,7 +403,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
   const float sc = (!split && g.scale) ? *g.scale : 1.0f;
   const bool beta = !split && g.beta;
   const float *bias = split ? nullptr : g.bias;
-  const bool full = m0 + kMfTile <= M && n0 + kMfTile <= N;
+  const bool full = m0 + BM <= M && n0 + BN <= N;
   float bj[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -401,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
     bj[j] = (bias && c < N) ? bias[c] : 0.0f;
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t r = m0 + wm + 16 * i + 4 * fr + v;
@@ -822,8 +832,9 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
   auto al16 = [](const float *p) { return ((uintptr_t)p & 15u) == 0; };
   const bool mfma = al16(A) && al16(B) && lda % 4 == 0 && ldb % 4 == 0 && (ta ? M : K) % 4 == 0 &&
                     (tb ? K : N) % 4 == 0;
-  const int64_t tile = mfma ? train::kMfTile : 64;
-  const int64_t tiles = ((M + tile - 1) / tile) * ((N + tile - 1) / tile);
+  // reductions of at most 256 get 64-row tiles: twice the blocks to cover their short k loops
+  const int64_t tm = mfma ? (K <= 256 ? 64 : train::kMfTile) : 64, tn = mfma ? train::kMfTile : 64;
+  const int64_t tiles = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
   // split long reductions over k so that about two blocks per compute unit are busy
   int64_t splits = std::max<int64_t>(1, std::min<int64_t>((2 * (int64_t)cu_count + tiles - 1) / tiles, (K + 255) / 256));
   splits = std::min<int64_t>(splits, part_floats / (M * N));
@@ -833,12 +844,18 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
   if (g.kchunk < kq) g.kchunk = kq;
   splits = (K + g.kchunk - 1) / g.kchunk;
   if (splits < 1) splits = 1;
-  const dim3 grid((unsigned)((N + tile - 1) / tile), (unsigned)((M + tile - 1) / tile), (unsigned)splits);
+  const dim3 grid((unsigned)((N + tn - 1) / tn), (unsigned)((M + tm - 1) / tm), (unsigned)splits);
   if (mfma) {
-    if (ta && tb) hipLaunchKernelGGL((train::k_gemm_mfma<true, true>), grid, dim3(train::kThreads), 0, s, g);
-    else if (ta) hipLaunchKernelGGL((train::k_gemm_mfma<true, false>), grid, dim3(train::kThreads), 0, s, g);
-    else if (tb) hipLaunchKernelGGL((train::k_gemm_mfma<false, true>), grid, dim3(train::kThreads), 0, s, g);
-    else hipLaunchKernelGGL((train::k_gemm_mfma<false, false>), grid, dim3(train::kThreads), 0, s, g);
+#define AECCT_MF_GO(TA_, TB_)                                                                          \
+  do {                                                                                                 \
+    if (tm == 64) hipLaunchKernelGGL((train::k_gemm_mfma<TA_, TB_, 64>), grid, dim3(train::kThreads), 0, s, g); \
+    else hipLaunchKernelGGL((train::k_gemm_mfma<TA_, TB_, 128>), grid, dim3(train::kThreads), 0, s, g);        \
+  } while (0)
+    if (ta && tb) AECCT_MF_GO(true, true);
+    else if (ta) AECCT_MF_GO(true, false);
+    else if (tb) AECCT_MF_GO(false, true);
+    else AECCT_MF_GO(false, false);
+#undef AECCT_MF_GO
   } else if (ta && tb) {
     hipLaunchKernelGGL((train::k_gemm<true, true>), grid, dim3(train::kThreads), 0, s, g);
   } else if (ta) {
