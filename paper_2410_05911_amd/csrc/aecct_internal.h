@@ -203,9 +203,10 @@ struct TrainAttn {
   float *dqkv;          // [rows][3d] gradients of Q | K | V (backward)
   float *Dv;            // [rows][heads] dO . O (backward)
 };
-// the six maps of one layer per launch, passed by value
-struct TrainAapJobs { TrainAapJob j[6]; };
-struct TrainDeltaJobs { TrainDeltaJob j[6]; };
+// the six maps of up to eight layers per launch (one block per matrix), passed by value
+constexpr int kTrainJobsPerLaunch = 48;
+struct TrainAapJobs { TrainAapJob j[kTrainJobsPerLaunch]; int n; };
+struct TrainDeltaJobs { TrainDeltaJob j[kTrainJobsPerLaunch]; int n; };
 hipError_t train_aap(const TrainAapJobs &jobs, float eps, hipStream_t s);
 hipError_t train_delta_grad(const TrainDeltaJobs &jobs, float eps, hipStream_t s);
 hipError_t train_embed(const float *y, int64_t rows, int n, int L, int d, const int32_t *chk_ptr,

@@ -799,12 +799,14 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 }
 
 hipError_t train_aap(const TrainAapJobs &jobs, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(train::k_aap, dim3(6), dim3(train::kAapThreads), 0, s, jobs, eps);
+  if (jobs.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_aap, dim3((unsigned)jobs.n), dim3(train::kAapThreads), 0, s, jobs, eps);
   return hipGetLastError();
 }
 
 hipError_t train_delta_grad(const TrainDeltaJobs &jobs, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(train::k_delta_grad, dim3(6), dim3(train::kAapThreads), 0, s, jobs, eps);
+  if (jobs.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(train::k_delta_grad, dim3((unsigned)jobs.n), dim3(train::kAapThreads), 0, s, jobs, eps);
   return hipGetLastError();
 }
 

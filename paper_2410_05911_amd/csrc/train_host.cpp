@@ -1,6 +1,7 @@
 // Host side of the quantisation-aware training step (Section 6, second phase): validation, the
 // Tanner-graph lists on the device, the workspace layout and the launch sequence of one forward
 // and backward pass.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -220,11 +221,14 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
   } while (0)
 
   // ---- forward -------------------------------------------------------------------------------
-  for (int l = 0; l < N; ++l) {
+  // Eq. 1 of every layer's six matrices first (they depend on the weights only), a launch per
+  // eight layers
+  for (int l0 = 0; l0 < N; l0 += kTrainJobsPerLaunch / 6) {
     TrainAapJobs jobs{};
-    for (int k = 0; k < 6; ++k)
-      jobs.j[k] = TrainAapJob{pw[k] + wofs(l, k), tmat(l, k), K_in[k] * K_out[k], p->delta + 6 * l + k,
-                              gam + 6 * l + k, sc + 6 * l + k};
+    for (int l = l0; l < std::min(N, l0 + kTrainJobsPerLaunch / 6); ++l)
+      for (int k = 0; k < 6; ++k)
+        jobs.j[jobs.n++] = TrainAapJob{pw[k] + wofs(l, k), tmat(l, k), K_in[k] * K_out[k], p->delta + 6 * l + k,
+                                       gam + 6 * l + k, sc + 6 * l + k};
     AECCT_TRY(train_aap(jobs, T.aap_eps, s));
   }
   float *X = ws + W.x, *X1 = ws + W.x1, *Y = ws + W.y, *tv = ws + W.t;
@@ -307,10 +311,15 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
       AECCT_TRY(colsum(dQKV + k * d, 3 * d, nullptr, nullptr, R, d, gb[k] + ld_));
       AECCT_TRY(gemm(false, true, dQKV + k * d, 3 * d, tmat(l, k), d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
     }
+  }
+  // the straight-through Eq. 1 gradients of every matrix from its G = Xh^T dY (nothing in the
+  // backward reads G once it is formed), a launch per eight layers
+  for (int l0 = 0; l0 < N; l0 += kTrainJobsPerLaunch / 6) {
     TrainDeltaJobs dj{};
-    for (int k = 0; k < 6; ++k)
-      dj.j[k] = TrainDeltaJob{gw[k] + wofs(l, k), pw[k] + wofs(l, k), tmat(l, k), K_in[k] * K_out[k], gam + 6 * l + k,
-                              sc + 6 * l + k, g->delta + 6 * l + k};
+    for (int l = l0; l < std::min(N, l0 + kTrainJobsPerLaunch / 6); ++l)
+      for (int k = 0; k < 6; ++k)
+        dj.j[dj.n++] = TrainDeltaJob{gw[k] + wofs(l, k), pw[k] + wofs(l, k), tmat(l, k), K_in[k] * K_out[k],
+                                     gam + 6 * l + k, sc + 6 * l + k, g->delta + 6 * l + k};
     AECCT_TRY(train_delta_grad(dj, T.aap_eps, s));
   }
   AECCT_TRY(train_embed_grad(tv, dX, B, T.L, d, g->embed, s));
