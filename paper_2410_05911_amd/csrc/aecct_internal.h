@@ -124,8 +124,11 @@ hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, flo
                             hipStream_t s);
 // Q/K/V projection and attention fused per word, one 16-dimension head group at a time, into
 // fp32 O, then (when oq is not null) Eq. 2 per token of O: the layered decode's path for
-// d = 64, 128 when L tokens' Q, K, V of a group fit LDS.
+// d = 64, 128 when L tokens' Q, K, V of a group fit LDS.  Where the lane-pair form holds a row's
+// outputs of every group in registers (qkv_attention_pair_quantises: d = 128, 16-dimension heads,
+// at most 384 tokens) and oq is given, the kernel writes only the codes and scales (o unused).
 bool qkv_attention_supported(const Model &M);
+bool qkv_attention_pair_quantises(const Model &M);
 hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t words,
                                 float *o, int8_t *oq, float *ao, bool lane_order, hipStream_t s);
 // The same with keys and values kept in LDS as int16 accumulators (words too long for the fp32

@@ -1078,13 +1078,16 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
   // With the token block, X and Xq are kept in its lane order from the embedding to the head.
   // The fused projection + attention (keys and values in LDS as fp32, or as int16 accumulators
   // for long words) leaves O in fp32 (in the QKV space); the token block then applies Eq. 2
-  // itself. The unfused attention quantises O as it writes it (a quarter of the bytes).  With one
+  // itself. The lane-pair form on words of at most 384 tokens and the unfused attention quantise
+  // O as they write it (a quarter of the bytes).  With one
   // alpha per word every quantisation point is redone over the whole word from the fp32 values
   // (natural layout, unfused form, no token block).
   const bool pw = M.act_word != 0;
   const bool tb = !pw && aecct::token_block_supported(M);
   const bool qa = M.lattn == AECCT_LAYERED_ATTN_LDS_F32, qw = M.lattn == AECCT_LAYERED_ATTN_LDS_I16;
   const bool qs = M.lattn == AECCT_LAYERED_ATTN_LDS_SPLIT;
+  // the lane-pair form that writes O as Eq. 2 codes, which the token block then takes as they are
+  const bool qa_codes = qa && tb && aecct::qkv_attention_pair_quantises(M);
   for (int64_t w0 = 0; w0 < batch; w0 += cw) {
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
@@ -1092,7 +1095,7 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
     if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x, nw, M.d, false, xq, ax, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
       if (qa) {
-        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb ? nullptr : oq, ao, tb, s);
+        e = aecct::launch_qkv_attention(M, l, xq, ax, nw, qkv, tb && !qa_codes ? nullptr : oq, ao, tb, s);
       } else if (qw) {
         e = aecct::launch_qkv_attention_i16(M, l, xq, ax, nw, qkv, tb, s);
       } else if (qs) {
@@ -1104,7 +1107,7 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
       }
       if (e != hipSuccess) break;
       if (tb) {
-        e = qa || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
+        e = (qa && !qa_codes) || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
                      : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);

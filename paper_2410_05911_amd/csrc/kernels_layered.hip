@@ -365,6 +365,10 @@ struct QkvAttnArgs {
   const int2 *meta1, *meta2;   // per token: first group, entry count (first ring, second ring)
   const uint2 *tab1, *tab2;    // four 16-bit token indices per group
   float *o;                    // [rows][d]
+  // k_qkv_attention_pair with the quantised output: Eq. 2 codes [rows][d] and scales [rows] of
+  // O instead of o
+  int8_t *oq;
+  float *ao;
   int resident;                // k_qkv_attention: every head group's weight tiles stay in LDS
   // k_qkv_attention_split: the same lists with every entry counted from the first token of its
   // node type (variables from 0, checks from n), the variable count n, and the LDS capacity in
@@ -683,6 +687,15 @@ constexpr int kQpTilesPerWave = 3;
 // during the previous word's last group of rows.
 constexpr bool kQpWordLoads = true;
 
+// Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
+__device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
+  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
+  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
+  return (long)(((uint64_t)hi << 32) | lo);
+}
+
 // the partner lane's value (lane ^ 1) within the quad
 __device__ __forceinline__ float pair_other(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, true));
@@ -703,7 +716,7 @@ __device__ __forceinline__ void qp_step(const float (&q)[8], const float (&k)[8]
 // half; entries as in qa_row, the first group in g0.  Both lanes of a pair run it with the same
 // row.
 __device__ __forceinline__ void qp_row_q(const float (&q)[8], const float *kb, const uint2 *eg, uint2 g0, int cnt,
-                                         float *orow) {
+                                         float (&out)[8]) {
   constexpr int R = kQaRow;
   float S_ = 0.0f, acc[8];
 #pragma unroll
@@ -751,21 +764,27 @@ __device__ __forceinline__ void qp_row_q(const float (&q)[8], const float *kb, c
     }
   }
   const float rS = cnt > 0 ? recip_softmax_sum(S_) : 0.0f;
-  *(float4 *)orow = make_float4(acc[0] * rS, acc[1] * rS, acc[2] * rS, acc[3] * rS);
-  *(float4 *)(orow + 4) = make_float4(acc[4] * rS, acc[5] * rS, acc[6] * rS, acc[7] * rS);
+#pragma unroll
+  for (int t = 0; t < 8; ++t) out[t] = acc[t] * rS;
 }
 
-// The same with the query half read from qrow first.
+// The same with the query half read from qrow first and the outputs stored to orow.
 __device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const uint2 *eg, uint2 g0, int cnt,
                                        float *orow) {
-  float q[8];
+  float q[8], out[8];
   qa_load<8>(q, qrow);
-  qp_row_q(q, kb, eg, g0, cnt, orow);
+  qp_row_q(q, kb, eg, g0, cnt, out);
+  *(float4 *)orow = make_float4(out[0], out[1], out[2], out[3]);
+  *(float4 *)(orow + 4) = make_float4(out[4], out[5], out[6], out[7]);
 }
 
-template <int D>
+// OQ: a word of at most 384 tokens (one row per lane pair) keeps each row's outputs of all head
+// groups in registers (64 per lane) and writes the row's Eq. 2 codes and scale once the last
+// group is done, so the token block reads a quarter of the bytes; else fp32 rows per group.
+template <int D, bool OQ>
 __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArgs p) {
-  constexpr int S = D / 32, G = D / 16, TW = kQpTilesPerWave, NWV = kQpThreads / 64, FW = 3 * S * 64;
+  // token tiles per wave: 384 tokens take two of the 12 waves' tiles
+  constexpr int S = D / 32, G = D / 16, TW = OQ ? 2 : kQpTilesPerWave, NWV = kQpThreads / 64, FW = 3 * S * 64;
   static_assert(D == 128, "16-dimension heads, one per head group");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int L = p.L, ntiles = (L + 15) / 16;
@@ -780,60 +799,104 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
     st.store(bfa + hg * FW, tid);
   }
   for (int u = tid; u < 3 * D; u += kQpThreads) bl[u] = p.bias[u];
-  // this pair's first row (token tid / 2): list metadata of both masks held for the kernel
+  // this pair's first row (token tid / 2): list metadata of both masks held for the kernel, in
+  // registers, or with the quantised output (whose row outputs take 64 registers) in LDS
   const int r0 = tid >> 1, i0 = r0 < L ? r0 : 0;
-  const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
-  const uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
+  int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
+  uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
+  uint4 *mdl = (uint4 *)(bl + 3 * D) + 2 * tid;
+  if constexpr (OQ) {
+    mdl[0] = make_uint4((uint32_t)mt1.x, (uint32_t)mt1.y, (uint32_t)mt2.x, (uint32_t)mt2.y);
+    mdl[1] = make_uint4(g01.x, g01.y, g02.x, g02.y);
+  }
   __syncthreads();
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
-  if constexpr (!kQpWordLoads) {
-    const int64_t w = blockIdx.x;
-#pragma unroll
-    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wave + NWV * k, L, lane, afr[k], alw[k]);
-  }
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
-    if constexpr (kQpWordLoads) {
-      // the word's token tiles, waited for here: no global load is then outstanding inside the
-      // group loop, where a wait would also wait for the row outputs being written
-      int wv = wave;
-      __asm__ volatile("" : "+v"(wv));
+    // the word's token tiles, waited for here: no global load is then outstanding inside the
+    // group loop, where a wait would also wait for the row outputs being written
+    int wv = wave;
+    __asm__ volatile("" : "+v"(wv));
 #pragma unroll
-      for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wv + NWV * k, L, lane, afr[k], alw[k]);
+    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wv + NWV * k, L, lane, afr[k], alw[k]);
 #pragma unroll
-      for (int k = 0; k < TW; ++k) {
+    for (int k = 0; k < TW; ++k) {
 #pragma unroll
-        for (int s2 = 0; s2 < S; ++s2) __asm__ volatile("" : "+v"(afr[k][s2]));
-        __asm__ volatile("" : "+v"(alw[k][0]), "+v"(alw[k][1]), "+v"(alw[k][2]), "+v"(alw[k][3]));
-      }
+      for (int s2 = 0; s2 < S; ++s2) __asm__ volatile("" : "+v"(afr[k][s2]));
+      __asm__ volatile("" : "+v"(alw[k][0]), "+v"(alw[k][1]), "+v"(alw[k][2]), "+v"(alw[k][3]));
     }
-    for (int hg = 0; hg < G; ++hg) {
+    // head group hg: its Q, K, V into LDS, then its rows; row r0's outputs to out
+    auto group = [&](int hg, float (&out)[8]) {
       const uint64_t *bf = bfa + hg * FW;
       const float bq = bl[16 * hg + col], bk = bl[D + 16 * hg + col], bv = bl[2 * D + 16 * hg + col];
       int wg = wave;
       __asm__ volatile("" : "+v"(wg));
 #pragma unroll
-      for (int k = 0; k < TW; ++k)
+      for (int k = 0; k < TW; ++k) {
         if (wg + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wg + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
-      block_sync_lds();
-      const int64_t wn = w + gridDim.x;
-      if (!kQpWordLoads && hg == G - 1 && wn < p.words) {  // the next word's tiles, read during these rows
-#pragma unroll
-        for (int k = 0; k < TW; ++k)
-          qa_load_tile<D>(p.xq + wn * L * D, p.ax + wn * L, wave + NWV * k, L, lane, afr[k], alw[k]);
+        if constexpr (OQ) __builtin_amdgcn_sched_barrier(0);   // one tile's products at a time
       }
+      block_sync_lds();
       const bool first = hg < p.hf;
-      float *ow = p.o + w * L * D + hg * 16 + 8 * half;
-      if (r0 < L)
-        qp_row(qs + r0 * 16 + 8 * half, kv + 8 * half, (first ? p.tab1 : p.tab2) + (first ? mt1.x : mt2.x),
-               first ? g01 : g02, first ? mt1.y : mt2.y, ow + (size_t)r0 * D);
-      for (int r = r0 + kQpThreads / 2; r < L; r += kQpThreads / 2) {   // words of more than 384 tokens
-        const int2 mt = (first ? p.meta1 : p.meta2)[r];
-        const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
-        qp_row(qs + r * 16 + 8 * half, kv + 8 * half, eg, eg[0], mt.y, ow + (size_t)r * D);
+      if constexpr (OQ) {
+        uint32_t *mdp = (uint32_t *)mdl;
+        __asm__ volatile("" : "+v"(mdp));   // read here, not kept from the kernel's start
+        const uint4 m0 = *(const uint4 *)mdp, m1 = *(const uint4 *)(mdp + 4);
+        mt1 = make_int2((int)m0.x, (int)m0.y);
+        mt2 = make_int2((int)m0.z, (int)m0.w);
+        g01 = make_uint2(m1.x, m1.y);
+        g02 = make_uint2(m1.z, m1.w);
+      }
+      if (r0 < L) {
+        float q[8];
+        qa_load<8>(q, qs + r0 * 16 + 8 * half);
+        qp_row_q(q, kv + 8 * half, (first ? p.tab1 : p.tab2) + (first ? mt1.x : mt2.x), first ? g01 : g02,
+                 first ? mt1.y : mt2.y, out);
+      }
+      if constexpr (!OQ) {
+        float *ow = p.o + w * L * D + hg * 16 + 8 * half;
+        if (r0 < L) {
+          *(float4 *)(ow + (size_t)r0 * D) = make_float4(out[0], out[1], out[2], out[3]);
+          *(float4 *)(ow + (size_t)r0 * D + 4) = make_float4(out[4], out[5], out[6], out[7]);
+        }
+        for (int r = r0 + kQpThreads / 2; r < L; r += kQpThreads / 2) {   // words of more than 384 tokens
+          const int2 mt = (first ? p.meta1 : p.meta2)[r];
+          const uint2 *eg = (first ? p.tab1 : p.tab2) + mt.x;
+          qp_row(qs + r * 16 + 8 * half, kv + 8 * half, eg, eg[0], mt.y, ow + (size_t)r * D);
+        }
       }
       block_sync_lds();
+    };
+    if constexpr (OQ) {
+      float ko[G][8];
+#pragma unroll
+      for (int hg = 0; hg < G; ++hg) group(hg, ko[hg]);
+      if (r0 < L) {
+        // Eq. 2 of the row: alpha = max |O| over the pair's 2 x 64 features (the same value in
+        // both lanes), the codes of this lane's features 16 hg + 8 half + t
+        float om = 0.0f;
+#pragma unroll
+        for (int hg = 0; hg < G; ++hg)
+#pragma unroll
+          for (int t = 0; t < 8; ++t) om = fmaxf(om, fabsf(ko[hg][t]));
+        om = fmaxf(om, pair_other(om));
+        const float inv = inv127(om);
+        int8_t *orow = p.oq + (w * L + r0) * D + 8 * half;
+#pragma unroll
+        for (int hg = 0; hg < G; ++hg) {
+          uint32_t b[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) b[t] = quant_bits(ko[hg][t], inv);
+          *(long *)(orow + 16 * hg) = tb_pack8(b);
+        }
+        if (half == 0) p.ao[w * L + r0] = om;
+      }
+    } else {
+      for (int hg = 0; hg < G; ++hg) {
+        float out[8];
+        group(hg, out);
+      }
     }
   }
 }
@@ -1396,6 +1459,9 @@ struct TbIn {
         const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
         o[s][k] = f.x; o[s][k + 1] = f.y; o[s][k + 2] = f.z; o[s][k + 3] = f.w;
       }
+    load_x(p, tl, g);
+  }
+  __device__ __forceinline__ void load_x(const TokenBlockArgs &p, int64_t tl, int g) {
 #pragma unroll
     for (int u = 0; u < D / 4; u += 4) {
       const float4 r = *(const float4 *)(p.x + tl * D + g * (D / 4) + u);
@@ -1431,14 +1497,6 @@ __device__ __forceinline__ float tb_token_max(float a) {
   u = max(u, tb_lane_xor<32>(u));
   u = max(u, tb_lane_xor<16>(u));
   return __builtin_bit_cast(float, u);
-}
-// Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
-__device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
-  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
-                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
-  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
-                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
-  return (long)(((uint64_t)hi << 32) | lo);
 }
 
 template <int D, bool OQ>
@@ -1480,6 +1538,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     const bool ok = tok < p.rows;
     const int64_t tl = load_row(strip);
     if constexpr (!PF && !OQ) cur.load(p, tl, g);
+    if constexpr (OQ) cur.load_x(p, tl, g);
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
@@ -1516,19 +1575,11 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         v4i acc = v4i{0, 0, 0, 0};
         acc = mfma_i8_steps<S>([&](int s) { return (long)fo[(o * S + s) * 64 + lane]; }, [&](int s) { return bq[s]; }, acc);
         // the residual: four consecutive values of X in lane order
-        float res[4];
-        if constexpr (OQ) {
-          const float4 r = *(const float4 *)(p.x + tl * D + g * V + 4 * o);
-          res[0] = r.x; res[1] = r.y; res[2] = r.z; res[3] = r.w;
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) res[i] = cur.x[4 * o + i];
-        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int v = 4 * o + i;
           const float y = __builtin_fmaf((float)acc[i], sc, vb_o[v]);
-          x1[v] = res[i] + y;
+          x1[v] = cur.x[v] + y;
         }
       }
       const float mean = tb_token_sum<V>(x1) / (float)D;
@@ -2043,18 +2094,27 @@ static hipError_t run_qkv_attention(const Model &M, const QkvAttnArgs &a, size_t
 }
 
 // The lane-pair form (16-dimension heads): every group's weights resident, up to 36 token tiles.
-size_t qkv_attention_pair_lds(const Model &M) { return qkv_attention_lds(M, true); }
+size_t qkv_attention_pair_lds(const Model &M, bool quantised = false) {
+  return qkv_attention_lds(M, true) + (quantised ? (size_t)kQpThreads * 32 : 0);
+}
 
 bool qkv_attention_pair_supported(const Model &M) {
   return M.d == 128 && M.dh == 16 && M.grouped && M.L <= 16 * (kQpThreads / 64) * kQpTilesPerWave &&
          qkv_attention_pair_lds(M) <= M.lds_max;
 }
 
+// The lane-pair form writes the Eq. 2 codes of O itself when a word has at most one row per lane
+// pair.
+bool qkv_attention_pair_quantises(const Model &M) {
+  return qkv_attention_pair_supported(M) && M.L <= kQpThreads / 2 && qkv_attention_pair_lds(M, true) <= M.lds_max;
+}
+
 template <int D>
 static hipError_t run_qkv_attention_pair(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
   const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
   const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
-  hipLaunchKernelGGL((k_qkv_attention_pair<D>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
+  if (a.oq) hipLaunchKernelGGL((k_qkv_attention_pair<D, true>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
+  else hipLaunchKernelGGL((k_qkv_attention_pair<D, false>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
   return hipGetLastError();
 }
 
@@ -2081,6 +2141,11 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   a.resident = qkv_attention_resident(M) ? 1 : 0;
   const size_t lds = qkv_attention_lds(M, a.resident != 0);
   hipError_t e = hipErrorInvalidValue;
+  if (oq && qkv_attention_pair_quantises(M)) {   // O straight to its codes, no fp32 rows
+    a.oq = oq;
+    a.ao = ao;
+    return run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M, true), s);
+  }
   if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M), s);
   else if (M.d == 64 && M.dh == 8) e = run_qkv_attention<64, 8>(M, a, lds, s);
   else if (M.d == 128 && M.dh == 16) e = run_qkv_attention<128, 16>(M, a, lds, s);
@@ -2307,7 +2372,8 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
   const void *fns[] = {
       (const void *)k_qkv_attention<64, 8>,      (const void *)k_qkv_attention<128, 16>,
       (const void *)k_qkv_attention<128, 8>,     (const void *)k_qkv_attention<64, 16>,
-      (const void *)k_qkv_attention_pair<128>,   (const void *)k_qkv_attention_i16<128, 16>,
+      (const void *)k_qkv_attention_pair<128, false>, (const void *)k_qkv_attention_pair<128, true>,
+      (const void *)k_qkv_attention_i16<128, 16>,
       (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
       (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
       (const void *)k_qkv_attention_v16<128>,    (const void *)k_qkv_attention_split<128>,

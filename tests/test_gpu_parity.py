@@ -354,11 +354,14 @@ def _random_parity_check(m, n, seed, col_weight=3):
                                                  (128, 25, 51, 4, "hpsa"), (128, 9, 20, 6, "casa"),
                                                  (64, 40, 90, 0, "hpsa"), (128, 37, 70, 8, "hpsa"),
                                                  (64, 100, 201, 4, "hpsa"), (64, 131, 263, 2, "casa"),
-                                                 (128, 200, 401, 4, "hpsa"), (128, 255, 510, 6, "hpsa")])
+                                                 (128, 150, 299, 4, "hpsa"), (128, 200, 401, 4, "hpsa"),
+                                                 (128, 255, 510, 6, "hpsa")])
 def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attention):
     """d = 64 and 128 on token counts L = n + m that are not multiples of 16 (partial token
     tiles in the fused projection/attention kernels), several head splits and CASA.  Words of up
-    to 256 (d = 64) or 512 (d = 128) tokens keep keys and values in LDS as fp32; the longer ones
+    to 256 (d = 64) or 512 (d = 128) tokens keep keys and values in LDS as fp32 (at d = 128 up to
+    384 tokens with O written as Eq. 2 codes, one row per lane pair, and L = 449 with fp32 O and
+    a second row on some lane pairs); the longer ones
     (L = 301, 394, 601, 765) as int16 accumulators, or (d = 128 with head partitioning) one node
     type's rows at a time with the other type's keys and values in LDS as fp32, whose token tiles
     straddle the variable/check boundary when n is not a multiple of 16."""
