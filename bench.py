@@ -74,8 +74,8 @@ def algorithmic_counts(H, w, attention: str = "hpsa"):
 def kernel_source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2410_05911_amd", "csrc")
-    # the fused kernel, what it includes, and the host code that packs its tables
-    for f in ("aecct_internal.h", "device_common.h", "host.cpp", "kernel_fused.hip"):
+    # the fused kernel, its device helpers and table layout, and the host code that packs its tables
+    for f in ("kernel_fused.hip", "device_common.h", "fused_layout.h", "host_fused.h", "host_fused.cpp"):
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 

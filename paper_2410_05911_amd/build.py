@@ -13,7 +13,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libaecct.so")
-SOURCES = ["host.cpp", "aap.cpp", "kernels_layered.hip", "kernel_fused.hip", "arith_check.hip", "spe.hip",
+SOURCES = ["host.cpp", "host_fused.cpp", "aap.cpp", "kernels_layered.hip", "kernel_fused.hip", "arith_check.hip", "spe.hip",
            "train.hip", "train_host.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
