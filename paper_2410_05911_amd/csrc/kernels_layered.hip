@@ -1438,30 +1438,33 @@ struct TokenBlockArgs {
 };
 
 constexpr int kTbWaves = 8;
-// Whether a wavefront reads the next strip's attention output and residual while it runs the
-// current strip's feed-forward block (fp32 O input only).
-constexpr bool kTbPrefetch = false;
 // Whether pass 1 keeps the hidden row's fp32 values in registers for pass 2 (instead of pass 2
 // recomputing them).
 constexpr bool kTbKeepHidden = true;
 
-// A strip's fp32 inputs as one lane holds them: O features 32 s + 8 g + k (its B-operand
-// slots) and the residual X in lane order (register v = feature 4 v + g).
-template <int D>
+// A strip's inputs as one lane holds them: the attention output's features 32 s + 8 g + k (its
+// B-operand slots) in fp32, or (OQ) their Eq. 2 codes and the token's scale, and the residual X
+// in lane order (register v = feature 4 v + g).
+template <int D, bool OQ>
 struct TbIn {
-  float o[D / 32][8];
+  float o[OQ ? 1 : D / 32][8];
+  long oc[OQ ? D / 32 : 1];
+  float ao;
   float x[D / 4];
   __device__ __forceinline__ void load(const TokenBlockArgs &p, int64_t tl, int g) {
+    if constexpr (OQ) {
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s)
+      for (int s = 0; s < D / 32; ++s) oc[s] = *(const long *)(p.oq + tl * D + 32 * s + 8 * g);
+      ao = p.ao[tl];
+    } else {
 #pragma unroll
-      for (int k = 0; k < 8; k += 4) {
-        const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
-        o[s][k] = f.x; o[s][k + 1] = f.y; o[s][k + 2] = f.z; o[s][k + 3] = f.w;
-      }
-    load_x(p, tl, g);
-  }
-  __device__ __forceinline__ void load_x(const TokenBlockArgs &p, int64_t tl, int g) {
+      for (int s = 0; s < D / 32; ++s)
+#pragma unroll
+        for (int k = 0; k < 8; k += 4) {
+          const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
+          o[s][k] = f.x; o[s][k + 1] = f.y; o[s][k + 2] = f.z; o[s][k + 3] = f.w;
+        }
+    }
 #pragma unroll
     for (int u = 0; u < D / 4; u += 4) {
       const float4 r = *(const float4 *)(p.x + tl * D + g * (D / 4) + u);
@@ -1528,17 +1531,11 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
   // loads of a padding column read the last row instead: each column's results depend on
   // that column alone and padding columns are never stored
   auto load_row = [&](int64_t st) { const int64_t t = st * 16 + c; return t < p.rows ? t : p.rows - 1; };
-  constexpr bool PF = kTbPrefetch && !OQ;
-  TbIn<D> cur;
-  if constexpr (PF) {
-    if ((int64_t)blockIdx.x * kTbWaves + wave < nstrips) cur.load(p, load_row((int64_t)blockIdx.x * kTbWaves + wave), g);
-  }
   for (int64_t strip = (int64_t)blockIdx.x * kTbWaves + wave; strip < nstrips; strip += sstride) {
     const int64_t row0 = strip * 16, tok = row0 + c;
     const bool ok = tok < p.rows;
-    const int64_t tl = load_row(strip);
-    if constexpr (!PF && !OQ) cur.load(p, tl, g);
-    if constexpr (OQ) cur.load_x(p, tl, g);
+    TbIn<D, OQ> cur;
+    cur.load(p, load_row(strip), g);
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
@@ -1550,8 +1547,8 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       float sc;
       if constexpr (OQ) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) bq[s] = *(const long *)(p.oq + tl * D + 32 * s + 8 * g);
-        sc = p.ao[tl] * p.sq_o;
+        for (int s = 0; s < S; ++s) bq[s] = cur.oc[s];
+        sc = cur.ao * p.sq_o;
       } else {
         const float (&ov)[S][8] = cur.o;
         float om = 0.0f;
@@ -1615,15 +1612,39 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     float am = 0.0f;
     [[maybe_unused]] float hid[kTbKeepHidden ? TH : 1][4];
     if constexpr (kTbKeepHidden) {
+      // software-pipelined: tile o + 2's fragments and bias are read and tile o + 1's products
+      // issued before tile o's epilogue, so the LDS reads and the MFMA latency overlap the VALU
+      long fq[2][S];
+      float4 bq1[2];
+      auto ldf = [&](int o, long (&f)[S], float4 &b) {
+#pragma unroll
+        for (int s2 = 0; s2 < S; ++s2) f[s2] = (long)f1l[(o * S + s2) * 64];
+        b = *(const float4 *)(b1l + 16 * o);
+      };
+      const auto xbf = [&](int s2) { return xb[s2]; };
+      ldf(0, fq[0], bq1[0]);
+      ldf(1, fq[1], bq1[1]);
+      v4i acc = mfma_i8_steps<S>([&](int s2) { return fq[0][s2]; }, xbf, v4i{0, 0, 0, 0});
+      float4 bc = bq1[0];
 #pragma unroll
       for (int o = 0; o < TH; ++o) {
-        v4i acc = v4i{0, 0, 0, 0};
-        acc = mfma_i8_steps<S>([&](int s) { return (long)f1l[(o * S + s) * 64]; }, [&](int s) { return xb[s]; }, acc);
+        v4i acn = v4i{0, 0, 0, 0};
+        float4 bn = bc;
+        if (o + 1 < TH) {
+          acn = mfma_i8_steps<S>([&](int s2) { return fq[(o + 1) & 1][s2]; }, xbf, acn);
+          bn = bq1[(o + 1) & 1];
+        }
+        if (o + 2 < TH) ldf(o + 2, fq[o & 1], bq1[o & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        const float bb[4] = {bc.x, bc.y, bc.z, bc.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          hid[o][i] = __builtin_fmaf((float)acc[i], sc1, b1l[16 * o + i]);
+          hid[o][i] = __builtin_fmaf((float)acc[i], sc1, bb[i]);
           am = fmaxf(am, hid[o][i]);
         }
+        __builtin_amdgcn_sched_barrier(0);
+        acc = acn;
+        bc = bn;
       }
     } else {
 #pragma unroll 2
@@ -1635,10 +1656,6 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
       }
     }
     am = tb_token_max(am + 0.0f);
-    if constexpr (PF) {                                     // the next strip's inputs
-      const int64_t ns = strip + sstride;
-      cur.load(p, load_row(ns < nstrips ? ns : strip), g);
-    }
     const float inv1 = inv127(am);
     v4i acc2[TO];
 #pragma unroll
