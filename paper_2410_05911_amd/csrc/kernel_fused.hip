@@ -280,7 +280,11 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   }
   const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
 
-  for (int64_t w = (int64_t)blockIdx.x * nw + wave; w < p.words; w += (int64_t)gridDim.x * nw) {
+  // Words go to waves wave-major (word w to wave w / gridDim.x of block w % gridDim.x, then every
+  // gridDim.x * nw words): when the batch is not a multiple of the waves in flight, the waves that
+  // take one word more are the lowest-numbered waves of every block, one per SIMD, rather than
+  // every wave of the first blocks, so no SIMD runs more than one extra word.
+  for (int64_t w = (int64_t)wave * gridDim.x + blockIdx.x; w < p.words; w += (int64_t)gridDim.x * nw) {
     // Per-word copy of the lane index: the addresses of the embedding and head steps derive
     // from it, so they are recomputed per word rather than held through the layers.
     int lw = lane;
