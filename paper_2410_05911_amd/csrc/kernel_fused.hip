@@ -280,11 +280,18 @@ __global__ __launch_bounds__(WAVES * 64, 1) void k_fused_decode(FusedArgs p) {
   }
   const int mask1 = g < p.hf ? 0 : 1, mask2 = 4 + g < p.hf ? 0 : 1;
 
-  // Words go to waves wave-major (word w to wave w / gridDim.x of block w % gridDim.x, then every
-  // gridDim.x * nw words): when the batch is not a multiple of the waves in flight, the waves that
-  // take one word more are the lowest-numbered waves of every block, one per SIMD, rather than
-  // every wave of the first blocks, so no SIMD runs more than one extra word.
-  for (int64_t w = (int64_t)wave * gridDim.x + blockIdx.x; w < p.words; w += (int64_t)gridDim.x * nw) {
+  // Words in rounds of one per wave, consecutive words to the waves of one block (their y rows and
+  // outputs adjacent in memory).  The last, partial round goes to the lowest-numbered waves of
+  // every block (q or q + 1 per block), one per SIMD, rather than to every wave of the first
+  // blocks: no SIMD then runs more than one word above the others.  v runs over the rounds
+  // wave-major, which selects exactly those waves for the last round; w is the word it stands for.
+  // (32-bit indices: the launcher passes at most 2^31 - 1 words per launch.)
+  const uint32_t words = (uint32_t)p.words, wt = gridDim.x * (uint32_t)nw, full = words / wt;
+  const uint32_t rq = (words - full * wt) / gridDim.x, rr = words - full * wt - rq * gridDim.x;
+  const uint32_t last_w = full * wt + blockIdx.x * rq + min(blockIdx.x, rr) + (uint32_t)wave;
+  uint32_t base = blockIdx.x * (uint32_t)nw + (uint32_t)wave;
+  for (uint32_t v = (uint32_t)wave * gridDim.x + blockIdx.x; v < words; v += wt, base += wt) {
+    const int64_t w = base < full * wt ? base : last_w;
     // Per-word copy of the lane index: the addresses of the embedding and head steps derive
     // from it, so they are recomputed per word rather than held through the layers.
     int lw = lane;
@@ -537,6 +544,15 @@ static hipError_t launch_nt(const FusedArgs &a, size_t lds, int grid, int waves,
 hipError_t launch_fused(const Model &M, const float *y, int64_t words, uint8_t *bits, float *logits,
                         hipStream_t s) {
   if (words <= 0) return hipSuccess;
+  constexpr int64_t kMaxWords = INT32_MAX;   // the kernel's word indices are 32-bit
+  if (words > kMaxWords) {
+    for (int64_t w0 = 0; w0 < words; w0 += kMaxWords) {
+      const int64_t nw = std::min(kMaxWords, words - w0);
+      const hipError_t e = launch_fused(M, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   const FusedTables &T = M.fused;
   const int NT = fused_tiles(M);
   FusedArgs a{};
