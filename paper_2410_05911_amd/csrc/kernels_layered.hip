@@ -683,9 +683,6 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
 // ------------------------------------------------------------------------------------------
 constexpr int kQpThreads = 768;
 constexpr int kQpTilesPerWave = 3;
-// Whether a word's token tiles are read at the word's start (and waited for there) rather than
-// during the previous word's last group of rows.
-constexpr bool kQpWordLoads = true;
 
 // Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
 __device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
@@ -835,7 +832,6 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
 #pragma unroll
       for (int k = 0; k < TW; ++k) {
         if (wg + NWV * k < ntiles) qa_project<D>(bf, afr[k], alw[k], wg + NWV * k, L, lane, bq, bk, bv, sq, qs, kv);
-        if constexpr (OQ) __builtin_amdgcn_sched_barrier(0);   // one tile's products at a time
       }
       block_sync_lds();
       const bool first = hg < p.hf;
