@@ -188,6 +188,20 @@ hipError_t train_embed(const float *y, int64_t rows, int n, int L, int d, const 
 hipError_t train_quant(const float *x, int64_t rows, int K, bool relu, float *xh, hipStream_t s);
 // C[M][N] = (accumulate ? C : 0) + scale (op(A) op(B)) + bias; ta: A stored [K][M]; tb: B stored [N][K].
 // part: scratch of part_floats floats for split reductions over K.
+// Products with a ternary right operand on the bf16 matrix cores (fp32 A split exactly into three
+// bf16 parts): train_pack_tern lays each job's T [R][C] (or its transpose) out as B fragments in
+// out (2 R C bytes), train_gemm_tern forms C = beta C + scale (A B) + bias; N a multiple of 64, K
+// of 32.
+bool train_tern_shape_ok(int64_t N, int64_t K);
+struct TernPackJob {
+  const float *T;
+  int R, C, trans;
+  void *out;
+};
+struct TernPackJobs { TernPackJob j[kTrainJobsPerLaunch]; int n; };
+hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s);
+hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
+                           int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s);
 hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc,
                       int64_t M, int64_t N, int64_t K, const float *scale, const float *bias, bool accumulate,
                       float *part, int64_t part_floats, int cu_count, hipStream_t s);

@@ -427,6 +427,138 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
     }
 }
 
+// ------------------------------------------------------------------------------------------
+// Products with a ternary operand: C[M][N] = beta C + scale (A B) + bias[N] where B holds only
+// -1, 0, +1 (Eq. 1's T, or its transpose) and A is fp32.  Each fp32 a splits exactly into three
+// bf16 parts, a = hi + mid + lo (hi the leading 8 significant bits by truncation, mid the next 8,
+// lo the remaining at most 8), each part times a ternary entry is exact, and the three
+// v_mfma_f32_16x16x32_bf16 products accumulate in fp32: the result is an fp32-accumulated sum of
+// exact products, as in the fp32 kernels, at the bf16 matrix rate.  B comes pre-packed as bf16 MFMA
+// B fragments (k_pack_tern).  A wave computes 16 RT rows x 16 NJ columns, a block four waves.
+// ------------------------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct GemmTern {
+  const float *A;
+  const uint4 *B;       // fragment (nt, kt) at (nt * K / 32 + kt) * 64: lane l holds column
+                        // 16 nt + (l & 15), k = 32 kt + 8 (l >> 4) + e in bf16 e = 0..7
+  float *C;
+  int64_t M, N, K, lda, ldc;
+  const float *scale;   // device scalar or null (1)
+  const float *bias;    // [N] or null
+  int beta;
+};
+
+// Ternary matrix T [R][C] (fp32 -1 / 0 / +1, row-major) as bf16 B fragments of B = T (k = row,
+// n = column) or, with trans, B = T^T (k = column, n = row); one job per blockIdx.y.
+__global__ __launch_bounds__(kThreads) void k_pack_tern(TernPackJobs jobs) {
+  const TernPackJob &J = jobs.j[blockIdx.y];
+  const float *T = J.T;
+  const int R = J.R, Cc = J.C, trans = J.trans;
+  uint4 *out = (uint4 *)J.out;
+  const int K = trans ? Cc : R, N = trans ? R : Cc, KT = K / 32;
+  const int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (u >= (int64_t)(N / 16) * KT * 64) return;
+  const int l = (int)(u & 63), f = (int)(u >> 6), nt = f / KT, kt = f - nt * KT;
+  const int n = 16 * nt + (l & 15), k0 = 32 * kt + 8 * (l >> 4);
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float t = trans ? T[(int64_t)n * Cc + k0 + e] : T[(int64_t)(k0 + e) * Cc + n];
+    h[e] = t > 0.0f ? 0x3F80u : (t < 0.0f ? 0xBF80u : 0u);   // bf16 of +1, -1, 0
+  }
+  out[u] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
+}
+
+// the bf16 bit patterns of eight fp32 values that are exact in bf16 (low 16 bits zero)
+__device__ __forceinline__ bf16x8 bf16_hi8(const float (&v)[8]) {
+  uint4 w;
+  w.x = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, v[1]), __builtin_bit_cast(uint32_t, v[0]), 0x07060302u);
+  w.y = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, v[3]), __builtin_bit_cast(uint32_t, v[2]), 0x07060302u);
+  w.z = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, v[5]), __builtin_bit_cast(uint32_t, v[4]), 0x07060302u);
+  w.w = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, v[7]), __builtin_bit_cast(uint32_t, v[6]), 0x07060302u);
+  return __builtin_bit_cast(bf16x8, w);
+}
+
+template <int NJ, int RT>
+__global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, col = l & 15, grp = l >> 4;
+  // the wave's RT row tiles of 16 share every B fragment it reads
+  const int64_t m0 = (int64_t)blockIdx.y * (64 * RT) + 16 * RT * wave, n0 = (int64_t)blockIdx.x * (16 * NJ);
+  const int64_t KT = g.K / 32;
+  const float *arow[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const int64_t r = m0 + 16 * t + col;
+    arow[t] = g.A + (r < g.M ? r : g.M - 1) * g.lda + 8 * grp;   // rows past M: a copy, never stored
+  }
+  const uint4 *bcol = g.B + (n0 / 16) * KT * 64 + l;
+  f32x4 acc[RT][NJ];
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[t][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  float4 a0[RT], a1[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    a0[t] = *(const float4 *)arow[t];
+    a1[t] = *(const float4 *)(arow[t] + 4);
+  }
+  for (int64_t kt = 0; kt < KT; ++kt) {
+    bf16x8 ph[RT], pm[RT], pl[RT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+      const float a[8] = {a0[t].x, a0[t].y, a0[t].z, a0[t].w, a1[t].x, a1[t].y, a1[t].z, a1[t].w};
+      float hi[8], mid[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[e]) & 0xFFFF0000u);
+        const float rm = a[e] - hi[e];
+        mid[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, rm) & 0xFFFF0000u);
+        lo[e] = rm - mid[e];
+      }
+      ph[t] = bf16_hi8(hi);
+      pm[t] = bf16_hi8(mid);
+      pl[t] = bf16_hi8(lo);
+    }
+    if (kt + 1 < KT) {   // the next k-step's A
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        a0[t] = *(const float4 *)(arow[t] + 32 * (kt + 1));
+        a1[t] = *(const float4 *)(arow[t] + 32 * (kt + 1) + 4);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const bf16x8 b = __builtin_bit_cast(bf16x8, bcol[(j * KT + kt) * 64]);
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[t], b, acc[t][j], 0, 0, 0);
+        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[t], b, acc[t][j], 0, 0, 0);
+        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[t], b, acc[t][j], 0, 0, 0);
+      }
+    }
+  }
+  const float sc = g.scale ? *g.scale : 1.0f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int64_t c = n0 + 16 * j + col;
+    if (c >= g.N) continue;
+    const float bj = g.bias ? g.bias[c] : 0.0f;
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t rr = m0 + 16 * t + 4 * grp + i;
+        if (rr >= g.M) continue;
+        float o = sc * acc[t][j][i] + bj;
+        if (g.beta) o += g.C[rr * g.ldc + c];
+        g.C[rr * g.ldc + c] = o;
+      }
+  }
+}
+
 // Split-k partial products summed in a fixed order: a block covers 64 outputs, its four lanes per
 // output sum the splits z = lane, lane + 4, ... and are added in lane order.
 __global__ __launch_bounds__(kThreads) void k_gemm_reduce(GemmF32 g, int splits) {
@@ -870,6 +1002,33 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
   if (splits > 1)
     hipLaunchKernelGGL(train::k_gemm_reduce, dim3(blocks_for(M * N, 64)), dim3(train::kThreads), 0, s, g,
                        (int)splits);
+  return hipGetLastError();
+}
+
+bool train_tern_shape_ok(int64_t N, int64_t K) { return K % 32 == 0 && N % 64 == 0; }
+
+hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s) {
+  if (jobs.n <= 0) return hipSuccess;
+  int64_t lanes = 0;
+  for (int i = 0; i < jobs.n; ++i) {
+    const TernPackJob &J = jobs.j[i];
+    if (!train_tern_shape_ok(J.trans ? J.R : J.C, J.trans ? J.C : J.R)) return hipErrorInvalidValue;
+    lanes = std::max<int64_t>(lanes, (int64_t)J.R * J.C / 8);   // one lane per 8 entries
+  }
+  hipLaunchKernelGGL(train::k_pack_tern, dim3(blocks_for(lanes, train::kThreads), (unsigned)jobs.n), dim3(train::kThreads), 0,
+                     s, jobs);
+  return hipGetLastError();
+}
+
+hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
+                           int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (!train_tern_shape_ok(N, K) || lda % 4 != 0 || ((uintptr_t)A & 15u) != 0) return hipErrorInvalidValue;
+  train::GemmTern g{A, (const uint4 *)frag, C, M, N, K, lda, ldc, scale, bias, accumulate ? 1 : 0};
+  constexpr int RT = 2;   // two row tiles per wave: 37.8 us against 39.4 us for one (LDPC(256,128) step)
+  const unsigned gy = (unsigned)((M + 64 * RT - 1) / (64 * RT));
+  if (N % 128 == 0) hipLaunchKernelGGL((train::k_gemm_tern<8, RT>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
+  else hipLaunchKernelGGL((train::k_gemm_tern<4, RT>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
   return hipGetLastError();
 }
 

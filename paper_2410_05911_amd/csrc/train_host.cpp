@@ -29,7 +29,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct TrainWs {
   struct Layer { size_t xh, qkv, lse, o, oh, xn1, rho1, x1h, f, gh, xn2, rho2; };
   std::vector<Layer> layer;
-  size_t t, x, x1, y, z, fo, df, dz, tw, gam, sc, lpart, dx, dr, dx1, dg, dO, dqkv, dv, part;
+  size_t t, x, x1, y, z, fo, df, dz, tw, tb16, gam, sc, lpart, dx, dr, dx1, dg, dO, dqkv, dv, part;
   size_t part_floats, total_bytes;
 };
 
@@ -66,6 +66,7 @@ TrainWs train_ws(const aecct_trainer &T, int64_t batch) {
   w.df = take((size_t)batch * T.n);
   w.dz = take(R);
   w.tw = take(weight_floats(T));
+  w.tb16 = take(weight_floats(T));   // every ternary matrix as bf16 B fragments, T and T^T
   w.gam = take((size_t)T.N * 6);
   w.sc = take((size_t)T.N * 6);
   w.lpart = take(((size_t)batch * T.n + 255) / 256 + 1);
@@ -213,6 +214,18 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     return ws + o;
   };
   float *gam = ws + W.gam, *sc = ws + W.sc;
+  // the ternary matrices as bf16 fragments of B = T (the forward products) and B = T^T (the input
+  // gradients): at d, d_ff multiples of 64 every product with a ternary operand runs on
+  // train_gemm_tern, else on the fp32 kernels
+  const bool tern = d % 64 == 0 && dff % 64 == 0;
+  auto tfrag = [&](int l, int k, bool trans) {
+    size_t o = 0;   // in uint16 units
+    for (int ll = 0; ll < l; ++ll)
+      for (int kk = 0; kk < 6; ++kk) o += 2 * (size_t)K_in[kk] * K_out[kk];
+    for (int kk = 0; kk < k; ++kk) o += 2 * (size_t)K_in[kk] * K_out[kk];
+    if (trans) o += (size_t)K_in[k] * K_out[k];
+    return (void *)((uint16_t *)(ws + W.tb16) + o);
+  };
   hipError_t e = hipSuccess;
 #define AECCT_TRY(call)              \
   do {                               \
@@ -231,32 +244,45 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
                                        gam + 6 * l + k, sc + 6 * l + k};
     AECCT_TRY(train_aap(jobs, T.aap_eps, s));
   }
+  if (tern)   // both layouts of every matrix, a launch per four layers
+    for (int l0 = 0; l0 < N; l0 += kTrainJobsPerLaunch / 12) {
+      TernPackJobs pj{};
+      for (int l = l0; l < std::min(N, l0 + kTrainJobsPerLaunch / 12); ++l)
+        for (int k = 0; k < 6; ++k)
+          for (int tr = 0; tr < 2; ++tr)
+            pj.j[pj.n++] = TernPackJob{tmat(l, k), (int)K_in[k], (int)K_out[k], tr, tfrag(l, k, tr != 0)};
+      AECCT_TRY(train_pack_tern(pj, s));
+    }
   float *X = ws + W.x, *X1 = ws + W.x1, *Y = ws + W.y, *tv = ws + W.t;
   AECCT_TRY(train_embed(y, R, T.n, T.L, d, T.chk_ptr, T.chk_idx, p->embed, p->pos, X, tv, s));
   auto gemm = [&](bool ta, bool tb, const float *A, int64_t lda, const float *Bm, int64_t ldb, float *C, int64_t ldc,
                   int64_t M, int64_t Nn, int64_t K, const float *scale, const float *bias, bool acc) {
     return train_gemm(ta, tb, A, lda, Bm, ldb, C, ldc, M, Nn, K, scale, bias, acc, part, (int64_t)PF, T.cu_count, s);
   };
+  // C = scale (A op(T)) + bias (+ C) for ternary matrix k of layer l, op(T) = T or (trans) T^T
+  auto tgemm = [&](bool trans, int l, int k, const float *A, int64_t lda, float *C, int64_t ldc, int64_t M, int64_t Nn,
+                   int64_t K, const float *scale, const float *bias, bool acc) {
+    if (tern && lda % 4 == 0 && ((uintptr_t)A & 15u) == 0)
+      return train_gemm_tern(A, lda, tfrag(l, k, trans), C, ldc, M, Nn, K, scale, bias, acc, s);
+    return gemm(false, trans, A, lda, tmat(l, k), trans ? K : Nn, C, ldc, M, Nn, K, scale, bias, acc);
+  };
   for (int l = 0; l < N; ++l) {
     const TrainWs::Layer &q = W.layer[l];
     float *Xh = ws + q.xh, *QKV = ws + q.qkv;
     AECCT_TRY(train_quant(X, R, d, false, Xh, s));
     for (int k = 0; k < 3; ++k)
-      AECCT_TRY(gemm(false, false, Xh, d, tmat(l, k), d, QKV + k * d, 3 * d, R, d, d, sc + 6 * l + k,
-                     pb[k] + (size_t)l * d, false));
+      AECCT_TRY(tgemm(false, l, k, Xh, d, QKV + k * d, 3 * d, R, d, d, sc + 6 * l + k, pb[k] + (size_t)l * d, false));
     TrainAttn at{QKV, R, T.L, d, T.heads, T.hf, T.m1_ptr, T.m1_idx, T.m2_ptr, T.m2_idx, ws + q.o, ws + q.lse,
                  nullptr, nullptr, nullptr};
     AECCT_TRY(train_attention(0, T.dh, at, s));
     AECCT_TRY(train_quant(ws + q.o, R, d, false, ws + q.oh, s));
-    AECCT_TRY(gemm(false, false, ws + q.oh, d, tmat(l, 3), d, Y, d, R, d, d, sc + 6 * l + 3, pb[3] + (size_t)l * d, false));
+    AECCT_TRY(tgemm(false, l, 3, ws + q.oh, d, Y, d, R, d, d, sc + 6 * l + 3, pb[3] + (size_t)l * d, false));
     AECCT_TRY(train_ln_fwd(X, Y, R, d, p->ln1_g + (size_t)l * d, p->ln1_b + (size_t)l * d, T.ln_eps, X1, ws + q.xn1,
                            ws + q.rho1, s));
     AECCT_TRY(train_quant(X1, R, d, false, ws + q.x1h, s));
-    AECCT_TRY(gemm(false, false, ws + q.x1h, d, tmat(l, 4), dff, ws + q.f, dff, R, dff, d, sc + 6 * l + 4,
-                   pb[4] + (size_t)l * dff, false));
+    AECCT_TRY(tgemm(false, l, 4, ws + q.x1h, d, ws + q.f, dff, R, dff, d, sc + 6 * l + 4, pb[4] + (size_t)l * dff, false));
     AECCT_TRY(train_quant(ws + q.f, R, dff, true, ws + q.gh, s));
-    AECCT_TRY(gemm(false, false, ws + q.gh, dff, tmat(l, 5), d, Y, d, R, d, dff, sc + 6 * l + 5, pb[5] + (size_t)l * d,
-                   false));
+    AECCT_TRY(tgemm(false, l, 5, ws + q.gh, dff, Y, d, R, d, dff, sc + 6 * l + 5, pb[5] + (size_t)l * d, false));
     AECCT_TRY(train_ln_fwd(X1, Y, R, d, p->ln2_g + (size_t)l * d, p->ln2_b + (size_t)l * d, T.ln_eps, X, ws + q.xn2,
                            ws + q.rho2, s));
   }
@@ -286,12 +312,12 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     AECCT_TRY(colsum(dX, d, nullptr, nullptr, R, d, g->ln2_b + ld_));
     AECCT_TRY(gemm(true, false, ws + q.gh, dff, dR, d, gw[5] + wofs(l, 5), d, dff, d, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dR, d, nullptr, nullptr, R, d, gb[5] + ld_));
-    AECCT_TRY(gemm(false, true, dR, d, tmat(l, 5), d, dG, dff, R, dff, d, sc + 6 * l + 5, nullptr, false));
+    AECCT_TRY(tgemm(true, l, 5, dR, d, dG, dff, R, dff, d, sc + 6 * l + 5, nullptr, false));
     AECCT_TRY(train_relu_bwd(dG, ws + q.f, R * dff, s));
     AECCT_TRY(gemm(true, false, ws + q.x1h, d, dG, dff, gw[4] + wofs(l, 4), dff, d, dff, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dG, dff, nullptr, nullptr, R, dff, gb[4] + (size_t)l * dff));
     AECCT_TRY(hipMemcpyAsync(dX1, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
-    AECCT_TRY(gemm(false, true, dG, dff, tmat(l, 4), dff, dX1, d, R, d, dff, sc + 6 * l + 4, nullptr, true));
+    AECCT_TRY(tgemm(true, l, 4, dG, dff, dX1, d, R, d, dff, sc + 6 * l + 4, nullptr, true));
     // LN1, output map
     AECCT_TRY(train_ln_bwd(dX1, p->ln1_g + ld_, ws + q.xn1, ws + q.rho1, R, d, dR, s));
     AECCT_TRY(colsum(dX1, d, ws + q.xn1, nullptr, R, d, g->ln1_g + ld_));
@@ -299,7 +325,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     AECCT_TRY(hipMemcpyAsync(dX, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
     AECCT_TRY(gemm(true, false, ws + q.oh, d, dR, d, gw[3] + wofs(l, 3), d, d, d, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dR, d, nullptr, nullptr, R, d, gb[3] + ld_));
-    AECCT_TRY(gemm(false, true, dR, d, tmat(l, 3), d, dO, d, R, d, d, sc + 6 * l + 3, nullptr, false));
+    AECCT_TRY(tgemm(true, l, 3, dR, d, dO, d, R, d, d, sc + 6 * l + 3, nullptr, false));
     // attention, then the query, key and value maps
     TrainAttn at{ws + q.qkv, R, T.L, d, T.heads, T.hf, T.m1_ptr, T.m1_idx, T.m2_ptr, T.m2_idx, ws + q.o, ws + q.lse,
                  dO, dQKV, ws + W.dv};
@@ -309,7 +335,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
       AECCT_TRY(gemm(true, false, ws + q.xh, d, dQKV + k * d, 3 * d, gw[k] + wofs(l, k), d, d, d, R, nullptr, nullptr,
                      false));
       AECCT_TRY(colsum(dQKV + k * d, 3 * d, nullptr, nullptr, R, d, gb[k] + ld_));
-      AECCT_TRY(gemm(false, true, dQKV + k * d, 3 * d, tmat(l, k), d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
+      AECCT_TRY(tgemm(true, l, k, dQKV + k * d, 3 * d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
     }
   }
   // the straight-through Eq. 1 gradients of every matrix from its G = Xh^T dY (nothing in the
