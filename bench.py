@@ -269,9 +269,11 @@ def train_bench(c: int, batch: int, steps: int, warmup: int):
                       "config": {"workload": f"qat_{cfg.name}_batch{batch}", "tokens": L, "d": d, "layers": N,
                                  "batch": batch},
                       "gemm_fma_per_step": fma, "gemm_fma_rate_T": fma / (ms * 1e-3) / 1e12,
-                      # fp32 MFMA roofline of the step's products: every GEMM flop over the whole
-                      # step time (a lower bound of the GEMM kernels' own rate)
-                      "roofline": {"bound": "mfma", "kernel": "k_gemm_mfma (all step GEMMs, whole-step time)",
+                      # the step's products as fp32 work against the fp32 MFMA peak: every GEMM flop
+                      # over the whole step time (a lower bound of the GEMM kernels' own rate; the
+                      # products with a ternary operand run on the bf16 matrix cores, three exact
+                      # bf16 products per fp32 one, at d and d_ff multiples of 64)
+                      "roofline": {"bound": "mfma", "kernel": "k_gemm_tern + k_gemm_mfma (all step GEMMs, whole-step time)",
                                    "achieved": 2 * fma / (ms * 1e-3) / 1e12, "peak": 157.3, "unit": "TFLOP/s",
                                    "frac": 2 * fma / (ms * 1e-3) / 1e12 / 157.3, "traffic": None},
                       "cpu_baseline": {"value": k / dt, "unit": "codewords/s", "cores": 1, "kind": "oracle",
