@@ -67,6 +67,7 @@ struct Model {
   const uint16_t *g1s_tab, *g2s_tab;
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;
+  const float *head_w1_lo;    // W_{d->1} in the token block's lane order ([4][d/4], d = 64, 128), or null
   float head_b1;
   LayerWeights layer[kMaxLayers];
   FusedTables fused;
@@ -119,8 +120,10 @@ hipError_t launch_qkv_attention_i16(const Model &M, int layer, const int8_t *xq,
 bool token_block_supported(const Model &M);
 // words processed at once by the layered attention form `form` (aecct_layered_attention)
 int64_t attention_word_slots(const Model &M, int form);
+// With z (the last layer): the head's z_i = W_{d->1} x_i + b1 of every output row to z [rows], and
+// neither x nor xq nor ax written.
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
-                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s);
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z = nullptr);
 hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,
                            int64_t rows, float *x1, int8_t *x1q, float *a1, hipStream_t s);
 hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, int8_t *gq,
@@ -129,7 +132,7 @@ hipError_t launch_ffn2_ln(const Model &M, int layer, const int8_t *gq, const flo
                           int64_t rows, float *x, int8_t *xq, float *ax, hipStream_t s);
 // The head of a decode: z per token into zbuf (words * L floats), then the word-tiled product.
 hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
-                             float *logits, bool lane_order, float *zbuf, hipStream_t s);
+                             float *logits, bool lane_order, float *zbuf, hipStream_t s, bool z_ready = false);
 hipError_t launch_head(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
                        float *logits, bool lane_order, hipStream_t s);
 hipError_t launch_ternary_gemm(const Model &M, int layer, int kind, const int8_t *a, int64_t rows, int32_t *acc,

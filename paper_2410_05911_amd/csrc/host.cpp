@@ -92,7 +92,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 
 // Device memory plan: byte offsets inside the model's single allocation.
 struct Plan {
-  size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, wo, bo, total;
+  size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, w1lo, wo, bo, total;
   size_t g1_meta, g1_tab, g2_meta, g2_tab;   // grouped neighbour lists (layered attention)
   size_t g1s_tab, g2s_tab;                    // the same, counted within each node type
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
@@ -118,6 +118,7 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
   p.embed = take(sizeof(float) * L * d);
   p.pos = has_pos ? take(sizeof(float) * L * d) : 0;
   p.w1 = take(sizeof(float) * d);
+  p.w1lo = take(sizeof(float) * d);
   p.wo = take(sizeof(float) * (size_t)L * n);
   p.bo = take(sizeof(float) * n);
   p.layer.resize(N);
@@ -493,6 +494,12 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   put(P.embed, w->embed, 4 * (size_t)L * D);
   if (w->pos) put(P.pos, w->pos, 4 * (size_t)L * D);
   put(P.w1, w->head_w1, 4 * D);
+  {
+    std::vector<float> w1lo(D);   // [g][v] = W_{d->1}[4 v + g]
+    for (size_t g = 0; g < 4; ++g)
+      for (size_t v = 0; v < D / 4; ++v) w1lo[g * (D / 4) + v] = w->head_w1[4 * v + g];
+    put(P.w1lo, w1lo.data(), 4 * D);
+  }
   put(P.wo, w->head_wo, 4 * (size_t)L * n);
   put(P.bo, w->head_bo, 4 * (size_t)n);
   put(P.f_frag, FI.frag.data(), 2 * FI.frag.size());
@@ -609,6 +616,7 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.embed = (const float *)(b + P.embed);
   M.pos = w->pos ? (const float *)(b + P.pos) : nullptr;
   M.head_w1 = (const float *)(b + P.w1);
+  M.head_w1_lo = (const float *)(b + P.w1lo);
   M.head_wo = (const float *)(b + P.wo);
   M.head_bo = (const float *)(b + P.bo);
   for (int l = 0; l < n_layers; ++l) {
@@ -742,8 +750,10 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
       }
       if (e != hipSuccess) break;
       if (tb) {
-        e = (qa && !qa_codes) || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s)
-                     : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s);
+        // the last layer leaves the head's z per token in a1 (free once the layers are done)
+        float *zl = l == M.n_layers - 1 ? a1 : nullptr;
+        e = (qa && !qa_codes) || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s, zl)
+                     : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s, zl);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
         if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x1, nw, M.d, false, x1q, a1, s);
@@ -759,7 +769,7 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
     }
     if (e == hipSuccess)
       e = aecct::launch_head_tiled(M, x, y + w0 * M.n, nw, bits + w0 * M.n, logits ? logits + w0 * M.n : nullptr, tb,
-                                   a1, s);   // a1 (rows floats) is free once the layers are done
+                                   a1, s, tb);   // with the token block, z is already in a1
     if (e != hipSuccess) return AECCT_ERR_DEVICE;
   }
   return AECCT_OK;

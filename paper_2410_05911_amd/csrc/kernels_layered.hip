@@ -1431,6 +1431,10 @@ struct TokenBlockArgs {
   int64_t rows;
   int8_t *xq;                   // [rows][d] Eq. 2 codes of the output
   float *ax;                    // [rows]
+  // the last layer: z_i = W_{d->1} x_i + b1 of the output rows to z [rows] instead of x, xq, ax
+  float *z;
+  const float *w1;              // [4][d/4] W_{d->1} in lane order (with z)
+  float head_b1;
 };
 
 constexpr int kTbWaves = 8;
@@ -1469,10 +1473,11 @@ struct TbIn {
   }
 };
 
-// LDS: the FF1, FF2 and O fragments (9 d^2 bytes), then the six d-vectors and the FF1 bias.
+// LDS: the FF1, FF2 and O fragments (9 d^2 bytes), then the six d-vectors, the FF1 bias and
+// W_{d->1} in lane order.
 template <int D>
 constexpr size_t token_block_lds() {
-  return (size_t)9 * D * D + (size_t)10 * D * 4;
+  return (size_t)9 * D * D + (size_t)11 * D * 4;
 }
 
 // v of lane (this lane xor M), M = 16 or 32
@@ -1498,7 +1503,8 @@ __device__ __forceinline__ float tb_token_max(float a) {
   return __builtin_bit_cast(float, u);
 }
 
-template <int D, bool OQ>
+// Z: the last layer, which leaves the head's z per token (TokenBlockArgs::z) instead of x, xq, ax.
+template <int D, bool OQ, bool Z>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
   constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -1510,6 +1516,8 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
   float *lv = (float *)(smem + frag_bytes);
   for (int u = threadIdx.x; u < 6 * D; u += kTbWaves * 64) lv[u] = p.vec[u];
   for (int u = threadIdx.x; u < 4 * D; u += kTbWaves * 64) lv[6 * D + u] = p.b1[u];
+  if constexpr (Z)
+    for (int u = threadIdx.x; u < D; u += kTbWaves * 64) lv[10 * D + u] = p.w1[u];
   const float *vec = lv;
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
@@ -1721,23 +1729,34 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
         v2[v] = __builtin_fmaf(e[v] * rho, vg2[v], vbb2[v]);
         amax = fmaxf(amax, fabsf(v2[v]));
       }
-      if (ok) {
+      if constexpr (Z) {
+        // the last layer: the head's z of the token, pairwise over its features like the LayerNorm
+        // sums (Section 3, W_{d->1}); X itself is not needed any more
+        const float *w1l = vec + 10 * D + g * V;
+        float pr[V];
 #pragma unroll
-        for (int u = 0; u < V; u += 4)
-          *(float4 *)(p.x + tok * D + g * V + u) = make_float4(v2[u], v2[u + 1], v2[u + 2], v2[u + 3]);
-      }
-      amax = tb_token_max(amax);
-      const float inv = inv127(amax);
-      if (ok) {
-        // the next layer's codes in lane order: step s's eight codes of this lane as one word
+        for (int v = 0; v < V; ++v) pr[v] = v2[v] * w1l[v];
+        const float zt = tb_token_sum<V>(pr) + p.head_b1;
+        if (ok && g == 0) p.z[tok] = zt;
+      } else {
+        if (ok) {
 #pragma unroll
-        for (int s = 0; s < S; ++s) {
-          uint32_t b[8];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) b[k] = quant_bits(v2[8 * s + k], inv);
-          *(long *)(p.xq + tok * D + 32 * s + 8 * g) = tb_pack8(b);
+          for (int u = 0; u < V; u += 4)
+            *(float4 *)(p.x + tok * D + g * V + u) = make_float4(v2[u], v2[u + 1], v2[u + 2], v2[u + 3]);
         }
-        if (g == 0) p.ax[tok] = amax;
+        amax = tb_token_max(amax);
+        const float inv = inv127(amax);
+        if (ok) {
+          // the next layer's codes in lane order: step s's eight codes of this lane as one word
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+            uint32_t b[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) b[k] = quant_bits(v2[8 * s + k], inv);
+            *(long *)(p.xq + tok * D + 32 * s + 8 * g) = tb_pack8(b);
+          }
+          if (g == 0) p.ax[tok] = amax;
+        }
       }
     }
     // keeps the scheduler from overlapping strips (their live ranges would not fit the registers)
@@ -2296,18 +2315,18 @@ bool token_block_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && M.dff == 4 * M.d && M.layer[0].tb_o != nullptr;
 }
 
-template <int D, bool OQ>
+template <int D, bool OQ, bool Z>
 static hipError_t run_token_block(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
   constexpr size_t lds = token_block_lds<D>();
   const int64_t strips = (a.rows + 15) / 16;
   const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
   const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, (int64_t)M.cu_count * per_cu);
-  hipLaunchKernelGGL((k_token_block<D, OQ>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
+  hipLaunchKernelGGL((k_token_block<D, OQ, Z>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
-                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s) {
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z) {
   if (rows <= 0) return hipSuccess;
   if (!token_block_supported(M)) return hipErrorInvalidValue;
   const LayerWeights &W = M.layer[layer];
@@ -2328,19 +2347,26 @@ hipError_t launch_token_block(const Model &M, int layer, const float *o, const i
   a.rows = rows;
   a.xq = xq;
   a.ax = ax;
-  if (!oq == !o) return hipErrorInvalidValue;
-  if (oq) return M.d == 64 ? run_token_block<64, true>(M, a, s) : run_token_block<128, true>(M, a, s);
-  return M.d == 64 ? run_token_block<64, false>(M, a, s) : run_token_block<128, false>(M, a, s);
+  a.z = z;
+  a.w1 = M.head_w1_lo;
+  a.head_b1 = M.head_b1;
+  if (!oq == !o || (z && !M.head_w1_lo)) return hipErrorInvalidValue;
+  if (z) {
+    if (oq) return M.d == 64 ? run_token_block<64, true, true>(M, a, s) : run_token_block<128, true, true>(M, a, s);
+    return M.d == 64 ? run_token_block<64, false, true>(M, a, s) : run_token_block<128, false, true>(M, a, s);
+  }
+  if (oq) return M.d == 64 ? run_token_block<64, true, false>(M, a, s) : run_token_block<128, true, false>(M, a, s);
+  return M.d == 64 ? run_token_block<64, false, false>(M, a, s) : run_token_block<128, false, false>(M, a, s);
 }
 
 hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
-                             float *logits, bool lane_order, float *zbuf, hipStream_t s) {
+                             float *logits, bool lane_order, float *zbuf, hipStream_t s, bool z_ready) {
   if (words <= 0) return hipSuccess;
   if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
   HeadArgs a{x, y, M.n, M.L, M.head_w1, M.head_wo, M.head_bo, M.head_b1, bits, logits};
   const int64_t rows = words * M.L;
   const unsigned zgrid = (unsigned)std::min<int64_t>((rows + 15) / 16, (int64_t)M.cu_count * 64);
-  switch (M.d) {
+  if (!z_ready) switch (M.d) {
     case 32: hipLaunchKernelGGL((k_head_z<32, false>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf); break;
     case 64:
       if (lane_order) hipLaunchKernelGGL((k_head_z<64, true>), dim3(zgrid), dim3(256), 0, s, a, rows, zbuf);
@@ -2390,9 +2416,10 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
       (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
       (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
       (const void *)k_qkv_attention_v16<128>,    (const void *)k_qkv_attention_split<128>,
-      (const void *)k_token_block<64, true>,
-      (const void *)k_token_block<64, false>,    (const void *)k_token_block<128, true>,
-      (const void *)k_token_block<128, false>};
+      (const void *)k_token_block<64, true, false>,   (const void *)k_token_block<64, false, false>,
+      (const void *)k_token_block<128, true, false>,  (const void *)k_token_block<128, false, false>,
+      (const void *)k_token_block<64, true, true>,    (const void *)k_token_block<64, false, true>,
+      (const void *)k_token_block<128, true, true>,   (const void *)k_token_block<128, false, true>};
   for (const void *f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)M.lds_max);
     if (e != hipSuccess) return e;
