@@ -68,6 +68,7 @@ struct Model {
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;
   const float *head_w1_lo;    // W_{d->1} in the token block's lane order ([4][d/4], d = 64, 128), or null
+  const float *embed_lo, *pos_lo;   // embedding / positional rows in that lane order ([L][4][d/4]), or null
   float head_b1;
   LayerWeights layer[kMaxLayers];
   FusedTables fused;
@@ -89,7 +90,7 @@ void casa_union(TannerLists &T);   // M2 lists := M1 | M2 (every head on the ECC
 // byte 32 s + 8 g + k (a lane's eight codes of step s as one 8-byte word); the Q/K/V map is
 // packed a second time to read its inputs in that byte order.
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
-                        bool lane_order, hipStream_t s);
+                        bool lane_order, hipStream_t s, float *t = nullptr);
 hipError_t launch_qkv(const Model &M, int layer, const int8_t *xq, const float *ax, int64_t rows, float *qkv,
                       bool lane_order, hipStream_t s);
 hipError_t launch_attention(const Model &M, const float *qkv, int64_t words, float *o, int8_t *oq, float *ao,
@@ -122,8 +123,10 @@ bool token_block_supported(const Model &M);
 int64_t attention_word_slots(const Model &M, int form);
 // With z (the last layer): the head's z_i = W_{d->1} x_i + b1 of every output row to z [rows], and
 // neither x nor xq nor ax written.
+// With t (the first layer): x is not read; X is rebuilt from each token's t_i and the embedding.
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
-                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z = nullptr);
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z = nullptr,
+                              const float *t = nullptr);
 hipError_t launch_oproj_ln(const Model &M, int layer, const int8_t *oq, const float *ao, const float *x,
                            int64_t rows, float *x1, int8_t *x1q, float *a1, hipStream_t s);
 hipError_t launch_ffn1(const Model &M, int layer, const int8_t *x1q, const float *a1, int64_t rows, int8_t *gq,

@@ -92,7 +92,7 @@ size_t packed_words(int K, int N) { return (size_t)(K / 32) * (N / 16) * 64; }
 
 // Device memory plan: byte offsets inside the model's single allocation.
 struct Plan {
-  size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, w1, w1lo, wo, bo, total;
+  size_t chk_ptr, chk_idx, m1_ptr, m1_idx, m2_ptr, m2_idx, embed, pos, embed_lo, pos_lo, w1, w1lo, wo, bo, total;
   size_t g1_meta, g1_tab, g2_meta, g2_tab;   // grouped neighbour lists (layered attention)
   size_t g1s_tab, g2s_tab;                    // the same, counted within each node type
   size_t f_frag, f_vec, f_nbr, f_slot, f_tile, f_chk, f_tok, f_e, f_p, f_w1;
@@ -117,6 +117,8 @@ Plan make_plan(int n, int m, int d, int N, int dff, size_t E, size_t nnz1, size_
   p.m2_idx = take(sizeof(int32_t) * nnz2);
   p.embed = take(sizeof(float) * L * d);
   p.pos = has_pos ? take(sizeof(float) * L * d) : 0;
+  p.embed_lo = take(sizeof(float) * L * d);
+  p.pos_lo = has_pos ? take(sizeof(float) * L * d) : 0;
   p.w1 = take(sizeof(float) * d);
   p.w1lo = take(sizeof(float) * d);
   p.wo = take(sizeof(float) * (size_t)L * n);
@@ -495,6 +497,18 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   if (w->pos) put(P.pos, w->pos, 4 * (size_t)L * D);
   put(P.w1, w->head_w1, 4 * D);
   {
+    // the token block's lane order: [i][g][v] = row_i[4 v + g]
+    std::vector<float> lo((size_t)L * D);
+    auto to_lo = [&](const float *src, size_t off) {
+      for (size_t i = 0; i < (size_t)L; ++i)
+        for (size_t g = 0; g < 4; ++g)
+          for (size_t v = 0; v < D / 4; ++v) lo[i * D + g * (D / 4) + v] = src[i * D + 4 * v + g];
+      put(off, lo.data(), 4 * (size_t)L * D);
+    };
+    to_lo(w->embed, P.embed_lo);
+    if (w->pos) to_lo(w->pos, P.pos_lo);
+  }
+  {
     std::vector<float> w1lo(D);   // [g][v] = W_{d->1}[4 v + g]
     for (size_t g = 0; g < 4; ++g)
       for (size_t v = 0; v < D / 4; ++v) w1lo[g * (D / 4) + v] = w->head_w1[4 * v + g];
@@ -617,6 +631,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.pos = w->pos ? (const float *)(b + P.pos) : nullptr;
   M.head_w1 = (const float *)(b + P.w1);
   M.head_w1_lo = (const float *)(b + P.w1lo);
+  M.embed_lo = (const float *)(b + P.embed_lo);
+  M.pos_lo = w->pos ? (const float *)(b + P.pos_lo) : nullptr;
   M.head_wo = (const float *)(b + P.wo);
   M.head_bo = (const float *)(b + P.bo);
   for (int l = 0; l < n_layers; ++l) {
@@ -734,7 +750,10 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
   for (int64_t w0 = 0; w0 < batch; w0 += cw) {
     const int64_t nw = batch - w0 < cw ? batch - w0 : cw;
     const int64_t rows = nw * M.L;
-    hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, x, xq, ax, tb, s);
+    // with the token block the embedding leaves t_i per token (in ag, unused on that path) and
+    // the first token block rebuilds X from it rather than reading X back
+    float *tt = tb && rows <= INT32_MAX ? ag : nullptr;
+    hipError_t e = aecct::launch_embed(M, y + w0 * M.n, nw, tt ? nullptr : x, xq, ax, tb, s, tt);
     if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x, nw, M.d, false, xq, ax, s);
     for (int l = 0; l < M.n_layers && e == hipSuccess; ++l) {
       if (qa) {
@@ -752,8 +771,10 @@ static aecct_status decode_chunks(const Model &M, const float *y, int64_t batch,
       if (tb) {
         // the last layer leaves the head's z per token in a1 (free once the layers are done)
         float *zl = l == M.n_layers - 1 ? a1 : nullptr;
-        e = (qa && !qa_codes) || qw || qs ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s, zl)
-                     : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s, zl);
+        const float *t0 = l == 0 ? tt : nullptr;
+        e = (qa && !qa_codes) || qw || qs
+                ? aecct::launch_token_block(M, l, qkv, nullptr, nullptr, x, rows, xq, ax, s, zl, t0)
+                : aecct::launch_token_block(M, l, nullptr, oq, ao, x, rows, xq, ax, s, zl, t0);
       } else {
         e = aecct::launch_oproj_ln(M, l, oq, ao, x, rows, x1, x1q, a1, s);
         if (pw && e == hipSuccess) e = aecct::launch_word_quant(M, x1, nw, M.d, false, x1q, a1, s);

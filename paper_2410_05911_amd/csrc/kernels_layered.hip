@@ -32,6 +32,8 @@ struct EmbedArgs {
   float *x;
   int8_t *xq;
   float *ax;
+  float *t;   // with x null: each token's t_i (|y_i| or the syndrome sign), from which the first
+              // token block rebuilds X
 };
 
 template <int D, bool LO>
@@ -57,7 +59,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   for (int tt = 0; tt < T; ++tt) {
     const int col = 16 * tt + c;
     v[tt] = __builtin_fmaf(t, p.embed[(int64_t)i * D + col], p.pos ? p.pos[(int64_t)i * D + col] : 0.0f);
-    p.x[g * D + (LO ? lane_order_x<D>(col) : col)] = v[tt];
+    if (p.x) p.x[g * D + (LO ? lane_order_x<D>(col) : col)] = v[tt];
     amax = fmaxf(amax, fabsf(v[tt]));
   }
   amax = row16_max(amax);
@@ -65,6 +67,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) p.xq[g * D + (LO ? lane_order_q(16 * tt + c) : 16 * tt + c)] = quant_code(v[tt], inv);
   if (c == 0) p.ax[g] = amax;
+  if (c == 0 && p.t) p.t[g] = t;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1435,6 +1438,10 @@ struct TokenBlockArgs {
   float *z;
   const float *w1;              // [4][d/4] W_{d->1} in lane order (with z)
   float head_b1;
+  // the first layer: x is not read; X = fma(t_i, E_i, P_i) from each token's t [rows] and the
+  // embedding (and positional) rows in lane order [L][4][d/4] (pos may be null)
+  const float *t, *elo, *plo;
+  int L;
 };
 
 constexpr int kTbWaves = 8;
@@ -1451,6 +1458,8 @@ struct TbIn {
   long oc[OQ ? D / 32 : 1];
   float ao;
   float x[D / 4];
+  // E: the first layer, whose X is rebuilt from t_i and the embedding rows
+  template <bool E>
   __device__ __forceinline__ void load(const TokenBlockArgs &p, int64_t tl, int g) {
     if constexpr (OQ) {
 #pragma unroll
@@ -1464,6 +1473,19 @@ struct TbIn {
           const float4 f = *(const float4 *)(p.o + tl * D + 32 * s + 8 * g + k);
           o[s][k] = f.x; o[s][k + 1] = f.y; o[s][k + 2] = f.z; o[s][k + 3] = f.w;
         }
+    }
+    if constexpr (E) {   // X as the embedding computes it
+      const float tt = p.t[tl];
+      const uint32_t i = (uint32_t)tl % (uint32_t)p.L;   // rows < 2^31 with t (checked at launch)
+      const float *er = p.elo + i * D + g * (D / 4), *pr = p.plo ? p.plo + i * D + g * (D / 4) : nullptr;
+#pragma unroll
+      for (int u = 0; u < D / 4; u += 4) {
+        const float4 e = *(const float4 *)(er + u);
+        const float4 q = pr ? *(const float4 *)(pr + u) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        x[u] = __builtin_fmaf(tt, e.x, q.x); x[u + 1] = __builtin_fmaf(tt, e.y, q.y);
+        x[u + 2] = __builtin_fmaf(tt, e.z, q.z); x[u + 3] = __builtin_fmaf(tt, e.w, q.w);
+      }
+      return;
     }
 #pragma unroll
     for (int u = 0; u < D / 4; u += 4) {
@@ -1504,7 +1526,8 @@ __device__ __forceinline__ float tb_token_max(float a) {
 }
 
 // Z: the last layer, which leaves the head's z per token (TokenBlockArgs::z) instead of x, xq, ax.
-template <int D, bool OQ, bool Z>
+// E: the first layer, which rebuilds its residual X from t_i and the embedding instead of reading x.
+template <int D, bool OQ, bool Z, bool E>
 __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p) {
   constexpr int V = D / 4, S = D / 32, TO = D / 16, TH = D / 4, SH = D / 8;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -1539,7 +1562,7 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     const int64_t row0 = strip * 16, tok = row0 + c;
     const bool ok = tok < p.rows;
     TbIn<D, OQ> cur;
-    cur.load(p, load_row(strip), g);
+    cur.template load<E>(p, load_row(strip), g);
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
@@ -1954,9 +1977,10 @@ GemmArgs gemm_base(const int8_t *a, const float *alpha, const uint16_t *bpack, i
 }  // namespace
 
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
-                        bool lane_order, hipStream_t s) {
-  EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax};
+                        bool lane_order, hipStream_t s, float *t) {
+  EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax, t};
   if (a.rows <= 0) return hipSuccess;
+  if (!x && !t) return hipErrorInvalidValue;
   if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((a.rows + 15) / 16));
   switch (M.d) {
@@ -2315,18 +2339,35 @@ bool token_block_supported(const Model &M) {
   return (M.d == 64 || M.d == 128) && M.dff == 4 * M.d && M.layer[0].tb_o != nullptr;
 }
 
-template <int D, bool OQ, bool Z>
+template <int D, bool OQ, bool Z, bool E>
 static hipError_t run_token_block(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
   constexpr size_t lds = token_block_lds<D>();
   const int64_t strips = (a.rows + 15) / 16;
   const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
   const int64_t blocks = std::min<int64_t>((strips + kTbWaves - 1) / kTbWaves, (int64_t)M.cu_count * per_cu);
-  hipLaunchKernelGGL((k_token_block<D, OQ, Z>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
+  hipLaunchKernelGGL((k_token_block<D, OQ, Z, E>), dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(kTbWaves * 64), lds, s, a);
   return hipGetLastError();
+}
+// the instantiation for the arguments' form: codes or fp32 O, last layer, first layer
+template <int D, bool OQ, bool Z>
+static hipError_t run_token_block_e(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
+  return a.t ? run_token_block<D, OQ, Z, true>(M, a, s) : run_token_block<D, OQ, Z, false>(M, a, s);
+}
+template <int D, bool OQ>
+static hipError_t run_token_block_z(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
+  return a.z ? run_token_block_e<D, OQ, true>(M, a, s) : run_token_block_e<D, OQ, false>(M, a, s);
+}
+template <int D>
+static hipError_t run_token_block_oq(const Model &M, const TokenBlockArgs &a, hipStream_t s) {
+  return a.oq ? run_token_block_z<D, true>(M, a, s) : run_token_block_z<D, false>(M, a, s);
+}
+template <int D, int K>
+static const void *token_block_kernel() {
+  return (const void *)k_token_block<D, (K & 1) != 0, (K & 2) != 0, (K & 4) != 0>;
 }
 
 hipError_t launch_token_block(const Model &M, int layer, const float *o, const int8_t *oq, const float *ao,
-                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z) {
+                              float *x, int64_t rows, int8_t *xq, float *ax, hipStream_t s, float *z, const float *t) {
   if (rows <= 0) return hipSuccess;
   if (!token_block_supported(M)) return hipErrorInvalidValue;
   const LayerWeights &W = M.layer[layer];
@@ -2350,13 +2391,12 @@ hipError_t launch_token_block(const Model &M, int layer, const float *o, const i
   a.z = z;
   a.w1 = M.head_w1_lo;
   a.head_b1 = M.head_b1;
-  if (!oq == !o || (z && !M.head_w1_lo)) return hipErrorInvalidValue;
-  if (z) {
-    if (oq) return M.d == 64 ? run_token_block<64, true, true>(M, a, s) : run_token_block<128, true, true>(M, a, s);
-    return M.d == 64 ? run_token_block<64, false, true>(M, a, s) : run_token_block<128, false, true>(M, a, s);
-  }
-  if (oq) return M.d == 64 ? run_token_block<64, true, false>(M, a, s) : run_token_block<128, true, false>(M, a, s);
-  return M.d == 64 ? run_token_block<64, false, false>(M, a, s) : run_token_block<128, false, false>(M, a, s);
+  a.t = t;
+  a.elo = M.embed_lo;
+  a.plo = M.pos_lo;
+  a.L = M.L;
+  if (!oq == !o || (z && !M.head_w1_lo) || (t && (!M.embed_lo || rows > INT32_MAX))) return hipErrorInvalidValue;
+  return M.d == 64 ? run_token_block_oq<64>(M, a, s) : run_token_block_oq<128>(M, a, s);
 }
 
 hipError_t launch_head_tiled(const Model &M, const float *x, const float *y, int64_t words, uint8_t *bits,
@@ -2416,10 +2456,12 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
       (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
       (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
       (const void *)k_qkv_attention_v16<128>,    (const void *)k_qkv_attention_split<128>,
-      (const void *)k_token_block<64, true, false>,   (const void *)k_token_block<64, false, false>,
-      (const void *)k_token_block<128, true, false>,  (const void *)k_token_block<128, false, false>,
-      (const void *)k_token_block<64, true, true>,    (const void *)k_token_block<64, false, true>,
-      (const void *)k_token_block<128, true, true>,   (const void *)k_token_block<128, false, true>};
+      token_block_kernel<64, 0>(),  token_block_kernel<64, 1>(),  token_block_kernel<64, 2>(),
+      token_block_kernel<64, 3>(),  token_block_kernel<64, 4>(),  token_block_kernel<64, 5>(),
+      token_block_kernel<64, 6>(),  token_block_kernel<64, 7>(),  token_block_kernel<128, 0>(),
+      token_block_kernel<128, 1>(), token_block_kernel<128, 2>(), token_block_kernel<128, 3>(),
+      token_block_kernel<128, 4>(), token_block_kernel<128, 5>(), token_block_kernel<128, 6>(),
+      token_block_kernel<128, 7>()};
   for (const void *f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)M.lds_max);
     if (e != hipSuccess) return e;
