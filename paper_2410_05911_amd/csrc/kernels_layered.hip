@@ -1502,10 +1502,29 @@ constexpr size_t token_block_lds() {
   return (size_t)9 * D * D + (size_t)11 * D * 4;
 }
 
-// v of lane (this lane xor M), M = 16 or 32
+// The two values of lanes l and l ^ M (M = 16 or 32) with the gfx950 lane swaps: a swap of v
+// with itself returns, in some order, the lane's own v and its partner's, so their sum or
+// maximum is the butterfly step's (both operations commute).  The second operand is an opaque
+// copy, else the compiler treats the two results as equal.
 template <int M>
-__device__ __forceinline__ uint32_t tb_lane_xor(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((__builtin_amdgcn_workitem_id_x() & 63u) ^ M) << 2), (int)v);
+__device__ __forceinline__ void tb_swap_pair(uint32_t v, uint32_t &a, uint32_t &b) {
+  uint32_t w = v;
+  __asm__ volatile("" : "+v"(w));
+  if constexpr (M == 32) {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, w, false, false);
+    a = r[0];
+    b = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, w, false, false);
+    a = r[0];
+    b = r[1];
+  }
+}
+template <int M>
+__device__ __forceinline__ float tb_xor_add(float t) {
+  uint32_t a, b;
+  tb_swap_pair<M>(__builtin_bit_cast(uint32_t, t), a, b);
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 // Pairwise sum of a token's d features held as x[v] = feature 4 v + g.
 template <int V>
@@ -1513,16 +1532,14 @@ __device__ __forceinline__ float tb_token_sum(const float (&x)[V]) {
   float u[V];
 #pragma unroll
   for (int v = 0; v < V; ++v) u[v] = x[v];
-  float t = lane_tree<V>(u);
-  t = t + __builtin_bit_cast(float, tb_lane_xor<32>(__builtin_bit_cast(uint32_t, t)));
-  return t + __builtin_bit_cast(float, tb_lane_xor<16>(__builtin_bit_cast(uint32_t, t)));
+  return tb_xor_add<16>(tb_xor_add<32>(lane_tree<V>(u)));
 }
 // Maximum over the four lanes of a token (non-negative floats order like their bit patterns).
 __device__ __forceinline__ float tb_token_max(float a) {
-  uint32_t u = __builtin_bit_cast(uint32_t, a);
-  u = max(u, tb_lane_xor<32>(u));
-  u = max(u, tb_lane_xor<16>(u));
-  return __builtin_bit_cast(float, u);
+  uint32_t u = __builtin_bit_cast(uint32_t, a), p, q;
+  tb_swap_pair<32>(u, p, q);
+  tb_swap_pair<16>(max(p, q), p, q);
+  return __builtin_bit_cast(float, max(p, q));
 }
 
 // Z: the last layer, which leaves the head's z per token (TokenBlockArgs::z) instead of x, xq, ax.
