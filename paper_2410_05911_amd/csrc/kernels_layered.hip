@@ -19,6 +19,31 @@ template <int D>
 __device__ __forceinline__ int lane_order_x(int f) { return (f & 3) * (D / 4) + (f >> 2); }
 __device__ __forceinline__ int lane_order_q(int f) { return (f & ~31) + 8 * (f & 3) + ((f >> 2) & 7); }
 
+// The two values of lanes l and l ^ M (M = 16 or 32) with the gfx950 lane swaps: a swap of v
+// with itself returns, in some order, the lane's own v and its partner's, so their sum or
+// maximum is a butterfly step's (both operations commute).  The swap's two results are taken
+// out of its vector as integers: __builtin_bit_cast applied directly to an element of a vector
+// reads element 0 with this compiler.
+template <int M>
+__device__ __forceinline__ void lane_swap_pair(uint32_t v, uint32_t &a, uint32_t &b) {
+  if constexpr (M == 32) {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    a = r[0];
+    b = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    a = r[0];
+    b = r[1];
+  }
+}
+// v of this lane plus v of lane l ^ M (the same bits in both lanes)
+template <int M>
+__device__ __forceinline__ float lane_xor_add(float t) {
+  uint32_t a, b;
+  lane_swap_pair<M>(__builtin_bit_cast(uint32_t, t), a, b);
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+
 // ------------------------------------------------------------------------------------------
 // Embedding: pre-processing h(y) (Section 3), X = t * E (+ P), and the Eq. 2 code of X.
 // 16 lanes per row; lane c holds features c + 16 t, t < D / 16.  LO: X and Xq in lane order.
@@ -419,6 +444,15 @@ struct QaStage {
     for (int k = 0; k < kPer; ++k) {
       const int u = tid + k * NT;
       if (u < kWords) bf[u] = unpack_ternary8(pk[k]);
+    }
+  }
+  // only the query map's fragments (Q) or only the key and value maps' (!Q)
+  template <bool Q>
+  __device__ __forceinline__ void store_part(uint64_t *bf, int tid) const {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int u = tid + k * NT;
+      if (u < kWords && (u < (D / 32) * 64) == Q) bf[u] = unpack_ternary8(pk[k]);
     }
   }
 };
@@ -1059,12 +1093,17 @@ __global__ __launch_bounds__(kQaThreads) void k_qkv_attention_i16(QkvAttnArgs p)
 // ------------------------------------------------------------------------------------------
 // Long words with 16-dimension heads (d = 128, up to 1536 tokens): keys in LDS as fp32
 // (dequantised once, in the projection), values as their int16 accumulators, rebuilt by
-// fma(acc, alpha s_v, bias) at every gather as in k_qkv_attention_i16; every row split over a
-// lane pair as in k_qkv_attention_pair (lane 2 r + h takes dimensions 8 h .. 8 h + 7, the pair
-// adds the two score halves with one DPP exchange).  Blocks of 12 wavefronts (three per SIMD
-// with rows in flight).  Each wavefront keeps the int8 codes of its token tiles in registers for
-// all head groups of a word, read at the word's start with the tokens' Eq. 2 scales alpha, which
-// sit in LDS beside the keys and values.
+// fma(acc, alpha s_v, bias) at every gather as in k_qkv_attention_i16.  Blocks of 12 wavefronts
+// (three per SIMD with rows in flight).  Each wavefront keeps the int8 codes of its token tiles in
+// registers for all head groups of a word, read at the word's start with the tokens' Eq. 2 scales
+// alpha, which sit in LDS beside the keys and values.  The queries never leave registers: a
+// wavefront owns pairs of adjacent token tiles and runs their rows itself, forming a pair's
+// queries just before its rows with the transposed product (weights as the MFMA A operand, codes
+// as B), whose result holds one token and four query dimensions per lane; one lane swap per
+// dimension then leaves lane (t, r) (t = lane mod 16, r = lane / 16) with query dimensions
+// 8 (r / 2) .. 8 (r / 2) + 7 of token t of the pair's tile r mod 2, the half row that lane runs;
+// the two halves of a row sit in lanes l and l ^ 32 and add their score halves with a lane swap
+// (the canonical order: low half + high half, commuted bit for bit).
 // ------------------------------------------------------------------------------------------
 constexpr int kQvThreads = 768;
 constexpr int kQvTilesPerWave = 8;
@@ -1085,29 +1124,25 @@ __device__ __forceinline__ void qv_dequant(uint4 a, float c, const float (&b)[8]
   }
 }
 
-// One neighbour of a half row: k this lane's key half, va its value accumulators, c their scale.
+// One neighbour of a half row: k this lane's key half, va its value accumulators, c their scale;
+// the row's other half runs in lane l ^ 32.
 __device__ __forceinline__ void qv_step(const float (&q)[8], const float (&k)[8], uint4 va, float c,
                                         const float (&bv)[8], float shift, float &S, float (&acc)[8]) {
   float v[8];
   qv_dequant(va, c, bv, v);
   const float h = dot_seq<8>(q, k);
-  const float ex = softmax_exp2(h + pair_other(h) - shift);
+  const float ex = softmax_exp2(lane_xor_add<32>(h) - shift);
   S = S + ex;
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
 }
 
-// Attention of one half row: kb (keys) and vb (value accumulators) already offset to this lane's
-// half, orow to its 8 outputs (the query's half is read there first); a value's scale is
-// alpha sv, alpha from al.  Both lanes of a pair run it with the same row.
-__device__ __forceinline__ void qv_row(float *orow, const float *kb, const int16_t *vb, const float *al, float sv,
-                                       const float (&bv)[8], const uint2 *eg, int cnt) {
+// Attention of one half row with query half q: kb (keys) and vb (value accumulators) already
+// offset to this lane's half, orow to its 8 outputs; a value's scale is alpha sv, alpha from al.
+// Both lanes of a row run it with the same lists.
+__device__ __forceinline__ void qv_row(const float (&q)[8], float *orow, const float *kb, const int16_t *vb,
+                                       const float *al, float sv, const float (&bv)[8], const uint2 *eg, int cnt) {
   constexpr int R = kQvRow, RV = 2 * kQvRow;
-  float q[8];
-  {
-    const float4 a = *(const float4 *)orow, b = *(const float4 *)(orow + 4);
-    q[0] = a.x; q[1] = a.y; q[2] = a.z; q[3] = a.w; q[4] = b.x; q[5] = b.y; q[6] = b.z; q[7] = b.w;
-  }
   float S_ = 0.0f, acc[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = 0.0f;
@@ -1141,8 +1176,7 @@ __device__ __forceinline__ void qv_row(float *orow, const float *kb, const int16
     for (int e = 0; e < cnt; ++e) {
       float k[8];
       qa_load<8>(k, kb + qa_entry(eg, e) * R);
-      const float h = dot_seq<8>(q, k);
-      mu = fmaxf(mu, h + pair_other(h));
+      mu = fmaxf(mu, lane_xor_add<32>(dot_seq<8>(q, k)));
     }
     S_ = 0.0f;
 #pragma unroll
@@ -1170,13 +1204,16 @@ __device__ __forceinline__ void qa_load_codes(const int8_t *xw, int tt, int L, i
 template <int D>
 __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p) {
   constexpr int S = D / 32, G = D / 16, R = kQvRow, NT = kQvThreads, NWV = NT / 64, TW = kQvTilesPerWave;
+  static_assert(TW % 2 == 0, "tiles in pairs");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int L = p.L, ntiles = (L + 15) / 16;
   uint64_t *bf = (uint64_t *)smem;                                   // [3][S][64] weight fragments
   float *kvf = (float *)(smem + qa_frag_bytes<D>());                 // [L][R] keys, value accumulators
   int16_t *kvi = (int16_t *)kvf;
   float *als = kvf + (size_t)L * R;                                  // [L] the word's alpha per token
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4, half = tid & 1;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 15, rg = lane >> 4;
+  // the half row this lane runs in a tile pair: tile rg & 1 of the pair, dimensions 8 hq ..
+  const int hq = rg >> 1;
   if (blockIdx.x >= p.words) return;
   {
     QaStage<D, NT> st;
@@ -1185,34 +1222,35 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
   }
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
-  // Global loads are waited for only at the word's first barrier and after each projection (the
-  // barrier that publishes the queries): vmcnt counts stores too, so any other wait would also
-  // wait for the outputs still being written.
+  // Global loads are waited for only at the word's first barrier and after each projection:
+  // vmcnt counts stores too, so any other wait would also wait for the outputs still being written.
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     float *ow = p.o + w * L * D;
     // the word's token tiles (registers, for all head groups) and alphas (LDS); the previous word's
-    // rows are done with both
-    // an opaque copy of the wave index per word and per group: the per-tile addresses derived
+    // rows are done with both.  Tile k of a wavefront: 2 wave + (k mod 2) + 2 NWV (k / 2), so that
+    // k = 2 j, 2 j + 1 are the adjacent tiles of the wavefront's j-th pair.
+    // An opaque copy of the wave index per word and per group: the per-tile addresses derived
     // from it are not hoisted out of the loops (held for all tiles, they would not fit the
-    // registers)
+    // registers).
     int wv = wave;
     __asm__ volatile("" : "+v"(wv));
 #pragma unroll
-    for (int k = 0; k < TW; ++k) qa_load_codes<D>(p.xq + w * L * D, wv + NWV * k, L, lane, afr[k]);
+    for (int k = 0; k < TW; ++k)
+      qa_load_codes<D>(p.xq + w * L * D, 2 * wv + (k & 1) + 2 * NWV * (k >> 1), L, lane, afr[k]);
     for (int t = tid; t < L; t += NT) als[t] = p.ax[w * L + t];
     __syncthreads();
     for (int hg = 0; hg < G; ++hg) {
-      // the next group's weight tiles: read now, written to LDS once this projection is done
+      // the next group's weight tiles: read now; the key and value maps' written to LDS once
+      // this projection is done, the query map's once this group's rows are
       const bool more = hg + 1 < G || w + gridDim.x < p.words;
       QaStage<D, NT> st;
       if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
-      float bq = p.bias[16 * hg + col], bkc = p.bias[D + 16 * hg + col];
+      float bkc = p.bias[D + 16 * hg + col];
       int wg = wave;
-      // waited for here, before the first query store (not behind it)
-      __asm__ volatile("" : "+v"(wg), "+v"(bq), "+v"(bkc));
+      __asm__ volatile("" : "+v"(wg), "+v"(bkc));
 #pragma unroll
       for (int k = 0; k < TW; ++k) {
-        const int tt = wg + NWV * k;
+        const int tt = 2 * wg + (k & 1) + 2 * NWV * (k >> 1);
         if (tt >= ntiles) continue;
         float alv[4];
 #pragma unroll
@@ -1220,32 +1258,59 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
           const int tok = 16 * tt + 4 * rg + i;
           alv[i] = tok < L ? als[tok] : 0.0f;
         }
-        v4i aq = v4i{0, 0, 0, 0}, ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
+        v4i ak = v4i{0, 0, 0, 0}, av = v4i{0, 0, 0, 0};
         const auto fa = [&](int s) { return afr[k][s]; };
-        aq = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; }, aq);
         ak = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(1 * S + s) * 64 + lane]; }, ak);
         av = mfma_i8_steps<S>(fa, [&](int s) { return (long)bf[(2 * S + s) * 64 + lane]; }, av);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * tt + 4 * rg + i;
           if (tok < L) {
-            ow[(size_t)tok * D + 16 * hg + col] = __builtin_fmaf((float)aq[i], alv[i] * sq[0], bq);
             kvf[tok * R + col] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
             kvi[tok * 2 * R + 32 + col] = (int16_t)av[i];
           }
         }
       }
-      __syncthreads();   // also orders the queries written to memory before their rows read them
-      if (more) st.store(bf, tid);   // no wave reads this group's fragments any more
+      __syncthreads();
+      if (more) st.template store_part<false>(bf, tid);   // no wave reads this group's K, V fragments any more
       const bool first = hg < p.hf;
-      float bv[8];
-      qa_load<8>(bv, p.bias + 2 * D + 16 * hg + 8 * half);
-      for (int r = tid >> 1; r < L; r += NT / 2) {
-        const int2 mt = (first ? p.meta1 : p.meta2)[r];
-        qv_row(ow + (size_t)r * D + 16 * hg + 8 * half, kvf + 8 * half, kvi + 32 + 8 * half, als, sq[2], bv,
-               (first ? p.tab1 : p.tab2) + mt.x, mt.y);
+      float bv[8], bq[4];
+      qa_load<8>(bv, p.bias + 2 * D + 16 * hg + 8 * hq);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bq[i] = p.bias[16 * hg + 4 * rg + i];
+#pragma unroll
+      for (int j = 0; j < TW / 2; ++j) {
+        const int ta = 2 * wg + 2 * NWV * j;   // the pair's first tile
+        if (ta >= ntiles) break;
+        // the pair's queries, transposed: lane (t, r) gets query dimensions 4 r + i of token t
+        // of each tile, dequantised as the projection defines them
+        v4i qa = v4i{0, 0, 0, 0}, qb = v4i{0, 0, 0, 0};
+        const auto fw = [&](int s) { return (long)bf[(0 * S + s) * 64 + lane]; };
+        qa = mfma_i8_steps<S>(fw, [&](int s) { return afr[2 * j][s]; }, qa);
+        qb = mfma_i8_steps<S>(fw, [&](int s) { return afr[2 * j + 1][s]; }, qb);
+        const int ra = 16 * ta + col, rb = ra + 16;
+        const float sa = (ra < L ? als[ra] : 0.0f) * sq[0], sb = (rb < L ? als[rb] : 0.0f) * sq[0];
+        float q[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float va = __builtin_fmaf((float)qa[i], sa, bq[i]), vb = __builtin_fmaf((float)qb[i], sb, bq[i]);
+          // rows 0, 1 | 2, 3 of the lanes: (a of row 2 u, b of row 2 u) | (a of row 2 u + 1, b of
+          // row 2 u + 1) -> lane row 2 u + c: tile c's dimensions 8 u + i and 8 u + 4 + i
+          const auto sw = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, va),
+                                                           __builtin_bit_cast(uint32_t, vb), false, false);
+          const uint32_t lo = sw[0], hi = sw[1];   // as integers first (see lane_swap_pair)
+          q[i] = __builtin_bit_cast(float, lo);
+          q[4 + i] = __builtin_bit_cast(float, hi);
+        }
+        const int r = 16 * (ta + (rg & 1)) + col;
+        if (r < L) {
+          const int2 mt = (first ? p.meta1 : p.meta2)[r];
+          qv_row(q, ow + (size_t)r * D + 16 * hg + 8 * hq, kvf + 8 * hq, kvi + 32 + 8 * hq, als, sq[2], bv,
+                 (first ? p.tab1 : p.tab2) + mt.x, mt.y);
+        }
       }
       block_sync_lds();            // the next group's projection overwrites keys and values
+      if (more) st.template store_part<true>(bf, tid);   // read only by the next group's rows
     }
   }
 }
@@ -1458,9 +1523,10 @@ struct TbIn {
   long oc[OQ ? D / 32 : 1];
   float ao;
   float x[D / 4];
-  // E: the first layer, whose X is rebuilt from t_i and the embedding rows
+  // E: the first layer, whose X is rebuilt from t_i and the embedding rows (ie: the token's
+  // position i in its word, or any position for a padding column)
   template <bool E>
-  __device__ __forceinline__ void load(const TokenBlockArgs &p, int64_t tl, int g) {
+  __device__ __forceinline__ void load(const TokenBlockArgs &p, int64_t tl, int g, uint32_t ie) {
     if constexpr (OQ) {
 #pragma unroll
       for (int s = 0; s < D / 32; ++s) oc[s] = *(const long *)(p.oq + tl * D + 32 * s + 8 * g);
@@ -1476,8 +1542,7 @@ struct TbIn {
     }
     if constexpr (E) {   // X as the embedding computes it
       const float tt = p.t[tl];
-      const uint32_t i = (uint32_t)tl % (uint32_t)p.L;   // rows < 2^31 with t (checked at launch)
-      const float *er = p.elo + i * D + g * (D / 4), *pr = p.plo ? p.plo + i * D + g * (D / 4) : nullptr;
+      const float *er = p.elo + ie * D + g * (D / 4), *pr = p.plo ? p.plo + ie * D + g * (D / 4) : nullptr;
 #pragma unroll
       for (int u = 0; u < D / 4; u += 4) {
         const float4 e = *(const float4 *)(er + u);
@@ -1502,43 +1567,19 @@ constexpr size_t token_block_lds() {
   return (size_t)9 * D * D + (size_t)11 * D * 4;
 }
 
-// The two values of lanes l and l ^ M (M = 16 or 32) with the gfx950 lane swaps: a swap of v
-// with itself returns, in some order, the lane's own v and its partner's, so their sum or
-// maximum is the butterfly step's (both operations commute).  The second operand is an opaque
-// copy, else the compiler treats the two results as equal.
-template <int M>
-__device__ __forceinline__ void tb_swap_pair(uint32_t v, uint32_t &a, uint32_t &b) {
-  uint32_t w = v;
-  __asm__ volatile("" : "+v"(w));
-  if constexpr (M == 32) {
-    const auto r = __builtin_amdgcn_permlane32_swap(v, w, false, false);
-    a = r[0];
-    b = r[1];
-  } else {
-    const auto r = __builtin_amdgcn_permlane16_swap(v, w, false, false);
-    a = r[0];
-    b = r[1];
-  }
-}
-template <int M>
-__device__ __forceinline__ float tb_xor_add(float t) {
-  uint32_t a, b;
-  tb_swap_pair<M>(__builtin_bit_cast(uint32_t, t), a, b);
-  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
-}
 // Pairwise sum of a token's d features held as x[v] = feature 4 v + g.
 template <int V>
 __device__ __forceinline__ float tb_token_sum(const float (&x)[V]) {
   float u[V];
 #pragma unroll
   for (int v = 0; v < V; ++v) u[v] = x[v];
-  return tb_xor_add<16>(tb_xor_add<32>(lane_tree<V>(u)));
+  return lane_xor_add<16>(lane_xor_add<32>(lane_tree<V>(u)));
 }
 // Maximum over the four lanes of a token (non-negative floats order like their bit patterns).
 __device__ __forceinline__ float tb_token_max(float a) {
   uint32_t u = __builtin_bit_cast(uint32_t, a), p, q;
-  tb_swap_pair<32>(u, p, q);
-  tb_swap_pair<16>(max(p, q), p, q);
+  lane_swap_pair<32>(u, p, q);
+  lane_swap_pair<16>(max(p, q), p, q);
   return __builtin_bit_cast(float, max(p, q));
 }
 
@@ -1579,7 +1620,15 @@ __global__ __launch_bounds__(kTbWaves * 64) void k_token_block(TokenBlockArgs p)
     const int64_t row0 = strip * 16, tok = row0 + c;
     const bool ok = tok < p.rows;
     TbIn<D, OQ> cur;
-    cur.template load<E>(p, load_row(strip), g);
+    uint32_t ie = 0;
+    if constexpr (E) {
+      // the strip's first row is wave-uniform, so its position in the word is scalar work; rows
+      // < 2^31 with t (checked at launch)
+      const uint32_t L = (uint32_t)p.L;
+      ie = (uint32_t)row0 % L + (uint32_t)c;
+      while (ie >= L) ie -= L;
+    }
+    cur.template load<E>(p, load_row(strip), g, ie);
     // ---- output projection, residual, LN1, Eq. 2 ----
     float x1[V];
     long xb[S];
