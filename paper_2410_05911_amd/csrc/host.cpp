@@ -159,19 +159,25 @@ struct WsPlan {
 
 WsPlan ws_plan(const Model &M, int64_t words) {
   const size_t R = (size_t)words * M.L, d = M.d, dff = M.dff;
+  // With the token block a layer needs X, its codes, the attention output (fp32 in the qkv region,
+  // d wide, from the fused forms that leave it so; the separate GEMM's Q, K, V there, 3 d wide;
+  // codes in oq otherwise) and per-token scalars (the head's z in a1, the embedding's t in ag);
+  // X1, its codes and the hidden codes stay in the token block's registers.
+  const bool tb = !M.act_word && aecct::token_block_supported(M);
+  const bool unf = M.lattn == AECCT_LAYERED_ATTN_UNFUSED;
   WsPlan w{};
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   w.x = take(4 * R * d);
   w.xq = take(R * d);
   w.ax = take(4 * R);
-  w.qkv = take(4 * R * 3 * d);
+  w.qkv = take(4 * R * (tb && !unf ? 1 : 3) * d);
   w.oq = take(R * d);
   w.ao = take(4 * R);
-  w.x1 = take(4 * R * d);
-  w.x1q = take(R * d);
+  w.x1 = take(tb ? 0 : 4 * R * d);
+  w.x1q = take(tb ? 0 : R * d);
   w.a1 = take(4 * R);
-  w.gq = take(R * dff);
+  w.gq = take(tb ? 0 : R * dff);
   w.ag = take(4 * R);
   if (M.act_word) {
     w.o32 = take(4 * R * d);

@@ -44,9 +44,22 @@ __device__ __forceinline__ float lane_xor_add(float t) {
   return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
+// Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
+__device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
+  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
+  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
+  return (long)(((uint64_t)hi << 32) | lo);
+}
+
 // ------------------------------------------------------------------------------------------
 // Embedding: pre-processing h(y) (Section 3), X = t * E (+ P), and the Eq. 2 code of X.
-// 16 lanes per row; lane c holds features c + 16 t, t < D / 16.  LO: X and Xq in lane order.
+// 16 lanes per row.  Natural layout: lane c holds features c + 16 t, t < D / 16.  LO: X and Xq in
+// lane order, lane c holding the D / 16 consecutive lane-order positions from c D / 16 on (of
+// Xq, position 32 s + 8 g + e holds feature 32 s + 4 e + g; of X and of the lane-order
+// embedding rows, position g D / 4 + v holds feature 4 v + g, the same features), so that its
+// reads and writes are contiguous.
 // ------------------------------------------------------------------------------------------
 struct EmbedArgs {
   const float *y;
@@ -59,6 +72,7 @@ struct EmbedArgs {
   float *ax;
   float *t;   // with x null: each token's t_i (|y_i| or the syndrome sign), from which the first
               // token block rebuilds X
+  const float *elo, *plo;   // LO: embedding and positional rows in lane order (plo may be null)
 };
 
 template <int D, bool LO>
@@ -77,6 +91,40 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
     int s = 0;
     for (int e = p.chk_ptr[i - p.n]; e < p.chk_ptr[i - p.n + 1]; ++e) s ^= (yw[p.chk_idx[e]] < 0.0f) ? 1 : 0;
     t = s ? -1.0f : 1.0f;
+  }
+  if constexpr (LO) {
+    // positions F c .. F c + F - 1 of Xq: s = F c / 32, g = (F c / 8) mod 4, e from F c mod 8;
+    // their features 32 s + 4 e + g sit at lane-order position g D / 4 + 8 s + e of X
+    constexpr int F = T;
+    const int q0 = F * c, sx = q0 >> 5, gx = (q0 >> 3) & 3, e0 = q0 & 7;
+    const int xo = gx * (D / 4) + 8 * sx + e0;
+    float v[F];
+    float amax = 0.0f;
+#pragma unroll
+    for (int u = 0; u < F; u += 4) {
+      const float4 e = *(const float4 *)(p.elo + (int64_t)i * D + xo + u);
+      const float4 q = p.plo ? *(const float4 *)(p.plo + (int64_t)i * D + xo + u) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      v[u] = __builtin_fmaf(t, e.x, q.x);
+      v[u + 1] = __builtin_fmaf(t, e.y, q.y);
+      v[u + 2] = __builtin_fmaf(t, e.z, q.z);
+      v[u + 3] = __builtin_fmaf(t, e.w, q.w);
+      if (p.x) *(float4 *)(p.x + g * D + xo + u) = make_float4(v[u], v[u + 1], v[u + 2], v[u + 3]);
+    }
+#pragma unroll
+    for (int u = 0; u < F; ++u) amax = fmaxf(amax, fabsf(v[u]));
+    amax = row16_max(amax);
+    const float inv = inv127(amax);
+    uint32_t b[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) b[u] = quant_bits(v[u < F ? u : 0], inv);
+    if constexpr (F == 8) {
+      *(long *)(p.xq + g * D + q0) = tb_pack8(b);
+    } else {
+      *(uint32_t *)(p.xq + g * D + q0) = (uint32_t)tb_pack8(b);
+    }
+    if (c == 0) p.ax[g] = amax;
+    if (c == 0 && p.t) p.t[g] = t;
+    return;
   }
   float v[T];
   float amax = 0.0f;
@@ -721,14 +769,6 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
 constexpr int kQpThreads = 768;
 constexpr int kQpTilesPerWave = 3;
 
-// Byte 0 of eight Eq. 2 code patterns into one 64-bit B operand (byte e from b[e]).
-__device__ __forceinline__ long tb_pack8(const uint32_t (&b)[8]) {
-  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
-                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
-  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
-                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
-  return (long)(((uint64_t)hi << 32) | lo);
-}
 
 // the partner lane's value (lane ^ 1) within the quad
 __device__ __forceinline__ float pair_other(float v) {
@@ -2044,10 +2084,10 @@ GemmArgs gemm_base(const int8_t *a, const float *alpha, const uint16_t *bpack, i
 
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
                         bool lane_order, hipStream_t s, float *t) {
-  EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax, t};
+  EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax, t, M.embed_lo, M.pos_lo};
   if (a.rows <= 0) return hipSuccess;
   if (!x && !t) return hipErrorInvalidValue;
-  if (lane_order && M.d != 64 && M.d != 128) return hipErrorInvalidValue;
+  if (lane_order && ((M.d != 64 && M.d != 128) || !M.embed_lo)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((a.rows + 15) / 16));
   switch (M.d) {
     case 32: hipLaunchKernelGGL((k_embed<32, false>), grid, dim3(256), 0, s, a); break;
