@@ -75,6 +75,74 @@ struct EmbedArgs {
   const float *elo, *plo;   // LO: embedding and positional rows in lane order (plo may be null)
 };
 
+// Row g (token i of its word, t = t_i) in lane order, lane c of the row's 16: positions F c ..
+// F c + F - 1 of Xq (F = D / 16): s = F c / 32, g = (F c / 8) mod 4, e from F c mod 8, whose
+// features 32 s + 4 e + g sit at lane-order position g D / 4 + 8 s + e of X and of the
+// lane-order embedding rows.
+template <int D>
+__device__ __forceinline__ void embed_row_lo(const EmbedArgs &p, int64_t g, int i, float t, int c) {
+  constexpr int F = D / 16;
+  const int q0 = F * c, sx = q0 >> 5, gx = (q0 >> 3) & 3, e0 = q0 & 7;
+  const int xo = gx * (D / 4) + 8 * sx + e0;
+  float v[F];
+  float amax = 0.0f;
+#pragma unroll
+  for (int u = 0; u < F; u += 4) {
+    const float4 e = *(const float4 *)(p.elo + (int64_t)i * D + xo + u);
+    const float4 q = p.plo ? *(const float4 *)(p.plo + (int64_t)i * D + xo + u) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    v[u] = __builtin_fmaf(t, e.x, q.x);
+    v[u + 1] = __builtin_fmaf(t, e.y, q.y);
+    v[u + 2] = __builtin_fmaf(t, e.z, q.z);
+    v[u + 3] = __builtin_fmaf(t, e.w, q.w);
+    if (p.x) *(float4 *)(p.x + g * D + xo + u) = make_float4(v[u], v[u + 1], v[u + 2], v[u + 3]);
+  }
+#pragma unroll
+  for (int u = 0; u < F; ++u) amax = fmaxf(amax, fabsf(v[u]));
+  amax = row16_max(amax);
+  const float inv = inv127(amax);
+  uint32_t b[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) b[u] = quant_bits(v[u < F ? u : 0], inv);
+  if constexpr (F == 8) {
+    *(long *)(p.xq + g * D + q0) = tb_pack8(b);
+  } else {
+    *(uint32_t *)(p.xq + g * D + q0) = (uint32_t)tb_pack8(b);
+  }
+  if (c == 0) p.ax[g] = amax;
+  if (c == 0 && p.t) p.t[g] = t;
+}
+
+// Lane order, one word per block (persistent over the words): the word's y in LDS, every
+// token's t_i from it (the checks' lists from the L2), then the rows, 16 lanes each.
+constexpr int kEwThreads = 256;
+template <int D>
+__global__ __launch_bounds__(kEwThreads) void k_embed_words(EmbedArgs p, int64_t words) {
+  extern __shared__ float esm[];   // [n] the word's y, [L] its t
+  float *ys = esm, *ts = esm + p.n;
+  const int tid = threadIdx.x, c = tid & 15;
+  for (int64_t w = blockIdx.x; w < words; w += gridDim.x) {
+    const float *yw = p.y + w * p.n;
+    for (int i = tid; i < p.n; i += kEwThreads) ys[i] = yw[i];
+    __syncthreads();
+    for (int i = tid; i < p.L; i += kEwThreads) {
+      float t;
+      if (i < p.n) {
+        t = fabsf(ys[i]);
+      } else {
+        int s = 0;
+        for (int e = p.chk_ptr[i - p.n]; e < p.chk_ptr[i - p.n + 1]; ++e) s ^= (ys[p.chk_idx[e]] < 0.0f) ? 1 : 0;
+        t = s ? -1.0f : 1.0f;
+      }
+      ts[i] = t;
+    }
+    __syncthreads();
+    for (int i = tid >> 4; i < p.L; i += kEwThreads / 16) embed_row_lo<D>(p, w * p.L + i, i, ts[i], c);
+    __syncthreads();   // the next word overwrites y and t
+  }
+}
+
+// 16 lanes per row, one row per 16 lanes of the grid: the natural layout, or (LO) the lane order
+// for words whose y and t do not fit LDS.
 template <int D, bool LO>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   constexpr int T = D / 16;
@@ -93,37 +161,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
     t = s ? -1.0f : 1.0f;
   }
   if constexpr (LO) {
-    // positions F c .. F c + F - 1 of Xq: s = F c / 32, g = (F c / 8) mod 4, e from F c mod 8;
-    // their features 32 s + 4 e + g sit at lane-order position g D / 4 + 8 s + e of X
-    constexpr int F = T;
-    const int q0 = F * c, sx = q0 >> 5, gx = (q0 >> 3) & 3, e0 = q0 & 7;
-    const int xo = gx * (D / 4) + 8 * sx + e0;
-    float v[F];
-    float amax = 0.0f;
-#pragma unroll
-    for (int u = 0; u < F; u += 4) {
-      const float4 e = *(const float4 *)(p.elo + (int64_t)i * D + xo + u);
-      const float4 q = p.plo ? *(const float4 *)(p.plo + (int64_t)i * D + xo + u) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      v[u] = __builtin_fmaf(t, e.x, q.x);
-      v[u + 1] = __builtin_fmaf(t, e.y, q.y);
-      v[u + 2] = __builtin_fmaf(t, e.z, q.z);
-      v[u + 3] = __builtin_fmaf(t, e.w, q.w);
-      if (p.x) *(float4 *)(p.x + g * D + xo + u) = make_float4(v[u], v[u + 1], v[u + 2], v[u + 3]);
-    }
-#pragma unroll
-    for (int u = 0; u < F; ++u) amax = fmaxf(amax, fabsf(v[u]));
-    amax = row16_max(amax);
-    const float inv = inv127(amax);
-    uint32_t b[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) b[u] = quant_bits(v[u < F ? u : 0], inv);
-    if constexpr (F == 8) {
-      *(long *)(p.xq + g * D + q0) = tb_pack8(b);
-    } else {
-      *(uint32_t *)(p.xq + g * D + q0) = (uint32_t)tb_pack8(b);
-    }
-    if (c == 0) p.ax[g] = amax;
-    if (c == 0 && p.t) p.t[g] = t;
+    embed_row_lo<D>(p, g, i, t, c);
     return;
   }
   float v[T];
@@ -132,15 +170,14 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
   for (int tt = 0; tt < T; ++tt) {
     const int col = 16 * tt + c;
     v[tt] = __builtin_fmaf(t, p.embed[(int64_t)i * D + col], p.pos ? p.pos[(int64_t)i * D + col] : 0.0f);
-    if (p.x) p.x[g * D + (LO ? lane_order_x<D>(col) : col)] = v[tt];
+    if (p.x) p.x[g * D + col] = v[tt];
     amax = fmaxf(amax, fabsf(v[tt]));
   }
   amax = row16_max(amax);
   const float inv = inv127(amax);
 #pragma unroll
-  for (int tt = 0; tt < T; ++tt) p.xq[g * D + (LO ? lane_order_q(16 * tt + c) : 16 * tt + c)] = quant_code(v[tt], inv);
+  for (int tt = 0; tt < T; ++tt) p.xq[g * D + 16 * tt + c] = quant_code(v[tt], inv);
   if (c == 0) p.ax[g] = amax;
-  if (c == 0 && p.t) p.t[g] = t;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -2082,6 +2119,9 @@ GemmArgs gemm_base(const int8_t *a, const float *alpha, const uint16_t *bpack, i
 
 }  // namespace
 
+// LDS of k_embed_words: the word's y and t.
+static size_t embed_words_lds(const Model &M) { return sizeof(float) * (size_t)(M.n + M.L); }
+
 hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x, int8_t *xq, float *ax,
                         bool lane_order, hipStream_t s, float *t) {
   EmbedArgs a{y, words * M.L, M.n, M.L, M.chk_ptr, M.chk_idx, M.embed, M.pos, x, xq, ax, t, M.embed_lo, M.pos_lo};
@@ -2089,16 +2129,24 @@ hipError_t launch_embed(const Model &M, const float *y, int64_t words, float *x,
   if (!x && !t) return hipErrorInvalidValue;
   if (lane_order && ((M.d != 64 && M.d != 128) || !M.embed_lo)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((a.rows + 15) / 16));
+  if (lane_order) {
+    const size_t lds = embed_words_lds(M);
+    if (lds <= M.lds_max) {
+      const unsigned wgrid = (unsigned)std::min<int64_t>(words, (int64_t)M.cu_count * 8);
+      if (M.d == 64) hipLaunchKernelGGL((k_embed_words<64>), dim3(wgrid), dim3(kEwThreads), lds, s, a, words);
+      else hipLaunchKernelGGL((k_embed_words<128>), dim3(wgrid), dim3(kEwThreads), lds, s, a, words);
+    } else if (M.d == 64) {
+      hipLaunchKernelGGL((k_embed<64, true>), grid, dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_embed<128, true>), grid, dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+  }
+  if (t) return hipErrorInvalidValue;   // t only with the lane order (the token block's first layer)
   switch (M.d) {
     case 32: hipLaunchKernelGGL((k_embed<32, false>), grid, dim3(256), 0, s, a); break;
-    case 64:
-      if (lane_order) hipLaunchKernelGGL((k_embed<64, true>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_embed<64, false>), grid, dim3(256), 0, s, a);
-      break;
-    case 128:
-      if (lane_order) hipLaunchKernelGGL((k_embed<128, true>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_embed<128, false>), grid, dim3(256), 0, s, a);
-      break;
+    case 64: hipLaunchKernelGGL((k_embed<64, false>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((k_embed<128, false>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -2567,7 +2615,8 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
       token_block_kernel<64, 6>(),  token_block_kernel<64, 7>(),  token_block_kernel<128, 0>(),
       token_block_kernel<128, 1>(), token_block_kernel<128, 2>(), token_block_kernel<128, 3>(),
       token_block_kernel<128, 4>(), token_block_kernel<128, 5>(), token_block_kernel<128, 6>(),
-      token_block_kernel<128, 7>()};
+      token_block_kernel<128, 7>(),                   (const void *)k_embed_words<64>,
+      (const void *)k_embed_words<128>};
   for (const void *f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)M.lds_max);
     if (e != hipSuccess) return e;
