@@ -1201,6 +1201,17 @@ __device__ __forceinline__ void qv_dequant(uint4 a, float c, const float (&b)[8]
   }
 }
 
+// A token's key in LDS as four 16-byte chunks holding dimensions 0-3, 8-11, 4-7, 12-15: the two
+// lanes of a row then read chunks h and h + 2 (dimensions 8 h .. 8 h + 7), so that with the 96-byte
+// token rows (6 bank groups of 16 bytes apart) the two halves' reads fall on bank groups of both
+// parities, where chunks 2 h, 2 h + 1 put every first read on an even group.
+__device__ __forceinline__ int qv_key_slot(int dim) { return (dim & 3) | ((dim & 4) << 1) | ((dim & 8) >> 1); }
+// this lane's key half of a token: kh points at the token's chunk h
+__device__ __forceinline__ void qv_load_key(float (&k)[8], const float *kh) {
+  const float4 a = *(const float4 *)kh, b = *(const float4 *)(kh + 8);
+  k[0] = a.x; k[1] = a.y; k[2] = a.z; k[3] = a.w; k[4] = b.x; k[5] = b.y; k[6] = b.z; k[7] = b.w;
+}
+
 // One neighbour of a half row: k this lane's key half, va its value accumulators, c their scale;
 // the row's other half runs in lane l ^ 32.
 __device__ __forceinline__ void qv_step(const float (&q)[8], const float (&k)[8], uint4 va, float c,
@@ -1214,8 +1225,9 @@ __device__ __forceinline__ void qv_step(const float (&q)[8], const float (&k)[8]
   for (int t = 0; t < 8; ++t) acc[t] = __builtin_fmaf(ex, v[t], acc[t]);
 }
 
-// Attention of one half row with query half q: kb (keys) and vb (value accumulators) already
-// offset to this lane's half, orow to its 8 outputs; a value's scale is alpha sv, alpha from al.
+// Attention of one half row with query half q: kb (keys, at this lane's chunk h) and vb (value
+// accumulators, at this lane's half) already offset, orow to its 8 outputs; a value's scale is
+// alpha sv, alpha from al.
 // Both lanes of a row run it with the same lists.
 __device__ __forceinline__ void qv_row(const float (&q)[8], float *orow, const float *kb, const int16_t *vb,
                                        const float *al, float sv, const float (&bv)[8], const uint2 *eg, int cnt) {
@@ -1228,11 +1240,11 @@ __device__ __forceinline__ void qv_row(const float (&q)[8], float *orow, const f
   // token 0)
   uint2 gc = eg[0];
   float ka[8], kn[8];
-  qa_load<8>(ka, kb + (gc.x & 0xffffu) * R);
+  qv_load_key(ka, kb + (gc.x & 0xffffu) * R);
   auto stage = [&](uint32_t cur, uint32_t nxt, float (&kc)[8], float (&kx)[8]) {
     const uint4 va = *(const uint4 *)(vb + cur * RV);
     const float c = al[cur] * sv;
-    qa_load<8>(kx, kb + nxt * R);
+    qv_load_key(kx, kb + nxt * R);
     qv_step(q, kc, va, c, bv, 0.0f, S_, acc);
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -1252,7 +1264,7 @@ __device__ __forceinline__ void qv_row(const float (&q)[8], float *orow, const f
     float mu = -INFINITY;
     for (int e = 0; e < cnt; ++e) {
       float k[8];
-      qa_load<8>(k, kb + qa_entry(eg, e) * R);
+      qv_load_key(k, kb + qa_entry(eg, e) * R);
       mu = fmaxf(mu, lane_xor_add<32>(dot_seq<8>(q, k)));
     }
     S_ = 0.0f;
@@ -1261,7 +1273,7 @@ __device__ __forceinline__ void qv_row(const float (&q)[8], float *orow, const f
     for (int e = 0; e < cnt; ++e) {
       const uint32_t j = qa_entry(eg, e);
       float k[8];
-      qa_load<8>(k, kb + j * R);
+      qv_load_key(k, kb + j * R);
       qv_step(q, k, *(const uint4 *)(vb + j * RV), al[j] * sv, bv, mu, S_, acc);
     }
   }
@@ -1343,7 +1355,7 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * tt + 4 * rg + i;
           if (tok < L) {
-            kvf[tok * R + col] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
+            kvf[tok * R + qv_key_slot(col)] = __builtin_fmaf((float)ak[i], alv[i] * sq[1], bkc);
             kvi[tok * 2 * R + 32 + col] = (int16_t)av[i];
           }
         }
@@ -1382,7 +1394,7 @@ __global__ __launch_bounds__(kQvThreads) void k_qkv_attention_v16(QkvAttnArgs p)
         const int r = 16 * (ta + (rg & 1)) + col;
         if (r < L) {
           const int2 mt = (first ? p.meta1 : p.meta2)[r];
-          qv_row(q, ow + (size_t)r * D + 16 * hg + 8 * hq, kvf + 8 * hq, kvi + 32 + 8 * hq, als, sq[2], bv,
+          qv_row(q, ow + (size_t)r * D + 16 * hg + 8 * hq, kvf + 4 * hq, kvi + 32 + 8 * hq, als, sq[2], bv,
                  (first ? p.tab1 : p.tab2) + mt.x, mt.y);
         }
       }
