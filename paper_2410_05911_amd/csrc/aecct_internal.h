@@ -65,6 +65,7 @@ struct Model {
   // with head partitioning every list holds one node type: the same lists with entries counted
   // from the first token of that type (variables from 0, checks from n), or null
   const uint16_t *g1s_tab, *g2s_tab;
+  int32_t g1_groups, g2_groups;      // groups of four entries in g1_tab, g2_tab
   const float *embed, *pos;   // pos may be null
   const float *head_w1, *head_wo, *head_bo;
   const float *head_w1_lo;    // W_{d->1} in the token block's lane order ([4][d/4], d = 64, 128), or null

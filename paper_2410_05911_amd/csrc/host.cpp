@@ -631,6 +631,8 @@ aecct_status aecct_create(const uint8_t *H, int32_t m, int32_t n, const aecct_we
   M.g1_tab = (const uint16_t *)(b + P.g1_tab);
   M.g2_meta = (const int32_t *)(b + P.g2_meta);
   M.g2_tab = (const uint16_t *)(b + P.g2_tab);
+  M.g1_groups = (int32_t)(G1.size() / 4);
+  M.g2_groups = (int32_t)(G2.size() / 4);
   M.g1s_tab = G1s.empty() ? nullptr : (const uint16_t *)(b + P.g1s_tab);
   M.g2s_tab = G2s.empty() ? nullptr : (const uint16_t *)(b + P.g2s_tab);
   M.embed = (const float *)(b + P.embed);

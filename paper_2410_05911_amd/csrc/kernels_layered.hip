@@ -488,6 +488,7 @@ struct QkvAttnArgs {
   // tokens of the larger node type
   const uint2 *tab1s, *tab2s;
   int n_var, kv_cap;
+  int tab1_n, tab2_n;          // groups in tab1, tab2 (k_qkv_attention_pair with the lists in LDS)
 };
 
 constexpr int kQaThreads = 512;
@@ -892,7 +893,11 @@ __device__ __forceinline__ void qp_row(const float *qrow, const float *kb, const
 // OQ: a word of at most 384 tokens (one row per lane pair) keeps each row's outputs of all head
 // groups in registers (64 per lane) and writes the row's Eq. 2 codes and scale once the last
 // group is done, so the token block reads a quarter of the bytes; else fp32 rows per group.
-template <int D, bool OQ>
+// LT (with OQ): the neighbour lists and their per-token metadata are staged in LDS once per block,
+// so the rows issue no global loads, and the next word's token tiles are read into registers
+// right after the last group's projection, while its rows run (a wait for any global load would
+// also wait for every earlier one).
+template <int D, bool OQ, bool LT = false>
 __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArgs p) {
   // token tiles per wave: 384 tokens take two of the 12 waves' tiles
   constexpr int S = D / 32, G = D / 16, TW = OQ ? 2 : kQpTilesPerWave, NWV = kQpThreads / 64, FW = 3 * S * 64;
@@ -910,27 +915,50 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
     st.store(bfa + hg * FW, tid);
   }
   for (int u = tid; u < 3 * D; u += kQpThreads) bl[u] = p.bias[u];
+  static_assert(!LT || OQ, "lists in LDS with the quantised output");
+  // LT: [L] metadata of both masks, then both lists, after the biases
+  int2 *ml1 = (int2 *)(bl + 3 * D), *ml2 = ml1 + L;
+  uint2 *tl1 = (uint2 *)(ml2 + L), *tl2 = tl1 + p.tab1_n;
+  if constexpr (LT) {
+    for (int u = tid; u < L; u += kQpThreads) {
+      ml1[u] = p.meta1[u];
+      ml2[u] = p.meta2[u];
+    }
+    for (int u = tid; u < p.tab1_n; u += kQpThreads) tl1[u] = p.tab1[u];
+    for (int u = tid; u < p.tab2_n; u += kQpThreads) tl2[u] = p.tab2[u];
+  }
   // this pair's first row (token tid / 2): list metadata of both masks held for the kernel, in
   // registers, or with the quantised output (whose row outputs take 64 registers) in LDS
   const int r0 = tid >> 1, i0 = r0 < L ? r0 : 0;
-  int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
-  uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
+  int2 mt1 = make_int2(0, 0), mt2 = make_int2(0, 0);
+  uint2 g01 = make_uint2(0, 0), g02 = make_uint2(0, 0);
   uint4 *mdl = (uint4 *)(bl + 3 * D) + 2 * tid;
-  if constexpr (OQ) {
-    mdl[0] = make_uint4((uint32_t)mt1.x, (uint32_t)mt1.y, (uint32_t)mt2.x, (uint32_t)mt2.y);
-    mdl[1] = make_uint4(g01.x, g01.y, g02.x, g02.y);
+  if constexpr (!LT) {
+    mt1 = p.meta1[i0];
+    mt2 = p.meta2[i0];
+    g01 = p.tab1[mt1.x];
+    g02 = p.tab2[mt2.x];
+    if constexpr (OQ) {
+      mdl[0] = make_uint4((uint32_t)mt1.x, (uint32_t)mt1.y, (uint32_t)mt2.x, (uint32_t)mt2.y);
+      mdl[1] = make_uint4(g01.x, g01.y, g02.x, g02.y);
+    }
   }
   __syncthreads();
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
-  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
-    // the word's token tiles, waited for here: no global load is then outstanding inside the
-    // group loop, where a wait would also wait for the row outputs being written
+  auto load_tiles = [&](int64_t w) {
     int wv = wave;
     __asm__ volatile("" : "+v"(wv));
 #pragma unroll
     for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wv + NWV * k, L, lane, afr[k], alw[k]);
+  };
+  if constexpr (LT) load_tiles(blockIdx.x);
+  for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
+    // the word's token tiles, waited for here: no global load is then outstanding inside the
+    // group loop, where a wait would also wait for the row outputs being written (LT: read
+    // during the previous word's last rows)
+    if constexpr (!LT) load_tiles(w);
 #pragma unroll
     for (int k = 0; k < TW; ++k) {
 #pragma unroll
@@ -949,7 +977,12 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
       }
       block_sync_lds();
       const bool first = hg < p.hf;
-      if constexpr (OQ) {
+      if constexpr (LT) {
+        // the projection of the word's last group has read its tiles: the next word's now
+        if (hg == G - 1 && w + gridDim.x < p.words) load_tiles(w + gridDim.x);
+        mt1 = ml1[i0];
+        mt2 = ml2[i0];
+      } else if constexpr (OQ) {
         uint32_t *mdp = (uint32_t *)mdl;
         __asm__ volatile("" : "+v"(mdp));   // read here, not kept from the kernel's start
         const uint4 m0 = *(const uint4 *)mdp, m1 = *(const uint4 *)(mdp + 4);
@@ -961,8 +994,13 @@ __global__ __launch_bounds__(kQpThreads, 1) void k_qkv_attention_pair(QkvAttnArg
       if (r0 < L) {
         float q[8];
         qa_load<8>(q, qs + r0 * 16 + 8 * half);
-        qp_row_q(q, kv + 8 * half, (first ? p.tab1 : p.tab2) + (first ? mt1.x : mt2.x), first ? g01 : g02,
-                 first ? mt1.y : mt2.y, out);
+        if constexpr (LT) {
+          const uint2 *eg = first ? tl1 + mt1.x : tl2 + mt2.x;
+          qp_row_q(q, kv + 8 * half, eg, eg[0], first ? mt1.y : mt2.y, out);
+        } else {
+          qp_row_q(q, kv + 8 * half, (first ? p.tab1 : p.tab2) + (first ? mt1.x : mt2.x), first ? g01 : g02,
+                   first ? mt1.y : mt2.y, out);
+        }
       }
       if constexpr (!OQ) {
         float *ow = p.o + w * L * D + hg * 16 + 8 * half;
@@ -2327,6 +2365,11 @@ bool qkv_attention_pair_supported(const Model &M) {
 
 // The lane-pair form writes the Eq. 2 codes of O itself when a word has at most one row per lane
 // pair.
+// The quantised-output form with the lists and their metadata in LDS.
+size_t qkv_attention_pair_lists_lds(const Model &M) {
+  return qkv_attention_lds(M, true) + (size_t)16 * M.L + (size_t)8 * (M.g1_groups + M.g2_groups);
+}
+
 bool qkv_attention_pair_quantises(const Model &M) {
   return qkv_attention_pair_supported(M) && M.L <= kQpThreads / 2 && qkv_attention_pair_lds(M, true) <= M.lds_max;
 }
@@ -2335,7 +2378,8 @@ template <int D>
 static hipError_t run_qkv_attention_pair(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
   const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
   const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
-  if (a.oq) hipLaunchKernelGGL((k_qkv_attention_pair<D, true>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
+  if (a.oq && a.tab1_n > 0) hipLaunchKernelGGL((k_qkv_attention_pair<D, true, true>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
+  else if (a.oq) hipLaunchKernelGGL((k_qkv_attention_pair<D, true>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
   else hipLaunchKernelGGL((k_qkv_attention_pair<D, false>), dim3((unsigned)blocks), dim3(kQpThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -2366,6 +2410,11 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   if (oq && qkv_attention_pair_quantises(M)) {   // O straight to its codes, no fp32 rows
     a.oq = oq;
     a.ao = ao;
+    if (qkv_attention_pair_lists_lds(M) <= M.lds_max) {   // and the lists in LDS
+      a.tab1_n = M.g1_groups;
+      a.tab2_n = M.g2_groups;
+      return run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lists_lds(M), s);
+    }
     return run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M, true), s);
   }
   if (qkv_attention_pair_supported(M)) e = run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M), s);
@@ -2618,6 +2667,7 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
       (const void *)k_qkv_attention<64, 8>,      (const void *)k_qkv_attention<128, 16>,
       (const void *)k_qkv_attention<128, 8>,     (const void *)k_qkv_attention<64, 16>,
       (const void *)k_qkv_attention_pair<128, false>, (const void *)k_qkv_attention_pair<128, true>,
+      (const void *)k_qkv_attention_pair<128, true, true>,
       (const void *)k_qkv_attention_i16<128, 16>,
       (const void *)k_qkv_attention_i16<64, 16>, (const void *)k_qkv_attention_i16<64, 8>,
       (const void *)k_qkv_attention_i16<128, 8>, (const void *)k_qkv_attention_v16<64>,
