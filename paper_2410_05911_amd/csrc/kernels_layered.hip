@@ -707,7 +707,10 @@ __device__ __forceinline__ void qa_load_tile(const int8_t *xw, const float *aw, 
   }
 }
 
-template <int D, int DH>
+// LT (every group's weights resident, the word's tiles kept in registers): the neighbour lists and
+// their metadata staged in LDS once per block, so the rows issue no global loads, and the next
+// word's token tiles read right after the last group's projection, while its rows run.
+template <int D, int DH, bool LT = false>
 __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qkv_attention(QkvAttnArgs p) {
   constexpr int NWV = kQaThreads / 64;
   // at most kQaThreads rows of L tokens x 16 / d_h heads: a wave holds up to TW of the L / 16 tiles
@@ -730,27 +733,46 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
     st.store(bfa + hg * FW, tid);
   }
   for (int u = tid; u < 3 * D; u += kQaThreads) bl[u] = p.bias[u];
+  static_assert(!LT || qa_keep_tiles<D, DH>(), "lists in LDS with the tiles kept in registers");
+  // LT: [L] metadata of both masks, then both lists, after the biases
+  int2 *ml1 = (int2 *)(bl + 3 * D), *ml2 = ml1 + L;
+  uint2 *tl1 = (uint2 *)(ml2 + L), *tl2 = tl1 + p.tab1_n;
+  if constexpr (LT) {
+    for (int u = tid; u < L; u += kQaThreads) {
+      ml1[u] = p.meta1[u];
+      ml2[u] = p.meta2[u];
+    }
+    for (int u = tid; u < p.tab1_n; u += kQaThreads) tl1[u] = p.tab1[u];
+    for (int u = tid; u < p.tab2_n; u += kQaThreads) tl2[u] = p.tab2[u];
+    __syncthreads();
+  }
+  const uint2 *tab1 = LT ? tl1 : p.tab1, *tab2 = LT ? tl2 : p.tab2;
   // the thread's row (token i0, head hh0 of the group; L d / (16 d_h) <= kQaThreads rows): its
   // list metadata and first entry group for both masks stay in registers for the whole kernel
   const bool row0 = tid < L * HPG;
   const int hh0 = row0 ? tid / L : 0, i0 = row0 ? tid - hh0 * L : 0;
-  const int2 mt1 = p.meta1[i0], mt2 = p.meta2[i0];
-  const uint2 g01 = p.tab1[mt1.x], g02 = p.tab2[mt2.x];
+  const int2 mt1 = LT ? ml1[i0] : p.meta1[i0], mt2 = LT ? ml2[i0] : p.meta2[i0];
+  const uint2 g01 = tab1[mt1.x], g02 = tab2[mt2.x];
   __syncthreads();
   const float sq[3] = {p.sq[0], p.sq[1], p.sq[2]};
   long afr[TW][S];
   float alw[TW][4];
+  auto load_tiles = [&](int64_t w) {
+    int wv = wave;
+    __asm__ volatile("" : "+v"(wv));   // per-tile addresses are not hoisted out of the loops
+#pragma unroll
+    for (int k = 0; k < TW; ++k) qa_load_tile<D>(p.xq + w * L * D, p.ax + w * L, wv + NWV * k, L, lane, afr[k], alw[k]);
+  };
+  if constexpr (LT) load_tiles(blockIdx.x);
   for (int64_t w = blockIdx.x; w < p.words; w += gridDim.x) {
     const int8_t *xw = p.xq + w * L * D;
     const float *aw = p.ax + w * L;
     if constexpr (qa_keep_tiles<D, DH>()) {
       // the wave's token tiles of the word, used by all its head groups and waited for here: no
       // global load is then outstanding inside the group loop, where a wait would also wait for
-      // the row outputs being written (vmcnt counts stores too)
-      int wv = wave;
-      __asm__ volatile("" : "+v"(wv));   // per-tile addresses are not hoisted out of the loops
-#pragma unroll
-      for (int k = 0; k < TW; ++k) qa_load_tile<D>(xw, aw, wv + NWV * k, L, lane, afr[k], alw[k]);
+      // the row outputs being written (vmcnt counts stores too; LT: read during the previous
+      // word's last rows)
+      if constexpr (!LT) load_tiles(w);
 #pragma unroll
       for (int k = 0; k < TW; ++k) {
 #pragma unroll
@@ -776,16 +798,19 @@ __global__ __launch_bounds__(kQaThreads, (qa_waves_per_simd<D, DH>())) void k_qk
         }
       }
       block_sync_lds();
+      // LT: the projection of the word's last group has read its tiles: the next word's now
+      if constexpr (LT)
+        if (hg == G - 1 && w + gridDim.x < p.words) load_tiles(w + gridDim.x);
       // not resident: the fragments were last read before the barrier above, so the next group's
       // weights are loaded now and written after the rows
-      const bool more = !resident && (hg + 1 < G || w + gridDim.x < p.words);
+      const bool more = !LT && !resident && (hg + 1 < G || w + gridDim.x < p.words);
       QaStage<D> st;
       if (more) st.load(p.bpack, hg + 1 < G ? hg + 1 : 0, tid);
       if (row0) {
         const int h = hg * HPG + hh0;
         const bool first = h < p.hf;
         const int2 mt = first ? mt1 : mt2;
-        qa_row<DH, D == 128>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? p.tab1 : p.tab2) + mt.x, first ? g01 : g02,
+        qa_row<DH, D == 128>(qs + i0 * 16 + hh0 * DH, kv + hh0 * DH, (first ? tab1 : tab2) + mt.x, first ? g01 : g02,
                    mt.y, p.o + (w * L + i0) * D + h * DH);
       }
       if (more) st.store(bfa, tid);
@@ -2345,10 +2370,37 @@ bool qkv_attention_supported(const Model &M) {
          qkv_attention_lds(M) <= M.lds_max;
 }
 
+// Blocks of k_qkv_attention resident on a CU: as many as LDS holds, at most as many as its
+// register budget (qa_waves_per_simd waves per SIMD, blocks of kQaThreads / 64 waves on 4 SIMDs)
+// leaves room for; a grid of more would run its last blocks in a half-empty round.
+static int64_t qkv_attention_blocks_per_cu(const Model &M, size_t lds) {
+  const int64_t by_lds = std::max<int64_t>(1, (int64_t)(M.lds_max / std::max<size_t>(lds, 1)));
+  const int64_t by_waves = std::max<int64_t>(1, (M.d == 128 ? 2 : 4) * 4 / (kQaThreads / 64));
+  return std::min(by_lds, by_waves);
+}
+
+// The lists and their metadata in LDS beside the form's own use (LT).
+static size_t qkv_attention_lists_lds(const Model &M) {
+  return qkv_attention_lds(M, true) + (size_t)16 * M.L + (size_t)8 * (M.g1_groups + M.g2_groups);
+}
+
 template <int D, int DH>
 static hipError_t run_qkv_attention(const Model &M, const QkvAttnArgs &a, size_t lds, hipStream_t s) {
-  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(M.lds_max / lds));
-  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * per_cu);
+  // LT where every group's weights stay resident, the tiles stay in registers and the lists fit
+  // without fewer resident blocks
+  if constexpr (qa_keep_tiles<D, DH>()) {
+    const size_t ll = qkv_attention_lists_lds(M);
+    if (a.resident && ll <= M.lds_max &&
+        qkv_attention_blocks_per_cu(M, ll) >= qkv_attention_blocks_per_cu(M, lds)) {
+      QkvAttnArgs b = a;
+      b.tab1_n = M.g1_groups;
+      b.tab2_n = M.g2_groups;
+      const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * qkv_attention_blocks_per_cu(M, ll));
+      hipLaunchKernelGGL((k_qkv_attention<D, DH, true>), dim3((unsigned)blocks), dim3(kQaThreads), ll, s, b);
+      return hipGetLastError();
+    }
+  }
+  const int64_t blocks = std::min<int64_t>(a.words, (int64_t)M.cu_count * qkv_attention_blocks_per_cu(M, lds));
   hipLaunchKernelGGL((k_qkv_attention<D, DH>), dim3((unsigned)blocks), dim3(kQaThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -2365,10 +2417,6 @@ bool qkv_attention_pair_supported(const Model &M) {
 
 // The lane-pair form writes the Eq. 2 codes of O itself when a word has at most one row per lane
 // pair.
-// The quantised-output form with the lists and their metadata in LDS.
-size_t qkv_attention_pair_lists_lds(const Model &M) {
-  return qkv_attention_lds(M, true) + (size_t)16 * M.L + (size_t)8 * (M.g1_groups + M.g2_groups);
-}
 
 bool qkv_attention_pair_quantises(const Model &M) {
   return qkv_attention_pair_supported(M) && M.L <= kQpThreads / 2 && qkv_attention_pair_lds(M, true) <= M.lds_max;
@@ -2410,10 +2458,10 @@ hipError_t launch_qkv_attention(const Model &M, int layer, const int8_t *xq, con
   if (oq && qkv_attention_pair_quantises(M)) {   // O straight to its codes, no fp32 rows
     a.oq = oq;
     a.ao = ao;
-    if (qkv_attention_pair_lists_lds(M) <= M.lds_max) {   // and the lists in LDS
+    if (qkv_attention_lists_lds(M) <= M.lds_max) {   // and the lists in LDS
       a.tab1_n = M.g1_groups;
       a.tab2_n = M.g2_groups;
-      return run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lists_lds(M), s);
+      return run_qkv_attention_pair<128>(M, a, qkv_attention_lists_lds(M), s);
     }
     return run_qkv_attention_pair<128>(M, a, qkv_attention_pair_lds(M, true), s);
   }
@@ -2535,7 +2583,9 @@ int64_t attention_word_slots(const Model &M, int form) {
   size_t lds = 0;
   switch (form) {
     case 1:   // fp32 keys and values of the whole word
-      lds = qkv_attention_pair_supported(M) ? qkv_attention_pair_lds(M) : qkv_attention_lds(M, qkv_attention_resident(M));
+      if (!qkv_attention_pair_supported(M))
+        return (int64_t)M.cu_count * qkv_attention_blocks_per_cu(M, qkv_attention_lds(M, qkv_attention_resident(M)));
+      lds = qkv_attention_pair_lds(M);
       break;
     case 2:   // int16 accumulators
       lds = qkv_attention_v16_supported(M) ? (M.d == 64 ? qkv_attention_v16_lds_bytes<64>(M.L) : qkv_attention_v16_lds_bytes<128>(M.L))
@@ -2666,6 +2716,8 @@ hipError_t set_layered_kernel_attributes(const Model &M) {
   const void *fns[] = {
       (const void *)k_qkv_attention<64, 8>,      (const void *)k_qkv_attention<128, 16>,
       (const void *)k_qkv_attention<128, 8>,     (const void *)k_qkv_attention<64, 16>,
+      (const void *)k_qkv_attention<64, 8, true>, (const void *)k_qkv_attention<128, 16, true>,
+      (const void *)k_qkv_attention<128, 8, true>,
       (const void *)k_qkv_attention_pair<128, false>, (const void *)k_qkv_attention_pair<128, true>,
       (const void *)k_qkv_attention_pair<128, true, true>,
       (const void *)k_qkv_attention_i16<128, 16>,
