@@ -2358,18 +2358,6 @@ size_t qkv_attention_lds(const Model &M, bool resident = false) {
          (size_t)3 * M.d * 4;
 }
 
-// Keep every head group's weight tiles in LDS when that does not lower the blocks per CU.
-bool qkv_attention_resident(const Model &M) {
-  const size_t one = qkv_attention_lds(M, false), all = qkv_attention_lds(M, true);
-  return all <= M.lds_max && (M.lds_max / all) >= (M.lds_max / one);
-}
-
-bool qkv_attention_supported(const Model &M) {
-  return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped &&
-         M.L <= 16 * (kQaThreads / 64) * kQaTilesPerWave && M.L * (16 / M.dh) <= kQaThreads &&
-         qkv_attention_lds(M) <= M.lds_max;
-}
-
 // Blocks of k_qkv_attention resident on a CU: as many as LDS holds, at most as many as its
 // register budget (qa_waves_per_simd waves per SIMD, blocks of kQaThreads / 64 waves on 4 SIMDs)
 // leaves room for; a grid of more would run its last blocks in a half-empty round.
@@ -2378,6 +2366,19 @@ static int64_t qkv_attention_blocks_per_cu(const Model &M, size_t lds) {
   const int64_t by_waves = std::max<int64_t>(1, (M.d == 128 ? 2 : 4) * 4 / (kQaThreads / 64));
   return std::min(by_lds, by_waves);
 }
+
+// Keep every head group's weight tiles in LDS when that does not lower the blocks per CU.
+bool qkv_attention_resident(const Model &M) {
+  const size_t one = qkv_attention_lds(M, false), all = qkv_attention_lds(M, true);
+  return all <= M.lds_max && qkv_attention_blocks_per_cu(M, all) >= qkv_attention_blocks_per_cu(M, one);
+}
+
+bool qkv_attention_supported(const Model &M) {
+  return (M.d == 64 || M.d == 128) && (M.dh == 8 || M.dh == 16) && M.grouped &&
+         M.L <= 16 * (kQaThreads / 64) * kQaTilesPerWave && M.L * (16 / M.dh) <= kQaThreads &&
+         qkv_attention_lds(M) <= M.lds_max;
+}
+
 
 // The lists and their metadata in LDS beside the form's own use (LT).
 static size_t qkv_attention_lists_lds(const Model &M) {

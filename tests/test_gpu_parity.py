@@ -385,6 +385,27 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
+@pytest.mark.parametrize("m,n,hf,words", [(25, 51, 8, 37), (40, 90, 5, 300), (60, 121, 11, 9)])
+def test_layered_d128_sixteen_heads(P, oracle_mod, m, n, hf, words):
+    """d = 128 with sixteen 8-dimension heads (two per head group): the fused projection +
+    attention with one row per thread, its neighbour lists staged in LDS and the next word's tiles
+    read during the last group's rows; several words per block (300 words) so the read-ahead
+    crosses word boundaries, and first-ring head counts that split a group between the rings."""
+    from workloads import random_weights
+    print(f"[d128 h16] m {m} n {n} hf {hf} words {words}", flush=True)
+    H = _random_parity_check(m, n, seed=3 * m + n)
+    w = random_weights(n, m, 128, 2, 16, seed=m + 7 * n, first_ring_heads=hf)
+    rng = np.random.default_rng(11)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (words, n)) + 0.6 * rng.standard_normal((words, n))).astype(np.float32)
+    k = min(words, 40)
+    idx = np.unique(np.linspace(0, words - 1, k).astype(np.int64))
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y[idx], n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.path == P.PATH_LAYERED and dec.info.layered_attention == P.LAYERED_ATTN_LDS_F32
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits)[idx], fo, _np(bits)[idx], bo, y[idx])
+
+
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("regime", ["mixed", "underflow", "zero_values"])
 def test_long_words_shifted_softmax(P, oracle_mod, regime, d):
