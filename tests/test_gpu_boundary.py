@@ -2,7 +2,7 @@
 
 - One alpha per word (aecct_act_scale WORD, the paper-literal reading of Eq. 2): GPU decodes
   against the oracle in the same mode, bit for bit, and the forms that cannot take it refuse.
-- The spec rule against the oracle's plain fp64 reference decode (dense masked softmax,
+- The logit tolerance rule against the oracle's plain fp64 reference decode (dense masked softmax,
   libm exp, exact division and square root): |f_gpu - f_64| <= 1e-3 and identical bits where
   |f_64| > 1e-3.  The fp64 decode takes the canonical oracle's int8 decision only where its own
   activation lies within 1e-3 of a rounding tie of Eq. 2 (both decisions are right there; a flip
@@ -87,7 +87,7 @@ _FP64_SAMPLE = {1: 256, 2: 64, 3: 8, 4: 4, 5: 2}
                                          (1, "word"), (2, "word"), (3, "word")])
 def test_decode_against_fp64_reference(P, oracle_mod, c, act_scale):
     """The GPU decode of the configured batch, on a spread sample of words, against the plain
-    fp64 definition under the spec rule (near-tie codes decided as described above)."""
+    fp64 definition under the logit tolerance rule (near-tie codes decided as described above)."""
     cfg = CONFIGS[c]
     print(f"[fp64] config {c} alpha per {act_scale}", flush=True)
     cfg, H, G, w, y, x = build_workload(c, act_scale=act_scale)

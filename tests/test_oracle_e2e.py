@@ -93,7 +93,7 @@ def test_fp32_canonical_close_to_fp64_reference(oracle_mod, c, words, attention)
                                                (2, 48, "word"), (3, 4, "token"), (3, 4, "word"),
                                                (4, 1, "token"), (5, 1, "token")])
 def test_canonical_equals_fp64_up_to_near_tie_codes(oracle_mod, c, words, act_scale):
-    """Survey pin P10 on every workload.  The fp64 reference decode, taking the canonical code
+    """The canonical decode pinned to the fp64 reference on every workload.  The fp64 reference decode, taking the canonical code
     only where its own value lies within 1e-3 of a rounding tie, reproduces the canonical logits
     within 1e-5: no canonical code differs from the fp64 decision away from a tie, so every
     departure of the canonical fp32 order from the plain definition (folded score scale, base-2
