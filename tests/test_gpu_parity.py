@@ -385,6 +385,25 @@ def test_layered_wide_models_odd_token_counts(P, oracle_mod, d, m, n, hf, attent
         _assert_logits(_np(logits), fo, _np(bits), bo, y)
 
 
+@pytest.mark.parametrize("d,with_pos", [(64, False), (64, True), (128, False), (128, True)])
+def test_layered_single_layer(P, oracle_mod, d, with_pos):
+    """One layer: its token block is both the first (X rebuilt from t_i and the embedding rows, with
+    or without a positional table) and the last (the head's z per token instead of X)."""
+    from workloads import random_weights
+    print(f"[one layer] d {d} pos {with_pos}", flush=True)
+    m, n = 30, 61
+    H = _random_parity_check(m, n, seed=5 * d + int(with_pos))
+    w = random_weights(n, m, d, 1, 8, seed=d + 3, with_pos=with_pos)
+    rng = np.random.default_rng(13)
+    y = (1.0 - 2.0 * rng.integers(0, 2, (300, n)) + 0.6 * rng.standard_normal((300, n))).astype(np.float32)
+    idx = np.unique(np.linspace(0, 299, 40).astype(np.int64))
+    bo, fo = oracle_mod.OracleModel(H, w).decode(y[idx], n_threads=16)
+    dec = P.Decoder(H, w)
+    assert dec.path == P.PATH_LAYERED
+    bits, logits = dec.decode(_dev(y))
+    _assert_logits(_np(logits)[idx], fo, _np(bits)[idx], bo, y[idx])
+
+
 @pytest.mark.parametrize("m,n,hf,words", [(25, 51, 8, 37), (40, 90, 5, 300), (60, 121, 11, 9)])
 def test_layered_d128_sixteen_heads(P, oracle_mod, m, n, hf, words):
     """d = 128 with sixteen 8-dimension heads (two per head group): the fused projection +
