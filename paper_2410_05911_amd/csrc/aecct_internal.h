@@ -198,8 +198,10 @@ hipError_t train_quant(const float *x, int64_t rows, int K, bool relu, float *xh
 // Products with a ternary right operand on the bf16 matrix cores (fp32 A split exactly into three
 // bf16 parts): train_pack_tern lays each job's T [R][C] (or its transpose) out as B fragments in
 // out (2 R C bytes), train_gemm_tern forms C = beta C + scale (A B) + bias; N a multiple of 64, K
-// of 32.
+// of 32, A, C and the bias 16-byte aligned with lda and ldc multiples of 4 (train_tern_operands_ok).
 bool train_tern_shape_ok(int64_t N, int64_t K);
+bool train_tern_operands_ok(const float *A, int64_t lda, const float *C, int64_t ldc, const float *bias, int64_t N,
+                            int64_t K);
 struct TernPackJob {
   const float *T;
   int R, C, trans;

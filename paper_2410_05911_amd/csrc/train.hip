@@ -434,7 +434,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
 // lo the remaining at most 8), each part times a ternary entry is exact, and the three
 // v_mfma_f32_16x16x32_bf16 products accumulate in fp32: the result is an fp32-accumulated sum of
 // exact products, as in the fp32 kernels, at the bf16 matrix rate.  B comes pre-packed as bf16 MFMA
-// B fragments (k_pack_tern).  A wave computes 16 RT rows x 16 NJ columns, a block four waves.
+// B fragments (k_pack_tern).  A wave computes 16 rows x 16 NJ columns, a block four waves.
 // ------------------------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -481,81 +481,92 @@ __device__ __forceinline__ bf16x8 bf16_hi8(const float (&v)[8]) {
   return __builtin_bit_cast(bf16x8, w);
 }
 
-template <int NJ, int RT>
+// the three bf16 parts of eight fp32 values as MFMA operands
+__device__ __forceinline__ void split_bf16x3(const float4 &x0, const float4 &x1, bf16x8 &ph, bf16x8 &pm, bf16x8 &pl) {
+  const float a[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  float hi[8], mid[8], lo[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    hi[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[e]) & 0xFFFF0000u);
+    const float rm = a[e] - hi[e];
+    mid[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, rm) & 0xFFFF0000u);
+    lo[e] = rm - mid[e];
+  }
+  ph = bf16_hi8(hi);
+  pm = bf16_hi8(mid);
+  pl = bf16_hi8(lo);
+}
+
+// The MFMA takes the ternary fragment as its first operand and A's as its second, so it forms the
+// transposed tile: lane (col, grp) ends with row 16 t + col, columns 16 j + 4 grp .. + 3 of C, one
+// 16-byte store (and, with beta, one 16-byte load) per tile.  Both operands of k-step kt + S - 1 are
+// loaded before step kt is computed, from a ring of S register slots: the vector-memory counter
+// retires loads in issue order, so a B fragment loaded just before its use would also wait for
+// every A prefetch issued ahead of it.  C goes out with ordinary stores: the next kernel reads it,
+// partly from the caches (nontemporal stores measured slower over a training step).
+template <int NJ, int S>
 __global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, col = l & 15, grp = l >> 4;
-  // the wave's RT row tiles of 16 share every B fragment it reads
-  const int64_t m0 = (int64_t)blockIdx.y * (64 * RT) + 16 * RT * wave, n0 = (int64_t)blockIdx.x * (16 * NJ);
-  const int64_t KT = g.K / 32;
-  const float *arow[RT];
-#pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int64_t r = m0 + 16 * t + col;
-    arow[t] = g.A + (r < g.M ? r : g.M - 1) * g.lda + 8 * grp;   // rows past M: a copy, never stored
-  }
+  const int64_t m0 = (int64_t)blockIdx.y * 64 + 16 * wave, n0 = (int64_t)blockIdx.x * (16 * NJ);
+  const int KT = (int)(g.K / 32);
+  const int64_t r = m0 + col;
+  const float *arow = g.A + (r < g.M ? r : g.M - 1) * g.lda + 8 * grp;   // rows past M: a copy, never stored
   const uint4 *bcol = g.B + (n0 / 16) * KT * 64 + l;
-  f32x4 acc[RT][NJ];
+  f32x4 acc[NJ];
 #pragma unroll
-  for (int t = 0; t < RT; ++t)
+  for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  float4 a[S][2];
+  uint4 b[S][NJ];
+  auto issue = [&](int kt, float4 (&as)[2], uint4 (&bs)[NJ]) {
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[t][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  float4 a0[RT], a1[RT];
+    for (int j = 0; j < NJ; ++j) bs[j] = bcol[(j * KT + kt) * 64];
+    as[0] = *(const float4 *)(arow + 32 * kt);
+    as[1] = *(const float4 *)(arow + 32 * kt + 4);
+  };
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    a0[t] = *(const float4 *)arow[t];
-    a1[t] = *(const float4 *)(arow[t] + 4);
-  }
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    bf16x8 ph[RT], pm[RT], pl[RT];
+  for (int s = 0; s < S - 1; ++s)
+    if (s < KT) issue(s, a[s], b[s]);
+  for (int k0 = 0; k0 < KT; k0 += S) {
 #pragma unroll
-    for (int t = 0; t < RT; ++t) {
-      const float a[8] = {a0[t].x, a0[t].y, a0[t].z, a0[t].w, a1[t].x, a1[t].y, a1[t].z, a1[t].w};
-      float hi[8], mid[8], lo[8];
+    for (int s = 0; s < S; ++s) {   // step k0 + s sits in slot s
+      const int kt = k0 + s;
+      if (kt >= KT) break;
+      if (kt + S - 1 < KT) issue(kt + S - 1, a[(s + S - 1) % S], b[(s + S - 1) % S]);
+      bf16x8 ph, pm, pl;
+      split_bf16x3(a[s][0], a[s][1], ph, pm, pl);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        hi[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[e]) & 0xFFFF0000u);
-        const float rm = a[e] - hi[e];
-        mid[e] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, rm) & 0xFFFF0000u);
-        lo[e] = rm - mid[e];
-      }
-      ph[t] = bf16_hi8(hi);
-      pm[t] = bf16_hi8(mid);
-      pl[t] = bf16_hi8(lo);
-    }
-    if (kt + 1 < KT) {   // the next k-step's A
-#pragma unroll
-      for (int t = 0; t < RT; ++t) {
-        a0[t] = *(const float4 *)(arow[t] + 32 * (kt + 1));
-        a1[t] = *(const float4 *)(arow[t] + 32 * (kt + 1) + 4);
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const bf16x8 b = __builtin_bit_cast(bf16x8, bcol[(j * KT + kt) * 64]);
-#pragma unroll
-      for (int t = 0; t < RT; ++t) {
-        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[t], b, acc[t][j], 0, 0, 0);
-        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pm[t], b, acc[t][j], 0, 0, 0);
-        acc[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[t], b, acc[t][j], 0, 0, 0);
+      for (int j = 0; j < NJ; ++j) {
+        const bf16x8 bb = __builtin_bit_cast(bf16x8, b[s][j]);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, pl, acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, pm, acc[j], 0, 0, 0);
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, ph, acc[j], 0, 0, 0);
       }
     }
   }
+  if (r >= g.M) return;
   const float sc = g.scale ? *g.scale : 1.0f;
+  float4 o[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int64_t c = n0 + 16 * j + col;
-    if (c >= g.N) continue;
-    const float bj = g.bias ? g.bias[c] : 0.0f;
+    const int64_t c = n0 + 16 * j + 4 * grp;
+    const float4 bj = g.bias ? *(const float4 *)(g.bias + c) : float4{0.0f, 0.0f, 0.0f, 0.0f};
+    o[j].x = sc * acc[j][0] + bj.x;
+    o[j].y = sc * acc[j][1] + bj.y;
+    o[j].z = sc * acc[j][2] + bj.z;
+    o[j].w = sc * acc[j][3] + bj.w;
+  }
+  float *crow = g.C + r * g.ldc + n0 + 4 * grp;
 #pragma unroll
-    for (int t = 0; t < RT; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t rr = m0 + 16 * t + 4 * grp + i;
-        if (rr >= g.M) continue;
-        float o = sc * acc[t][j][i] + bj;
-        if (g.beta) o += g.C[rr * g.ldc + c];
-        g.C[rr * g.ldc + c] = o;
-      }
+  for (int j = 0; j < NJ; ++j) {
+    float4 u = o[j];
+    if (g.beta) {
+      const float4 cv = *(const float4 *)(crow + 16 * j);
+      u.x += cv.x;
+      u.y += cv.y;
+      u.z += cv.z;
+      u.w += cv.w;
+    }
+    *(float4 *)(crow + 16 * j) = u;
   }
 }
 
@@ -1007,6 +1018,13 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
 
 bool train_tern_shape_ok(int64_t N, int64_t K) { return K % 32 == 0 && N % 64 == 0; }
 
+bool train_tern_operands_ok(const float *A, int64_t lda, const float *C, int64_t ldc, const float *bias, int64_t N,
+                            int64_t K) {
+  // 16-byte rows of A and C, 16-byte groups of the bias
+  const auto al16 = [](const float *q) { return ((uintptr_t)q & 15u) == 0; };
+  return train_tern_shape_ok(N, K) && lda % 4 == 0 && ldc % 4 == 0 && al16(A) && al16(C) && (!bias || al16(bias));
+}
+
 hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s) {
   if (jobs.n <= 0) return hipSuccess;
   int64_t lanes = 0;
@@ -1023,12 +1041,12 @@ hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s) {
 hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
                            int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (!train_tern_shape_ok(N, K) || lda % 4 != 0 || ((uintptr_t)A & 15u) != 0) return hipErrorInvalidValue;
+  if (!train_tern_operands_ok(A, lda, C, ldc, bias, N, K)) return hipErrorInvalidValue;
   train::GemmTern g{A, (const uint4 *)frag, C, M, N, K, lda, ldc, scale, bias, accumulate ? 1 : 0};
-  constexpr int RT = 2;   // two row tiles per wave: 37.8 us against 39.4 us for one (LDPC(256,128) step)
-  const unsigned gy = (unsigned)((M + 64 * RT - 1) / (64 * RT));
-  if (N % 128 == 0) hipLaunchKernelGGL((train::k_gemm_tern<8, RT>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
-  else hipLaunchKernelGGL((train::k_gemm_tern<4, RT>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
+  constexpr int S = 3;   // operands two k-steps ahead
+  const unsigned gy = (unsigned)((M + 63) / 64);
+  if (N % 128 == 0) hipLaunchKernelGGL((train::k_gemm_tern<8, S>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
+  else hipLaunchKernelGGL((train::k_gemm_tern<4, S>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
   return hipGetLastError();
 }
 

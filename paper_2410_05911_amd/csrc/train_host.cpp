@@ -262,7 +262,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
   // C = scale (A op(T)) + bias (+ C) for ternary matrix k of layer l, op(T) = T or (trans) T^T
   auto tgemm = [&](bool trans, int l, int k, const float *A, int64_t lda, float *C, int64_t ldc, int64_t M, int64_t Nn,
                    int64_t K, const float *scale, const float *bias, bool acc) {
-    if (tern && lda % 4 == 0 && ((uintptr_t)A & 15u) == 0)
+    if (tern && train_tern_operands_ok(A, lda, C, ldc, bias, Nn, K))
       return train_gemm_tern(A, lda, tfrag(l, k, trans), C, ldc, M, Nn, K, scale, bias, acc, s);
     return gemm(false, trans, A, lda, tmat(l, k), trans ? K : Nn, C, ldc, M, Nn, K, scale, bias, acc);
   };
