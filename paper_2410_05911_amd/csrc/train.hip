@@ -1104,11 +1104,10 @@ hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const floa
   }
   hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, (unsigned)chunks), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows,
                      C, cwl, chunk, part, 0);
-  // pass two over the partial rows with at least 16 lanes per column
-  const int cwl2 = std::min(cwl, 4);
-  hipLaunchKernelGGL(train::k_colsum, dim3(blocks_for(C, 1 << cwl2), 1), dim3(train::kThreads), 0, s, (const float *)part,
-                     (int64_t)C, (const float *)nullptr, (const float *)nullptr, chunks, C, cwl2, chunks, out,
-                     accumulate ? 1 : 0);
+  // pass two over the partial rows: a block per column, its 256 lanes over the partial rows (a few
+  // loads a lane, then the LDS tree), which takes a fraction of the 16-lanes-a-column form's time
+  hipLaunchKernelGGL(train::k_colsum, dim3((unsigned)C, 1), dim3(train::kThreads), 0, s, (const float *)part, (int64_t)C,
+                     (const float *)nullptr, (const float *)nullptr, chunks, C, 0, chunks, out, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 
