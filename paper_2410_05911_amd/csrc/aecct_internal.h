@@ -223,6 +223,14 @@ hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const 
 // out[c] (+)= sum_r A[r][c] (B[r][c] if B) (w[r] if w), rows of A lda apart, B dense [rows][C]
 hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
                         bool accumulate, float *part, int64_t part_floats, hipStream_t s);
+// out_ab[c] = sum_r A[r][c] B[r][c] and out_a[c] = sum_r A[r][c] in one pass (a LayerNorm's gain and
+// shift gradients)
+hipError_t train_colsum_dual(const float *A, int64_t lda, const float *Bm, int64_t rows, int C, float *out_ab,
+                             float *out_a, float *part, int64_t part_floats, hipStream_t s);
+// the column sums of A's nseg * seg columns, segment k to outs[k] (nseg <= 3: the query, key and value
+// bias gradients from one pass over the packed [rows][3 d] gradient)
+hipError_t train_colsum_split(const float *A, int64_t lda, int64_t rows, int seg, int nseg, float *const *outs,
+                              float *part, int64_t part_floats, hipStream_t s);
 hipError_t train_relu_bwd(float *dg, const float *f, int64_t count, hipStream_t s);
 hipError_t train_rowdot(const float *x, int64_t rows, int d, const float *w1, const float *b1, float *z, hipStream_t s);
 hipError_t train_outer(const float *dz, int64_t rows, const float *w1, int d, float *dx, hipStream_t s);

@@ -772,47 +772,67 @@ __global__ __launch_bounds__(kThreads) void k_ln_bwd(const float *dy, const floa
 }
 
 // ------------------------------------------------------------------------------------------
-// Column sums over rows, deterministic in two passes: out[c] (+)= sum_r A[r][c] (x B[r][c]) (x w[r]).
-// A block covers cw columns (a power of two up to 64) with 256 / cw row lanes; lane l of a block
-// sums the rows l, l + lanes, ... of its chunk (four interleaved partial sums), the lanes are
-// combined by a fixed tree in LDS.  Pass one writes a partial row per chunk, pass two sums the
-// partial rows with the same kernel.
+// Column sums over rows, deterministic in two passes: v(r, c) = A[r][c] (x B[r][c]) (x w[r]) summed
+// over r for each of A's C columns.  With dual (B given) each column also sums A alone, as column
+// C + c of the result.  Result column c goes to o[c / seg][c % seg] (several bias vectors from one
+// pass over a packed matrix, or the two sums of the dual form to two vectors).  A block covers cw
+// columns (a power of two up to 64) with 256 / cw row lanes; lane l of a block sums the rows l,
+// l + lanes, ... of its chunk (four interleaved partial sums; the factors present and the dual
+// form are template parameters, as a run-time test between one row's loads and the next row's
+// held each load until the previous one had landed), the lanes are combined by a fixed tree in LDS.  Pass one writes a
+// partial row per chunk, pass two sums the partial rows with the same kernel.
 // ------------------------------------------------------------------------------------------
+struct ColOut {
+  float *o[3];
+  int seg;
+  int64_t ld;   // distance between the rows of partial sums (pass one); 0 for the final sums
+};
+
+template <bool HB, bool HW, bool DUAL>
 __global__ __launch_bounds__(kThreads) void k_colsum(const float *A, int64_t lda, const float *Bm, const float *w,
-                                                     int64_t rows, int C, int cw_log2, int64_t chunk, float *out,
+                                                     int64_t rows, int C, int cw_log2, int64_t chunk, ColOut out,
                                                      int accumulate) {
-  __shared__ float red[kThreads];
+  constexpr int nv = DUAL ? 2 : 1;
+  __shared__ float red[nv][kThreads];
   const int cw = 1 << cw_log2, lanes = kThreads >> cw_log2;
   const int cl = threadIdx.x & (cw - 1), rl = threadIdx.x >> cw_log2;
   const int c = blockIdx.x * cw + cl;
   const int64_t r0 = (int64_t)blockIdx.y * chunk, r1 = std::min<int64_t>(rows, r0 + chunk);
-  auto val = [&](int64_t r) {
-    float v = A[r * lda + c];
-    if (Bm) v *= Bm[r * C + c];
-    if (w) v *= w[r];
-    return v;
+  float s[nv][4] = {};
+  auto add = [&](int k, int64_t r) {
+    const float a = A[r * lda + c];
+    float v = a;
+    if (HB) v *= Bm[r * C + c];
+    if (HW) v *= w[r];
+    s[0][k] += v;
+    if (DUAL) s[nv - 1][k] += a;
   };
-  float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
   if (c < C) {
     int64_t r = r0 + rl;
     for (; r + 3 * lanes < r1; r += 4 * lanes) {
-      s0 += val(r);
-      s1 += val(r + lanes);
-      s2 += val(r + 2 * lanes);
-      s3 += val(r + 3 * lanes);
+      add(0, r);
+      add(1, r + lanes);
+      add(2, r + 2 * lanes);
+      add(3, r + 3 * lanes);
     }
-    for (; r < r1; r += lanes) s0 += val(r);
+    for (; r < r1; r += lanes) add(0, r);
   }
-  red[threadIdx.x] = (s0 + s1) + (s2 + s3);
+#pragma unroll
+  for (int k = 0; k < nv; ++k) red[k][threadIdx.x] = (s[k][0] + s[k][1]) + (s[k][2] + s[k][3]);
   __syncthreads();
   for (int st = lanes >> 1; st > 0; st >>= 1) {
-    if (rl < st) red[threadIdx.x] += red[threadIdx.x + (st << cw_log2)];
+    if (rl < st)
+#pragma unroll
+      for (int k = 0; k < nv; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + (st << cw_log2)];
     __syncthreads();
   }
-  if (rl == 0 && c < C) {
-    float *o = out + (int64_t)blockIdx.y * C + c;
-    *o = accumulate ? *o + red[threadIdx.x] : red[threadIdx.x];
-  }
+  if (rl == 0 && c < C)
+#pragma unroll
+    for (int k = 0; k < nv; ++k) {
+      const int cc = c + k * C;
+      float *o = out.o[cc / out.seg] + (int64_t)blockIdx.y * out.ld + cc % out.seg;
+      *o = accumulate ? *o + red[k][threadIdx.x] : red[k][threadIdx.x];
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1085,30 +1105,60 @@ hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const 
   return hipGetLastError();
 }
 
-hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
-                        bool accumulate, float *part, int64_t part_floats, hipStream_t s) {
+namespace {
+// C columns of A summed into the Ct = C (or 2 C, dual) result columns of fin
+hipError_t colsum_run(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, bool dual,
+                      const train::ColOut &fin, bool accumulate, float *part, int64_t part_floats, hipStream_t s) {
   if (C <= 0) return hipSuccess;
+  const int Ct = dual ? 2 * C : C;
   int cwl = 0;
   while ((1 << cwl) < C && cwl < 6) ++cwl;
   const int lanes = train::kThreads >> cwl;
   const unsigned cblocks = blocks_for(C, 1 << cwl);
   // about 1024 blocks in all, each lane summing at least 8 rows
   int64_t chunks = std::min<int64_t>((rows + 8 * lanes - 1) / (8 * lanes), std::max<int64_t>(1, 1024 / cblocks));
-  chunks = std::max<int64_t>(1, std::min<int64_t>(chunks, part_floats / C));
+  chunks = std::max<int64_t>(1, std::min<int64_t>(chunks, part_floats / Ct));
   const int64_t chunk = std::max<int64_t>(1, (rows + chunks - 1) / chunks);
   chunks = std::max<int64_t>(1, (rows + chunk - 1) / chunk);
+  using K = decltype(&train::k_colsum<false, false, false>);
+  K pass1 = dual ? (w ? train::k_colsum<true, true, true> : train::k_colsum<true, false, true>)
+                 : Bm ? (w ? train::k_colsum<true, true, false> : train::k_colsum<true, false, false>)
+                      : (w ? train::k_colsum<false, true, false> : train::k_colsum<false, false, false>);
   if (chunks == 1) {
-    hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, 1), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows, C, cwl,
-                       chunk, out, accumulate ? 1 : 0);
+    hipLaunchKernelGGL(pass1, dim3(cblocks, 1), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows, C, cwl, chunk, fin,
+                       accumulate ? 1 : 0);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(train::k_colsum, dim3(cblocks, (unsigned)chunks), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows,
-                     C, cwl, chunk, part, 0);
+  const train::ColOut pt{{part, nullptr, nullptr}, Ct, (int64_t)Ct};
+  hipLaunchKernelGGL(pass1, dim3(cblocks, (unsigned)chunks), dim3(train::kThreads), 0, s, A, lda, Bm, w, rows, C, cwl,
+                     chunk, pt, 0);
   // pass two over the partial rows: a block per column, its 256 lanes over the partial rows (a few
   // loads a lane, then the LDS tree), which takes a fraction of the 16-lanes-a-column form's time
-  hipLaunchKernelGGL(train::k_colsum, dim3((unsigned)C, 1), dim3(train::kThreads), 0, s, (const float *)part, (int64_t)C,
-                     (const float *)nullptr, (const float *)nullptr, chunks, C, 0, chunks, out, accumulate ? 1 : 0);
+  hipLaunchKernelGGL((train::k_colsum<false, false, false>), dim3((unsigned)Ct, 1), dim3(train::kThreads), 0, s, (const float *)part,
+                     (int64_t)Ct, (const float *)nullptr, (const float *)nullptr, chunks, Ct, 0, chunks, fin,
+                     accumulate ? 1 : 0);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t train_colsum(const float *A, int64_t lda, const float *Bm, const float *w, int64_t rows, int C, float *out,
+                        bool accumulate, float *part, int64_t part_floats, hipStream_t s) {
+  return colsum_run(A, lda, Bm, w, rows, C, false, train::ColOut{{out, nullptr, nullptr}, std::max(C, 1), 0},
+                    accumulate, part, part_floats, s);
+}
+
+hipError_t train_colsum_dual(const float *A, int64_t lda, const float *Bm, int64_t rows, int C, float *out_ab,
+                             float *out_a, float *part, int64_t part_floats, hipStream_t s) {
+  if (!Bm) return hipErrorInvalidValue;
+  return colsum_run(A, lda, Bm, nullptr, rows, C, true, train::ColOut{{out_ab, out_a, nullptr}, std::max(C, 1), 0},
+                    false, part, part_floats, s);
+}
+
+hipError_t train_colsum_split(const float *A, int64_t lda, int64_t rows, int seg, int nseg, float *const *outs,
+                              float *part, int64_t part_floats, hipStream_t s) {
+  if (nseg < 1 || nseg > 3 || seg <= 0) return hipErrorInvalidValue;
+  train::ColOut fin{{outs[0], nseg > 1 ? outs[1] : nullptr, nseg > 2 ? outs[2] : nullptr}, seg, 0};
+  return colsum_run(A, lda, nullptr, nullptr, rows, seg * nseg, false, fin, false, part, part_floats, s);
 }
 
 hipError_t train_relu_bwd(float *dg, const float *f, int64_t count, hipStream_t s) {

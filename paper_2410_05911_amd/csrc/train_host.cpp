@@ -308,8 +308,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     const size_t ld_ = (size_t)l * d;
     // LN2, second feed-forward map, ReLU, first map
     AECCT_TRY(train_ln_bwd(dX, p->ln2_g + ld_, ws + q.xn2, ws + q.rho2, R, d, dR, s));
-    AECCT_TRY(colsum(dX, d, ws + q.xn2, nullptr, R, d, g->ln2_g + ld_));
-    AECCT_TRY(colsum(dX, d, nullptr, nullptr, R, d, g->ln2_b + ld_));
+    AECCT_TRY(train_colsum_dual(dX, d, ws + q.xn2, R, d, g->ln2_g + ld_, g->ln2_b + ld_, part, (int64_t)PF, s));
     AECCT_TRY(gemm(true, false, ws + q.gh, dff, dR, d, gw[5] + wofs(l, 5), d, dff, d, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dR, d, nullptr, nullptr, R, d, gb[5] + ld_));
     AECCT_TRY(tgemm(true, l, 5, dR, d, dG, dff, R, dff, d, sc + 6 * l + 5, nullptr, false));
@@ -320,8 +319,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     AECCT_TRY(tgemm(true, l, 4, dG, dff, dX1, d, R, d, dff, sc + 6 * l + 4, nullptr, true));
     // LN1, output map
     AECCT_TRY(train_ln_bwd(dX1, p->ln1_g + ld_, ws + q.xn1, ws + q.rho1, R, d, dR, s));
-    AECCT_TRY(colsum(dX1, d, ws + q.xn1, nullptr, R, d, g->ln1_g + ld_));
-    AECCT_TRY(colsum(dX1, d, nullptr, nullptr, R, d, g->ln1_b + ld_));
+    AECCT_TRY(train_colsum_dual(dX1, d, ws + q.xn1, R, d, g->ln1_g + ld_, g->ln1_b + ld_, part, (int64_t)PF, s));
     AECCT_TRY(hipMemcpyAsync(dX, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
     AECCT_TRY(gemm(true, false, ws + q.oh, d, dR, d, gw[3] + wofs(l, 3), d, d, d, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dR, d, nullptr, nullptr, R, d, gb[3] + ld_));
@@ -331,10 +329,11 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
                  dO, dQKV, ws + W.dv};
     AECCT_TRY(train_attention(1, T.dh, at, s));
     AECCT_TRY(train_attention(2, T.dh, at, s));
+    float *const gbq[3] = {gb[0] + ld_, gb[1] + ld_, gb[2] + ld_};
+    AECCT_TRY(train_colsum_split(dQKV, 3 * d, R, d, 3, gbq, part, (int64_t)PF, s));
     for (int k = 0; k < 3; ++k) {
       AECCT_TRY(gemm(true, false, ws + q.xh, d, dQKV + k * d, 3 * d, gw[k] + wofs(l, k), d, d, d, R, nullptr, nullptr,
                      false));
-      AECCT_TRY(colsum(dQKV + k * d, 3 * d, nullptr, nullptr, R, d, gb[k] + ld_));
       AECCT_TRY(tgemm(true, l, k, dQKV + k * d, 3 * d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
     }
   }
