@@ -216,8 +216,10 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
                       float *part, int64_t part_floats, int cu_count, hipStream_t s);
 // which: 0 forward (o, lse), 1 query gradients (dqkv's Q third, Dv), 2 key and value gradients
 hipError_t train_attention(int which, int dh, const TrainAttn &a, hipStream_t s);
+// out = LN(a + b), xn the normalised row, rho its 1 / sigma; xh (if given) the Eq. 2 codes of out and
+// their values, as train_quant forms them
 hipError_t train_ln_fwd(const float *a, const float *b, int64_t rows, int d, const float *g, const float *beta, float eps,
-                        float *out, float *xn, float *rho, hipStream_t s);
+                        float *out, float *xn, float *rho, float *xh, hipStream_t s);
 hipError_t train_ln_bwd(const float *dy, const float *g, const float *xn, const float *rho, int64_t rows, int d,
                         float *dR, hipStream_t s);
 // out[c] (+)= sum_r A[r][c] (B[r][c] if B) (w[r] if w), rows of A lda apart, B dense [rows][C]

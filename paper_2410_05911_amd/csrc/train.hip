@@ -718,7 +718,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_bwd_kv(AttnT p) {
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_ln_fwd(const float *a, const float *b, int64_t rows, int d,
                                                      const float *g, const float *beta, float eps, float *out,
-                                                     float *xn, float *rho) {
+                                                     float *xn, float *rho, float *xh) {
   const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= rows) return;
@@ -743,9 +743,23 @@ __global__ __launch_bounds__(kThreads) void k_ln_fwd(const float *a, const float
     if (c >= d) continue;
     const float x = (v[u] - mean) * rh;
     xn[r * d + c] = x;
-    out[r * d + c] = fmaf(x, g[c], beta[c]);
+    v[u] = fmaf(x, g[c], beta[c]);
+    out[r * d + c] = v[u];
   }
   if (lane == 0) rho[r] = rh;
+  if (!xh) return;
+  // the output row's Eq. 2 codes and their values, as k_quant_dequant forms them from out
+  float am = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    if (lane + 64 * u < d) am = fmaxf(am, fabsf(v[u]));
+  am = wave_max(am);
+  const float inv = inv127(am);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = lane + 64 * u;
+    if (c < d) xh[r * d + c] = am == 0.0f ? 0.0f : (float)quant_code(v[u], inv) * am / 127.0f;
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void k_ln_bwd(const float *dy, const float *g, const float *xn,
@@ -1089,11 +1103,11 @@ hipError_t train_attention(int which, int dh, const TrainAttn &a, hipStream_t s)
 }
 
 hipError_t train_ln_fwd(const float *a, const float *b, int64_t rows, int d, const float *g, const float *beta, float eps,
-                        float *out, float *xn, float *rho, hipStream_t s) {
+                        float *out, float *xn, float *rho, float *xh, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (d > 128) return hipErrorInvalidValue;
   hipLaunchKernelGGL(train::k_ln_fwd, dim3(blocks_for(rows, 4)), dim3(train::kThreads), 0, s, a, b, rows, d, g, beta, eps,
-                     out, xn, rho);
+                     out, xn, rho, xh);
   return hipGetLastError();
 }
 

@@ -269,7 +269,7 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
   for (int l = 0; l < N; ++l) {
     const TrainWs::Layer &q = W.layer[l];
     float *Xh = ws + q.xh, *QKV = ws + q.qkv;
-    AECCT_TRY(train_quant(X, R, d, false, Xh, s));
+    if (l == 0) AECCT_TRY(train_quant(X, R, d, false, Xh, s));   // later layers: from the previous LN2
     for (int k = 0; k < 3; ++k)
       AECCT_TRY(tgemm(false, l, k, Xh, d, QKV + k * d, 3 * d, R, d, d, sc + 6 * l + k, pb[k] + (size_t)l * d, false));
     TrainAttn at{QKV, R, T.L, d, T.heads, T.hf, T.m1_ptr, T.m1_idx, T.m2_ptr, T.m2_idx, ws + q.o, ws + q.lse,
@@ -278,13 +278,12 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     AECCT_TRY(train_quant(ws + q.o, R, d, false, ws + q.oh, s));
     AECCT_TRY(tgemm(false, l, 3, ws + q.oh, d, Y, d, R, d, d, sc + 6 * l + 3, pb[3] + (size_t)l * d, false));
     AECCT_TRY(train_ln_fwd(X, Y, R, d, p->ln1_g + (size_t)l * d, p->ln1_b + (size_t)l * d, T.ln_eps, X1, ws + q.xn1,
-                           ws + q.rho1, s));
-    AECCT_TRY(train_quant(X1, R, d, false, ws + q.x1h, s));
+                           ws + q.rho1, ws + q.x1h, s));
     AECCT_TRY(tgemm(false, l, 4, ws + q.x1h, d, ws + q.f, dff, R, dff, d, sc + 6 * l + 4, pb[4] + (size_t)l * dff, false));
     AECCT_TRY(train_quant(ws + q.f, R, dff, true, ws + q.gh, s));
     AECCT_TRY(tgemm(false, l, 5, ws + q.gh, dff, Y, d, R, d, dff, sc + 6 * l + 5, pb[5] + (size_t)l * d, false));
     AECCT_TRY(train_ln_fwd(X1, Y, R, d, p->ln2_g + (size_t)l * d, p->ln2_b + (size_t)l * d, T.ln_eps, X, ws + q.xn2,
-                           ws + q.rho2, s));
+                           ws + q.rho2, l + 1 < N ? ws + W.layer[l + 1].xh : nullptr, s));
   }
   // head and loss (Section 3, Section 6)
   float *z = ws + W.z, *fo = ws + W.fo, *df = ws + W.df, *dz = ws + W.dz;
