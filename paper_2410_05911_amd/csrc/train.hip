@@ -1015,8 +1015,9 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
   // the blocks to cover their short k loops, or the compute units
   const int64_t tm = mfma ? (K <= 256 || M * N <= 128 * 128 ? 64 : train::kMfTile) : 64, tn = mfma ? train::kMfTile : 64;
   const int64_t tiles = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
-  // split long reductions over k so that about two blocks per compute unit are busy
-  int64_t splits = std::max<int64_t>(1, std::min<int64_t>((2 * (int64_t)cu_count + tiles - 1) / tiles, (K + 255) / 256));
+  // split long reductions over k so that about two blocks per compute unit are busy (k chunks of at
+  // least 128)
+  int64_t splits = std::max<int64_t>(1, std::min<int64_t>((2 * (int64_t)cu_count + tiles - 1) / tiles, (K + 127) / 128));
   splits = std::min<int64_t>(splits, part_floats / (M * N));
   if (splits < 1) splits = 1;
   const int64_t kq = mfma ? train::kMfK : 16;
