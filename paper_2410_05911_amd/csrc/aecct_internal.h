@@ -211,6 +211,11 @@ struct TernPackJobs { TernPackJob j[kTrainJobsPerLaunch]; int n; };
 hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s);
 hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
                            int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s);
+// nseg (<= 3) ternary matrices side by side: C[:, k seg_n .. (k + 1) seg_n) = beta C + scale[k] (A T_k) +
+// bias[k] for each k, over one read of A
+hipError_t train_gemm_tern_seg(const float *A, int64_t lda, const void *const *frag, float *C, int64_t ldc, int64_t M,
+                               int64_t seg_n, int nseg, int64_t K, const float *const *scale, const float *const *bias,
+                               bool accumulate, hipStream_t s);
 hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc,
                       int64_t M, int64_t N, int64_t K, const float *scale, const float *bias, bool accumulate,
                       float *part, int64_t part_floats, int cu_count, hipStream_t s);

@@ -439,14 +439,18 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// The N columns of C come in column segments of seg_n (up to three matrices side by side, the
+// query, key and value maps over one read of their shared input); segment s has its own fragments,
+// scale and bias.
 struct GemmTern {
   const float *A;
-  const uint4 *B;       // fragment (nt, kt) at (nt * K / 32 + kt) * 64: lane l holds column
-                        // 16 nt + (l & 15), k = 32 kt + 8 (l >> 4) + e in bf16 e = 0..7
+  const uint4 *B[3];       // fragment (nt, kt) at (nt * K / 32 + kt) * 64: lane l holds column
+                           // 16 nt + (l & 15) of the segment, k = 32 kt + 8 (l >> 4) + e, bf16 e = 0..7
   float *C;
   int64_t M, N, K, lda, ldc;
-  const float *scale;   // device scalar or null (1)
-  const float *bias;    // [N] or null
+  const float *scale[3];   // device scalar or null (1)
+  const float *bias[3];    // [seg_n] or null
+  int64_t seg_n;           // a multiple of the block's 16 NJ columns
   int beta;
 };
 
@@ -508,10 +512,12 @@ template <int NJ, int S>
 __global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, col = l & 15, grp = l >> 4;
   const int64_t m0 = (int64_t)blockIdx.y * 64 + 16 * wave, n0 = (int64_t)blockIdx.x * (16 * NJ);
+  const int sg = (int)(n0 / g.seg_n);
+  const int64_t ns = n0 - sg * g.seg_n;   // the block's first column inside its segment
   const int KT = (int)(g.K / 32);
   const int64_t r = m0 + col;
   const float *arow = g.A + (r < g.M ? r : g.M - 1) * g.lda + 8 * grp;   // rows past M: a copy, never stored
-  const uint4 *bcol = g.B + (n0 / 16) * KT * 64 + l;
+  const uint4 *bcol = g.B[sg] + (ns / 16) * KT * 64 + l;
   f32x4 acc[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -544,12 +550,13 @@ __global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
     }
   }
   if (r >= g.M) return;
-  const float sc = g.scale ? *g.scale : 1.0f;
+  const float sc = g.scale[sg] ? *g.scale[sg] : 1.0f;
+  const float *bias = g.bias[sg];
   float4 o[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int64_t c = n0 + 16 * j + 4 * grp;
-    const float4 bj = g.bias ? *(const float4 *)(g.bias + c) : float4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int64_t c = ns + 16 * j + 4 * grp;
+    const float4 bj = bias ? *(const float4 *)(bias + c) : float4{0.0f, 0.0f, 0.0f, 0.0f};
     o[j].x = sc * acc[j][0] + bj.x;
     o[j].y = sc * acc[j][1] + bj.y;
     o[j].z = sc * acc[j][2] + bj.z;
@@ -1074,16 +1081,33 @@ hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
-                           int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s) {
-  if (M <= 0 || N <= 0) return hipSuccess;
-  if (!train_tern_operands_ok(A, lda, C, ldc, bias, N, K)) return hipErrorInvalidValue;
-  train::GemmTern g{A, (const uint4 *)frag, C, M, N, K, lda, ldc, scale, bias, accumulate ? 1 : 0};
+hipError_t train_gemm_tern_seg(const float *A, int64_t lda, const void *const *frag, float *C, int64_t ldc, int64_t M,
+                               int64_t seg_n, int nseg, int64_t K, const float *const *scale, const float *const *bias,
+                               bool accumulate, hipStream_t s) {
+  if (M <= 0 || seg_n <= 0) return hipSuccess;
+  if (nseg < 1 || nseg > 3) return hipErrorInvalidValue;
+  for (int k = 0; k < nseg; ++k)
+    if (!train_tern_operands_ok(A, lda, C + k * seg_n, ldc, bias[k], seg_n, K)) return hipErrorInvalidValue;
+  const int64_t N = seg_n * nseg;
+  train::GemmTern g{A, {}, C, M, N, K, lda, ldc, {}, {}, seg_n, accumulate ? 1 : 0};
+  for (int k = 0; k < nseg; ++k) {
+    g.B[k] = (const uint4 *)frag[k];
+    g.scale[k] = scale[k];
+    g.bias[k] = bias[k];
+  }
   constexpr int S = 3;   // operands two k-steps ahead
   const unsigned gy = (unsigned)((M + 63) / 64);
-  if (N % 128 == 0) hipLaunchKernelGGL((train::k_gemm_tern<8, S>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
-  else hipLaunchKernelGGL((train::k_gemm_tern<4, S>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
+  // a block's 16 NJ columns never straddle two segments: seg_n is a multiple of 64 (and of 128 for NJ = 8)
+  if (seg_n % 128 == 0)
+    hipLaunchKernelGGL((train::k_gemm_tern<8, S>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
+  else
+    hipLaunchKernelGGL((train::k_gemm_tern<4, S>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
   return hipGetLastError();
+}
+
+hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,
+                           int64_t K, const float *scale, const float *bias, bool accumulate, hipStream_t s) {
+  return train_gemm_tern_seg(A, lda, &frag, C, ldc, M, N, 1, K, &scale, &bias, accumulate, s);
 }
 
 hipError_t train_attention(int which, int dh, const TrainAttn &a, hipStream_t s) {

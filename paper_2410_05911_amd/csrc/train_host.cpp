@@ -270,8 +270,19 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     const TrainWs::Layer &q = W.layer[l];
     float *Xh = ws + q.xh, *QKV = ws + q.qkv;
     if (l == 0) AECCT_TRY(train_quant(X, R, d, false, Xh, s));   // later layers: from the previous LN2
-    for (int k = 0; k < 3; ++k)
-      AECCT_TRY(tgemm(false, l, k, Xh, d, QKV + k * d, 3 * d, R, d, d, sc + 6 * l + k, pb[k] + (size_t)l * d, false));
+    {
+      // the query, key and value maps as one product over one read of Xh where the ternary path applies
+      const float *bq[3] = {pb[0] + (size_t)l * d, pb[1] + (size_t)l * d, pb[2] + (size_t)l * d};
+      const float *sq[3] = {sc + 6 * l, sc + 6 * l + 1, sc + 6 * l + 2};
+      bool fused = tern;
+      for (int k = 0; k < 3; ++k) fused = fused && train_tern_operands_ok(Xh, d, QKV + k * d, 3 * d, bq[k], d, d);
+      if (fused) {
+        const void *fq[3] = {tfrag(l, 0, false), tfrag(l, 1, false), tfrag(l, 2, false)};
+        AECCT_TRY(train_gemm_tern_seg(Xh, d, fq, QKV, 3 * d, R, d, 3, d, sq, bq, false, s));
+      } else {
+        for (int k = 0; k < 3; ++k) AECCT_TRY(tgemm(false, l, k, Xh, d, QKV + k * d, 3 * d, R, d, d, sq[k], bq[k], false));
+      }
+    }
     TrainAttn at{QKV, R, T.L, d, T.heads, T.hf, T.m1_ptr, T.m1_idx, T.m2_ptr, T.m2_idx, ws + q.o, ws + q.lse,
                  nullptr, nullptr, nullptr};
     AECCT_TRY(train_attention(0, T.dh, at, s));
