@@ -216,6 +216,12 @@ hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float 
 hipError_t train_gemm_tern_seg(const float *A, int64_t lda, const void *const *frag, float *C, int64_t ldc, int64_t M,
                                int64_t seg_n, int nseg, int64_t K, const float *const *scale, const float *const *bias,
                                bool accumulate, hipStream_t s);
+// C = D + sum_k scale[k] (A[:, k kseg .. (k + 1) kseg) T_k) over nseg (<= 3) ternary matrices along A's
+// row, D (optional, laid out like C, may be C) an addend: the input gradient summed over the query,
+// key and value maps from their packed gradient
+hipError_t train_gemm_tern_ksum(const float *A, int64_t lda, const void *const *frag, int nseg, int64_t kseg,
+                                const float *const *scale, const float *D, float *C, int64_t ldc, int64_t M, int64_t N,
+                                hipStream_t s);
 hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc,
                       int64_t M, int64_t N, int64_t K, const float *scale, const float *bias, bool accumulate,
                       float *part, int64_t part_floats, int cu_count, hipStream_t s);

@@ -439,20 +439,29 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(GemmF32 g) {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// The N columns of C come in column segments of seg_n (up to three matrices side by side, the
-// query, key and value maps over one read of their shared input); segment s has its own fragments,
-// scale and bias.
+// Up to three ternary matrices in one product, either side by side in C's columns (segments of
+// seg_n columns: the query, key and value maps over one read of their shared input) or one after
+// another along k (segments of kseg k-steps of A's row: the input gradient summed over the three
+// maps from the packed [rows][3 d] gradient).  Segment s has its own fragments and scale, a column
+// segment its own bias; C = D + sum_s scale_s (A_s T_s) + bias, D an optional addend laid out like C
+// (C itself to accumulate).
 struct GemmTern {
   const float *A;
-  const uint4 *B[3];       // fragment (nt, kt) at (nt * K / 32 + kt) * 64: lane l holds column
-                           // 16 nt + (l & 15) of the segment, k = 32 kt + 8 (l >> 4) + e, bf16 e = 0..7
+  const uint4 *B[3];       // fragment (nt, kt) at (nt * kt_s + kt) * 64, kt_s the segment's k-steps:
+                           // lane l holds column 16 nt + (l & 15), k = 32 kt + 8 (l >> 4) + e, bf16 e = 0..7
   float *C;
+  const float *D;
   int64_t M, N, K, lda, ldc;
   const float *scale[3];   // device scalar or null (1)
   const float *bias[3];    // [seg_n] or null
   int64_t seg_n;           // a multiple of the block's 16 NJ columns
-  int beta;
+  int kseg;                // k-steps per k segment (K / 32 when there is one)
 };
+
+template <typename T>
+__device__ __forceinline__ T pick3(const T (&v)[3], int i) {   // a selected kernel argument, no indexing
+  return i == 0 ? v[0] : (i == 1 ? v[1] : v[2]);
+}
 
 // Ternary matrix T [R][C] (fp32 -1 / 0 / +1, row-major) as bf16 B fragments of B = T (k = row,
 // n = column) or, with trans, B = T^T (k = column, n = row); one job per blockIdx.y.
@@ -514,21 +523,27 @@ __global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
   const int64_t m0 = (int64_t)blockIdx.y * 64 + 16 * wave, n0 = (int64_t)blockIdx.x * (16 * NJ);
   const int sg = (int)(n0 / g.seg_n);
   const int64_t ns = n0 - sg * g.seg_n;   // the block's first column inside its segment
-  const int KT = (int)(g.K / 32);
+  const int KT = (int)(g.K / 32), ks = g.kseg;
   const int64_t r = m0 + col;
   const float *arow = g.A + (r < g.M ? r : g.M - 1) * g.lda + 8 * grp;   // rows past M: a copy, never stored
-  const uint4 *bcol = g.B[sg] + (ns / 16) * KT * 64 + l;
   f32x4 acc[NJ];
+  float4 o[NJ];
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int j = 0; j < NJ; ++j) {
+    acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    o[j] = float4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
   float4 a[S][2];
   uint4 b[S][NJ];
   auto issue = [&](int kt, float4 (&as)[2], uint4 (&bs)[NJ]) {
+    const int s = kt / ks;   // the k segment (0 with one)
+    const uint4 *bcol = pick3(g.B, sg + s) + (ns / 16) * ks * 64 + l;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) bs[j] = bcol[(j * KT + kt) * 64];
+    for (int j = 0; j < NJ; ++j) bs[j] = bcol[(j * ks + kt - s * ks) * 64];
     as[0] = *(const float4 *)(arow + 32 * kt);
     as[1] = *(const float4 *)(arow + 32 * kt + 4);
   };
+  int kend = ks;   // the current k segment ends before step kend
 #pragma unroll
   for (int s = 0; s < S - 1; ++s)
     if (s < KT) issue(s, a[s], b[s]);
@@ -547,31 +562,44 @@ __global__ __launch_bounds__(kThreads) void k_gemm_tern(GemmTern g) {
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, pm, acc[j], 0, 0, 0);
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, ph, acc[j], 0, 0, 0);
       }
+      if (kt + 1 == kend) {   // a k segment's products, scaled, into o
+        const float *sp = pick3(g.scale, sg + kt / ks);
+        const float sc = sp ? *sp : 1.0f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          o[j].x += sc * acc[j][0];
+          o[j].y += sc * acc[j][1];
+          o[j].z += sc * acc[j][2];
+          o[j].w += sc * acc[j][3];
+          acc[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+        kend += ks;
+      }
     }
   }
   if (r >= g.M) return;
-  const float sc = g.scale[sg] ? *g.scale[sg] : 1.0f;
-  const float *bias = g.bias[sg];
-  float4 o[NJ];
+  const float *bias = pick3(g.bias, sg);
+  if (bias) {
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int64_t c = ns + 16 * j + 4 * grp;
-    const float4 bj = bias ? *(const float4 *)(bias + c) : float4{0.0f, 0.0f, 0.0f, 0.0f};
-    o[j].x = sc * acc[j][0] + bj.x;
-    o[j].y = sc * acc[j][1] + bj.y;
-    o[j].z = sc * acc[j][2] + bj.z;
-    o[j].w = sc * acc[j][3] + bj.w;
+    for (int j = 0; j < NJ; ++j) {
+      const float4 bj = *(const float4 *)(bias + ns + 16 * j + 4 * grp);
+      o[j].x += bj.x;
+      o[j].y += bj.y;
+      o[j].z += bj.z;
+      o[j].w += bj.w;
+    }
   }
   float *crow = g.C + r * g.ldc + n0 + 4 * grp;
+  const float *drow = g.D ? g.D + r * g.ldc + n0 + 4 * grp : nullptr;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     float4 u = o[j];
-    if (g.beta) {
-      const float4 cv = *(const float4 *)(crow + 16 * j);
-      u.x += cv.x;
-      u.y += cv.y;
-      u.z += cv.z;
-      u.w += cv.w;
+    if (drow) {
+      const float4 dv = *(const float4 *)(drow + 16 * j);
+      u.x += dv.x;
+      u.y += dv.y;
+      u.z += dv.z;
+      u.w += dv.w;
     }
     *(float4 *)(crow + 16 * j) = u;
   }
@@ -1081,6 +1109,20 @@ hipError_t train_pack_tern(const TernPackJobs &jobs, hipStream_t s) {
   return hipGetLastError();
 }
 
+namespace {
+hipError_t gemm_tern_go(const train::GemmTern &g, hipStream_t s) {
+  constexpr int S = 3;   // operands two k-steps ahead
+  const unsigned gy = (unsigned)((g.M + 63) / 64);
+  // a block's 16 NJ columns never straddle two column segments: seg_n is a multiple of 64 (and of
+  // 128 for NJ = 8)
+  if (g.seg_n % 128 == 0)
+    hipLaunchKernelGGL((train::k_gemm_tern<8, S>), dim3((unsigned)(g.N / 128), gy), dim3(train::kThreads), 0, s, g);
+  else
+    hipLaunchKernelGGL((train::k_gemm_tern<4, S>), dim3((unsigned)(g.N / 64), gy), dim3(train::kThreads), 0, s, g);
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t train_gemm_tern_seg(const float *A, int64_t lda, const void *const *frag, float *C, int64_t ldc, int64_t M,
                                int64_t seg_n, int nseg, int64_t K, const float *const *scale, const float *const *bias,
                                bool accumulate, hipStream_t s) {
@@ -1088,21 +1130,28 @@ hipError_t train_gemm_tern_seg(const float *A, int64_t lda, const void *const *f
   if (nseg < 1 || nseg > 3) return hipErrorInvalidValue;
   for (int k = 0; k < nseg; ++k)
     if (!train_tern_operands_ok(A, lda, C + k * seg_n, ldc, bias[k], seg_n, K)) return hipErrorInvalidValue;
-  const int64_t N = seg_n * nseg;
-  train::GemmTern g{A, {}, C, M, N, K, lda, ldc, {}, {}, seg_n, accumulate ? 1 : 0};
+  train::GemmTern g{A, {}, C, accumulate ? C : nullptr, M, seg_n * nseg, K, lda, ldc, {}, {}, seg_n, (int)(K / 32)};
   for (int k = 0; k < nseg; ++k) {
     g.B[k] = (const uint4 *)frag[k];
     g.scale[k] = scale[k];
     g.bias[k] = bias[k];
   }
-  constexpr int S = 3;   // operands two k-steps ahead
-  const unsigned gy = (unsigned)((M + 63) / 64);
-  // a block's 16 NJ columns never straddle two segments: seg_n is a multiple of 64 (and of 128 for NJ = 8)
-  if (seg_n % 128 == 0)
-    hipLaunchKernelGGL((train::k_gemm_tern<8, S>), dim3((unsigned)(N / 128), gy), dim3(train::kThreads), 0, s, g);
-  else
-    hipLaunchKernelGGL((train::k_gemm_tern<4, S>), dim3((unsigned)(N / 64), gy), dim3(train::kThreads), 0, s, g);
-  return hipGetLastError();
+  return gemm_tern_go(g, s);
+}
+
+hipError_t train_gemm_tern_ksum(const float *A, int64_t lda, const void *const *frag, int nseg, int64_t kseg,
+                                const float *const *scale, const float *D, float *C, int64_t ldc, int64_t M, int64_t N,
+                                hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (nseg < 1 || nseg > 3 || kseg <= 0 || kseg % 32 != 0) return hipErrorInvalidValue;
+  if (!train_tern_operands_ok(A, lda, C, ldc, nullptr, N, kseg * nseg) || (D && ((uintptr_t)D & 15u) != 0))
+    return hipErrorInvalidValue;
+  train::GemmTern g{A, {}, C, D, M, N, kseg * nseg, lda, ldc, {}, {}, N, (int)(kseg / 32)};
+  for (int k = 0; k < nseg; ++k) {
+    g.B[k] = (const uint4 *)frag[k];
+    g.scale[k] = scale[k];
+  }
+  return gemm_tern_go(g, s);
 }
 
 hipError_t train_gemm_tern(const float *A, int64_t lda, const void *frag, float *C, int64_t ldc, int64_t M, int64_t N,

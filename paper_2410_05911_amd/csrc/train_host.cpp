@@ -325,12 +325,24 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     AECCT_TRY(train_relu_bwd(dG, ws + q.f, R * dff, s));
     AECCT_TRY(gemm(true, false, ws + q.x1h, d, dG, dff, gw[4] + wofs(l, 4), dff, d, dff, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dG, dff, nullptr, nullptr, R, dff, gb[4] + (size_t)l * dff));
-    AECCT_TRY(hipMemcpyAsync(dX1, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
-    AECCT_TRY(tgemm(true, l, 4, dG, dff, dX1, d, R, d, dff, sc + 6 * l + 4, nullptr, true));
+    // dX1 = dR + dG T4^T: on the ternary path with dR as the product's addend, else a copy and an
+    // accumulating product
+    if (tern && train_tern_operands_ok(dG, dff, dX1, d, nullptr, d, dff) && ((uintptr_t)dR & 15u) == 0) {
+      const void *f4 = tfrag(l, 4, true);
+      const float *s4 = sc + 6 * l + 4;
+      AECCT_TRY(train_gemm_tern_ksum(dG, dff, &f4, 1, dff, &s4, dR, dX1, d, R, d, s));
+    } else {
+      AECCT_TRY(hipMemcpyAsync(dX1, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
+      AECCT_TRY(tgemm(true, l, 4, dG, dff, dX1, d, R, d, dff, sc + 6 * l + 4, nullptr, true));
+    }
     // LN1, output map
     AECCT_TRY(train_ln_bwd(dX1, p->ln1_g + ld_, ws + q.xn1, ws + q.rho1, R, d, dR, s));
     AECCT_TRY(train_colsum_dual(dX1, d, ws + q.xn1, R, d, g->ln1_g + ld_, g->ln1_b + ld_, part, (int64_t)PF, s));
-    AECCT_TRY(hipMemcpyAsync(dX, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
+    // dX = dR + sum_k dQKV_k T_k^T below: one product over the packed gradient with dR as its addend
+    // on the ternary path, else a copy now and three accumulating products
+    const bool qkv_sum = tern && train_tern_operands_ok(dQKV, 3 * d, dX, d, nullptr, d, 3 * d) &&
+                         ((uintptr_t)dR & 15u) == 0;
+    if (!qkv_sum) AECCT_TRY(hipMemcpyAsync(dX, dR, sizeof(float) * R * d, hipMemcpyDeviceToDevice, s));
     AECCT_TRY(gemm(true, false, ws + q.oh, d, dR, d, gw[3] + wofs(l, 3), d, d, d, R, nullptr, nullptr, false));
     AECCT_TRY(colsum(dR, d, nullptr, nullptr, R, d, gb[3] + ld_));
     AECCT_TRY(tgemm(true, l, 3, dR, d, dO, d, R, d, d, sc + 6 * l + 3, nullptr, false));
@@ -344,7 +356,12 @@ aecct_status aecct_train_grad(const aecct_trainer *tr, const aecct_train_params 
     for (int k = 0; k < 3; ++k) {
       AECCT_TRY(gemm(true, false, ws + q.xh, d, dQKV + k * d, 3 * d, gw[k] + wofs(l, k), d, d, d, R, nullptr, nullptr,
                      false));
-      AECCT_TRY(tgemm(true, l, k, dQKV + k * d, 3 * d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
+      if (!qkv_sum) AECCT_TRY(tgemm(true, l, k, dQKV + k * d, 3 * d, dX, d, R, d, d, sc + 6 * l + k, nullptr, true));
+    }
+    if (qkv_sum) {
+      const void *fq[3] = {tfrag(l, 0, true), tfrag(l, 1, true), tfrag(l, 2, true)};
+      const float *sq[3] = {sc + 6 * l, sc + 6 * l + 1, sc + 6 * l + 2};
+      AECCT_TRY(train_gemm_tern_ksum(dQKV, 3 * d, fq, 3, d, sq, dR, dX, d, R, d, s));
     }
   }
   // the straight-through Eq. 1 gradients of every matrix from its G = Xh^T dY (nothing in the
