@@ -1046,9 +1046,9 @@ hipError_t train_gemm(bool ta, bool tb, const float *A, int64_t lda, const float
   auto al16 = [](const float *p) { return ((uintptr_t)p & 15u) == 0; };
   const bool mfma = al16(A) && al16(B) && lda % 4 == 0 && ldb % 4 == 0 && (ta ? M : K) % 4 == 0 &&
                     (tb ? K : N) % 4 == 0;
-  // reductions of at most 256, and products of at most 128 x 128 outputs, get 64-row tiles: twice
+  // reductions of at most 256, and products of at most 128 x 512 outputs, get 64-row tiles: twice
   // the blocks to cover their short k loops, or the compute units
-  const int64_t tm = mfma ? (K <= 256 || M * N <= 128 * 128 ? 64 : train::kMfTile) : 64, tn = mfma ? train::kMfTile : 64;
+  const int64_t tm = mfma ? (K <= 256 || M * N <= 128 * 512 ? 64 : train::kMfTile) : 64, tn = mfma ? train::kMfTile : 64;
   const int64_t tiles = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
   // split long reductions over k so that about two blocks per compute unit are busy (k chunks of at
   // least 128)
