@@ -681,13 +681,21 @@ __global__ __launch_bounds__(kThreads) void k_attn_fwd(AttnT p) {
   float q[DH];
 #pragma unroll
   for (int t = 0; t < DH; ++t) q[t] = p.qkv[row * ld + h * DH + t];
-  float mu = -INFINITY;
-  for (int e = ptr[i]; e < ptr[i + 1]; ++e)
-    mu = fmaxf(mu, dot_dh<DH>(q, p.qkv + (base + idx[e]) * ld + d + h * DH) * kappa);
-  float S = 0.0f, acc[DH] = {};
+  // one pass with a running maximum: when a score raises it, the sum and the accumulated values so
+  // far are rescaled by exp(old - new) (each key read once instead of once for the maximum and once
+  // for the weights)
+  float mu = -INFINITY, S = 0.0f, acc[DH] = {};
   for (int e = ptr[i]; e < ptr[i + 1]; ++e) {
     const int64_t j = base + idx[e];
-    const float pe = expf(dot_dh<DH>(q, p.qkv + j * ld + d + h * DH) * kappa - mu);
+    const float s = dot_dh<DH>(q, p.qkv + j * ld + d + h * DH) * kappa;
+    if (s > mu) {
+      const float c = expf(mu - s);   // 0 at the first key
+      S *= c;
+#pragma unroll
+      for (int t = 0; t < DH; ++t) acc[t] *= c;
+      mu = s;
+    }
+    const float pe = expf(s - mu);
     S += pe;
 #pragma unroll
     for (int t = 0; t < DH; ++t) acc[t] = fmaf(pe, p.qkv[j * ld + 2 * d + h * DH + t], acc[t]);
