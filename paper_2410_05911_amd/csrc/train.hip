@@ -640,12 +640,11 @@ __global__ __launch_bounds__(kThreads) void k_gemm_reduce(GemmF32 g, int splits)
 // ------------------------------------------------------------------------------------------
 using AttnT = TrainAttn;
 
-// Thread gid to (row, head) in the backward kernels: the first-ring heads of every row first
-// (row-major, a row's h_f heads on adjacent lanes), then the second-ring heads, so that a wavefront
-// walks one kind of list and its lanes run loops of similar length (with both kinds in one
-// wavefront the first-ring lanes idled through the longer second-ring lists), while a row's heads
-// of one kind still read adjacent stretches of each neighbour's row.  The forward, whose two passes
-// over the list re-read each key, measured faster with all heads of a row on adjacent lanes.
+// Thread gid to (row, head): the first-ring heads of every row first (row-major, a row's h_f heads
+// on adjacent lanes), then the second-ring heads, so that a wavefront walks one kind of list and
+// its lanes run loops of similar length (with both kinds in one wavefront the first-ring lanes idled
+// through the longer second-ring lists), while a row's heads of one kind still read adjacent
+// stretches of each neighbour's row.
 __device__ __forceinline__ void attn_row_head(const AttnT &p, int64_t gid, int64_t &row, int &h) {
   const int64_t n1 = p.rows * p.hf;
   if (gid < n1) {
@@ -671,8 +670,9 @@ template <int DH>
 __global__ __launch_bounds__(kThreads) void k_attn_fwd(AttnT p) {
   const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (gid >= p.rows * p.heads) return;
-  const int64_t row = gid / p.heads;   // all heads of a row on adjacent lanes (measured faster here)
-  const int h = (int)(gid - row * p.heads);
+  int64_t row;
+  int h;
+  attn_row_head(p, gid, row, h);
   const int64_t base = (row / p.L) * p.L;
   const int i = (int)(row - base);
   const int32_t *ptr = h < p.hf ? p.m1_ptr : p.m2_ptr, *idx = h < p.hf ? p.m1_idx : p.m2_idx;
