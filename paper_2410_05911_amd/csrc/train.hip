@@ -184,6 +184,25 @@ __global__ __launch_bounds__(kThreads) void k_quant_dequant(const float *x, int6
   if (r >= rows) return;
   const float *xr = x + r * K;
   float a = 0.0f;
+  constexpr int kHeld = 8;   // rows up to 512 wide are read whole before their maximum is formed
+  if (K <= 64 * kHeld) {
+    float v[kHeld];
+#pragma unroll
+    for (int u = 0; u < kHeld; ++u) v[u] = lane + 64 * u < K ? xr[lane + 64 * u] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < kHeld; ++u) {
+      if (RELU) v[u] = fmaxf(v[u], 0.0f);
+      a = fmaxf(a, fabsf(v[u]));
+    }
+    a = wave_max(a);
+    const float inv = inv127(a);
+#pragma unroll
+    for (int u = 0; u < kHeld; ++u) {
+      const int c = lane + 64 * u;
+      if (c < K) xh[r * K + c] = a == 0.0f ? 0.0f : (float)quant_code(v[u], inv) * a / 127.0f;
+    }
+    return;
+  }
   for (int c = lane; c < K; c += 64) {
     const float v = RELU ? fmaxf(xr[c], 0.0f) : xr[c];
     a = fmaxf(a, fabsf(v));
